@@ -1,0 +1,162 @@
+"""Seeded synthetic workloads for the multi-draft selection hot path.
+
+This module holds input generation only: it draws target/draft distributions,
+the drafted tokens and the per-position uniforms.  It contains none of the
+selection method's arithmetic (no weights, no induced distribution, no
+acceptance or residual), so both the fp64 oracle tests and the GPU path can
+take their inputs from it without sharing any of the method's code.
+
+Notation follows the selection method as implemented here: ``p`` is the TARGET
+distribution and ``q`` the DRAFT distribution (the paper writes them the other
+way round: its ``p`` is the draft model and its ``q`` the target model).
+
+Every row is generated from its own ``numpy.random.Generator(PCG64(SeedSequence(
+[seed, stream, row])))`` so that any subset of rows can be regenerated on its
+own.  Streams: 0 logits / Dirichlet draw of p, 1 noise / Dirichlet draw of q,
+2 permutation, 3 drafts, 4 uniforms.
+
+Values are produced in fp64 (softmax in fp64) and cast to fp32, without any
+renormalisation after the cast.  Drafted tokens are drawn i.i.d. from the fp32
+draft row by inverse CDF, so a drafted token always has q > 0.  Uniforms are
+24-bit dyadic rationals k / 2**24 in [0, 1), exactly representable in fp32.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Callable, Dict, Optional, Sequence
+
+import numpy as np
+
+__all__ = ["Config", "CONFIGS", "generate", "uniforms24", "draw_drafts"]
+
+_S_LOGIT, _S_NOISE, _S_PERM, _S_DRAFT, _S_UNIF = 0, 1, 2, 3, 4
+
+
+def _rng(seed: int, stream: int, row: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, stream, row])))
+
+
+def _softmax64(z: np.ndarray) -> np.ndarray:
+    z = z - z.max()
+    e = np.exp(z)
+    return e / e.sum()
+
+
+@dataclasses.dataclass(frozen=True)
+class Config:
+    name: str
+    seed: int
+    B: int
+    V: int
+    K: int
+    describe: str
+    row: Callable[["Config", int], "tuple[np.ndarray, np.ndarray]"]
+    s_max: int = 0  # support cap the K=3 path is run with (0: not used)
+
+
+def _row_dirichlet(cfg: Config, b: int):
+    p = _rng(cfg.seed, _S_LOGIT, b).dirichlet(np.full(cfg.V, 0.5))
+    q = _rng(cfg.seed, _S_NOISE, b).dirichlet(np.full(cfg.V, 0.5))
+    return p, q
+
+
+def _row_gauss(sigma: float, noise: float, temp: float):
+    def f(cfg: Config, b: int):
+        ell = _rng(cfg.seed, _S_LOGIT, b).normal(0.0, sigma, cfg.V)
+        eps = _rng(cfg.seed, _S_NOISE, b).normal(0.0, noise, cfg.V)
+        return _softmax64(ell / temp), _softmax64((ell + eps) / temp)
+    return f
+
+
+def _row_zipf(cfg: Config, b: int):
+    k = np.arange(1, cfg.V + 1, dtype=np.float64)
+    mass = k ** -1.1
+    mass /= mass.sum()
+    perm = _rng(cfg.seed, _S_PERM, b).permutation(cfg.V)
+    p = np.empty(cfg.V)
+    p[perm] = mass  # token perm[k-1] has rank k
+    eps = _rng(cfg.seed, _S_NOISE, b).normal(0.0, 1.0, cfg.V)
+    return p, _softmax64(np.log(p) + eps)
+
+
+def _row_topk(s: int):
+    base = _row_gauss(3.0, 1.0, 1.0)
+
+    def f(cfg: Config, b: int):
+        p, qfull = base(cfg, b)
+        # top-s of the draft row; ties broken by lower token id (stable order on (-q, id))
+        order = np.lexsort((np.arange(cfg.V), -qfull))
+        keep = order[:s]
+        q = np.zeros(cfg.V)
+        q[keep] = qfull[keep]
+        q /= q.sum()
+        return p, q
+    return f
+
+
+CONFIGS: Dict[str, Config] = {
+    c.name: c
+    for c in [
+        Config("tiny", 1001, 64, 16, 2,
+               "V=16, K=2, 64 positions, p and q independent Dirichlet(0.5)", _row_dirichlet),
+        Config("llm32k", 1002, 256, 32000, 2,
+               "V=32000, K=2, 256 positions, logits N(0,3^2), draft logits + N(0,1) noise, T=1",
+               _row_gauss(3.0, 1.0, 1.0)),
+        Config("batch50k", 1003, 1024, 50272, 2,
+               "V=50272, K=2, 1024 positions (32 sequences x 32 steps), logits N(0,2.5^2), "
+               "draft noise N(0,1.5^2), T=0.7", _row_gauss(2.5, 1.5, 0.7)),
+        Config("zipf128k", 1004, 512, 128256, 2,
+               "V=128256, K=2, 512 positions, target Zipf k^-1.1 over a per-position permutation, "
+               "draft softmax(log p + N(0,1))", _row_zipf),
+        Config("k3top1024", 1005, 256, 32000, 3,
+               "V=32000, K=3, 256 positions, draft truncated to its top-1024 tokens and "
+               "renormalised, logits N(0,3^2), draft noise N(0,1)", _row_topk(1024), s_max=1024),
+    ]
+}
+
+
+def uniforms24(seed: int, row: int, n: int = 3) -> np.ndarray:
+    """n uniforms in [0,1) as exact 24-bit dyadics (fp32)."""
+    k = _rng(seed, _S_UNIF, row).integers(0, 1 << 24, size=n, dtype=np.int64)
+    return (k.astype(np.float64) / float(1 << 24)).astype(np.float32)
+
+
+def draw_drafts(q32: np.ndarray, K: int, seed: int, row: int) -> np.ndarray:
+    """K i.i.d. tokens from the fp32 draft row by inverse CDF (the draft model's sampling)."""
+    cdf = np.cumsum(q32.astype(np.float64))
+    u = _rng(seed, _S_DRAFT, row).random(K)
+    t = np.searchsorted(cdf, u * cdf[-1], side="right")
+    return np.minimum(t, len(q32) - 1).astype(np.int32)
+
+
+def generate(name: str, rows: Optional[Sequence[int]] = None, B: Optional[int] = None) -> dict:
+    """Build the workload ``name`` (all rows, an explicit row list, or the first ``B`` rows).
+
+    Returns a dict with ``p``, ``q`` (fp32 [n][V]), ``drafts`` (int32 [n][K]),
+    ``u`` (fp32 [n][3]: selection, accept and residual uniforms), ``rows`` and ``config``.
+    """
+    cfg = CONFIGS[name]
+    if rows is None:
+        rows = range(cfg.B if B is None else B)
+    rows = list(rows)
+    n = len(rows)
+    p = np.empty((n, cfg.V), np.float32)
+    q = np.empty((n, cfg.V), np.float32)
+    drafts = np.empty((n, cfg.K), np.int32)
+    u = np.empty((n, 3), np.float32)
+    for i, b in enumerate(rows):
+        p64, q64 = cfg.row(cfg, b)
+        p[i] = p64.astype(np.float32)
+        q[i] = q64.astype(np.float32)
+        drafts[i] = draw_drafts(q[i], cfg.K, cfg.seed, b)
+        u[i] = uniforms24(cfg.seed, b)
+    return {"p": p, "q": q, "drafts": drafts, "u": u, "rows": np.asarray(rows, np.int64), "config": cfg}
+
+
+def dirichlet_instances(seed: int, V: int, count: int, alpha: float = 0.5):
+    """Independent (p, q) pairs from Dirichlet(alpha) at a tiny vocabulary (fp64)."""
+    out = []
+    for i in range(count):
+        g = _rng(seed, V, i)
+        out.append((g.dirichlet(np.full(V, alpha)), g.dirichlet(np.full(V, alpha))))
+    return out
