@@ -1,0 +1,217 @@
+"""Throughput of the multi-draft selection hot path on one MI355X.
+
+One step = the whole path over one batch resident in HBM: induced distribution
+r (K drafts), importance-weighted selection, accept / resample (Algorithm 1).
+Default workload: V = 32000, K = 2, 256 positions of LLM-shaped synthetic
+distributions.  Prints ONE JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config llm32k] [--no-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP32_PEAK_TFLOPS = 157.3  # MI355X fp32 vector peak
+HBM_PEAK_GBS = 8000.0     # MI355X HBM3E
+METRIC = "positions/sec (V=32000, K=2) + % FP32 VALU peak (r) / % HBM BW (resample)"
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for f in ("api.hip", "common.h", "induced.hip", "sample.hip"):
+        with open(os.path.join(ROOT, "paper_2410_18234_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counted_traffic(kernel: str, digest: str):
+    """HBM bytes per launch from the committed PMC summary, only if it was taken on
+    the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+    try:
+        with open(path) as fh:
+            d = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    e = d.get(kernel)
+    if not e or e.get("source_digest") != digest:
+        return None
+    return e.get("bytes_per_launch")
+
+
+def pair_flops(q_np, K: int) -> float:
+    """Algorithmic work of r: K = 2: 6 FLOPs per unordered support pair (add,
+    reciprocal, two FMAs) = 3 n (n - 1) per row; K = 3: 4 FLOPs per (query,
+    unordered pair) = 2 n^2 (n + 1) per row."""
+    import numpy as np
+    n = (q_np > 0).sum(1).astype(np.float64)
+    if K == 2:
+        return float((3.0 * n * (n - 1.0)).sum())
+    return float((2.0 * n * n * (n + 1.0)).sum())
+
+
+def cpu_baseline(w, budget_rows: int):
+    """The fp64 oracle (as it stands) on the first rows of the same workload."""
+    import numpy as np
+
+    import oracle
+    rows = min(budget_rows, w["p"].shape[0])
+    p, q, d, u = (np.ascontiguousarray(w[k][:rows]) for k in ("p", "q", "drafts", "u"))
+    oracle.step(p[:1, :64], q[:1, :64], d[:1], u[:1])  # load the library outside the timing
+    t0 = time.perf_counter()
+    oracle.step(p, q, d, u)
+    dt = time.perf_counter() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    cores = min(cores, os.cpu_count() or cores, rows)
+    return {"value": rows / dt, "unit": "positions/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {rows} positions of the same workload, whole path (r by enumeration of all "
+                      f"ordered draft pairs, selection, accept/resample), {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="llm32k")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline leg")
+    ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample size (0: one per core, 2 rounds)")
+    ap.add_argument("--resample-reps", type=int, default=20)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); positions are independent, "
+              "so a multi-GPU run would shard rows with no exchange and is not part of this build",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2410_18234_amd as mdss
+    from workloads import CONFIGS, generate
+
+    cfg = CONFIGS[args.config]
+    w = generate(args.config)
+    dev = torch.device("cuda:0")
+    p = torch.from_numpy(w["p"]).to(dev)
+    q = torch.from_numpy(w["q"]).to(dev)
+    drafts = torch.from_numpy(w["drafts"]).to(dev)
+    u = torch.from_numpy(w["u"]).to(dev)
+    B, V, K = p.shape[0], p.shape[1], cfg.K
+    s_max = cfg.s_max
+    r = torch.empty_like(p)
+    status = torch.zeros(B, dtype=torch.int32, device=dev)
+    ws = torch.empty(mdss.workspace_bytes(B, V, K, s_max), dtype=torch.uint8, device=dev)
+
+    def one_step(ev=None):
+        status.zero_()
+        if ev is not None:
+            ev[0].record()
+        mdss.induced_dist(p, q, K, s_max=s_max, r=r, row_status=status, workspace=ws)
+        if ev is not None:
+            ev[1].record()
+        _, sel_token = mdss.select_intermediate(p, q, drafts, u, row_status=status)
+        out, acc, _, _ = mdss.accept_or_resample(p, r, sel_token, u, row_status=status)
+        return out, acc
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        out, acc = one_step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    r_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    ms_per_step = wall * 1e3 / args.steps
+    assert int(status.abs().sum()) == 0, "rows flagged during the bench"
+    accept_rate = float(acc.float().mean())
+
+    flops = pair_flops(w["q"], K)
+    achieved = flops / (r_ms * 1e-3) / 1e12
+    digest = kernel_source_digest()
+    sweep_name = "sweep_k2_kernel" if K == 2 else "sweep_k3_kernel"
+    roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / FP32_PEAK_TFLOPS, 4), "traffic": counted_traffic(sweep_name, digest),
+                "kernel": f"mdss_induced_dist ({sweep_name} + preparation)", "avg_ms": round(r_ms, 4),
+                "flops_per_launch": flops}
+
+    # accept / resample pass over every row with the residual written (12 B per token)
+    _, sel_token = mdss.select_intermediate(p, q, drafts, u)
+    res = torch.empty_like(p)
+    mass = torch.empty(B, dtype=torch.float64, device=dev)
+    import ctypes
+    lib = mdss.load_library()
+    out_t = torch.empty(B, dtype=torch.int32, device=dev)
+    acc_t = torch.empty(B, dtype=torch.uint8, device=dev)
+    stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+    def resample_full():
+        rc = lib.mdss_accept_or_resample(ctypes.c_void_p(p.data_ptr()), ctypes.c_void_p(r.data_ptr()),
+                                         ctypes.c_void_p(sel_token.data_ptr()), ctypes.c_void_p(u.data_ptr()),
+                                         ctypes.c_uint64(0), ctypes.c_uint64(0), B, V,
+                                         ctypes.c_void_p(out_t.data_ptr()), ctypes.c_void_p(acc_t.data_ptr()),
+                                         ctypes.c_void_p(res.data_ptr()), ctypes.c_void_p(mass.data_ptr()), None,
+                                         stream)
+        assert rc == 0
+
+    for _ in range(3):
+        resample_full()
+    torch.cuda.synchronize()
+    rev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.resample_reps)]
+    for a, b in rev:
+        a.record()
+        resample_full()
+        b.record()
+    torch.cuda.synchronize()
+    res_ms = float(np.median([a.elapsed_time(b) for a, b in rev]))
+    res_bytes = 12.0 * B * V
+    res_gbs = res_bytes / (res_ms * 1e-3) / 1e9
+    roofline_resample = {"bound": "hbm", "achieved": round(res_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(res_gbs / HBM_PEAK_GBS, 4),
+                         "traffic": counted_traffic("accept_kernel", digest),
+                         "kernel": "mdss_accept_or_resample, residual and mass written for every row",
+                         "avg_ms": round(res_ms, 4), "bytes_per_launch": res_bytes,
+                         "note": "%.1f MB per launch: %s the 256 MB Infinity Cache" %
+                                 (res_bytes / 1e6, "fits in" if res_bytes < 256e6 else "exceeds")}
+
+    line = {
+        "metric": METRIC,
+        "value": round(B / (ms_per_step * 1e-3), 2),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.describe}", "B": B, "V": V, "K": K,
+                   "s_max": s_max or None, "accept_rate": round(accept_rate, 4)},
+        "roofline": roofline,
+        "roofline_resample": roofline_resample,
+        "cpu_baseline": None,
+        "kernel_source_digest": digest,
+    }
+    if not args.no_cpu:
+        ncores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        rows = args.cpu_rows or 2 * ncores
+        line["cpu_baseline"] = cpu_baseline(w, rows)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,135 @@
+/*
+ * mdss.h -- C ABI of the MI355X (gfx950) multi-draft selection library.
+ *
+ * Method: Khisti et al., "Multi-Draft Speculative Sampling: Canonical
+ * Decomposition and Theoretical Limits" (ICLR 2025).  Theorem 1 splits the
+ * token-level selection of one output token from K drafted tokens into
+ *   (1) importance weighted sampling (Definition 1) of one intermediate token
+ *       Y among the drafts, here with the classical weights named right after
+ *       Definition 1: Pr(I = i | x_1..x_K) proportional to w(x_i), and
+ *   (2) single-draft speculative sampling (Algorithm 1, appendix on
+ *       speculative decoding) of Y against the target, with the induced
+ *       distribution r of Y in the role of the draft distribution.
+ *
+ * Notation used throughout this library: p = TARGET distribution, q = DRAFT
+ * distribution, w(x) = p(x)/q(x).  (The paper uses the letters the other way
+ * round: its p is the draft model and its q the target model.)
+ *
+ * Conventions shared by every entry point:
+ *   - p, q, r and residual are row-major [B][V] fp32 arrays in device memory,
+ *     rows contiguous (leading dimension V).  They are read as given: rows
+ *     are not renormalised.
+ *   - All pointers are HIP device pointers unless stated otherwise.  The
+ *     caller owns every buffer, including the workspace; the library never
+ *     allocates, frees or keeps device memory between calls.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Every call only enqueues work on it and returns; the caller
+ *     synchronises.  Calls on one stream run in issue order.
+ *   - Argument errors (null pointer, bad size, K or workspace) are returned
+ *     synchronously before anything is launched, and nothing is written.
+ *     A failed launch returns MDSS_EDEVICE.
+ *   - Per-row data problems are reported in row_status[b] (nullable), as bits
+ *     OR-ed into the existing value: the caller zeroes row_status before the
+ *     first call of a step.  A flagged row gets r = NaN and token -1.
+ *   - Uniforms: u is [B][3] fp32 (device): u[b][0] for the selection draw,
+ *     u[b][1] for the accept test, u[b][2] for the residual draw, each in
+ *     [0, 1).  If u is NULL they are generated on the device from
+ *     Philox4x32-10 (Salmon et al., SC'11) with key = seed and counter =
+ *     (offset + b) (low word first, upper two counter words zero): output
+ *     word j gives u_j = (word_j >> 8) * 2^-24.
+ */
+#ifndef MDSS_H
+#define MDSS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum mdss_status {
+  MDSS_OK = 0,
+  MDSS_EINVAL = 1,       /* null pointer or invalid argument value */
+  MDSS_ESHAPE = 2,       /* B outside [1, MDSS_MAX_B] or V outside [2, MDSS_MAX_V] */
+  MDSS_EUNSUPPORTED = 3, /* K outside {2, 3}, or K = 3 with s_max outside [1, MDSS_K3_MAX_SUPPORT] */
+  MDSS_EDEVICE = 4,      /* a HIP call or kernel launch failed */
+  MDSS_EWORKSPACE = 5    /* workspace missing or smaller than mdss_workspace_bytes() */
+} mdss_status;
+
+/* row_status bits */
+#define MDSS_ROW_BAD_PROB 1  /* NaN, infinite or negative probability in the row (or in p/q at a draft) */
+#define MDSS_ROW_BAD_DRAFT 2 /* drafted / selected token out of [0, V) or with q = 0 */
+#define MDSS_ROW_SUPPORT 4   /* K = 3: more than s_max tokens with q > 0 */
+#define MDSS_ROW_FORCED 8    /* rejection with zero residual mass: the selected token is output */
+
+#define MDSS_MAX_V 8388608LL /* rows longer than 2^23 tokens are rejected with MDSS_ESHAPE */
+#define MDSS_MAX_B 65535LL   /* at most 65535 positions per call */
+#define MDSS_K3_MAX_SUPPORT 4096 /* largest s_max accepted for K = 3 */
+
+/* Bytes of device workspace mdss_induced_dist needs for these sizes
+ * (0 if the arguments are invalid).  The workspace is caller-owned scratch:
+ * its content on entry is ignored and on exit is unspecified. */
+size_t mdss_workspace_bytes(int64_t B, int64_t V, int32_t K, int32_t s_max);
+
+/* Induced distribution r of the selected token (step 1 of Theorem 1), for K
+ * i.i.d. drafts from q and the classical importance weights w = p/q:
+ *   r(y) = sum over ordered draft tuples x of prod_i q(x_i) * beta_y(x),
+ *   beta_y(x) = sum over i with x_i = y of w(x_i) / sum_j w(x_j)
+ * (Definition 1; the marginal in the proof of Theorem 1).  For K = 2 this is
+ * the pair form of the selected-token distribution (eq. p_Ieq0) with
+ * w_{k,i} = w(k)/(w(k)+w(i)).  The library evaluates it through the
+ * exchangeable form
+ *   r(y) = K p(y) sum_{x_2..x_K in supp q} prod_j q(x_j) / (w(y) + sum_j w(x_j))
+ * for q(y) > 0, p(y) > 0; r(y) = q(y) Q0^(K-1) for q(y) > 0, p(y) = 0 (Q0 =
+ * draft mass of such zero-weight tokens: all weights of such a tuple are zero
+ * and the index is then chosen uniformly); r(y) = 0 for q(y) = 0.
+ *   K = 2: O(n^2) pair sum per row, n = |supp q| <= V.
+ *   K = 3: O(n^3) triple sum, only for rows with n <= s_max (else the row is
+ *          flagged MDSS_ROW_SUPPORT): use it on top-s truncated draft rows.
+ * p, q: [B][V] in; r: [B][V] out (every entry written).  s_max is ignored for
+ * K = 2.  workspace: device buffer of at least mdss_workspace_bytes(B, V, K,
+ * s_max) bytes, 256-byte aligned. */
+mdss_status mdss_induced_dist(const float* p, const float* q, int64_t B, int64_t V, int32_t K, int32_t s_max,
+                              float* r, int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Importance weighted selection of one drafted index (Definition 1, index form
+ * with the classical weights).  For row b with drafts x_1..x_K (drafts is
+ * [B][K] int32), w_i = p(x_i)/q(x_i) in fp64, W = w_1 + ... + w_K, running
+ * sums C_i = w_1 + ... + w_i (left to right); the selected index is the
+ * smallest i with u_sel * W < C_i, or floor(u_sel * K) when W = 0.
+ * sel_index and sel_token ([B] int32 out) receive i (0-based) and x_i, or -1
+ * for a row whose drafts are invalid (MDSS_ROW_BAD_DRAFT / MDSS_ROW_BAD_PROB).
+ * u may be NULL (Philox, see above).  K in {2, 3}. */
+mdss_status mdss_select_intermediate(const float* p, const float* q, const int32_t* drafts, const float* u,
+                                     uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
+                                     int32_t* sel_index, int32_t* sel_token, int32_t* row_status, void* stream);
+
+/* Single-draft speculative sampling of the selected token Y = sel_token[b]
+ * against the target, with r as the proposal distribution (Algorithm 1):
+ *   accept iff u_acc * r(Y) < p(Y)   (fp64; exact for fp32 r, p and a 24-bit u),
+ *   otherwise output the smallest token j with C_j > u_res * Z, where
+ *   res(x) = max(0, p(x) - r(x)) in fp64, Z = sum_x res(x) and C_j the running
+ *   sum in ascending token id.  Z = 0 on a rejection: output Y, accepted = 1,
+ *   MDSS_ROW_FORCED.
+ * out_token [B] int32 and accepted [B] uint8 are outputs (-1 / 0 for an
+ * invalid row: Y = -1, Y out of range, or NaN/negative/inf in p or r).
+ * residual ([B][V] fp32, nullable) receives res for every row and
+ * residual_mass ([B] fp64, nullable) receives Z; when both are NULL, rows
+ * whose token is accepted do not read p or r beyond p(Y), r(Y). */
+mdss_status mdss_accept_or_resample(const float* p, const float* r, const int32_t* sel_token, const float* u,
+                                    uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t* out_token,
+                                    uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
+                                    void* stream);
+
+/* Static, thread-safe description of a status code. */
+const char* mdss_status_string(mdss_status s);
+
+/* ABI version of this header (incremented on incompatible changes). */
+int32_t mdss_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MDSS_H */

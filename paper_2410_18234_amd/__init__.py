@@ -1,0 +1,26 @@
+"""Multi-draft speculative sampling hot path on MI355X (gfx950).
+
+Thin Python binding over the C ABI of ``libmdss.so`` (declared in
+``include/mdss.h``): argument checks and marshalling only, every step runs in
+the HIP kernels of the library.  PyTorch supplies device buffers and the
+current HIP stream.
+
+Notation: ``p`` = target distribution, ``q`` = draft distribution (the paper
+writes them the other way round), both ``[B][V]`` fp32 on the GPU.
+"""
+from __future__ import annotations
+
+from .binding import (  # noqa: F401
+    MDSS_ROW_BAD_DRAFT,
+    MDSS_ROW_BAD_PROB,
+    MDSS_ROW_FORCED,
+    MDSS_ROW_SUPPORT,
+    MdssError,
+    accept_or_resample,
+    induced_dist,
+    library_path,
+    load_library,
+    select_intermediate,
+    step,
+    workspace_bytes,
+)

@@ -1,0 +1,197 @@
+"""ctypes binding of libmdss.so with the same names as the C ABI.
+
+Each function checks dtypes, devices, shapes and contiguity, passes raw device
+pointers and ``torch.cuda.current_stream()`` to the library, and raises
+``MdssError`` on a non-zero status.  There is no fallback: when the library
+is not built, or no GPU is present, the calls fail.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libmdss.so")
+
+MDSS_ROW_BAD_PROB = 1
+MDSS_ROW_BAD_DRAFT = 2
+MDSS_ROW_SUPPORT = 4
+MDSS_ROW_FORCED = 8
+
+_STATUS = {0: "MDSS_OK", 1: "MDSS_EINVAL", 2: "MDSS_ESHAPE", 3: "MDSS_EUNSUPPORTED", 4: "MDSS_EDEVICE",
+           5: "MDSS_EWORKSPACE"}
+
+_lib = None
+_lock = threading.Lock()
+_ws_cache = {}
+
+
+class MdssError(RuntimeError):
+    def __init__(self, fn: str, code: int, msg: str):
+        super().__init__(f"{fn} failed: {_STATUS.get(code, code)} ({msg})")
+        self.code = code
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libmdss.so and declare the C signatures (raises if it is not built)."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is not built; run __graft_entry__.build() first")
+        lib = ctypes.CDLL(_LIB_PATH)
+        P, i64, i32, u64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t
+        lib.mdss_workspace_bytes.argtypes = [i64, i64, i32, i32]
+        lib.mdss_workspace_bytes.restype = sz
+        lib.mdss_induced_dist.argtypes = [P, P, i64, i64, i32, i32, P, P, P, sz, P]
+        lib.mdss_select_intermediate.argtypes = [P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P]
+        lib.mdss_accept_or_resample.argtypes = [P, P, P, P, u64, u64, i64, i64, P, P, P, P, P, P]
+        for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample"):
+            getattr(lib, f).restype = ctypes.c_int
+        lib.mdss_status_string.argtypes = [ctypes.c_int]
+        lib.mdss_status_string.restype = ctypes.c_char_p
+        lib.mdss_abi_version.argtypes = []
+        lib.mdss_abi_version.restype = ctypes.c_int32
+        _lib = lib
+        return lib
+
+
+def _check(fn: str, code: int):
+    if code != 0:
+        raise MdssError(fn, code, load_library().mdss_status_string(code).decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape: tuple, device: torch.device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _pq(p: torch.Tensor, q: torch.Tensor):
+    if p.dim() != 2:
+        raise ValueError("p must be [B][V]")
+    if p.device.type != "cuda":
+        raise ValueError("p must be a GPU tensor")
+    B, V = p.shape
+    _need(p, "p", torch.float32, (B, V), p.device)
+    _need(q, "q", torch.float32, (B, V), p.device)
+    return B, V, p.device
+
+
+def workspace_bytes(B: int, V: int, K: int, s_max: int = 0) -> int:
+    return int(load_library().mdss_workspace_bytes(B, V, K, s_max))
+
+
+def _workspace(device: torch.device, nbytes: int) -> torch.Tensor:
+    key = (device, nbytes)
+    ws = _ws_cache.get(key)
+    if ws is None:
+        _ws_cache.clear()
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        _ws_cache[key] = ws
+    return ws
+
+
+def induced_dist(p: torch.Tensor, q: torch.Tensor, K: int, s_max: int = 0, r: Optional[torch.Tensor] = None,
+                 row_status: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """r [B][V] fp32: distribution of the token picked by importance-weighted selection among K drafts."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    need = int(lib.mdss_workspace_bytes(B, V, K, s_max))
+    if need == 0:
+        _check("mdss_workspace_bytes", 3 if K not in (2, 3) or (K == 3 and not 1 <= s_max <= 4096) else 2)
+    if workspace is None:
+        workspace = _workspace(dev, need)
+    elif workspace.dtype != torch.uint8 or workspace.device != dev or workspace.numel() < need:
+        raise ValueError(f"workspace must be a uint8 tensor on {dev} of at least {need} bytes")
+    _check("mdss_induced_dist",
+           lib.mdss_induced_dist(_ptr(p), _ptr(q), B, V, K, s_max, _ptr(r), _ptr(row_status), _ptr(workspace),
+                                 workspace.numel(), _stream(dev)))
+    return r
+
+
+def select_intermediate(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[torch.Tensor] = None,
+                        seed: int = 0, offset: int = 0, row_status: Optional[torch.Tensor] = None):
+    """(sel_index, sel_token): importance-weighted choice of one drafted token per position."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if drafts.dim() != 2:
+        raise ValueError("drafts must be [B][K]")
+    K = drafts.shape[1]
+    _need(drafts, "drafts", torch.int32, (B, K), dev)
+    if u is not None:
+        _need(u, "u", torch.float32, (B, 3), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    sel_index = torch.empty(B, dtype=torch.int32, device=dev)
+    sel_token = torch.empty(B, dtype=torch.int32, device=dev)
+    _check("mdss_select_intermediate",
+           lib.mdss_select_intermediate(_ptr(p), _ptr(q), _ptr(drafts), _ptr(u), ctypes.c_uint64(seed),
+                                        ctypes.c_uint64(offset), B, V, K, _ptr(sel_index), _ptr(sel_token),
+                                        _ptr(row_status), _stream(dev)))
+    return sel_index, sel_token
+
+
+def accept_or_resample(p: torch.Tensor, r: torch.Tensor, sel_token: torch.Tensor, u: Optional[torch.Tensor] = None,
+                       seed: int = 0, offset: int = 0, want_residual: bool = False, want_mass: bool = False,
+                       row_status: Optional[torch.Tensor] = None):
+    """(out_token, accepted, residual or None, residual_mass or None): Algorithm 1 with proposal r."""
+    lib = load_library()
+    B, V, dev = _pq(p, r)
+    _need(sel_token, "sel_token", torch.int32, (B,), dev)
+    if u is not None:
+        _need(u, "u", torch.float32, (B, 3), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    out = torch.empty(B, dtype=torch.int32, device=dev)
+    acc = torch.empty(B, dtype=torch.uint8, device=dev)
+    res = torch.empty((B, V), dtype=torch.float32, device=dev) if want_residual else None
+    mass = torch.empty(B, dtype=torch.float64, device=dev) if want_mass else None
+    _check("mdss_accept_or_resample",
+           lib.mdss_accept_or_resample(_ptr(p), _ptr(r), _ptr(sel_token), _ptr(u), ctypes.c_uint64(seed),
+                                       ctypes.c_uint64(offset), B, V, _ptr(out), _ptr(acc), _ptr(res), _ptr(mass),
+                                       _ptr(row_status), _stream(dev)))
+    return out, acc, res, mass
+
+
+def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[torch.Tensor] = None, seed: int = 0,
+         offset: int = 0, s_max: int = 0, want_residual: bool = False):
+    """The whole path for one batch: r, selection, accept / resample (three launches on one stream)."""
+    B = p.shape[0]
+    K = drafts.shape[1]
+    status = torch.zeros(B, dtype=torch.int32, device=p.device)
+    r = induced_dist(p, q, K, s_max=s_max, row_status=status)
+    sel_index, sel_token = select_intermediate(p, q, drafts, u, seed, offset, row_status=status)
+    out, acc, res, mass = accept_or_resample(p, r, sel_token, u, seed, offset, want_residual=want_residual,
+                                             want_mass=want_residual, row_status=status)
+    return {"r": r, "sel_index": sel_index, "sel_token": sel_token, "out_token": out, "accepted": acc,
+            "residual": res, "mass": mass, "status": status}

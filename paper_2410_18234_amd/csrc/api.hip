@@ -1,0 +1,86 @@
+// C ABI entry points: argument validation and launches on the caller's stream.
+#include "mdss.h"
+
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+
+namespace {
+
+constexpr int32_t kAbiVersion = 1;
+
+mdss_status check_shape(int64_t B, int64_t V) {
+  if (B < 1 || B > MDSS_MAX_B || V < 2 || V > MDSS_MAX_V) return MDSS_ESHAPE;
+  return MDSS_OK;
+}
+
+mdss_status check_k(int32_t K, int32_t s_max) {
+  if (K != 2 && K != 3) return MDSS_EUNSUPPORTED;
+  if (K == 3 && (s_max < 1 || s_max > MDSS_K3_MAX_SUPPORT)) return MDSS_EUNSUPPORTED;
+  return MDSS_OK;
+}
+
+mdss_status from_hip(hipError_t e) { return e == hipSuccess ? MDSS_OK : MDSS_EDEVICE; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t mdss_abi_version(void) { return kAbiVersion; }
+
+const char* mdss_status_string(mdss_status s) {
+  switch (s) {
+    case MDSS_OK: return "ok";
+    case MDSS_EINVAL: return "invalid argument (null pointer or bad value)";
+    case MDSS_ESHAPE: return "invalid shape (B outside [1, MDSS_MAX_B] or V outside [2, MDSS_MAX_V])";
+    case MDSS_EUNSUPPORTED: return "unsupported configuration (K not 2 or 3, or K = 3 with s_max out of range)";
+    case MDSS_EDEVICE: return "HIP error while launching";
+    case MDSS_EWORKSPACE: return "workspace missing or too small";
+  }
+  return "unknown status";
+}
+
+size_t mdss_workspace_bytes(int64_t B, int64_t V, int32_t K, int32_t s_max) {
+  if (check_shape(B, V) != MDSS_OK || check_k(K, s_max) != MDSS_OK) return 0;
+  const int P = mdss::choose_splits(B, V, K, s_max);
+  return mdss::workspace_bytes(B, V, K, s_max, P);
+}
+
+mdss_status mdss_induced_dist(const float* p, const float* q, int64_t B, int64_t V, int32_t K, int32_t s_max,
+                              float* r, int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!p || !q || !r) return MDSS_EINVAL;
+  mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  if ((s = check_k(K, s_max)) != MDSS_OK) return s;
+  const int P = mdss::choose_splits(B, V, K, s_max);
+  const size_t need = mdss::workspace_bytes(B, V, K, s_max, P);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) % 256) != 0)
+    return MDSS_EWORKSPACE;
+  mdss::Workspace ws;
+  mdss::carve_workspace(workspace, B, V, K, s_max, P, &ws);
+  return from_hip(mdss::launch_induced(p, q, B, V, K, s_max, r, row_status, ws, static_cast<hipStream_t>(stream)));
+}
+
+mdss_status mdss_select_intermediate(const float* p, const float* q, const int32_t* drafts, const float* u,
+                                     uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
+                                     int32_t* sel_index, int32_t* sel_token, int32_t* row_status, void* stream) {
+  if (!p || !q || !drafts || !sel_index || !sel_token) return MDSS_EINVAL;
+  mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  if (K != 2 && K != 3) return MDSS_EUNSUPPORTED;
+  return from_hip(mdss::launch_select(p, q, drafts, u, seed, offset, B, V, K, sel_index, sel_token, row_status,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+mdss_status mdss_accept_or_resample(const float* p, const float* r, const int32_t* sel_token, const float* u,
+                                    uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t* out_token,
+                                    uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
+                                    void* stream) {
+  if (!p || !r || !sel_token || !out_token || !accepted) return MDSS_EINVAL;
+  mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  return from_hip(mdss::launch_accept(p, r, sel_token, u, seed, offset, B, V, out_token, accepted, residual,
+                                      residual_mass, row_status, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,133 @@
+// Internal declarations of the gfx950 multi-draft selection library.
+// Notation: p = target, q = draft, w = p / q (importance weight).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mdss {
+
+// Per-row record written by the preparation kernel.
+struct alignas(32) RowHdr {
+  int32_t n;      // support size |{x : q(x) > 0}|
+  int32_t scale;  // exponent s: scaled weights w' = w * 2^s
+  int32_t mode;   // Mode below
+  int32_t flags;  // row status bits found by the preparation
+  double q0;      // draft mass of support tokens with p = 0 (zero weight)
+  double pad;
+};
+
+// How a row's pair sum is evaluated.
+enum Mode : int32_t {
+  kSkip = 0,    // flagged row (r already set to NaN)
+  kDirect = 1,  // one reciprocal per (query, pole)
+  kRat4 = 4,    // rational form over chunks of 4 poles
+  kRat8 = 8,    // rational form over chunks of 8 poles
+};
+
+constexpr int kRowBadProb = 1;
+constexpr int kRowBadDraft = 2;
+constexpr int kRowSupport = 4;
+constexpr int kRowForced = 8;
+
+// Workspace layout for mdss_induced_dist.
+struct Workspace {
+  RowHdr* hdr;      // [B]
+  int32_t* idx;     // [B][Sp] compacted token ids (ascending), -1 in the padding
+  float* wc;        // [B][Sp] compacted scaled weights w'
+  float* qc;        // [B][Sp] compacted draft probabilities
+  float* stream;    // [B][2 * Sp] pole stream (coefficients or (w', q) pairs)
+  double* part;     // [B][P][Sp] partial sums when the pole range is split, else unused
+  int64_t Sp;       // padded compacted row length (multiple of 8)
+  int32_t P;        // number of pole-range splits
+};
+
+size_t workspace_bytes(int64_t B, int64_t V, int K, int s_max, int P);
+void carve_workspace(void* base, int64_t B, int64_t V, int K, int s_max, int P, Workspace* ws);
+int choose_splits(int64_t B, int64_t V, int K, int s_max);
+
+hipError_t launch_induced(const float* p, const float* q, int64_t B, int64_t V, int K, int s_max, float* r,
+                          int32_t* row_status, const Workspace& ws, hipStream_t st);
+hipError_t launch_select(const float* p, const float* q, const int32_t* drafts, const float* u, uint64_t seed,
+                         uint64_t offset, int64_t B, int64_t V, int K, int32_t* sel_index, int32_t* sel_token,
+                         int32_t* row_status, hipStream_t st);
+hipError_t launch_accept(const float* p, const float* r, const int32_t* sel_token, const float* u, uint64_t seed,
+                         uint64_t offset, int64_t B, int64_t V, int32_t* out_token, uint8_t* accepted,
+                         float* residual, double* residual_mass, int32_t* row_status, hipStream_t st);
+
+// ---------------------------------------------------------------- device helpers
+__device__ __forceinline__ bool bad_prob(float v) { return !(v >= 0.0f) || isinf(v); }
+
+// Philox4x32-10 (Salmon et al., SC'11): ten rounds of the 4x32 S-box with the
+// published multipliers and Weyl key increments.
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint32_t lo0 = 0xD2511F53u * c[0], hi0 = __umulhi(0xD2511F53u, c[0]);
+    const uint32_t lo1 = 0xCD9E8D57u * c[2], hi1 = __umulhi(0xCD9E8D57u, c[2]);
+    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+}
+
+// Uniform j (0: select, 1: accept, 2: residual) of a position: from the
+// caller's array, else from Philox(seed, offset + b).
+__device__ __forceinline__ void position_uniforms(const float* u, uint64_t seed, uint64_t offset, int64_t b,
+                                                  float out[3]) {
+  if (u) {
+    out[0] = u[b * 3 + 0];
+    out[1] = u[b * 3 + 1];
+    out[2] = u[b * 3 + 2];
+    return;
+  }
+  const uint64_t pos = offset + (uint64_t)b;
+  uint32_t c[4] = {(uint32_t)pos, (uint32_t)(pos >> 32), 0u, 0u};
+  philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+#pragma unroll
+  for (int j = 0; j < 3; ++j) out[j] = (float)(c[j] >> 8) * 5.9604644775390625e-8f;  // 2^-24
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_min(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fminf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+// Inclusive prefix sum across the 64 lanes of a wave (Hillis-Steele, fixed order).
+__device__ __forceinline__ double wave_inclusive_scan(double v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double o = __shfl_up(v, off, 64);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+__device__ __forceinline__ int wave_inclusive_scan_int(int v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int o = __shfl_up(v, off, 64);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
+}  // namespace mdss

@@ -1,0 +1,589 @@
+// Induced distribution r of the importance-weighted selection (step 1 of the
+// canonical decomposition, Theorem 1), K = 2 and K = 3 i.i.d. drafts, gfx950.
+//
+// Notation: p = target, q = draft, w = p / q.  With the classical weights
+// (index probability proportional to w, stated after Definition 1), the
+// marginal of the selected token (proof of Theorem 1) is, by exchangeability
+// of the drafts,
+//   K = 2: r(y) = 2 p(y) S(y),  S(y) = sum_{x in supp} q(x) / (w(y) + w(x))
+//          (the pair form eq. p_Ieq0 with w_{k,i} = w(k)/(w(k)+w(i)));
+//   K = 3: r(y) = 3 p(y) sum_{x2,x3 in supp} q(x2) q(x3) / (w(y) + w(x2) + w(x3));
+//   r(y) = q(y) Q0^(K-1) when p(y) = 0 < q(y), and 0 when q(y) = 0.
+//
+// Both sums are Stieltjes sums sum_m c_m / (a + s_m) of a query a = w(y) over
+// the "poles" (s_m, c_m).  A reciprocal costs about three FMA issue slots on
+// gfx950, so poles are grouped in chunks of C (4 or 8) and a chunk is
+// evaluated as one rational function N(a) / D(a):
+//   D(a) = prod_c (a + s_c),   N(a) = sum_c c_c prod_{c' != c} (a + s_c'),
+// by Horner: 2C - 1 FMAs + 1 add + 1 reciprocal + 1 FMA per (query, chunk)
+// instead of C adds + C reciprocals + C FMAs.  All coefficients and the
+// argument are non-negative, so Horner has no cancellation; the weights are
+// scaled by a power of two per row (w' = w 2^s) so that D stays inside the
+// fp32 range, and rows whose weight range is too wide for that use one
+// reciprocal per pair.  Sums are accumulated in fp32 over one LDS tile
+// (<= 256 terms) and folded into fp64.
+#include "common.h"
+
+#include <math.h>
+
+#include <algorithm>
+
+namespace mdss {
+
+namespace {
+
+constexpr int kPrepThreads = 1024;
+constexpr int kSweepThreads = 256;
+constexpr int kTileFloats = 2048;  // pole-stream floats per LDS tile (8 KB)
+constexpr int kRat8MaxRange = 28;  // binary exponent range of the weights allowed for 8-pole chunks
+constexpr int kRat4MaxRange = 56;  // ... for 4-pole chunks
+
+__host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+__device__ inline int mode_chunk(int mode) { return mode == kRat8 ? 8 : (mode == kRat4 ? 4 : 1); }
+
+// ------------------------------------------------------------------ preparation
+// One workgroup per row: validate the row, count the support, find the draft
+// mass Q0 of zero-weight tokens and the weight range, choose the evaluation
+// mode and scale, compact the support (ascending token id) into the workspace
+// and write r for every token outside the support (and for flagged rows).
+__global__ __launch_bounds__(kPrepThreads) void prep_kernel(const float* __restrict__ p, const float* __restrict__ q,
+                                                             int64_t V, int K, int s_max, float* __restrict__ r,
+                                                             int32_t* __restrict__ row_status, Workspace ws) {
+  const int64_t b = blockIdx.x;
+  const float* pb = p + b * V;
+  const float* qb = q + b * V;
+  float* rb = r + b * V;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  constexpr int kWaves = kPrepThreads / 64;
+  __shared__ double s_q0[kWaves];
+  __shared__ int s_cnt[kWaves], s_bad[kWaves];
+  __shared__ float s_wmin[kWaves], s_wmax[kWaves];
+  __shared__ int s_scan[kWaves];
+  __shared__ RowHdr s_hdr;
+
+  int bad = 0, cnt = 0;
+  double q0 = 0.0;
+  float wmin = INFINITY, wmax = 0.0f;
+  for (int64_t x = tid; x < V; x += kPrepThreads) {
+    const float pv = pb[x], qv = qb[x];
+    bad |= (int)bad_prob(pv) | (int)bad_prob(qv);
+    if (qv > 0.0f) {
+      ++cnt;
+      if (pv == 0.0f) {
+        q0 += (double)qv;
+      } else {
+        const float w = pv / qv;
+        wmin = fminf(wmin, w);
+        wmax = fmaxf(wmax, w);
+      }
+    }
+  }
+  bad = wave_sum_int(bad);
+  cnt = wave_sum_int(cnt);
+  q0 = wave_sum(q0);
+  wmin = wave_min(wmin);
+  wmax = wave_max(wmax);
+  if (lane == 0) {
+    s_bad[wid] = bad;
+    s_cnt[wid] = cnt;
+    s_q0[wid] = q0;
+    s_wmin[wid] = wmin;
+    s_wmax[wid] = wmax;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int tb = 0, tc = 0;
+    double tq = 0.0;
+    float mn = INFINITY, mx = 0.0f;
+    for (int i = 0; i < kWaves; ++i) {
+      tb |= s_bad[i];
+      tc += s_cnt[i];
+      tq += s_q0[i];
+      mn = fminf(mn, s_wmin[i]);
+      mx = fmaxf(mx, s_wmax[i]);
+    }
+    RowHdr h;
+    h.n = tc;
+    h.q0 = tq;
+    h.pad = 0.0;
+    h.scale = 0;
+    h.flags = tb ? kRowBadProb : ((K == 3 && tc > s_max) ? kRowSupport : 0);
+    if (h.flags || tc == 0 || !(mx > 0.0f)) {
+      h.mode = kSkip;  // flagged, empty support, or every weight zero
+    } else {
+      int e_lo, e_hi;
+      frexpf(mn, &e_lo);
+      frexpf(mx, &e_hi);
+      const int range = e_hi - e_lo;
+      if (!isfinite(mx) || range > kRat4MaxRange) {
+        h.mode = kDirect;
+      } else {
+        h.mode = range <= kRat8MaxRange ? kRat8 : kRat4;
+        h.scale = -((e_lo + e_hi) >> 1);
+      }
+    }
+    s_hdr = h;
+    ws.hdr[b] = h;
+    if (row_status && h.flags) row_status[b] |= h.flags;
+  }
+  __syncthreads();
+  const RowHdr h = s_hdr;
+  if (h.flags) {
+    for (int64_t x = tid; x < V; x += kPrepThreads) rb[x] = NAN;
+    return;
+  }
+  const bool all_zero_weight = (h.mode == kSkip);  // support non-empty but every w == 0, or empty support
+  const double zero_w_factor = (K == 2) ? h.q0 : h.q0 * h.q0;
+
+  int32_t* idx = ws.idx + b * ws.Sp;
+  float* wc = ws.wc + b * ws.Sp;
+  float* qc = ws.qc + b * ws.Sp;
+  int running = 0;
+  for (int64_t base = 0; base < V; base += 4 * kPrepThreads) {
+    const int64_t x0 = base + 4 * (int64_t)tid;
+    float pv[4], qv[4];
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t x = x0 + i;
+      pv[i] = (x < V) ? pb[x] : 0.0f;
+      qv[i] = (x < V) ? qb[x] : 0.0f;
+      c += (qv[i] > 0.0f);
+    }
+    const int incl = wave_inclusive_scan_int(c, lane);
+    if (lane == 63) s_scan[wid] = incl;
+    __syncthreads();
+    int wave_off = 0, total = 0;
+    for (int i = 0; i < kWaves; ++i) {
+      wave_off += (i < wid) ? s_scan[i] : 0;
+      total += s_scan[i];
+    }
+    int off = running + wave_off + incl - c;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t x = x0 + i;
+      if (x >= V) break;
+      if (qv[i] > 0.0f) {
+        if (all_zero_weight) {
+          rb[x] = (float)((double)qv[i] * zero_w_factor);
+        } else {
+          idx[off] = (int32_t)x;
+          const float w = pv[i] / qv[i];
+          wc[off] = (h.mode == kDirect) ? w : ldexpf(w, h.scale);
+          qc[off] = qv[i];
+        }
+        ++off;
+      } else {
+        rb[x] = 0.0f;
+      }
+    }
+    running += total;
+    __syncthreads();  // s_scan is reused by the next tile
+  }
+  if (!all_zero_weight) {
+    const int npad = (int)round_up(h.n, 8);
+    for (int j = h.n + tid; j < npad; j += kPrepThreads) {
+      idx[j] = -1;
+      wc[j] = 0.0f;
+      qc[j] = 0.0f;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ pole stream
+// Per row, the poles (w', q) of the compacted support become a stream of
+// 2 floats per pole: for the rational modes chunk c of C poles holds
+// [e_1 .. e_C, n_{C-1} .. n_0] with D(a) = a^C + e_1 a^(C-1) + ... + e_C and
+// N(a) = n_{C-1} a^(C-1) + ... + n_0 (coefficients formed in fp64); for the
+// direct mode the stream is the interleaved pairs (w', q).  One thread per
+// group of 8 poles.
+__global__ __launch_bounds__(256) void pole_stream_kernel(Workspace ws) {
+  const int64_t b = blockIdx.y;
+  const RowHdr h = ws.hdr[b];
+  if (h.mode == kSkip) return;
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // group of 8 poles
+  const int npad = (int)round_up(h.n, 8);
+  if (8 * g >= npad) return;
+  const float* wc = ws.wc + b * ws.Sp + 8 * g;
+  const float* qc = ws.qc + b * ws.Sp + 8 * g;
+  float* out = ws.stream + b * 2 * ws.Sp + 16 * g;
+  if (h.mode == kDirect) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      out[2 * i] = wc[i];
+      out[2 * i + 1] = qc[i];
+    }
+    return;
+  }
+  const int C = h.mode;
+  for (int c0 = 0; c0 < 8; c0 += C) {
+    double d[9] = {1.0, 0, 0, 0, 0, 0, 0, 0, 0};  // D coefficients, d[k] multiplies a^(deg - k)
+    int deg = 0;
+    for (int c = 0; c < C; ++c) {  // D *= (a + w_c)
+      const double w = wc[c0 + c];
+      for (int k = deg + 1; k >= 1; --k) d[k] += d[k - 1] * w;
+      ++deg;
+    }
+    double nn[8] = {0, 0, 0, 0, 0, 0, 0, 0};  // N coefficients, nn[k] multiplies a^(C-1-k)
+    for (int c = 0; c < C; ++c) {
+      double t[8] = {1.0, 0, 0, 0, 0, 0, 0, 0};
+      int dg = 0;
+      for (int c2 = 0; c2 < C; ++c2) {
+        if (c2 == c) continue;
+        const double w = wc[c0 + c2];
+        for (int k = dg + 1; k >= 1; --k) t[k] += t[k - 1] * w;
+        ++dg;
+      }
+      const double qq = qc[c0 + c];
+      for (int k = 0; k < C; ++k) nn[k] += qq * t[k];
+    }
+    float* o = out + 2 * c0;
+    for (int k = 0; k < C; ++k) o[k] = (float)d[k + 1];
+    for (int k = 0; k < C; ++k) o[C + k] = (float)nn[k];
+  }
+}
+
+// ------------------------------------------------------------------ chunk evaluation
+// Adds the chunks of an LDS tile to R running fp32 sums.
+template <int R>
+__device__ __forceinline__ void sweep_rat4(const float4* __restrict__ t, int nchunks, const float (&a)[R],
+                                           float (&s)[R]) {
+  for (int c = 0; c < nchunks; ++c) {
+    const float4 e = t[2 * c], n = t[2 * c + 1];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      float D = a[i] + e.x;
+      D = fmaf(D, a[i], e.y);
+      D = fmaf(D, a[i], e.z);
+      D = fmaf(D, a[i], e.w);
+      float N = fmaf(n.x, a[i], n.y);
+      N = fmaf(N, a[i], n.z);
+      N = fmaf(N, a[i], n.w);
+      s[i] = fmaf(N, __builtin_amdgcn_rcpf(D), s[i]);
+    }
+  }
+}
+
+template <int R>
+__device__ __forceinline__ void sweep_rat8(const float4* __restrict__ t, int nchunks, const float (&a)[R],
+                                           float (&s)[R]) {
+  for (int c = 0; c < nchunks; ++c) {
+    const float4 e0 = t[4 * c], e1 = t[4 * c + 1], n0 = t[4 * c + 2], n1 = t[4 * c + 3];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      float D = a[i] + e0.x;
+      D = fmaf(D, a[i], e0.y);
+      D = fmaf(D, a[i], e0.z);
+      D = fmaf(D, a[i], e0.w);
+      D = fmaf(D, a[i], e1.x);
+      D = fmaf(D, a[i], e1.y);
+      D = fmaf(D, a[i], e1.z);
+      D = fmaf(D, a[i], e1.w);
+      float N = fmaf(n0.x, a[i], n0.y);
+      N = fmaf(N, a[i], n0.z);
+      N = fmaf(N, a[i], n0.w);
+      N = fmaf(N, a[i], n1.x);
+      N = fmaf(N, a[i], n1.y);
+      N = fmaf(N, a[i], n1.z);
+      N = fmaf(N, a[i], n1.w);
+      s[i] = fmaf(N, __builtin_amdgcn_rcpf(D), s[i]);
+    }
+  }
+}
+
+// Direct pairs (w', q), two per float4.
+template <int R>
+__device__ __forceinline__ void sweep_direct(const float4* __restrict__ t, int npairs2, const float (&a)[R],
+                                             float (&s)[R]) {
+  for (int c = 0; c < npairs2; ++c) {
+    const float4 v = t[c];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      s[i] = fmaf(v.y, __builtin_amdgcn_rcpf(a[i] + v.x), s[i]);
+      s[i] = fmaf(v.w, __builtin_amdgcn_rcpf(a[i] + v.z), s[i]);
+    }
+  }
+}
+
+__device__ __forceinline__ void write_r(int64_t b, int64_t V, int K, const RowHdr& h, int32_t y, double S,
+                                        const float* __restrict__ p, const float* __restrict__ q,
+                                        float* __restrict__ r) {
+  const float pv = p[b * V + y];
+  double v;
+  if (pv == 0.0f) {
+    v = (double)q[b * V + y] * (K == 2 ? h.q0 : h.q0 * h.q0);
+  } else {
+    v = (double)K * (double)pv * ldexp(S, h.scale);
+  }
+  r[b * V + y] = (float)v;
+}
+
+// ------------------------------------------------------------------ K = 2 sweep
+// grid (query blocks of 256 * R, pole splits P, rows B); each lane holds R
+// queries; the pole stream of the split is staged through LDS tile by tile
+// (double buffered through registers) and read back as broadcasts.
+template <int R>
+__global__ __launch_bounds__(kSweepThreads) void sweep_k2_kernel(const float* __restrict__ p,
+                                                                  const float* __restrict__ q, int64_t V,
+                                                                  float* __restrict__ r, Workspace ws) {
+  const int64_t b = blockIdx.z;
+  const int split = blockIdx.y;
+  const RowHdr h = ws.hdr[b];
+  if (h.mode == kSkip) return;
+  const int n = h.n;
+  const int y0 = blockIdx.x * (kSweepThreads * R);
+  if (y0 >= n) return;
+  const int tid = threadIdx.x;
+  // the pole stream is split in groups of 8 poles (16 floats: one 8-chunk, two
+  // 4-chunks or eight direct pairs), so every split and tile holds whole chunks
+  const int ngroups = (int)(round_up(n, 8) / 8);
+  const int g_lo = (int)((int64_t)ngroups * split / ws.P);
+  const int g_hi = (int)((int64_t)ngroups * (split + 1) / ws.P);
+  const float* stream = ws.stream + b * 2 * ws.Sp;
+  const int64_t f_lo = 16 * (int64_t)g_lo, f_hi = 16 * (int64_t)g_hi;  // float range of the split
+
+  float a[R];
+  double acc[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int j = y0 + i * kSweepThreads + tid;
+    a[i] = (j < n) ? ws.wc[b * ws.Sp + j] : 1.0f;
+    acc[i] = 0.0;
+  }
+  __shared__ float4 tile[kTileFloats / 4];
+  const float4* src = reinterpret_cast<const float4*>(stream);
+  float4 reg0 = make_float4(0.f, 0.f, 0.f, 0.f), reg1 = reg0;
+  auto fetch = [&](int64_t f0) {
+    const int64_t i0 = f0 / 4 + tid, i1 = i0 + kSweepThreads;
+    reg0 = (4 * i0 < f_hi) ? src[i0] : make_float4(0.f, 0.f, 0.f, 0.f);
+    reg1 = (4 * i1 < f_hi) ? src[i1] : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  if (f_lo < f_hi) fetch(f_lo);
+  for (int64_t f0 = f_lo; f0 < f_hi; f0 += kTileFloats) {
+    __syncthreads();  // previous tile fully consumed
+    tile[tid] = reg0;
+    tile[tid + kSweepThreads] = reg1;
+    __syncthreads();
+    if (f0 + kTileFloats < f_hi) fetch(f0 + kTileFloats);
+    const int nf = (int)min((int64_t)kTileFloats, f_hi - f0);
+    float s[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) s[i] = 0.0f;
+    if (h.mode == kRat8) {
+      sweep_rat8<R>(tile, nf / 16, a, s);
+    } else if (h.mode == kRat4) {
+      sweep_rat4<R>(tile, nf / 8, a, s);
+    } else {
+      // fold every 128 pairs to keep fp32 partial sums short
+      for (int g = 0; g < nf / 4; g += 64) {
+        float s2[R];
+#pragma unroll
+        for (int i = 0; i < R; ++i) s2[i] = 0.0f;
+        sweep_direct<R>(tile + g, min(64, nf / 4 - g), a, s2);
+#pragma unroll
+        for (int i = 0; i < R; ++i) acc[i] += (double)s2[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < R; ++i) acc[i] += (double)s[i];
+  }
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int j = y0 + i * kSweepThreads + tid;
+    if (j >= n) continue;
+    if (ws.P == 1) {
+      write_r(b, V, 2, h, ws.idx[b * ws.Sp + j], acc[i], p, q, r);
+    } else {
+      ws.part[(b * ws.P + split) * ws.Sp + j] = acc[i];
+    }
+  }
+}
+
+// ------------------------------------------------------------------ K = 3 sweep
+// r(y) = 3 p(y) sum_{x2} q(x2) [ q(x2)/(a2 + w(x2)) + 2 sum_{x3 > x2} q(x3)/(a2 + w(x3)) ],
+// a2 = w(y) + w(x2) (unordered {x2, x3} pairs, diagonal once).  The whole
+// compacted row (<= s_max poles) and its pole stream live in LDS; grid
+// (query blocks, x2 splits P, rows B) with x2 ranges of equal triangular work.
+template <int R>
+__global__ __launch_bounds__(kSweepThreads) void sweep_k3_kernel(Workspace ws) {
+  extern __shared__ float4 lds[];
+  const int64_t b = blockIdx.z;
+  const int split = blockIdx.y;
+  const RowHdr h = ws.hdr[b];
+  if (h.mode == kSkip) return;
+  const int n = h.n;
+  const int y0 = blockIdx.x * (kSweepThreads * R);
+  if (y0 >= n) return;
+  const int tid = threadIdx.x;
+  const int C = mode_chunk(h.mode);
+  const int npad = (int)round_up(n, 8);
+  const int nchunks = npad / C;  // includes the zero padding poles, which add nothing
+
+  // LDS: [w' (npad)] [q (npad)] [stream (2 npad)]
+  float* s_w = reinterpret_cast<float*>(lds);
+  float* s_q = s_w + npad;
+  float4* s_stream = reinterpret_cast<float4*>(s_q + npad);
+  const float* gw = ws.wc + b * ws.Sp;
+  const float* gq = ws.qc + b * ws.Sp;
+  const float4* gs = reinterpret_cast<const float4*>(ws.stream + b * 2 * ws.Sp);
+  for (int j = tid; j < npad; j += kSweepThreads) {
+    s_w[j] = gw[j];
+    s_q[j] = gq[j];
+  }
+  for (int j = tid; j < npad / 2; j += kSweepThreads) s_stream[j] = gs[j];
+  __syncthreads();
+
+  // x2 range with equal shares of sum_{x2} (n - x2) work
+  const double T = 0.5 * (double)n * (double)(n + 1);
+  auto bound = [&](int k) -> int {
+    if (k <= 0) return 0;
+    if (k >= ws.P) return n;
+    const double np = (double)n + 0.5;
+    const double m = np - sqrt(np * np - 2.0 * T * (double)k / (double)ws.P);
+    return min(n, max(0, (int)llround(m)));
+  };
+  const int x2_lo = bound(split), x2_hi = bound(split + 1);
+
+  float a[R];
+  double acc[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int j = y0 + i * kSweepThreads + tid;
+    a[i] = (j < n) ? s_w[j] : 1.0f;
+    acc[i] = 0.0;
+  }
+  for (int x2 = x2_lo; x2 < x2_hi; ++x2) {
+    const float w2 = s_w[x2], q2 = s_q[x2];
+    float a2[R], off[R], dg[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      a2[i] = a[i] + w2;
+      off[i] = 0.0f;
+      dg[i] = q2 * __builtin_amdgcn_rcpf(a2[i] + w2);
+    }
+    if (h.mode == kDirect) {
+      for (int x3 = x2 + 1; x3 < n; ++x3) {
+        const float w3 = s_w[x3], q3 = s_q[x3];
+#pragma unroll
+        for (int i = 0; i < R; ++i) off[i] = fmaf(q3, __builtin_amdgcn_rcpf(a2[i] + w3), off[i]);
+      }
+    } else {
+      const int c2 = x2 / C;
+      const int head_end = min((c2 + 1) * C, n);
+      for (int x3 = x2 + 1; x3 < head_end; ++x3) {
+        const float w3 = s_w[x3], q3 = s_q[x3];
+#pragma unroll
+        for (int i = 0; i < R; ++i) off[i] = fmaf(q3, __builtin_amdgcn_rcpf(a2[i] + w3), off[i]);
+      }
+      const int cstart = c2 + 1;
+      if (cstart < nchunks) {
+        if (C == 8) {
+          sweep_rat8<R>(s_stream + 4 * cstart, nchunks - cstart, a2, off);
+        } else {
+          sweep_rat4<R>(s_stream + 2 * cstart, nchunks - cstart, a2, off);
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < R; ++i) acc[i] += (double)q2 * ((double)dg[i] + 2.0 * (double)off[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int j = y0 + i * kSweepThreads + tid;
+    if (j < n) ws.part[(b * ws.P + split) * ws.Sp + j] = acc[i];
+  }
+}
+
+// Sum the P partial sums of each support entry in split order and write r.
+__global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__ p, const float* __restrict__ q,
+                                                        int64_t V, int K, float* __restrict__ r, Workspace ws) {
+  const int64_t b = blockIdx.y;
+  const RowHdr h = ws.hdr[b];
+  if (h.mode == kSkip) return;
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= h.n) return;
+  double S = 0.0;
+  for (int s = 0; s < ws.P; ++s) S += ws.part[(b * ws.P + s) * ws.Sp + j];
+  write_r(b, V, K, h, ws.idx[b * ws.Sp + j], S, p, q, r);
+}
+
+constexpr int kK2R = 8;
+constexpr int kK3R = 4;
+
+}  // namespace
+
+int choose_splits(int64_t B, int64_t V, int K, int s_max) {
+  if (K == 2) {
+    const int64_t yb = (V + kSweepThreads * kK2R - 1) / (kSweepThreads * kK2R);
+    const int64_t wgs = yb * B;
+    int64_t P = (2048 + wgs - 1) / wgs;
+    const int64_t max_p = std::max<int64_t>(1, V / 2048);  // keep >= 2048 poles per split
+    P = std::min<int64_t>(P, std::min<int64_t>(16, max_p));
+    return (int)std::max<int64_t>(P, 1);
+  }
+  const int64_t n = std::min<int64_t>(s_max, V);
+  const int64_t yb = (n + kSweepThreads * kK3R - 1) / (kSweepThreads * kK3R);
+  int64_t P = (4096 + yb * B - 1) / (yb * B);
+  P = std::min<int64_t>(P, std::min<int64_t>(32, std::max<int64_t>(1, n / 16)));
+  return (int)std::max<int64_t>(P, 1);
+}
+
+static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+static int64_t padded_len(int64_t V, int K, int s_max) {
+  return round_up(K == 2 ? V : std::min<int64_t>(s_max, V), 8);
+}
+
+size_t workspace_bytes(int64_t B, int64_t V, int K, int s_max, int P) {
+  const int64_t Sp = padded_len(V, K, s_max);
+  size_t t = align256(sizeof(RowHdr) * B);
+  t += 3 * align256(sizeof(float) * B * Sp);
+  t += align256(sizeof(float) * 2 * B * Sp);
+  const bool need_part = (K == 3) || P > 1;
+  if (need_part) t += align256(sizeof(double) * B * P * Sp);
+  return t;
+}
+
+void carve_workspace(void* base, int64_t B, int64_t V, int K, int s_max, int P, Workspace* ws) {
+  const int64_t Sp = padded_len(V, K, s_max);
+  char* c = static_cast<char*>(base);
+  ws->hdr = reinterpret_cast<RowHdr*>(c);
+  c += align256(sizeof(RowHdr) * B);
+  ws->idx = reinterpret_cast<int32_t*>(c);
+  c += align256(sizeof(float) * B * Sp);
+  ws->wc = reinterpret_cast<float*>(c);
+  c += align256(sizeof(float) * B * Sp);
+  ws->qc = reinterpret_cast<float*>(c);
+  c += align256(sizeof(float) * B * Sp);
+  ws->stream = reinterpret_cast<float*>(c);
+  c += align256(sizeof(float) * 2 * B * Sp);
+  ws->part = ((K == 3) || P > 1) ? reinterpret_cast<double*>(c) : nullptr;
+  ws->Sp = Sp;
+  ws->P = P;
+}
+
+hipError_t launch_induced(const float* p, const float* q, int64_t B, int64_t V, int K, int s_max, float* r,
+                          int32_t* row_status, const Workspace& ws, hipStream_t st) {
+  hipLaunchKernelGGL(prep_kernel, dim3((unsigned)B), dim3(kPrepThreads), 0, st, p, q, V, K, s_max, r, row_status,
+                     ws);
+  const int64_t groups = ws.Sp / 8;
+  hipLaunchKernelGGL(pole_stream_kernel, dim3((unsigned)((groups + 255) / 256), (unsigned)B), dim3(256), 0, st, ws);
+  if (K == 2) {
+    const int64_t yb = (V + kSweepThreads * kK2R - 1) / (kSweepThreads * kK2R);
+    hipLaunchKernelGGL(sweep_k2_kernel<kK2R>, dim3((unsigned)yb, (unsigned)ws.P, (unsigned)B), dim3(kSweepThreads),
+                       0, st, p, q, V, r, ws);
+  } else {
+    const int64_t yb = (ws.Sp + kSweepThreads * kK3R - 1) / (kSweepThreads * kK3R);
+    const size_t lds = sizeof(float) * 4 * ws.Sp;  // w', q, stream (2 per pole)
+    hipLaunchKernelGGL(sweep_k3_kernel<kK3R>, dim3((unsigned)yb, (unsigned)ws.P, (unsigned)B), dim3(kSweepThreads),
+                       lds, st, ws);
+  }
+  if (K == 3 || ws.P > 1) {
+    hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)((ws.Sp + 255) / 256), (unsigned)B), dim3(256), 0, st, p, q,
+                       V, K, r, ws);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mdss

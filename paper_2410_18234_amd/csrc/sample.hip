@@ -1,0 +1,336 @@
+// Selection of the intermediate token (Definition 1, index form with the
+// classical weights) and single-draft speculative sampling of that token
+// against the target (Algorithm 1), gfx950.
+//
+// Notation: p = target, q = draft, r = induced distribution of the selected
+// token (the proposal of Algorithm 1).  Decisions are taken in fp64 with the
+// uniforms as 24-bit dyadics, so the accept test u * r(Y) < p(Y) is exact.
+#include "common.h"
+
+#include <math.h>
+
+namespace mdss {
+
+namespace {
+
+// ------------------------------------------------------------------ selection
+// One thread per position: w_i = p(x_i)/q(x_i) (fp64), W = sum_i w_i left to
+// right, index = smallest i with u_sel * W < w_1 + ... + w_i; floor(u_sel K)
+// when W = 0.
+__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ p, const float* __restrict__ q,
+                                                      const int32_t* __restrict__ drafts,
+                                                      const float* __restrict__ u, uint64_t seed, uint64_t offset,
+                                                      int64_t B, int64_t V, int K, int32_t* __restrict__ sel_index,
+                                                      int32_t* __restrict__ sel_token,
+                                                      int32_t* __restrict__ row_status) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int st = 0;
+  double w[3] = {0.0, 0.0, 0.0};
+  int32_t x[3] = {0, 0, 0};
+  for (int i = 0; i < K; ++i) {
+    x[i] = drafts[b * K + i];
+    if (x[i] < 0 || (int64_t)x[i] >= V) {
+      st |= kRowBadDraft;
+      continue;
+    }
+    const float pv = p[b * V + x[i]], qv = q[b * V + x[i]];
+    if (bad_prob(pv) || bad_prob(qv)) {
+      st |= kRowBadProb;
+      continue;
+    }
+    if (!(qv > 0.0f)) {
+      st |= kRowBadDraft;
+      continue;
+    }
+    w[i] = (double)pv / (double)qv;
+  }
+  if (st) {
+    sel_index[b] = -1;
+    sel_token[b] = -1;
+    if (row_status) row_status[b] |= st;
+    return;
+  }
+  float uu[3];
+  position_uniforms(u, seed, offset, b, uu);
+  double W = 0.0;
+  for (int i = 0; i < K; ++i) W += w[i];
+  const double us = (double)uu[0];
+  int istar = K - 1;
+  if (W > 0.0) {
+    const double t = us * W;
+    double C = 0.0;
+    for (int i = 0; i < K; ++i) {
+      C += w[i];
+      if (t < C) {
+        istar = i;
+        break;
+      }
+    }
+  } else {
+    istar = (int)floor(us * (double)K);
+  }
+  istar = istar < 0 ? 0 : (istar >= K ? K - 1 : istar);  // only a uniform outside [0, 1) can leave the range
+  sel_index[b] = istar;
+  sel_token[b] = x[istar];
+}
+
+// ------------------------------------------------------------------ accept / resample
+// One workgroup of 16 waves per position.  Pass 1 streams the row in
+// super-tiles of 1024 tokens (wave w takes super-tiles w, w+16, ...), forms
+// res = max(0, p - r) in fp64, optionally stores it, and keeps each
+// super-tile's sum in LDS.  Wave 0 then scans the super-tile sums, finds the
+// super-tile where the running sum first exceeds u_res * Z and re-reads only
+// that one (four 256-token sub-tiles, each a lane scan) to locate the token.
+constexpr int kAccThreads = 1024;
+constexpr int kAccWaves = kAccThreads / 64;
+constexpr int kSuper = 1024;
+
+template <bool kVec>
+__device__ __forceinline__ void load4(const float* __restrict__ a, int64_t x0, int64_t V, float v[4]) {
+  if (kVec && x0 + 3 < V) {
+    const float4 t = *reinterpret_cast<const float4*>(a + x0);
+    v[0] = t.x;
+    v[1] = t.y;
+    v[2] = t.z;
+    v[3] = t.w;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = (x0 + i < V) ? a[x0 + i] : 0.0f;
+  }
+}
+
+__device__ __forceinline__ double residual_of(float pv, float rv) {
+  const double d = (double)pv - (double)rv;
+  return d > 0.0 ? d : 0.0;
+}
+
+template <bool kVec>
+__global__ __launch_bounds__(kAccThreads) void accept_kernel(
+    const float* __restrict__ p, const float* __restrict__ r, const int32_t* __restrict__ sel_token,
+    const float* __restrict__ u, uint64_t seed, uint64_t offset, int64_t V, int32_t* __restrict__ out_token,
+    uint8_t* __restrict__ accepted, float* __restrict__ residual, double* __restrict__ residual_mass,
+    int32_t* __restrict__ row_status) {
+  extern __shared__ double s_tile[];  // one sum per super-tile
+  __shared__ int s_bad;
+  const int64_t b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const float* pb = p + b * V;
+  const float* rb = r + b * V;
+  const int32_t Y = sel_token[b];
+  const bool y_ok = (Y >= 0) && ((int64_t)Y < V);
+  const float pY = y_ok ? pb[Y] : 0.0f, rY = y_ok ? rb[Y] : 0.0f;
+  const bool bad_y = !y_ok || bad_prob(pY) || bad_prob(rY);
+  float uu[3];
+  position_uniforms(u, seed, offset, b, uu);
+  const bool acc = !bad_y && ((double)uu[1] * (double)rY < (double)pY);
+  const bool need_pass = (residual != nullptr) || (residual_mass != nullptr) || (!acc && !bad_y);
+  if (!need_pass) {
+    if (tid == 0) {
+      out_token[b] = bad_y ? -1 : Y;
+      accepted[b] = acc ? 1 : 0;
+      if (bad_y && row_status) row_status[b] |= y_ok ? kRowBadProb : kRowBadDraft;
+    }
+    return;
+  }
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  const int64_t nsuper = (V + kSuper - 1) / kSuper;
+  float* resb = residual ? residual + b * V : nullptr;
+  int bad = 0;
+  for (int64_t st = wid; st < nsuper; st += kAccWaves) {
+    double local = 0.0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t x0 = st * kSuper + 256 * k + 4 * lane;
+      float pv[4], rv[4];
+      load4<kVec>(pb, x0, V, pv);
+      load4<kVec>(rb, x0, V, rv);
+      float rs[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        bad |= (int)(bad_prob(pv[i]) | bad_prob(rv[i]));
+        const double d = residual_of(pv[i], rv[i]);
+        rs[i] = (float)d;
+        local += d;
+      }
+      if (resb) {
+        if (kVec && x0 + 3 < V) {
+          *reinterpret_cast<float4*>(resb + x0) = make_float4(rs[0], rs[1], rs[2], rs[3]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (x0 + i < V) resb[x0 + i] = rs[i];
+        }
+      }
+    }
+    const double tot = wave_sum(local);
+    if (lane == 0) s_tile[st] = tot;
+  }
+  if (bad) atomicOr(&s_bad, 1);
+  __syncthreads();
+  if (wid != 0) return;
+
+  // wave 0: totals, prefix over super-tiles, draw
+  const bool row_bad = s_bad != 0;
+  const int64_t per_lane = (nsuper + 63) / 64;
+  const int64_t s_lo = lane * per_lane, s_hi = (s_lo + per_lane < nsuper) ? s_lo + per_lane : nsuper;
+  double lane_sum = 0.0;
+  for (int64_t s = s_lo; s < s_hi; ++s) lane_sum += s_tile[s];
+  const double incl = wave_inclusive_scan(lane_sum, lane);
+  const double Z = __shfl(incl, 63, 64);
+  double excl = __shfl_up(incl, 1, 64);
+  if (lane == 0) excl = 0.0;
+  if (lane == 0 && residual_mass) residual_mass[b] = row_bad ? (double)NAN : Z;
+
+  if (row_bad || bad_y) {
+    if (lane == 0) {
+      out_token[b] = -1;
+      accepted[b] = 0;
+      if (row_status) row_status[b] |= (row_bad || y_ok) ? kRowBadProb : kRowBadDraft;
+    }
+    return;
+  }
+  if (acc) {
+    if (lane == 0) {
+      out_token[b] = Y;
+      accepted[b] = 1;
+    }
+    return;
+  }
+  if (!(Z > 0.0)) {
+    if (lane == 0) {
+      out_token[b] = Y;
+      accepted[b] = 1;
+      if (row_status) row_status[b] |= kRowForced;
+    }
+    return;
+  }
+  const double thr = (double)uu[2] * Z;
+  // first super-tile whose running sum exceeds thr
+  int64_t my_st = -1;
+  double my_prev = 0.0, run = excl;
+  for (int64_t s = s_lo; s < s_hi; ++s) {
+    const double prev = run;
+    run += s_tile[s];
+    if (run > thr) {
+      my_st = s;
+      my_prev = prev;
+      break;
+    }
+  }
+  const unsigned long long hit = __ballot(my_st >= 0);
+  int64_t st_star;
+  double prev_star;
+  if (hit) {
+    const int src = __ffsll((long long)hit) - 1;
+    st_star = __shfl(my_st, src, 64);
+    prev_star = __shfl(my_prev, src, 64);
+  } else {
+    // rounding put u_res * Z at or past every running sum: last super-tile with mass
+    int64_t last = -1;
+    for (int64_t s = s_lo; s < s_hi; ++s)
+      if (s_tile[s] > 0.0) last = s;
+    int64_t m = last;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const int64_t o = __shfl_xor(m, off, 64);
+      m = o > m ? o : m;
+    }
+    st_star = m;
+    prev_star = thr;  // forces the in-tile search to its own fallback
+  }
+  if (st_star < 0) {  // unreachable with Z > 0; keeps every load in bounds
+    if (lane == 0) {
+      out_token[b] = Y;
+      accepted[b] = 1;
+      if (row_status) row_status[b] |= kRowForced;
+    }
+    return;
+  }
+  // locate the token inside super-tile st_star
+  double base = prev_star;
+  int32_t found = -1;
+  for (int k = 0; k < 4 && found < 0; ++k) {
+    const int64_t x0 = st_star * kSuper + 256 * k + 4 * lane;
+    float pv[4], rv[4];
+    load4<kVec>(pb, x0, V, pv);
+    load4<kVec>(rb, x0, V, rv);
+    double rs[4], local = 0.0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      rs[i] = residual_of(pv[i], rv[i]);
+      local += rs[i];
+    }
+    const double li = wave_inclusive_scan(local, lane);
+    double le = __shfl_up(li, 1, 64);
+    if (lane == 0) le = 0.0;
+    double c = base + le;
+    int my = -1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      c += rs[i];
+      if (my < 0 && rs[i] > 0.0 && c > thr) my = i;
+    }
+    const unsigned long long h2 = __ballot(my >= 0);
+    if (h2) {
+      const int src = __ffsll((long long)h2) - 1;
+      const int mi = __shfl(my, src, 64);
+      found = (int32_t)(st_star * kSuper + 256 * k + 4 * src + mi);
+    } else {
+      base += __shfl(li, 63, 64);
+    }
+  }
+  if (found < 0) {
+    // fallback: last token of the super-tile with positive residual
+    int64_t last = -1;
+    for (int k = 0; k < 4; ++k) {
+      const int64_t x0 = st_star * kSuper + 256 * k + 4 * lane;
+      float pv[4], rv[4];
+      load4<kVec>(pb, x0, V, pv);
+      load4<kVec>(rb, x0, V, rv);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (x0 + i < V && residual_of(pv[i], rv[i]) > 0.0) last = x0 + i;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const int64_t o = __shfl_xor(last, off, 64);
+      last = o > last ? o : last;
+    }
+    found = (int32_t)last;
+  }
+  if (lane == 0) {
+    out_token[b] = found;
+    accepted[b] = 0;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select(const float* p, const float* q, const int32_t* drafts, const float* u, uint64_t seed,
+                         uint64_t offset, int64_t B, int64_t V, int K, int32_t* sel_index, int32_t* sel_token,
+                         int32_t* row_status, hipStream_t st) {
+  hipLaunchKernelGGL(select_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, p, q, drafts, u, seed, offset,
+                     B, V, K, sel_index, sel_token, row_status);
+  return hipGetLastError();
+}
+
+hipError_t launch_accept(const float* p, const float* r, const int32_t* sel_token, const float* u, uint64_t seed,
+                         uint64_t offset, int64_t B, int64_t V, int32_t* out_token, uint8_t* accepted,
+                         float* residual, double* residual_mass, int32_t* row_status, hipStream_t st) {
+  const int64_t nsuper = (V + kSuper - 1) / kSuper;
+  const size_t lds = sizeof(double) * (size_t)nsuper;
+  const bool vec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(r) |
+                                     reinterpret_cast<uintptr_t>(residual)) % 16 == 0);
+  if (vec) {
+    hipLaunchKernelGGL(accept_kernel<true>, dim3((unsigned)B), dim3(kAccThreads), lds, st, p, r, sel_token, u, seed,
+                       offset, V, out_token, accepted, residual, residual_mass, row_status);
+  } else {
+    hipLaunchKernelGGL(accept_kernel<false>, dim3((unsigned)B), dim3(kAccThreads), lds, st, p, r, sel_token, u, seed,
+                       offset, V, out_token, accepted, residual, residual_mass, row_status);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mdss

@@ -1,0 +1,83 @@
+"""The C-ABI library loads, exports what include/mdss.h declares, and rejects bad
+arguments synchronously, before any launch (no GPU needed: nothing is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mdss.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2410_18234_amd import load_library
+    return load_library()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mdss_[a-z_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported(lib):
+    names = _declared_functions()
+    assert {"mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample",
+            "mdss_workspace_bytes", "mdss_status_string", "mdss_abi_version"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in mdss.h but not exported"
+
+
+def test_status_strings_and_version(lib):
+    assert lib.mdss_abi_version() == 1
+    for code in range(6):
+        assert len(lib.mdss_status_string(code)) > 0
+    assert lib.mdss_status_string(99) == b"unknown status"
+
+
+def test_workspace_sizes(lib):
+    assert lib.mdss_workspace_bytes(256, 32000, 2, 0) > 256 * 32000 * 20
+    assert lib.mdss_workspace_bytes(256, 32000, 3, 1024) > 0
+    assert lib.mdss_workspace_bytes(256, 32000, 3, 1024) < lib.mdss_workspace_bytes(256, 32000, 2, 0)
+    assert lib.mdss_workspace_bytes(0, 32000, 2, 0) == 0
+    assert lib.mdss_workspace_bytes(4, 1, 2, 0) == 0
+    assert lib.mdss_workspace_bytes(4, 16, 4, 0) == 0
+    assert lib.mdss_workspace_bytes(4, 16, 3, 0) == 0
+    assert lib.mdss_workspace_bytes(4, 16, 3, 5000) == 0
+    assert lib.mdss_workspace_bytes(4, (1 << 23) + 1, 2, 0) == 0
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
+
+
+def test_induced_dist_argument_errors(lib):
+    f = lib.mdss_induced_dist
+    ws_ok = lib.mdss_workspace_bytes(4, 16, 2, 0)
+    assert f(None, FAKE, 4, 16, 2, 0, FAKE, None, FAKE, ws_ok, None) == 1
+    assert f(FAKE, FAKE, 0, 16, 2, 0, FAKE, None, FAKE, ws_ok, None) == 2
+    assert f(FAKE, FAKE, 4, 1, 2, 0, FAKE, None, FAKE, ws_ok, None) == 2
+    assert f(FAKE, FAKE, 4, 16, 5, 0, FAKE, None, FAKE, ws_ok, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 3, 0, FAKE, None, FAKE, ws_ok, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 2, 0, FAKE, None, None, ws_ok, None) == 5
+    assert f(FAKE, FAKE, 4, 16, 2, 0, FAKE, None, FAKE, ws_ok - 1, None) == 5
+    assert f(FAKE, FAKE, 4, 16, 2, 0, FAKE, None, ctypes.c_void_p(0x1010), ws_ok, None) == 5  # misaligned
+
+
+def test_select_and_accept_argument_errors(lib):
+    s = lib.mdss_select_intermediate
+    assert s(FAKE, FAKE, None, None, 0, 0, 4, 16, 2, FAKE, FAKE, None, None) == 1
+    assert s(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 4, FAKE, FAKE, None, None) == 3
+    assert s(FAKE, FAKE, FAKE, None, 0, 0, -1, 16, 2, FAKE, FAKE, None, None) == 2
+    a = lib.mdss_accept_or_resample
+    assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, None, FAKE, None, None, None, None) == 1
+    assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 1, FAKE, FAKE, None, None, None, None) == 2
+
+
+def test_python_binding_refuses_cpu_tensors():
+    import torch
+    import paper_2410_18234_amd as mdss
+    p = torch.full((2, 8), 0.125)
+    with pytest.raises(ValueError):
+        mdss.induced_dist(p, p, 2)
