@@ -85,6 +85,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline leg")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample size (0: one per core, 2 rounds)")
     ap.add_argument("--resample-reps", type=int, default=20)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); positions are independent, "
@@ -122,6 +124,12 @@ def main():
         out, acc, _, _ = mdss.accept_or_resample(p, r, sel_token, u, row_status=status)
         return out, acc
 
+    if args.copy_calibration:
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()

@@ -198,6 +198,61 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(const float* __restr
 // N(a) = n_{C-1} a^(C-1) + ... + n_0 (coefficients formed in fp64); for the
 // direct mode the stream is the interleaved pairs (w', q).  One thread per
 // group of 8 poles.
+// Coefficients of one chunk of C poles, fp64: D(a) = prod_c (a + w_c) and
+// N(a) = sum_c q_c prod_{c' != c} (a + w_c'), written highest power first
+// (the leading 1 of D is implicit).  N uses prefix and suffix products of the
+// linear factors, so every coefficient is a sum of non-negative terms.
+template <int C>
+__device__ __forceinline__ void chunk_coefficients(const float* __restrict__ w, const float* __restrict__ q,
+                                                   float* __restrict__ o) {
+  // pre[c]: prod_{c' < c} (a + w_c'), degree c; coefficient k multiplies a^(c - k)
+  double pre[C][C];
+  double suf[C + 1][C + 1];
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int k = 0; k < C; ++k) pre[c][k] = (c == 0 && k == 0) ? 1.0 : 0.0;
+#pragma unroll
+  for (int c = 1; c < C; ++c) {
+    const double wc = w[c - 1];
+#pragma unroll
+    for (int k = 0; k < C; ++k) pre[c][k] = (k <= c - 1 ? pre[c - 1][k] : 0.0) + (k >= 1 ? pre[c - 1][k - 1] * wc : 0.0);
+  }
+  // suf[c]: prod_{c' >= c} (a + w_c'), degree C - c
+#pragma unroll
+  for (int k = 0; k <= C; ++k) suf[C][k] = (k == 0) ? 1.0 : 0.0;
+#pragma unroll
+  for (int c = C - 1; c >= 0; --c) {
+    const double wc = w[c];
+#pragma unroll
+    for (int k = 0; k <= C; ++k)
+      suf[c][k] = (k <= C - c - 1 ? suf[c + 1][k] : 0.0) + (k >= 1 ? suf[c + 1][k - 1] * wc : 0.0);
+  }
+  // D = suf[0] (degree C, leading 1)
+#pragma unroll
+  for (int k = 1; k <= C; ++k) o[k - 1] = (float)suf[0][k];
+  // N = sum_c q_c pre[c] * suf[c + 1]   (degree C - 1)
+  double nn[C];
+#pragma unroll
+  for (int k = 0; k < C; ++k) nn[k] = 0.0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const double qc = q[c];
+    // pre[c] has degree c, suf[c+1] degree C-1-c; product coefficient k (k = 0..C-1)
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      if (i > c) continue;
+#pragma unroll
+      for (int j = 0; j < C; ++j) {
+        if (j > C - 1 - c) continue;
+        nn[i + j] += qc * pre[c][i] * suf[c + 1][j];
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < C; ++k) o[C + k] = (float)nn[k];
+}
+
 __global__ __launch_bounds__(256) void pole_stream_kernel(Workspace ws) {
   const int64_t b = blockIdx.y;
   const RowHdr h = ws.hdr[b];
@@ -214,33 +269,11 @@ __global__ __launch_bounds__(256) void pole_stream_kernel(Workspace ws) {
       out[2 * i] = wc[i];
       out[2 * i + 1] = qc[i];
     }
-    return;
-  }
-  const int C = h.mode;
-  for (int c0 = 0; c0 < 8; c0 += C) {
-    double d[9] = {1.0, 0, 0, 0, 0, 0, 0, 0, 0};  // D coefficients, d[k] multiplies a^(deg - k)
-    int deg = 0;
-    for (int c = 0; c < C; ++c) {  // D *= (a + w_c)
-      const double w = wc[c0 + c];
-      for (int k = deg + 1; k >= 1; --k) d[k] += d[k - 1] * w;
-      ++deg;
-    }
-    double nn[8] = {0, 0, 0, 0, 0, 0, 0, 0};  // N coefficients, nn[k] multiplies a^(C-1-k)
-    for (int c = 0; c < C; ++c) {
-      double t[8] = {1.0, 0, 0, 0, 0, 0, 0, 0};
-      int dg = 0;
-      for (int c2 = 0; c2 < C; ++c2) {
-        if (c2 == c) continue;
-        const double w = wc[c0 + c2];
-        for (int k = dg + 1; k >= 1; --k) t[k] += t[k - 1] * w;
-        ++dg;
-      }
-      const double qq = qc[c0 + c];
-      for (int k = 0; k < C; ++k) nn[k] += qq * t[k];
-    }
-    float* o = out + 2 * c0;
-    for (int k = 0; k < C; ++k) o[k] = (float)d[k + 1];
-    for (int k = 0; k < C; ++k) o[C + k] = (float)nn[k];
+  } else if (h.mode == kRat8) {
+    chunk_coefficients<8>(wc, qc, out);
+  } else {
+    chunk_coefficients<4>(wc, qc, out);
+    chunk_coefficients<4>(wc + 4, qc + 4, out + 8);
   }
 }
 
