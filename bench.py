@@ -148,7 +148,7 @@ def main():
     flops = pair_flops(w["q"], K)
     achieved = flops / (r_ms * 1e-3) / 1e12
     digest = kernel_source_digest()
-    sweep_name = "sweep_k2_kernel" if K == 2 else "sweep_k3_kernel"
+    sweep_name = "sweep_k2_mfma_kernel" if K == 2 else "sweep_k3_kernel"
     roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / FP32_PEAK_TFLOPS, 4), "traffic": counted_traffic(sweep_name, digest),
                 "kernel": f"mdss_induced_dist ({sweep_name} + preparation)", "avg_ms": round(r_ms, 4),

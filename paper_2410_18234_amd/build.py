@@ -17,6 +17,9 @@ HIPCC_FLAGS = [
     # no implicit contraction: every FMA in the kernels is written explicitly,
     # and the fp64 decisions of selection / acceptance round each operation
     "-ffp-contract=off",
+    # matrix-core results go straight to VGPRs (no AGPR copies before the VALU reads them)
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
+    "-DMDSS_MFMA_MT=2", "-DMDSS_MFMA_NW=4",
     "-Wall",
 ]
 

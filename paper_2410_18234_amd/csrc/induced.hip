@@ -37,6 +37,13 @@ constexpr int kSweepThreads = 256;
 constexpr int kTileFloats = 2048;  // pole-stream floats per LDS tile (8 KB)
 constexpr int kRat8MaxRange = 28;  // binary exponent range of the weights allowed for 8-pole chunks
 constexpr int kRat4MaxRange = 56;  // ... for 4-pole chunks
+constexpr int kBlockPolesPrep = 128;  // K = 2 rows are padded to whole 128-pole blocks
+#ifndef MDSS_MFMA_MT
+#define MDSS_MFMA_MT 2
+#endif
+#ifndef MDSS_MFMA_NW
+#define MDSS_MFMA_NW 4
+#endif
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -182,7 +189,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(const float* __restr
     __syncthreads();  // s_scan is reused by the next tile
   }
   if (!all_zero_weight) {
-    const int npad = (int)round_up(h.n, 8);
+    const int npad = (int)round_up(h.n, K == 2 ? kBlockPolesPrep : 8);
     for (int j = h.n + tid; j < npad; j += kPrepThreads) {
       idx[j] = -1;
       wc[j] = 0.0f;
@@ -253,27 +260,62 @@ __device__ __forceinline__ void chunk_coefficients(const float* __restrict__ w, 
   for (int k = 0; k < C; ++k) o[C + k] = (float)nn[k];
 }
 
-__global__ __launch_bounds__(256) void pole_stream_kernel(Workspace ws) {
+__global__ __launch_bounds__(256) void pole_stream_kernel(Workspace ws, int K) {
   const int64_t b = blockIdx.y;
   const RowHdr h = ws.hdr[b];
   if (h.mode == kSkip) return;
-  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // group of 8 poles
+  const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const float* wc = ws.wc + b * ws.Sp;
+  const float* qc = ws.qc + b * ws.Sp;
+  float* out = ws.stream + b * 2 * ws.Sp;
+  if (K == 2 && h.mode != kDirect) {
+    // matrix-core block layout, one thread per chunk (see sweep_k2_mfma_kernel)
+    const int C = h.mode;
+    const int64_t npad = round_up(h.n, kBlockPolesPrep);
+    if (u * C >= npad) return;
+    float o[16];
+    if (C == 8) {
+      chunk_coefficients<8>(wc + 8 * u, qc + 8 * u, o);
+      float* ob = out + 256 * (u / 16);
+      const int j = (int)(u % 16);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float* d = ob + 4 * (16 * g + j);
+        d[0] = o[7 - g];
+        d[1] = o[3 - g];
+        d[2] = o[15 - g];
+        d[3] = o[11 - g];
+      }
+    } else {
+      chunk_coefficients<4>(wc + 4 * u, qc + 4 * u, o);
+      float* ob = out + 256 * (u / 32);
+      const int sub = (int)((u % 32) / 16), j = (int)(u % 16);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float* d = ob + 4 * (16 * g + j) + 2 * sub;
+        d[0] = o[3 - g];
+        d[1] = o[7 - g];
+      }
+    }
+    return;
+  }
+  // groups of 8 poles: interleaved (w', q) pairs, or K = 3 chunks stored contiguously
   const int npad = (int)round_up(h.n, 8);
-  if (8 * g >= npad) return;
-  const float* wc = ws.wc + b * ws.Sp + 8 * g;
-  const float* qc = ws.qc + b * ws.Sp + 8 * g;
-  float* out = ws.stream + b * 2 * ws.Sp + 16 * g;
+  if (8 * u >= npad) return;
+  const float* w8 = wc + 8 * u;
+  const float* q8 = qc + 8 * u;
+  float* o8 = out + 16 * u;
   if (h.mode == kDirect) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      out[2 * i] = wc[i];
-      out[2 * i + 1] = qc[i];
+      o8[2 * i] = w8[i];
+      o8[2 * i + 1] = q8[i];
     }
   } else if (h.mode == kRat8) {
-    chunk_coefficients<8>(wc, qc, out);
+    chunk_coefficients<8>(w8, q8, o8);
   } else {
-    chunk_coefficients<4>(wc, qc, out);
-    chunk_coefficients<4>(wc + 4, qc + 4, out + 8);
+    chunk_coefficients<4>(w8, q8, o8);
+    chunk_coefficients<4>(w8 + 4, q8 + 4, o8 + 8);
   }
 }
 
@@ -352,24 +394,24 @@ __device__ __forceinline__ void write_r(int64_t b, int64_t V, int K, const RowHd
   r[b * V + y] = (float)v;
 }
 
-// ------------------------------------------------------------------ K = 2 sweep
-// grid (query blocks of 256 * R, pole splits P, rows B); each lane holds R
-// queries; the pole stream of the split is staged through LDS tile by tile
-// (double buffered through registers) and read back as broadcasts.
+// ------------------------------------------------------------------ K = 2 sweep, direct rows
+// Rows whose weight range is too wide for the rational form: one reciprocal
+// per (query, pole).  grid (query blocks of 256 * R, pole splits P, rows B);
+// each lane holds R queries; the (w', q) pairs of the split are staged through
+// LDS tile by tile (double buffered through registers) and read as broadcasts.
 template <int R>
-__global__ __launch_bounds__(kSweepThreads) void sweep_k2_kernel(const float* __restrict__ p,
+__global__ __launch_bounds__(kSweepThreads) void sweep_k2_direct_kernel(const float* __restrict__ p,
                                                                   const float* __restrict__ q, int64_t V,
                                                                   float* __restrict__ r, Workspace ws) {
   const int64_t b = blockIdx.z;
   const int split = blockIdx.y;
   const RowHdr h = ws.hdr[b];
-  if (h.mode == kSkip) return;
+  if (h.mode != kDirect) return;
   const int n = h.n;
   const int y0 = blockIdx.x * (kSweepThreads * R);
   if (y0 >= n) return;
   const int tid = threadIdx.x;
-  // the pole stream is split in groups of 8 poles (16 floats: one 8-chunk, two
-  // 4-chunks or eight direct pairs), so every split and tile holds whole chunks
+  // the pairs are split in groups of 8 poles (16 floats)
   const int ngroups = (int)(round_up(n, 8) / 8);
   const int g_lo = (int)((int64_t)ngroups * split / ws.P);
   const int g_hi = (int)((int64_t)ngroups * (split + 1) / ws.P);
@@ -400,26 +442,15 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_k2_kernel(const float* __
     __syncthreads();
     if (f0 + kTileFloats < f_hi) fetch(f0 + kTileFloats);
     const int nf = (int)min((int64_t)kTileFloats, f_hi - f0);
-    float s[R];
+    // fold every 128 pairs to keep fp32 partial sums short
+    for (int g = 0; g < nf / 4; g += 64) {
+      float s2[R];
 #pragma unroll
-    for (int i = 0; i < R; ++i) s[i] = 0.0f;
-    if (h.mode == kRat8) {
-      sweep_rat8<R>(tile, nf / 16, a, s);
-    } else if (h.mode == kRat4) {
-      sweep_rat4<R>(tile, nf / 8, a, s);
-    } else {
-      // fold every 128 pairs to keep fp32 partial sums short
-      for (int g = 0; g < nf / 4; g += 64) {
-        float s2[R];
+      for (int i = 0; i < R; ++i) s2[i] = 0.0f;
+      sweep_direct<R>(tile + g, min(64, nf / 4 - g), a, s2);
 #pragma unroll
-        for (int i = 0; i < R; ++i) s2[i] = 0.0f;
-        sweep_direct<R>(tile + g, min(64, nf / 4 - g), a, s2);
-#pragma unroll
-        for (int i = 0; i < R; ++i) acc[i] += (double)s2[i];
-      }
+      for (int i = 0; i < R; ++i) acc[i] += (double)s2[i];
     }
-#pragma unroll
-    for (int i = 0; i < R; ++i) acc[i] += (double)s[i];
   }
 #pragma unroll
   for (int i = 0; i < R; ++i) {
@@ -430,6 +461,203 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_k2_kernel(const float* __
     } else {
       ws.part[(b * ws.P + split) * ws.Sp + j] = acc[i];
     }
+  }
+}
+
+// ------------------------------------------------------------------ K = 2 sweep, matrix cores
+// For a block of 16 queries (rows i) and 16 chunks (columns j) the chunk
+// polynomials are a small dense contraction over the power index m:
+//   D[i][j] = a_i^C + sum_{m<C} a_i^m e_{C-m}(j),   N[i][j] = sum_{m<C} a_i^m n_m(j),
+// evaluated with v_mfma_f32_16x16x4_f32 (A[i][m] = a_i^m from registers, B from
+// the pole stream, the monic a^C term as the accumulator input); the VALU then
+// adds N/D per output.  Pole stream layout, per block of 128 poles (1 KB),
+// lane l (g = l / 16, j = l % 16) owns 4 floats at 4 l:
+//   C = 8 (16 chunks):  e_{8-g}(j), e_{4-g}(j), n_g(j), n_{4+g}(j)
+//   C = 4 (32 chunks):  e_{4-g}(j), n_g(j), e_{4-g}(16+j), n_g(16+j)
+// Each wave holds 4 M-tiles (64 queries); a workgroup of 4 waves covers 256
+// queries and streams the row's blocks through LDS.  Workgroups are mapped so
+// that each of the 8 XCDs takes a contiguous range (the query blocks of a row
+// share one XCD's L2).
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBlockPoles = 128;    // poles per 1 KB block
+constexpr int kMfmaTileBlocks = 16; // blocks per LDS tile (16 KB)
+constexpr int kMfmaMT = MDSS_MFMA_MT;  // 16-query M-tiles per wave
+constexpr int kMfmaNW = MDSS_MFMA_NW;  // waves per workgroup
+constexpr int kMfmaThreads = 64 * kMfmaNW;
+constexpr int kMfmaQueries = 16 * kMfmaMT * kMfmaNW;  // queries per workgroup
+
+// D and N of one block for the MT M-tiles (all MFMAs issued before any result is read).
+template <int C, int MT>
+__device__ __forceinline__ void mfma_block(const float4 bf, const float (&A0)[MT], const float (&A1)[MT],
+                                           const f32x4 (&cinit)[MT], f32x4 (&D)[2 * MT], f32x4 (&N)[2 * MT]) {
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  if (C == 8) {
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      D[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.x, cinit[t], 0, 0, 0);
+      N[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.z, zero, 0, 0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      D[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A1[t], bf.y, D[t], 0, 0, 0);
+      N[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A1[t], bf.w, N[t], 0, 0, 0);
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      D[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.x, cinit[t], 0, 0, 0);
+      N[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.y, zero, 0, 0, 0);
+      D[t + MT] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.z, cinit[t], 0, 0, 0);
+      N[t + MT] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.w, zero, 0, 0, 0);
+    }
+  }
+}
+
+// acc += N / D for the outputs of one block
+template <int C, int MT>
+__device__ __forceinline__ void mfma_consume(const f32x4 (&D)[2 * MT], const f32x4 (&N)[2 * MT],
+                                             float (&acc)[MT][4]) {
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      acc[t][r] = fmaf(N[t][r], __builtin_amdgcn_rcpf(D[t][r]), acc[t][r]);
+      if (C == 4) acc[t][r] = fmaf(N[t + MT][r], __builtin_amdgcn_rcpf(D[t + MT][r]), acc[t][r]);
+    }
+}
+
+template <int C, int MT>
+__device__ __forceinline__ void mfma_sweep(const float4* __restrict__ src, int nblocks, int tid, int lane,
+                                           const float (&A0)[MT], const float (&A1)[MT], const f32x4 (&cinit)[MT],
+                                           double (&acc64)[MT][4], float4* __restrict__ tile) {
+  constexpr int kLoads = kMfmaTileBlocks * 64 / kMfmaThreads;  // float4 per thread per tile
+  float4 reg[kLoads];
+  auto fetch = [&](int blk0) {
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) {
+      const int i = k * kMfmaThreads + tid;  // float4 index inside the tile
+      reg[k] = (blk0 * 64 + i < nblocks * 64) ? src[(int64_t)blk0 * 64 + i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  if (nblocks > 0) fetch(0);
+  for (int blk0 = 0; blk0 < nblocks; blk0 += kMfmaTileBlocks) {
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) tile[k * kMfmaThreads + tid] = reg[k];
+    __syncthreads();
+    if (blk0 + kMfmaTileBlocks < nblocks) fetch(blk0 + kMfmaTileBlocks);
+    const int nb = min(kMfmaTileBlocks, nblocks - blk0);
+    float acc[MT][4];
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[t][r] = 0.0f;
+    // software pipeline: the MFMAs of block bi + 1 are issued before the VALU work of block bi
+    f32x4 D0[2 * MT], N0[2 * MT], D1[2 * MT], N1[2 * MT];
+    mfma_block<C, MT>(tile[lane], A0, A1, cinit, D0, N0);
+    int bi = 1;
+    for (; bi + 1 < nb; bi += 2) {
+      mfma_block<C, MT>(tile[bi * 64 + lane], A0, A1, cinit, D1, N1);
+      mfma_consume<C, MT>(D0, N0, acc);
+      mfma_block<C, MT>(tile[(bi + 1) * 64 + lane], A0, A1, cinit, D0, N0);
+      mfma_consume<C, MT>(D1, N1, acc);
+    }
+    if (bi < nb) {
+      mfma_block<C, MT>(tile[bi * 64 + lane], A0, A1, cinit, D1, N1);
+      mfma_consume<C, MT>(D0, N0, acc);
+      mfma_consume<C, MT>(D1, N1, acc);
+    } else {
+      mfma_consume<C, MT>(D0, N0, acc);
+    }
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc64[t][r] += (double)acc[t][r];
+  }
+}
+
+__global__ __launch_bounds__(kMfmaThreads) void sweep_k2_mfma_kernel(const float* __restrict__ p,
+                                                                      const float* __restrict__ q, int64_t V,
+                                                                      float* __restrict__ r, Workspace ws, int nqb,
+                                                                      int64_t total) {
+  constexpr int MT = kMfmaMT;
+  // XCD-aware mapping: hardware block h runs on XCD h % 8; give each XCD a contiguous logical range
+  const int64_t hw = blockIdx.x;
+  const int64_t per = total / 8, rem = total % 8, x = hw % 8;
+  const int64_t logical = x * per + (x < rem ? x : rem) + hw / 8;
+  const int qb = (int)(logical % nqb);
+  const int64_t rest = logical / nqb;
+  const int split = (int)(rest % ws.P);
+  const int64_t b = rest / ws.P;
+  const RowHdr h = ws.hdr[b];
+  if (h.mode != kRat8 && h.mode != kRat4) return;
+  const int n = h.n;
+  const int q0 = qb * kMfmaQueries;
+  if (q0 >= n) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, col = lane & 15;
+  const int C = h.mode;
+  const float* wc = ws.wc + b * ws.Sp;
+
+  // A[i][m] = a_i^m (row i = col, m = g and 4 + g); accumulator input a^C for rows 4 g + r
+  float A0[MT], A1[MT];
+  f32x4 cinit[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    const int base = q0 + 16 * (MT * wave + t);
+    const float a = (base + col < n) ? wc[base + col] : 1.0f;
+    float pw = 1.0f;
+    for (int m = 0; m < g; ++m) pw *= a;
+    const float a2 = a * a, a4 = a2 * a2;
+    A0[t] = pw;
+    A1[t] = pw * a4;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int qi = base + 4 * g + rr;
+      const float ar = (qi < n) ? wc[qi] : 1.0f;
+      const float ar2 = ar * ar, ar4 = ar2 * ar2;
+      cinit[t][rr] = (C == 8) ? ar4 * ar4 : ar4;
+    }
+  }
+  const int nblocks = (int)(round_up(n, kBlockPoles) / kBlockPoles);
+  const int b_lo = (int)((int64_t)nblocks * split / ws.P);
+  const int b_hi = (int)((int64_t)nblocks * (split + 1) / ws.P);
+  const float4* src = reinterpret_cast<const float4*>(ws.stream + b * 2 * ws.Sp) + (int64_t)b_lo * 64;
+  __shared__ float4 tile[kMfmaTileBlocks * 64];
+  double acc64[MT][4];
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) acc64[t][rr] = 0.0;
+  if (C == 8) {
+    mfma_sweep<8, MT>(src, b_hi - b_lo, tid, lane, A0, A1, cinit, acc64, tile);
+  } else {
+    mfma_sweep<4, MT>(src, b_hi - b_lo, tid, lane, A0, A1, cinit, acc64, tile);
+  }
+  // each query row is spread over the 16 lanes of its group (one chunk column each)
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      double v = acc64[t][rr];
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off, 64);
+      acc64[t][rr] = v;
+    }
+  if (col == 0) {
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int qi = q0 + 16 * (MT * wave + t) + 4 * g + rr;
+        if (qi >= n) continue;
+        if (ws.P == 1) {
+          write_r(b, V, 2, h, ws.idx[b * ws.Sp + qi], acc64[t][rr], p, q, r);
+        } else {
+          ws.part[(b * ws.P + split) * ws.Sp + qi] = acc64[t][rr];
+        }
+      }
   }
 }
 
@@ -548,7 +776,7 @@ constexpr int kK3R = 4;
 
 int choose_splits(int64_t B, int64_t V, int K, int s_max) {
   if (K == 2) {
-    const int64_t yb = (V + kSweepThreads * kK2R - 1) / (kSweepThreads * kK2R);
+    const int64_t yb = (V + kMfmaQueries - 1) / kMfmaQueries;
     const int64_t wgs = yb * B;
     int64_t P = (2048 + wgs - 1) / wgs;
     const int64_t max_p = std::max<int64_t>(1, V / 2048);  // keep >= 2048 poles per split
@@ -565,7 +793,7 @@ int choose_splits(int64_t B, int64_t V, int K, int s_max) {
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 static int64_t padded_len(int64_t V, int K, int s_max) {
-  return round_up(K == 2 ? V : std::min<int64_t>(s_max, V), 8);
+  return K == 2 ? round_up(V, kBlockPoles) : round_up(std::min<int64_t>(s_max, V), 8);
 }
 
 size_t workspace_bytes(int64_t B, int64_t V, int K, int s_max, int P) {
@@ -600,12 +828,17 @@ hipError_t launch_induced(const float* p, const float* q, int64_t B, int64_t V, 
                           int32_t* row_status, const Workspace& ws, hipStream_t st) {
   hipLaunchKernelGGL(prep_kernel, dim3((unsigned)B), dim3(kPrepThreads), 0, st, p, q, V, K, s_max, r, row_status,
                      ws);
-  const int64_t groups = ws.Sp / 8;
-  hipLaunchKernelGGL(pole_stream_kernel, dim3((unsigned)((groups + 255) / 256), (unsigned)B), dim3(256), 0, st, ws);
+  const int64_t units = ws.Sp / 4;  // at most one thread per 4 poles
+  hipLaunchKernelGGL(pole_stream_kernel, dim3((unsigned)((units + 255) / 256), (unsigned)B), dim3(256), 0, st, ws,
+                     K);
   if (K == 2) {
+    const int nqb = (int)((V + kMfmaQueries - 1) / kMfmaQueries);
+    const int64_t total = (int64_t)nqb * ws.P * B;
+    hipLaunchKernelGGL(sweep_k2_mfma_kernel, dim3((unsigned)total), dim3(kMfmaThreads), 0, st, p, q, V, r, ws, nqb,
+                       total);
     const int64_t yb = (V + kSweepThreads * kK2R - 1) / (kSweepThreads * kK2R);
-    hipLaunchKernelGGL(sweep_k2_kernel<kK2R>, dim3((unsigned)yb, (unsigned)ws.P, (unsigned)B), dim3(kSweepThreads),
-                       0, st, p, q, V, r, ws);
+    hipLaunchKernelGGL(sweep_k2_direct_kernel<kK2R>, dim3((unsigned)yb, (unsigned)ws.P, (unsigned)B),
+                       dim3(kSweepThreads), 0, st, p, q, V, r, ws);
   } else {
     const int64_t yb = (ws.Sp + kSweepThreads * kK3R - 1) / (kSweepThreads * kK3R);
     const size_t lds = sizeof(float) * 4 * ws.Sp;  // w', q, stream (2 per pole)
