@@ -19,7 +19,7 @@ HIPCC_FLAGS = [
     "-ffp-contract=off",
     # matrix-core results go straight to VGPRs (no AGPR copies before the VALU reads them)
     "-mllvm", "-amdgpu-mfma-vgpr-form=1",
-    "-DMDSS_MFMA_MT=2", "-DMDSS_MFMA_NW=4",
+    "-DMDSS_MFMA_MT=4", "-DMDSS_MFMA_NW=4",
     "-Wall",
 ]
 

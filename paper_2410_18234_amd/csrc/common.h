@@ -36,7 +36,8 @@ struct Workspace {
   int32_t* idx;     // [B][Sp] compacted token ids (ascending), -1 in the padding
   float* wc;        // [B][Sp] compacted scaled weights w'
   float* qc;        // [B][Sp] compacted draft probabilities
-  float* stream;    // [B][2 * Sp] pole stream (coefficients or (w', q) pairs)
+  float* stream;    // [B][ld] pole stream: (w', q) pairs, chunk coefficients, or packed bf16 MFMA operands
+  int64_t ld;       // floats per row of the pole stream (8 Sp for K = 2, 2 Sp for K = 3)
   double* part;     // [B][P][Sp] partial sums when the pole range is split, else unused
   int64_t Sp;       // padded compacted row length (multiple of 8)
   int32_t P;        // number of pole-range splits

@@ -39,7 +39,7 @@ constexpr int kRat8MaxRange = 28;  // binary exponent range of the weights allow
 constexpr int kRat4MaxRange = 56;  // ... for 4-pole chunks
 constexpr int kBlockPolesPrep = 128;  // K = 2 rows are padded to whole 128-pole blocks
 #ifndef MDSS_MFMA_MT
-#define MDSS_MFMA_MT 2
+#define MDSS_MFMA_MT 4
 #endif
 #ifndef MDSS_MFMA_NW
 #define MDSS_MFMA_NW 4
@@ -267,38 +267,8 @@ __global__ __launch_bounds__(256) void pole_stream_kernel(Workspace ws, int K) {
   const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const float* wc = ws.wc + b * ws.Sp;
   const float* qc = ws.qc + b * ws.Sp;
-  float* out = ws.stream + b * 2 * ws.Sp;
-  if (K == 2 && h.mode != kDirect) {
-    // matrix-core block layout, one thread per chunk (see sweep_k2_mfma_kernel)
-    const int C = h.mode;
-    const int64_t npad = round_up(h.n, kBlockPolesPrep);
-    if (u * C >= npad) return;
-    float o[16];
-    if (C == 8) {
-      chunk_coefficients<8>(wc + 8 * u, qc + 8 * u, o);
-      float* ob = out + 256 * (u / 16);
-      const int j = (int)(u % 16);
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        float* d = ob + 4 * (16 * g + j);
-        d[0] = o[7 - g];
-        d[1] = o[3 - g];
-        d[2] = o[15 - g];
-        d[3] = o[11 - g];
-      }
-    } else {
-      chunk_coefficients<4>(wc + 4 * u, qc + 4 * u, o);
-      float* ob = out + 256 * (u / 32);
-      const int sub = (int)((u % 32) / 16), j = (int)(u % 16);
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        float* d = ob + 4 * (16 * g + j) + 2 * sub;
-        d[0] = o[3 - g];
-        d[1] = o[7 - g];
-      }
-    }
-    return;
-  }
+  float* out = ws.stream + b * ws.ld;
+  if (K == 2 && h.mode != kDirect) return;  // packed by pole_pack_mfma_kernel
   // groups of 8 poles: interleaved (w', q) pairs, or K = 3 chunks stored contiguously
   const int npad = (int)round_up(h.n, 8);
   if (8 * u >= npad) return;
@@ -415,7 +385,7 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_k2_direct_kernel(const fl
   const int ngroups = (int)(round_up(n, 8) / 8);
   const int g_lo = (int)((int64_t)ngroups * split / ws.P);
   const int g_hi = (int)((int64_t)ngroups * (split + 1) / ws.P);
-  const float* stream = ws.stream + b * 2 * ws.Sp;
+  const float* stream = ws.stream + b * ws.ld;
   const int64_t f_lo = 16 * (int64_t)g_lo, f_hi = 16 * (int64_t)g_hi;  // float range of the split
 
   float a[R];
@@ -465,110 +435,213 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_k2_direct_kernel(const fl
 }
 
 // ------------------------------------------------------------------ K = 2 sweep, matrix cores
-// For a block of 16 queries (rows i) and 16 chunks (columns j) the chunk
+// For a tile of 16 queries (rows i) and 16 chunks (columns j) the chunk
 // polynomials are a small dense contraction over the power index m:
-//   D[i][j] = a_i^C + sum_{m<C} a_i^m e_{C-m}(j),   N[i][j] = sum_{m<C} a_i^m n_m(j),
-// evaluated with v_mfma_f32_16x16x4_f32 (A[i][m] = a_i^m from registers, B from
-// the pole stream, the monic a^C term as the accumulator input); the VALU then
-// adds N/D per output.  Pole stream layout, per block of 128 poles (1 KB),
-// lane l (g = l / 16, j = l % 16) owns 4 floats at 4 l:
-//   C = 8 (16 chunks):  e_{8-g}(j), e_{4-g}(j), n_g(j), n_{4+g}(j)
-//   C = 4 (32 chunks):  e_{4-g}(j), n_g(j), e_{4-g}(16+j), n_g(16+j)
-// Each wave holds 4 M-tiles (64 queries); a workgroup of 4 waves covers 256
-// queries and streams the row's blocks through LDS.  Workgroups are mapped so
-// that each of the 8 XCDs takes a contiguous range (the query blocks of a row
-// share one XCD's L2).
+//   D[i][j] = a_i^C + sum_{m<C} a_i^m d_m(j),   N[i][j] = sum_{m<C} a_i^m n_m(j)
+// (d_m = e_{C-m}).  It runs on the bf16 matrix cores at fp32 accuracy: every
+// fp32 operand x is split exactly into three bf16 parts x = x_h + x_m + x_l,
+// and each product keeps the six cross terms above 2^-24 relative size,
+//   a b ~ a_h b_h + a_h b_m + a_m b_h + a_h b_l + a_m b_m + a_l b_h,
+// laid out along the contraction index k = 6 m + slot.  Products of bf16
+// values are exact in the fp32 accumulator; every term of D and N is
+// non-negative up to the small signed split corrections, so there is no
+// cancellation.  The monic a^C is the accumulator input.  The VALU then adds
+// N/D per output (one reciprocal per query and chunk).
+//   C = 8: k in [0, 48): v_mfma_f32_16x16x32_bf16 for k < 32, then
+//          v_mfma_f32_16x16x16_bf16 for k in [32, 48); 128-pole blocks, 3 KB.
+//   C = 4: k in [0, 24), padded to 32: one 16x16x32 MFMA; 64-pole blocks, 2 KB.
+// Block layout: planes of 64 lanes x 16 bytes (conflict-free ds_read_b128);
+// lane L = 16 g + j holds the operand column j for k in its lane group g.
+//   C = 8: plane 0 d (k = 8 g + e), plane 1 n (k = 8 g + e), plane 2 d then n (k = 32 + 4 g + e)
+//   C = 4: plane 0 d (k = 8 g + e), plane 1 n (k = 8 g + e)
+// Each wave holds MT M-tiles; workgroups are remapped so that each of the 8
+// XCDs takes a contiguous range (the query blocks of a row share one L2).
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBlockPoles = 128;    // poles per 1 KB block
-constexpr int kMfmaTileBlocks = 16; // blocks per LDS tile (16 KB)
-constexpr int kMfmaMT = MDSS_MFMA_MT;  // 16-query M-tiles per wave
-constexpr int kMfmaNW = MDSS_MFMA_NW;  // waves per workgroup
+constexpr int kBlockPoles = 128;        // poles per padded K = 2 block (C = 8 block)
+constexpr int kMfmaTileF4 = 1536;       // LDS tile: 24 KB of operand blocks
+constexpr int kMfmaMT = MDSS_MFMA_MT;   // 16-query M-tiles per wave
+constexpr int kMfmaNW = MDSS_MFMA_NW;   // waves per workgroup
 constexpr int kMfmaThreads = 64 * kMfmaNW;
 constexpr int kMfmaQueries = 16 * kMfmaMT * kMfmaNW;  // queries per workgroup
 
-// D and N of one block for the MT M-tiles (all MFMAs issued before any result is read).
+// exact split x = h + m + l into bf16 parts (each residual is exact in fp32)
+__device__ __forceinline__ void split3(float x, float (&c)[3]) {
+  const __bf16 h = (__bf16)x;
+  const float r1 = x - (float)h;
+  const __bf16 m = (__bf16)r1;
+  const float r2 = r1 - (float)m;
+  c[0] = (float)h;
+  c[1] = (float)m;
+  c[2] = (float)(__bf16)r2;
+}
+// product slots along k: (a part, b part) = (h,h) (h,m) (m,h) (h,l) (m,m) (l,h)
+__device__ __forceinline__ int slot_a(int s) { return (s == 2 || s == 4) ? 1 : (s == 5 ? 2 : 0); }
+__device__ __forceinline__ int slot_b(int s) { return (s == 1 || s == 4) ? 1 : (s == 3 ? 2 : 0); }
+__device__ __forceinline__ float pick3(const float (&c)[3], int i) { return i == 0 ? c[0] : (i == 1 ? c[1] : c[2]); }
+
+__device__ __forceinline__ float4 pack_bf16x8(const float (&v)[8]) {
+  bf16x8 t;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) t[e] = (__bf16)v[e];
+  return __builtin_bit_cast(float4, t);
+}
+
+// Packs the rational chunks of a K = 2 row into the bf16 operand blocks.
+// Thread block of 256 threads = 256 chunks = 16 operand blocks; phase 1: one
+// thread per chunk forms its coefficients (fp64, rounded to fp32) into LDS;
+// phase 2: every thread packs float4s of the blocks.
+__global__ __launch_bounds__(256) void pole_pack_mfma_kernel(Workspace ws) {
+  const int64_t b = blockIdx.y;
+  const RowHdr h = ws.hdr[b];
+  if (h.mode != kRat8 && h.mode != kRat4) return;
+  const int C = h.mode;
+  const int tid = threadIdx.x;
+  const int64_t npad = round_up(h.n, kBlockPoles);
+  const int64_t nch = npad / C;
+  const int64_t c0 = (int64_t)blockIdx.x * 256;
+  if (c0 >= nch) return;
+  __shared__ float s_d[256][8];  // d_m = e_{C-m}
+  __shared__ float s_n[256][8];  // n_m
+  const int64_t c = c0 + tid;
+  const float* wc = ws.wc + b * ws.Sp;
+  const float* qc = ws.qc + b * ws.Sp;
+  if (c < nch) {
+    float o[16];
+    if (C == 8) {
+      chunk_coefficients<8>(wc + 8 * c, qc + 8 * c, o);
+    } else {
+      chunk_coefficients<4>(wc + 4 * c, qc + 4 * c, o);
+    }
+    // o[k - 1] = e_k, o[C + k] = coefficient of a^(C - 1 - k) in N
+    for (int m = 0; m < C; ++m) {
+      s_d[tid][m] = o[C - 1 - m];
+      s_n[tid][m] = o[2 * C - 1 - m];
+    }
+  }
+  __syncthreads();
+  const int F = (C == 8) ? 192 : 128;         // float4 per operand block
+  const int64_t nblk = nch / 16;              // blocks in the row
+  const int64_t blk0 = c0 / 16;               // first block of this thread block
+  float4* out = reinterpret_cast<float4*>(ws.stream + b * ws.ld);
+  for (int o4 = tid; o4 < 16 * F; o4 += 256) {
+    const int blk = o4 / F, rem = o4 % F;
+    if (blk0 + blk >= nblk) break;
+    const int plane = rem / 64, L = rem % 64, g = L / 16, j = L % 16;
+    const int ch = 16 * blk + j;  // chunk inside this thread block
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      int k;
+      bool is_n;
+      if (plane < 2) {
+        k = 8 * g + e;
+        is_n = (plane == 1);
+      } else {
+        k = 32 + 4 * g + (e & 3);
+        is_n = (e >= 4);
+      }
+      const int m = k / 6, sl = k % 6;
+      float val = 0.0f;
+      if (m < C) {
+        float parts[3];
+        split3(is_n ? s_n[ch][m] : s_d[ch][m], parts);
+        val = pick3(parts, slot_b(sl));
+      }
+      v[e] = val;
+    }
+    out[(blk0 + blk) * F + rem] = pack_bf16x8(v);
+  }
+}
+
+// D and N of one operand block for the MT M-tiles (all MFMAs issued before any result is read).
 template <int C, int MT>
-__device__ __forceinline__ void mfma_block(const float4 bf, const float (&A0)[MT], const float (&A1)[MT],
-                                           const f32x4 (&cinit)[MT], f32x4 (&D)[2 * MT], f32x4 (&N)[2 * MT]) {
+__device__ __forceinline__ void mfma_block(const float4* __restrict__ blk, int lane, const bf16x8 (&AX)[MT],
+                                           const bf16x4 (&AY)[MT], const f32x4 (&cinit)[MT], f32x4 (&D)[MT],
+                                           f32x4 (&N)[MT]) {
   const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  const bf16x8 dx = __builtin_bit_cast(bf16x8, blk[lane]);
+  const bf16x8 nx = __builtin_bit_cast(bf16x8, blk[64 + lane]);
   if (C == 8) {
+    const float4 yy = blk[128 + lane];
+    const bf16x4 dy = __builtin_bit_cast(bf16x4, make_float2(yy.x, yy.y));
+    const bf16x4 ny = __builtin_bit_cast(bf16x4, make_float2(yy.z, yy.w));
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-      D[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.x, cinit[t], 0, 0, 0);
-      N[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.z, zero, 0, 0, 0);
+      D[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(AX[t], dx, cinit[t], 0, 0, 0);
+      N[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(AX[t], nx, zero, 0, 0, 0);
     }
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-      D[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A1[t], bf.y, D[t], 0, 0, 0);
-      N[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A1[t], bf.w, N[t], 0, 0, 0);
+      D[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(AY[t], dy, D[t], 0, 0, 0);
+      N[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(AY[t], ny, N[t], 0, 0, 0);
     }
   } else {
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-      D[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.x, cinit[t], 0, 0, 0);
-      N[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.y, zero, 0, 0, 0);
-      D[t + MT] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.z, cinit[t], 0, 0, 0);
-      N[t + MT] = __builtin_amdgcn_mfma_f32_16x16x4f32(A0[t], bf.w, zero, 0, 0, 0);
+      D[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(AX[t], dx, cinit[t], 0, 0, 0);
+      N[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(AX[t], nx, zero, 0, 0, 0);
     }
   }
 }
 
 // acc += N / D for the outputs of one block
-template <int C, int MT>
-__device__ __forceinline__ void mfma_consume(const f32x4 (&D)[2 * MT], const f32x4 (&N)[2 * MT],
-                                             float (&acc)[MT][4]) {
+template <int MT>
+__device__ __forceinline__ void mfma_consume(const f32x4 (&D)[MT], const f32x4 (&N)[MT], float (&acc)[MT][4]) {
 #pragma unroll
   for (int t = 0; t < MT; ++t)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      acc[t][r] = fmaf(N[t][r], __builtin_amdgcn_rcpf(D[t][r]), acc[t][r]);
-      if (C == 4) acc[t][r] = fmaf(N[t + MT][r], __builtin_amdgcn_rcpf(D[t + MT][r]), acc[t][r]);
-    }
+    for (int r = 0; r < 4; ++r) acc[t][r] = fmaf(N[t][r], __builtin_amdgcn_rcpf(D[t][r]), acc[t][r]);
 }
 
 template <int C, int MT>
 __device__ __forceinline__ void mfma_sweep(const float4* __restrict__ src, int nblocks, int tid, int lane,
-                                           const float (&A0)[MT], const float (&A1)[MT], const f32x4 (&cinit)[MT],
-                                           double (&acc64)[MT][4], float4* __restrict__ tile) {
-  constexpr int kLoads = kMfmaTileBlocks * 64 / kMfmaThreads;  // float4 per thread per tile
+                                           const bf16x8 (&AX)[MT], const bf16x4 (&AY)[MT],
+                                           const f32x4 (&cinit)[MT], double (&acc64)[MT][4],
+                                           float4* __restrict__ tile) {
+  constexpr int F = (C == 8) ? 192 : 128;           // float4 per block
+  constexpr int kTileBlocks = kMfmaTileF4 / F;      // 8 or 12 blocks per LDS tile
+  constexpr int kLoads = kMfmaTileF4 / kMfmaThreads;  // float4 per thread per tile
+  const int64_t total_f4 = (int64_t)nblocks * F;
   float4 reg[kLoads];
   auto fetch = [&](int blk0) {
 #pragma unroll
     for (int k = 0; k < kLoads; ++k) {
-      const int i = k * kMfmaThreads + tid;  // float4 index inside the tile
-      reg[k] = (blk0 * 64 + i < nblocks * 64) ? src[(int64_t)blk0 * 64 + i] : make_float4(0.f, 0.f, 0.f, 0.f);
+      const int64_t i = (int64_t)blk0 * F + k * kMfmaThreads + tid;
+      reg[k] = (i < total_f4) ? src[i] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
   if (nblocks > 0) fetch(0);
-  for (int blk0 = 0; blk0 < nblocks; blk0 += kMfmaTileBlocks) {
+  for (int blk0 = 0; blk0 < nblocks; blk0 += kTileBlocks) {
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < kLoads; ++k) tile[k * kMfmaThreads + tid] = reg[k];
     __syncthreads();
-    if (blk0 + kMfmaTileBlocks < nblocks) fetch(blk0 + kMfmaTileBlocks);
-    const int nb = min(kMfmaTileBlocks, nblocks - blk0);
+    if (blk0 + kTileBlocks < nblocks) fetch(blk0 + kTileBlocks);
+    const int nb = min(kTileBlocks, nblocks - blk0);
     float acc[MT][4];
 #pragma unroll
     for (int t = 0; t < MT; ++t)
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[t][r] = 0.0f;
     // software pipeline: the MFMAs of block bi + 1 are issued before the VALU work of block bi
-    f32x4 D0[2 * MT], N0[2 * MT], D1[2 * MT], N1[2 * MT];
-    mfma_block<C, MT>(tile[lane], A0, A1, cinit, D0, N0);
+    f32x4 D0[MT], N0[MT], D1[MT], N1[MT];
+    mfma_block<C, MT>(tile, lane, AX, AY, cinit, D0, N0);
     int bi = 1;
     for (; bi + 1 < nb; bi += 2) {
-      mfma_block<C, MT>(tile[bi * 64 + lane], A0, A1, cinit, D1, N1);
-      mfma_consume<C, MT>(D0, N0, acc);
-      mfma_block<C, MT>(tile[(bi + 1) * 64 + lane], A0, A1, cinit, D0, N0);
-      mfma_consume<C, MT>(D1, N1, acc);
+      mfma_block<C, MT>(tile + bi * F, lane, AX, AY, cinit, D1, N1);
+      mfma_consume<MT>(D0, N0, acc);
+      mfma_block<C, MT>(tile + (bi + 1) * F, lane, AX, AY, cinit, D0, N0);
+      mfma_consume<MT>(D1, N1, acc);
     }
     if (bi < nb) {
-      mfma_block<C, MT>(tile[bi * 64 + lane], A0, A1, cinit, D1, N1);
-      mfma_consume<C, MT>(D0, N0, acc);
-      mfma_consume<C, MT>(D1, N1, acc);
+      mfma_block<C, MT>(tile + bi * F, lane, AX, AY, cinit, D1, N1);
+      mfma_consume<MT>(D0, N0, acc);
+      mfma_consume<MT>(D1, N1, acc);
     } else {
-      mfma_consume<C, MT>(D0, N0, acc);
+      mfma_consume<MT>(D0, N0, acc);
     }
 #pragma unroll
     for (int t = 0; t < MT; ++t)
@@ -600,18 +673,38 @@ __global__ __launch_bounds__(kMfmaThreads) void sweep_k2_mfma_kernel(const float
   const int C = h.mode;
   const float* wc = ws.wc + b * ws.Sp;
 
-  // A[i][m] = a_i^m (row i = col, m = g and 4 + g); accumulator input a^C for rows 4 g + r
-  float A0[MT], A1[MT];
+  // A[i][k] = part slot_a(k % 6) of a_i^(k / 6) (row i = col); accumulator input a^C for rows 4 g + r
+  bf16x8 AX[MT];
+  bf16x4 AY[MT];
   f32x4 cinit[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) {
     const int base = q0 + 16 * (MT * wave + t);
     const float a = (base + col < n) ? wc[base + col] : 1.0f;
-    float pw = 1.0f;
-    for (int m = 0; m < g; ++m) pw *= a;
-    const float a2 = a * a, a4 = a2 * a2;
-    A0[t] = pw;
-    A1[t] = pw * a4;
+    float pw[8];
+    pw[0] = 1.0f;
+#pragma unroll
+    for (int m = 1; m < 8; ++m) pw[m] = pw[m - 1] * a;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int k = 8 * g + e, m = k / 6, sl = k % 6;
+      float parts[3];
+      float pm = pw[0];
+#pragma unroll
+      for (int mm = 1; mm < 8; ++mm) pm = (m == mm) ? pw[mm] : pm;
+      split3(pm, parts);
+      AX[t][e] = (__bf16)((m < C) ? pick3(parts, slot_a(sl)) : 0.0f);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int k = 32 + 4 * g + e, m = k / 6, sl = k % 6;
+      float parts[3];
+      float pm = pw[0];
+#pragma unroll
+      for (int mm = 1; mm < 8; ++mm) pm = (m == mm) ? pw[mm] : pm;
+      split3(pm, parts);
+      AY[t][e] = (__bf16)((m < C) ? pick3(parts, slot_a(sl)) : 0.0f);
+    }
 #pragma unroll
     for (int rr = 0; rr < 4; ++rr) {
       const int qi = base + 4 * g + rr;
@@ -620,20 +713,22 @@ __global__ __launch_bounds__(kMfmaThreads) void sweep_k2_mfma_kernel(const float
       cinit[t][rr] = (C == 8) ? ar4 * ar4 : ar4;
     }
   }
-  const int nblocks = (int)(round_up(n, kBlockPoles) / kBlockPoles);
+  const int poles_per_block = (C == 8) ? 128 : 64;
+  const int F = (C == 8) ? 192 : 128;
+  const int nblocks = (int)(round_up(n, kBlockPoles) / poles_per_block);
   const int b_lo = (int)((int64_t)nblocks * split / ws.P);
   const int b_hi = (int)((int64_t)nblocks * (split + 1) / ws.P);
-  const float4* src = reinterpret_cast<const float4*>(ws.stream + b * 2 * ws.Sp) + (int64_t)b_lo * 64;
-  __shared__ float4 tile[kMfmaTileBlocks * 64];
+  const float4* src = reinterpret_cast<const float4*>(ws.stream + b * ws.ld) + (int64_t)b_lo * F;
+  __shared__ float4 tile[kMfmaTileF4];
   double acc64[MT][4];
 #pragma unroll
   for (int t = 0; t < MT; ++t)
 #pragma unroll
     for (int rr = 0; rr < 4; ++rr) acc64[t][rr] = 0.0;
   if (C == 8) {
-    mfma_sweep<8, MT>(src, b_hi - b_lo, tid, lane, A0, A1, cinit, acc64, tile);
+    mfma_sweep<8, MT>(src, b_hi - b_lo, tid, lane, AX, AY, cinit, acc64, tile);
   } else {
-    mfma_sweep<4, MT>(src, b_hi - b_lo, tid, lane, A0, A1, cinit, acc64, tile);
+    mfma_sweep<4, MT>(src, b_hi - b_lo, tid, lane, AX, AY, cinit, acc64, tile);
   }
   // each query row is spread over the 16 lanes of its group (one chunk column each)
 #pragma unroll
@@ -687,7 +782,7 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_k3_kernel(Workspace ws) {
   float4* s_stream = reinterpret_cast<float4*>(s_q + npad);
   const float* gw = ws.wc + b * ws.Sp;
   const float* gq = ws.qc + b * ws.Sp;
-  const float4* gs = reinterpret_cast<const float4*>(ws.stream + b * 2 * ws.Sp);
+  const float4* gs = reinterpret_cast<const float4*>(ws.stream + b * ws.ld);
   for (int j = tid; j < npad; j += kSweepThreads) {
     s_w[j] = gw[j];
     s_q[j] = gq[j];
@@ -792,6 +887,9 @@ int choose_splits(int64_t B, int64_t V, int K, int s_max) {
 
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
+// K = 2 rows hold packed bf16 operands: up to 32 bytes per pole (4-pole chunks)
+static int64_t stream_ld(int K, int64_t Sp) { return K == 2 ? 8 * Sp : 2 * Sp; }
+
 static int64_t padded_len(int64_t V, int K, int s_max) {
   return K == 2 ? round_up(V, kBlockPoles) : round_up(std::min<int64_t>(s_max, V), 8);
 }
@@ -800,7 +898,7 @@ size_t workspace_bytes(int64_t B, int64_t V, int K, int s_max, int P) {
   const int64_t Sp = padded_len(V, K, s_max);
   size_t t = align256(sizeof(RowHdr) * B);
   t += 3 * align256(sizeof(float) * B * Sp);
-  t += align256(sizeof(float) * 2 * B * Sp);
+  t += align256(sizeof(float) * stream_ld(K, Sp) * B);
   const bool need_part = (K == 3) || P > 1;
   if (need_part) t += align256(sizeof(double) * B * P * Sp);
   return t;
@@ -818,9 +916,10 @@ void carve_workspace(void* base, int64_t B, int64_t V, int K, int s_max, int P, 
   ws->qc = reinterpret_cast<float*>(c);
   c += align256(sizeof(float) * B * Sp);
   ws->stream = reinterpret_cast<float*>(c);
-  c += align256(sizeof(float) * 2 * B * Sp);
+  c += align256(sizeof(float) * stream_ld(K, Sp) * B);
   ws->part = ((K == 3) || P > 1) ? reinterpret_cast<double*>(c) : nullptr;
   ws->Sp = Sp;
+  ws->ld = stream_ld(K, Sp);
   ws->P = P;
 }
 
@@ -832,6 +931,8 @@ hipError_t launch_induced(const float* p, const float* q, int64_t B, int64_t V, 
   hipLaunchKernelGGL(pole_stream_kernel, dim3((unsigned)((units + 255) / 256), (unsigned)B), dim3(256), 0, st, ws,
                      K);
   if (K == 2) {
+    hipLaunchKernelGGL(pole_pack_mfma_kernel, dim3((unsigned)((ws.Sp / 4 + 255) / 256), (unsigned)B), dim3(256), 0,
+                       st, ws);
     const int nqb = (int)((V + kMfmaQueries - 1) / kMfmaQueries);
     const int64_t total = (int64_t)nqb * ws.P * B;
     hipLaunchKernelGGL(sweep_k2_mfma_kernel, dim3((unsigned)total), dim3(kMfmaThreads), 0, st, p, q, V, r, ws, nqb,
