@@ -327,3 +327,37 @@ def test_monte_carlo_output_law():
     e2 = ro[0] / ro[0].sum() * N
     chi2s = float(((np.bincount(g["sel_token"], minlength=V) - e2) ** 2 / e2).sum())
     assert chi2s < 25.0
+
+
+def _ranged_rows(V, ranges, seed):
+    """Rows whose weights p/q span exactly `R` binary orders of magnitude, with a
+    quarter of the tokens at each end of the range (stresses the scaling of the
+    rational chunks and of the split matrix-core operands)."""
+    rng = np.random.default_rng(seed)
+    P, Q = [], []
+    for R in ranges:
+        q = rng.dirichlet(np.full(V, 2.0))
+        e = rng.uniform(-0.5, 0.5, V) * R
+        e[: V // 4] = -0.5 * R
+        e[V // 4: V // 2] = 0.5 * R
+        rng.shuffle(e)
+        p = q * np.exp2(e)
+        p /= p.sum()
+        P.append(p)
+        Q.append(q)
+    return np.array(P, np.float32), np.array(Q, np.float32)
+
+
+@pytest.mark.parametrize("K", [2, 3])
+def test_extreme_weight_ranges(K):
+    # binary ranges on both sides of the 8-pole (28) and 4-pole (56) limits
+    ranges = [4, 20, 27, 28, 29, 40, 55, 56, 57, 64]
+    V = 256 if K == 2 else 96
+    P, Q = _ranged_rows(V, ranges, 2024 + K)
+    r, st = gpu_r(P, Q, K, V if K == 3 else 0)
+    ro, _ = oracle.induced_dist(P, Q, K)
+    assert np.all(st == 0)
+    err = rel_l1(r, ro)
+    per_entry = np.max(np.abs(r - ro) / np.maximum(ro, 1e-300), axis=1)
+    print("\nrange  rel-L1  max-entry-rel:", [(R, f"{a:.1e}", f"{b:.1e}") for R, a, b in zip(ranges, err, per_entry)])
+    assert np.all(err <= RTOL_ROW), err
