@@ -489,70 +489,62 @@ __device__ __forceinline__ float4 pack_bf16x8(const float (&v)[8]) {
   return __builtin_bit_cast(float4, t);
 }
 
-// Packs the rational chunks of a K = 2 row into the bf16 operand blocks.
-// Thread block of 256 threads = 256 chunks = 16 operand blocks; phase 1: one
-// thread per chunk forms its coefficients (fp64, rounded to fp32) into LDS;
-// phase 2: every thread packs float4s of the blocks.
+// Packs the rational chunks of a K = 2 row into the bf16 operand blocks, one
+// thread per chunk: the 8 bf16 values of one lane's float4 (its k range for
+// column j) all come from the same chunk j, so a thread forms its chunk's
+// coefficients (fp64, rounded to fp32), splits each once and writes its
+// 12 (C = 8) or 8 (C = 4) float4s; threads j = 0..15 of a block write 16
+// adjacent float4s per (plane, lane group).
+template <int C>
+__device__ __forceinline__ void pack_chunk(const float* __restrict__ w, const float* __restrict__ q,
+                                           float4* __restrict__ blk, int j) {
+  float o[16];
+  chunk_coefficients<C>(w, q, o);  // o[k - 1] = e_k, o[C + k] = coefficient of a^(C - 1 - k) in N
+  float dp[C][3], np[C][3];        // split parts of d_m = e_{C-m} and n_m
+#pragma unroll
+  for (int m = 0; m < C; ++m) {
+    split3(o[C - 1 - m], dp[m]);
+    split3(o[2 * C - 1 - m], np[m]);
+  }
+  constexpr int kPlanes = (C == 8) ? 3 : 2;
+#pragma unroll
+  for (int plane = 0; plane < kPlanes; ++plane)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        int k;
+        bool is_n;
+        if (plane < 2) {
+          k = 8 * g + e;
+          is_n = (plane == 1);
+        } else {
+          k = 32 + 4 * g + (e & 3);
+          is_n = (e >= 4);
+        }
+        const int m = k / 6, sl = k % 6;
+        v[e] = (m < C) ? (is_n ? np[m][slot_b(sl)] : dp[m][slot_b(sl)]) : 0.0f;
+      }
+      blk[plane * 64 + 16 * g + j] = pack_bf16x8(v);
+    }
+}
+
 __global__ __launch_bounds__(256) void pole_pack_mfma_kernel(Workspace ws) {
   const int64_t b = blockIdx.y;
   const RowHdr h = ws.hdr[b];
   if (h.mode != kRat8 && h.mode != kRat4) return;
   const int C = h.mode;
-  const int tid = threadIdx.x;
-  const int64_t npad = round_up(h.n, kBlockPoles);
-  const int64_t nch = npad / C;
-  const int64_t c0 = (int64_t)blockIdx.x * 256;
-  if (c0 >= nch) return;
-  __shared__ float s_d[256][8];  // d_m = e_{C-m}
-  __shared__ float s_n[256][8];  // n_m
-  const int64_t c = c0 + tid;
+  const int64_t nch = round_up(h.n, kBlockPoles) / C;
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= nch) return;
   const float* wc = ws.wc + b * ws.Sp;
   const float* qc = ws.qc + b * ws.Sp;
-  if (c < nch) {
-    float o[16];
-    if (C == 8) {
-      chunk_coefficients<8>(wc + 8 * c, qc + 8 * c, o);
-    } else {
-      chunk_coefficients<4>(wc + 4 * c, qc + 4 * c, o);
-    }
-    // o[k - 1] = e_k, o[C + k] = coefficient of a^(C - 1 - k) in N
-    for (int m = 0; m < C; ++m) {
-      s_d[tid][m] = o[C - 1 - m];
-      s_n[tid][m] = o[2 * C - 1 - m];
-    }
-  }
-  __syncthreads();
-  const int F = (C == 8) ? 192 : 128;         // float4 per operand block
-  const int64_t nblk = nch / 16;              // blocks in the row
-  const int64_t blk0 = c0 / 16;               // first block of this thread block
   float4* out = reinterpret_cast<float4*>(ws.stream + b * ws.ld);
-  for (int o4 = tid; o4 < 16 * F; o4 += 256) {
-    const int blk = o4 / F, rem = o4 % F;
-    if (blk0 + blk >= nblk) break;
-    const int plane = rem / 64, L = rem % 64, g = L / 16, j = L % 16;
-    const int ch = 16 * blk + j;  // chunk inside this thread block
-    float v[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      int k;
-      bool is_n;
-      if (plane < 2) {
-        k = 8 * g + e;
-        is_n = (plane == 1);
-      } else {
-        k = 32 + 4 * g + (e & 3);
-        is_n = (e >= 4);
-      }
-      const int m = k / 6, sl = k % 6;
-      float val = 0.0f;
-      if (m < C) {
-        float parts[3];
-        split3(is_n ? s_n[ch][m] : s_d[ch][m], parts);
-        val = pick3(parts, slot_b(sl));
-      }
-      v[e] = val;
-    }
-    out[(blk0 + blk) * F + rem] = pack_bf16x8(v);
+  if (C == 8) {
+    pack_chunk<8>(wc + 8 * c, qc + 8 * c, out + (c / 16) * 192, (int)(c % 16));
+  } else {
+    pack_chunk<4>(wc + 4 * c, qc + 4 * c, out + (c / 16) * 128, (int)(c % 16));
   }
 }
 

@@ -138,34 +138,50 @@ __global__ __launch_bounds__(kAccThreads) void accept_kernel(
   const int64_t nsuper = (V + kSuper - 1) / kSuper;
   float* resb = residual ? residual + b * V : nullptr;
   int bad = 0;
-  for (int64_t st = wid; st < nsuper; st += kAccWaves) {
-    double local = 0.0;
+  // two super-tiles per wave and iteration: all 16 row loads are issued before any arithmetic
+  for (int64_t st0 = wid; st0 < nsuper; st0 += 2 * kAccWaves) {
+    float pv[2][4][4], rv[2][4][4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int64_t x0 = st * kSuper + 256 * k + 4 * lane;
-      float pv[4], rv[4];
-      load4<kVec>(pb, x0, V, pv);
-      load4<kVec>(rb, x0, V, rv);
-      float rs[4];
+    for (int h = 0; h < 2; ++h) {
+      const int64_t st = st0 + h * kAccWaves;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        bad |= (int)(bad_prob(pv[i]) | bad_prob(rv[i]));
-        const double d = residual_of(pv[i], rv[i]);
-        rs[i] = (float)d;
-        local += d;
-      }
-      if (resb) {
-        if (kVec && x0 + 3 < V) {
-          *reinterpret_cast<float4*>(resb + x0) = make_float4(rs[0], rs[1], rs[2], rs[3]);
-        } else {
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (x0 + i < V) resb[x0 + i] = rs[i];
-        }
+      for (int k = 0; k < 4; ++k) {
+        const int64_t x0 = st * kSuper + 256 * k + 4 * lane;
+        load4<kVec>(pb, x0, V, pv[h][k]);  // tokens at or past V (incl. a whole missing super-tile) read as 0
+        load4<kVec>(rb, x0, V, rv[h][k]);
       }
     }
-    const double tot = wave_sum(local);
-    if (lane == 0) s_tile[st] = tot;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t st = st0 + h * kAccWaves;
+      if (st >= nsuper) break;
+      double local = 0.0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int64_t x0 = st * kSuper + 256 * k + 4 * lane;
+        float rs[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          bad |= (int)(bad_prob(pv[h][k][i]) || bad_prob(rv[h][k][i]));
+          const double d = residual_of(pv[h][k][i], rv[h][k][i]);
+          rs[i] = (float)d;
+          local += d;
+        }
+        if (resb) {
+          if (kVec && x0 + 3 < V) {
+            typedef float f32x4v __attribute__((ext_vector_type(4)));
+            const f32x4v v = {rs[0], rs[1], rs[2], rs[3]};
+            __builtin_nontemporal_store(v, reinterpret_cast<f32x4v*>(resb + x0));
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (x0 + i < V) resb[x0 + i] = rs[i];
+          }
+        }
+      }
+      const double tot = wave_sum(local);
+      if (lane == 0) s_tile[st] = tot;
+    }
   }
   if (bad) atomicOr(&s_bad, 1);
   __syncthreads();
