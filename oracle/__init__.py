@@ -60,7 +60,11 @@ def _load():
         lib.oracle_induced_dist_entries.argtypes = [P, P, i64, i32, P, P, i64, P]
         lib.oracle_select.argtypes = [P, P, P, P, i64, i64, i32, P, P, P]
         lib.oracle_accept_resample.argtypes = [P, P, P, P, i64, i64, P, P, P, P, P]
-        for f in ("oracle_induced_dist", "oracle_induced_dist_entries", "oracle_select", "oracle_accept_resample"):
+        lib.oracle_induced_dist_pair.argtypes = [P, P, P, i64, i64, P, P]
+        lib.oracle_induced_dist_pair_entries.argtypes = [P, P, P, i64, P, P, i64, P]
+        lib.oracle_select_pair.argtypes = [P, P, P, P, P, i64, i64, P, P, P]
+        for f in ("oracle_induced_dist", "oracle_induced_dist_entries", "oracle_select", "oracle_accept_resample",
+                  "oracle_induced_dist_pair", "oracle_induced_dist_pair_entries", "oracle_select_pair"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
         return lib
@@ -116,6 +120,46 @@ def induced_dist_entries(p, q, K: int, rows, ys) -> np.ndarray:
     return out
 
 
+def induced_dist_pair(p, q1, q2):
+    """r [B][V] fp64 for two drafts X1 ~ q1, X2 ~ q2 (classical weights p/q_i), by enumeration."""
+    p, q1, q2 = _f32(p), _f32(q1), _f32(q2)
+    B, V = p.shape
+    r = np.zeros((B, V), np.float64)
+    st = np.zeros(B, np.int32)
+    rc = _load().oracle_induced_dist_pair(_ptr(p), _ptr(q1), _ptr(q2), B, V, _ptr(r), _ptr(st))
+    assert rc == 0
+    return r, st
+
+
+def induced_dist_pair_entries(p, q1, q2, rows, ys) -> np.ndarray:
+    p, q1, q2 = _f32(p), _f32(q1), _f32(q2)
+    B, V = p.shape
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    ys = np.ascontiguousarray(ys, dtype=np.int64)
+    assert rows.shape == ys.shape and (rows.size == 0 or (rows.min() >= 0 and rows.max() < B))
+    assert ys.size == 0 or (ys.min() >= 0 and ys.max() < V)
+    out = np.zeros(rows.shape, np.float64)
+    rc = _load().oracle_induced_dist_pair_entries(_ptr(p), _ptr(q1), _ptr(q2), V, _ptr(rows), _ptr(ys), rows.size,
+                                                  _ptr(out))
+    assert rc == 0
+    return out
+
+
+def select_pair(p, q1, q2, drafts, u):
+    """(sel_index, sel_token, status) for two drafts from q1 and q2."""
+    p, q1, q2 = _f32(p), _f32(q1), _f32(q2)
+    drafts = np.ascontiguousarray(drafts, dtype=np.int32)
+    u = _f32(u)
+    B, V = p.shape
+    si = np.zeros(B, np.int32)
+    stok = np.zeros(B, np.int32)
+    st = np.zeros(B, np.int32)
+    rc = _load().oracle_select_pair(_ptr(p), _ptr(q1), _ptr(q2), _ptr(drafts), _ptr(u), B, V, _ptr(si), _ptr(stok),
+                                    _ptr(st))
+    assert rc == 0
+    return si, stok, st
+
+
 def select(p, q, drafts, u):
     """(sel_index, sel_token, status), all int32 [B]."""
     p, q = _f32(p), _f32(q)
@@ -146,6 +190,16 @@ def accept_resample(p, r32, sel_token, u, want_residual: bool = True):
                                         _ptr(res), _ptr(mass), _ptr(st))
     assert rc == 0
     return out, acc, res, mass, st
+
+
+def step_pair(p, q1, q2, drafts, u):
+    """Whole two-draft path on the CPU (non-identical drafts)."""
+    r, st0 = induced_dist_pair(p, q1, q2)
+    r32 = r.astype(np.float32)
+    si, stok, st1 = select_pair(p, q1, q2, drafts, u)
+    out, acc, res, mass, st2 = accept_resample(p, r32, stok, u)
+    return {"r": r, "r32": r32, "sel_index": si, "sel_token": stok, "out_token": out, "accepted": acc,
+            "residual": res, "mass": mass, "status": st0 | st1 | st2}
 
 
 def step(p, q, drafts, u):

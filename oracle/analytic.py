@@ -72,23 +72,31 @@ def theorem2_condition(p, q, tol: float = 0.0) -> bool:
 
 
 def pstar_problem1_lp(p, q, K: int) -> float:
+    """Problem 1 with K i.i.d. drafts from q (see pstar_problem1_lp_multi)."""
+    return pstar_problem1_lp_multi(p, [q] * K)
+
+
+def pstar_problem1_lp_multi(p, qs) -> float:
     """Optimal acceptance of Problem 1 by linear programming (tiny V only).
 
-    Variables: P(z | x) for every ordered draft tuple x in Omega^K and z in
-    Omega.  Constraints: each conditional sums to one, and the output marginal
-    sum_x P(z|x) prod_i q(x_i) equals the target p(z) (a valid selection rule).
-    Objective: Pr(Z in {x_1..x_K}) = sum_x prod q(x_i) sum_{z in x} P(z|x)."""
+    Draft i is drawn from qs[i] independently (identical drafts: all equal;
+    Remark 1 covers different ones).  Variables: P(z | x) for every ordered
+    draft tuple x and output z.  Constraints: each conditional sums to one,
+    and the output marginal sum_x P(z|x) prod_i q_i(x_i) equals the target
+    p(z) (a valid selection rule).  Objective: Pr(Z in {x_1..x_K}) =
+    sum_x prod_i q_i(x_i) sum_{z in x} P(z|x)."""
     from scipy.optimize import linprog
 
     p = np.asarray(p, np.float64)
-    q = np.asarray(q, np.float64)
+    qs = [np.asarray(q, np.float64) for q in qs]
+    K = len(qs)
     n = len(p)
     tuples = list(itertools.product(range(n), repeat=K))
     nv = len(tuples) * n
     c = np.zeros(nv)
     A_eq, b_eq = [], []
     for t_i, t in enumerate(tuples):
-        prob = float(np.prod([q[x] for x in t]))
+        prob = float(np.prod([qs[i][x] for i, x in enumerate(t)]))
         row = np.zeros(nv)
         row[t_i * n:(t_i + 1) * n] = 1.0
         A_eq.append(row)
@@ -98,7 +106,7 @@ def pstar_problem1_lp(p, q, K: int) -> float:
     for z in range(n):
         row = np.zeros(nv)
         for t_i, t in enumerate(tuples):
-            row[t_i * n + z] = float(np.prod([q[x] for x in t]))
+            row[t_i * n + z] = float(np.prod([qs[i][x] for i, x in enumerate(t)]))
         A_eq.append(row)
         b_eq.append(p[z])
     res = linprog(c, A_eq=np.array(A_eq), b_eq=np.array(b_eq), bounds=(0, 1), method="highs")

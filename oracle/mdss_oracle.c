@@ -316,3 +316,127 @@ int oracle_accept_resample(const float* p, const float* r, const int32_t* sel_to
   }
   return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Two drafts from different distributions (Remark 1; the non-identical     */
+/* K = 2 appendix): X1 ~ q1, X2 ~ q2 independent.  The classical weight of */
+/* draft i is w_i(x) = p(x)/q_i(x) (target over the distribution that      */
+/* proposed it); Pr(I = i | x1, x2) = w_i(x_i) / (w_1(x1) + w_2(x2)), the   */
+/* uniform choice when both are zero.  r(y) sums q1(x1) q2(x2) times the    */
+/* probability of selecting y over all ordered pairs of the two supports.   */
+/* ------------------------------------------------------------------------ */
+static void induced_pair_row(const float* p, const float* q1, const float* q2, int64_t V, double* r) {
+  int64_t n1 = 0, n2 = 0;
+  int64_t* s1 = (int64_t*)malloc(sizeof(int64_t) * (size_t)V);
+  int64_t* s2 = (int64_t*)malloc(sizeof(int64_t) * (size_t)V);
+  for (int64_t x = 0; x < V; ++x) {
+    r[x] = 0.0;
+    if (q1[x] > 0.0f) s1[n1++] = x;
+    if (q2[x] > 0.0f) s2[n2++] = x;
+  }
+  double wt[2], beta[2];
+  for (int64_t i = 0; i < n1; ++i) {
+    const int64_t x1 = s1[i];
+    for (int64_t j = 0; j < n2; ++j) {
+      const int64_t x2 = s2[j];
+      const double prob = (double)q1[x1] * (double)q2[x2];
+      wt[0] = (double)p[x1] / (double)q1[x1];
+      wt[1] = (double)p[x2] / (double)q2[x2];
+      is_index_probs(wt, 2, beta);
+      r[x1] += prob * beta[0];
+      r[x2] += prob * beta[1];
+    }
+  }
+  free(s1);
+  free(s2);
+}
+
+int oracle_induced_dist_pair(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, double* r,
+                             int32_t* status) {
+  if (!p || !q1 || !q2 || !r || B < 0 || V < 1) return 1;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t b = 0; b < B; ++b) {
+    const float* pb = p + b * V;
+    const float* q1b = q1 + b * V;
+    const float* q2b = q2 + b * V;
+    double* rb = r + b * V;
+    if (row_is_bad(pb, q1b, V) || row_is_bad(pb, q2b, V)) {
+      for (int64_t x = 0; x < V; ++x) rb[x] = NAN;
+      if (status) status[b] |= ST_BAD_PROB;
+      continue;
+    }
+    induced_pair_row(pb, q1b, q2b, V, rb);
+  }
+  return 0;
+}
+
+/* One entry r(y) of the two-draft distribution, from the pairs with x1 = y or x2 = y. */
+int oracle_induced_dist_pair_entries(const float* p, const float* q1, const float* q2, int64_t V, const int64_t* rows,
+                                     const int64_t* ys, int64_t count, double* out) {
+  if (!p || !q1 || !q2 || !rows || !ys || !out || V < 1) return 1;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t i = 0; i < count; ++i) {
+    const float* pb = p + rows[i] * V;
+    const float* q1b = q1 + rows[i] * V;
+    const float* q2b = q2 + rows[i] * V;
+    const int64_t y = ys[i];
+    if (row_is_bad(pb, q1b, V) || row_is_bad(pb, q2b, V)) {
+      out[i] = NAN;
+      continue;
+    }
+    double total = 0.0, wt[2], beta[2];
+    /* pairs (y, x2) for every x2, then (x1, y) for x1 != y */
+    for (int pass = 0; pass < 2; ++pass) {
+      for (int64_t x = 0; x < V; ++x) {
+        const int64_t x1 = pass == 0 ? y : x, x2 = pass == 0 ? x : y;
+        if (pass == 1 && x == y) continue;
+        if (!(q1b[x1] > 0.0f) || !(q2b[x2] > 0.0f)) continue;
+        const double prob = (double)q1b[x1] * (double)q2b[x2];
+        wt[0] = (double)pb[x1] / (double)q1b[x1];
+        wt[1] = (double)pb[x2] / (double)q2b[x2];
+        is_index_probs(wt, 2, beta);
+        total += prob * ((x1 == y ? beta[0] : 0.0) + (x2 == y ? beta[1] : 0.0));
+      }
+    }
+    out[i] = total;
+  }
+  return 0;
+}
+
+/* Selection between two drafts proposed by different distributions:
+ * w_1 = p(x1)/q1(x1), w_2 = p(x2)/q2(x2), then the same inverse CDF as
+ * oracle_select (index 0 iff u * W < w_1; W = 0: floor(2 u)). */
+int oracle_select_pair(const float* p, const float* q1, const float* q2, const int32_t* drafts, const float* u,
+                       int64_t B, int64_t V, int32_t* sel_index, int32_t* sel_token, int32_t* status) {
+  if (!p || !q1 || !q2 || !drafts || !u || !sel_index || !sel_token || V < 1) return 1;
+  for (int64_t b = 0; b < B; ++b) {
+    const float* pb = p + b * V;
+    const float* qs[2] = {q1 + b * V, q2 + b * V};
+    int32_t st = 0;
+    double w[2] = {0.0, 0.0};
+    for (int i = 0; i < 2; ++i) {
+      int32_t x = drafts[b * 2 + i];
+      if (x < 0 || (int64_t)x >= V) { st |= ST_BAD_DRAFT; continue; }
+      if (bad_prob(pb[x]) || bad_prob(qs[i][x])) { st |= ST_BAD_PROB; continue; }
+      if (!(qs[i][x] > 0.0f)) { st |= ST_BAD_DRAFT; continue; }
+      w[i] = (double)pb[x] / (double)qs[i][x];
+    }
+    if (st) {
+      sel_index[b] = -1;
+      sel_token[b] = -1;
+      if (status) status[b] |= st;
+      continue;
+    }
+    const double W = w[0] + w[1];
+    const double us = (double)u[b * 3 + 0];
+    int istar;
+    if (W > 0.0) {
+      istar = (us * W < w[0]) ? 0 : 1;
+    } else {
+      istar = (int)floor(us * 2.0);
+    }
+    sel_index[b] = istar;
+    sel_token[b] = drafts[b * 2 + istar];
+  }
+  return 0;
+}

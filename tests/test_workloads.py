@@ -38,3 +38,13 @@ def test_zipf_target_is_a_permuted_power_law():
     ratio = s / (k ** -1.1)
     assert np.allclose(ratio, ratio[0], rtol=1e-6)
     assert np.argmax(w["p"][0]) != 0 or np.argmax(generate("zipf128k", rows=[3])["p"][0]) != 0
+
+
+def test_pair_workload_drafts_follow_their_own_distributions():
+    w = generate("pair32k", rows=[0, 1, 2])
+    assert w["q2"].shape == w["q"].shape and not np.array_equal(w["q"], w["q2"])
+    for i in range(3):
+        assert w["q"][i][w["drafts"][i, 0]] > 0 and w["q2"][i][w["drafts"][i, 1]] > 0
+    # the second draft is hotter (T = 2.0 vs 1.2): flatter distribution
+    ent = lambda a: -(a * np.log(np.maximum(a, 1e-30))).sum(1)
+    assert np.all(ent(w["q2"].astype(np.float64)) > ent(w["q"].astype(np.float64)))

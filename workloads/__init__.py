@@ -13,7 +13,8 @@ way round: its ``p`` is the draft model and its ``q`` the target model).
 Every row is generated from its own ``numpy.random.Generator(PCG64(SeedSequence(
 [seed, stream, row])))`` so that any subset of rows can be regenerated on its
 own.  Streams: 0 logits / Dirichlet draw of p, 1 noise / Dirichlet draw of q,
-2 permutation, 3 drafts, 4 uniforms.
+2 permutation, 3 drafts, 4 uniforms, 5 noise of a second draft distribution,
+6 tokens of the second draft.
 
 Values are produced in fp64 (softmax in fp64) and cast to fp32, without any
 renormalisation after the cast.  Drafted tokens are drawn i.i.d. from the fp32
@@ -29,7 +30,7 @@ import numpy as np
 
 __all__ = ["Config", "CONFIGS", "generate", "uniforms24", "draw_drafts"]
 
-_S_LOGIT, _S_NOISE, _S_PERM, _S_DRAFT, _S_UNIF = 0, 1, 2, 3, 4
+_S_LOGIT, _S_NOISE, _S_PERM, _S_DRAFT, _S_UNIF, _S_NOISE2, _S_DRAFT2 = 0, 1, 2, 3, 4, 5, 6
 
 
 def _rng(seed: int, stream: int, row: int) -> np.random.Generator:
@@ -52,6 +53,7 @@ class Config:
     describe: str
     row: Callable[["Config", int], "tuple[np.ndarray, np.ndarray]"]
     s_max: int = 0  # support cap the K=3 path is run with (0: not used)
+    pair: bool = False  # two drafts from different distributions q (first) and q2 (second)
 
 
 def _row_dirichlet(cfg: Config, b: int):
@@ -77,6 +79,16 @@ def _row_zipf(cfg: Config, b: int):
     p[perm] = mass  # token perm[k-1] has rank k
     eps = _rng(cfg.seed, _S_NOISE, b).normal(0.0, 1.0, cfg.V)
     return p, _softmax64(np.log(p) + eps)
+
+
+def _row_two_temps(sigma: float, t1: float, t2: float):
+    """Target softmax(l); drafts softmax((l + e_i) / t_i) with their own N(0,1) noise."""
+    def f(cfg: Config, b: int):
+        ell = _rng(cfg.seed, _S_LOGIT, b).normal(0.0, sigma, cfg.V)
+        e1 = _rng(cfg.seed, _S_NOISE, b).normal(0.0, 1.0, cfg.V)
+        e2 = _rng(cfg.seed, _S_NOISE2, b).normal(0.0, 1.0, cfg.V)
+        return _softmax64(ell), _softmax64((ell + e1) / t1), _softmax64((ell + e2) / t2)
+    return f
 
 
 def _row_topk(s: int):
@@ -111,6 +123,10 @@ CONFIGS: Dict[str, Config] = {
         Config("k3top1024", 1005, 256, 32000, 3,
                "V=32000, K=3, 256 positions, draft truncated to its top-1024 tokens and "
                "renormalised, logits N(0,3^2), draft noise N(0,1)", _row_topk(1024), s_max=1024),
+        Config("pair32k", 1006, 256, 32000, 2,
+               "V=32000, two drafts from different distributions, 256 positions, logits N(0,3^2), "
+               "draft i = softmax((logits + N(0,1)) / T_i) with T_1 = 1.2, T_2 = 2.0, target T = 1",
+               _row_two_temps(3.0, 1.2, 2.0), pair=True),
     ]
 }
 
@@ -121,10 +137,10 @@ def uniforms24(seed: int, row: int, n: int = 3) -> np.ndarray:
     return (k.astype(np.float64) / float(1 << 24)).astype(np.float32)
 
 
-def draw_drafts(q32: np.ndarray, K: int, seed: int, row: int) -> np.ndarray:
+def draw_drafts(q32: np.ndarray, K: int, seed: int, row: int, stream: int = _S_DRAFT) -> np.ndarray:
     """K i.i.d. tokens from the fp32 draft row by inverse CDF (the draft model's sampling)."""
     cdf = np.cumsum(q32.astype(np.float64))
-    u = _rng(seed, _S_DRAFT, row).random(K)
+    u = _rng(seed, stream, row).random(K)
     t = np.searchsorted(cdf, u * cdf[-1], side="right")
     return np.minimum(t, len(q32) - 1).astype(np.int32)
 
@@ -133,7 +149,9 @@ def generate(name: str, rows: Optional[Sequence[int]] = None, B: Optional[int] =
     """Build the workload ``name`` (all rows, an explicit row list, or the first ``B`` rows).
 
     Returns a dict with ``p``, ``q`` (fp32 [n][V]), ``drafts`` (int32 [n][K]),
-    ``u`` (fp32 [n][3]: selection, accept and residual uniforms), ``rows`` and ``config``.
+    ``u`` (fp32 [n][3]: selection, accept and residual uniforms), ``rows`` and ``config``;
+    two-distribution workloads also return ``q2`` (the second draft's distribution;
+    ``drafts[:, 0]`` is drawn from ``q``, ``drafts[:, 1]`` from ``q2``).
     """
     cfg = CONFIGS[name]
     if rows is None:
@@ -144,13 +162,22 @@ def generate(name: str, rows: Optional[Sequence[int]] = None, B: Optional[int] =
     q = np.empty((n, cfg.V), np.float32)
     drafts = np.empty((n, cfg.K), np.int32)
     u = np.empty((n, 3), np.float32)
+    q2 = np.empty((n, cfg.V), np.float32) if cfg.pair else None
     for i, b in enumerate(rows):
-        p64, q64 = cfg.row(cfg, b)
-        p[i] = p64.astype(np.float32)
-        q[i] = q64.astype(np.float32)
-        drafts[i] = draw_drafts(q[i], cfg.K, cfg.seed, b)
+        vals = cfg.row(cfg, b)
+        p[i] = vals[0].astype(np.float32)
+        q[i] = vals[1].astype(np.float32)
+        if cfg.pair:
+            q2[i] = vals[2].astype(np.float32)
+            drafts[i, 0] = draw_drafts(q[i], 1, cfg.seed, b)[0]
+            drafts[i, 1] = draw_drafts(q2[i], 1, cfg.seed, b, stream=_S_DRAFT2)[0]
+        else:
+            drafts[i] = draw_drafts(q[i], cfg.K, cfg.seed, b)
         u[i] = uniforms24(cfg.seed, b)
-    return {"p": p, "q": q, "drafts": drafts, "u": u, "rows": np.asarray(rows, np.int64), "config": cfg}
+    out = {"p": p, "q": q, "drafts": drafts, "u": u, "rows": np.asarray(rows, np.int64), "config": cfg}
+    if cfg.pair:
+        out["q2"] = q2
+    return out
 
 
 def dirichlet_instances(seed: int, V: int, count: int, alpha: float = 0.5):
