@@ -122,6 +122,30 @@ mdss_status mdss_accept_or_resample(const float* p, const float* r, const int32_
                                     uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
                                     void* stream);
 
+/* ---- Two drafts from different distributions (K = 2) --------------------
+ * Remark 1 (and the non-identical K = 2 appendix): X1 ~ q1 and X2 ~ q2
+ * independently.  The classical weight of draft i is w_i(x) = p(x)/q_i(x),
+ * the target over the distribution that proposed it, and
+ * Pr(I = i | x1, x2) = w_i(x_i) / (w_1(x1) + w_2(x2)) (uniform when both are
+ * zero).  The induced distribution is
+ *   r(y) = p(y) [ sum_{x in supp q2} q2(x) / (w_1(y) + w_2(x))      (if q1(y) > 0)
+ *               + sum_{x in supp q1} q1(x) / (w_1(x) + w_2(y)) ]    (if q2(y) > 0)
+ * and, for p(y) = 0, r(y) = (q1(y) Q2_0 + q2(y) Q1_0) / 2, Qi_0 = q_i-mass of
+ * the tokens with p = 0.  Two O(n1 n2) sums per row.  Same conventions and
+ * errors as the identical-draft calls; q1, q2 are [B][V] fp32. */
+size_t mdss_workspace_bytes_pair(int64_t B, int64_t V);
+
+mdss_status mdss_induced_dist_pair(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, float* r,
+                                   int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Selection between drafts[b][0] ~ q1 and drafts[b][1] ~ q2: w_1 = p(x1)/q1(x1),
+ * w_2 = p(x2)/q2(x2) in fp64; index 0 iff u_sel (w_1 + w_2) < w_1; both zero:
+ * floor(2 u_sel).  Outputs and row flags as mdss_select_intermediate. */
+mdss_status mdss_select_intermediate_pair(const float* p, const float* q1, const float* q2, const int32_t* drafts,
+                                          const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+                                          int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
+                                          void* stream);
+
 /* Static, thread-safe description of a status code. */
 const char* mdss_status_string(mdss_status s);
 

@@ -18,9 +18,13 @@ from .binding import (  # noqa: F401
     MdssError,
     accept_or_resample,
     induced_dist,
+    induced_dist_pair,
     library_path,
     load_library,
     select_intermediate,
+    select_intermediate_pair,
     step,
+    step_pair,
     workspace_bytes,
+    workspace_bytes_pair,
 )

@@ -55,7 +55,12 @@ def load_library():
         lib.mdss_induced_dist.argtypes = [P, P, i64, i64, i32, i32, P, P, P, sz, P]
         lib.mdss_select_intermediate.argtypes = [P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P]
         lib.mdss_accept_or_resample.argtypes = [P, P, P, P, u64, u64, i64, i64, P, P, P, P, P, P]
-        for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample"):
+        lib.mdss_workspace_bytes_pair.argtypes = [i64, i64]
+        lib.mdss_workspace_bytes_pair.restype = sz
+        lib.mdss_induced_dist_pair.argtypes = [P, P, P, i64, i64, P, P, P, sz, P]
+        lib.mdss_select_intermediate_pair.argtypes = [P, P, P, P, P, u64, u64, i64, i64, P, P, P, P]
+        for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample",
+                  "mdss_induced_dist_pair", "mdss_select_intermediate_pair"):
             getattr(lib, f).restype = ctypes.c_int
         lib.mdss_status_string.argtypes = [ctypes.c_int]
         lib.mdss_status_string.restype = ctypes.c_char_p
@@ -181,6 +186,69 @@ def accept_or_resample(p: torch.Tensor, r: torch.Tensor, sel_token: torch.Tensor
                                        ctypes.c_uint64(offset), B, V, _ptr(out), _ptr(acc), _ptr(res), _ptr(mass),
                                        _ptr(row_status), _stream(dev)))
     return out, acc, res, mass
+
+
+def workspace_bytes_pair(B: int, V: int) -> int:
+    return int(load_library().mdss_workspace_bytes_pair(B, V))
+
+
+def induced_dist_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, r: Optional[torch.Tensor] = None,
+                      row_status: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """r [B][V] fp32 for two drafts X1 ~ q1, X2 ~ q2 with the classical weights p / q_i."""
+    lib = load_library()
+    B, V, dev = _pq(p, q1)
+    _need(q2, "q2", torch.float32, (B, V), dev)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    need = int(lib.mdss_workspace_bytes_pair(B, V))
+    if need == 0:
+        _check("mdss_workspace_bytes_pair", 2)
+    if workspace is None:
+        workspace = _workspace(dev, need)
+    elif workspace.dtype != torch.uint8 or workspace.device != dev or workspace.numel() < need:
+        raise ValueError(f"workspace must be a uint8 tensor on {dev} of at least {need} bytes")
+    _check("mdss_induced_dist_pair",
+           lib.mdss_induced_dist_pair(_ptr(p), _ptr(q1), _ptr(q2), B, V, _ptr(r), _ptr(row_status),
+                                      _ptr(workspace), workspace.numel(), _stream(dev)))
+    return r
+
+
+def select_intermediate_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, drafts: torch.Tensor,
+                             u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0,
+                             row_status: Optional[torch.Tensor] = None):
+    """(sel_index, sel_token) between drafts[:, 0] ~ q1 and drafts[:, 1] ~ q2."""
+    lib = load_library()
+    B, V, dev = _pq(p, q1)
+    _need(q2, "q2", torch.float32, (B, V), dev)
+    _need(drafts, "drafts", torch.int32, (B, 2), dev)
+    if u is not None:
+        _need(u, "u", torch.float32, (B, 3), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    sel_index = torch.empty(B, dtype=torch.int32, device=dev)
+    sel_token = torch.empty(B, dtype=torch.int32, device=dev)
+    _check("mdss_select_intermediate_pair",
+           lib.mdss_select_intermediate_pair(_ptr(p), _ptr(q1), _ptr(q2), _ptr(drafts), _ptr(u),
+                                             ctypes.c_uint64(seed), ctypes.c_uint64(offset), B, V, _ptr(sel_index),
+                                             _ptr(sel_token), _ptr(row_status), _stream(dev)))
+    return sel_index, sel_token
+
+
+def step_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, drafts: torch.Tensor,
+              u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False):
+    """The whole path for two drafts from different distributions."""
+    B = p.shape[0]
+    status = torch.zeros(B, dtype=torch.int32, device=p.device)
+    r = induced_dist_pair(p, q1, q2, row_status=status)
+    sel_index, sel_token = select_intermediate_pair(p, q1, q2, drafts, u, seed, offset, row_status=status)
+    out, acc, res, mass = accept_or_resample(p, r, sel_token, u, seed, offset, want_residual=want_residual,
+                                             want_mass=want_residual, row_status=status)
+    return {"r": r, "sel_index": sel_index, "sel_token": sel_token, "out_token": out, "accepted": acc,
+            "residual": res, "mass": mass, "status": status}
 
 
 def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[torch.Tensor] = None, seed: int = 0,

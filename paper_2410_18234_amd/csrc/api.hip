@@ -61,6 +61,34 @@ mdss_status mdss_induced_dist(const float* p, const float* q, int64_t B, int64_t
   return from_hip(mdss::launch_induced(p, q, B, V, K, s_max, r, row_status, ws, static_cast<hipStream_t>(stream)));
 }
 
+size_t mdss_workspace_bytes_pair(int64_t B, int64_t V) {
+  if (check_shape(B, V) != MDSS_OK) return 0;
+  return mdss::workspace_bytes_pair(B, V);
+}
+
+mdss_status mdss_induced_dist_pair(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, float* r,
+                                   int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!p || !q1 || !q2 || !r) return MDSS_EINVAL;
+  const mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  const size_t need = mdss::workspace_bytes_pair(B, V);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) % 256) != 0)
+    return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_induced_pair(p, q1, q2, B, V, r, row_status, workspace,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+mdss_status mdss_select_intermediate_pair(const float* p, const float* q1, const float* q2, const int32_t* drafts,
+                                          const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+                                          int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
+                                          void* stream) {
+  if (!p || !q1 || !q2 || !drafts || !sel_index || !sel_token) return MDSS_EINVAL;
+  const mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  return from_hip(mdss::launch_select_pair(p, q1, q2, drafts, u, seed, offset, B, V, sel_index, sel_token,
+                                           row_status, static_cast<hipStream_t>(stream)));
+}
+
 mdss_status mdss_select_intermediate(const float* p, const float* q, const int32_t* drafts, const float* u,
                                      uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
                                      int32_t* sel_index, int32_t* sel_token, int32_t* row_status, void* stream) {

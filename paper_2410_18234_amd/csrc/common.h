@@ -49,6 +49,12 @@ int choose_splits(int64_t B, int64_t V, int K, int s_max);
 
 hipError_t launch_induced(const float* p, const float* q, int64_t B, int64_t V, int K, int s_max, float* r,
                           int32_t* row_status, const Workspace& ws, hipStream_t st);
+size_t workspace_bytes_pair(int64_t B, int64_t V);
+hipError_t launch_induced_pair(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, float* r,
+                               int32_t* row_status, void* workspace, hipStream_t st);
+hipError_t launch_select_pair(const float* p, const float* q1, const float* q2, const int32_t* drafts,
+                              const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+                              int32_t* sel_index, int32_t* sel_token, int32_t* row_status, hipStream_t st);
 hipError_t launch_select(const float* p, const float* q, const int32_t* drafts, const float* u, uint64_t seed,
                          uint64_t offset, int64_t B, int64_t V, int K, int32_t* sel_index, int32_t* sel_token,
                          int32_t* row_status, hipStream_t st);

@@ -364,6 +364,22 @@ __device__ __forceinline__ void write_r(int64_t b, int64_t V, int K, const RowHd
   r[b * V + y] = (float)v;
 }
 
+// Result of a K = 2 sweep for query j of row b: with one pole split, r is
+// written directly (identical drafts) or the unscaled sum is stored by token
+// into `dense` (two draft distributions); otherwise the split's partial sum.
+__device__ __forceinline__ void store_sum(int64_t b, int64_t V, const RowHdr& h, int j, int split, double S,
+                                          const Workspace& wq, double* __restrict__ dense,
+                                          const float* __restrict__ p, const float* __restrict__ q,
+                                          float* __restrict__ r) {
+  if (wq.P > 1) {
+    wq.part[(b * wq.P + split) * wq.Sp + j] = S;
+  } else if (dense) {
+    dense[b * V + wq.idx[b * wq.Sp + j]] = S;
+  } else {
+    write_r(b, V, 2, h, wq.idx[b * wq.Sp + j], S, p, q, r);
+  }
+}
+
 // ------------------------------------------------------------------ K = 2 sweep, direct rows
 // Rows whose weight range is too wide for the rational form: one reciprocal
 // per (query, pole).  grid (query blocks of 256 * R, pole splits P, rows B);
@@ -372,20 +388,22 @@ __device__ __forceinline__ void write_r(int64_t b, int64_t V, int K, const RowHd
 template <int R>
 __global__ __launch_bounds__(kSweepThreads) void sweep_k2_direct_kernel(const float* __restrict__ p,
                                                                   const float* __restrict__ q, int64_t V,
-                                                                  float* __restrict__ r, Workspace ws) {
+                                                                  float* __restrict__ r, Workspace wq, Workspace wp,
+                                                                  double* __restrict__ dense) {
   const int64_t b = blockIdx.z;
   const int split = blockIdx.y;
-  const RowHdr h = ws.hdr[b];
+  const RowHdr h = wq.hdr[b];
   if (h.mode != kDirect) return;
   const int n = h.n;
+  const int npole = wp.hdr[b].n;
   const int y0 = blockIdx.x * (kSweepThreads * R);
   if (y0 >= n) return;
   const int tid = threadIdx.x;
   // the pairs are split in groups of 8 poles (16 floats)
-  const int ngroups = (int)(round_up(n, 8) / 8);
-  const int g_lo = (int)((int64_t)ngroups * split / ws.P);
-  const int g_hi = (int)((int64_t)ngroups * (split + 1) / ws.P);
-  const float* stream = ws.stream + b * ws.ld;
+  const int ngroups = (int)(round_up(npole, 8) / 8);
+  const int g_lo = (int)((int64_t)ngroups * split / wq.P);
+  const int g_hi = (int)((int64_t)ngroups * (split + 1) / wq.P);
+  const float* stream = wp.stream + b * wp.ld;
   const int64_t f_lo = 16 * (int64_t)g_lo, f_hi = 16 * (int64_t)g_hi;  // float range of the split
 
   float a[R];
@@ -393,7 +411,7 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_k2_direct_kernel(const fl
 #pragma unroll
   for (int i = 0; i < R; ++i) {
     const int j = y0 + i * kSweepThreads + tid;
-    a[i] = (j < n) ? ws.wc[b * ws.Sp + j] : 1.0f;
+    a[i] = (j < n) ? wq.wc[b * wq.Sp + j] : 1.0f;
     acc[i] = 0.0;
   }
   __shared__ float4 tile[kTileFloats / 4];
@@ -426,11 +444,7 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_k2_direct_kernel(const fl
   for (int i = 0; i < R; ++i) {
     const int j = y0 + i * kSweepThreads + tid;
     if (j >= n) continue;
-    if (ws.P == 1) {
-      write_r(b, V, 2, h, ws.idx[b * ws.Sp + j], acc[i], p, q, r);
-    } else {
-      ws.part[(b * ws.P + split) * ws.Sp + j] = acc[i];
-    }
+    store_sum(b, V, h, j, split, acc[i], wq, dense, p, q, r);
   }
 }
 
@@ -644,7 +658,8 @@ __device__ __forceinline__ void mfma_sweep(const float4* __restrict__ src, int n
 
 __global__ __launch_bounds__(kMfmaThreads) void sweep_k2_mfma_kernel(const float* __restrict__ p,
                                                                       const float* __restrict__ q, int64_t V,
-                                                                      float* __restrict__ r, Workspace ws, int nqb,
+                                                                      float* __restrict__ r, Workspace wq, Workspace wp,
+                                                                      double* __restrict__ dense, int nqb,
                                                                       int64_t total) {
   constexpr int MT = kMfmaMT;
   // XCD-aware mapping: hardware block h runs on XCD h % 8; give each XCD a contiguous logical range
@@ -653,17 +668,18 @@ __global__ __launch_bounds__(kMfmaThreads) void sweep_k2_mfma_kernel(const float
   const int64_t logical = x * per + (x < rem ? x : rem) + hw / 8;
   const int qb = (int)(logical % nqb);
   const int64_t rest = logical / nqb;
-  const int split = (int)(rest % ws.P);
-  const int64_t b = rest / ws.P;
-  const RowHdr h = ws.hdr[b];
+  const int split = (int)(rest % wq.P);
+  const int64_t b = rest / wq.P;
+  const RowHdr h = wq.hdr[b];
   if (h.mode != kRat8 && h.mode != kRat4) return;
   const int n = h.n;
+  const int npole = wp.hdr[b].n;
   const int q0 = qb * kMfmaQueries;
   if (q0 >= n) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, col = lane & 15;
   const int C = h.mode;
-  const float* wc = ws.wc + b * ws.Sp;
+  const float* wc = wq.wc + b * wq.Sp;
 
   // A[i][k] = part slot_a(k % 6) of a_i^(k / 6) (row i = col); accumulator input a^C for rows 4 g + r
   bf16x8 AX[MT];
@@ -707,10 +723,10 @@ __global__ __launch_bounds__(kMfmaThreads) void sweep_k2_mfma_kernel(const float
   }
   const int poles_per_block = (C == 8) ? 128 : 64;
   const int F = (C == 8) ? 192 : 128;
-  const int nblocks = (int)(round_up(n, kBlockPoles) / poles_per_block);
-  const int b_lo = (int)((int64_t)nblocks * split / ws.P);
-  const int b_hi = (int)((int64_t)nblocks * (split + 1) / ws.P);
-  const float4* src = reinterpret_cast<const float4*>(ws.stream + b * ws.ld) + (int64_t)b_lo * F;
+  const int nblocks = (int)(round_up(npole, kBlockPoles) / poles_per_block);
+  const int b_lo = (int)((int64_t)nblocks * split / wq.P);
+  const int b_hi = (int)((int64_t)nblocks * (split + 1) / wq.P);
+  const float4* src = reinterpret_cast<const float4*>(wp.stream + b * wp.ld) + (int64_t)b_lo * F;
   __shared__ float4 tile[kMfmaTileF4];
   double acc64[MT][4];
 #pragma unroll
@@ -739,11 +755,7 @@ __global__ __launch_bounds__(kMfmaThreads) void sweep_k2_mfma_kernel(const float
       for (int rr = 0; rr < 4; ++rr) {
         const int qi = q0 + 16 * (MT * wave + t) + 4 * g + rr;
         if (qi >= n) continue;
-        if (ws.P == 1) {
-          write_r(b, V, 2, h, ws.idx[b * ws.Sp + qi], acc64[t][rr], p, q, r);
-        } else {
-          ws.part[(b * ws.P + split) * ws.Sp + qi] = acc64[t][rr];
-        }
+        store_sum(b, V, h, qi, split, acc64[t][rr], wq, dense, p, q, r);
       }
   }
 }
@@ -856,6 +868,224 @@ __global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__
   write_r(b, V, K, h, ws.idx[b * ws.Sp + j], S, p, q, r);
 }
 
+
+// ------------------------------------------------------------------ two draft distributions (K = 2)
+// Drafts X1 ~ q1, X2 ~ q2 with the classical weights w_i = p / q_i (Remark 1;
+// the non-identical K = 2 appendix).  Splitting the drafted pairs by which
+// index holds y gives
+//   r(y) = p(y) [ S_2(w_1(y)) + S_1(w_2(y)) ],  S_i(a) = sum_{x in supp q_i} q_i(x) / (a + w_i(x)),
+// the first term only when q1(y) > 0 and the second only when q2(y) > 0;
+// a zero-target token gets (q1(y) Q2_0 + q2(y) Q1_0) / 2, Qi_0 the q_i-mass of
+// the zero-weight tokens of draft i (both weights zero: uniform index).
+// Each S_i is one sweep of the K = 2 kernels with the queries of one draft
+// and the poles of the other, sharing one scale over both drafts' weights.
+__global__ __launch_bounds__(kPrepThreads) void prep_pair_kernel(const float* __restrict__ p,
+                                                                  const float* __restrict__ q1,
+                                                                  const float* __restrict__ q2, int64_t V,
+                                                                  float* __restrict__ r,
+                                                                  int32_t* __restrict__ row_status, Workspace w1,
+                                                                  Workspace w2) {
+  const int64_t b = blockIdx.x;
+  const float* pb = p + b * V;
+  const float* ab = q1 + b * V;
+  const float* cb = q2 + b * V;
+  float* rb = r + b * V;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  constexpr int kWaves = kPrepThreads / 64;
+  __shared__ double s_z1[kWaves], s_z2[kWaves];
+  __shared__ int s_n1[kWaves], s_n2[kWaves], s_bad[kWaves];
+  __shared__ float s_wmin[kWaves], s_wmax[kWaves];
+  __shared__ int s_scan1[kWaves], s_scan2[kWaves];
+  __shared__ RowHdr s_h1, s_h2;
+
+  int bad = 0, n1 = 0, n2 = 0;
+  double z1 = 0.0, z2 = 0.0;
+  float wmin = INFINITY, wmax = 0.0f;
+  for (int64_t x = tid; x < V; x += kPrepThreads) {
+    const float pv = pb[x], av = ab[x], cv = cb[x];
+    bad |= (int)(bad_prob(pv) || bad_prob(av) || bad_prob(cv));
+    if (av > 0.0f) {
+      ++n1;
+      if (pv == 0.0f) {
+        z1 += (double)av;
+      } else {
+        const float w = pv / av;
+        wmin = fminf(wmin, w);
+        wmax = fmaxf(wmax, w);
+      }
+    }
+    if (cv > 0.0f) {
+      ++n2;
+      if (pv == 0.0f) {
+        z2 += (double)cv;
+      } else {
+        const float w = pv / cv;
+        wmin = fminf(wmin, w);
+        wmax = fmaxf(wmax, w);
+      }
+    }
+  }
+  bad = wave_sum_int(bad);
+  n1 = wave_sum_int(n1);
+  n2 = wave_sum_int(n2);
+  z1 = wave_sum(z1);
+  z2 = wave_sum(z2);
+  wmin = wave_min(wmin);
+  wmax = wave_max(wmax);
+  if (lane == 0) {
+    s_bad[wid] = bad;
+    s_n1[wid] = n1;
+    s_n2[wid] = n2;
+    s_z1[wid] = z1;
+    s_z2[wid] = z2;
+    s_wmin[wid] = wmin;
+    s_wmax[wid] = wmax;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int tb = 0, t1 = 0, t2 = 0;
+    double tz1 = 0.0, tz2 = 0.0;
+    float mn = INFINITY, mx = 0.0f;
+    for (int i = 0; i < kWaves; ++i) {
+      tb |= s_bad[i];
+      t1 += s_n1[i];
+      t2 += s_n2[i];
+      tz1 += s_z1[i];
+      tz2 += s_z2[i];
+      mn = fminf(mn, s_wmin[i]);
+      mx = fmaxf(mx, s_wmax[i]);
+    }
+    RowHdr h;
+    h.pad = 0.0;
+    h.scale = 0;
+    h.flags = tb ? kRowBadProb : 0;
+    if (h.flags || !(mx > 0.0f)) {
+      h.mode = kSkip;  // flagged, or no positive weight (every support token has p = 0)
+    } else {
+      int e_lo, e_hi;
+      frexpf(mn, &e_lo);
+      frexpf(mx, &e_hi);
+      const int range = e_hi - e_lo;
+      if (!isfinite(mx) || range > kRat4MaxRange) {
+        h.mode = kDirect;
+      } else {
+        h.mode = range <= kRat8MaxRange ? kRat8 : kRat4;
+        h.scale = -((e_lo + e_hi) >> 1);
+      }
+    }
+    RowHdr h1 = h, h2 = h;
+    h1.n = t1;
+    h1.q0 = tz1;
+    h2.n = t2;
+    h2.q0 = tz2;
+    s_h1 = h1;
+    s_h2 = h2;
+    w1.hdr[b] = h1;
+    w2.hdr[b] = h2;
+    if (row_status && h.flags) row_status[b] |= h.flags;
+  }
+  __syncthreads();
+  const RowHdr h1 = s_h1, h2 = s_h2;
+  if (h1.flags) {
+    for (int64_t x = tid; x < V; x += kPrepThreads) rb[x] = NAN;
+    return;
+  }
+  if (h1.mode == kSkip) return;  // r is formed by finalize_pair_kernel alone
+  int run1 = 0, run2 = 0;
+  for (int64_t base = 0; base < V; base += 4 * kPrepThreads) {
+    const int64_t x0 = base + 4 * (int64_t)tid;
+    float pv[4], av[4], cv[4];
+    int c1 = 0, c2 = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t x = x0 + i;
+      pv[i] = (x < V) ? pb[x] : 0.0f;
+      av[i] = (x < V) ? ab[x] : 0.0f;
+      cv[i] = (x < V) ? cb[x] : 0.0f;
+      c1 += (av[i] > 0.0f);
+      c2 += (cv[i] > 0.0f);
+    }
+    const int i1 = wave_inclusive_scan_int(c1, lane), i2 = wave_inclusive_scan_int(c2, lane);
+    if (lane == 63) {
+      s_scan1[wid] = i1;
+      s_scan2[wid] = i2;
+    }
+    __syncthreads();
+    int off1 = 0, off2 = 0, tot1 = 0, tot2 = 0;
+    for (int i = 0; i < kWaves; ++i) {
+      off1 += (i < wid) ? s_scan1[i] : 0;
+      off2 += (i < wid) ? s_scan2[i] : 0;
+      tot1 += s_scan1[i];
+      tot2 += s_scan2[i];
+    }
+    int o1 = run1 + off1 + i1 - c1, o2 = run2 + off2 + i2 - c2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t x = x0 + i;
+      if (x >= V) break;
+      if (av[i] > 0.0f) {
+        const float w = pv[i] / av[i];
+        w1.idx[b * w1.Sp + o1] = (int32_t)x;
+        w1.wc[b * w1.Sp + o1] = (h1.mode == kDirect) ? w : ldexpf(w, h1.scale);
+        w1.qc[b * w1.Sp + o1] = av[i];
+        ++o1;
+      }
+      if (cv[i] > 0.0f) {
+        const float w = pv[i] / cv[i];
+        w2.idx[b * w2.Sp + o2] = (int32_t)x;
+        w2.wc[b * w2.Sp + o2] = (h2.mode == kDirect) ? w : ldexpf(w, h2.scale);
+        w2.qc[b * w2.Sp + o2] = cv[i];
+        ++o2;
+      }
+    }
+    run1 += tot1;
+    run2 += tot2;
+    __syncthreads();
+  }
+  const int np1 = (int)round_up(h1.n, kBlockPolesPrep), np2 = (int)round_up(h2.n, kBlockPolesPrep);
+  for (int j = h1.n + tid; j < np1; j += kPrepThreads) {
+    w1.idx[b * w1.Sp + j] = -1;
+    w1.wc[b * w1.Sp + j] = 0.0f;
+    w1.qc[b * w1.Sp + j] = 0.0f;
+  }
+  for (int j = h2.n + tid; j < np2; j += kPrepThreads) {
+    w2.idx[b * w2.Sp + j] = -1;
+    w2.wc[b * w2.Sp + j] = 0.0f;
+    w2.qc[b * w2.Sp + j] = 0.0f;
+  }
+}
+
+// Sum of the pole splits of each query, stored by token into `dense`.
+__global__ __launch_bounds__(256) void dense_from_parts_kernel(int64_t V, Workspace wq, double* __restrict__ dense) {
+  const int64_t b = blockIdx.y;
+  const RowHdr h = wq.hdr[b];
+  if (h.mode == kSkip) return;
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= h.n) return;
+  double S = 0.0;
+  for (int s = 0; s < wq.P; ++s) S += wq.part[(b * wq.P + s) * wq.Sp + j];
+  dense[b * V + wq.idx[b * wq.Sp + j]] = S;
+}
+
+__global__ __launch_bounds__(256) void finalize_pair_kernel(const float* __restrict__ p,
+                                                             const float* __restrict__ q1,
+                                                             const float* __restrict__ q2, int64_t V,
+                                                             float* __restrict__ r, Workspace w1, Workspace w2,
+                                                             const double* __restrict__ s_a,
+                                                             const double* __restrict__ s_b) {
+  const int64_t b = blockIdx.y;
+  const RowHdr h1 = w1.hdr[b], h2 = w2.hdr[b];
+  if (h1.flags) return;
+  const int64_t y = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (y >= V) return;
+  const int64_t i = b * V + y;
+  const float pv = p[i], av = q1[i], cv = q2[i];
+  double v = 0.0;
+  if (av > 0.0f) v += (pv > 0.0f) ? (double)pv * ldexp(s_a[i], h1.scale) : 0.5 * (double)av * h2.q0;
+  if (cv > 0.0f) v += (pv > 0.0f) ? (double)pv * ldexp(s_b[i], h1.scale) : 0.5 * (double)cv * h1.q0;
+  r[i] = (float)v;
+}
+
 constexpr int kK2R = 8;
 constexpr int kK3R = 4;
 
@@ -927,11 +1157,11 @@ hipError_t launch_induced(const float* p, const float* q, int64_t B, int64_t V, 
                        st, ws);
     const int nqb = (int)((V + kMfmaQueries - 1) / kMfmaQueries);
     const int64_t total = (int64_t)nqb * ws.P * B;
-    hipLaunchKernelGGL(sweep_k2_mfma_kernel, dim3((unsigned)total), dim3(kMfmaThreads), 0, st, p, q, V, r, ws, nqb,
-                       total);
+    hipLaunchKernelGGL(sweep_k2_mfma_kernel, dim3((unsigned)total), dim3(kMfmaThreads), 0, st, p, q, V, r, ws, ws,
+                       nullptr, nqb, total);
     const int64_t yb = (V + kSweepThreads * kK2R - 1) / (kSweepThreads * kK2R);
     hipLaunchKernelGGL(sweep_k2_direct_kernel<kK2R>, dim3((unsigned)yb, (unsigned)ws.P, (unsigned)B),
-                       dim3(kSweepThreads), 0, st, p, q, V, r, ws);
+                       dim3(kSweepThreads), 0, st, p, q, V, r, ws, ws, nullptr);
   } else {
     const int64_t yb = (ws.Sp + kSweepThreads * kK3R - 1) / (kSweepThreads * kK3R);
     const size_t lds = sizeof(float) * 4 * ws.Sp;  // w', q, stream (2 per pole)
@@ -942,6 +1172,54 @@ hipError_t launch_induced(const float* p, const float* q, int64_t B, int64_t V, 
     hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)((ws.Sp + 255) / 256), (unsigned)B), dim3(256), 0, st, p, q,
                        V, K, r, ws);
   }
+  return hipGetLastError();
+}
+
+
+size_t workspace_bytes_pair(int64_t B, int64_t V) {
+  const int P = choose_splits(B, V, 2, 0);
+  return 2 * workspace_bytes(B, V, 2, 0, P) + 2 * align256(sizeof(double) * B * V);
+}
+
+hipError_t launch_induced_pair(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, float* r,
+                               int32_t* row_status, void* workspace, hipStream_t st) {
+  const int P = choose_splits(B, V, 2, 0);
+  const size_t one = workspace_bytes(B, V, 2, 0, P);
+  Workspace w1, w2;
+  char* base = static_cast<char*>(workspace);
+  carve_workspace(base, B, V, 2, 0, P, &w1);
+  carve_workspace(base + one, B, V, 2, 0, P, &w2);
+  double* s_a = reinterpret_cast<double*>(base + 2 * one);
+  double* s_b = reinterpret_cast<double*>(base + 2 * one + align256(sizeof(double) * B * V));
+  hipLaunchKernelGGL(prep_pair_kernel, dim3((unsigned)B), dim3(kPrepThreads), 0, st, p, q1, q2, V, r, row_status, w1,
+                     w2);
+  const int64_t units = w1.Sp / 4;
+  for (const Workspace* w : {&w1, &w2}) {
+    hipLaunchKernelGGL(pole_stream_kernel, dim3((unsigned)((units + 255) / 256), (unsigned)B), dim3(256), 0, st, *w,
+                       2);
+    hipLaunchKernelGGL(pole_pack_mfma_kernel, dim3((unsigned)((units + 255) / 256), (unsigned)B), dim3(256), 0, st,
+                       *w);
+  }
+  const int nqb = (int)((V + kMfmaQueries - 1) / kMfmaQueries);
+  const int64_t total = (int64_t)nqb * P * B;
+  const int64_t yb = (V + kSweepThreads * kK2R - 1) / (kSweepThreads * kK2R);
+  // S_2 at the draft-1 weights, then S_1 at the draft-2 weights
+  hipLaunchKernelGGL(sweep_k2_mfma_kernel, dim3((unsigned)total), dim3(kMfmaThreads), 0, st, p, q1, V, r, w1, w2, s_a,
+                     nqb, total);
+  hipLaunchKernelGGL(sweep_k2_direct_kernel<kK2R>, dim3((unsigned)yb, (unsigned)P, (unsigned)B), dim3(kSweepThreads),
+                     0, st, p, q1, V, r, w1, w2, s_a);
+  if (P > 1)
+    hipLaunchKernelGGL(dense_from_parts_kernel, dim3((unsigned)((w1.Sp + 255) / 256), (unsigned)B), dim3(256), 0, st,
+                       V, w1, s_a);
+  hipLaunchKernelGGL(sweep_k2_mfma_kernel, dim3((unsigned)total), dim3(kMfmaThreads), 0, st, p, q2, V, r, w2, w1, s_b,
+                     nqb, total);
+  hipLaunchKernelGGL(sweep_k2_direct_kernel<kK2R>, dim3((unsigned)yb, (unsigned)P, (unsigned)B), dim3(kSweepThreads),
+                     0, st, p, q2, V, r, w2, w1, s_b);
+  if (P > 1)
+    hipLaunchKernelGGL(dense_from_parts_kernel, dim3((unsigned)((w2.Sp + 255) / 256), (unsigned)B), dim3(256), 0, st,
+                       V, w2, s_b);
+  hipLaunchKernelGGL(finalize_pair_kernel, dim3((unsigned)((V + 255) / 256), (unsigned)B), dim3(256), 0, st, p, q1,
+                     q2, V, r, w1, w2, s_a, s_b);
   return hipGetLastError();
 }
 

@@ -75,6 +75,60 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ p
   sel_token[b] = x[istar];
 }
 
+
+// Two drafts proposed by different distributions: w_i = p(x_i) / q_i(x_i).
+__global__ __launch_bounds__(256) void select_pair_kernel(const float* __restrict__ p,
+                                                           const float* __restrict__ q1,
+                                                           const float* __restrict__ q2,
+                                                           const int32_t* __restrict__ drafts,
+                                                           const float* __restrict__ u, uint64_t seed,
+                                                           uint64_t offset, int64_t B, int64_t V,
+                                                           int32_t* __restrict__ sel_index,
+                                                           int32_t* __restrict__ sel_token,
+                                                           int32_t* __restrict__ row_status) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int st = 0;
+  double w[2] = {0.0, 0.0};
+  int32_t x[2];
+  for (int i = 0; i < 2; ++i) {
+    x[i] = drafts[b * 2 + i];
+    if (x[i] < 0 || (int64_t)x[i] >= V) {
+      st |= kRowBadDraft;
+      continue;
+    }
+    const float pv = p[b * V + x[i]], qv = (i == 0 ? q1 : q2)[b * V + x[i]];
+    if (bad_prob(pv) || bad_prob(qv)) {
+      st |= kRowBadProb;
+      continue;
+    }
+    if (!(qv > 0.0f)) {
+      st |= kRowBadDraft;
+      continue;
+    }
+    w[i] = (double)pv / (double)qv;
+  }
+  if (st) {
+    sel_index[b] = -1;
+    sel_token[b] = -1;
+    if (row_status) row_status[b] |= st;
+    return;
+  }
+  float uu[3];
+  position_uniforms(u, seed, offset, b, uu);
+  const double W = w[0] + w[1];
+  const double us = (double)uu[0];
+  int istar;
+  if (W > 0.0) {
+    istar = (us * W < w[0]) ? 0 : 1;
+  } else {
+    istar = (int)floor(us * 2.0);
+    istar = istar < 0 ? 0 : (istar > 1 ? 1 : istar);
+  }
+  sel_index[b] = istar;
+  sel_token[b] = x[istar];
+}
+
 // ------------------------------------------------------------------ accept / resample
 // One workgroup of 16 waves per position.  Pass 1 streams the row in
 // super-tiles of 1024 tokens (wave w takes super-tiles w, w+16, ...), forms
@@ -329,6 +383,14 @@ hipError_t launch_select(const float* p, const float* q, const int32_t* drafts, 
                          int32_t* row_status, hipStream_t st) {
   hipLaunchKernelGGL(select_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, p, q, drafts, u, seed, offset,
                      B, V, K, sel_index, sel_token, row_status);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_pair(const float* p, const float* q1, const float* q2, const int32_t* drafts,
+                              const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+                              int32_t* sel_index, int32_t* sel_token, int32_t* row_status, hipStream_t st) {
+  hipLaunchKernelGGL(select_pair_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, p, q1, q2, drafts, u,
+                     seed, offset, B, V, sel_index, sel_token, row_status);
   return hipGetLastError();
 }
 

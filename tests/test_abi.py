@@ -25,7 +25,8 @@ def _declared_functions():
 def test_header_symbols_exported(lib):
     names = _declared_functions()
     assert {"mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample",
-            "mdss_workspace_bytes", "mdss_status_string", "mdss_abi_version"} <= set(names)
+            "mdss_workspace_bytes", "mdss_status_string", "mdss_abi_version", "mdss_induced_dist_pair",
+            "mdss_select_intermediate_pair", "mdss_workspace_bytes_pair"} <= set(names)
     for n in names:
         assert hasattr(lib, n), f"{n} declared in mdss.h but not exported"
 
@@ -81,3 +82,16 @@ def test_python_binding_refuses_cpu_tensors():
     p = torch.full((2, 8), 0.125)
     with pytest.raises(ValueError):
         mdss.induced_dist(p, p, 2)
+
+
+def test_pair_argument_errors(lib):
+    ws = lib.mdss_workspace_bytes_pair(4, 16)
+    assert ws > lib.mdss_workspace_bytes(4, 16, 2, 0)
+    assert lib.mdss_workspace_bytes_pair(0, 16) == 0
+    f = lib.mdss_induced_dist_pair
+    assert f(FAKE, FAKE, None, 4, 16, FAKE, None, FAKE, ws, None) == 1
+    assert f(FAKE, FAKE, FAKE, 4, 1, FAKE, None, FAKE, ws, None) == 2
+    assert f(FAKE, FAKE, FAKE, 4, 16, FAKE, None, FAKE, ws - 1, None) == 5
+    s = lib.mdss_select_intermediate_pair
+    assert s(FAKE, FAKE, FAKE, None, None, 0, 0, 4, 16, FAKE, FAKE, None, None) == 1
+    assert s(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 70000, 16, FAKE, FAKE, None, None) == 2
