@@ -32,27 +32,31 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def counted_traffic(kernel: str, digest: str):
-    """HBM bytes per launch from the committed PMC summary, only if it was taken on
-    the current kernel sources (else None)."""
+def counted_traffic(workload: str, kernel: str, digest: str):
+    """HBM bytes per launch from the committed PMC summary of this workload, only if
+    it was taken on the current kernel sources (else None)."""
     path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
     try:
         with open(path) as fh:
             d = json.load(fh)
     except (OSError, ValueError):
         return None
-    e = d.get(kernel)
+    e = d.get(workload, {}).get(kernel)
     if not e or e.get("source_digest") != digest:
         return None
     return e.get("bytes_per_launch")
 
 
-def pair_flops(q_np, K: int) -> float:
+def pair_flops(q_np, K: int, q2_np=None) -> float:
     """Algorithmic work of r: K = 2: 6 FLOPs per unordered support pair (add,
     reciprocal, two FMAs) = 3 n (n - 1) per row; K = 3: 4 FLOPs per (query,
-    unordered pair) = 2 n^2 (n + 1) per row."""
+    unordered pair) = 2 n^2 (n + 1) per row.  Two drafts from different
+    distributions: one denominator w1(y) + w2(x) per (y, x) in supp(q1) x
+    supp(q2) serves both sums, 6 FLOPs each = 6 n1 n2 per row."""
     import numpy as np
     n = (q_np > 0).sum(1).astype(np.float64)
+    if q2_np is not None:
+        return float((6.0 * n * (q2_np > 0).sum(1)).sum())
     if K == 2:
         return float((3.0 * n * (n - 1.0)).sum())
     return float((2.0 * n * n * (n + 1.0)).sum())
@@ -67,7 +71,10 @@ def cpu_baseline(w, budget_rows: int):
     p, q, d, u = (np.ascontiguousarray(w[k][:rows]) for k in ("p", "q", "drafts", "u"))
     oracle.step(p[:1, :64], q[:1, :64], d[:1], u[:1])  # load the library outside the timing
     t0 = time.perf_counter()
-    oracle.step(p, q, d, u)
+    if "q2" in w:
+        oracle.step_pair(p, q, np.ascontiguousarray(w["q2"][:rows]), d, u)
+    else:
+        oracle.step(p, q, d, u)
     dt = time.perf_counter() - t0
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     cores = min(cores, os.cpu_count() or cores, rows)
@@ -105,22 +112,35 @@ def main():
     dev = torch.device("cuda:0")
     p = torch.from_numpy(w["p"]).to(dev)
     q = torch.from_numpy(w["q"]).to(dev)
+    q2 = torch.from_numpy(w["q2"]).to(dev) if cfg.pair else None
     drafts = torch.from_numpy(w["drafts"]).to(dev)
     u = torch.from_numpy(w["u"]).to(dev)
     B, V, K = p.shape[0], p.shape[1], cfg.K
     s_max = cfg.s_max
     r = torch.empty_like(p)
     status = torch.zeros(B, dtype=torch.int32, device=dev)
-    ws = torch.empty(mdss.workspace_bytes(B, V, K, s_max), dtype=torch.uint8, device=dev)
+    ws_bytes = mdss.workspace_bytes_pair(B, V) if cfg.pair else mdss.workspace_bytes(B, V, K, s_max)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+
+    def induced():
+        if cfg.pair:
+            mdss.induced_dist_pair(p, q, q2, r=r, row_status=status, workspace=ws)
+        else:
+            mdss.induced_dist(p, q, K, s_max=s_max, r=r, row_status=status, workspace=ws)
+
+    def select():
+        if cfg.pair:
+            return mdss.select_intermediate_pair(p, q, q2, drafts, u, row_status=status)
+        return mdss.select_intermediate(p, q, drafts, u, row_status=status)
 
     def one_step(ev=None):
         status.zero_()
         if ev is not None:
             ev[0].record()
-        mdss.induced_dist(p, q, K, s_max=s_max, r=r, row_status=status, workspace=ws)
+        induced()
         if ev is not None:
             ev[1].record()
-        _, sel_token = mdss.select_intermediate(p, q, drafts, u, row_status=status)
+        _, sel_token = select()
         out, acc, _, _ = mdss.accept_or_resample(p, r, sel_token, u, row_status=status)
         return out, acc
 
@@ -145,17 +165,17 @@ def main():
     assert int(status.abs().sum()) == 0, "rows flagged during the bench"
     accept_rate = float(acc.float().mean())
 
-    flops = pair_flops(w["q"], K)
+    flops = pair_flops(w["q"], K, w.get("q2"))
     achieved = flops / (r_ms * 1e-3) / 1e12
     digest = kernel_source_digest()
     sweep_name = "sweep_k2_mfma_kernel" if K == 2 else "sweep_k3_kernel"
     roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / FP32_PEAK_TFLOPS, 4), "traffic": counted_traffic(sweep_name, digest),
-                "kernel": f"mdss_induced_dist ({sweep_name} + preparation)", "avg_ms": round(r_ms, 4),
+                "frac": round(achieved / FP32_PEAK_TFLOPS, 4), "traffic": counted_traffic(cfg.name, sweep_name, digest),
+                "kernel": f"{'mdss_induced_dist_pair' if cfg.pair else 'mdss_induced_dist'} ({sweep_name} + preparation)", "avg_ms": round(r_ms, 4),
                 "flops_per_launch": flops}
 
     # accept / resample pass over every row with the residual written (12 B per token)
-    _, sel_token = mdss.select_intermediate(p, q, drafts, u)
+    _, sel_token = select()
     res = torch.empty_like(p)
     mass = torch.empty(B, dtype=torch.float64, device=dev)
     import ctypes
@@ -188,7 +208,7 @@ def main():
     res_gbs = res_bytes / (res_ms * 1e-3) / 1e9
     roofline_resample = {"bound": "hbm", "achieved": round(res_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": round(res_gbs / HBM_PEAK_GBS, 4),
-                         "traffic": counted_traffic("accept_kernel", digest),
+                         "traffic": counted_traffic(cfg.name, "accept_kernel", digest),
                          "kernel": "mdss_accept_or_resample, residual and mass written for every row",
                          "avg_ms": round(res_ms, 4), "bytes_per_launch": res_bytes,
                          "note": "%.1f MB per launch: %s the 256 MB Infinity Cache" %
@@ -208,7 +228,8 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.describe}", "B": B, "V": V, "K": K,
-                   "s_max": s_max or None, "accept_rate": round(accept_rate, 4)},
+                   "s_max": s_max or None, "two_draft_distributions": cfg.pair,
+                   "accept_rate": round(accept_rate, 4)},
         "roofline": roofline,
         "roofline_resample": roofline_resample,
         "cpu_baseline": None,
