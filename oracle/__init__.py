@@ -12,6 +12,9 @@ Contents:
   * ``analytic.py``    -- numpy/scipy: output distribution of Algorithm 1,
     acceptance probabilities, the optimal acceptance P* by linear programming
     (Problem 1) and by the explicit expression of Theorem 3.
+  * ``tlp.py``         -- numpy/scipy: the truncated linear program (Algorithm 2,
+    its sort-free variant and the two-distribution version), its LP solved by
+    HiGHS in the paper's own variables.
 
 Notation: ``p`` = TARGET, ``q`` = DRAFT (the paper uses the opposite letters).
 """
