@@ -52,7 +52,8 @@ typedef enum mdss_status {
   MDSS_OK = 0,
   MDSS_EINVAL = 1,       /* null pointer or invalid argument value */
   MDSS_ESHAPE = 2,       /* B outside [1, MDSS_MAX_B] or V outside [2, MDSS_MAX_V] */
-  MDSS_EUNSUPPORTED = 3, /* K outside {2, 3}, or K = 3 with s_max outside [1, MDSS_K3_MAX_SUPPORT] */
+  MDSS_EUNSUPPORTED = 3, /* K outside {2, 3}, K = 3 with s_max outside [1, MDSS_K3_MAX_SUPPORT],
+                            or a truncated-LP s outside [1, MDSS_TLP_MAX_S] */
   MDSS_EDEVICE = 4,      /* a HIP call or kernel launch failed */
   MDSS_EWORKSPACE = 5    /* workspace missing or smaller than mdss_workspace_bytes() */
 } mdss_status;
@@ -62,6 +63,7 @@ typedef enum mdss_status {
 #define MDSS_ROW_BAD_DRAFT 2 /* drafted / selected token out of [0, V) or with q = 0 */
 #define MDSS_ROW_SUPPORT 4   /* K = 3: more than s_max tokens with q > 0 */
 #define MDSS_ROW_FORCED 8    /* rejection with zero residual mass: the selected token is output */
+#define MDSS_ROW_LP_LIMIT 16 /* truncated LP stopped after its augmentation limit (result feasible, maybe not optimal) */
 
 #define MDSS_MAX_V 8388608LL /* rows longer than 2^23 tokens are rejected with MDSS_ESHAPE */
 #define MDSS_MAX_B 65535LL   /* at most 65535 positions per call */
@@ -145,6 +147,65 @@ mdss_status mdss_select_intermediate_pair(const float* p, const float* q1, const
                                           const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
                                           int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
                                           void* stream);
+
+/* ---- Truncated linear program (K = 2) -------------------------------------
+ * The paper's practical selection rule (Algorithm 2, eq. heur, eq. p_Ieq and
+ * the bound eq. p_acc_bnd), for identical drafts (q2 = NULL: both from q1) or
+ * drafts from two distributions (X1 ~ q1, X2 ~ q2; non-identical appendix).
+ * Ranking: tokens ordered by the key p - q1 q2 (computed in fp64, rounded once
+ * to fp32; -0 counts as +0), larger first, ties by lower token id; every
+ * token of the vocabulary is ranked.  Omega_1 = the first min(s, V) ranked
+ * tokens, Omega_2 = the rest.  For a drafted pair {x, y}, x != y:
+ *   both in Omega_2:  tail = MDSS_TLP_SORTED: the earlier-ranked one is selected
+ *                     (eq. heur); tail = MDSS_TLP_HALF: each with probability 1/2
+ *                     (the sort-free variant, eq. heur2);
+ *   one in Omega_1:   that one is selected;
+ *   both in Omega_1:  x is selected with probability w[x][y] (either drafting
+ *                     order), the weights maximising sum over Omega_1 of
+ *                     min(p(k), r(k)) -- the truncated linear program, solved
+ *                     exactly (as a maximum flow) on the device.
+ * Equal drafts select the first one.  r is the resulting distribution of the
+ * selected token (eq. p_Ieq, eq. p_Ieq3 for the HALF tail; the appendix's p~_I
+ * for two distributions); it is the proposal of Algorithm 1
+ * (mdss_accept_or_resample), and acceptance = sum_y min(p(y), r(y)).
+ * At most one LP per position; the SORTED tail sorts each row (O(V) radix
+ * passes), the HALF tail only selects the top s. */
+#define MDSS_TLP_MAX_S 16
+#define MDSS_TLP_SORTED 0
+#define MDSS_TLP_HALF 1
+
+/* Workspace bytes of mdss_truncated_lp (0 if the arguments are invalid). */
+size_t mdss_workspace_bytes_tlp(int64_t B, int64_t V, int32_t tail);
+
+/* p, q1 (and q2 unless NULL): [B][V] fp32 in.  s in [1, MDSS_TLP_MAX_S], tail
+ * MDSS_TLP_SORTED or MDSS_TLP_HALF.  Outputs:
+ *   r       [B][V] fp32, every entry written;
+ *   omega1  [B][s] int32: the Omega_1 tokens in rank order (-1 past min(s, V));
+ *   w       [B][s][s] fp64: w[x][y] (x, y < min(s, V), x != y) = probability
+ *           that Omega_1 token x is selected from the drafted pair {x, y};
+ *           w[y][x] = 1 - w[x][y] as rounded, w[x][x] = 1, other entries 0;
+ *           the selection reads only the entries with x < y;
+ *   accept  [B] fp64 (nullable): sum_y min(p(y), r(y)), computed from r before
+ *           its rounding to fp32.
+ * The optimal weights need not be unique; r on Omega_2, omega1 and the
+ * optimum value are.  A row with a NaN, infinite or negative entry in p, q1
+ * or q2 is flagged MDSS_ROW_BAD_PROB: r and w NaN, omega1 -1, accept NaN.
+ * workspace: at least mdss_workspace_bytes_tlp(B, V, tail) bytes, 256-byte
+ * aligned. */
+mdss_status mdss_truncated_lp(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, int32_t s,
+                              int32_t tail, float* r, int32_t* omega1, double* w, double* accept,
+                              int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Selection between drafts[b][0] ~ q1 and drafts[b][1] ~ q2 (q2 = NULL: q1)
+ * under the truncated rule of mdss_truncated_lp, given its omega1 and w for
+ * the same p, q1, q2, s and tail: f = Pr(Y = X1 | X1, X2) as above (1 for
+ * X1 = X2), index 0 iff u_sel < f (fp64).  A row whose omega1[b][0] is -1 is
+ * flagged MDSS_ROW_BAD_PROB; a drafted id outside [0, V) or with q1(X1) = 0 or
+ * q2(X2) = 0, MDSS_ROW_BAD_DRAFT; such rows get -1. */
+mdss_status mdss_select_truncated_lp(const float* p, const float* q1, const float* q2, const int32_t* drafts,
+                                     const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t s,
+                                     int32_t tail, const int32_t* omega1, const double* w, int32_t* sel_index,
+                                     int32_t* sel_token, int32_t* row_status, void* stream);
 
 /* Static, thread-safe description of a status code. */
 const char* mdss_status_string(mdss_status s);

@@ -14,7 +14,11 @@ from .binding import (  # noqa: F401
     MDSS_ROW_BAD_DRAFT,
     MDSS_ROW_BAD_PROB,
     MDSS_ROW_FORCED,
+    MDSS_ROW_LP_LIMIT,
     MDSS_ROW_SUPPORT,
+    MDSS_TLP_HALF,
+    MDSS_TLP_MAX_S,
+    MDSS_TLP_SORTED,
     MdssError,
     accept_or_resample,
     induced_dist,
@@ -23,8 +27,12 @@ from .binding import (  # noqa: F401
     load_library,
     select_intermediate,
     select_intermediate_pair,
+    select_truncated_lp,
     step,
     step_pair,
+    step_truncated_lp,
+    truncated_lp,
     workspace_bytes,
     workspace_bytes_pair,
+    workspace_bytes_tlp,
 )

@@ -21,6 +21,10 @@ MDSS_ROW_BAD_PROB = 1
 MDSS_ROW_BAD_DRAFT = 2
 MDSS_ROW_SUPPORT = 4
 MDSS_ROW_FORCED = 8
+MDSS_ROW_LP_LIMIT = 16
+MDSS_TLP_MAX_S = 16
+MDSS_TLP_SORTED = 0
+MDSS_TLP_HALF = 1
 
 _STATUS = {0: "MDSS_OK", 1: "MDSS_EINVAL", 2: "MDSS_ESHAPE", 3: "MDSS_EUNSUPPORTED", 4: "MDSS_EDEVICE",
            5: "MDSS_EWORKSPACE"}
@@ -59,8 +63,13 @@ def load_library():
         lib.mdss_workspace_bytes_pair.restype = sz
         lib.mdss_induced_dist_pair.argtypes = [P, P, P, i64, i64, P, P, P, sz, P]
         lib.mdss_select_intermediate_pair.argtypes = [P, P, P, P, P, u64, u64, i64, i64, P, P, P, P]
+        lib.mdss_workspace_bytes_tlp.argtypes = [i64, i64, i32]
+        lib.mdss_workspace_bytes_tlp.restype = sz
+        lib.mdss_truncated_lp.argtypes = [P, P, P, i64, i64, i32, i32, P, P, P, P, P, P, sz, P]
+        lib.mdss_select_truncated_lp.argtypes = [P, P, P, P, P, u64, u64, i64, i64, i32, i32, P, P, P, P, P, P]
         for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample",
-                  "mdss_induced_dist_pair", "mdss_select_intermediate_pair"):
+                  "mdss_induced_dist_pair", "mdss_select_intermediate_pair", "mdss_truncated_lp",
+                  "mdss_select_truncated_lp"):
             getattr(lib, f).restype = ctypes.c_int
         lib.mdss_status_string.argtypes = [ctypes.c_int]
         lib.mdss_status_string.restype = ctypes.c_char_p
@@ -263,3 +272,87 @@ def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[tor
                                              want_mass=want_residual, row_status=status)
     return {"r": r, "sel_index": sel_index, "sel_token": sel_token, "out_token": out, "accepted": acc,
             "residual": res, "mass": mass, "status": status}
+
+
+def workspace_bytes_tlp(B: int, V: int, tail: int = MDSS_TLP_SORTED) -> int:
+    return int(load_library().mdss_workspace_bytes_tlp(B, V, tail))
+
+
+def truncated_lp(p: torch.Tensor, q1: torch.Tensor, q2: Optional[torch.Tensor] = None, s: int = 5,
+                 tail: int = MDSS_TLP_SORTED, r: Optional[torch.Tensor] = None, omega1: Optional[torch.Tensor] = None,
+                 w: Optional[torch.Tensor] = None, accept: Optional[torch.Tensor] = None,
+                 row_status: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    """(r, omega1, w, accept) of the truncated linear program (q2 None: identical drafts from q1)."""
+    lib = load_library()
+    B, V, dev = _pq(p, q1)
+    if q2 is not None:
+        _need(q2, "q2", torch.float32, (B, V), dev)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    if omega1 is None:
+        omega1 = torch.empty((B, s), dtype=torch.int32, device=dev)
+    if w is None:
+        w = torch.empty((B, s, s), dtype=torch.float64, device=dev)
+    if accept is None:
+        accept = torch.empty(B, dtype=torch.float64, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    _need(omega1, "omega1", torch.int32, (B, s), dev)
+    _need(w, "w", torch.float64, (B, s, s), dev)
+    _need(accept, "accept", torch.float64, (B,), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    need = int(lib.mdss_workspace_bytes_tlp(B, V, tail))
+    if need == 0:
+        _check("mdss_workspace_bytes_tlp", 1 if tail not in (MDSS_TLP_SORTED, MDSS_TLP_HALF) else 2)
+    if workspace is None:
+        workspace = _workspace(dev, need)
+    elif workspace.dtype != torch.uint8 or workspace.device != dev or workspace.numel() < need:
+        raise ValueError(f"workspace must be a uint8 tensor on {dev} of at least {need} bytes")
+    _check("mdss_truncated_lp",
+           lib.mdss_truncated_lp(_ptr(p), _ptr(q1), _ptr(q2), B, V, s, tail, _ptr(r), _ptr(omega1), _ptr(w),
+                                 _ptr(accept), _ptr(row_status), _ptr(workspace), workspace.numel(), _stream(dev)))
+    return r, omega1, w, accept
+
+
+def select_truncated_lp(p: torch.Tensor, q1: torch.Tensor, q2: Optional[torch.Tensor], drafts: torch.Tensor,
+                        omega1: torch.Tensor, w: torch.Tensor, tail: int = MDSS_TLP_SORTED,
+                        u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0,
+                        row_status: Optional[torch.Tensor] = None):
+    """(sel_index, sel_token) under the truncated rule given truncated_lp's omega1 and w."""
+    lib = load_library()
+    B, V, dev = _pq(p, q1)
+    if q2 is not None:
+        _need(q2, "q2", torch.float32, (B, V), dev)
+    if omega1.dim() != 2:
+        raise ValueError("omega1 must be [B][s]")
+    s = omega1.shape[1]
+    _need(omega1, "omega1", torch.int32, (B, s), dev)
+    _need(w, "w", torch.float64, (B, s, s), dev)
+    _need(drafts, "drafts", torch.int32, (B, 2), dev)
+    if u is not None:
+        _need(u, "u", torch.float32, (B, 3), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    sel_index = torch.empty(B, dtype=torch.int32, device=dev)
+    sel_token = torch.empty(B, dtype=torch.int32, device=dev)
+    _check("mdss_select_truncated_lp",
+           lib.mdss_select_truncated_lp(_ptr(p), _ptr(q1), _ptr(q2), _ptr(drafts), _ptr(u), ctypes.c_uint64(seed),
+                                        ctypes.c_uint64(offset), B, V, s, tail, _ptr(omega1), _ptr(w),
+                                        _ptr(sel_index), _ptr(sel_token), _ptr(row_status), _stream(dev)))
+    return sel_index, sel_token
+
+
+def step_truncated_lp(p: torch.Tensor, q1: torch.Tensor, q2: Optional[torch.Tensor], drafts: torch.Tensor, s: int = 5,
+                      tail: int = MDSS_TLP_SORTED, u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0,
+                      want_residual: bool = False):
+    """The whole path with the truncated rule: plan, selection, accept / resample."""
+    B = p.shape[0]
+    status = torch.zeros(B, dtype=torch.int32, device=p.device)
+    r, omega1, w, accept = truncated_lp(p, q1, q2, s, tail, row_status=status)
+    sel_index, sel_token = select_truncated_lp(p, q1, q2, drafts, omega1, w, tail, u, seed, offset,
+                                               row_status=status)
+    out, acc, res, mass = accept_or_resample(p, r, sel_token, u, seed, offset, want_residual=want_residual,
+                                             want_mass=want_residual, row_status=status)
+    return {"r": r, "omega1": omega1, "w": w, "accept_prob": accept, "sel_index": sel_index,
+            "sel_token": sel_token, "out_token": out, "accepted": acc, "residual": res, "mass": mass,
+            "status": status}

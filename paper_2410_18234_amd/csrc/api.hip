@@ -33,7 +33,7 @@ const char* mdss_status_string(mdss_status s) {
     case MDSS_OK: return "ok";
     case MDSS_EINVAL: return "invalid argument (null pointer or bad value)";
     case MDSS_ESHAPE: return "invalid shape (B outside [1, MDSS_MAX_B] or V outside [2, MDSS_MAX_V])";
-    case MDSS_EUNSUPPORTED: return "unsupported configuration (K not 2 or 3, or K = 3 with s_max out of range)";
+    case MDSS_EUNSUPPORTED: return "unsupported configuration (K not 2 or 3, K = 3 with s_max out of range, or s outside [1, MDSS_TLP_MAX_S])";
     case MDSS_EDEVICE: return "HIP error while launching";
     case MDSS_EWORKSPACE: return "workspace missing or too small";
   }
@@ -87,6 +87,39 @@ mdss_status mdss_select_intermediate_pair(const float* p, const float* q1, const
   if (s != MDSS_OK) return s;
   return from_hip(mdss::launch_select_pair(p, q1, q2, drafts, u, seed, offset, B, V, sel_index, sel_token,
                                            row_status, static_cast<hipStream_t>(stream)));
+}
+
+size_t mdss_workspace_bytes_tlp(int64_t B, int64_t V, int32_t tail) {
+  if (check_shape(B, V) != MDSS_OK || (tail != MDSS_TLP_SORTED && tail != MDSS_TLP_HALF)) return 0;
+  return mdss::workspace_bytes_tlp(B, V, tail);
+}
+
+mdss_status mdss_truncated_lp(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, int32_t s,
+                              int32_t tail, float* r, int32_t* omega1, double* w, double* accept,
+                              int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!p || !q1 || !r || !omega1 || !w) return MDSS_EINVAL;
+  if (tail != MDSS_TLP_SORTED && tail != MDSS_TLP_HALF) return MDSS_EINVAL;
+  const mdss_status st = check_shape(B, V);
+  if (st != MDSS_OK) return st;
+  if (s < 1 || s > MDSS_TLP_MAX_S) return MDSS_EUNSUPPORTED;
+  const size_t need = mdss::workspace_bytes_tlp(B, V, tail);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) % 256) != 0)
+    return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_tlp(p, q1, q2, B, V, s, tail, r, omega1, w, accept, row_status, workspace,
+                                   static_cast<hipStream_t>(stream)));
+}
+
+mdss_status mdss_select_truncated_lp(const float* p, const float* q1, const float* q2, const int32_t* drafts,
+                                     const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t s,
+                                     int32_t tail, const int32_t* omega1, const double* w, int32_t* sel_index,
+                                     int32_t* sel_token, int32_t* row_status, void* stream) {
+  if (!p || !q1 || !drafts || !omega1 || !w || !sel_index || !sel_token) return MDSS_EINVAL;
+  if (tail != MDSS_TLP_SORTED && tail != MDSS_TLP_HALF) return MDSS_EINVAL;
+  const mdss_status st = check_shape(B, V);
+  if (st != MDSS_OK) return st;
+  if (s < 1 || s > MDSS_TLP_MAX_S) return MDSS_EUNSUPPORTED;
+  return from_hip(mdss::launch_select_tlp(p, q1, q2, drafts, u, seed, offset, B, V, s, tail, omega1, w, sel_index,
+                                          sel_token, row_status, static_cast<hipStream_t>(stream)));
 }
 
 mdss_status mdss_select_intermediate(const float* p, const float* q, const int32_t* drafts, const float* u,
