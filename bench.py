@@ -10,6 +10,7 @@ distributions.  Prints ONE JSON line.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -26,7 +27,7 @@ METRIC = "positions/sec (V=32000, K=2) + % FP32 VALU peak (r) / % HBM BW (resamp
 
 def kernel_source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("api.hip", "common.h", "induced.hip", "sample.hip"):
+    for f in ("api.hip", "common.h", "induced.hip", "sample.hip", "tlp.hip"):
         with open(os.path.join(ROOT, "paper_2410_18234_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -62,25 +63,52 @@ def pair_flops(q_np, K: int, q2_np=None) -> float:
     return float((2.0 * n * n * (n + 1.0)).sum())
 
 
+def cpu_tlp_step(p, q1, q2, drafts, u, s, tail):
+    """The truncated-LP path by the oracle: plan per row, selection, Algorithm 1."""
+    import numpy as np
+
+    import oracle
+    from oracle import tlp
+    B, V = p.shape
+    r = np.empty((B, V), np.float32)
+    om = np.full((B, s), -1, np.int32)
+    betas = np.zeros((B, s, s))
+    for b in range(B):
+        res = tlp.plan_row(p[b], q1[b], None if q2 is None else q2[b], s=s, tail=tail)
+        r[b] = res["r"].astype(np.float32)
+        om[b, :len(res["omega1"])] = res["omega1"]
+        betas[b, :len(res["omega1"]), :len(res["omega1"])] = res["beta"]
+    _, stok, _ = tlp.select(p, q1, q2, drafts, u, om, betas, tail)
+    return oracle.accept_resample(p, r, stok, u)
+
+
 def cpu_baseline(w, budget_rows: int):
     """The fp64 oracle (as it stands) on the first rows of the same workload."""
     import numpy as np
 
     import oracle
+    cfg = w["config"]
     rows = min(budget_rows, w["p"].shape[0])
     p, q, d, u = (np.ascontiguousarray(w[k][:rows]) for k in ("p", "q", "drafts", "u"))
+    q2 = np.ascontiguousarray(w["q2"][:rows]) if "q2" in w else None
     oracle.step(p[:1, :64], q[:1, :64], d[:1], u[:1])  # load the library outside the timing
     t0 = time.perf_counter()
-    if "q2" in w:
-        oracle.step_pair(p, q, np.ascontiguousarray(w["q2"][:rows]), d, u)
+    if cfg.tlp_s:
+        cpu_tlp_step(p, q, q2, d, u, cfg.tlp_s, cfg.tlp_tail)
+    elif q2 is not None:
+        oracle.step_pair(p, q, q2, d, u)
     else:
         oracle.step(p, q, d, u)
     dt = time.perf_counter() - t0
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    cores = min(cores, os.cpu_count() or cores, rows)
+    if cfg.tlp_s:
+        cores = 1  # numpy ranking and a HiGHS LP per position, one thread
+        what = "truncated LP per position (numpy ranking, HiGHS LP), selection, accept/resample"
+    else:
+        cores = min(cores, os.cpu_count() or cores, rows)
+        what = "r by enumeration of all ordered draft pairs, selection, accept/resample"
     return {"value": rows / dt, "unit": "positions/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {rows} positions of the same workload, whole path (r by enumeration of all "
-                      f"ordered draft pairs, selection, accept/resample), {dt:.1f} s wall"}
+            "sample": f"first {rows} positions of the same workload, whole path ({what}), {dt:.1f} s wall"}
 
 
 def main():
@@ -92,6 +120,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline leg")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample size (0: one per core, 2 rounds)")
     ap.add_argument("--resample-reps", type=int, default=20)
+    ap.add_argument("--tlp-tail", choices=["sorted", "half"], default=None,
+                    help="truncated-LP workloads: Omega_2 sorted (Algorithm 2) or halves (its sort-free variant)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -113,22 +143,42 @@ def main():
     p = torch.from_numpy(w["p"]).to(dev)
     q = torch.from_numpy(w["q"]).to(dev)
     q2 = torch.from_numpy(w["q2"]).to(dev) if cfg.pair else None
+    tlp_s, tail = cfg.tlp_s, cfg.tlp_tail
+    if args.tlp_tail is not None:
+        tail = 0 if args.tlp_tail == "sorted" else 1
+        desc = cfg.describe.replace("sorted Omega_2", "sorted Omega_2" if tail == 0 else "Omega_2 pairs split in halves")
+        cfg = dataclasses.replace(cfg, tlp_tail=tail, describe=desc)
+        w["config"] = cfg
+    if tlp_s:
+        omega1 = torch.empty((p.shape[0], tlp_s), dtype=torch.int32, device=dev)
+        wtab = torch.empty((p.shape[0], tlp_s, tlp_s), dtype=torch.float64, device=dev)
+        acc_prob = torch.empty(p.shape[0], dtype=torch.float64, device=dev)
     drafts = torch.from_numpy(w["drafts"]).to(dev)
     u = torch.from_numpy(w["u"]).to(dev)
     B, V, K = p.shape[0], p.shape[1], cfg.K
     s_max = cfg.s_max
     r = torch.empty_like(p)
     status = torch.zeros(B, dtype=torch.int32, device=dev)
-    ws_bytes = mdss.workspace_bytes_pair(B, V) if cfg.pair else mdss.workspace_bytes(B, V, K, s_max)
+    if tlp_s:
+        ws_bytes = mdss.workspace_bytes_tlp(B, V, tail)
+    elif cfg.pair:
+        ws_bytes = mdss.workspace_bytes_pair(B, V)
+    else:
+        ws_bytes = mdss.workspace_bytes(B, V, K, s_max)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
 
     def induced():
-        if cfg.pair:
+        if tlp_s:
+            mdss.truncated_lp(p, q, q2, tlp_s, tail, r=r, omega1=omega1, w=wtab, accept=acc_prob,
+                              row_status=status, workspace=ws)
+        elif cfg.pair:
             mdss.induced_dist_pair(p, q, q2, r=r, row_status=status, workspace=ws)
         else:
             mdss.induced_dist(p, q, K, s_max=s_max, r=r, row_status=status, workspace=ws)
 
     def select():
+        if tlp_s:
+            return mdss.select_truncated_lp(p, q, q2, drafts, omega1, wtab, tail, u, row_status=status)
         if cfg.pair:
             return mdss.select_intermediate_pair(p, q, q2, drafts, u, row_status=status)
         return mdss.select_intermediate(p, q, drafts, u, row_status=status)
@@ -165,14 +215,25 @@ def main():
     assert int(status.abs().sum()) == 0, "rows flagged during the bench"
     accept_rate = float(acc.float().mean())
 
-    flops = pair_flops(w["q"], K, w.get("q2"))
-    achieved = flops / (r_ms * 1e-3) / 1e12
     digest = kernel_source_digest()
-    sweep_name = "sweep_k2_mfma_kernel" if K == 2 else "sweep_k3_kernel"
-    roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / FP32_PEAK_TFLOPS, 4), "traffic": counted_traffic(cfg.name, sweep_name, digest),
-                "kernel": f"{'mdss_induced_dist_pair' if cfg.pair else 'mdss_induced_dist'} ({sweep_name} + preparation)", "avg_ms": round(r_ms, 4),
-                "flops_per_launch": flops}
+    if tlp_s:
+        # HBM-bound: read p, q1 (and q2), write r once
+        nbytes = float(B) * V * (16 if cfg.pair else 12)
+        gbs = nbytes / (r_ms * 1e-3) / 1e9
+        rank_name = "tlp_rank_sorted_kernel" if tail == 0 else "tlp_rank_half_kernel"
+        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": counted_traffic(cfg.name, rank_name, digest),
+                    "kernel": f"mdss_truncated_lp ({rank_name} + tlp_lp_kernel)", "avg_ms": round(r_ms, 4),
+                    "bytes_per_launch": nbytes, "s": tlp_s, "tail": "sorted" if tail == 0 else "half"}
+    else:
+        flops = pair_flops(w["q"], K, w.get("q2"))
+        achieved = flops / (r_ms * 1e-3) / 1e12
+        sweep_name = "sweep_k2_mfma_kernel" if K == 2 else "sweep_k3_kernel"
+        roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / FP32_PEAK_TFLOPS, 4),
+                    "traffic": counted_traffic(cfg.name, sweep_name, digest),
+                    "kernel": f"{'mdss_induced_dist_pair' if cfg.pair else 'mdss_induced_dist'} ({sweep_name} + "
+                              "preparation)", "avg_ms": round(r_ms, 4), "flops_per_launch": flops}
 
     # accept / resample pass over every row with the residual written (12 B per token)
     _, sel_token = select()
@@ -229,6 +290,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.describe}", "B": B, "V": V, "K": K,
                    "s_max": s_max or None, "two_draft_distributions": cfg.pair,
+                   "selection": "truncated LP" if tlp_s else "classical importance weights",
                    "accept_rate": round(accept_rate, 4)},
         "roofline": roofline,
         "roofline_resample": roofline_resample,
@@ -237,7 +299,7 @@ def main():
     }
     if not args.no_cpu:
         ncores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-        rows = args.cpu_rows or 2 * ncores
+        rows = args.cpu_rows or (B if tlp_s else 2 * ncores)
         line["cpu_baseline"] = cpu_baseline(w, rows)
     print(json.dumps(line), flush=True)
 

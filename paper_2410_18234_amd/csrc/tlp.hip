@@ -11,10 +11,10 @@
 //
 // Per row:
 //   rank kernel (one workgroup of 1024 threads):
-//     SORTED tail: stable LSD radix sort of the rank words (4 passes of 8 bits,
-//       ping-pong in the workspace), then one reverse scan over the ranked
-//       order: r(k) = q1 q2 + q2(k) S1(k) + q1(k) S2(k) with S_i(k) the q_i
-//       mass ranked after k;
+//     SORTED tail: one stable scatter of the row into 256 bins by the top 8
+//       bits of the rank word, each group of bins then sorted in LDS, and one
+//       reverse scan over the ranked order: r(k) = q1 q2 + q2(k) S1(k) +
+//       q1(k) S2(k) with S_i(k) the q_i mass ranked after k;
 //     HALF tail: top-s selection only, then r(k) = q1 q2 + (q2 (A - q1) + q1
 //       (B - q2)) / 2 with A, B the Omega_2 masses.
 //   LP kernel (one wave): the Omega_1 program maximises sum_k min(p_k, c_k +
@@ -71,16 +71,72 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, uint64_t act) {
 
 __device__ __forceinline__ uint64_t lanes_below(int lane) { return (1ull << lane) - 1ull; }
 
-// One stable counting pass on bits [shift, shift + 8) of the rank words,
-// (kin, iin) -> (kout, iout).  Wave w owns the contiguous segment
-// [w seg, (w+1) seg) and walks it in order, 64 elements per step, so the pass
-// keeps the input order of equal digits.  cnt is [16][256] in LDS, tot [256].
-__device__ __forceinline__ void radix_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ iin,
-                           uint32_t* __restrict__ kout, uint32_t* __restrict__ iout, int n, int shift,
-                           uint32_t (*cnt)[256], uint32_t* tot) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// Contiguous segment [lo, hi) of n elements walked by this wave (64 elements
+// per step, segments in wave order), so per-wave counting keeps input order.
+__device__ __forceinline__ void wave_segment(int n, int* lo, int* hi) {
   const int seg = ((n + kRankWaves - 1) / kRankWaves + 63) & ~63;
-  const int lo = min(n, wave * seg), hi = min(n, lo + seg);
+  *lo = min(n, (int)(threadIdx.x >> 6) * seg);
+  *hi = min(n, *lo + seg);
+}
+
+// Per-wave digit counts cnt[w][d] -> output positions: cnt[w][d] = base +
+// (elements with a smaller digit) + (elements with digit d in waves < w).
+// bin_cnt / bin_start (nullable) receive the digit totals and their starts.
+// Returns true if one digit holds all n elements (the pass would not move any).
+__device__ __forceinline__ bool digit_offsets(uint32_t (*cnt)[256], uint32_t* tot, uint32_t base, int n,
+                                              uint32_t* bin_cnt, uint32_t* bin_start, int* flag) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (threadIdx.x == 0) *flag = 0;
+  __syncthreads();
+  if (threadIdx.x < 256) {
+    const int d = threadIdx.x;
+    uint32_t run = 0;
+    for (int w = 0; w < kRankWaves; ++w) {
+      const uint32_t c = cnt[w][d];
+      cnt[w][d] = run;
+      run += c;
+    }
+    tot[d] = run;
+    if (bin_cnt) bin_cnt[d] = run;
+    if (run == (uint32_t)n) *flag = 1;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    uint32_t v[4];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[j] = tot[lane * 4 + j];
+      sum += v[j];
+    }
+    const int incl = wave_inclusive_scan_int((int)sum, lane);
+    uint32_t run = base + (uint32_t)incl - sum;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      tot[lane * 4 + j] = run;
+      if (bin_start) bin_start[lane * 4 + j] = run;
+      run += v[j];
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < 256) {
+    const int d = threadIdx.x;
+    const uint32_t b0 = tot[d];
+    for (int w = 0; w < kRankWaves; ++w) cnt[w][d] += b0;
+  }
+  const bool uniform = *flag != 0;
+  __syncthreads();
+  return uniform;
+}
+
+// One stable counting pass on bits [shift, shift + 8) of the words,
+// (kin, iin) -> (kout, iout), over n elements (global memory or LDS).
+// Returns false, writing nothing, when every element has the same digit.
+__device__ __forceinline__ bool radix_pass(const uint32_t* kin, const uint32_t* iin, uint32_t* kout, uint32_t* iout,
+                                           int n, int shift, uint32_t (*cnt)[256], uint32_t* tot, int* flag) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int lo, hi;
+  wave_segment(n, &lo, &hi);
   for (int d = lane; d < 256; d += 64) cnt[wave][d] = 0u;
   constexpr int kBatch = 8;
   for (int base = lo; base < hi; base += 64 * kBatch) {
@@ -101,40 +157,7 @@ __device__ __forceinline__ void radix_pass(const uint32_t* __restrict__ kin, con
     }
   }
   __syncthreads();
-  if (threadIdx.x < 256) {
-    const int d = threadIdx.x;
-    uint32_t run = 0;
-    for (int w = 0; w < kRankWaves; ++w) {
-      const uint32_t c = cnt[w][d];
-      cnt[w][d] = run;
-      run += c;
-    }
-    tot[d] = run;
-  }
-  __syncthreads();
-  if (wave == 0) {
-    uint32_t v[4];
-    uint32_t s = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      v[j] = tot[lane * 4 + j];
-      s += v[j];
-    }
-    const int incl = wave_inclusive_scan_int((int)s, lane);
-    uint32_t run = (uint32_t)incl - s;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      tot[lane * 4 + j] = run;
-      run += v[j];
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x < 256) {
-    const int d = threadIdx.x;
-    const uint32_t b0 = tot[d];
-    for (int w = 0; w < kRankWaves; ++w) cnt[w][d] += b0;
-  }
-  __syncthreads();
+  if (digit_offsets(cnt, tot, 0u, n, nullptr, nullptr, flag)) return false;
   for (int base = lo; base < hi; base += 64 * kBatch) {
     uint32_t kr[kBatch], ir[kBatch];
 #pragma unroll
@@ -159,20 +182,7 @@ __device__ __forceinline__ void radix_pass(const uint32_t* __restrict__ kin, con
     }
   }
   __syncthreads();
-}
-
-// Row validity (every entry of p, q1, q2 finite and >= 0), block-wide.
-__device__ __forceinline__ int row_flags(const float* pb, const float* ab, const float* bb, int64_t V, int* red) {
-  int bad = 0;
-  for (int64_t i = threadIdx.x; i < V; i += kRankThreads)
-    bad |= (bad_prob(pb[i]) || bad_prob(ab[i]) || bad_prob(bb[i])) ? 1 : 0;
-  bad = __ballot(bad) != 0ull;
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = bad;
-  __syncthreads();
-  int any = 0;
-  for (int w = 0; w < kRankWaves; ++w) any |= red[w];
-  __syncthreads();
-  return any ? kRowBadProb : 0;
+  return true;
 }
 
 __device__ __forceinline__ void flag_row(int64_t b, int64_t V, int s, float* rb, int32_t* omega1, TlpHdr* hdr,
@@ -198,22 +208,30 @@ __device__ __forceinline__ double block_sum(double v, double* red) {
   return t;
 }
 
-// Exclusive prefix sums over the block in thread order, two values at once;
-// also returns the block totals.
-__device__ __forceinline__ void block_exclusive_scan2(double a, double b, double* ea, double* eb, double* ta, double* tb,
-                                      double* sa, double* sb) {
+// Exclusive suffix sums over the block in thread order (the sum over higher
+// threads), two values at once; also returns the block totals.
+__device__ __forceinline__ void block_exclusive_suffix2(double a, double b, double* ea, double* eb, double* ta,
+                                                        double* tb, double* sa, double* sb) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const double ia = wave_inclusive_scan(a, lane), ib = wave_inclusive_scan(b, lane);
-  double xa = __shfl_up(ia, 1, 64), xb = __shfl_up(ib, 1, 64);
-  if (lane == 0) xa = xb = 0.0;
-  if (lane == 63) {
+  double ia = a, ib = b;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double oa = __shfl_down(ia, off, 64), ob = __shfl_down(ib, off, 64);
+    if (lane + off < 64) {
+      ia += oa;
+      ib += ob;
+    }
+  }
+  double xa = __shfl_down(ia, 1, 64), xb = __shfl_down(ib, 1, 64);
+  if (lane == 63) xa = xb = 0.0;
+  if (lane == 0) {
     sa[wave] = ia;
     sb[wave] = ib;
   }
   __syncthreads();
   double oa = 0.0, ob = 0.0, fa = 0.0, fb = 0.0;
-  for (int w = 0; w < kRankWaves; ++w) {
-    if (w < wave) {
+  for (int w = kRankWaves - 1; w >= 0; --w) {
+    if (w > wave) {
       oa += sa[w];
       ob += sb[w];
     }
@@ -228,65 +246,231 @@ __device__ __forceinline__ void block_exclusive_scan2(double a, double b, double
 }
 
 // ---------------------------------------------------------------- SORTED tail
+// Bin-ordered copy of a row made by the scatter pass (structure of arrays).
+struct BinRow {
+  uint32_t* word;
+  uint32_t* id;
+  float* p;
+  float* a;
+  float* b;
+};
+
+constexpr int kGroup = 8192;  // entries sorted in LDS at once
+
+// Reverse scan of one ranked chunk: sorted[g] (g < G <= kGroup) = index into
+// the bin order of the entry with rank first_rank + g.  Entries ranked in
+// Omega_1 are recorded and take no part in the sums; every other entry k gets
+// r(k) = a b + b S_a + a S_b with S the q1 / q2 mass ranked after k.
+// The entries are first gathered (thread-strided, many loads in flight) into
+// the LDS staging arrays A, Bq, P, ID (kGroup entries each; `sorted` may
+// alias one of them), then scanned from LDS, E consecutive ranks per thread.
+constexpr int kStride = kGroup / kRankThreads;
+__device__ __forceinline__ void scan_chunk(const uint32_t* sorted, int G, uint32_t first_rank, uint32_t bin_base,
+                                           const BinRow& br, int s, int64_t b, float* rb, int32_t* omega1,
+                                           double* ca, double* cb, double* acc, double* sa, double* sb, float* A,
+                                           float* Bq, float* P, uint32_t* ID) {
+  uint32_t at[kStride];
+#pragma unroll
+  for (int k = 0; k < kStride; ++k) {
+    const int g = (int)threadIdx.x + k * kRankThreads;
+    at[k] = g < G ? bin_base + sorted[g] : 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kStride; ++k) {
+    const int g = (int)threadIdx.x + k * kRankThreads;
+    if (g < G) {
+      A[g] = br.a[at[k]];
+      Bq[g] = br.b[at[k]];
+      P[g] = br.p[at[k]];
+      ID[g] = br.id[at[k]];
+    }
+  }
+  __syncthreads();
+  const int E = (G + kRankThreads - 1) / kRankThreads;
+  const int g0 = min(G, (int)threadIdx.x * E), g1 = min(G, g0 + E);
+  double la = 0.0, lb = 0.0;  // this thread's Omega_2 mass (consecutive ranks)
+  for (int g = g0; g < g1; ++g) {
+    if (first_rank + (uint32_t)g < (uint32_t)s) continue;
+    la += (double)A[g];
+    lb += (double)Bq[g];
+  }
+  double ea, eb, ta, tb;
+  block_exclusive_suffix2(la, lb, &ea, &eb, &ta, &tb, sa, sb);
+  double s1 = *ca + ea, s2 = *cb + eb;  // mass ranked after the entry being visited
+  for (int g = g1 - 1; g >= g0; --g) {
+    const uint32_t rank = first_rank + (uint32_t)g;
+    const int id = (int)ID[g];
+    if (rank < (uint32_t)s) {
+      omega1[b * s + rank] = id;
+      continue;
+    }
+    const double av = (double)A[g], bv = (double)Bq[g];
+    const double rv = av * bv + bv * s1 + av * s2;
+    rb[id] = (float)rv;
+    *acc += fmin((double)P[g], rv);
+    s1 += av;
+    s2 += bv;
+  }
+  *ca += ta;
+  *cb += tb;
+  __syncthreads();  // the staging arrays are reused by the next chunk
+}
+
+// One workgroup per row.  Pass 1 counts the top 8 bits of the rank words per
+// wave (stable) and checks the row; pass 2 scatters (word, id, p, q1, q2) into
+// bin order; then bins are taken from the last-ranked down, consecutive bins
+// grouped up to kGroup entries, each group sorted in LDS (stable LSD passes) and
+// scanned.  A single bin above kGroup entries is sorted by global LSD passes on
+// its lower 24 bits and scanned in chunks.
 __global__ __launch_bounds__(kRankThreads) void tlp_rank_sorted_kernel(
     const float* __restrict__ p, const float* __restrict__ q1, const float* __restrict__ q2, int64_t V, int s,
-    float* __restrict__ r, int32_t* __restrict__ omega1, TlpHdr* __restrict__ hdr, uint32_t* __restrict__ kA,
-    uint32_t* __restrict__ iA, uint32_t* __restrict__ kB, uint32_t* __restrict__ iB,
+    float* __restrict__ r, int32_t* __restrict__ omega1, TlpHdr* __restrict__ hdr, BinRow bins,
+    uint32_t* __restrict__ kA, uint32_t* __restrict__ iA, uint32_t* __restrict__ kB, uint32_t* __restrict__ iB,
     int32_t* __restrict__ row_status) {
   __shared__ uint32_t cnt[kRankWaves][256];
-  __shared__ uint32_t tot[256];
+  __shared__ uint32_t tot[256], bin_cnt[256], bin_start[256];
+  __shared__ uint32_t kx[2][kGroup], ix[2][kGroup];
   __shared__ double sa[kRankWaves], sb[kRankWaves];
   __shared__ int red[kRankWaves];
+  __shared__ int flag;
   const int64_t b = blockIdx.x;
   const float* pb = p + b * V;
   const float* ab = q1 + b * V;
   const float* bb = q2 + b * V;
   float* rb = r + b * V;
   const int n = (int)V;
-  const int flags = row_flags(pb, ab, bb, V, red);
-  if (flags) {
-    flag_row(b, V, s, rb, omega1, hdr, row_status, flags);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const BinRow br = {bins.word + b * V, bins.id + b * V, bins.p + b * V, bins.a + b * V, bins.b + b * V};
+  int lo, hi;
+  wave_segment(n, &lo, &hi);
+  constexpr int kBatch = 4;
+  // pass 1: validity and per-wave counts of the top digit
+  for (int d = lane; d < 256; d += 64) cnt[wave][d] = 0u;
+  int bad = 0;
+  for (int base = lo; base < hi; base += 64 * kBatch) {
+    float pr[kBatch], ar[kBatch], brr[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int i = base + j * 64 + lane;
+      pr[j] = i < hi ? pb[i] : 0.0f;
+      ar[j] = i < hi ? ab[i] : 0.0f;
+      brr[j] = i < hi ? bb[i] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int i = base + j * 64 + lane;
+      const uint64_t act = __ballot(i < hi);
+      if (!act) break;
+      bad |= (bad_prob(pr[j]) || bad_prob(ar[j]) || bad_prob(brr[j])) ? 1 : 0;
+      const uint32_t d = rank_word(pr[j], ar[j], brr[j]) >> 24;
+      const uint64_t m = match_digit(d, act);
+      if (i < hi && lane == __ffsll((long long)m) - 1) cnt[wave][d] += (uint32_t)__popcll(m);
+    }
+  }
+  bad = __ballot(bad) != 0ull;
+  if (lane == 0) red[wave] = bad;
+  __syncthreads();
+  int any = 0;
+  for (int w = 0; w < kRankWaves; ++w) any |= red[w];
+  if (any) {
+    flag_row(b, V, s, rb, omega1, hdr, row_status, kRowBadProb);
     return;
   }
-  uint32_t* ka = kA + b * V;
-  uint32_t* ia = iA + b * V;
-  uint32_t* kb = kB + b * V;
-  uint32_t* ib = iB + b * V;
-  for (int i = threadIdx.x; i < n; i += kRankThreads) {
-    ka[i] = rank_word(pb[i], ab[i], bb[i]);
-    ia[i] = (uint32_t)i;
+  digit_offsets(cnt, tot, 0u, n, bin_cnt, bin_start, &flag);
+  // pass 2: stable scatter into bin order, with the values the scan needs
+  for (int base = lo; base < hi; base += 64 * kBatch) {
+    float pr[kBatch], ar[kBatch], brr[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int i = base + j * 64 + lane;
+      pr[j] = i < hi ? pb[i] : 0.0f;
+      ar[j] = i < hi ? ab[i] : 0.0f;
+      brr[j] = i < hi ? bb[i] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int i = base + j * 64 + lane;
+      const uint64_t act = __ballot(i < hi);
+      if (!act) break;
+      const uint32_t wd = rank_word(pr[j], ar[j], brr[j]);
+      const uint32_t d = wd >> 24;
+      const uint64_t m = match_digit(d, act);
+      if (i < hi) {
+        const uint32_t pos = cnt[wave][d] + (uint32_t)__popcll(m & lanes_below(lane));
+        br.word[pos] = wd;
+        br.id[pos] = (uint32_t)i;
+        br.p[pos] = pr[j];
+        br.a[pos] = ar[j];
+        br.b[pos] = brr[j];
+        if (lane == __ffsll((long long)m) - 1) cnt[wave][d] += (uint32_t)__popcll(m);
+      }
+    }
   }
   __syncthreads();
-  radix_pass(ka, ia, kb, ib, n, 0, cnt, tot);
-  radix_pass(kb, ib, ka, ia, n, 8, cnt, tot);
-  radix_pass(ka, ia, kb, ib, n, 16, cnt, tot);
-  radix_pass(kb, ib, ka, ia, n, 24, cnt, tot);
-  const int se = min(s, n);
-  if (threadIdx.x < s) omega1[b * s + threadIdx.x] = threadIdx.x < se ? (int32_t)ia[threadIdx.x] : -1;
-  // reverse scan over ranked positions [se, n): thread 0 takes the last position of each tile
+  // pass 3: groups of bins, last-ranked first
   double ca = 0.0, cb = 0.0, acc = 0.0;
-  for (int top = n; top > se; top -= kRankThreads) {
-    const int pos = top - 1 - (int)threadIdx.x;
-    const bool valid = pos >= se;
-    double av = 0.0, bv = 0.0, pv = 0.0;
-    int id = 0;
-    if (valid) {
-      id = (int)ia[pos];
-      av = (double)ab[id];
-      bv = (double)bb[id];
-      pv = (double)pb[id];
+  int dh = 255;
+  while (dh >= 0) {
+    int dl = dh;
+    uint32_t G = bin_cnt[dh];
+    while (dl > 0 && G + bin_cnt[dl - 1] <= (uint32_t)kGroup) G += bin_cnt[--dl];
+    const uint32_t g_lo = bin_start[dl];
+    if (G == 0) {
+      dh = dl - 1;
+      continue;
     }
-    double ea, eb, ta, tb;
-    block_exclusive_scan2(av, bv, &ea, &eb, &ta, &tb, sa, sb);
-    if (valid) {
-      const double s1 = ca + ea, s2 = cb + eb;
-      const double rv = av * bv + bv * s1 + av * s2;
-      rb[id] = (float)rv;
-      acc += fmin(pv, rv);
+    if (G <= (uint32_t)kGroup) {
+      for (uint32_t g = threadIdx.x; g < G; g += kRankThreads) {
+        kx[0][g] = br.word[g_lo + g];
+        ix[0][g] = g;
+      }
+      __syncthreads();
+      int nonempty = 0;
+      for (int d = dl; d <= dh; ++d) nonempty += bin_cnt[d] > 0u;
+      const int top = nonempty > 1 ? 32 : 24;  // one bin: the top digit is shared
+      int cur = 0;
+      for (int shift = 0; shift < top; shift += 8)
+        if (radix_pass(kx[cur], ix[cur], kx[cur ^ 1], ix[cur ^ 1], (int)G, shift, cnt, tot, &flag)) cur ^= 1;
+      scan_chunk(ix[cur], (int)G, g_lo, g_lo, br, s, b, rb, omega1, &ca, &cb, &acc, sa, sb,
+                 reinterpret_cast<float*>(kx[0]), reinterpret_cast<float*>(kx[1]), reinterpret_cast<float*>(ix[0]),
+                 ix[1]);
+    } else {
+      // one bin above the LDS capacity: its words share the top digit
+      uint32_t* ka = kA + b * V;
+      uint32_t* ia = iA + b * V;
+      uint32_t* kb = kB + b * V;
+      uint32_t* ib = iB + b * V;
+      for (uint32_t g = threadIdx.x; g < G; g += kRankThreads) {
+        ka[g] = br.word[g_lo + g];
+        ia[g] = g;
+      }
+      __syncthreads();
+      uint32_t *k_in = ka, *i_in = ia, *k_out = kb, *i_out = ib;
+      for (int shift = 0; shift < 24; shift += 8) {
+        if (radix_pass(k_in, i_in, k_out, i_out, (int)G, shift, cnt, tot, &flag)) {
+          uint32_t* t = k_in;
+          k_in = k_out;
+          k_out = t;
+          t = i_in;
+          i_in = i_out;
+          i_out = t;
+        }
+      }
+      const uint32_t* sorted = i_in;
+      const int chunks = (int)((G + kGroup - 1) / kGroup);
+      for (int c = chunks - 1; c >= 0; --c) {
+        const uint32_t c0 = (uint32_t)c * kGroup;
+        const int Gc = (int)min((uint32_t)kGroup, G - c0);
+        scan_chunk(sorted + c0, Gc, g_lo + c0, g_lo, br, s, b, rb, omega1, &ca, &cb, &acc, sa, sb,
+                   reinterpret_cast<float*>(kx[0]), reinterpret_cast<float*>(kx[1]),
+                   reinterpret_cast<float*>(ix[0]), ix[1]);
+      }
     }
-    ca += ta;
-    cb += tb;
+    dh = dl - 1;
   }
+  const int se = min(s, n);
+  if (threadIdx.x >= se && threadIdx.x < s) omega1[b * s + threadIdx.x] = -1;
   acc = block_sum(acc, sa);
   if (threadIdx.x == 0) {
     TlpHdr h = {};
@@ -344,18 +528,16 @@ __global__ __launch_bounds__(kRankThreads) void tlp_rank_half_kernel(
   float* rb = r + b * V;
   const int n = (int)V;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int flags = row_flags(pb, ab, bb, V, red);
-  if (flags) {
-    flag_row(b, V, s, rb, omega1, hdr, row_status, flags);
-    return;
-  }
   const int se = min(s, n);
-  // per-thread s smallest composites (sorted), then per wave, then per block
+  // pass 1: validity and the s smallest composites per thread (sorted), then per wave, then per block
   uint64_t l[kMaxS];
 #pragma unroll
   for (int j = 0; j < kMaxS; ++j) l[j] = ~0ull;
+  int bad = 0;
   for (int i = threadIdx.x; i < n; i += kRankThreads) {
-    const uint64_t c = composite(pb[i], ab[i], bb[i], i);
+    const float pv = pb[i], av = ab[i], bv = bb[i];
+    bad |= (bad_prob(pv) || bad_prob(av) || bad_prob(bv)) ? 1 : 0;
+    const uint64_t c = composite(pv, av, bv, i);
     if (c < l[kMaxS - 1]) {
 #pragma unroll
       for (int j = kMaxS - 1; j > 0; --j) {
@@ -364,6 +546,15 @@ __global__ __launch_bounds__(kRankThreads) void tlp_rank_half_kernel(
       }
       l[0] = l[0] < c ? l[0] : c;
     }
+  }
+  bad = __ballot(bad) != 0ull;
+  if (lane == 0) red[wave] = bad;
+  __syncthreads();
+  int any = 0;
+  for (int w = 0; w < kRankWaves; ++w) any |= red[w];
+  if (any) {
+    flag_row(b, V, s, rb, omega1, hdr, row_status, kRowBadProb);
+    return;
   }
   uint64_t got[kMaxS];
   wave_merge_smallest(l, se, got);
@@ -383,22 +574,33 @@ __global__ __launch_bounds__(kRankThreads) void tlp_rank_half_kernel(
   }
   __syncthreads();
   if (threadIdx.x < s) omega1[b * s + threadIdx.x] = threadIdx.x < se ? (int32_t)(uint32_t)best[threadIdx.x] : -1;
-  const uint64_t last = best[se - 1];  // a token is in Omega_1 iff its composite <= last
+  int om[kMaxS];  // Omega_1 ids (-1 past s_eff)
+#pragma unroll
+  for (int t = 0; t < kMaxS; ++t) om[t] = t < se ? (int)(uint32_t)best[t] : -1;
+  auto in_omega1 = [&](int i) {
+    bool hit = false;
+#pragma unroll
+    for (int t = 0; t < kMaxS; ++t) hit |= om[t] == i;
+    return hit;
+  };
+  // pass 2: Omega_2 masses
   double A = 0.0, Bm = 0.0;
   for (int i = threadIdx.x; i < n; i += kRankThreads) {
-    if (composite(pb[i], ab[i], bb[i], i) <= last) continue;
-    A += (double)ab[i];
-    Bm += (double)bb[i];
+    const float av = ab[i], bv = bb[i];
+    if (in_omega1(i)) continue;
+    A += (double)av;
+    Bm += (double)bv;
   }
   A = block_sum(A, sa);
   Bm = block_sum(Bm, sa);
+  // pass 3: r(k) = q1 q2 + (q2 (A - q1) + q1 (B - q2)) / 2 = (q2 A + q1 B) / 2 on Omega_2
   double acc = 0.0;
   for (int i = threadIdx.x; i < n; i += kRankThreads) {
-    if (composite(pb[i], ab[i], bb[i], i) <= last) continue;
-    const double av = (double)ab[i], bv = (double)bb[i];
-    const double rv = av * bv + 0.5 * (bv * (A - av) + av * (Bm - bv));
+    const float av = ab[i], bv = bb[i], pv = pb[i];
+    if (in_omega1(i)) continue;
+    const double rv = 0.5 * ((double)bv * A + (double)av * Bm);
     rb[i] = (float)rv;
-    acc += fmin((double)pb[i], rv);
+    acc += fmin((double)pv, rv);
   }
   acc = block_sum(acc, sa);
   if (threadIdx.x == 0) {
@@ -607,9 +809,11 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
+// SORTED tail: 5 planes of the bin-ordered row copy + 4 planes for a bin
+// above the LDS capacity, each [B][V] 32-bit words.
 size_t workspace_bytes_tlp(int64_t B, int64_t V, int tail) {
   size_t bytes = align256((size_t)B * sizeof(TlpHdr));
-  if (tail == kTailSorted) bytes += 4 * align256((size_t)B * (size_t)V * sizeof(uint32_t));
+  if (tail == kTailSorted) bytes += 9 * align256((size_t)B * (size_t)V * sizeof(uint32_t));
   return bytes;
 }
 
@@ -622,12 +826,18 @@ hipError_t launch_tlp(const float* p, const float* q1, const float* q2, int64_t 
   base += align256((size_t)B * sizeof(TlpHdr));
   if (tail == kTailSorted) {
     const size_t plane = align256((size_t)B * (size_t)V * sizeof(uint32_t));
-    uint32_t* kA = reinterpret_cast<uint32_t*>(base);
-    uint32_t* iA = reinterpret_cast<uint32_t*>(base + plane);
-    uint32_t* kB = reinterpret_cast<uint32_t*>(base + 2 * plane);
-    uint32_t* iB = reinterpret_cast<uint32_t*>(base + 3 * plane);
+    BinRow bins;
+    bins.word = reinterpret_cast<uint32_t*>(base);
+    bins.id = reinterpret_cast<uint32_t*>(base + plane);
+    bins.p = reinterpret_cast<float*>(base + 2 * plane);
+    bins.a = reinterpret_cast<float*>(base + 3 * plane);
+    bins.b = reinterpret_cast<float*>(base + 4 * plane);
+    uint32_t* kA = reinterpret_cast<uint32_t*>(base + 5 * plane);
+    uint32_t* iA = reinterpret_cast<uint32_t*>(base + 6 * plane);
+    uint32_t* kB = reinterpret_cast<uint32_t*>(base + 7 * plane);
+    uint32_t* iB = reinterpret_cast<uint32_t*>(base + 8 * plane);
     hipLaunchKernelGGL(tlp_rank_sorted_kernel, dim3((unsigned)B), dim3(kRankThreads), 0, st, p, q1, q2, V, s, r,
-                       omega1, hdr, kA, iA, kB, iB, row_status);
+                       omega1, hdr, bins, kA, iA, kB, iB, row_status);
   } else {
     hipLaunchKernelGGL(tlp_rank_half_kernel, dim3((unsigned)B), dim3(kRankThreads), 0, st, p, q1, q2, V, s, r,
                        omega1, hdr, row_status);

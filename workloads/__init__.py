@@ -54,6 +54,8 @@ class Config:
     row: Callable[["Config", int], "tuple[np.ndarray, np.ndarray]"]
     s_max: int = 0  # support cap the K=3 path is run with (0: not used)
     pair: bool = False  # two drafts from different distributions q (first) and q2 (second)
+    tlp_s: int = 0      # truncated linear program with |Omega_1| = tlp_s (0: classical importance weights)
+    tlp_tail: int = 0   # truncated LP: 0 = sorted Omega_2 (Algorithm 2), 1 = halves (sort-free variant)
 
 
 def _row_dirichlet(cfg: Config, b: int):
@@ -127,6 +129,12 @@ CONFIGS: Dict[str, Config] = {
                "V=32000, two drafts from different distributions, 256 positions, logits N(0,3^2), "
                "draft i = softmax((logits + N(0,1)) / T_i) with T_1 = 1.2, T_2 = 2.0, target T = 1",
                _row_two_temps(3.0, 1.2, 2.0), pair=True),
+        Config("tlp_pair32k", 1006, 256, 32000, 2,
+               "truncated LP (Algorithm 2), s = 5, sorted Omega_2, on the pair32k rows: V=32000, drafts at "
+               "T_1 = 1.2 and T_2 = 2.0, 256 positions", _row_two_temps(3.0, 1.2, 2.0), pair=True, tlp_s=5),
+        Config("tlp_llm32k", 1002, 256, 32000, 2,
+               "truncated LP (Algorithm 2), s = 5, sorted Omega_2, identical drafts, on the llm32k rows",
+               _row_gauss(3.0, 1.0, 1.0), tlp_s=5),
     ]
 }
 
