@@ -12,6 +12,8 @@ Contents:
   * ``analytic.py``    -- numpy/scipy: output distribution of Algorithm 1,
     acceptance probabilities, the optimal acceptance P* by linear programming
     (Problem 1) and by the explicit expression of Theorem 3.
+  * ``successive.py``  -- the successive pairwise reduction of K > 2 drafts
+    (Remark 4) on top of the two enumerations above.
   * ``tlp.py``         -- numpy/scipy: the truncated linear program (Algorithm 2,
     its sort-free variant and the two-distribution version), its LP solved by
     HiGHS in the paper's own variables.
