@@ -52,8 +52,9 @@ typedef enum mdss_status {
   MDSS_OK = 0,
   MDSS_EINVAL = 1,       /* null pointer or invalid argument value */
   MDSS_ESHAPE = 2,       /* B outside [1, MDSS_MAX_B] or V outside [2, MDSS_MAX_V] */
-  MDSS_EUNSUPPORTED = 3, /* K outside {2, 3}, K = 3 with s_max outside [1, MDSS_K3_MAX_SUPPORT],
-                            or a truncated-LP s outside [1, MDSS_TLP_MAX_S] */
+  MDSS_EUNSUPPORTED = 3, /* K outside {2, 3} (outside [2, MDSS_SUCCESSIVE_MAX_K] for the successive
+                            calls), K = 3 with s_max outside [1, MDSS_K3_MAX_SUPPORT], or a
+                            truncated-LP s outside [1, MDSS_TLP_MAX_S] */
   MDSS_EDEVICE = 4,      /* a HIP call or kernel launch failed */
   MDSS_EWORKSPACE = 5    /* workspace missing or smaller than mdss_workspace_bytes() */
 } mdss_status;
@@ -147,6 +148,43 @@ mdss_status mdss_select_intermediate_pair(const float* p, const float* q1, const
                                           const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
                                           int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
                                           void* stream);
+
+/* ---- Successive pairwise selection (K >= 2) -------------------------------
+ * Remark 4: K drafts X1..XK i.i.d. from q are reduced two at a time.  Stage 1
+ * selects between X1 and X2 as mdss_select_intermediate does for K = 2 and
+ * keeps Y1, whose law is r_1 = the K = 2 induced distribution; stage j >= 2
+ * selects between Y_{j-1} (law r_{j-1}) and X_{j+1} (law q) as two drafts of
+ * different distributions (mdss_induced_dist_pair with q1 = r_{j-1}, q2 = q),
+ * and keeps Y_j with law r_j.  r_{K-1} is the proposal of Algorithm 1.  Each
+ * stage's law is used in its fp32 storage by the next stage.  Cost: K - 1
+ * pair sums of O(n^2) per row, against O(n^K) for the direct K-draft rule. */
+#define MDSS_SUCCESSIVE_MAX_K 8
+
+/* Workspace bytes of mdss_induced_dist_successive (0 if the shape is invalid). */
+size_t mdss_workspace_bytes_successive(int64_t B, int64_t V);
+
+/* r_stages: [K-1][B][V] fp32 out, stage j (1-based) at offset (j-1) B V; the
+ * last stage is the proposal.  K in [2, MDSS_SUCCESSIVE_MAX_K].  Row flags as
+ * mdss_induced_dist (a flagged row is NaN in every later stage).  workspace: at
+ * least mdss_workspace_bytes_successive(B, V) bytes, 256-byte aligned. */
+mdss_status mdss_induced_dist_successive(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
+                                         float* r_stages, int32_t* row_status, void* workspace,
+                                         size_t workspace_bytes, void* stream);
+
+/* Chained selection over drafts [B][K]: stage 1 keeps X1 iff u_1 (w1 + w2) < w1
+ * with w_i = p(X_i)/q(X_i); stage j >= 2 keeps Y iff u_j (wY + wX) < wY with
+ * wY = p(Y)/r_{j-1}(Y), wX = p(X_{j+1})/q(X_{j+1}); both weights zero: keep iff
+ * floor(2 u_j) = 0 (fp64 throughout).  u_sel: [B][K-1] fp32 (u_j = u_sel[b][j-1])
+ * or NULL: u_j from word 0 of Philox4x32-10 with key = seed and counter =
+ * (offset + b (low, high word), j, 0), a stream apart from the one the other
+ * calls use (third counter word 0).  sel_index = the draft index finally kept,
+ * sel_token its id; -1 for a row with an invalid draft (out of range, q = 0, or
+ * a kept token whose stage law is 0 or NaN: MDSS_ROW_BAD_DRAFT) or a NaN /
+ * negative p or q at a draft (MDSS_ROW_BAD_PROB).  r_stages may be NULL for K = 2. */
+mdss_status mdss_select_successive(const float* p, const float* q, const float* r_stages, const int32_t* drafts,
+                                   const float* u_sel, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+                                   int32_t K, int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
+                                   void* stream);
 
 /* ---- Truncated linear program (K = 2) -------------------------------------
  * The paper's practical selection rule (Algorithm 2, eq. heur, eq. p_Ieq and

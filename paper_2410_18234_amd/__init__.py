@@ -16,6 +16,7 @@ from .binding import (  # noqa: F401
     MDSS_ROW_FORCED,
     MDSS_ROW_LP_LIMIT,
     MDSS_ROW_SUPPORT,
+    MDSS_SUCCESSIVE_MAX_K,
     MDSS_TLP_HALF,
     MDSS_TLP_MAX_S,
     MDSS_TLP_SORTED,
@@ -23,16 +24,20 @@ from .binding import (  # noqa: F401
     accept_or_resample,
     induced_dist,
     induced_dist_pair,
+    induced_dist_successive,
     library_path,
     load_library,
     select_intermediate,
     select_intermediate_pair,
+    select_successive,
     select_truncated_lp,
     step,
     step_pair,
+    step_successive,
     step_truncated_lp,
     truncated_lp,
     workspace_bytes,
     workspace_bytes_pair,
+    workspace_bytes_successive,
     workspace_bytes_tlp,
 )

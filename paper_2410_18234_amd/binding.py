@@ -25,6 +25,7 @@ MDSS_ROW_LP_LIMIT = 16
 MDSS_TLP_MAX_S = 16
 MDSS_TLP_SORTED = 0
 MDSS_TLP_HALF = 1
+MDSS_SUCCESSIVE_MAX_K = 8
 
 _STATUS = {0: "MDSS_OK", 1: "MDSS_EINVAL", 2: "MDSS_ESHAPE", 3: "MDSS_EUNSUPPORTED", 4: "MDSS_EDEVICE",
            5: "MDSS_EWORKSPACE"}
@@ -67,6 +68,12 @@ def load_library():
         lib.mdss_workspace_bytes_tlp.restype = sz
         lib.mdss_truncated_lp.argtypes = [P, P, P, i64, i64, i32, i32, P, P, P, P, P, P, sz, P]
         lib.mdss_select_truncated_lp.argtypes = [P, P, P, P, P, u64, u64, i64, i64, i32, i32, P, P, P, P, P, P]
+        lib.mdss_workspace_bytes_successive.argtypes = [i64, i64]
+        lib.mdss_workspace_bytes_successive.restype = sz
+        lib.mdss_induced_dist_successive.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P]
+        lib.mdss_select_successive.argtypes = [P, P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P]
+        for f in ("mdss_induced_dist_successive", "mdss_select_successive"):
+            getattr(lib, f).restype = ctypes.c_int
         for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample",
                   "mdss_induced_dist_pair", "mdss_select_intermediate_pair", "mdss_truncated_lp",
                   "mdss_select_truncated_lp"):
@@ -356,3 +363,69 @@ def step_truncated_lp(p: torch.Tensor, q1: torch.Tensor, q2: Optional[torch.Tens
     return {"r": r, "omega1": omega1, "w": w, "accept_prob": accept, "sel_index": sel_index,
             "sel_token": sel_token, "out_token": out, "accepted": acc, "residual": res, "mass": mass,
             "status": status}
+
+
+def workspace_bytes_successive(B: int, V: int) -> int:
+    return int(load_library().mdss_workspace_bytes_successive(B, V))
+
+
+def induced_dist_successive(p: torch.Tensor, q: torch.Tensor, K: int, r_stages: Optional[torch.Tensor] = None,
+                            row_status: Optional[torch.Tensor] = None,
+                            workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """r_stages [K-1][B][V] fp32: the laws of the kept token after each pairwise stage (Remark 4)."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if r_stages is None:
+        r_stages = torch.empty((K - 1, B, V), dtype=torch.float32, device=dev)
+    _need(r_stages, "r_stages", torch.float32, (K - 1, B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    need = int(lib.mdss_workspace_bytes_successive(B, V))
+    if need == 0:
+        _check("mdss_workspace_bytes_successive", 2)
+    if workspace is None:
+        workspace = _workspace(dev, need)
+    elif workspace.dtype != torch.uint8 or workspace.device != dev or workspace.numel() < need:
+        raise ValueError(f"workspace must be a uint8 tensor on {dev} of at least {need} bytes")
+    _check("mdss_induced_dist_successive",
+           lib.mdss_induced_dist_successive(_ptr(p), _ptr(q), B, V, K, _ptr(r_stages), _ptr(row_status),
+                                            _ptr(workspace), workspace.numel(), _stream(dev)))
+    return r_stages
+
+
+def select_successive(p: torch.Tensor, q: torch.Tensor, r_stages: Optional[torch.Tensor], drafts: torch.Tensor,
+                      u_sel: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0,
+                      row_status: Optional[torch.Tensor] = None):
+    """(sel_index, sel_token) of the chained pairwise selection over drafts [B][K]."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if drafts.dim() != 2:
+        raise ValueError("drafts must be [B][K]")
+    K = drafts.shape[1]
+    _need(drafts, "drafts", torch.int32, (B, K), dev)
+    if r_stages is not None:
+        _need(r_stages, "r_stages", torch.float32, (K - 1, B, V), dev)
+    if u_sel is not None:
+        _need(u_sel, "u_sel", torch.float32, (B, K - 1), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    sel_index = torch.empty(B, dtype=torch.int32, device=dev)
+    sel_token = torch.empty(B, dtype=torch.int32, device=dev)
+    _check("mdss_select_successive",
+           lib.mdss_select_successive(_ptr(p), _ptr(q), _ptr(r_stages), _ptr(drafts), _ptr(u_sel),
+                                      ctypes.c_uint64(seed), ctypes.c_uint64(offset), B, V, K, _ptr(sel_index),
+                                      _ptr(sel_token), _ptr(row_status), _stream(dev)))
+    return sel_index, sel_token
+
+
+def step_successive(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u_sel: Optional[torch.Tensor] = None,
+                    u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False):
+    """The whole path with successive pairwise selection: stage laws, chained selection, Algorithm 1."""
+    B, K = drafts.shape
+    status = torch.zeros(B, dtype=torch.int32, device=p.device)
+    rs = induced_dist_successive(p, q, K, row_status=status)
+    sel_index, sel_token = select_successive(p, q, rs, drafts, u_sel, seed, offset, row_status=status)
+    out, acc, res, mass = accept_or_resample(p, rs[K - 2], sel_token, u, seed, offset, want_residual=want_residual,
+                                             want_mass=want_residual, row_status=status)
+    return {"r_stages": rs, "r": rs[K - 2], "sel_index": sel_index, "sel_token": sel_token, "out_token": out,
+            "accepted": acc, "residual": res, "mass": mass, "status": status}

@@ -33,7 +33,7 @@ const char* mdss_status_string(mdss_status s) {
     case MDSS_OK: return "ok";
     case MDSS_EINVAL: return "invalid argument (null pointer or bad value)";
     case MDSS_ESHAPE: return "invalid shape (B outside [1, MDSS_MAX_B] or V outside [2, MDSS_MAX_V])";
-    case MDSS_EUNSUPPORTED: return "unsupported configuration (K not 2 or 3, K = 3 with s_max out of range, or s outside [1, MDSS_TLP_MAX_S])";
+    case MDSS_EUNSUPPORTED: return "unsupported configuration (K out of range, K = 3 with s_max out of range, or s outside [1, MDSS_TLP_MAX_S])";
     case MDSS_EDEVICE: return "HIP error while launching";
     case MDSS_EWORKSPACE: return "workspace missing or too small";
   }
@@ -87,6 +87,38 @@ mdss_status mdss_select_intermediate_pair(const float* p, const float* q1, const
   if (s != MDSS_OK) return s;
   return from_hip(mdss::launch_select_pair(p, q1, q2, drafts, u, seed, offset, B, V, sel_index, sel_token,
                                            row_status, static_cast<hipStream_t>(stream)));
+}
+
+size_t mdss_workspace_bytes_successive(int64_t B, int64_t V) {
+  if (check_shape(B, V) != MDSS_OK) return 0;
+  return mdss::workspace_bytes_pair(B, V);
+}
+
+mdss_status mdss_induced_dist_successive(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
+                                         float* r_stages, int32_t* row_status, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
+  if (!p || !q || !r_stages) return MDSS_EINVAL;
+  const mdss_status st = check_shape(B, V);
+  if (st != MDSS_OK) return st;
+  if (K < 2 || K > MDSS_SUCCESSIVE_MAX_K) return MDSS_EUNSUPPORTED;
+  const size_t need = mdss::workspace_bytes_pair(B, V);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) % 256) != 0)
+    return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_induced_successive(p, q, B, V, K, r_stages, row_status, workspace,
+                                                  static_cast<hipStream_t>(stream)));
+}
+
+mdss_status mdss_select_successive(const float* p, const float* q, const float* r_stages, const int32_t* drafts,
+                                   const float* u_sel, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+                                   int32_t K, int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
+                                   void* stream) {
+  if (!p || !q || !drafts || !sel_index || !sel_token) return MDSS_EINVAL;
+  const mdss_status st = check_shape(B, V);
+  if (st != MDSS_OK) return st;
+  if (K < 2 || K > MDSS_SUCCESSIVE_MAX_K) return MDSS_EUNSUPPORTED;
+  if (K > 2 && !r_stages) return MDSS_EINVAL;
+  return from_hip(mdss::launch_select_successive(p, q, r_stages, drafts, u_sel, seed, offset, B, V, K, sel_index,
+                                                 sel_token, row_status, static_cast<hipStream_t>(stream)));
 }
 
 size_t mdss_workspace_bytes_tlp(int64_t B, int64_t V, int32_t tail) {

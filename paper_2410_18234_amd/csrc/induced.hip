@@ -1223,4 +1223,18 @@ hipError_t launch_induced_pair(const float* p, const float* q1, const float* q2,
   return hipGetLastError();
 }
 
+// Successive pairwise reduction (Remark 4): r_1 = the K = 2 law of (q, q),
+// r_j = the law of a pair drawn from (r_{j-1}, q), each stage read back in fp32.
+hipError_t launch_induced_successive(const float* p, const float* q, int64_t B, int64_t V, int K, float* r_stages,
+                                     int32_t* row_status, void* workspace, hipStream_t st) {
+  const int P = choose_splits(B, V, 2, 0);
+  Workspace ws;
+  carve_workspace(workspace, B, V, 2, 0, P, &ws);
+  hipError_t e = launch_induced(p, q, B, V, 2, 0, r_stages, row_status, ws, st);
+  const int64_t plane = B * V;
+  for (int j = 1; j < K - 1 && e == hipSuccess; ++j)
+    e = launch_induced_pair(p, r_stages + (j - 1) * plane, q, B, V, r_stages + j * plane, row_status, workspace, st);
+  return e;
+}
+
 }  // namespace mdss

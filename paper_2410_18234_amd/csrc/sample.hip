@@ -76,6 +76,72 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ p
 }
 
 
+// Successive pairwise selection (Remark 4).  Stage 1 chooses between X1 and
+// X2 (both from q, weights p/q); stage j >= 2 between the token Y kept so far
+// (law r_{j-1}, weight p(Y)/r_{j-1}(Y)) and X_{j+1} (weight p/q).  Y is kept
+// iff u_j (w_Y + w_X) < w_Y (fp64), or floor(2 u_j) = 0 when both weights are
+// zero.  u_j = u_sel[b][j-1], else word 0 of Philox(seed, (offset + b, j)).
+__global__ __launch_bounds__(256) void select_successive_kernel(
+    const float* __restrict__ p, const float* __restrict__ q, const float* __restrict__ r_stages,
+    const int32_t* __restrict__ drafts, const float* __restrict__ u_sel, uint64_t seed, uint64_t offset, int64_t B,
+    int64_t V, int K, int32_t* __restrict__ sel_index, int32_t* __restrict__ sel_token,
+    int32_t* __restrict__ row_status) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int st = 0;
+  for (int i = 0; i < K; ++i) {
+    const int32_t x = drafts[b * K + i];
+    if (x < 0 || (int64_t)x >= V) {
+      st |= kRowBadDraft;
+      continue;
+    }
+    const float pv = p[b * V + x], qv = q[b * V + x];
+    if (bad_prob(pv) || bad_prob(qv))
+      st |= kRowBadProb;
+    else if (!(qv > 0.0f))
+      st |= kRowBadDraft;
+  }
+  int32_t y = -1;
+  int idx = 0;
+  if (!st) {
+    y = drafts[b * K];
+    for (int j = 1; j < K; ++j) {
+      const int32_t x = drafts[b * K + j];
+      const float ly = j == 1 ? q[b * V + y] : r_stages[(int64_t)(j - 2) * B * V + b * V + y];
+      if (!(ly > 0.0f)) {
+        st = kRowBadDraft;
+        break;
+      }
+      const double wa = (double)p[b * V + y] / (double)ly;
+      const double wb = (double)p[b * V + x] / (double)q[b * V + x];
+      float u;
+      if (u_sel) {
+        u = u_sel[b * (K - 1) + (j - 1)];
+      } else {
+        const uint64_t pos = offset + (uint64_t)b;
+        uint32_t c[4] = {(uint32_t)pos, (uint32_t)(pos >> 32), (uint32_t)j, 0u};
+        philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+        u = (float)(c[0] >> 8) * 5.9604644775390625e-8f;  // 2^-24
+      }
+      const double W = wa + wb;
+      const bool keep = W > 0.0 ? (double)u * W < wa : floor(2.0 * (double)u) == 0.0;
+      if (!keep) {
+        y = x;
+        idx = j;
+      }
+    }
+  }
+  if (st) {
+    sel_index[b] = -1;
+    sel_token[b] = -1;
+    if (row_status) row_status[b] |= st;
+    return;
+  }
+  sel_index[b] = idx;
+  sel_token[b] = y;
+}
+
+
 // Two drafts proposed by different distributions: w_i = p(x_i) / q_i(x_i).
 __global__ __launch_bounds__(256) void select_pair_kernel(const float* __restrict__ p,
                                                            const float* __restrict__ q1,
@@ -383,6 +449,14 @@ hipError_t launch_select(const float* p, const float* q, const int32_t* drafts, 
                          int32_t* row_status, hipStream_t st) {
   hipLaunchKernelGGL(select_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, p, q, drafts, u, seed, offset,
                      B, V, K, sel_index, sel_token, row_status);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_successive(const float* p, const float* q, const float* r_stages, const int32_t* drafts,
+                                    const float* u_sel, uint64_t seed, uint64_t offset, int64_t B, int64_t V, int K,
+                                    int32_t* sel_index, int32_t* sel_token, int32_t* row_status, hipStream_t st) {
+  hipLaunchKernelGGL(select_successive_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, p, q, r_stages,
+                     drafts, u_sel, seed, offset, B, V, K, sel_index, sel_token, row_status);
   return hipGetLastError();
 }
 

@@ -95,3 +95,30 @@ def test_pair_argument_errors(lib):
     s = lib.mdss_select_intermediate_pair
     assert s(FAKE, FAKE, FAKE, None, None, 0, 0, 4, 16, FAKE, FAKE, None, None) == 1
     assert s(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 70000, 16, FAKE, FAKE, None, None) == 2
+
+
+def test_successive_and_tlp_argument_errors(lib):
+    assert lib.mdss_workspace_bytes_successive(4, 16) == lib.mdss_workspace_bytes_pair(4, 16)
+    assert lib.mdss_workspace_bytes_successive(4, 1) == 0
+    ws = lib.mdss_workspace_bytes_successive(4, 16)
+    f = lib.mdss_induced_dist_successive
+    assert f(FAKE, FAKE, 4, 16, 3, None, None, FAKE, ws, None) == 1
+    assert f(FAKE, FAKE, 4, 16, 1, FAKE, None, FAKE, ws, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 9, FAKE, None, FAKE, ws, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 3, FAKE, None, FAKE, ws - 1, None) == 5
+    g = lib.mdss_select_successive
+    assert g(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 3, FAKE, FAKE, None, None) == 1
+    assert g(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 9, FAKE, FAKE, None, None) == 3
+    assert lib.mdss_workspace_bytes_tlp(4, 16, 2) == 0
+    assert lib.mdss_workspace_bytes_tlp(4, 16, 1) < lib.mdss_workspace_bytes_tlp(4, 16, 0)
+    wt = lib.mdss_workspace_bytes_tlp(4, 16, 0)
+    t = lib.mdss_truncated_lp
+    assert t(FAKE, FAKE, None, 4, 16, 5, 0, FAKE, None, FAKE, None, None, FAKE, wt, None) == 1
+    assert t(FAKE, FAKE, None, 4, 16, 5, 2, FAKE, FAKE, FAKE, None, None, FAKE, wt, None) == 1
+    assert t(FAKE, FAKE, None, 4, 16, 0, 0, FAKE, FAKE, FAKE, None, None, FAKE, wt, None) == 3
+    assert t(FAKE, FAKE, None, 4, 16, 17, 0, FAKE, FAKE, FAKE, None, None, FAKE, wt, None) == 3
+    assert t(FAKE, FAKE, None, 4, 16, 5, 0, FAKE, FAKE, FAKE, None, None, FAKE, wt - 1, None) == 5
+    assert t(FAKE, FAKE, None, 0, 16, 5, 0, FAKE, FAKE, FAKE, None, None, FAKE, wt, None) == 2
+    sel = lib.mdss_select_truncated_lp
+    assert sel(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 5, 0, None, FAKE, FAKE, FAKE, None, None) == 1
+    assert sel(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 17, 0, FAKE, FAKE, FAKE, FAKE, None, None) == 3
