@@ -82,6 +82,14 @@ def cpu_tlp_step(p, q1, q2, drafts, u, s, tail):
     return oracle.accept_resample(p, r, stok, u)
 
 
+def succ_flops(q_np, K: int) -> float:
+    """Successive pairwise selection: stage 1 is the K = 2 pair sum (3 n (n - 1)),
+    each later stage a two-law pair sum over supp(r_{j-1}) x supp(q) = n x n (6 n^2)."""
+    import numpy as np
+    n = (q_np > 0).sum(1).astype(np.float64)
+    return float((3.0 * n * (n - 1.0) + (K - 2) * 6.0 * n * n).sum())
+
+
 def cpu_baseline(w, budget_rows: int):
     """The fp64 oracle (as it stands) on the first rows of the same workload."""
     import numpy as np
@@ -95,6 +103,9 @@ def cpu_baseline(w, budget_rows: int):
     t0 = time.perf_counter()
     if cfg.tlp_s:
         cpu_tlp_step(p, q, q2, d, u, cfg.tlp_s, cfg.tlp_tail)
+    elif cfg.successive:
+        from oracle import successive
+        successive.step(p, q, d, np.ascontiguousarray(u[:, :1].repeat(d.shape[1] - 1, 1)), u)
     elif q2 is not None:
         oracle.step_pair(p, q, q2, d, u)
     else:
@@ -104,6 +115,9 @@ def cpu_baseline(w, budget_rows: int):
     if cfg.tlp_s:
         cores = 1  # numpy ranking and a HiGHS LP per position, one thread
         what = "truncated LP per position (numpy ranking, HiGHS LP), selection, accept/resample"
+    elif cfg.successive:
+        cores = min(cores, os.cpu_count() or cores, rows)
+        what = "stage laws by enumeration of ordered pairs per stage, chained selection, accept/resample"
     else:
         cores = min(cores, os.cpu_count() or cores, rows)
         what = "r by enumeration of all ordered draft pairs, selection, accept/resample"
@@ -161,6 +175,11 @@ def main():
     status = torch.zeros(B, dtype=torch.int32, device=dev)
     if tlp_s:
         ws_bytes = mdss.workspace_bytes_tlp(B, V, tail)
+    elif cfg.successive:
+        ws_bytes = mdss.workspace_bytes_successive(B, V)
+        r_stages = torch.empty((K - 1, B, V), dtype=torch.float32, device=dev)
+        r = r_stages[K - 2]
+        u_sel = torch.from_numpy(np.ascontiguousarray(w["u"][:, :1].repeat(K - 1, 1))).to(dev)
     elif cfg.pair:
         ws_bytes = mdss.workspace_bytes_pair(B, V)
     else:
@@ -171,6 +190,8 @@ def main():
         if tlp_s:
             mdss.truncated_lp(p, q, q2, tlp_s, tail, r=r, omega1=omega1, w=wtab, accept=acc_prob,
                               row_status=status, workspace=ws)
+        elif cfg.successive:
+            mdss.induced_dist_successive(p, q, K, r_stages=r_stages, row_status=status, workspace=ws)
         elif cfg.pair:
             mdss.induced_dist_pair(p, q, q2, r=r, row_status=status, workspace=ws)
         else:
@@ -179,6 +200,8 @@ def main():
     def select():
         if tlp_s:
             return mdss.select_truncated_lp(p, q, q2, drafts, omega1, wtab, tail, u, row_status=status)
+        if cfg.successive:
+            return mdss.select_successive(p, q, r_stages, drafts, u_sel, row_status=status)
         if cfg.pair:
             return mdss.select_intermediate_pair(p, q, q2, drafts, u, row_status=status)
         return mdss.select_intermediate(p, q, drafts, u, row_status=status)
@@ -214,6 +237,8 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     assert int(status.abs().sum()) == 0, "rows flagged during the bench"
     accept_rate = float(acc.float().mean())
+    # expected acceptance sum_y min(p, r) of the proposal, averaged over positions (measurement only)
+    expected_acc = float(torch.minimum(p.double(), r.double()).sum(1).mean())
 
     digest = kernel_source_digest()
     if tlp_s:
@@ -226,13 +251,13 @@ def main():
                     "kernel": f"mdss_truncated_lp ({rank_name} + tlp_lp_kernel)", "avg_ms": round(r_ms, 4),
                     "bytes_per_launch": nbytes, "s": tlp_s, "tail": "sorted" if tail == 0 else "half"}
     else:
-        flops = pair_flops(w["q"], K, w.get("q2"))
+        flops = succ_flops(w["q"], K) if cfg.successive else pair_flops(w["q"], K, w.get("q2"))
         achieved = flops / (r_ms * 1e-3) / 1e12
-        sweep_name = "sweep_k2_mfma_kernel" if K == 2 else "sweep_k3_kernel"
+        sweep_name = "sweep_k2_mfma_kernel" if K == 2 or cfg.successive else "sweep_k3_kernel"
         roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(achieved / FP32_PEAK_TFLOPS, 4),
                     "traffic": counted_traffic(cfg.name, sweep_name, digest),
-                    "kernel": f"{'mdss_induced_dist_pair' if cfg.pair else 'mdss_induced_dist'} ({sweep_name} + "
+                    "kernel": f"{'mdss_induced_dist_successive' if cfg.successive else 'mdss_induced_dist_pair' if cfg.pair else 'mdss_induced_dist'} ({sweep_name} + "
                               "preparation)", "avg_ms": round(r_ms, 4), "flops_per_launch": flops}
 
     # accept / resample pass over every row with the residual written (12 B per token)
@@ -290,8 +315,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.describe}", "B": B, "V": V, "K": K,
                    "s_max": s_max or None, "two_draft_distributions": cfg.pair,
-                   "selection": "truncated LP" if tlp_s else "classical importance weights",
-                   "accept_rate": round(accept_rate, 4)},
+                   "selection": "truncated LP" if tlp_s else ("successive pairwise, classical importance weights"
+                                                              if cfg.successive else "classical importance weights"),
+                   "successive": cfg.successive, "accept_rate": round(accept_rate, 4),
+                   "expected_acceptance": round(expected_acc, 5)},
         "roofline": roofline,
         "roofline_resample": roofline_resample,
         "cpu_baseline": None,
@@ -299,7 +326,7 @@ def main():
     }
     if not args.no_cpu:
         ncores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-        rows = args.cpu_rows or (B if tlp_s else 2 * ncores)
+        rows = args.cpu_rows or (B if tlp_s or cfg.successive else 2 * ncores)
         line["cpu_baseline"] = cpu_baseline(w, rows)
     print(json.dumps(line), flush=True)
 
