@@ -186,6 +186,40 @@ mdss_status mdss_select_successive(const float* p, const float* q, const float* 
                                    int32_t K, int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
                                    void* stream);
 
+/* ---- Optimal acceptance diagnostics ---------------------------------------
+ * Theorem 3: for K = 2 drafts from q the best acceptance probability of any
+ * token-level selection rule is
+ *   P* = min over token sets S of P(S) + Q(S^c)^2 + 2 Q(S) Q(S^c)
+ *      = Qt^2 + min_S (P(S) - Q(S)^2)      (P, Q: target / draft mass, Qt = Q(all));
+ * Remark 2's K-draft form Qt^K + min_S (P(S) - Q(S)^K) is computed for K > 2
+ * (a conjecture of the paper for K > 2, exact for K = 2).  The library
+ * evaluates the minimum over the V + 1 prefixes of the tokens ordered by
+ * w = p/q ascending (w rounded once to fp32 from the fp64 ratio; q = 0 last;
+ * ties by lower token id), which is the minimum over all sets: a minimising set
+ * is {w < threshold} by strict convexity of x^K.  O(V) ranking and one scan per
+ * row, fp64 sums. */
+#define MDSS_OPTIMUM_MAX_K 8
+
+/* Workspace bytes of mdss_optimal_acceptance (0 if the shape is invalid). */
+size_t mdss_workspace_bytes_optimum(int64_t B, int64_t V);
+
+/* pstar [B] fp64 out: the value above for K in [2, MDSS_OPTIMUM_MAX_K];
+ * kstar [B] int32 (nullable): the smallest prefix length of the w order that
+ * attains it (0 = the empty set).  A row with a NaN, infinite or negative entry
+ * in p or q gets NaN / -1 and MDSS_ROW_BAD_PROB.  workspace: at least
+ * mdss_workspace_bytes_optimum(B, V) bytes, 256-byte aligned. */
+mdss_status mdss_optimal_acceptance(const float* p, const float* q, int64_t B, int64_t V, int32_t K, double* pstar,
+                                    int32_t* kstar, int32_t* row_status, void* workspace, size_t workspace_bytes,
+                                    void* stream);
+
+/* Acceptance probability of Algorithm 1 with proposal r against target p:
+ * accept[b] = sum_y min(p(y), r(y)) in fp64 (NaN and MDSS_ROW_BAD_PROB for a
+ * row with a NaN, infinite or negative entry).  With r from any of the
+ * induced-distribution calls, accept / pstar is the fraction of the optimum a
+ * selection rule achieves. */
+mdss_status mdss_acceptance(const float* p, const float* r, int64_t B, int64_t V, double* accept,
+                            int32_t* row_status, void* stream);
+
 /* ---- Truncated linear program (K = 2) -------------------------------------
  * The paper's practical selection rule (Algorithm 2, eq. heur, eq. p_Ieq and
  * the bound eq. p_acc_bnd), for identical drafts (q2 = NULL: both from q1) or

@@ -15,6 +15,7 @@ from .binding import (  # noqa: F401
     MDSS_ROW_BAD_PROB,
     MDSS_ROW_FORCED,
     MDSS_ROW_LP_LIMIT,
+    MDSS_OPTIMUM_MAX_K,
     MDSS_ROW_SUPPORT,
     MDSS_SUCCESSIVE_MAX_K,
     MDSS_TLP_HALF,
@@ -22,11 +23,13 @@ from .binding import (  # noqa: F401
     MDSS_TLP_SORTED,
     MdssError,
     accept_or_resample,
+    acceptance,
     induced_dist,
     induced_dist_pair,
     induced_dist_successive,
     library_path,
     load_library,
+    optimal_acceptance,
     select_intermediate,
     select_intermediate_pair,
     select_successive,
@@ -37,6 +40,7 @@ from .binding import (  # noqa: F401
     step_truncated_lp,
     truncated_lp,
     workspace_bytes,
+    workspace_bytes_optimum,
     workspace_bytes_pair,
     workspace_bytes_successive,
     workspace_bytes_tlp,

@@ -26,6 +26,7 @@ MDSS_TLP_MAX_S = 16
 MDSS_TLP_SORTED = 0
 MDSS_TLP_HALF = 1
 MDSS_SUCCESSIVE_MAX_K = 8
+MDSS_OPTIMUM_MAX_K = 8
 
 _STATUS = {0: "MDSS_OK", 1: "MDSS_EINVAL", 2: "MDSS_ESHAPE", 3: "MDSS_EUNSUPPORTED", 4: "MDSS_EDEVICE",
            5: "MDSS_EWORKSPACE"}
@@ -72,7 +73,12 @@ def load_library():
         lib.mdss_workspace_bytes_successive.restype = sz
         lib.mdss_induced_dist_successive.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P]
         lib.mdss_select_successive.argtypes = [P, P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P]
-        for f in ("mdss_induced_dist_successive", "mdss_select_successive"):
+        lib.mdss_workspace_bytes_optimum.argtypes = [i64, i64]
+        lib.mdss_workspace_bytes_optimum.restype = sz
+        lib.mdss_optimal_acceptance.argtypes = [P, P, i64, i64, i32, P, P, P, P, sz, P]
+        lib.mdss_acceptance.argtypes = [P, P, i64, i64, P, P, P]
+        for f in ("mdss_induced_dist_successive", "mdss_select_successive", "mdss_optimal_acceptance",
+                  "mdss_acceptance"):
             getattr(lib, f).restype = ctypes.c_int
         for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample",
                   "mdss_induced_dist_pair", "mdss_select_intermediate_pair", "mdss_truncated_lp",
@@ -429,3 +435,40 @@ def step_successive(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u_se
                                              want_mass=want_residual, row_status=status)
     return {"r_stages": rs, "r": rs[K - 2], "sel_index": sel_index, "sel_token": sel_token, "out_token": out,
             "accepted": acc, "residual": res, "mass": mass, "status": status}
+
+
+def workspace_bytes_optimum(B: int, V: int) -> int:
+    return int(load_library().mdss_workspace_bytes_optimum(B, V))
+
+
+def optimal_acceptance(p: torch.Tensor, q: torch.Tensor, K: int = 2, row_status: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None):
+    """(pstar [B] fp64, kstar [B] int32): Theorem 3's optimum (Remark 2's K-draft form for K > 2)."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    need = int(lib.mdss_workspace_bytes_optimum(B, V))
+    if need == 0:
+        _check("mdss_workspace_bytes_optimum", 2)
+    if workspace is None:
+        workspace = _workspace(dev, need)
+    elif workspace.dtype != torch.uint8 or workspace.device != dev or workspace.numel() < need:
+        raise ValueError(f"workspace must be a uint8 tensor on {dev} of at least {need} bytes")
+    pstar = torch.empty(B, dtype=torch.float64, device=dev)
+    kstar = torch.empty(B, dtype=torch.int32, device=dev)
+    _check("mdss_optimal_acceptance",
+           lib.mdss_optimal_acceptance(_ptr(p), _ptr(q), B, V, K, _ptr(pstar), _ptr(kstar), _ptr(row_status),
+                                       _ptr(workspace), workspace.numel(), _stream(dev)))
+    return pstar, kstar
+
+
+def acceptance(p: torch.Tensor, r: torch.Tensor, row_status: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """accept [B] fp64: sum_y min(p(y), r(y)), the acceptance of Algorithm 1 with proposal r."""
+    lib = load_library()
+    B, V, dev = _pq(p, r)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    out = torch.empty(B, dtype=torch.float64, device=dev)
+    _check("mdss_acceptance", lib.mdss_acceptance(_ptr(p), _ptr(r), B, V, _ptr(out), _ptr(row_status), _stream(dev)))
+    return out

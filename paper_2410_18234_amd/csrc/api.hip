@@ -121,6 +121,33 @@ mdss_status mdss_select_successive(const float* p, const float* q, const float* 
                                                  sel_token, row_status, static_cast<hipStream_t>(stream)));
 }
 
+size_t mdss_workspace_bytes_optimum(int64_t B, int64_t V) {
+  if (check_shape(B, V) != MDSS_OK) return 0;
+  return mdss::workspace_bytes_optimum(B, V);
+}
+
+mdss_status mdss_optimal_acceptance(const float* p, const float* q, int64_t B, int64_t V, int32_t K, double* pstar,
+                                    int32_t* kstar, int32_t* row_status, void* workspace, size_t workspace_bytes,
+                                    void* stream) {
+  if (!p || !q || !pstar) return MDSS_EINVAL;
+  const mdss_status st = check_shape(B, V);
+  if (st != MDSS_OK) return st;
+  if (K < 2 || K > MDSS_OPTIMUM_MAX_K) return MDSS_EUNSUPPORTED;
+  const size_t need = mdss::workspace_bytes_optimum(B, V);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) % 256) != 0)
+    return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_optimum(p, q, B, V, K, pstar, kstar, row_status, workspace,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+mdss_status mdss_acceptance(const float* p, const float* r, int64_t B, int64_t V, double* accept,
+                            int32_t* row_status, void* stream) {
+  if (!p || !r || !accept) return MDSS_EINVAL;
+  const mdss_status st = check_shape(B, V);
+  if (st != MDSS_OK) return st;
+  return from_hip(mdss::launch_acceptance(p, r, B, V, accept, row_status, static_cast<hipStream_t>(stream)));
+}
+
 size_t mdss_workspace_bytes_tlp(int64_t B, int64_t V, int32_t tail) {
   if (check_shape(B, V) != MDSS_OK || (tail != MDSS_TLP_SORTED && tail != MDSS_TLP_HALF)) return 0;
   return mdss::workspace_bytes_tlp(B, V, tail);

@@ -62,6 +62,11 @@ hipError_t launch_select_successive(const float* p, const float* q, const float*
                                     const float* u_sel, uint64_t seed, uint64_t offset, int64_t B, int64_t V, int K,
                                     int32_t* sel_index, int32_t* sel_token, int32_t* row_status, hipStream_t st);
 constexpr int kSuccessiveMaxK = 8;
+size_t workspace_bytes_optimum(int64_t B, int64_t V);
+hipError_t launch_optimum(const float* p, const float* q, int64_t B, int64_t V, int K, double* pstar, int32_t* kstar,
+                          int32_t* row_status, void* workspace, hipStream_t st);
+hipError_t launch_acceptance(const float* p, const float* r, int64_t B, int64_t V, double* out, int32_t* row_status,
+                             hipStream_t st);
 size_t workspace_bytes_tlp(int64_t B, int64_t V, int tail);
 hipError_t launch_tlp(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, int s, int tail,
                       float* r, int32_t* omega1, double* w, double* accept, int32_t* row_status, void* workspace,

@@ -24,7 +24,7 @@
 //     credited to its earlier-ranked token, then move mass along shortest
 //     augmenting paths (Edmonds-Karp) from tokens above their target mass to
 //     tokens below it.  The resulting shares give the selection table w.
-#include "common.h"
+#include "rank.h"
 
 #include <math.h>
 
@@ -32,8 +32,6 @@ namespace mdss {
 
 namespace {
 
-constexpr int kRankThreads = 1024;
-constexpr int kRankWaves = kRankThreads / 64;
 constexpr int kMaxS = 16;       // largest s accepted by the library
 constexpr int kLpMaxIter = 4096;  // augmentations before a row is flagged (bound for s = 16: (s+2)(s(s-1)+2s) = 4608)
 constexpr int kTailSorted = 0;
@@ -58,133 +56,6 @@ __device__ __forceinline__ uint32_t rank_word(float p, float a, float b) {
   return ~asc;
 }
 
-// Lanes of the wave whose digit equals this lane's (restricted to `act`).
-__device__ __forceinline__ uint64_t match_digit(uint32_t d, uint64_t act) {
-  uint64_t m = act;
-#pragma unroll
-  for (int bit = 0; bit < 8; ++bit) {
-    const uint64_t bb = __ballot((d >> bit) & 1u);
-    m &= ((d >> bit) & 1u) ? bb : ~bb;
-  }
-  return m;
-}
-
-__device__ __forceinline__ uint64_t lanes_below(int lane) { return (1ull << lane) - 1ull; }
-
-// Contiguous segment [lo, hi) of n elements walked by this wave (64 elements
-// per step, segments in wave order), so per-wave counting keeps input order.
-__device__ __forceinline__ void wave_segment(int n, int* lo, int* hi) {
-  const int seg = ((n + kRankWaves - 1) / kRankWaves + 63) & ~63;
-  *lo = min(n, (int)(threadIdx.x >> 6) * seg);
-  *hi = min(n, *lo + seg);
-}
-
-// Per-wave digit counts cnt[w][d] -> output positions: cnt[w][d] = base +
-// (elements with a smaller digit) + (elements with digit d in waves < w).
-// bin_cnt / bin_start (nullable) receive the digit totals and their starts.
-// Returns true if one digit holds all n elements (the pass would not move any).
-__device__ __forceinline__ bool digit_offsets(uint32_t (*cnt)[256], uint32_t* tot, uint32_t base, int n,
-                                              uint32_t* bin_cnt, uint32_t* bin_start, int* flag) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (threadIdx.x == 0) *flag = 0;
-  __syncthreads();
-  if (threadIdx.x < 256) {
-    const int d = threadIdx.x;
-    uint32_t run = 0;
-    for (int w = 0; w < kRankWaves; ++w) {
-      const uint32_t c = cnt[w][d];
-      cnt[w][d] = run;
-      run += c;
-    }
-    tot[d] = run;
-    if (bin_cnt) bin_cnt[d] = run;
-    if (run == (uint32_t)n) *flag = 1;
-  }
-  __syncthreads();
-  if (wave == 0) {
-    uint32_t v[4];
-    uint32_t sum = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      v[j] = tot[lane * 4 + j];
-      sum += v[j];
-    }
-    const int incl = wave_inclusive_scan_int((int)sum, lane);
-    uint32_t run = base + (uint32_t)incl - sum;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      tot[lane * 4 + j] = run;
-      if (bin_start) bin_start[lane * 4 + j] = run;
-      run += v[j];
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x < 256) {
-    const int d = threadIdx.x;
-    const uint32_t b0 = tot[d];
-    for (int w = 0; w < kRankWaves; ++w) cnt[w][d] += b0;
-  }
-  const bool uniform = *flag != 0;
-  __syncthreads();
-  return uniform;
-}
-
-// One stable counting pass on bits [shift, shift + 8) of the words,
-// (kin, iin) -> (kout, iout), over n elements (global memory or LDS).
-// Returns false, writing nothing, when every element has the same digit.
-__device__ __forceinline__ bool radix_pass(const uint32_t* kin, const uint32_t* iin, uint32_t* kout, uint32_t* iout,
-                                           int n, int shift, uint32_t (*cnt)[256], uint32_t* tot, int* flag) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int lo, hi;
-  wave_segment(n, &lo, &hi);
-  for (int d = lane; d < 256; d += 64) cnt[wave][d] = 0u;
-  constexpr int kBatch = 8;
-  for (int base = lo; base < hi; base += 64 * kBatch) {
-    uint32_t kr[kBatch];
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int i = base + j * 64 + lane;
-      kr[j] = i < hi ? kin[i] : 0u;
-    }
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int i = base + j * 64 + lane;
-      const uint64_t act = __ballot(i < hi);
-      if (!act) break;
-      const uint32_t d = (kr[j] >> shift) & 255u;
-      const uint64_t m = match_digit(d, act);
-      if (i < hi && lane == __ffsll((long long)m) - 1) cnt[wave][d] += (uint32_t)__popcll(m);
-    }
-  }
-  __syncthreads();
-  if (digit_offsets(cnt, tot, 0u, n, nullptr, nullptr, flag)) return false;
-  for (int base = lo; base < hi; base += 64 * kBatch) {
-    uint32_t kr[kBatch], ir[kBatch];
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int i = base + j * 64 + lane;
-      kr[j] = i < hi ? kin[i] : 0u;
-      ir[j] = i < hi ? iin[i] : 0u;
-    }
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int i = base + j * 64 + lane;
-      const uint64_t act = __ballot(i < hi);
-      if (!act) break;
-      const uint32_t d = (kr[j] >> shift) & 255u;
-      const uint64_t m = match_digit(d, act);
-      if (i < hi) {
-        const uint32_t pos = cnt[wave][d] + (uint32_t)__popcll(m & lanes_below(lane));
-        kout[pos] = kr[j];
-        iout[pos] = ir[j];
-        if (lane == __ffsll((long long)m) - 1) cnt[wave][d] += (uint32_t)__popcll(m);
-      }
-    }
-  }
-  __syncthreads();
-  return true;
-}
-
 __device__ __forceinline__ void flag_row(int64_t b, int64_t V, int s, float* rb, int32_t* omega1, TlpHdr* hdr,
                          int32_t* row_status, int flags) {
   for (int64_t i = threadIdx.x; i < V; i += kRankThreads) rb[i] = __int_as_float(0x7fc00000);
@@ -197,289 +68,82 @@ __device__ __forceinline__ void flag_row(int64_t b, int64_t V, int s, float* rb,
   }
 }
 
-// Block-wide sum in a fixed order (wave tree, then waves in index order).
-__device__ __forceinline__ double block_sum(double v, double* red) {
-  v = wave_sum(v);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  double t = 0.0;
-  for (int w = 0; w < kRankWaves; ++w) t += red[w];
-  __syncthreads();
-  return t;
-}
-
-// Exclusive suffix sums over the block in thread order (the sum over higher
-// threads), two values at once; also returns the block totals.
-__device__ __forceinline__ void block_exclusive_suffix2(double a, double b, double* ea, double* eb, double* ta,
-                                                        double* tb, double* sa, double* sb) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  double ia = a, ib = b;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const double oa = __shfl_down(ia, off, 64), ob = __shfl_down(ib, off, 64);
-    if (lane + off < 64) {
-      ia += oa;
-      ib += ob;
-    }
-  }
-  double xa = __shfl_down(ia, 1, 64), xb = __shfl_down(ib, 1, 64);
-  if (lane == 63) xa = xb = 0.0;
-  if (lane == 0) {
-    sa[wave] = ia;
-    sb[wave] = ib;
-  }
-  __syncthreads();
-  double oa = 0.0, ob = 0.0, fa = 0.0, fb = 0.0;
-  for (int w = kRankWaves - 1; w >= 0; --w) {
-    if (w > wave) {
-      oa += sa[w];
-      ob += sb[w];
-    }
-    fa += sa[w];
-    fb += sb[w];
-  }
-  __syncthreads();
-  *ea = oa + xa;
-  *eb = ob + xb;
-  *ta = fa;
-  *tb = fb;
-}
-
 // ---------------------------------------------------------------- SORTED tail
-// Bin-ordered copy of a row made by the scatter pass (structure of arrays).
-struct BinRow {
-  uint32_t* word;
-  uint32_t* id;
-  float* p;
-  float* a;
-  float* b;
+// The ranking of Algorithm 2 on the rank scan: values (p, q1, q2); the scan
+// masses are (q1, q2) of the Omega_2 entries; an Omega_1 entry (rank < s) is
+// recorded in omega1, every Omega_2 entry k gets r(k) = q1 q2 + q2 S1 + q1 S2.
+struct TlpSpec {
+  struct Args {
+    const float *p, *q1, *q2;
+    float* r;
+    int32_t* omega1;
+    TlpHdr* hdr;
+    int32_t* row_status;
+    int s;
+  };
+  struct Row {
+    const float *in0, *in1, *in2;
+    float* rb;
+    int32_t* omega1;
+    TlpHdr* hdr;
+    int32_t* row_status;
+    int64_t b, V;
+    int s;
+  };
+  struct State {
+    double acc = 0.0;  // sum over Omega_2 of min(p, r)
+  };
+  static __device__ __forceinline__ Row row(const Args& a, int64_t b, int64_t V);
+  static __device__ __forceinline__ uint32_t word(float p, float q1, float q2) { return rank_word(p, q1, q2); }
+  static __device__ __forceinline__ void set_totals(Row&, double, double) {}
+  static __device__ __forceinline__ void masses(const Row& r, uint32_t rank, float, float q1, float q2, double* m1,
+                                                double* m2) {
+    const bool om1 = rank < (uint32_t)r.s;
+    *m1 = om1 ? 0.0 : (double)q1;
+    *m2 = om1 ? 0.0 : (double)q2;
+  }
+  static __device__ __forceinline__ void visit(const Row& r, State& st, uint32_t rank, int id, float p, float q1,
+                                               float q2, double s1, double s2) {
+    if (rank < (uint32_t)r.s) {
+      r.omega1[r.b * r.s + rank] = id;
+      return;
+    }
+    const double av = (double)q1, bv = (double)q2;
+    const double rv = av * bv + bv * s1 + av * s2;
+    r.rb[id] = (float)rv;
+    st.acc += fmin((double)p, rv);
+  }
+  static __device__ __forceinline__ void flag(const Row& r, int64_t V, int flags) {
+    flag_row(r.b, V, r.s, r.rb, r.omega1, r.hdr, r.row_status, flags);
+  }
+  static __device__ __forceinline__ void finish(const Row& r, State& st, double c1, double c2, double* red) {
+    const int se = (int)min((int64_t)r.s, r.V);
+    if ((int)threadIdx.x >= se && (int)threadIdx.x < r.s) r.omega1[r.b * r.s + threadIdx.x] = -1;
+    const double acc = block_sum(st.acc, red);
+    if (threadIdx.x == 0) {
+      TlpHdr h = {};
+      h.s_eff = se;
+      h.a_tail = c1;
+      h.b_tail = c2;
+      h.tail_accept = acc;
+      r.hdr[r.b] = h;
+    }
+  }
 };
 
-constexpr int kGroup = 8192;  // entries sorted in LDS at once
-
-// Reverse scan of one ranked chunk: sorted[g] (g < G <= kGroup) = index into
-// the bin order of the entry with rank first_rank + g.  Entries ranked in
-// Omega_1 are recorded and take no part in the sums; every other entry k gets
-// r(k) = a b + b S_a + a S_b with S the q1 / q2 mass ranked after k.
-// The entries are first gathered (thread-strided, many loads in flight) into
-// the LDS staging arrays A, Bq, P, ID (kGroup entries each; `sorted` may
-// alias one of them), then scanned from LDS, E consecutive ranks per thread.
-constexpr int kStride = kGroup / kRankThreads;
-__device__ __forceinline__ void scan_chunk(const uint32_t* sorted, int G, uint32_t first_rank, uint32_t bin_base,
-                                           const BinRow& br, int s, int64_t b, float* rb, int32_t* omega1,
-                                           double* ca, double* cb, double* acc, double* sa, double* sb, float* A,
-                                           float* Bq, float* P, uint32_t* ID) {
-  uint32_t at[kStride];
-#pragma unroll
-  for (int k = 0; k < kStride; ++k) {
-    const int g = (int)threadIdx.x + k * kRankThreads;
-    at[k] = g < G ? bin_base + sorted[g] : 0u;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < kStride; ++k) {
-    const int g = (int)threadIdx.x + k * kRankThreads;
-    if (g < G) {
-      A[g] = br.a[at[k]];
-      Bq[g] = br.b[at[k]];
-      P[g] = br.p[at[k]];
-      ID[g] = br.id[at[k]];
-    }
-  }
-  __syncthreads();
-  const int E = (G + kRankThreads - 1) / kRankThreads;
-  const int g0 = min(G, (int)threadIdx.x * E), g1 = min(G, g0 + E);
-  double la = 0.0, lb = 0.0;  // this thread's Omega_2 mass (consecutive ranks)
-  for (int g = g0; g < g1; ++g) {
-    if (first_rank + (uint32_t)g < (uint32_t)s) continue;
-    la += (double)A[g];
-    lb += (double)Bq[g];
-  }
-  double ea, eb, ta, tb;
-  block_exclusive_suffix2(la, lb, &ea, &eb, &ta, &tb, sa, sb);
-  double s1 = *ca + ea, s2 = *cb + eb;  // mass ranked after the entry being visited
-  for (int g = g1 - 1; g >= g0; --g) {
-    const uint32_t rank = first_rank + (uint32_t)g;
-    const int id = (int)ID[g];
-    if (rank < (uint32_t)s) {
-      omega1[b * s + rank] = id;
-      continue;
-    }
-    const double av = (double)A[g], bv = (double)Bq[g];
-    const double rv = av * bv + bv * s1 + av * s2;
-    rb[id] = (float)rv;
-    *acc += fmin((double)P[g], rv);
-    s1 += av;
-    s2 += bv;
-  }
-  *ca += ta;
-  *cb += tb;
-  __syncthreads();  // the staging arrays are reused by the next chunk
-}
-
-// One workgroup per row.  Pass 1 counts the top 8 bits of the rank words per
-// wave (stable) and checks the row; pass 2 scatters (word, id, p, q1, q2) into
-// bin order; then bins are taken from the last-ranked down, consecutive bins
-// grouped up to kGroup entries, each group sorted in LDS (stable LSD passes) and
-// scanned.  A single bin above kGroup entries is sorted by global LSD passes on
-// its lower 24 bits and scanned in chunks.
-__global__ __launch_bounds__(kRankThreads) void tlp_rank_sorted_kernel(
-    const float* __restrict__ p, const float* __restrict__ q1, const float* __restrict__ q2, int64_t V, int s,
-    float* __restrict__ r, int32_t* __restrict__ omega1, TlpHdr* __restrict__ hdr, BinRow bins,
-    uint32_t* __restrict__ kA, uint32_t* __restrict__ iA, uint32_t* __restrict__ kB, uint32_t* __restrict__ iB,
-    int32_t* __restrict__ row_status) {
-  __shared__ uint32_t cnt[kRankWaves][256];
-  __shared__ uint32_t tot[256], bin_cnt[256], bin_start[256];
-  __shared__ uint32_t kx[2][kGroup], ix[2][kGroup];
-  __shared__ double sa[kRankWaves], sb[kRankWaves];
-  __shared__ int red[kRankWaves];
-  __shared__ int flag;
-  const int64_t b = blockIdx.x;
-  const float* pb = p + b * V;
-  const float* ab = q1 + b * V;
-  const float* bb = q2 + b * V;
-  float* rb = r + b * V;
-  const int n = (int)V;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const BinRow br = {bins.word + b * V, bins.id + b * V, bins.p + b * V, bins.a + b * V, bins.b + b * V};
-  int lo, hi;
-  wave_segment(n, &lo, &hi);
-  constexpr int kBatch = 4;
-  // pass 1: validity and per-wave counts of the top digit
-  for (int d = lane; d < 256; d += 64) cnt[wave][d] = 0u;
-  int bad = 0;
-  for (int base = lo; base < hi; base += 64 * kBatch) {
-    float pr[kBatch], ar[kBatch], brr[kBatch];
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int i = base + j * 64 + lane;
-      pr[j] = i < hi ? pb[i] : 0.0f;
-      ar[j] = i < hi ? ab[i] : 0.0f;
-      brr[j] = i < hi ? bb[i] : 0.0f;
-    }
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int i = base + j * 64 + lane;
-      const uint64_t act = __ballot(i < hi);
-      if (!act) break;
-      bad |= (bad_prob(pr[j]) || bad_prob(ar[j]) || bad_prob(brr[j])) ? 1 : 0;
-      const uint32_t d = rank_word(pr[j], ar[j], brr[j]) >> 24;
-      const uint64_t m = match_digit(d, act);
-      if (i < hi && lane == __ffsll((long long)m) - 1) cnt[wave][d] += (uint32_t)__popcll(m);
-    }
-  }
-  bad = __ballot(bad) != 0ull;
-  if (lane == 0) red[wave] = bad;
-  __syncthreads();
-  int any = 0;
-  for (int w = 0; w < kRankWaves; ++w) any |= red[w];
-  if (any) {
-    flag_row(b, V, s, rb, omega1, hdr, row_status, kRowBadProb);
-    return;
-  }
-  digit_offsets(cnt, tot, 0u, n, bin_cnt, bin_start, &flag);
-  // pass 2: stable scatter into bin order, with the values the scan needs
-  for (int base = lo; base < hi; base += 64 * kBatch) {
-    float pr[kBatch], ar[kBatch], brr[kBatch];
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int i = base + j * 64 + lane;
-      pr[j] = i < hi ? pb[i] : 0.0f;
-      ar[j] = i < hi ? ab[i] : 0.0f;
-      brr[j] = i < hi ? bb[i] : 0.0f;
-    }
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int i = base + j * 64 + lane;
-      const uint64_t act = __ballot(i < hi);
-      if (!act) break;
-      const uint32_t wd = rank_word(pr[j], ar[j], brr[j]);
-      const uint32_t d = wd >> 24;
-      const uint64_t m = match_digit(d, act);
-      if (i < hi) {
-        const uint32_t pos = cnt[wave][d] + (uint32_t)__popcll(m & lanes_below(lane));
-        br.word[pos] = wd;
-        br.id[pos] = (uint32_t)i;
-        br.p[pos] = pr[j];
-        br.a[pos] = ar[j];
-        br.b[pos] = brr[j];
-        if (lane == __ffsll((long long)m) - 1) cnt[wave][d] += (uint32_t)__popcll(m);
-      }
-    }
-  }
-  __syncthreads();
-  // pass 3: groups of bins, last-ranked first
-  double ca = 0.0, cb = 0.0, acc = 0.0;
-  int dh = 255;
-  while (dh >= 0) {
-    int dl = dh;
-    uint32_t G = bin_cnt[dh];
-    while (dl > 0 && G + bin_cnt[dl - 1] <= (uint32_t)kGroup) G += bin_cnt[--dl];
-    const uint32_t g_lo = bin_start[dl];
-    if (G == 0) {
-      dh = dl - 1;
-      continue;
-    }
-    if (G <= (uint32_t)kGroup) {
-      for (uint32_t g = threadIdx.x; g < G; g += kRankThreads) {
-        kx[0][g] = br.word[g_lo + g];
-        ix[0][g] = g;
-      }
-      __syncthreads();
-      int nonempty = 0;
-      for (int d = dl; d <= dh; ++d) nonempty += bin_cnt[d] > 0u;
-      const int top = nonempty > 1 ? 32 : 24;  // one bin: the top digit is shared
-      int cur = 0;
-      for (int shift = 0; shift < top; shift += 8)
-        if (radix_pass(kx[cur], ix[cur], kx[cur ^ 1], ix[cur ^ 1], (int)G, shift, cnt, tot, &flag)) cur ^= 1;
-      scan_chunk(ix[cur], (int)G, g_lo, g_lo, br, s, b, rb, omega1, &ca, &cb, &acc, sa, sb,
-                 reinterpret_cast<float*>(kx[0]), reinterpret_cast<float*>(kx[1]), reinterpret_cast<float*>(ix[0]),
-                 ix[1]);
-    } else {
-      // one bin above the LDS capacity: its words share the top digit
-      uint32_t* ka = kA + b * V;
-      uint32_t* ia = iA + b * V;
-      uint32_t* kb = kB + b * V;
-      uint32_t* ib = iB + b * V;
-      for (uint32_t g = threadIdx.x; g < G; g += kRankThreads) {
-        ka[g] = br.word[g_lo + g];
-        ia[g] = g;
-      }
-      __syncthreads();
-      uint32_t *k_in = ka, *i_in = ia, *k_out = kb, *i_out = ib;
-      for (int shift = 0; shift < 24; shift += 8) {
-        if (radix_pass(k_in, i_in, k_out, i_out, (int)G, shift, cnt, tot, &flag)) {
-          uint32_t* t = k_in;
-          k_in = k_out;
-          k_out = t;
-          t = i_in;
-          i_in = i_out;
-          i_out = t;
-        }
-      }
-      const uint32_t* sorted = i_in;
-      const int chunks = (int)((G + kGroup - 1) / kGroup);
-      for (int c = chunks - 1; c >= 0; --c) {
-        const uint32_t c0 = (uint32_t)c * kGroup;
-        const int Gc = (int)min((uint32_t)kGroup, G - c0);
-        scan_chunk(sorted + c0, Gc, g_lo + c0, g_lo, br, s, b, rb, omega1, &ca, &cb, &acc, sa, sb,
-                   reinterpret_cast<float*>(kx[0]), reinterpret_cast<float*>(kx[1]),
-                   reinterpret_cast<float*>(ix[0]), ix[1]);
-      }
-    }
-    dh = dl - 1;
-  }
-  const int se = min(s, n);
-  if (threadIdx.x >= se && threadIdx.x < s) omega1[b * s + threadIdx.x] = -1;
-  acc = block_sum(acc, sa);
-  if (threadIdx.x == 0) {
-    TlpHdr h = {};
-    h.s_eff = se;
-    h.a_tail = ca;
-    h.b_tail = cb;
-    h.tail_accept = acc;
-    hdr[b] = h;
-  }
+__device__ __forceinline__ TlpSpec::Row TlpSpec::row(const Args& a, int64_t b, int64_t V) {
+  Row r;
+  r.in0 = a.p + b * V;
+  r.in1 = a.q1 + b * V;
+  r.in2 = a.q2 + b * V;
+  r.rb = a.r + b * V;
+  r.omega1 = a.omega1;
+  r.hdr = a.hdr;
+  r.row_status = a.row_status;
+  r.b = b;
+  r.V = V;
+  r.s = a.s;
+  return r;
 }
 
 // ------------------------------------------------------------------ HALF tail
@@ -809,11 +473,9 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
-// SORTED tail: 5 planes of the bin-ordered row copy + 4 planes for a bin
-// above the LDS capacity, each [B][V] 32-bit words.
 size_t workspace_bytes_tlp(int64_t B, int64_t V, int tail) {
   size_t bytes = align256((size_t)B * sizeof(TlpHdr));
-  if (tail == kTailSorted) bytes += 9 * align256((size_t)B * (size_t)V * sizeof(uint32_t));
+  if (tail == kTailSorted) bytes += rank_workspace_bytes(B, V);
   return bytes;
 }
 
@@ -825,19 +487,9 @@ hipError_t launch_tlp(const float* p, const float* q1, const float* q2, int64_t 
   TlpHdr* hdr = reinterpret_cast<TlpHdr*>(base);
   base += align256((size_t)B * sizeof(TlpHdr));
   if (tail == kTailSorted) {
-    const size_t plane = align256((size_t)B * (size_t)V * sizeof(uint32_t));
-    BinRow bins;
-    bins.word = reinterpret_cast<uint32_t*>(base);
-    bins.id = reinterpret_cast<uint32_t*>(base + plane);
-    bins.p = reinterpret_cast<float*>(base + 2 * plane);
-    bins.a = reinterpret_cast<float*>(base + 3 * plane);
-    bins.b = reinterpret_cast<float*>(base + 4 * plane);
-    uint32_t* kA = reinterpret_cast<uint32_t*>(base + 5 * plane);
-    uint32_t* iA = reinterpret_cast<uint32_t*>(base + 6 * plane);
-    uint32_t* kB = reinterpret_cast<uint32_t*>(base + 7 * plane);
-    uint32_t* iB = reinterpret_cast<uint32_t*>(base + 8 * plane);
-    hipLaunchKernelGGL(tlp_rank_sorted_kernel, dim3((unsigned)B), dim3(kRankThreads), 0, st, p, q1, q2, V, s, r,
-                       omega1, hdr, bins, kA, iA, kB, iB, row_status);
+    TlpSpec::Args args = {p, q1, q2, r, omega1, hdr, row_status, s};
+    hipLaunchKernelGGL(rank_scan_kernel<TlpSpec>, dim3((unsigned)B), dim3(kRankThreads), 0, st, args, V,
+                       carve_rank_planes(base, B, V));
   } else {
     hipLaunchKernelGGL(tlp_rank_half_kernel, dim3((unsigned)B), dim3(kRankThreads), 0, st, p, q1, q2, V, s, r,
                        omega1, hdr, row_status);

@@ -122,3 +122,17 @@ def test_successive_and_tlp_argument_errors(lib):
     sel = lib.mdss_select_truncated_lp
     assert sel(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 5, 0, None, FAKE, FAKE, FAKE, None, None) == 1
     assert sel(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 17, 0, FAKE, FAKE, FAKE, FAKE, None, None) == 3
+
+
+def test_optimum_argument_errors(lib):
+    ws = lib.mdss_workspace_bytes_optimum(4, 16)
+    assert ws > 0 and lib.mdss_workspace_bytes_optimum(0, 16) == 0
+    f = lib.mdss_optimal_acceptance
+    assert f(FAKE, FAKE, 4, 16, 2, None, None, None, FAKE, ws, None) == 1
+    assert f(FAKE, FAKE, 4, 16, 1, FAKE, None, None, FAKE, ws, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 9, FAKE, None, None, FAKE, ws, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 2, FAKE, None, None, FAKE, ws - 1, None) == 5
+    assert f(FAKE, FAKE, 4, 1, 2, FAKE, None, None, FAKE, ws, None) == 2
+    a = lib.mdss_acceptance
+    assert a(FAKE, None, 4, 16, FAKE, None, None) == 1
+    assert a(FAKE, FAKE, 4, 1, FAKE, None, None) == 2
