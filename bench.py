@@ -101,7 +101,12 @@ def cpu_baseline(w, budget_rows: int):
     q2 = np.ascontiguousarray(w["q2"][:rows]) if "q2" in w else None
     oracle.step(p[:1, :64], q[:1, :64], d[:1], u[:1])  # load the library outside the timing
     t0 = time.perf_counter()
-    if cfg.tlp_s:
+    if cfg.diag:
+        from oracle import optimum
+        for b in range(rows):
+            optimum.prefix_optimum(p[b], q[b], 2)
+        optimum.achieved(p, q)  # the proposal is an input of the step; any fp32 law costs the same
+    elif cfg.tlp_s:
         cpu_tlp_step(p, q, q2, d, u, cfg.tlp_s, cfg.tlp_tail)
     elif cfg.successive:
         from oracle import successive
@@ -112,7 +117,10 @@ def cpu_baseline(w, budget_rows: int):
         oracle.step(p, q, d, u)
     dt = time.perf_counter() - t0
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    if cfg.tlp_s:
+    if cfg.diag:
+        cores = 1
+        what = "P* by the prefix form (numpy sort and cumulative sums) and the acceptance sum per position"
+    elif cfg.tlp_s:
         cores = 1  # numpy ranking and a HiGHS LP per position, one thread
         what = "truncated LP per position (numpy ranking, HiGHS LP), selection, accept/resample"
     elif cfg.successive:
@@ -206,10 +214,21 @@ def main():
             return mdss.select_intermediate_pair(p, q, q2, drafts, u, row_status=status)
         return mdss.select_intermediate(p, q, drafts, u, row_status=status)
 
+    if cfg.diag:
+        # the proposal whose share of the optimum is reported: the importance-weighted r, an input here
+        mdss.induced_dist(p, q, K, r=r)
+        ws_opt = torch.empty(mdss.workspace_bytes_optimum(B, V), dtype=torch.uint8, device=dev)
+
     def one_step(ev=None):
         status.zero_()
         if ev is not None:
             ev[0].record()
+        if cfg.diag:
+            pstar, _ = mdss.optimal_acceptance(p, q, 2, row_status=status, workspace=ws_opt)
+            achieved = mdss.acceptance(p, r, row_status=status)
+            if ev is not None:
+                ev[1].record()
+            return pstar, achieved
         induced()
         if ev is not None:
             ev[1].record()
@@ -236,12 +255,23 @@ def main():
     r_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
     ms_per_step = wall * 1e3 / args.steps
     assert int(status.abs().sum()) == 0, "rows flagged during the bench"
+    if cfg.diag:
+        pstar_t, achieved_t = out, acc
+        acc = torch.zeros(1, device=dev)
     accept_rate = float(acc.float().mean())
     # expected acceptance sum_y min(p, r) of the proposal, averaged over positions (measurement only)
     expected_acc = float(torch.minimum(p.double(), r.double()).sum(1).mean())
 
     digest = kernel_source_digest()
-    if tlp_s:
+    if cfg.diag:
+        # HBM-bound: P* reads p, q; the acceptance reads p, r (8 + 8 B/token)
+        nbytes = float(B) * V * 16
+        gbs = nbytes / (r_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                    "kernel": "mdss_optimal_acceptance (rank_scan_kernel) + mdss_acceptance", "avg_ms": round(r_ms, 4),
+                    "bytes_per_launch": nbytes}
+    elif tlp_s:
         # HBM-bound: read p, q1 (and q2), write r once
         nbytes = float(B) * V * (16 if cfg.pair else 12)
         gbs = nbytes / (r_ms * 1e-3) / 1e9
@@ -317,7 +347,9 @@ def main():
                    "s_max": s_max or None, "two_draft_distributions": cfg.pair,
                    "selection": "truncated LP" if tlp_s else ("successive pairwise, classical importance weights"
                                                               if cfg.successive else "classical importance weights"),
-                   "successive": cfg.successive, "accept_rate": round(accept_rate, 4),
+                   "successive": cfg.successive, "accept_rate": None if cfg.diag else round(accept_rate, 4),
+                   **({"mean_pstar": round(float(pstar_t.mean()), 5),
+                       "mean_fraction_of_optimum": round(float((achieved_t / pstar_t).mean()), 5)} if cfg.diag else {}),
                    "expected_acceptance": round(expected_acc, 5)},
         "roofline": roofline,
         "roofline_resample": roofline_resample,
@@ -326,7 +358,7 @@ def main():
     }
     if not args.no_cpu:
         ncores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-        rows = args.cpu_rows or (B if tlp_s or cfg.successive else 2 * ncores)
+        rows = args.cpu_rows or (B if tlp_s or cfg.successive or cfg.diag else 2 * ncores)
         line["cpu_baseline"] = cpu_baseline(w, rows)
     print(json.dumps(line), flush=True)
 
