@@ -64,12 +64,12 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(const float* __restr
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   constexpr int kWaves = kPrepThreads / 64;
   __shared__ double s_q0[kWaves];
-  __shared__ int s_cnt[kWaves], s_bad[kWaves];
+  __shared__ int s_cnt[kWaves], s_cnt_pos[kWaves], s_bad[kWaves];
   __shared__ float s_wmin[kWaves], s_wmax[kWaves];
   __shared__ int s_scan[kWaves];
   __shared__ RowHdr s_hdr;
 
-  int bad = 0, cnt = 0;
+  int bad = 0, cnt = 0, cnt_pos = 0;
   double q0 = 0.0;
   float wmin = INFINITY, wmax = 0.0f;
   for (int64_t x = tid; x < V; x += kPrepThreads) {
@@ -77,6 +77,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(const float* __restr
     bad |= (int)bad_prob(pv) | (int)bad_prob(qv);
     if (qv > 0.0f) {
       ++cnt;
+      cnt_pos += pv > 0.0f;
       if (pv == 0.0f) {
         q0 += (double)qv;
       } else {
@@ -88,30 +89,35 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(const float* __restr
   }
   bad = wave_sum_int(bad);
   cnt = wave_sum_int(cnt);
+  cnt_pos = wave_sum_int(cnt_pos);
   q0 = wave_sum(q0);
   wmin = wave_min(wmin);
   wmax = wave_max(wmax);
   if (lane == 0) {
     s_bad[wid] = bad;
     s_cnt[wid] = cnt;
+    s_cnt_pos[wid] = cnt_pos;
     s_q0[wid] = q0;
     s_wmin[wid] = wmin;
     s_wmax[wid] = wmax;
   }
   __syncthreads();
   if (tid == 0) {
-    int tb = 0, tc = 0;
+    int tb = 0, tc = 0, tp = 0;
     double tq = 0.0;
     float mn = INFINITY, mx = 0.0f;
     for (int i = 0; i < kWaves; ++i) {
       tb |= s_bad[i];
       tc += s_cnt[i];
+      tp += s_cnt_pos[i];
       tq += s_q0[i];
       mn = fminf(mn, s_wmin[i]);
       mx = fmaxf(mx, s_wmax[i]);
     }
     RowHdr h;
-    h.n = tc;
+    // K = 2 compacts the positive-weight tokens only (a zero-weight pole adds q(y) Q0 in closed form);
+    // K = 3 keeps the whole support as poles
+    h.n = K == 2 ? tp : tc;
     h.q0 = tq;
     h.pad = 0.0;
     h.scale = 0;
@@ -156,7 +162,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(const float* __restr
       const int64_t x = x0 + i;
       pv[i] = (x < V) ? pb[x] : 0.0f;
       qv[i] = (x < V) ? qb[x] : 0.0f;
-      c += (qv[i] > 0.0f);
+      c += (qv[i] > 0.0f) && (K != 2 || pv[i] > 0.0f);
     }
     const int incl = wave_inclusive_scan_int(c, lane);
     if (lane == 63) s_scan[wid] = incl;
@@ -172,8 +178,9 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(const float* __restr
       const int64_t x = x0 + i;
       if (x >= V) break;
       if (qv[i] > 0.0f) {
-        if (all_zero_weight) {
+        if (all_zero_weight || (K == 2 && !(pv[i] > 0.0f))) {
           rb[x] = (float)((double)qv[i] * zero_w_factor);
+          continue;
         } else {
           idx[off] = (int32_t)x;
           const float w = pv[i] / qv[i];
@@ -360,6 +367,8 @@ __device__ __forceinline__ void write_r(int64_t b, int64_t V, int K, const RowHd
     v = (double)q[b * V + y] * (K == 2 ? h.q0 : h.q0 * h.q0);
   } else {
     v = (double)K * (double)pv * ldexp(S, h.scale);
+    // K = 2: the zero-weight tokens are not poles; each adds p(y) q(x) / w(y) = q(y) q(x)
+    if (K == 2) v += 2.0 * (double)q[b * V + y] * h.q0;
   }
   r[b * V + y] = (float)v;
 }
@@ -905,7 +914,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_pair_kernel(const float* __
     const float pv = pb[x], av = ab[x], cv = cb[x];
     bad |= (int)(bad_prob(pv) || bad_prob(av) || bad_prob(cv));
     if (av > 0.0f) {
-      ++n1;
+      n1 += pv > 0.0f;
       if (pv == 0.0f) {
         z1 += (double)av;
       } else {
@@ -915,7 +924,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_pair_kernel(const float* __
       }
     }
     if (cv > 0.0f) {
-      ++n2;
+      n2 += pv > 0.0f;
       if (pv == 0.0f) {
         z2 += (double)cv;
       } else {
@@ -1002,8 +1011,8 @@ __global__ __launch_bounds__(kPrepThreads) void prep_pair_kernel(const float* __
       pv[i] = (x < V) ? pb[x] : 0.0f;
       av[i] = (x < V) ? ab[x] : 0.0f;
       cv[i] = (x < V) ? cb[x] : 0.0f;
-      c1 += (av[i] > 0.0f);
-      c2 += (cv[i] > 0.0f);
+      c1 += (av[i] > 0.0f) && (pv[i] > 0.0f);
+      c2 += (cv[i] > 0.0f) && (pv[i] > 0.0f);
     }
     const int i1 = wave_inclusive_scan_int(c1, lane), i2 = wave_inclusive_scan_int(c2, lane);
     if (lane == 63) {
@@ -1023,6 +1032,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_pair_kernel(const float* __
     for (int i = 0; i < 4; ++i) {
       const int64_t x = x0 + i;
       if (x >= V) break;
+      if (!(pv[i] > 0.0f)) continue;  // zero-weight tokens: closed form in finalize_pair_kernel
       if (av[i] > 0.0f) {
         const float w = pv[i] / av[i];
         w1.idx[b * w1.Sp + o1] = (int32_t)x;
@@ -1081,8 +1091,11 @@ __global__ __launch_bounds__(256) void finalize_pair_kernel(const float* __restr
   const int64_t i = b * V + y;
   const float pv = p[i], av = q1[i], cv = q2[i];
   double v = 0.0;
-  if (av > 0.0f) v += (pv > 0.0f) ? (double)pv * ldexp(s_a[i], h1.scale) : 0.5 * (double)av * h2.q0;
-  if (cv > 0.0f) v += (pv > 0.0f) ? (double)pv * ldexp(s_b[i], h1.scale) : 0.5 * (double)cv * h1.q0;
+  // zero-weight poles of the other draft add p(y) q_j(x) / w_i(y) = q_i(y) q_j(x): q_i(y) Qj_0 in all
+  if (av > 0.0f)
+    v += (pv > 0.0f) ? (double)pv * ldexp(s_a[i], h1.scale) + (double)av * h2.q0 : 0.5 * (double)av * h2.q0;
+  if (cv > 0.0f)
+    v += (pv > 0.0f) ? (double)pv * ldexp(s_b[i], h1.scale) + (double)cv * h1.q0 : 0.5 * (double)cv * h1.q0;
   r[i] = (float)v;
 }
 

@@ -122,20 +122,32 @@ struct OptSpec {
 };
 
 // sum over the row of min(p, r), fp64, in a fixed order; NaN if the row is bad
-__global__ __launch_bounds__(256) void acceptance_kernel(const float* __restrict__ p, const float* __restrict__ r,
-                                                         int64_t V, double* __restrict__ out,
-                                                         int32_t* __restrict__ row_status) {
-  __shared__ double red[4];
-  __shared__ int bad_w[4];
+constexpr int kAccThreads = 1024;
+__global__ __launch_bounds__(kAccThreads) void acceptance_kernel(const float* __restrict__ p,
+                                                                 const float* __restrict__ r, int64_t V,
+                                                                 double* __restrict__ out,
+                                                                 int32_t* __restrict__ row_status) {
+  __shared__ double red[kAccThreads / 64];
+  __shared__ int bad_w[kAccThreads / 64];
   const int64_t b = blockIdx.x;
   const float* pb = p + b * V;
   const float* rb = r + b * V;
   double acc = 0.0;
   int bad = 0;
-  for (int64_t i = threadIdx.x; i < V; i += 256) {
-    const float pv = pb[i], rv = rb[i];
-    bad |= (bad_prob(pv) || bad_prob(rv)) ? 1 : 0;
-    acc += fmin((double)pv, (double)rv);
+  constexpr int kU = 4;
+  for (int64_t i0 = threadIdx.x; i0 < V; i0 += kU * kAccThreads) {
+    float pv[kU], rv[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int64_t i = i0 + (int64_t)u * kAccThreads;
+      pv[u] = i < V ? pb[i] : 0.0f;
+      rv[u] = i < V ? rb[i] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      bad |= (bad_prob(pv[u]) || bad_prob(rv[u])) ? 1 : 0;
+      acc += fmin((double)pv[u], (double)rv[u]);
+    }
   }
   acc = wave_sum(acc);
   bad = __ballot(bad) != 0ull;
@@ -145,8 +157,13 @@ __global__ __launch_bounds__(256) void acceptance_kernel(const float* __restrict
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    const int any = bad_w[0] | bad_w[1] | bad_w[2] | bad_w[3];
-    out[b] = any ? __longlong_as_double(0x7ff8000000000000ll) : ((red[0] + red[1]) + red[2]) + red[3];
+    int any = 0;
+    double t = 0.0;
+    for (int w = 0; w < kAccThreads / 64; ++w) {
+      any |= bad_w[w];
+      t += red[w];
+    }
+    out[b] = any ? __longlong_as_double(0x7ff8000000000000ll) : t;
     if (any && row_status) row_status[b] |= kRowBadProb;
   }
 }
@@ -165,7 +182,7 @@ hipError_t launch_optimum(const float* p, const float* q, int64_t B, int64_t V, 
 
 hipError_t launch_acceptance(const float* p, const float* r, int64_t B, int64_t V, double* out, int32_t* row_status,
                              hipStream_t st) {
-  hipLaunchKernelGGL(acceptance_kernel, dim3((unsigned)B), dim3(256), 0, st, p, r, V, out, row_status);
+  hipLaunchKernelGGL(acceptance_kernel, dim3((unsigned)B), dim3(kAccThreads), 0, st, p, r, V, out, row_status);
   return hipGetLastError();
 }
 

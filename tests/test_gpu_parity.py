@@ -361,3 +361,36 @@ def test_extreme_weight_ranges(K):
     per_entry = np.max(np.abs(r - ro) / np.maximum(ro, 1e-300), axis=1)
     print("\nrange  rel-L1  max-entry-rel:", [(R, f"{a:.1e}", f"{b:.1e}") for R, a, b in zip(ranges, err, per_entry)])
     assert np.all(err <= RTOL_ROW), err
+
+
+@pytest.mark.parametrize("keep", [1, 40, 2000])
+def test_truncated_target_rows(keep):
+    # most tokens have zero weight: their poles enter in closed form (q(y) Q0 per query)
+    w = generate("llm32k", rows=range(12))
+    p = w["p"].astype(np.float64)
+    for b in range(p.shape[0]):
+        cut = np.sort(p[b])[-keep]
+        p[b][p[b] < cut] = 0.0
+        p[b] /= p[b].sum()
+    p = p.astype(np.float32)
+    q = w["q"]
+    r, st = gpu_r(p, q, 2)
+    assert np.all(st == 0)
+    mass = q.astype(np.float64).sum(1) ** 2
+    assert np.all(np.abs(r.astype(np.float64).sum(1) - mass) <= RTOL_ROW * mass)
+    rng = np.random.default_rng(keep)
+    rows = rng.integers(0, 12, 120)
+    ys = rng.integers(0, p.shape[1], 120)
+    ys[:60] = [int(rng.choice(np.flatnonzero(p[b] > 0))) for b in rows[:60]]
+    e = oracle.induced_dist_entries(p, q, 2, rows, ys)
+    got = r[rows, ys].astype(np.float64)
+    assert np.all(np.abs(got - e) <= RTOL_ROW * e + 1e-30), np.max(np.abs(got - e) / np.maximum(e, 1e-300))
+    # two draft laws on the same truncated targets
+    q2 = w["q"][::-1].copy()
+    st2 = torch.zeros(12, dtype=torch.int32, device=DEV)
+    r2 = mdss.induced_dist_pair(dev(p), dev(q), dev(q2), row_status=st2).cpu().numpy()
+    e2 = oracle.induced_dist_pair_entries(p, q, q2, rows, ys)
+    got2 = r2[rows, ys].astype(np.float64)
+    assert np.all(np.abs(got2 - e2) <= RTOL_ROW * e2 + 1e-30), np.max(np.abs(got2 - e2) / np.maximum(e2, 1e-300))
+    mass2 = q.astype(np.float64).sum(1) * q2.astype(np.float64).sum(1)
+    assert np.all(np.abs(r2.astype(np.float64).sum(1) - mass2) <= RTOL_ROW * mass2)
