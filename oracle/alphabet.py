@@ -9,7 +9,8 @@ complement in proportion to p.  The output has law p_a p~ + p 1[complement] = p.
 Readings shared with the GPU library: p~ = fp32(p / p(Omega_0)) with the mass in
 fp64; Z is kept iff u_keep < p_a (fp64); the complement draw is the smallest id
 j outside Omega_0 with C_j > u_draw Z_c (C the running complement mass in
-ascending id, fp64); Z_c = 0 keeps Z.  Notation: p = TARGET.
+ascending id, fp64); Z_c = 0 keeps Z; an invalid Z (-1, from a flagged row) is
+passed on as -1 and not counted as kept.  Notation: p = TARGET.
 """
 from __future__ import annotations
 
@@ -46,6 +47,9 @@ def post(p, inside, mass0, token, u2):
     out = np.asarray(token, np.int32).copy()
     kept = np.ones(B, np.uint8)
     for b in range(B):
+        if out[b] < 0:
+            kept[b] = 0
+            continue
         if float(u2[b, 0]) < mass0[b]:
             continue
         comp = np.where(inside[b], 0.0, p[b].astype(np.float64))

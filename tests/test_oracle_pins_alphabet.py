@@ -77,3 +77,10 @@ def test_monte_carlo_whole_scheme():
     exp = p.astype(np.float64) * N
     chi2 = float(((obs - exp) ** 2 / np.maximum(exp, 1e-12)).sum())
     assert chi2 < 30.0, (obs, exp)
+
+
+def test_invalid_z_is_passed_on():
+    p = np.array([[0.5, 0.25, 0.25]], np.float32)
+    pt, mass, inside = alphabet.truncate(p, 1)
+    out, kept = alphabet.post(p, inside, mass, np.array([-1], np.int32), np.array([[0.9, 0.5]], np.float32))
+    assert out[0] == -1 and kept[0] == 0
