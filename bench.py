@@ -27,7 +27,7 @@ METRIC = "positions/sec (V=32000, K=2) + % FP32 VALU peak (r) / % HBM BW (resamp
 
 def kernel_source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("api.hip", "common.h", "induced.hip", "sample.hip", "tlp.hip", "rank.h", "optimum.hip"):
+    for f in ("api.hip", "common.h", "induced.hip", "sample.hip", "tlp.hip", "rank.h", "optimum.hip", "alphabet.hip"):
         with open(os.path.join(ROOT, "paper_2410_18234_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -186,6 +186,32 @@ mdss_status mdss_select_successive(const float* p, const float* q, const float* 
                                    int32_t K, int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
                                    void* stream);
 
+/* ---- Truncated alphabet ---------------------------------------------------
+ * Section 4 (after the truncated LP): Omega_0 = the m tokens of largest target
+ * probability (ties by lower id).  Run any selection and Algorithm 1 with the
+ * renormalised target p~ = p 1[Omega_0] / p(Omega_0) in place of p; their output
+ * Z has law p~.  mdss_alphabet_post then keeps Z with probability
+ * p_a = p(Omega_0) and otherwise draws from the complement of Omega_0 in
+ * proportion to p, so the output has law p.  The selection with p~ costs O(m^2)
+ * per row on the K = 2 paths (only positive-weight tokens are poles). */
+
+/* p_trunc [B][V] fp32 out: p~ = fp32(p / p(Omega_0)) on Omega_0, 0 elsewhere;
+ * mass0 [B] fp64 out: p(Omega_0).  m >= 1 (m >= V keeps every token).  A row with
+ * a NaN, infinite or negative entry is flagged MDSS_ROW_BAD_PROB (p_trunc NaN,
+ * mass0 NaN).  No workspace. */
+mdss_status mdss_truncate_alphabet(const float* p, int64_t B, int64_t V, int32_t m, float* p_trunc, double* mass0,
+                                   int32_t* row_status, void* stream);
+
+/* token [B]: Z, the output of Algorithm 1 with target p_trunc (-1 is passed on).
+ * Keep Z iff u_keep < mass0 (fp64); else out = the smallest id j with p_trunc(j)
+ * = 0 and C_j > u_draw Z_c, C the running sum of p over those tokens in
+ * ascending id and Z_c its total (Z_c = 0: keep Z).  u2: [B][2] fp32 (u_keep,
+ * u_draw) or NULL: words 0 and 1 of Philox4x32-10 with key = seed and counter
+ * (offset + b (low, high word), 0, 1).  out_token [B] int32, kept [B] uint8. */
+mdss_status mdss_alphabet_post(const float* p, const float* p_trunc, const double* mass0, const int32_t* token,
+                               const float* u2, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+                               int32_t* out_token, uint8_t* kept, void* stream);
+
 /* ---- Optimal acceptance diagnostics ---------------------------------------
  * Theorem 3: for K = 2 drafts from q the best acceptance probability of any
  * token-level selection rule is

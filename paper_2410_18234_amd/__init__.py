@@ -23,6 +23,7 @@ from .binding import (  # noqa: F401
     MDSS_TLP_SORTED,
     MdssError,
     accept_or_resample,
+    alphabet_post,
     acceptance,
     induced_dist,
     induced_dist_pair,
@@ -35,9 +36,11 @@ from .binding import (  # noqa: F401
     select_successive,
     select_truncated_lp,
     step,
+    step_alphabet,
     step_pair,
     step_successive,
     step_truncated_lp,
+    truncate_alphabet,
     truncated_lp,
     workspace_bytes,
     workspace_bytes_optimum,

@@ -73,6 +73,10 @@ def load_library():
         lib.mdss_workspace_bytes_successive.restype = sz
         lib.mdss_induced_dist_successive.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P]
         lib.mdss_select_successive.argtypes = [P, P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P]
+        lib.mdss_truncate_alphabet.argtypes = [P, i64, i64, i32, P, P, P, P]
+        lib.mdss_alphabet_post.argtypes = [P, P, P, P, P, u64, u64, i64, i64, P, P, P]
+        lib.mdss_truncate_alphabet.restype = ctypes.c_int
+        lib.mdss_alphabet_post.restype = ctypes.c_int
         lib.mdss_workspace_bytes_optimum.argtypes = [i64, i64]
         lib.mdss_workspace_bytes_optimum.restype = sz
         lib.mdss_optimal_acceptance.argtypes = [P, P, i64, i64, i32, P, P, P, P, sz, P]
@@ -472,3 +476,51 @@ def acceptance(p: torch.Tensor, r: torch.Tensor, row_status: Optional[torch.Tens
     out = torch.empty(B, dtype=torch.float64, device=dev)
     _check("mdss_acceptance", lib.mdss_acceptance(_ptr(p), _ptr(r), B, V, _ptr(out), _ptr(row_status), _stream(dev)))
     return out
+
+
+def truncate_alphabet(p: torch.Tensor, m: int, row_status: Optional[torch.Tensor] = None):
+    """(p_trunc [B][V] fp32, mass0 [B] fp64): the target restricted to its m most probable tokens, renormalised."""
+    lib = load_library()
+    if p.dim() != 2 or p.device.type != "cuda":
+        raise ValueError("p must be a [B][V] GPU tensor")
+    B, V = p.shape
+    dev = p.device
+    _need(p, "p", torch.float32, (B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    pt = torch.empty((B, V), dtype=torch.float32, device=dev)
+    mass0 = torch.empty(B, dtype=torch.float64, device=dev)
+    _check("mdss_truncate_alphabet",
+           lib.mdss_truncate_alphabet(_ptr(p), B, V, m, _ptr(pt), _ptr(mass0), _ptr(row_status), _stream(dev)))
+    return pt, mass0
+
+
+def alphabet_post(p: torch.Tensor, p_trunc: torch.Tensor, mass0: torch.Tensor, token: torch.Tensor,
+                  u2: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0):
+    """(out_token, kept): keep Z = token with probability mass0, else draw from the complement of Omega_0."""
+    lib = load_library()
+    B, V, dev = _pq(p, p_trunc)
+    _need(mass0, "mass0", torch.float64, (B,), dev)
+    _need(token, "token", torch.int32, (B,), dev)
+    if u2 is not None:
+        _need(u2, "u2", torch.float32, (B, 2), dev)
+    out = torch.empty(B, dtype=torch.int32, device=dev)
+    kept = torch.empty(B, dtype=torch.uint8, device=dev)
+    _check("mdss_alphabet_post",
+           lib.mdss_alphabet_post(_ptr(p), _ptr(p_trunc), _ptr(mass0), _ptr(token), _ptr(u2), ctypes.c_uint64(seed),
+                                  ctypes.c_uint64(offset), B, V, _ptr(out), _ptr(kept), _stream(dev)))
+    return out, kept
+
+
+def step_alphabet(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, m: int, u: Optional[torch.Tensor] = None,
+                  u2: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0):
+    """Truncated alphabet around the importance-weighted path: p~, selection and Algorithm 1 with p~, post."""
+    B, K = drafts.shape
+    status = torch.zeros(B, dtype=torch.int32, device=p.device)
+    pt, mass0 = truncate_alphabet(p, m, row_status=status)
+    r = induced_dist(pt, q, K, row_status=status)
+    sel_index, sel_token = select_intermediate(pt, q, drafts, u, seed, offset, row_status=status)
+    z, acc, _, _ = accept_or_resample(pt, r, sel_token, u, seed, offset, row_status=status)
+    out, kept = alphabet_post(p, pt, mass0, z, u2, seed, offset)
+    return {"p_trunc": pt, "mass0": mass0, "r": r, "sel_index": sel_index, "sel_token": sel_token, "z": z,
+            "accepted": acc, "out_token": out, "kept": kept, "status": status}

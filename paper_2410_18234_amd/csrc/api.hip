@@ -121,6 +121,25 @@ mdss_status mdss_select_successive(const float* p, const float* q, const float* 
                                                  sel_token, row_status, static_cast<hipStream_t>(stream)));
 }
 
+mdss_status mdss_truncate_alphabet(const float* p, int64_t B, int64_t V, int32_t m, float* p_trunc, double* mass0,
+                                   int32_t* row_status, void* stream) {
+  if (!p || !p_trunc || !mass0 || m < 1) return MDSS_EINVAL;
+  const mdss_status st = check_shape(B, V);
+  if (st != MDSS_OK) return st;
+  return from_hip(mdss::launch_alphabet_truncate(p, B, V, m, p_trunc, mass0, row_status,
+                                                 static_cast<hipStream_t>(stream)));
+}
+
+mdss_status mdss_alphabet_post(const float* p, const float* p_trunc, const double* mass0, const int32_t* token,
+                               const float* u2, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+                               int32_t* out_token, uint8_t* kept, void* stream) {
+  if (!p || !p_trunc || !mass0 || !token || !out_token || !kept) return MDSS_EINVAL;
+  const mdss_status st = check_shape(B, V);
+  if (st != MDSS_OK) return st;
+  return from_hip(mdss::launch_alphabet_post(p, p_trunc, mass0, token, u2, seed, offset, B, V, out_token, kept,
+                                             static_cast<hipStream_t>(stream)));
+}
+
 size_t mdss_workspace_bytes_optimum(int64_t B, int64_t V) {
   if (check_shape(B, V) != MDSS_OK) return 0;
   return mdss::workspace_bytes_optimum(B, V);

@@ -63,6 +63,11 @@ hipError_t launch_select_successive(const float* p, const float* q, const float*
                                     int32_t* sel_index, int32_t* sel_token, int32_t* row_status, hipStream_t st);
 constexpr int kSuccessiveMaxK = 8;
 size_t workspace_bytes_optimum(int64_t B, int64_t V);
+hipError_t launch_alphabet_truncate(const float* p, int64_t B, int64_t V, int m, float* pt, double* mass0,
+                                    int32_t* row_status, hipStream_t st);
+hipError_t launch_alphabet_post(const float* p, const float* pt, const double* mass0, const int32_t* token,
+                                const float* u2, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+                                int32_t* out_token, uint8_t* kept, hipStream_t st);
 hipError_t launch_optimum(const float* p, const float* q, int64_t B, int64_t V, int K, double* pstar, int32_t* kstar,
                           int32_t* row_status, void* workspace, hipStream_t st);
 hipError_t launch_acceptance(const float* p, const float* r, int64_t B, int64_t V, double* out, int32_t* row_status,

@@ -136,3 +136,13 @@ def test_optimum_argument_errors(lib):
     a = lib.mdss_acceptance
     assert a(FAKE, None, 4, 16, FAKE, None, None) == 1
     assert a(FAKE, FAKE, 4, 1, FAKE, None, None) == 2
+
+
+def test_alphabet_argument_errors(lib):
+    t = lib.mdss_truncate_alphabet
+    assert t(FAKE, 4, 16, 0, FAKE, FAKE, None, None) == 1
+    assert t(None, 4, 16, 3, FAKE, FAKE, None, None) == 1
+    assert t(FAKE, 0, 16, 3, FAKE, FAKE, None, None) == 2
+    a = lib.mdss_alphabet_post
+    assert a(FAKE, FAKE, FAKE, None, None, 0, 0, 4, 16, FAKE, FAKE, None) == 1
+    assert a(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 1, FAKE, FAKE, None) == 2
