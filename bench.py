@@ -101,7 +101,12 @@ def cpu_baseline(w, budget_rows: int):
     q2 = np.ascontiguousarray(w["q2"][:rows]) if "q2" in w else None
     oracle.step(p[:1, :64], q[:1, :64], d[:1], u[:1])  # load the library outside the timing
     t0 = time.perf_counter()
-    if cfg.diag:
+    if cfg.alphabet:
+        from oracle import alphabet
+        pt, mass, inside = alphabet.truncate(p, cfg.alphabet)
+        res = oracle.step(pt, q, d, u)
+        alphabet.post(p, inside, mass, res["out_token"], np.ascontiguousarray(u[:, ::-1][:, :2]))  # timing only
+    elif cfg.diag:
         from oracle import optimum
         for b in range(rows):
             optimum.prefix_optimum(p[b], q[b], 2)
@@ -117,7 +122,11 @@ def cpu_baseline(w, budget_rows: int):
         oracle.step(p, q, d, u)
     dt = time.perf_counter() - t0
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    if cfg.diag:
+    if cfg.alphabet:
+        cores = min(cores, os.cpu_count() or cores, rows)
+        what = ("truncation to Omega_0, r of the truncated target by enumeration of all ordered draft pairs, "
+                "selection, accept/resample, post-processing")
+    elif cfg.diag:
         cores = 1
         what = "P* by the prefix form (numpy sort and cumulative sums) and the acceptance sum per position"
     elif cfg.tlp_s:
@@ -214,6 +223,10 @@ def main():
             return mdss.select_intermediate_pair(p, q, q2, drafts, u, row_status=status)
         return mdss.select_intermediate(p, q, drafts, u, row_status=status)
 
+    if cfg.alphabet:
+        pt = torch.empty_like(p)
+        mass0 = torch.empty(B, dtype=torch.float64, device=dev)
+        u2 = None  # the post-processing draws its own uniforms (a Philox stream apart from Algorithm 1's)
     if cfg.diag:
         # the proposal whose share of the optimum is reported: the importance-weighted r, an input here
         mdss.induced_dist(p, q, K, r=r)
@@ -223,6 +236,16 @@ def main():
         status.zero_()
         if ev is not None:
             ev[0].record()
+        if cfg.alphabet:
+            # p~ on the m most probable target tokens, the importance-weighted path with p~, the post-processing
+            ptr, m0 = mdss.truncate_alphabet(p, cfg.alphabet, row_status=status)
+            mdss.induced_dist(ptr, q, K, r=r, row_status=status, workspace=ws)
+            if ev is not None:
+                ev[1].record()
+            _, sel_token = mdss.select_intermediate(ptr, q, drafts, u, row_status=status)
+            z, acc, _, _ = mdss.accept_or_resample(ptr, r, sel_token, u, row_status=status)
+            out, _ = mdss.alphabet_post(p, ptr, m0, z, u2)
+            return out, acc
         if cfg.diag:
             pstar, _ = mdss.optimal_acceptance(p, q, 2, row_status=status, workspace=ws_opt)
             achieved = mdss.acceptance(p, r, row_status=status)
@@ -263,7 +286,15 @@ def main():
     expected_acc = float(torch.minimum(p.double(), r.double()).sum(1).mean())
 
     digest = kernel_source_digest()
-    if cfg.diag:
+    if cfg.alphabet:
+        # HBM-bound: read p (truncation) and p~, q (weights), write p~ and r
+        nbytes = float(B) * V * 20
+        gbs = nbytes / (r_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                    "kernel": "mdss_truncate_alphabet + mdss_induced_dist with the truncated target",
+                    "avg_ms": round(r_ms, 4), "bytes_per_launch": nbytes, "alphabet": cfg.alphabet}
+    elif cfg.diag:
         # HBM-bound: P* reads p, q; the acceptance reads p, r (8 + 8 B/token)
         nbytes = float(B) * V * 16
         gbs = nbytes / (r_ms * 1e-3) / 1e9
@@ -346,7 +377,10 @@ def main():
         "config": {"workload": f"{cfg.name}: {cfg.describe}", "B": B, "V": V, "K": K,
                    "s_max": s_max or None, "two_draft_distributions": cfg.pair,
                    "selection": "truncated LP" if tlp_s else ("successive pairwise, classical importance weights"
-                                                              if cfg.successive else "classical importance weights"),
+                                                              if cfg.successive else
+                                                              f"classical importance weights, alphabet truncated to "
+                                                              f"{cfg.alphabet} tokens" if cfg.alphabet else
+                                                              "classical importance weights"),
                    "successive": cfg.successive, "accept_rate": None if cfg.diag else round(accept_rate, 4),
                    **({"mean_pstar": round(float(pstar_t.mean()), 5),
                        "mean_fraction_of_optimum": round(float((achieved_t / pstar_t).mean()), 5)} if cfg.diag else {}),

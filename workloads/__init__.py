@@ -58,6 +58,7 @@ class Config:
     tlp_tail: int = 0   # truncated LP: 0 = sorted Omega_2 (Algorithm 2), 1 = halves (sort-free variant)
     successive: bool = False  # K drafts reduced two at a time (successive pairwise selection)
     diag: bool = False  # optimal-acceptance diagnostics (Theorem 3) instead of a selection step
+    alphabet: int = 0   # truncated alphabet: |Omega_0| (0: the whole vocabulary)
 
 
 def _row_dirichlet(cfg: Config, b: int):
@@ -137,6 +138,9 @@ CONFIGS: Dict[str, Config] = {
         Config("succ_k3top1024", 1005, 256, 32000, 3,
                "successive pairwise selection of K=3 drafts on the k3top1024 rows: V=32000, draft truncated to "
                "its top-1024 tokens, 256 positions", _row_topk(1024), successive=True),
+        Config("alpha_llm32k", 1002, 256, 32000, 2,
+               "truncated alphabet |Omega_0| = 40 around the importance-weighted path (K=2), on the llm32k rows",
+               _row_gauss(3.0, 1.0, 1.0), alphabet=40),
         Config("opt_llm32k", 1002, 256, 32000, 2,
                "optimal acceptance P* (Theorem 3) and the acceptance of the importance-weighted proposal per "
                "position, on the llm32k rows", _row_gauss(3.0, 1.0, 1.0), diag=True),
