@@ -218,35 +218,15 @@ struct RankPlanes {
   uint32_t *kA, *iA, *kB, *iB;
 };
 
-// Reverse scan of one ranked chunk: sorted[g] (g < G <= kGroup) = index into
-// the bin order of the entry with rank first_rank + g.  The entries are first
-// gathered (thread-strided, many loads in flight) into the LDS staging arrays
-// V0, V1, V2, ID (`sorted` may alias one of them), then scanned from LDS, E
-// consecutive ranks per thread; Spec::visit sees each entry with the two
-// masses (Spec::masses) ranked after it.
+// Reverse scan of a ranked chunk whose entries are staged in LDS in rank order
+// (V0, V1, V2, ID; g < G <= kGroup, rank first_rank + g): each thread owns E
+// consecutive ranks, the block scan gives every entry the two masses
+// (Spec::masses) ranked after it, and Spec::visit sees each entry with them.
 template <class Spec>
-__device__ __forceinline__ void scan_chunk(const uint32_t* sorted, int G, uint32_t first_rank, uint32_t bin_base,
-                                           const BinRow& br, const typename Spec::Row& row,
-                                           typename Spec::State& state, double* c1, double* c2, double* sa,
-                                           double* sb, float* V0, float* V1, float* V2, uint32_t* ID) {
-  uint32_t at[kStride];
-#pragma unroll
-  for (int k = 0; k < kStride; ++k) {
-    const int g = (int)threadIdx.x + k * kRankThreads;
-    at[k] = g < G ? bin_base + sorted[g] : 0u;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < kStride; ++k) {
-    const int g = (int)threadIdx.x + k * kRankThreads;
-    if (g < G) {
-      V0[g] = br.v0[at[k]];
-      V1[g] = br.v1[at[k]];
-      V2[g] = br.v2[at[k]];
-      ID[g] = br.id[at[k]];
-    }
-  }
-  __syncthreads();
+__device__ __forceinline__ void scan_staged(int G, uint32_t first_rank, const typename Spec::Row& row,
+                                            typename Spec::State& state, double* c1, double* c2, double* sa,
+                                            double* sb, const float* V0, const float* V1, const float* V2,
+                                            const uint32_t* ID) {
   const int E = (G + kRankThreads - 1) / kRankThreads;
   const int g0 = min(G, (int)threadIdx.x * E), g1 = min(G, g0 + E);
   double l1 = 0.0, l2 = 0.0;  // this thread's masses (consecutive ranks)
@@ -270,6 +250,65 @@ __device__ __forceinline__ void scan_chunk(const uint32_t* sorted, int G, uint32
   *c1 += t1;
   *c2 += t2;
   __syncthreads();  // the staging arrays are reused by the next chunk
+}
+
+// A group sorted in LDS: inv[i] = rank within the group of bin-order entry i
+// (i < G).  The entries are read in bin order (coalesced) and written to their
+// rank's slot of the staging arrays (`inv` may alias one of them), then scanned.
+template <class Spec>
+__device__ __forceinline__ void scan_group(const uint32_t* inv, int G, uint32_t g_lo, const BinRow& br,
+                                           const typename Spec::Row& row, typename Spec::State& state, double* c1,
+                                           double* c2, double* sa, double* sb, float* V0, float* V1, float* V2,
+                                           uint32_t* ID) {
+  uint32_t slot[kStride];
+#pragma unroll
+  for (int k = 0; k < kStride; ++k) {
+    const int i = (int)threadIdx.x + k * kRankThreads;
+    slot[k] = i < G ? inv[i] : 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kStride; ++k) {
+    const int i = (int)threadIdx.x + k * kRankThreads;
+    if (i < G) {
+      const uint32_t at = g_lo + (uint32_t)i;
+      V0[slot[k]] = br.v0[at];
+      V1[slot[k]] = br.v1[at];
+      V2[slot[k]] = br.v2[at];
+      ID[slot[k]] = br.id[at];
+    }
+  }
+  __syncthreads();
+  scan_staged<Spec>(G, g_lo, row, state, c1, c2, sa, sb, V0, V1, V2, ID);
+}
+
+// A chunk of a bin sorted in global memory: sorted[g] = bin-order index of
+// rank first_rank + g; the entries are gathered (thread-strided, many loads in
+// flight) into the staging arrays, then scanned.
+template <class Spec>
+__device__ __forceinline__ void scan_chunk(const uint32_t* sorted, int G, uint32_t first_rank, uint32_t bin_base,
+                                           const BinRow& br, const typename Spec::Row& row,
+                                           typename Spec::State& state, double* c1, double* c2, double* sa,
+                                           double* sb, float* V0, float* V1, float* V2, uint32_t* ID) {
+  uint32_t at[kStride];
+#pragma unroll
+  for (int k = 0; k < kStride; ++k) {
+    const int g = (int)threadIdx.x + k * kRankThreads;
+    at[k] = g < G ? bin_base + sorted[g] : 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kStride; ++k) {
+    const int g = (int)threadIdx.x + k * kRankThreads;
+    if (g < G) {
+      V0[g] = br.v0[at[k]];
+      V1[g] = br.v1[at[k]];
+      V2[g] = br.v2[at[k]];
+      ID[g] = br.id[at[k]];
+    }
+  }
+  __syncthreads();
+  scan_staged<Spec>(G, first_rank, row, state, c1, c2, sa, sb, V0, V1, V2, ID);
 }
 
 // The ranking kernel.  Spec provides:
@@ -397,7 +436,10 @@ __global__ __launch_bounds__(kRankThreads) void rank_scan_kernel(typename Spec::
       int cur = 0;
       for (int shift = 0; shift < top; shift += 8)
         if (radix_pass(kx[cur], ix[cur], kx[cur ^ 1], ix[cur ^ 1], (int)G, shift, cnt, tot, &flag)) cur ^= 1;
-      scan_chunk<Spec>(ix[cur], (int)G, g_lo, g_lo, br, row, state, &c1, &c2, sa, sb, V0, V1, V2, ix[1]);
+      // inverse permutation (rank of each bin-order entry) into the free index buffer
+      for (uint32_t g = threadIdx.x; g < G; g += kRankThreads) ix[cur ^ 1][ix[cur][g]] = g;
+      __syncthreads();
+      scan_group<Spec>(ix[cur ^ 1], (int)G, g_lo, br, row, state, &c1, &c2, sa, sb, V0, V1, V2, ix[1]);
     } else {
       // one bin above the LDS capacity: its words share the top digit
       uint32_t* ka = planes.kA + b * V;
