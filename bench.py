@@ -158,7 +158,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); positions are independent, "
-              "so a multi-GPU run would shard rows with no exchange and is not part of this build",
+              "so several GPUs would each take a share of the rows with no exchange; run it with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
