@@ -1,7 +1,8 @@
 """GPU parity of the truncated alphabet (Section 4) against oracle/alphabet.py:
 Omega_0 membership bit-exact, p~ within one fp32 ulp, p(Omega_0) to 1e-15,
 keep decisions bit-exact on common inputs, complement draws equal except within
-1e-6 of a CDF boundary.  Notation: p = target, q = draft."""
+1e-6 of a CDF boundary.  The post-processing and the sampled r entries take
+the oracle's truncation as their common input.  Notation: p = target, q = draft."""
 import numpy as np
 import pytest
 import torch
@@ -58,7 +59,7 @@ def test_truncate_full_size():
 def test_post_decisions():
     w = generate("llm32k", rows=range(64))
     p = w["p"]
-    pt, mass, _ = gpu_truncate(p, 40)
+    pt, mass, _ = alphabet.truncate(p, 40)
     rng = np.random.default_rng(1100)
     z = rng.integers(0, p.shape[1], 64).astype(np.int32)
     z[:3] = -1
@@ -79,7 +80,7 @@ def test_post_decisions():
 def test_post_philox():
     w = generate("llm32k", rows=range(32))
     p = w["p"]
-    pt, mass, _ = gpu_truncate(p, 5)
+    pt, mass, _ = alphabet.truncate(p, 5)
     z = np.zeros(32, np.int32)
     seed, offset = 0xDEADBEEF12345, 11
     out, kept = mdss.alphabet_post(dev(p), dev(pt), dev(mass), dev(z), None, seed=seed, offset=offset)
@@ -99,11 +100,14 @@ def test_step_with_truncated_target():
     pt = g["p_trunc"].cpu().numpy()
     r = g["r"].cpu().numpy()
     assert np.all(g["status"].cpu().numpy() == 0)
+    opt, _, _ = alphabet.truncate(w["p"], 40)
+    np.testing.assert_array_equal(pt > 0, opt > 0)
     rng = np.random.default_rng(1200)
     rows = rng.integers(0, 48, 64)
-    ys = np.array([int(rng.choice(np.flatnonzero(pt[b] > 0))) if i % 2 else int(rng.integers(0, pt.shape[1]))
+    ys = np.array([int(rng.choice(np.flatnonzero(opt[b] > 0))) if i % 2 else int(rng.integers(0, opt.shape[1]))
                    for i, b in enumerate(rows)])
-    e = oracle.induced_dist_entries(pt, w["q"], 2, rows, ys)
+    # r from the oracle's p~ (the GPU's p~ is within one fp32 ulp of it)
+    e = oracle.induced_dist_entries(opt, w["q"], 2, rows, ys)
     assert np.all(np.abs(r[rows, ys] - e) <= RTOL_ROW * e + 1e-30)
     out, kept = g["out_token"].cpu().numpy(), g["kept"].cpu().numpy()
     assert np.all(pt[np.arange(48)[kept == 1], out[kept == 1]] > 0)

@@ -9,8 +9,9 @@ import torch
 
 import oracle
 import paper_2410_18234_amd as mdss
-from test_gpu_parity import RTOL_ROW, check_step2, dev, rel_l1
-from workloads import CONFIGS, generate
+from test_gpu_parity import (RTOL_ROW, check_accept_at_selected, check_step2_invariants, dev, rel_l1,
+                             step2_common)
+from workloads import CONFIGS, generate, proposal_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -42,7 +43,8 @@ def test_small_rows_full_oracle():
     ref = oracle.step_pair(p, q1, q2, drafts, u)
     assert np.all(rel_l1(g["r"], ref["r"]) <= RTOL_ROW), rel_l1(g["r"], ref["r"]).max()
     assert np.array_equal(g["sel_index"], ref["sel_index"])
-    check_step2(p, g["r"], g["sel_token"], u, g["out_token"], g["accepted"], g["residual"], g["mass"])
+    check_step2_invariants(p, g["r"], g["sel_token"], u, g["out_token"], g["accepted"], g["residual"], g["mass"])
+    step2_common(p, ref["r32"], ref["sel_token"], u)
 
 
 def test_identical_distributions_match_k2_path():
@@ -74,7 +76,11 @@ def test_pair32k_full_size():
     assert np.all(np.abs(got - e) <= RTOL_ROW * e), np.max(np.abs(got - e) / np.maximum(e, 1e-300))
     si, stok, _ = oracle.select_pair(p, q1, q2, w["drafts"], w["u"])
     assert np.array_equal(g["sel_index"], si) and np.array_equal(g["sel_token"], stok)
-    check_step2(p, g["r"], g["sel_token"], w["u"], g["out_token"], g["accepted"], g["residual"], g["mass"])
+    check_step2_invariants(p, g["r"], g["sel_token"], w["u"], g["out_token"], g["accepted"], g["residual"], g["mass"])
+    rows2 = rng.choice(B, size=64, replace=False)
+    check_accept_at_selected(p, w["u"], rows2, stok[rows2],
+                             oracle.induced_dist_pair_entries(p, q1, q2, rows2, stok[rows2]), g["accepted"])
+    step2_common(p, proposal_rows(p, q2, cfg.seed), stok, w["u"])
 
 
 def test_pair32k_rows_full_oracle():

@@ -4,6 +4,11 @@ Bars: r and the residual within 1e-5 relative L1 per row; selection indices
 bit-exact; accept decisions bit-exact on a common r; output tokens identical
 except where the residual uniform lies within 1e-6 of a CDF boundary (or, end
 to end, within the r error of the row).  Notation: p = target, q = draft.
+
+The oracle only ever sees seeded inputs and its own results: the second step is
+compared on a common proposal that the oracle or the input generator produced,
+and outputs the GPU computed from its own r are checked by Algorithm 1's
+invariants written out here.
 """
 import zlib
 
@@ -13,7 +18,7 @@ import torch
 
 import oracle
 import paper_2410_18234_amd as mdss
-from workloads import CONFIGS, generate
+from workloads import CONFIGS, generate, proposal_rows
 
 pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda:0")
@@ -39,7 +44,9 @@ def gpu_r(p, q, K, s_max=0):
 
 
 def check_step2(p, r32, sel, u, out_g, acc_g, res_g=None, mass_g=None, window=None):
-    """Step 2 on a common fp32 r: decisions exact, tokens equal outside boundary windows."""
+    """Step 2 on a common fp32 proposal r32 (made by the oracle or the input
+    generator, never by the GPU): decisions exact, tokens equal outside boundary
+    windows."""
     out_o, acc_o, res_o, mass_o, st_o = oracle.accept_resample(p, r32, sel, u, want_residual=True)
     valid = out_o >= 0
     assert np.array_equal(acc_g, acc_o), "accept decisions differ"
@@ -65,6 +72,56 @@ def check_step2(p, r32, sel, u, out_g, acc_g, res_g=None, mass_g=None, window=No
     return excluded
 
 
+def step2_common(p, r32, sel, u):
+    """The GPU's accept / resample on a common proposal, against the oracle's."""
+    out, acc, res, mass = mdss.accept_or_resample(dev(p), dev(r32), dev(sel), dev(u), want_residual=True,
+                                                  want_mass=True)
+    torch.cuda.synchronize()
+    return check_step2(p, r32, sel, u, out.cpu().numpy(), acc.cpu().numpy(), res.cpu().numpy(), mass.cpu().numpy())
+
+
+def check_step2_invariants(p, r, sel, u, out, acc, res=None, mass=None):
+    """Algorithm 1 on outputs the GPU computed from its own proposal r (no oracle
+    involved): accepted iff u1 r(Y) < p(Y) (fp64 products of the fp32 values) or
+    the residual is empty; an accepted row returns Y; the residual is (p - r)^+
+    and the mass its sum; a rejection returns a token with p > r whose interval
+    of the residual's CDF holds u2 Z, up to a window of 1e-6 Z."""
+    p64 = np.asarray(p, np.float32).astype(np.float64)
+    r64 = np.asarray(r, np.float32).astype(np.float64)
+    sel = np.asarray(sel)
+    assert np.all((sel >= 0) & (sel < p64.shape[1]))
+    res_e = np.maximum(p64 - r64, 0.0)
+    Z = res_e.sum(1)
+    rows = np.arange(len(sel))
+    u1 = u[:, 1].astype(np.float64)
+    u2 = u[:, 2].astype(np.float64)
+    take = (u1 * r64[rows, sel] < p64[rows, sel]) | ~(Z > 0)
+    assert np.array_equal(np.asarray(acc).astype(bool), take)
+    assert np.array_equal(out[take], sel[take])
+    for b in np.flatnonzero(~take):
+        j = int(out[b])
+        assert 0 <= j < p64.shape[1] and res_e[b, j] > 0, b
+        C = np.cumsum(res_e[b])
+        t = u2[b] * Z[b]
+        assert (C[j - 1] if j > 0 else 0.0) - 1e-6 * Z[b] <= t < C[j] + 1e-6 * Z[b], b
+    if res is not None:
+        ok = Z > 0
+        assert np.all(rel_l1(res[ok], res_e[ok]) <= RTOL_ROW)
+    if mass is not None:
+        np.testing.assert_allclose(mass, Z, rtol=1e-12, atol=1e-300)
+
+
+def check_accept_at_selected(p, u, rows, Y, r_entries, acc_g):
+    """Accept decisions of sampled rows against the oracle's r at the selected
+    token, outside a window of the r tolerance around the decision boundary."""
+    rY = np.asarray(r_entries, np.float64).astype(np.float32).astype(np.float64)
+    pY = p[rows, Y].astype(np.float64)
+    u1 = u[rows, 1].astype(np.float64)
+    clear = np.abs(u1 * rY - pY) > 2 * RTOL_ROW * rY
+    assert clear.sum() >= 0.9 * len(rows)
+    np.testing.assert_array_equal(np.asarray(acc_g)[rows][clear].astype(bool), (u1 * rY < pY)[clear])
+
+
 def run_gpu_step(w, s_max=0, want_residual=True):
     out = mdss.step(dev(w["p"]), dev(w["q"]), dev(w["drafts"]), dev(w["u"]), s_max=s_max,
                     want_residual=want_residual)
@@ -81,8 +138,10 @@ def test_tiny_end_to_end():
     assert np.array_equal(g["sel_index"], ref["sel_index"])
     assert np.array_equal(g["sel_token"], ref["sel_token"])
     assert np.all(g["status"] == 0) and np.all(ref["status"] == 0)
-    # step 2 on the GPU's own r
-    check_step2(w["p"], g["r"], g["sel_token"], w["u"], g["out_token"], g["accepted"], g["residual"], g["mass"])
+    # step 2: the GPU's outputs against Algorithm 1, and both sides on the oracle's r
+    check_step2_invariants(w["p"], g["r"], g["sel_token"], w["u"], g["out_token"], g["accepted"], g["residual"],
+                           g["mass"])
+    step2_common(w["p"], ref["r32"], ref["sel_token"], w["u"])
     # end to end against the oracle's r: tokens may differ only inside the r-error window
     window = np.abs(g["r"].astype(np.float64) - ref["r"]).sum(1) / np.maximum(ref["mass"], 1e-300)
     agree = g["out_token"] == ref["out_token"]
@@ -123,8 +182,14 @@ def test_full_size(name):
     # selection bit-exact at every row
     si, stok, st = oracle.select(p, q, w["drafts"], w["u"])
     assert np.array_equal(g["sel_index"], si) and np.array_equal(g["sel_token"], stok)
-    # step 2 at every row on the GPU's r
-    check_step2(p, g["r"], g["sel_token"], w["u"], g["out_token"], g["accepted"], g["residual"], g["mass"])
+    # step 2: Algorithm 1 on the GPU's own r at every row, the accept decisions of
+    # sampled rows against the oracle's r at the selected token, and both sides at
+    # the full size on a common stand-in proposal
+    check_step2_invariants(p, g["r"], g["sel_token"], w["u"], g["out_token"], g["accepted"], g["residual"], g["mass"])
+    rows2 = rng.choice(B, size=min(B, 64 if K == 2 else 32), replace=False)
+    check_accept_at_selected(p, w["u"], rows2, stok[rows2],
+                             oracle.induced_dist_entries(p, q, K, rows2, stok[rows2]), g["accepted"])
+    step2_common(p, proposal_rows(p, q, cfg.seed, K), stok, w["u"])
 
 
 def test_llm32k_rows_full_oracle():
@@ -268,11 +333,12 @@ def test_philox_uniforms_in_kernel():
     pg, qg = dev(w["p"]), dev(w["q"])
     si, stok = mdss.select_intermediate(pg, qg, dev(w["drafts"]), None, seed=seed, offset=offset)
     osi, ostok, _ = oracle.select(w["p"], w["q"], w["drafts"], u)
-    assert np.array_equal(si.cpu().numpy(), osi)
-    r = mdss.induced_dist(pg, qg, 2)
-    out, acc, _, _ = mdss.accept_or_resample(pg, r, stok, None, seed=seed, offset=offset)
+    assert np.array_equal(si.cpu().numpy(), osi) and np.array_equal(stok.cpu().numpy(), ostok)
+    ro, _ = oracle.induced_dist(w["p"], w["q"], 2)
+    r32 = ro.astype(np.float32)
+    out, acc, _, _ = mdss.accept_or_resample(pg, dev(r32), dev(ostok), None, seed=seed, offset=offset)
     torch.cuda.synchronize()
-    check_step2(w["p"], r.cpu().numpy(), ostok, u, out.cpu().numpy(), acc.cpu().numpy())
+    check_step2(w["p"], r32, ostok, u, out.cpu().numpy(), acc.cpu().numpy())
 
 
 def test_unaligned_and_ragged_rows():

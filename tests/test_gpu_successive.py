@@ -1,6 +1,9 @@
 """GPU parity of successive pairwise selection (Remark 4) through the C ABI,
 against oracle/successive.py.  Stage laws within 1e-5 relative L1 per row;
-selection bit-exact on common stage laws.  Notation: p = target, q = draft."""
+selection bit-exact on common stage laws (the oracle's, handed to both sides);
+the whole step's selection from the GPU's own laws equal to the oracle's except
+at decisions within the law tolerance of their boundary.  Notation: p = target,
+q = draft."""
 import numpy as np
 import pytest
 import torch
@@ -8,7 +11,7 @@ import torch
 import oracle
 import paper_2410_18234_amd as mdss
 from oracle import successive as succ
-from test_gpu_parity import RTOL_ROW, check_step2, dev, rel_l1
+from test_gpu_parity import RTOL_ROW, check_step2_invariants, dev, rel_l1, step2_common
 from workloads import generate
 
 pytestmark = pytest.mark.gpu
@@ -52,9 +55,9 @@ def test_small_rows(K):
     d = _drafts(q, K, rng)
     u_sel = (rng.integers(0, 1 << 24, (64, K - 1)) / float(1 << 24)).astype(np.float32)
     sti = torch.zeros(64, dtype=torch.int32, device="cuda:0")
-    si, stok = mdss.select_successive(dev(p), dev(q), dev(rs), dev(d), dev(u_sel), row_status=sti)
+    si, stok = mdss.select_successive(dev(p), dev(q), dev(np.stack(ro)), dev(d), dev(u_sel), row_status=sti)
     torch.cuda.synchronize()
-    osi, ost, ostat = succ.select(p, q, list(rs), d, u_sel)
+    osi, ost, ostat = succ.select(p, q, ro, d, u_sel)
     np.testing.assert_array_equal(si.cpu().numpy(), osi)
     np.testing.assert_array_equal(stok.cpu().numpy(), ost)
     np.testing.assert_array_equal(sti.cpu().numpy(), ostat)
@@ -70,9 +73,9 @@ def test_k2_chain_is_k2_path():
 def test_philox_stage_uniforms():
     p, q, rng = _rows(600, 40, 17)
     K, seed, offset = 4, 0x1234ABCD5678, 77
-    rs, _ = gpu_stages(p, q, K)
+    ro, _ = succ.stage_dists(p, q, K)
     d = _drafts(q, K, rng)
-    si, stok = mdss.select_successive(dev(p), dev(q), dev(rs), dev(d), None, seed=seed, offset=offset)
+    si, stok = mdss.select_successive(dev(p), dev(q), dev(np.stack(ro)), dev(d), None, seed=seed, offset=offset)
     torch.cuda.synchronize()
     u_sel = np.zeros((40, K - 1), np.float32)
     for b in range(40):
@@ -80,9 +83,27 @@ def test_philox_stage_uniforms():
         for j in range(1, K):
             c = oracle.philox4x32_10([pos & 0xFFFFFFFF, pos >> 32, j, 0], [seed & 0xFFFFFFFF, seed >> 32])
             u_sel[b, j - 1] = np.float32((int(c[0]) >> 8) * 2.0 ** -24)
-    osi, ost, _ = succ.select(p, q, list(rs), d, u_sel)
+    osi, ost, _ = succ.select(p, q, ro, d, u_sel)
     np.testing.assert_array_equal(si.cpu().numpy(), osi)
     np.testing.assert_array_equal(stok.cpu().numpy(), ost)
+
+
+def _min_margin(p, q, r_stages, drafts, u_sel, b):
+    """Smallest relative distance of u (wa + wb) to wa over the stages of row b
+    along the oracle's chain (where a law error can flip a decision)."""
+    x = [int(t) for t in drafts[b]]
+    y, best = x[0], np.inf
+    for j in range(1, len(x)):
+        law = q[b] if j == 1 else r_stages[j - 2][b]
+        if not float(law[y]) > 0:
+            return 0.0
+        wa = float(p[b, y]) / float(law[y])
+        wb = float(p[b, x[j]]) / float(q[b, x[j]])
+        t = float(u_sel[b, j - 1]) * (wa + wb)
+        best = min(best, abs(t - wa) / max(wa + wb, 1e-300))
+        if not t < wa:
+            y = x[j]
+    return best
 
 
 def test_full_size_k3top1024():
@@ -97,11 +118,16 @@ def test_full_size_k3top1024():
     u_sel = (rng.integers(0, 1 << 24, (p.shape[0], 2)) / float(1 << 24)).astype(np.float32)
     g = mdss.step_successive(dev(p), dev(q), dev(d), dev(u_sel), dev(u), want_residual=True)
     torch.cuda.synchronize()
-    osi, ost, _ = succ.select(p, q, list(rs), d, u_sel)
-    np.testing.assert_array_equal(g["sel_index"].cpu().numpy(), osi)
-    np.testing.assert_array_equal(g["sel_token"].cpu().numpy(), ost)
-    check_step2(p, rs[1], ost, u, g["out_token"].cpu().numpy(), g["accepted"].cpu().numpy(),
-                g["residual"].cpu().numpy(), g["mass"].cpu().numpy())
+    g = {k: v.cpu().numpy() for k, v in g.items() if v is not None}
+    # the whole step's selection (from the GPU's laws) against the oracle's chain
+    osi, ost, _ = succ.select(p, q, ro, d, u_sel)
+    diff = np.flatnonzero(g["sel_index"] != osi)
+    assert len(diff) <= 2, diff
+    for b in diff:
+        assert _min_margin(p, q, ro, d, u_sel, b) < 4 * RTOL_ROW, b
+    # step 2: Algorithm 1 on the GPU's last law, and both sides on the oracle's
+    check_step2_invariants(p, g["r"], g["sel_token"], u, g["out_token"], g["accepted"], g["residual"], g["mass"])
+    step2_common(p, ro[-1], ost, u)
 
 
 def test_full_vocab_sampled_entries():
@@ -114,9 +140,15 @@ def test_full_vocab_sampled_entries():
     ys = rng.integers(0, p.shape[1], 96)
     ys[:32] = [int(np.argmax(rs[1][b])) for b in rows[:32]]
     e1 = oracle.induced_dist_entries(p, q, 2, rows, ys)
-    e2 = oracle.induced_dist_pair_entries(p, rs[0], q, rows, ys)  # stage 2 from the GPU's stage-1 law
     assert np.all(np.abs(rs[0][rows, ys] - e1) <= RTOL_ROW * e1)
-    assert np.all(np.abs(rs[1][rows, ys] - e2) <= RTOL_ROW * e2)
+    # stage 2 needs a whole stage-1 law: the oracle's, on three rows
+    few = np.array([0, 5, 11])
+    r1o, _ = oracle.induced_dist(p[few], q[few], 2)
+    loc = rng.integers(0, 3, 48)
+    ys2 = rng.integers(0, p.shape[1], 48)
+    ys2[:16] = [int(np.argmax(rs[1][few[i]])) for i in loc[:16]]
+    e2 = oracle.induced_dist_pair_entries(p[few], r1o.astype(np.float32), q[few], loc, ys2)
+    assert np.all(np.abs(rs[1][few[loc], ys2] - e2) <= RTOL_ROW * e2)
     mass = q.astype(np.float64).sum(1)
     assert np.all(np.abs(rs[1].astype(np.float64).sum(1) - rs[0].astype(np.float64).sum(1) * mass) <= 1e-5 * mass)
 
@@ -133,8 +165,8 @@ def test_invalid_rows_and_drafts():
     q[4, d[4, 2]] = 0.0    # drafted token with q = 0
     u_sel = np.full((6, 2), 0.5, np.float32)
     sti = torch.zeros(6, dtype=torch.int32, device="cuda:0")
-    si, stok = mdss.select_successive(dev(p), dev(q), dev(rs), dev(d), dev(u_sel), row_status=sti)
+    si, stok = mdss.select_successive(dev(p), dev(q), dev(np.stack(ro)), dev(d), dev(u_sel), row_status=sti)
     torch.cuda.synchronize()
-    osi, ost, ostat = succ.select(p, q, list(rs), d, u_sel)
+    osi, ost, ostat = succ.select(p, q, ro, d, u_sel)
     np.testing.assert_array_equal(si.cpu().numpy(), osi)
     np.testing.assert_array_equal(sti.cpu().numpy(), ostat)

@@ -14,7 +14,7 @@ Every row is generated from its own ``numpy.random.Generator(PCG64(SeedSequence(
 [seed, stream, row])))`` so that any subset of rows can be regenerated on its
 own.  Streams: 0 logits / Dirichlet draw of p, 1 noise / Dirichlet draw of q,
 2 permutation, 3 drafts, 4 uniforms, 5 noise of a second draft distribution,
-6 tokens of the second draft.
+6 tokens of the second draft, 7 stand-in proposals, 8 stand-in pair tables.
 
 Values are produced in fp64 (softmax in fp64) and cast to fp32, without any
 renormalisation after the cast.  Drafted tokens are drawn i.i.d. from the fp32
@@ -28,9 +28,10 @@ from typing import Callable, Dict, Optional, Sequence
 
 import numpy as np
 
-__all__ = ["Config", "CONFIGS", "generate", "uniforms24", "draw_drafts"]
+__all__ = ["Config", "CONFIGS", "generate", "uniforms24", "draw_drafts", "proposal_rows", "pair_tables"]
 
 _S_LOGIT, _S_NOISE, _S_PERM, _S_DRAFT, _S_UNIF, _S_NOISE2, _S_DRAFT2 = 0, 1, 2, 3, 4, 5, 6
+_S_PROPOSAL, _S_TABLE = 7, 8
 
 
 def _rng(seed: int, stream: int, row: int) -> np.random.Generator:
@@ -206,4 +207,42 @@ def dirichlet_instances(seed: int, V: int, count: int, alpha: float = 0.5):
     for i in range(count):
         g = _rng(seed, V, i)
         out.append((g.dirichlet(np.full(V, alpha)), g.dirichlet(np.full(V, alpha))))
+    return out
+
+
+def proposal_rows(p32: np.ndarray, q32: np.ndarray, seed: int, mass_power: int = 2,
+                  spread: float = 0.5) -> np.ndarray:
+    """A seeded stand-in for the proposal an accept / resample step reads (fp32
+    [n][V]): positive exactly where q > 0, a log-normal perturbation of (p + q) / 2
+    there, scaled to total mass (sum q)**mass_power.  Random shape only: it lets
+    a test hand the same proposal to both sides of a comparison."""
+    p64 = np.asarray(p32, np.float32).astype(np.float64)
+    q64 = np.asarray(q32, np.float32).astype(np.float64)
+    out = np.zeros(q64.shape, np.float32)
+    for b in range(q64.shape[0]):
+        g = _rng(seed, _S_PROPOSAL, b)
+        v = 0.5 * (p64[b] + q64[b]) * np.exp(spread * g.standard_normal(q64.shape[1]))
+        v[~(q64[b] > 0)] = 0.0
+        v *= q64[b].sum() ** mass_power / v.sum()
+        out[b] = v.astype(np.float32)
+    return out
+
+
+def pair_tables(seed: int, n: int, s: int, size: int = 16) -> np.ndarray:
+    """Seeded stand-in selection tables (fp64 [n][size][size]) of the form the
+    truncated linear program hands to its selection step: for a < b < s the entry
+    w[a][b] is a 24-bit dyadic in [0, 1] (exact 0 and 1 included), w[b][a] =
+    1 - w[a][b], ones on the diagonal up to s, zeros elsewhere."""
+    out = np.zeros((n, size, size), np.float64)
+    for i in range(n):
+        g = _rng(seed, _S_TABLE, i)
+        k = g.integers(0, (1 << 24) + 1, size=(s, s)).astype(np.float64)
+        k[g.random((s, s)) < 0.15] = 0.0
+        k[g.random((s, s)) < 0.15] = float(1 << 24)
+        w = k / float(1 << 24)
+        for a in range(s):
+            out[i, a, a] = 1.0
+            for b in range(a + 1, s):
+                out[i, a, b] = w[a, b]
+                out[i, b, a] = 1.0 - w[a, b]
     return out
