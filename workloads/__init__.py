@@ -145,6 +145,12 @@ CONFIGS: Dict[str, Config] = {
         Config("opt_llm32k", 1002, 256, 32000, 2,
                "optimal acceptance P* (Theorem 3) and the acceptance of the importance-weighted proposal per "
                "position, on the llm32k rows", _row_gauss(3.0, 1.0, 1.0), diag=True),
+        Config("maxvocab", 1007, 2, 1 << 23, 2,
+               "the longest accepted row: V = 2^23 tokens, K=2, 2 positions, logits N(0,3^2), draft noise N(0,1)",
+               _row_gauss(3.0, 1.0, 1.0)),
+        Config("maxbatch", 1008, 65535, 16, 2,
+               "the largest accepted batch: 65535 positions, V=16, K=2, p and q independent Dirichlet(0.5)",
+               _row_dirichlet),
         Config("tlp_llm32k", 1002, 256, 32000, 2,
                "truncated LP (Algorithm 2), s = 5, sorted Omega_2, identical drafts, on the llm32k rows",
                _row_gauss(3.0, 1.0, 1.0), tlp_s=5),
