@@ -28,6 +28,10 @@
  *   - Argument errors (null pointer, bad size, K or workspace) are returned
  *     synchronously before anything is launched, and nothing is written.
  *     A failed launch returns MDSS_EDEVICE.
+ *   - B = 0 is an empty batch: once the sizes and the other parameters
+ *     (K, s_max, s, tail, m) have been checked, the call returns MDSS_OK
+ *     without reading, writing or launching anything; its pointers and its
+ *     workspace may then be NULL, and the workspace-size queries return 0.
  *   - Per-row data problems are reported in row_status[b] (nullable), as bits
  *     OR-ed into the existing value: the caller zeroes row_status before the
  *     first call of a step.  A flagged row gets r = NaN and token -1.
@@ -51,7 +55,7 @@ extern "C" {
 typedef enum mdss_status {
   MDSS_OK = 0,
   MDSS_EINVAL = 1,       /* null pointer or invalid argument value */
-  MDSS_ESHAPE = 2,       /* B outside [1, MDSS_MAX_B] or V outside [2, MDSS_MAX_V] */
+  MDSS_ESHAPE = 2,       /* B outside [0, MDSS_MAX_B] or V outside [2, MDSS_MAX_V] */
   MDSS_EUNSUPPORTED = 3, /* K outside {2, 3} (outside [2, MDSS_SUCCESSIVE_MAX_K] for the successive
                             calls), K = 3 with s_max outside [1, MDSS_K3_MAX_SUPPORT], or a
                             truncated-LP s outside [1, MDSS_TLP_MAX_S] */
@@ -71,7 +75,7 @@ typedef enum mdss_status {
 #define MDSS_K3_MAX_SUPPORT 4096 /* largest s_max accepted for K = 3 */
 
 /* Bytes of device workspace mdss_induced_dist needs for these sizes
- * (0 if the arguments are invalid).  The workspace is caller-owned scratch:
+ * (0 if the arguments are invalid or B = 0).  The workspace is caller-owned scratch:
  * its content on entry is ignored and on exit is unspecified. */
 size_t mdss_workspace_bytes(int64_t B, int64_t V, int32_t K, int32_t s_max);
 
@@ -160,7 +164,7 @@ mdss_status mdss_select_intermediate_pair(const float* p, const float* q1, const
  * pair sums of O(n^2) per row, against O(n^K) for the direct K-draft rule. */
 #define MDSS_SUCCESSIVE_MAX_K 8
 
-/* Workspace bytes of mdss_induced_dist_successive (0 if the shape is invalid). */
+/* Workspace bytes of mdss_induced_dist_successive (0 if the shape is invalid or B = 0). */
 size_t mdss_workspace_bytes_successive(int64_t B, int64_t V);
 
 /* r_stages: [K-1][B][V] fp32 out, stage j (1-based) at offset (j-1) B V; the
@@ -226,7 +230,7 @@ mdss_status mdss_alphabet_post(const float* p, const float* p_trunc, const doubl
  * row, fp64 sums. */
 #define MDSS_OPTIMUM_MAX_K 8
 
-/* Workspace bytes of mdss_optimal_acceptance (0 if the shape is invalid). */
+/* Workspace bytes of mdss_optimal_acceptance (0 if the shape is invalid or B = 0). */
 size_t mdss_workspace_bytes_optimum(int64_t B, int64_t V);
 
 /* pstar [B] fp64 out: the value above for K in [2, MDSS_OPTIMUM_MAX_K];
@@ -272,7 +276,7 @@ mdss_status mdss_acceptance(const float* p, const float* r, int64_t B, int64_t V
 #define MDSS_TLP_SORTED 0
 #define MDSS_TLP_HALF 1
 
-/* Workspace bytes of mdss_truncated_lp (0 if the arguments are invalid). */
+/* Workspace bytes of mdss_truncated_lp (0 if the arguments are invalid or B = 0). */
 size_t mdss_workspace_bytes_tlp(int64_t B, int64_t V, int32_t tail);
 
 /* p, q1 (and q2 unless NULL): [B][V] fp32 in.  s in [1, MDSS_TLP_MAX_S], tail

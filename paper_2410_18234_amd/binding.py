@@ -158,7 +158,7 @@ def induced_dist(p: torch.Tensor, q: torch.Tensor, K: int, s_max: int = 0, r: Op
     if row_status is not None:
         _need(row_status, "row_status", torch.int32, (B,), dev)
     need = int(lib.mdss_workspace_bytes(B, V, K, s_max))
-    if need == 0:
+    if need == 0 and B > 0:
         _check("mdss_workspace_bytes", 3 if K not in (2, 3) or (K == 3 and not 1 <= s_max <= 4096) else 2)
     if workspace is None:
         workspace = _workspace(dev, need)
@@ -231,7 +231,7 @@ def induced_dist_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, r: Op
     if row_status is not None:
         _need(row_status, "row_status", torch.int32, (B,), dev)
     need = int(lib.mdss_workspace_bytes_pair(B, V))
-    if need == 0:
+    if need == 0 and B > 0:
         _check("mdss_workspace_bytes_pair", 2)
     if workspace is None:
         workspace = _workspace(dev, need)
@@ -319,7 +319,7 @@ def truncated_lp(p: torch.Tensor, q1: torch.Tensor, q2: Optional[torch.Tensor] =
     if row_status is not None:
         _need(row_status, "row_status", torch.int32, (B,), dev)
     need = int(lib.mdss_workspace_bytes_tlp(B, V, tail))
-    if need == 0:
+    if need == 0 and B > 0:
         _check("mdss_workspace_bytes_tlp", 1 if tail not in (MDSS_TLP_SORTED, MDSS_TLP_HALF) else 2)
     if workspace is None:
         workspace = _workspace(dev, need)
@@ -391,7 +391,7 @@ def induced_dist_successive(p: torch.Tensor, q: torch.Tensor, K: int, r_stages: 
     if row_status is not None:
         _need(row_status, "row_status", torch.int32, (B,), dev)
     need = int(lib.mdss_workspace_bytes_successive(B, V))
-    if need == 0:
+    if need == 0 and B > 0:
         _check("mdss_workspace_bytes_successive", 2)
     if workspace is None:
         workspace = _workspace(dev, need)
@@ -453,7 +453,7 @@ def optimal_acceptance(p: torch.Tensor, q: torch.Tensor, K: int = 2, row_status:
     if row_status is not None:
         _need(row_status, "row_status", torch.int32, (B,), dev)
     need = int(lib.mdss_workspace_bytes_optimum(B, V))
-    if need == 0:
+    if need == 0 and B > 0:
         _check("mdss_workspace_bytes_optimum", 2)
     if workspace is None:
         workspace = _workspace(dev, need)

@@ -57,7 +57,7 @@ def test_induced_dist_argument_errors(lib):
     f = lib.mdss_induced_dist
     ws_ok = lib.mdss_workspace_bytes(4, 16, 2, 0)
     assert f(None, FAKE, 4, 16, 2, 0, FAKE, None, FAKE, ws_ok, None) == 1
-    assert f(FAKE, FAKE, 0, 16, 2, 0, FAKE, None, FAKE, ws_ok, None) == 2
+    assert f(FAKE, FAKE, -1, 16, 2, 0, FAKE, None, FAKE, ws_ok, None) == 2
     assert f(FAKE, FAKE, 4, 1, 2, 0, FAKE, None, FAKE, ws_ok, None) == 2
     assert f(FAKE, FAKE, 4, 16, 5, 0, FAKE, None, FAKE, ws_ok, None) == 3
     assert f(FAKE, FAKE, 4, 16, 3, 0, FAKE, None, FAKE, ws_ok, None) == 3
@@ -118,7 +118,7 @@ def test_successive_and_tlp_argument_errors(lib):
     assert t(FAKE, FAKE, None, 4, 16, 0, 0, FAKE, FAKE, FAKE, None, None, FAKE, wt, None) == 3
     assert t(FAKE, FAKE, None, 4, 16, 17, 0, FAKE, FAKE, FAKE, None, None, FAKE, wt, None) == 3
     assert t(FAKE, FAKE, None, 4, 16, 5, 0, FAKE, FAKE, FAKE, None, None, FAKE, wt - 1, None) == 5
-    assert t(FAKE, FAKE, None, 0, 16, 5, 0, FAKE, FAKE, FAKE, None, None, FAKE, wt, None) == 2
+    assert t(FAKE, FAKE, None, -1, 16, 5, 0, FAKE, FAKE, FAKE, None, None, FAKE, wt, None) == 2
     sel = lib.mdss_select_truncated_lp
     assert sel(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 5, 0, None, FAKE, FAKE, FAKE, None, None) == 1
     assert sel(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 17, 0, FAKE, FAKE, FAKE, FAKE, None, None) == 3
@@ -142,7 +142,35 @@ def test_alphabet_argument_errors(lib):
     t = lib.mdss_truncate_alphabet
     assert t(FAKE, 4, 16, 0, FAKE, FAKE, None, None) == 1
     assert t(None, 4, 16, 3, FAKE, FAKE, None, None) == 1
-    assert t(FAKE, 0, 16, 3, FAKE, FAKE, None, None) == 2
+    assert t(FAKE, -1, 16, 3, FAKE, FAKE, None, None) == 2
     a = lib.mdss_alphabet_post
     assert a(FAKE, FAKE, FAKE, None, None, 0, 0, 4, 16, FAKE, FAKE, None) == 1
     assert a(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 1, FAKE, FAKE, None) == 2
+
+
+def test_empty_batch_is_a_no_op(lib):
+    # B = 0: sizes and parameters are still checked, then nothing is read, written or launched,
+    # so NULL pointers and a NULL workspace are accepted (no device is touched)
+    N = None
+    for ws in ("mdss_workspace_bytes_pair", "mdss_workspace_bytes_successive", "mdss_workspace_bytes_optimum"):
+        assert getattr(lib, ws)(0, 16) == 0
+    assert lib.mdss_workspace_bytes(0, 16, 2, 0) == 0 and lib.mdss_workspace_bytes_tlp(0, 16, 0) == 0
+    assert lib.mdss_induced_dist(N, N, 0, 16, 2, 0, N, N, N, 0, N) == 0
+    assert lib.mdss_induced_dist(N, N, 0, 16, 4, 0, N, N, N, 0, N) == 3          # K still checked
+    assert lib.mdss_induced_dist(N, N, 0, 1, 2, 0, N, N, N, 0, N) == 2           # V still checked
+    assert lib.mdss_induced_dist_pair(N, N, N, 0, 16, N, N, N, 0, N) == 0
+    assert lib.mdss_select_intermediate(N, N, N, N, 0, 0, 0, 16, 2, N, N, N, N) == 0
+    assert lib.mdss_select_intermediate_pair(N, N, N, N, N, 0, 0, 0, 16, N, N, N, N) == 0
+    assert lib.mdss_accept_or_resample(N, N, N, N, 0, 0, 0, 16, N, N, N, N, N, N) == 0
+    assert lib.mdss_induced_dist_successive(N, N, 0, 16, 3, N, N, N, 0, N) == 0
+    assert lib.mdss_induced_dist_successive(N, N, 0, 16, 9, N, N, N, 0, N) == 3
+    assert lib.mdss_select_successive(N, N, N, N, N, 0, 0, 0, 16, 3, N, N, N, N) == 0
+    assert lib.mdss_truncate_alphabet(N, 0, 16, 3, N, N, N, N) == 0
+    assert lib.mdss_truncate_alphabet(N, 0, 16, 0, N, N, N, N) == 1             # m still checked
+    assert lib.mdss_alphabet_post(N, N, N, N, N, 0, 0, 0, 16, N, N, N) == 0
+    assert lib.mdss_optimal_acceptance(N, N, 0, 16, 2, N, N, N, N, 0, N) == 0
+    assert lib.mdss_acceptance(N, N, 0, 16, N, N, N) == 0
+    assert lib.mdss_truncated_lp(N, N, N, 0, 16, 5, 0, N, N, N, N, N, N, 0, N) == 0
+    assert lib.mdss_truncated_lp(N, N, N, 0, 16, 17, 0, N, N, N, N, N, N, 0, N) == 3
+    assert lib.mdss_truncated_lp(N, N, N, 0, 16, 5, 2, N, N, N, N, N, N, 0, N) == 1
+    assert lib.mdss_select_truncated_lp(N, N, N, N, N, 0, 0, 0, 16, 5, 0, N, N, N, N, N, N) == 0
