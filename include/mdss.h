@@ -56,9 +56,10 @@ typedef enum mdss_status {
   MDSS_OK = 0,
   MDSS_EINVAL = 1,       /* null pointer or invalid argument value */
   MDSS_ESHAPE = 2,       /* B outside [0, MDSS_MAX_B] or V outside [2, MDSS_MAX_V] */
-  MDSS_EUNSUPPORTED = 3, /* K outside {2, 3} (outside [2, MDSS_SUCCESSIVE_MAX_K] for the successive
-                            calls), K = 3 with s_max outside [1, MDSS_K3_MAX_SUPPORT], or a
-                            truncated-LP s outside [1, MDSS_TLP_MAX_S] */
+  MDSS_EUNSUPPORTED = 3, /* K outside {2, 3} for mdss_induced_dist, outside [2, MDSS_MAX_K] for
+                            the selection and the exponential-sum calls (MDSS_SUCCESSIVE_MAX_K for
+                            the successive calls), K = 3 with s_max outside [1, MDSS_K3_MAX_SUPPORT],
+                            or a truncated-LP s outside [1, MDSS_TLP_MAX_S] */
   MDSS_EDEVICE = 4,      /* a HIP call or kernel launch failed */
   MDSS_EWORKSPACE = 5    /* workspace missing or smaller than mdss_workspace_bytes() */
 } mdss_status;
@@ -69,10 +70,13 @@ typedef enum mdss_status {
 #define MDSS_ROW_SUPPORT 4   /* K = 3: more than s_max tokens with q > 0 */
 #define MDSS_ROW_FORCED 8    /* rejection with zero residual mass: the selected token is output */
 #define MDSS_ROW_LP_LIMIT 16 /* truncated LP stopped after its augmentation limit (result feasible, maybe not optimal) */
+#define MDSS_ROW_RANGE 32    /* exponential-sum calls: the row's positive weights span more than 2^300 (possible
+                                only with probabilities far above 1); r = NaN */
 
 #define MDSS_MAX_V 8388608LL /* rows longer than 2^23 tokens are rejected with MDSS_ESHAPE */
 #define MDSS_MAX_B 65535LL   /* at most 65535 positions per call */
 #define MDSS_K3_MAX_SUPPORT 4096 /* largest s_max accepted for K = 3 */
+#define MDSS_MAX_K 8         /* largest K of the direct K-draft selection and of mdss_induced_dist_expsum */
 
 /* Bytes of device workspace mdss_induced_dist needs for these sizes
  * (0 if the arguments are invalid or B = 0).  The workspace is caller-owned scratch:
@@ -107,7 +111,7 @@ mdss_status mdss_induced_dist(const float* p, const float* q, int64_t B, int64_t
  * smallest i with u_sel * W < C_i, or floor(u_sel * K) when W = 0.
  * sel_index and sel_token ([B] int32 out) receive i (0-based) and x_i, or -1
  * for a row whose drafts are invalid (MDSS_ROW_BAD_DRAFT / MDSS_ROW_BAD_PROB).
- * u may be NULL (Philox, see above).  K in {2, 3}. */
+ * u may be NULL (Philox, see above).  K in [2, MDSS_MAX_K]. */
 mdss_status mdss_select_intermediate(const float* p, const float* q, const int32_t* drafts, const float* u,
                                      uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
                                      int32_t* sel_index, int32_t* sel_token, int32_t* row_status, void* stream);
@@ -189,6 +193,51 @@ mdss_status mdss_select_successive(const float* p, const float* q, const float* 
                                    const float* u_sel, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
                                    int32_t K, int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
                                    void* stream);
+
+/* ---- Induced distribution by an exponential-sum quadrature ---------------
+ * The same r as mdss_induced_dist (K i.i.d. drafts), mdss_induced_dist_pair
+ * (two draft laws) and mdss_induced_dist_successive (successive pairwise),
+ * evaluated in O(n) per node instead of O(n^K) per row.  Every denominator D
+ * of those sums (a sum of positive weights) enters through
+ *   1/D = integral over t of exp(t - D e^t) dt,
+ * so for K i.i.d. drafts
+ *   r(y) = K p(y) integral of e^t exp(-e^t w(y)) S(e^t)^(K-1) dt,
+ *   S(a) = sum_{x in supp q} q(x) exp(-a w(x)),
+ * and the two-law sums factor the same way.  The integral is taken by the
+ * trapezoidal rule with step 1/2 on t, cut where both tails are below 1e-8
+ * of every denominator of the row: about (ln(D_max/D_min) + 21.3) * 2 nodes
+ * (60 on LLM-like rows).  Relative error of every entry: at most 2 sum_m
+ * |Gamma(1 + 4 pi i m)| + 2e-8 = 7e-8 for the rule (all terms are positive)
+ * plus fp32 rounding (rows whose weights span more than 2^180 are evaluated in
+ * fp64).  The zero-weight closed forms are the ones stated above.  Any K in
+ * [2, MDSS_MAX_K] (no support cap).  A row whose weights span more than 2^300
+ * is flagged MDSS_ROW_RANGE (r = NaN); other flags and outputs as
+ * mdss_induced_dist.  Workspace: caller-owned, 256-byte aligned. */
+
+/* Bytes of workspace for mdss_induced_dist_expsum (0 if the arguments are invalid or B = 0). */
+size_t mdss_workspace_bytes_expsum(int64_t B, int64_t V, int32_t K);
+
+/* r: [B][V] fp32 out, the induced distribution of K i.i.d. drafts from q with
+ * the classical weights (as mdss_induced_dist, for any K in [2, MDSS_MAX_K]). */
+mdss_status mdss_induced_dist_expsum(const float* p, const float* q, int64_t B, int64_t V, int32_t K, float* r,
+                                     int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace for mdss_induced_dist_pair_expsum and
+ * mdss_induced_dist_successive_expsum (0 if the shape is invalid or B = 0). */
+size_t mdss_workspace_bytes_pair_expsum(int64_t B, int64_t V);
+
+/* r: [B][V] fp32 out, the induced distribution of X1 ~ q1, X2 ~ q2 (as
+ * mdss_induced_dist_pair). */
+mdss_status mdss_induced_dist_pair_expsum(const float* p, const float* q1, const float* q2, int64_t B, int64_t V,
+                                          float* r, int32_t* row_status, void* workspace, size_t workspace_bytes,
+                                          void* stream);
+
+/* r_stages: [K-1][B][V] fp32 out, the stage laws of successive pairwise
+ * selection (as mdss_induced_dist_successive), K in [2, MDSS_SUCCESSIVE_MAX_K].
+ * workspace: at least mdss_workspace_bytes_pair_expsum(B, V) bytes. */
+mdss_status mdss_induced_dist_successive_expsum(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
+                                                float* r_stages, int32_t* row_status, void* workspace,
+                                                size_t workspace_bytes, void* stream);
 
 /* ---- Truncated alphabet ---------------------------------------------------
  * Section 4 (after the truncated LP): Omega_0 = the m tokens of largest target

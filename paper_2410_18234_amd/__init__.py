@@ -15,6 +15,8 @@ from .binding import (  # noqa: F401
     MDSS_ROW_BAD_PROB,
     MDSS_ROW_FORCED,
     MDSS_ROW_LP_LIMIT,
+    MDSS_ROW_RANGE,
+    MDSS_MAX_K,
     MDSS_OPTIMUM_MAX_K,
     MDSS_ROW_SUPPORT,
     MDSS_SUCCESSIVE_MAX_K,
@@ -26,8 +28,11 @@ from .binding import (  # noqa: F401
     alphabet_post,
     acceptance,
     induced_dist,
+    induced_dist_expsum,
     induced_dist_pair,
+    induced_dist_pair_expsum,
     induced_dist_successive,
+    induced_dist_successive_expsum,
     library_path,
     load_library,
     optimal_acceptance,
@@ -43,6 +48,8 @@ from .binding import (  # noqa: F401
     truncate_alphabet,
     truncated_lp,
     workspace_bytes,
+    workspace_bytes_expsum,
+    workspace_bytes_pair_expsum,
     workspace_bytes_optimum,
     workspace_bytes_pair,
     workspace_bytes_successive,

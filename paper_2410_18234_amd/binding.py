@@ -22,6 +22,8 @@ MDSS_ROW_BAD_DRAFT = 2
 MDSS_ROW_SUPPORT = 4
 MDSS_ROW_FORCED = 8
 MDSS_ROW_LP_LIMIT = 16
+MDSS_ROW_RANGE = 32
+MDSS_MAX_K = 8
 MDSS_TLP_MAX_S = 16
 MDSS_TLP_SORTED = 0
 MDSS_TLP_HALF = 1
@@ -81,8 +83,16 @@ def load_library():
         lib.mdss_workspace_bytes_optimum.restype = sz
         lib.mdss_optimal_acceptance.argtypes = [P, P, i64, i64, i32, P, P, P, P, sz, P]
         lib.mdss_acceptance.argtypes = [P, P, i64, i64, P, P, P]
+        lib.mdss_workspace_bytes_expsum.argtypes = [i64, i64, i32]
+        lib.mdss_workspace_bytes_expsum.restype = sz
+        lib.mdss_induced_dist_expsum.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P]
+        lib.mdss_workspace_bytes_pair_expsum.argtypes = [i64, i64]
+        lib.mdss_workspace_bytes_pair_expsum.restype = sz
+        lib.mdss_induced_dist_pair_expsum.argtypes = [P, P, P, i64, i64, P, P, P, sz, P]
+        lib.mdss_induced_dist_successive_expsum.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P]
         for f in ("mdss_induced_dist_successive", "mdss_select_successive", "mdss_optimal_acceptance",
-                  "mdss_acceptance"):
+                  "mdss_acceptance", "mdss_induced_dist_expsum", "mdss_induced_dist_pair_expsum",
+                  "mdss_induced_dist_successive_expsum"):
             getattr(lib, f).restype = ctypes.c_int
         for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample",
                   "mdss_induced_dist_pair", "mdss_select_intermediate_pair", "mdss_truncated_lp",
@@ -265,11 +275,17 @@ def select_intermediate_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor
 
 
 def step_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, drafts: torch.Tensor,
-              u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False):
-    """The whole path for two drafts from different distributions."""
+              u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False,
+              method: str = "exact"):
+    """The whole path for two drafts from different distributions (method as in step)."""
     B = p.shape[0]
     status = torch.zeros(B, dtype=torch.int32, device=p.device)
-    r = induced_dist_pair(p, q1, q2, row_status=status)
+    if method == "expsum":
+        r = induced_dist_pair_expsum(p, q1, q2, row_status=status)
+    elif method == "exact":
+        r = induced_dist_pair(p, q1, q2, row_status=status)
+    else:
+        raise ValueError(f"method must be 'exact' or 'expsum', got {method!r}")
     sel_index, sel_token = select_intermediate_pair(p, q1, q2, drafts, u, seed, offset, row_status=status)
     out, acc, res, mass = accept_or_resample(p, r, sel_token, u, seed, offset, want_residual=want_residual,
                                              want_mass=want_residual, row_status=status)
@@ -278,12 +294,19 @@ def step_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, drafts: torch
 
 
 def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[torch.Tensor] = None, seed: int = 0,
-         offset: int = 0, s_max: int = 0, want_residual: bool = False):
-    """The whole path for one batch: r, selection, accept / resample (three launches on one stream)."""
+         offset: int = 0, s_max: int = 0, want_residual: bool = False, method: str = "exact"):
+    """The whole path for one batch: r, selection, accept / resample (three calls on one stream).
+    method "exact": r by the pairwise sums (K in {2, 3}); "expsum": r by the exponential-sum
+    quadrature (any K in [2, MDSS_MAX_K])."""
     B = p.shape[0]
     K = drafts.shape[1]
     status = torch.zeros(B, dtype=torch.int32, device=p.device)
-    r = induced_dist(p, q, K, s_max=s_max, row_status=status)
+    if method == "expsum":
+        r = induced_dist_expsum(p, q, K, row_status=status)
+    elif method == "exact":
+        r = induced_dist(p, q, K, s_max=s_max, row_status=status)
+    else:
+        raise ValueError(f"method must be 'exact' or 'expsum', got {method!r}")
     sel_index, sel_token = select_intermediate(p, q, drafts, u, seed, offset, row_status=status)
     out, acc, res, mass = accept_or_resample(p, r, sel_token, u, seed, offset, want_residual=want_residual,
                                              want_mass=want_residual, row_status=status)
@@ -429,11 +452,18 @@ def select_successive(p: torch.Tensor, q: torch.Tensor, r_stages: Optional[torch
 
 
 def step_successive(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u_sel: Optional[torch.Tensor] = None,
-                    u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False):
-    """The whole path with successive pairwise selection: stage laws, chained selection, Algorithm 1."""
+                    u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False,
+                    method: str = "exact"):
+    """The whole path with successive pairwise selection: stage laws, chained selection, Algorithm 1
+    (method as in step)."""
     B, K = drafts.shape
     status = torch.zeros(B, dtype=torch.int32, device=p.device)
-    rs = induced_dist_successive(p, q, K, row_status=status)
+    if method == "expsum":
+        rs = induced_dist_successive_expsum(p, q, K, row_status=status)
+    elif method == "exact":
+        rs = induced_dist_successive(p, q, K, row_status=status)
+    else:
+        raise ValueError(f"method must be 'exact' or 'expsum', got {method!r}")
     sel_index, sel_token = select_successive(p, q, rs, drafts, u_sel, seed, offset, row_status=status)
     out, acc, res, mass = accept_or_resample(p, rs[K - 2], sel_token, u, seed, offset, want_residual=want_residual,
                                              want_mass=want_residual, row_status=status)
@@ -524,3 +554,83 @@ def step_alphabet(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, m: int
     out, kept = alphabet_post(p, pt, mass0, z, u2, seed, offset)
     return {"p_trunc": pt, "mass0": mass0, "r": r, "sel_index": sel_index, "sel_token": sel_token, "z": z,
             "accepted": acc, "out_token": out, "kept": kept, "status": status}
+
+
+def _ws_arg(dev, need: int, workspace: Optional[torch.Tensor]) -> torch.Tensor:
+    if workspace is None:
+        return _workspace(dev, need)
+    if workspace.dtype != torch.uint8 or workspace.device != dev or workspace.numel() < need:
+        raise ValueError(f"workspace must be a uint8 tensor on {dev} of at least {need} bytes")
+    return workspace
+
+
+def workspace_bytes_expsum(B: int, V: int, K: int) -> int:
+    return int(load_library().mdss_workspace_bytes_expsum(B, V, K))
+
+
+def induced_dist_expsum(p: torch.Tensor, q: torch.Tensor, K: int, r: Optional[torch.Tensor] = None,
+                        row_status: Optional[torch.Tensor] = None,
+                        workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """r [B][V] fp32 of K i.i.d. drafts, by the exponential-sum quadrature (K in [2, MDSS_MAX_K])."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    need = int(lib.mdss_workspace_bytes_expsum(B, V, K))
+    if need == 0 and B > 0:
+        _check("mdss_workspace_bytes_expsum", 3 if not 2 <= K <= MDSS_MAX_K else 2)
+    workspace = _ws_arg(dev, need, workspace)
+    _check("mdss_induced_dist_expsum",
+           lib.mdss_induced_dist_expsum(_ptr(p), _ptr(q), B, V, K, _ptr(r), _ptr(row_status), _ptr(workspace),
+                                        workspace.numel(), _stream(dev)))
+    return r
+
+
+def workspace_bytes_pair_expsum(B: int, V: int) -> int:
+    return int(load_library().mdss_workspace_bytes_pair_expsum(B, V))
+
+
+def induced_dist_pair_expsum(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, r: Optional[torch.Tensor] = None,
+                             row_status: Optional[torch.Tensor] = None,
+                             workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """r [B][V] fp32 of X1 ~ q1, X2 ~ q2, by the exponential-sum quadrature."""
+    lib = load_library()
+    B, V, dev = _pq(p, q1)
+    _need(q2, "q2", torch.float32, (B, V), dev)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    need = int(lib.mdss_workspace_bytes_pair_expsum(B, V))
+    if need == 0 and B > 0:
+        _check("mdss_workspace_bytes_pair_expsum", 2)
+    workspace = _ws_arg(dev, need, workspace)
+    _check("mdss_induced_dist_pair_expsum",
+           lib.mdss_induced_dist_pair_expsum(_ptr(p), _ptr(q1), _ptr(q2), B, V, _ptr(r), _ptr(row_status),
+                                             _ptr(workspace), workspace.numel(), _stream(dev)))
+    return r
+
+
+def induced_dist_successive_expsum(p: torch.Tensor, q: torch.Tensor, K: int, r_stages: Optional[torch.Tensor] = None,
+                                   row_status: Optional[torch.Tensor] = None,
+                                   workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """r_stages [K-1][B][V] fp32 of successive pairwise selection, every stage by the quadrature."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if r_stages is None:
+        r_stages = torch.empty((K - 1, B, V), dtype=torch.float32, device=dev)
+    _need(r_stages, "r_stages", torch.float32, (K - 1, B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    need = int(lib.mdss_workspace_bytes_pair_expsum(B, V))
+    if need == 0 and B > 0:
+        _check("mdss_workspace_bytes_pair_expsum", 2)
+    workspace = _ws_arg(dev, need, workspace)
+    _check("mdss_induced_dist_successive_expsum",
+           lib.mdss_induced_dist_successive_expsum(_ptr(p), _ptr(q), B, V, K, _ptr(r_stages), _ptr(row_status),
+                                                   _ptr(workspace), workspace.numel(), _stream(dev)))
+    return r_stages

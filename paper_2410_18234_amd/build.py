@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libmdss.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "induced.hip", "sample.hip", "tlp.hip", "optimum.hip", "alphabet.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "induced.hip", "sample.hip", "tlp.hip", "optimum.hip", "alphabet.hip", "expsum.hip")]
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",

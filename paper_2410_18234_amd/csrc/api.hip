@@ -213,12 +213,59 @@ mdss_status mdss_select_truncated_lp(const float* p, const float* q1, const floa
                                           sel_token, row_status, static_cast<hipStream_t>(stream)));
 }
 
+size_t mdss_workspace_bytes_expsum(int64_t B, int64_t V, int32_t K) {
+  if (check_shape(B, V) != MDSS_OK || K < 2 || K > MDSS_MAX_K || B == 0) return 0;
+  return mdss::workspace_bytes_expsum(B, V, 1);
+}
+
+mdss_status mdss_induced_dist_expsum(const float* p, const float* q, int64_t B, int64_t V, int32_t K, float* r,
+                                     int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream) {
+  const mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  if (K < 2 || K > MDSS_MAX_K) return MDSS_EUNSUPPORTED;
+  if (B == 0) return MDSS_OK;
+  if (!p || !q || !r) return MDSS_EINVAL;
+  if (!workspace_ok(workspace, workspace_bytes, mdss::workspace_bytes_expsum(B, V, 1))) return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_induced_expsum(p, q, nullptr, B, V, K, r, row_status, workspace,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+size_t mdss_workspace_bytes_pair_expsum(int64_t B, int64_t V) {
+  if (check_shape(B, V) != MDSS_OK || B == 0) return 0;
+  return mdss::workspace_bytes_expsum(B, V, 2);
+}
+
+mdss_status mdss_induced_dist_pair_expsum(const float* p, const float* q1, const float* q2, int64_t B, int64_t V,
+                                          float* r, int32_t* row_status, void* workspace, size_t workspace_bytes,
+                                          void* stream) {
+  const mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  if (B == 0) return MDSS_OK;
+  if (!p || !q1 || !q2 || !r) return MDSS_EINVAL;
+  if (!workspace_ok(workspace, workspace_bytes, mdss::workspace_bytes_expsum(B, V, 2))) return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_induced_expsum(p, q1, q2, B, V, 2, r, row_status, workspace,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+mdss_status mdss_induced_dist_successive_expsum(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
+                                                float* r_stages, int32_t* row_status, void* workspace,
+                                                size_t workspace_bytes, void* stream) {
+  const mdss_status st = check_shape(B, V);
+  if (st != MDSS_OK) return st;
+  if (K < 2 || K > MDSS_SUCCESSIVE_MAX_K) return MDSS_EUNSUPPORTED;
+  if (B == 0) return MDSS_OK;
+  if (!p || !q || !r_stages) return MDSS_EINVAL;
+  if (!workspace_ok(workspace, workspace_bytes, mdss::workspace_bytes_expsum(B, V, 2))) return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_induced_successive_expsum(p, q, B, V, K, r_stages, row_status, workspace,
+                                                         static_cast<hipStream_t>(stream)));
+}
+
 mdss_status mdss_select_intermediate(const float* p, const float* q, const int32_t* drafts, const float* u,
                                      uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
                                      int32_t* sel_index, int32_t* sel_token, int32_t* row_status, void* stream) {
   mdss_status s = check_shape(B, V);
   if (s != MDSS_OK) return s;
-  if (K != 2 && K != 3) return MDSS_EUNSUPPORTED;
+  if (K < 2 || K > MDSS_MAX_K) return MDSS_EUNSUPPORTED;
   if (B == 0) return MDSS_OK;
   if (!p || !q || !drafts || !sel_index || !sel_token) return MDSS_EINVAL;
   return from_hip(mdss::launch_select(p, q, drafts, u, seed, offset, B, V, K, sel_index, sel_token, row_status,

@@ -30,6 +30,8 @@ constexpr int kRowBadDraft = 2;
 constexpr int kRowSupport = 4;
 constexpr int kRowForced = 8;
 constexpr int kRowLpLimit = 16;
+constexpr int kRowRange = 32;
+constexpr int kMaxK = 8;  // direct K-draft selection and its induced distribution
 
 // Workspace layout for mdss_induced_dist.
 struct Workspace {
@@ -63,6 +65,11 @@ hipError_t launch_select_successive(const float* p, const float* q, const float*
                                     int32_t* sel_index, int32_t* sel_token, int32_t* row_status, hipStream_t st);
 constexpr int kSuccessiveMaxK = 8;
 size_t workspace_bytes_optimum(int64_t B, int64_t V);
+size_t workspace_bytes_expsum(int64_t B, int64_t V, int L);
+hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, int K,
+                                 float* r, int32_t* row_status, void* workspace, hipStream_t st);
+hipError_t launch_induced_successive_expsum(const float* p, const float* q, int64_t B, int64_t V, int K,
+                                            float* r_stages, int32_t* row_status, void* workspace, hipStream_t st);
 hipError_t launch_alphabet_truncate(const float* p, int64_t B, int64_t V, int m, float* pt, double* mass0,
                                     int32_t* row_status, hipStream_t st);
 hipError_t launch_alphabet_post(const float* p, const float* pt, const double* mass0, const int32_t* token,

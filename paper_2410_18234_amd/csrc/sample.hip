@@ -26,9 +26,10 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ p
   const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
   int st = 0;
-  double w[3] = {0.0, 0.0, 0.0};
-  int32_t x[3] = {0, 0, 0};
+  double w[kMaxK];
+  int32_t x[kMaxK];
   for (int i = 0; i < K; ++i) {
+    w[i] = 0.0;
     x[i] = drafts[b * K + i];
     if (x[i] < 0 || (int64_t)x[i] >= V) {
       st |= kRowBadDraft;

@@ -69,7 +69,8 @@ def test_induced_dist_argument_errors(lib):
 def test_select_and_accept_argument_errors(lib):
     s = lib.mdss_select_intermediate
     assert s(FAKE, FAKE, None, None, 0, 0, 4, 16, 2, FAKE, FAKE, None, None) == 1
-    assert s(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 4, FAKE, FAKE, None, None) == 3
+    assert s(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 9, FAKE, FAKE, None, None) == 3
+    assert s(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 1, FAKE, FAKE, None, None) == 3
     assert s(FAKE, FAKE, FAKE, None, 0, 0, -1, 16, 2, FAKE, FAKE, None, None) == 2
     a = lib.mdss_accept_or_resample
     assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, None, FAKE, None, None, None, None) == 1
@@ -124,6 +125,36 @@ def test_successive_and_tlp_argument_errors(lib):
     assert sel(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 17, 0, FAKE, FAKE, FAKE, FAKE, None, None) == 3
 
 
+def test_expsum_argument_errors(lib):
+    ws = lib.mdss_workspace_bytes_expsum(4, 16, 2)
+    ws2 = lib.mdss_workspace_bytes_pair_expsum(4, 16)
+    assert 0 < ws < ws2
+    for K in (3, 8):
+        assert lib.mdss_workspace_bytes_expsum(4, 16, K) == ws  # the layout does not depend on K
+    assert lib.mdss_workspace_bytes_expsum(4, 16, 1) == 0 and lib.mdss_workspace_bytes_expsum(4, 16, 9) == 0
+    assert lib.mdss_workspace_bytes_expsum(4, 1, 2) == 0 and lib.mdss_workspace_bytes_pair_expsum(0, 16) == 0
+    assert lib.mdss_workspace_bytes_expsum(65535, 1 << 23, 2) > 0
+    f = lib.mdss_induced_dist_expsum
+    assert f(None, FAKE, 4, 16, 2, FAKE, None, FAKE, ws, None) == 1
+    assert f(FAKE, FAKE, 4, 16, 2, None, None, FAKE, ws, None) == 1
+    assert f(FAKE, FAKE, 4, 1, 2, FAKE, None, FAKE, ws, None) == 2
+    assert f(FAKE, FAKE, 65536, 16, 2, FAKE, None, FAKE, ws, None) == 2
+    assert f(FAKE, FAKE, 4, 16, 1, FAKE, None, FAKE, ws, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 9, FAKE, None, FAKE, ws, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 2, FAKE, None, None, ws, None) == 5
+    assert f(FAKE, FAKE, 4, 16, 2, FAKE, None, FAKE, ws - 1, None) == 5
+    assert f(FAKE, FAKE, 4, 16, 2, FAKE, None, ctypes.c_void_p(0x1010), ws, None) == 5  # misaligned
+    g = lib.mdss_induced_dist_pair_expsum
+    assert g(FAKE, FAKE, None, 4, 16, FAKE, None, FAKE, ws2, None) == 1
+    assert g(FAKE, FAKE, FAKE, 4, 1, FAKE, None, FAKE, ws2, None) == 2
+    assert g(FAKE, FAKE, FAKE, 4, 16, FAKE, None, FAKE, ws2 - 1, None) == 5
+    h = lib.mdss_induced_dist_successive_expsum
+    assert h(FAKE, FAKE, 4, 16, 3, None, None, FAKE, ws2, None) == 1
+    assert h(FAKE, FAKE, 4, 16, 1, FAKE, None, FAKE, ws2, None) == 3
+    assert h(FAKE, FAKE, 4, 16, 9, FAKE, None, FAKE, ws2, None) == 3
+    assert h(FAKE, FAKE, 4, 16, 3, FAKE, None, FAKE, ws2 - 1, None) == 5
+
+
 def test_optimum_argument_errors(lib):
     ws = lib.mdss_workspace_bytes_optimum(4, 16)
     assert ws > 0 and lib.mdss_workspace_bytes_optimum(0, 16) == 0
@@ -174,3 +205,10 @@ def test_empty_batch_is_a_no_op(lib):
     assert lib.mdss_truncated_lp(N, N, N, 0, 16, 17, 0, N, N, N, N, N, N, 0, N) == 3
     assert lib.mdss_truncated_lp(N, N, N, 0, 16, 5, 2, N, N, N, N, N, N, 0, N) == 1
     assert lib.mdss_select_truncated_lp(N, N, N, N, N, 0, 0, 0, 16, 5, 0, N, N, N, N, N, N) == 0
+    assert lib.mdss_workspace_bytes_expsum(0, 16, 2) == 0
+    assert lib.mdss_induced_dist_expsum(N, N, 0, 16, 8, N, N, N, 0, N) == 0
+    assert lib.mdss_induced_dist_expsum(N, N, 0, 16, 9, N, N, N, 0, N) == 3
+    assert lib.mdss_induced_dist_pair_expsum(N, N, N, 0, 16, N, N, N, 0, N) == 0
+    assert lib.mdss_induced_dist_successive_expsum(N, N, 0, 16, 4, N, N, N, 0, N) == 0
+    assert lib.mdss_select_intermediate(N, N, N, N, 0, 0, 0, 16, 8, N, N, N, N) == 0
+    assert lib.mdss_select_intermediate(N, N, N, N, 0, 0, 0, 16, 9, N, N, N, N) == 3

@@ -1,0 +1,296 @@
+"""GPU parity of the exponential-sum evaluation of r (mdss_induced_dist_expsum,
+mdss_induced_dist_pair_expsum, mdss_induced_dist_successive_expsum) through the
+C ABI, against the fp64 oracle's enumeration of the drafted tuples.
+
+Bars as for the pairwise path: r within 1e-5 relative L1 per row, sampled
+entries within 1e-5 relative each, selection bit-exact, Algorithm 1's
+invariants on the GPU's own r.  The quadrature's own error bound is 7e-8
+relative per entry, so the bars are met with two orders of magnitude to spare;
+the tests also hold the error under 2e-6 per row to catch a node-range or
+scale mistake that would still pass 1e-5 on some rows.  Notation: p = target,
+q = draft.
+"""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2410_18234_amd as mdss
+from oracle import successive as succ
+from test_gpu_parity import RTOL_ROW, _edge_rows, check_step2_invariants, dev, rel_l1, step2_common
+from workloads import CONFIGS, dirichlet_instances, generate, proposal_rows
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+TIGHT = 2e-6
+
+
+def es_r(p, q, K):
+    st = torch.zeros(p.shape[0], dtype=torch.int32, device=DEV)
+    r = mdss.induced_dist_expsum(dev(p), dev(q), K, row_status=st)
+    torch.cuda.synchronize()
+    return r.cpu().numpy(), st.cpu().numpy()
+
+
+def es_pair(p, q1, q2):
+    st = torch.zeros(p.shape[0], dtype=torch.int32, device=DEV)
+    r = mdss.induced_dist_pair_expsum(dev(p), dev(q1), dev(q2), row_status=st)
+    torch.cuda.synchronize()
+    return r.cpu().numpy(), st.cpu().numpy()
+
+
+def _dirichlet_rows(seed, B, V, alpha=0.5, zeros=0.0):
+    rng = np.random.default_rng(seed)
+    p = rng.dirichlet(np.full(V, alpha), size=B)
+    q = rng.dirichlet(np.full(V, alpha), size=B)
+    if zeros:
+        p[rng.random((B, V)) < zeros] = 0.0
+        q[rng.random((B, V)) < zeros] = 0.0
+        q[:, 0] += 1e-3
+    return p.astype(np.float32), q.astype(np.float32)
+
+
+# ------------------------------------------------------------------ every K, whole rows against the definition
+@pytest.mark.parametrize("K,V", [(2, 16), (3, 16), (4, 10), (5, 8), (6, 7), (8, 5)])
+def test_small_rows_every_k(K, V):
+    p, q = _dirichlet_rows(700 + K, 48, V, zeros=0.1)
+    r, st = es_r(p, q, K)
+    ro, sto = oracle.induced_dist(p, q, K)
+    np.testing.assert_array_equal(st, sto)
+    err = rel_l1(r, ro)
+    assert np.all(err <= TIGHT), err.max()
+
+
+def test_tiny_configuration_step():
+    w = generate("tiny")
+    out = mdss.step(dev(w["p"]), dev(w["q"]), dev(w["drafts"]), dev(w["u"]), want_residual=True, method="expsum")
+    torch.cuda.synchronize()
+    g = {k: (v.cpu().numpy() if v is not None else None) for k, v in out.items()}
+    ref = oracle.step(w["p"], w["q"], w["drafts"], w["u"])
+    assert np.all(rel_l1(g["r"], ref["r"]) <= TIGHT)
+    assert np.array_equal(g["sel_index"], ref["sel_index"])
+    assert np.all(g["status"] == 0)
+    check_step2_invariants(w["p"], g["r"], g["sel_token"], w["u"], g["out_token"], g["accepted"], g["residual"],
+                           g["mass"])
+
+
+def test_lp_instances_small_vocab():
+    # the independent Dirichlet(0.5) instances at V = 2..6 used for the optimum checks
+    for V in range(2, 7):
+        inst = dirichlet_instances(1011, V, 64)
+        p = np.stack([a for a, _ in inst]).astype(np.float32)
+        q = np.stack([b for _, b in inst]).astype(np.float32)
+        for K in (2, 3):
+            r, st = es_r(p, q, K)
+            ro, _ = oracle.induced_dist(p, q, K)
+            assert np.all(st == 0)
+            assert np.all(rel_l1(r, ro) <= TIGHT), (V, K, rel_l1(r, ro).max())
+
+
+# ------------------------------------------------------------------ full sizes
+@pytest.mark.parametrize("name", ["llm32k", "batch50k", "zipf128k", "k3top1024"])
+def test_full_size(name):
+    cfg = CONFIGS[name]
+    w = generate(name)
+    p, q, K = w["p"], w["q"], cfg.K
+    B, V = p.shape
+    out = mdss.step(dev(p), dev(q), dev(w["drafts"]), dev(w["u"]), want_residual=True, method="expsum")
+    torch.cuda.synchronize()
+    g = {k: (v.cpu().numpy() if v is not None else None) for k, v in out.items()}
+    assert np.all(g["status"] & 7 == 0)
+    r = g["r"].astype(np.float64)
+    assert np.all(r >= 0) and np.all(r[q == 0] == 0)
+    mass_q = q.astype(np.float64).sum(1) ** K
+    assert np.all(np.abs(r.sum(1) - mass_q) / mass_q <= TIGHT)
+    rng = np.random.default_rng(zlib.crc32(name.encode()) + 1)
+    n_samp = 256 if K == 2 else 64
+    rows = rng.integers(0, B, n_samp)
+    ys = np.array([rng.choice(np.flatnonzero(q[b] > 0)) for b in rows])
+    ys[: n_samp // 4] = [int(np.argmax(r[b])) for b in rows[: n_samp // 4]]
+    ys[n_samp // 4: n_samp // 2] = [w["drafts"][b, 0] for b in rows[n_samp // 4: n_samp // 2]]
+    e = oracle.induced_dist_entries(p, q, K, rows, ys)
+    got = r[rows, ys]
+    assert np.all(np.abs(got - e) <= RTOL_ROW * e), np.max(np.abs(got - e) / e)
+    si, stok, _ = oracle.select(p, q, w["drafts"], w["u"])
+    assert np.array_equal(g["sel_index"], si) and np.array_equal(g["sel_token"], stok)
+    check_step2_invariants(p, g["r"], g["sel_token"], w["u"], g["out_token"], g["accepted"], g["residual"], g["mass"])
+    step2_common(p, proposal_rows(p, q, cfg.seed, K), stok, w["u"])
+
+
+def test_llm32k_rows_full_oracle():
+    w = generate("llm32k")
+    rows = [0, 77, 255]
+    r, st = es_r(w["p"], w["q"], 2)
+    ro, _ = oracle.induced_dist(w["p"][rows], w["q"][rows], 2)
+    err = rel_l1(r[rows], ro)
+    assert np.all(err <= TIGHT), err
+
+
+def test_k3_rows_full_oracle():
+    w = generate("k3top1024", rows=[0, 1, 2, 3])
+    r, st = es_r(w["p"], w["q"], 3)
+    assert np.all(st == 0)
+    ro, _ = oracle.induced_dist(w["p"][:2], w["q"][:2], 3)
+    assert np.all(rel_l1(r[:2], ro) <= TIGHT), rel_l1(r[:2], ro)
+
+
+@pytest.mark.parametrize("K", [3, 4])
+def test_direct_k_on_whole_vocabulary(K):
+    # K drafts over the untruncated 32000-token rows: no support cap on this path.
+    # Entries against the definition restricted to the tuples containing y
+    # (K n^(K-1) terms each), the total mass (sum q)^K at every row.
+    w = generate("llm32k", rows=list(range(8)))
+    p, q = w["p"], w["q"]
+    r, st = es_r(p, q, K)
+    assert np.all(st == 0)
+    mass_q = q.astype(np.float64).sum(1) ** K
+    assert np.all(np.abs(r.astype(np.float64).sum(1) - mass_q) / mass_q <= TIGHT)
+    if K == 3:
+        rows = np.array([0, 3, 5, 7])
+        ys = np.array([int(np.argmax(r[b])) for b in rows])
+        e = oracle.induced_dist_entries(p, q, 3, rows, ys)
+        assert np.all(np.abs(r[rows, ys] - e) <= RTOL_ROW * e), np.abs(r[rows, ys] - e) / e
+
+
+def test_selection_any_k():
+    # the direct K-draft selection, bit-exact against the oracle for K up to 8
+    for K in (4, 6, 8):
+        p, q = _dirichlet_rows(900 + K, 512, 40, zeros=0.1)
+        rng = np.random.default_rng(K)
+        d = np.empty((512, K), np.int32)
+        for b in range(512):
+            c = np.cumsum(q[b].astype(np.float64))
+            d[b] = np.minimum(np.searchsorted(c, rng.random(K) * c[-1], side="right"), 39)
+        u = (rng.integers(0, 1 << 24, (512, 3)) / float(1 << 24)).astype(np.float32)
+        si, stok = mdss.select_intermediate(dev(p), dev(q), dev(d), dev(u))
+        torch.cuda.synchronize()
+        osi, ost, _ = oracle.select(p, q, d, u)
+        assert np.array_equal(si.cpu().numpy(), osi) and np.array_equal(stok.cpu().numpy(), ost)
+
+
+# ------------------------------------------------------------------ two draft laws, successive stages
+def test_pair_small_rows():
+    p, q1 = _dirichlet_rows(31, 64, 19, zeros=0.15)
+    _, q2 = _dirichlet_rows(32, 64, 19, zeros=0.15)
+    r, st = es_pair(p, q1, q2)
+    ro, sto = oracle.induced_dist_pair(p, q1, q2)
+    np.testing.assert_array_equal(st, sto)
+    assert np.all(rel_l1(r, ro) <= TIGHT), rel_l1(r, ro).max()
+    # identical laws reduce to the K = 2 path
+    ri, _ = es_pair(p, q1, q1)
+    rk, _ = es_r(p, q1, 2)
+    ro2, _ = oracle.induced_dist(p, q1, 2)
+    assert np.all(rel_l1(ri, ro2) <= TIGHT) and np.all(rel_l1(rk, ro2) <= TIGHT)
+
+
+def test_pair32k_full_size():
+    w = generate("pair32k")
+    p, q1, q2 = w["p"], w["q"], w["q2"]
+    r, st = es_pair(p, q1, q2)
+    assert np.all(st == 0)
+    mass = q1.astype(np.float64).sum(1) * q2.astype(np.float64).sum(1)
+    assert np.all(np.abs(r.astype(np.float64).sum(1) - mass) / mass <= TIGHT)
+    rng = np.random.default_rng(77)
+    rows = rng.integers(0, p.shape[0], 128)
+    ys = np.array([rng.choice(np.flatnonzero((q1[b] > 0) | (q2[b] > 0))) for b in rows])
+    e = oracle.induced_dist_pair_entries(p, q1, q2, rows, ys)
+    assert np.all(np.abs(r[rows, ys] - e) <= RTOL_ROW * e)
+    ro, _ = oracle.induced_dist_pair(p[:2], q1[:2], q2[:2])
+    assert np.all(rel_l1(r[:2], ro) <= TIGHT)
+
+
+@pytest.mark.parametrize("K", [2, 3, 5])
+def test_successive_stages(K):
+    p, q = _dirichlet_rows(600 + K, 64, 23, zeros=0.15)
+    st = torch.zeros(64, dtype=torch.int32, device=DEV)
+    rs = mdss.induced_dist_successive_expsum(dev(p), dev(q), K, row_status=st)
+    torch.cuda.synchronize()
+    rs = rs.cpu().numpy()
+    ro, sto = succ.stage_dists(p, q, K)
+    np.testing.assert_array_equal(st.cpu().numpy(), sto)
+    for j in range(K - 1):
+        assert np.all(rel_l1(rs[j], ro[j]) <= TIGHT), (j, rel_l1(rs[j], ro[j]).max())
+
+
+# ------------------------------------------------------------------ edge rows
+@pytest.mark.parametrize("K,V", [(2, 37), (3, 37), (2, 1001), (3, 9), (4, 9)])
+def test_edge_rows(K, V):
+    P, Q = _edge_rows(V, 300 + V + K)
+    r, st = es_r(P, Q, K)
+    ro, sto = oracle.induced_dist(P, Q, K)
+    assert np.array_equal(st & 1, sto & 1)
+    bad = (sto & 1) != 0
+    assert np.all(np.isnan(r[bad]))
+    ok = ~bad
+    assert np.all(rel_l1(r[ok], ro[ok]) <= TIGHT), rel_l1(r[ok], ro[ok])
+
+
+def test_two_token_rows():
+    rng = np.random.default_rng(5)
+    P = rng.dirichlet(np.ones(2), size=8).astype(np.float32)
+    Q = rng.dirichlet(np.ones(2), size=8).astype(np.float32)
+    Q[1] = [1.0, 0.0]
+    P[2] = [0.0, 1.0]
+    for K in (2, 3, 8):
+        r, st = es_r(P, Q, K)
+        ro, _ = oracle.induced_dist(P, Q, K)
+        assert np.all(st == 0) and np.all(rel_l1(r, ro) <= TIGHT)
+
+
+@pytest.mark.parametrize("V", [4095, 4097, 2049, 12289])
+def test_ragged_tiles(V):
+    # rows that end inside a moments tile (4096 tokens) or an evaluation tile (2048)
+    w = generate("llm32k", rows=[4, 9])
+    p, q = w["p"][:, :V].copy(), w["q"][:, :V].copy()
+    q[1, -1] = 0.0
+    p[1, -2] = 0.0
+    r, st = es_r(p, q, 2)
+    ro, _ = oracle.induced_dist(p, q, 2)
+    assert np.all(st == 0) and np.all(rel_l1(r, ro) <= TIGHT)
+
+
+def test_wide_weight_range_rows_in_fp64():
+    # positive weights spanning more than 2^180: the fp64 instantiation of the kernels
+    rng = np.random.default_rng(44)
+    V = 24
+    P = rng.dirichlet(np.full(V, 0.5), size=4)
+    Q = rng.dirichlet(np.full(V, 0.5), size=4)
+    P[:, 0] = 1e-42          # denormal target entry: w near 2^-140
+    Q[:, 1] = 1e-41          # denormal draft entry: w near 2^+135
+    Q[2, 2:5] = 1e-30
+    P, Q = P.astype(np.float32), Q.astype(np.float32)
+    w = P.astype(np.float64) / np.where(Q > 0, Q, 1)
+    assert np.log2(w.max(1) / w[w > 0].min()).min() > 181
+    for K in (2, 3):
+        r, st = es_r(P, Q, K)
+        ro, _ = oracle.induced_dist(P, Q, K)
+        assert np.all(st == 0)
+        assert np.all(rel_l1(r, ro) <= TIGHT), (K, rel_l1(r, ro))
+    r, st = es_pair(P, Q, Q[::-1].copy())
+    ro, _ = oracle.induced_dist_pair(P, Q, Q[::-1].copy())
+    assert np.all(st == 0) and np.all(rel_l1(r, ro) <= TIGHT)
+
+
+def test_range_flag_and_bad_rows():
+    rng = np.random.default_rng(3)
+    V = 16
+    P = rng.dirichlet(np.ones(V), size=4).astype(np.float32)
+    Q = rng.dirichlet(np.ones(V), size=4).astype(np.float32)
+    P[1, 0] = 3e38           # unnormalised: w up to 2^276 against 2^-139 -> range flag
+    Q[1, 0] = 1e-45
+    P[1, 1] = 1e-42
+    P[2, 3] = -1.0           # invalid probability
+    r, st = es_r(P, Q, 2)
+    assert list(st) == [0, mdss.MDSS_ROW_RANGE, mdss.MDSS_ROW_BAD_PROB, 0]
+    assert np.all(np.isnan(r[1])) and np.all(np.isnan(r[2]))
+    ro, _ = oracle.induced_dist(P[[0, 3]], Q[[0, 3]], 2)
+    assert np.all(rel_l1(r[[0, 3]], ro) <= TIGHT)
+
+
+def test_deterministic_reruns():
+    w = generate("llm32k", rows=list(range(16)))
+    a, _ = es_r(w["p"], w["q"], 2)
+    b, _ = es_r(w["p"], w["q"], 2)
+    assert np.array_equal(a, b)
