@@ -11,26 +11,36 @@
 // so with S(a) = sum_x q(x) exp(-a w(x)) the K-draft sum is
 //   integral of exp(t) exp(-e^t w(y)) S(e^t)^(K-1) dt,
 // and the pair sums factor the same way.  The trapezoidal rule on the grid
-// t_k = k h turns the O(n^K) sum into O(n) work per node:
+// t_k = k h (k an integer, the same grid for every row) turns the O(n^K) sum
+// into O(n) work per node:
 //   moments    S_k = sum_x q(x) exp(-a_k w(x)),   a_k = e^(t_k),
 //   evaluation r(y) = p(y) sum_k c_k exp(-a_k w(y)),  c_k = K h a_k S_k^(K-1).
 // Error of the rule (relative, for every D, independently of D): by Poisson
 // summation the integrand exp(t - D e^t) has Fourier transform
 // D^(-1+iv) Gamma(1 - iv), so the step-h sum differs from 1/D by at most
-// 2 sum_{m>=1} |Gamma(1 + 2 pi i m / h)| / D, 4.8e-8 for h = 1/2.  The grid is
-// cut where the left tail (t < t_lo: relative D e^t_lo) and the right tail
+// 2 sum_{m>=1} |Gamma(1 + 2 pi i m / h)| / D, 4.8e-8 for h = 1/2.  A row's grid
+// is cut where the left tail (t < t_lo: relative D e^t_lo) and the right tail
 // (t > t_hi: relative exp(-D e^t_hi)) are below 1e-8 for every denominator of
 // the row.  Every term is positive, so these relative bounds hold for the
-// sums and for r; fp32 evaluation adds a few 1e-8.  A row's node count is
-// (ln(D_max / D_min) + 21.3) / h: about 60 for LLM-like rows.
+// sums and for r; fp32 evaluation adds a few 1e-8.
 //
-// Weights are scaled by a power of two per row (w' = w 2^sigma, the scale
-// undone in r); rows whose positive weights span more than kEsWideRange
-// binary exponents run the same kernels in fp64 (node parameters outside the
-// fp32 range).  Decisions and closed forms are as in the pairwise kernels:
-// zero-weight tokens (p = 0 < q) enter in closed form, a flagged row gets NaN.
+// Windows.  For a tile of tokens with positive weights in [wlo, whi],
+// exp(-a_k w) rounds to 1 in fp32 for every token once a_k whi < 2^-25 and to 0
+// once a_k wlo > 104.  Each tile therefore evaluates exponentials only on its
+// own window of nodes between those limits: below the window a tile adds its
+// draft mass to S_k, above it nothing, and a query tile takes the prefix sum of
+// c_k below its window.  Moments need no row-wide information, so they run
+// first; one workgroup per row then merges the tiles, fixes the row's grid
+// range and coefficients; evaluation follows.
+//
+// Precision: each tile scales its weights by a power of two (w' = w 2^tau, the
+// node rates by 2^-tau) and evaluates in fp32; a tile whose weight ratios leave
+// the fp32 normal range or span more than 2^160 is left to an fp64 kernel that
+// scans the tile records.  Zero-weight tokens (p = 0 < q) enter in closed
+// form; a flagged row gets NaN.
 #include "common.h"
 
+#include <float.h>
 #include <math.h>
 
 #include <algorithm>
@@ -40,53 +50,57 @@ namespace mdss {
 namespace {
 
 constexpr int kEsThreads = 256;
-constexpr int kEsMomPer = 16;                           // tokens per thread, moments pass
-constexpr int kEsMomTile = kEsThreads * kEsMomPer;      // 4096 tokens per moments workgroup
-constexpr int kEsEvalPer = 8;                           // tokens per thread, evaluation pass
-constexpr int kEsEvalTile = kEsThreads * kEsEvalPer;    // 2048 tokens per evaluation workgroup
-constexpr int kEsNB = 16;                               // nodes per unrolled block
-constexpr int kEsMaxNodes = 480;                        // nodes of a row whose weights span <= 2^310
+constexpr int kEsWaves = kEsThreads / 64;
+constexpr int kEsMomPer = 16;                           // tokens per thread, moments
+constexpr int kEsMomTile = kEsThreads * kEsMomPer;      // 4096 tokens per moments tile
+constexpr int kEsEvalPer = 8;                           // tokens per thread, evaluation
+constexpr int kEsEvalTile = kEsThreads * kEsEvalPer;    // 2048 tokens per evaluation tile
+constexpr int kEsMaxNodes = 480;                        // nodes of a row (weights spanning <= 2^300)
+constexpr int kEsMaxWin = 496;                          // nodes of a tile window; table stride
+constexpr int kEsScanWGs = 64;                          // workgroups of the fp64 tile kernels
 constexpr double kEsStep = 0.5;                         // h
 constexpr double kEsLnEps = -18.420680743952367;        // ln 1e-8: left-tail cut
 constexpr double kEsLnLnInvEps = 2.9134941423228814;    // ln ln 1e8: right-tail cut
+constexpr double kEsLnOne = -17.328679513998633;        // ln 2^-25: below, exp(-z) rounds to 1
+constexpr double kEsLnZero = 4.6443908991413725;        // ln 104: above, exp(-z) < 2^-150
 constexpr double kEsLog2e = 1.4426950408889634;
-constexpr int kEsWideRange = 180;  // binary exponent range of the weights above which fp64 is used
+constexpr int kEsWideRange = 160;  // binary exponent range of a tile's weights kept in fp32
 
-// Per (row, moments tile, law): statistics of the positive weights.
-struct alignas(32) EsTileStat {
-  double wmin;   // smallest positive weight, fp64 ratio (+inf if none)
+// Per (row, moments tile, law).
+struct alignas(64) EsTile {
+  double wmin;   // smallest positive weight (+inf if none)
   double wmax;   // largest weight (0 if none)
-  int32_t npos;  // tokens with p > 0 and q > 0
-  int32_t bad;   // a NaN, negative or infinite probability was read
+  double qpos;   // draft mass of the positive-weight tokens
   double q0;     // draft mass of zero-weight tokens (q > 0 = p)
+  int32_t npos;  // positive-weight tokens
+  int32_t bad;   // a NaN, negative or infinite probability was read
+  int32_t ka;    // first node of the window
+  int32_t nw;    // window length (0: no positive weight)
+  int32_t wide;  // 1: the moments are taken by the fp64 kernel
+  int32_t pad[3];
 };
 
-// Per row: the evaluation plan.
+// Per row.
 struct alignas(64) EsPlan {
   int32_t flags;  // row status bits; a flagged row gets r = NaN
-  int32_t k_lo;   // first node index: t_k = (k_lo + k) h
-  int32_t nk;     // nodes (0: no quadrature term in this row)
-  int32_t sigma;  // weight scale: w' = w 2^sigma
-  int32_t wide;   // 1: nodes evaluated in fp64
-  int32_t w64;    // 1: some weight p/q leaves the fp32 normal range: ratios taken in fp64
-  int32_t pad[2];
+  int32_t k_lo;   // first node of the row's grid
+  int32_t nk;     // nodes of the row's grid (0: no quadrature term)
+  int32_t pad0;
   double q0[2];   // per law: draft mass of zero-weight tokens
-  double pad2[2];
+  double pad[5];
 };
 
 struct EsWork {
-  EsTileStat* stat;  // [B][T1][L]
-  EsPlan* plan;      // [B]
-  float* beta;       // [B][kEsMaxNodes] fp32 node rates a_k log2(e) (scaled weights)
-  double* alpha;     // [B][kEsMaxNodes] fp64 node rates a_k
-  double* part;      // [B][T1][L][kEsMaxNodes] moments of each tile
-  float* coef;       // [B][L][kEsMaxNodes] c_k (fp32 rows)
-  double* coef64;    // [B][L][kEsMaxNodes] c_k (fp64 rows)
-  int64_t T1;        // moments tiles per row
+  EsTile* tile;     // [B][T1][L]
+  double* part;     // [B][T1][L][kEsMaxWin] moments of each tile over its window
+  EsPlan* plan;     // [B]
+  double* ctab;     // [B][L][kEsMaxWin] c_k, k = k_lo + i
+  double* ptab;     // [B][L][kEsMaxWin] prefix sums: ptab[i] = c_(k_lo) + ... + c_(k_lo + i - 1)
+  int32_t* wide2;   // [B][T2] evaluation tiles left to the fp64 kernel
+  int64_t T1, T2;
 };
 
 __host__ __device__ inline int64_t es_tiles(int64_t V, int tile) { return (V + tile - 1) / tile; }
-__host__ __device__ inline int es_pad(int nk) { return (nk + kEsNB - 1) / kEsNB * kEsNB; }
 
 __device__ __forceinline__ double wave_min64(double v) {
 #pragma unroll
@@ -99,186 +113,50 @@ __device__ __forceinline__ double wave_max64(double v) {
   return v;
 }
 
-// ------------------------------------------------------------------ statistics
-// grid (T1, B, L): min / max positive weight, count, zero-weight mass and bad
-// values of law l = blockIdx.z over one tile of the row.
-__global__ __launch_bounds__(kEsThreads) void es_stats_kernel(const float* __restrict__ p,
-                                                               const float* __restrict__ q1,
-                                                               const float* __restrict__ q2, int64_t V, EsWork es) {
-  const int64_t t = blockIdx.x, b = blockIdx.y;
-  const int l = blockIdx.z, L = gridDim.z;
-  const float* pb = p + b * V;
-  const float* qb = (l == 0 ? q1 : q2) + b * V;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  double wmin = INFINITY, wmax = 0.0;
-  int npos = 0, bad = 0;
-  double q0 = 0.0;
-  const int64_t base = t * kEsMomTile;
-#pragma unroll 4
-  for (int i = 0; i < kEsMomPer; ++i) {
-    const int64_t x = base + i * kEsThreads + tid;
-    if (x >= V) break;
-    const float pv = pb[x], qv = qb[x];
-    bad |= (int)bad_prob(pv) | (int)bad_prob(qv);
-    if (qv > 0.0f) {
-      if (pv > 0.0f) {
-        const double w = (double)pv / (double)qv;
-        wmin = fmin(wmin, w);
-        wmax = fmax(wmax, w);
-        ++npos;
-      } else {
-        q0 += (double)qv;
-      }
-    }
-  }
-  wmin = wave_min64(wmin);
-  wmax = wave_max64(wmax);
-  npos = wave_sum_int(npos);
-  bad = wave_sum_int(bad);
-  q0 = wave_sum(q0);
-  __shared__ EsTileStat s[kEsThreads / 64];
-  if (lane == 0) {
-    s[wid].wmin = wmin;
-    s[wid].wmax = wmax;
-    s[wid].npos = npos;
-    s[wid].bad = bad;
-    s[wid].q0 = q0;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    EsTileStat o = s[0];
-    for (int i = 1; i < kEsThreads / 64; ++i) {
-      o.wmin = fmin(o.wmin, s[i].wmin);
-      o.wmax = fmax(o.wmax, s[i].wmax);
-      o.npos += s[i].npos;
-      o.bad |= s[i].bad;
-      o.q0 += s[i].q0;
-    }
-    es.stat[(b * es.T1 + t) * L + l] = o;
-  }
+// Window of a tile whose positive weights lie in [wlo, whi]: the nodes k where
+// exp(-a_k w) is neither 1 nor 0 in fp32 for some token of the tile.
+__device__ inline void es_window(double wlo, double whi, int& ka, int& nw) {
+  const int a = (int)ceil((kEsLnOne - log(whi)) / kEsStep);
+  const int z = (int)floor((kEsLnZero - log(wlo)) / kEsStep);
+  ka = a;
+  nw = max(0, min(z - a + 1, kEsMaxWin));
 }
 
-// ------------------------------------------------------------------ plan
-// One wave per row: the row's totals (tiles summed in a fixed order), its
-// weight scale, node range and node table.  K >= 2 identical drafts (L = 1)
-// or two draft laws (L = 2, K = 2).
-__global__ __launch_bounds__(64) void es_plan_kernel(int K, int L, EsWork es,
-                                                      int32_t* __restrict__ row_status) {
-  const int64_t b = blockIdx.x;
-  const int lane = threadIdx.x;
-  double wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0, 0.0};
-  int npos[2] = {0, 0}, bad = 0;
-  double q0[2] = {0.0, 0.0};
-  for (int64_t t = lane; t < es.T1; t += 64) {
-    for (int l = 0; l < L; ++l) {
-      const EsTileStat s = es.stat[(b * es.T1 + t) * L + l];
-      wmin[l] = fmin(wmin[l], s.wmin);
-      wmax[l] = fmax(wmax[l], s.wmax);
-      npos[l] += s.npos;
-      bad |= s.bad;
-      q0[l] += s.q0;
-    }
-  }
-  for (int l = 0; l < 2; ++l) {
-    wmin[l] = wave_min64(wmin[l]);
-    wmax[l] = wave_max64(wmax[l]);
-    npos[l] = wave_sum_int(npos[l]);
-    q0[l] = wave_sum(q0[l]);
-  }
-  bad = wave_sum_int(bad);
-  EsPlan pl;
-  pl.flags = bad ? kRowBadProb : 0;
-  pl.k_lo = 0;
-  pl.nk = 0;
-  pl.sigma = 0;
-  pl.wide = 0;
-  pl.w64 = 0;
-  pl.pad[0] = pl.pad[1] = 0;
-  pl.q0[0] = q0[0];
-  pl.q0[1] = q0[1];
-  pl.pad2[0] = pl.pad2[1] = 0.0;
-  const bool any = (L == 1) ? npos[0] > 0 : (npos[0] > 0 && npos[1] > 0);
-  if (!pl.flags && any) {
-    double lo = wmin[0], hi = wmax[0];
-    if (L == 2) {
-      lo = fmin(lo, wmin[1]);
-      hi = fmax(hi, wmax[1]);
-    }
-    int e_lo, e_hi;
-    frexp(lo, &e_lo);
-    frexp(hi, &e_hi);
-    pl.sigma = -((e_lo + e_hi) >> 1);
-    pl.wide = (e_hi - e_lo) > kEsWideRange;
-    pl.w64 = e_lo < -124 || e_hi > 126;  // an fp32 ratio p/q could be denormal or overflow
-    // smallest and largest denominator of the row (scaled weights, fp64)
-    double dmin, dmax;
-    if (L == 1) {
-      const double a = ldexp(wmin[0], pl.sigma), z = ldexp(wmax[0], pl.sigma);
-      // K = 2 takes the zero-weight tokens in closed form; K >= 3 keeps them in S (denominator w(y) alone)
-      dmin = (K == 2 || q0[0] == 0.0) ? K * a : a;
-      dmax = K * z;
-    } else {
-      dmin = ldexp(wmin[0], pl.sigma) + ldexp(wmin[1], pl.sigma);
-      dmax = ldexp(wmax[0], pl.sigma) + ldexp(wmax[1], pl.sigma);
-    }
-    const int k_lo = (int)floor((kEsLnEps - log(dmax)) / kEsStep);
-    const int k_hi = (int)ceil((kEsLnLnInvEps - log(dmin)) / kEsStep);
-    pl.k_lo = k_lo;
-    pl.nk = k_hi - k_lo + 1;
-    if (pl.nk > kEsMaxNodes) {  // only rows with probabilities far above 1 get here
-      pl.flags = kRowRange;
-      pl.nk = 0;
-    }
-  }
-  if (lane == 0) {
-    es.plan[b] = pl;
-    if (row_status && pl.flags) row_status[b] |= pl.flags;
-  }
-  // node table, padded to whole blocks (padding rates are 1: their coefficients are 0)
-  const int np = es_pad(pl.nk);
-  for (int k = lane; k < np; k += 64) {
-    const double a = (k < pl.nk) ? exp((double)(pl.k_lo + k) * kEsStep) : 1.0;
-    es.alpha[b * kEsMaxNodes + k] = a;
-    es.beta[b * kEsMaxNodes + k] = (float)(a * kEsLog2e);
-  }
+// Power-of-two scale that centres [wlo, whi] on 1 and the binary range it spans.
+__device__ inline void es_scale(double wlo, double whi, int& tau, int& range) {
+  int e_lo, e_hi;
+  frexp(wlo, &e_lo);
+  frexp(whi, &e_hi);
+  tau = -((e_lo + e_hi) >> 1);
+  range = e_hi - e_lo;
 }
 
-// Scaled weight w' = (p / q) 2^sigma in the row's precision.  fp32 rows take the
-// correctly rounded fp32 ratio (equal to the fp64 ratio rounded once) unless a
-// ratio of the row leaves the fp32 normal range.
+// node rate in the precision of the tile: fp32 a_k log2(e) 2^-tau (for exp2), fp64 a_k
 template <typename Real>
-__device__ __forceinline__ Real es_weight(float p, float q, const EsPlan& pl);
+__device__ __forceinline__ Real es_rate(int k, int tau);
 template <>
-__device__ __forceinline__ float es_weight<float>(float p, float q, const EsPlan& pl) {
-  return pl.w64 ? (float)ldexp((double)p / (double)q, pl.sigma) : ldexpf(p / q, pl.sigma);
+__device__ __forceinline__ float es_rate<float>(int k, int tau) {
+  return (float)ldexp(exp((double)k * kEsStep) * kEsLog2e, -tau);
 }
 template <>
-__device__ __forceinline__ double es_weight<double>(float p, float q, const EsPlan& pl) {
-  return ldexp((double)p / (double)q, pl.sigma);
+__device__ __forceinline__ double es_rate<double>(int k, int tau) {
+  return ldexp(exp((double)k * kEsStep), -tau);
 }
 
+__device__ __forceinline__ float es_decay(float beta, float w) { return __builtin_amdgcn_exp2f(-beta * w); }
+__device__ __forceinline__ double es_decay(double alpha, double w) { return exp(-alpha * w); }
 __device__ __forceinline__ float es_fma(float a, float b, float c) { return fmaf(a, b, c); }
 __device__ __forceinline__ double es_fma(double a, double b, double c) { return ::fma(a, b, c); }
 
-// exp(-a w) from the node rate in the row's precision
-__device__ __forceinline__ float es_decay(float beta, float w) { return __builtin_amdgcn_exp2f(-beta * w); }
-__device__ __forceinline__ double es_decay(double alpha, double w) { return exp(-alpha * w); }
-
-// The node tables are read-only inside the sweeps and uniform across a
-// workgroup: reading them through the constant address space lets every wave
-// take them with scalar loads into SGPRs.
-template <typename T>
-using const_as = const __attribute__((address_space(4))) T;
-
 template <typename Real>
-__device__ __forceinline__ const_as<Real>* es_rates(const EsWork& es, int64_t b);
+__device__ __forceinline__ Real es_ratio(float p, float q);
 template <>
-__device__ __forceinline__ const_as<float>* es_rates<float>(const EsWork& es, int64_t b) {
-  return (const_as<float>*)(es.beta + b * kEsMaxNodes);
+__device__ __forceinline__ float es_ratio<float>(float p, float q) {
+  return p / q;  // correctly rounded: the fp64 ratio rounded once
 }
 template <>
-__device__ __forceinline__ const_as<double>* es_rates<double>(const EsWork& es, int64_t b) {
-  return (const_as<double>*)(es.alpha + b * kEsMaxNodes);
+__device__ __forceinline__ double es_ratio<double>(float p, float q) {
+  return (double)p / (double)q;
 }
 
 // Block-wide compaction: every thread holds `per` flags; returns this thread's
@@ -295,7 +173,7 @@ __device__ __forceinline__ int block_compact_offset(const bool (&flag)[per], int
   int off = 0;
   total = 0;
 #pragma unroll
-  for (int i = 0; i < kEsThreads / 64; ++i) {
+  for (int i = 0; i < kEsWaves; ++i) {
     off += (i < wid) ? s_wave[i] : 0;
     total += s_wave[i];
   }
@@ -305,8 +183,8 @@ __device__ __forceinline__ int block_compact_offset(const bool (&flag)[per], int
 // One halving stage of a wave reduce-scatter: lanes with bit OFF set keep the
 // upper HALF of their values, the others the lower HALF; each kept value gets
 // its partner lane's copy added.
-template <int OFF, int HALF, typename Real>
-__device__ __forceinline__ void rs_stage(Real (&v)[16], int lane) {
+template <int OFF, int HALF, int N, typename Real>
+__device__ __forceinline__ void rs_stage(Real (&v)[N], int lane) {
   const bool up = (lane & OFF) != 0;
 #pragma unroll
   for (int i = 0; i < HALF; ++i) {
@@ -316,203 +194,496 @@ __device__ __forceinline__ void rs_stage(Real (&v)[16], int lane) {
   }
 }
 
-// Sum of 16 per-lane values over the 64 lanes of a wave, scattered: afterwards
-// lane l holds the total of value (l >> 2) (fixed order, deterministic).
-template <typename Real>
-__device__ __forceinline__ Real wave_reduce_scatter16(Real (&v)[16], int lane) {
-  rs_stage<32, 8>(v, lane);
-  rs_stage<16, 4>(v, lane);
-  rs_stage<8, 2>(v, lane);
-  rs_stage<4, 1>(v, lane);
+// Sum of NB per-lane values over the 64 lanes of a wave, scattered: afterwards
+// lane l holds the total of value l / (64 / NB) (fixed order, deterministic).
+template <int NB, typename Real>
+__device__ __forceinline__ Real wave_reduce_scatter(Real (&v)[NB], int lane) {
+  static_assert(NB == 4 || NB == 8 || NB == 16, "block sizes");
+  rs_stage<32, NB / 2>(v, lane);
+  rs_stage<16, NB / 4>(v, lane);
+  if constexpr (NB >= 8) rs_stage<8, NB / 8>(v, lane);
+  if constexpr (NB >= 16) rs_stage<4, NB / 16>(v, lane);
   Real x = v[0];
-  x += __shfl_xor(x, 2, 64);
-  x += __shfl_xor(x, 1, 64);
+#pragma unroll
+  for (int off = 64 / NB / 2; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
   return x;
 }
 
 // ------------------------------------------------------------------ moments
-// grid (T1, B, L): S_k over one tile of law l: sum of q(x) exp(-a_k w'(x)) over
-// its positive-weight tokens, for every node of the row.  Tokens are compacted
-// into LDS; each thread keeps 16 node sums for its tokens, which are summed
-// over the wave (reduce-scatter) and then over the four waves.
+// Statistics and moments of one tile of one law.  The fp32 instantiation
+// leaves a tile with an out-of-range ratio or a weight span above 2^160 to the
+// fp64 one (record.wide = 1).
+template <int NB, typename Real>
+__device__ __forceinline__ void es_moments_block(const Real* __restrict__ s_w, const float* __restrict__ s_q,
+                                                 const Real* __restrict__ s_rate, int M, int nb, int tid, int lane,
+                                                 int wid, Real (*s_red)[kEsMaxWin]) {
+  Real rt[NB], acc[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    rt[i] = s_rate[nb + i];
+    acc[i] = (Real)0;
+  }
+  for (int m = 0; m < M; ++m) {
+    const int j = tid + m * kEsThreads;
+    const Real w = s_w[j];
+    const Real qq = (Real)s_q[j];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) acc[i] = es_fma(qq, es_decay(rt[i], w), acc[i]);
+  }
+  const Real tot = wave_reduce_scatter<NB, Real>(acc, lane);
+  if ((lane & (64 / NB - 1)) == 0) s_red[wid][nb + lane / (64 / NB)] = tot;
+}
+
 template <typename Real>
+__device__ void es_moments_tile(const float* __restrict__ pb, const float* __restrict__ qb, int64_t V, int64_t t,
+                                EsTile* __restrict__ rec, double* __restrict__ part) {
+  constexpr bool f64 = sizeof(Real) == 8;
+  __shared__ Real s_w[kEsMomTile];
+  __shared__ float s_q[kEsMomTile];
+  __shared__ Real s_red[kEsWaves][kEsMaxWin];
+  __shared__ Real s_rate[kEsMaxWin];
+  __shared__ int s_wave[kEsWaves];
+  __shared__ double s_d[kEsWaves][4];
+  __shared__ int s_i[kEsWaves][3];
+  __shared__ int s_dec[4];  // ka, nw, tau, proceed
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t base = t * kEsMomTile;
+
+  bool pos[kEsMomPer];
+  Real wv[kEsMomPer];
+  float qv[kEsMomPer];
+  double wmin = INFINITY, wmax = 0.0, q0 = 0.0, qpos = 0.0;
+  int npos = 0, bad = 0, odd = 0;
+#pragma unroll
+  for (int i = 0; i < kEsMomPer; ++i) {
+    const int64_t x = base + i * kEsThreads + tid;
+    const float pp = (x < V) ? pb[x] : 0.0f;
+    const float qq = (x < V) ? qb[x] : 0.0f;
+    bad |= (int)bad_prob(pp) | (int)bad_prob(qq);
+    pos[i] = pp > 0.0f && qq > 0.0f;
+    const Real w = pos[i] ? es_ratio<Real>(pp, qq) : (Real)0;
+    if (!f64 && pos[i]) odd |= !((float)w >= FLT_MIN && (float)w <= FLT_MAX);
+    wv[i] = w;
+    qv[i] = qq;
+    if (pos[i]) {
+      wmin = fmin(wmin, (double)w);
+      wmax = fmax(wmax, (double)w);
+      qpos += (double)qq;
+      ++npos;
+    } else if (qq > 0.0f && pp == 0.0f) {
+      q0 += (double)qq;
+    }
+  }
+  wmin = wave_min64(wmin);
+  wmax = wave_max64(wmax);
+  q0 = wave_sum(q0);
+  qpos = wave_sum(qpos);
+  npos = wave_sum_int(npos);
+  bad = wave_sum_int(bad);
+  odd = wave_sum_int(odd);
+  if (lane == 0) {
+    s_d[wid][0] = wmin;
+    s_d[wid][1] = wmax;
+    s_d[wid][2] = q0;
+    s_d[wid][3] = qpos;
+    s_i[wid][0] = npos;
+    s_i[wid][1] = bad;
+    s_i[wid][2] = odd;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    wmin = s_d[0][0];
+    wmax = s_d[0][1];
+    for (int i = 1; i < kEsWaves; ++i) {
+      wmin = fmin(wmin, s_d[i][0]);
+      wmax = fmax(wmax, s_d[i][1]);
+    }
+    double a = 0.0, c = 0.0;
+    int n = 0, bd = 0, od = 0;
+    for (int i = 0; i < kEsWaves; ++i) {
+      a += s_d[i][2];
+      c += s_d[i][3];
+      n += s_i[i][0];
+      bd |= s_i[i][1];
+      od |= s_i[i][2];
+    }
+    EsTile o;
+    o.wmin = wmin;
+    o.wmax = wmax;
+    o.q0 = a;
+    o.qpos = c;
+    o.npos = n;
+    o.bad = bd != 0;
+    o.ka = 0;
+    o.nw = 0;
+    o.wide = f64 ? 1 : 0;
+    o.pad[0] = o.pad[1] = o.pad[2] = 0;
+    int tau = 0, range = 0;
+    if (n > 0) {
+      es_scale(wmin, wmax, tau, range);
+      if (!f64 && (od || range > kEsWideRange)) o.wide = 1;
+      es_window(wmin, wmax, o.ka, o.nw);
+    }
+    *rec = o;
+    s_dec[0] = o.ka;
+    s_dec[1] = o.nw;
+    s_dec[2] = f64 ? 0 : tau;
+    s_dec[3] = (!o.bad && o.nw > 0 && (f64 || !o.wide)) ? 1 : 0;
+  }
+  __syncthreads();
+  if (!s_dec[3]) return;
+  const int ka = s_dec[0], nw = s_dec[1], tau = s_dec[2];
+  const int npad = (nw + 15) / 16 * 16;
+  for (int k = tid; k < npad; k += kEsThreads) s_rate[k] = (k < nw) ? es_rate<Real>(ka + k, tau) : (Real)1;
+  int n = 0;
+  int off = block_compact_offset<kEsMomPer>(pos, s_wave, n);
+#pragma unroll
+  for (int i = 0; i < kEsMomPer; ++i) {
+    if (pos[i]) {
+      s_w[off] = f64 ? wv[i] : (Real)ldexpf((float)wv[i], tau);
+      s_q[off] = qv[i];
+      ++off;
+    }
+  }
+  const int M = (n + kEsThreads - 1) / kEsThreads;
+  for (int j = n + tid; j < M * kEsThreads; j += kEsThreads) {  // padding entries contribute 0
+    s_w[j] = (Real)0;
+    s_q[j] = 0.0f;
+  }
+  __syncthreads();
+  int nb = 0;
+  for (; nb + 16 <= nw; nb += 16) es_moments_block<16, Real>(s_w, s_q, s_rate, M, nb, tid, lane, wid, s_red);
+  if (nb + 8 <= nw) {
+    es_moments_block<8, Real>(s_w, s_q, s_rate, M, nb, tid, lane, wid, s_red);
+    nb += 8;
+  }
+  for (; nb < nw; nb += 4) es_moments_block<4, Real>(s_w, s_q, s_rate, M, nb, tid, lane, wid, s_red);
+  __syncthreads();
+  for (int k = tid; k < nw; k += kEsThreads) {
+    Real s = s_red[0][k];
+#pragma unroll
+    for (int i = 1; i < kEsWaves; ++i) s += s_red[i][k];
+    part[k] = (double)s;
+  }
+}
+
+// grid (T1, B, L): one tile of law l = blockIdx.z in fp32.
 __global__ __launch_bounds__(kEsThreads) void es_moments_kernel(const float* __restrict__ p,
                                                                  const float* __restrict__ q1,
                                                                  const float* __restrict__ q2, int64_t V,
                                                                  EsWork es) {
   const int64_t t = blockIdx.x, b = blockIdx.y;
   const int l = blockIdx.z, L = gridDim.z;
-  const EsPlan pl = es.plan[b];
-  if (pl.flags || pl.nk == 0 || pl.wide != (sizeof(Real) == 8)) return;
-  const float* pb = p + b * V;
-  const float* qb = (l == 0 ? q1 : q2) + b * V;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  __shared__ Real s_w[kEsMomTile];
-  __shared__ float s_q[kEsMomTile];
-  __shared__ Real s_red[kEsThreads / 64][kEsMaxNodes];
-  __shared__ int s_wave[kEsThreads / 64];
-
-  const int64_t base = t * kEsMomTile;
-  bool pos[kEsMomPer];
-  Real wv[kEsMomPer];
-  float qv[kEsMomPer];
-#pragma unroll
-  for (int i = 0; i < kEsMomPer; ++i) {
-    const int64_t x = base + i * kEsThreads + tid;
-    const float pp = (x < V) ? pb[x] : 0.0f;
-    const float qq = (x < V) ? qb[x] : 0.0f;
-    pos[i] = pp > 0.0f && qq > 0.0f;
-    wv[i] = pos[i] ? es_weight<Real>(pp, qq, pl) : (Real)0;
-    qv[i] = qq;
-  }
-  int n = 0;
-  int off = block_compact_offset<kEsMomPer>(pos, s_wave, n);
-#pragma unroll
-  for (int i = 0; i < kEsMomPer; ++i) {
-    if (pos[i]) {
-      s_w[off] = wv[i];
-      s_q[off] = qv[i];
-      ++off;
-    }
-  }
-  __syncthreads();
-  const int M = (n + kEsThreads - 1) / kEsThreads;
-  const_as<Real>* rate = es_rates<Real>(es, b);
-  const int np = es_pad(pl.nk);
-  for (int nb = 0; nb < np; nb += kEsNB) {
-    Real rt[kEsNB], acc[kEsNB];
-#pragma unroll
-    for (int i = 0; i < kEsNB; ++i) {
-      rt[i] = rate[nb + i];
-      acc[i] = (Real)0;
-    }
-    for (int m = 0; m < M; ++m) {
-      const int j = tid + m * kEsThreads;
-      const Real w = (j < n) ? s_w[j] : (Real)0;
-      const Real qq = (j < n) ? (Real)s_q[j] : (Real)0;
-#pragma unroll
-      for (int i = 0; i < kEsNB; ++i) acc[i] = es_fma(qq, es_decay(rt[i], w), acc[i]);
-    }
-    const Real tot = wave_reduce_scatter16<Real>(acc, lane);
-    if ((lane & 3) == 0) s_red[wid][nb + (lane >> 2)] = tot;
-  }
-  __syncthreads();
-  double* out = es.part + ((b * es.T1 + t) * L + l) * kEsMaxNodes;
-  for (int k = tid; k < pl.nk; k += kEsThreads) {
-    Real s = s_red[0][k];
-#pragma unroll
-    for (int i = 1; i < kEsThreads / 64; ++i) s += s_red[i][k];
-    out[k] = (double)s;
-  }
+  const int64_t idx = (b * es.T1 + t) * L + l;
+  es_moments_tile<float>(p + b * V, (l == 0 ? q1 : q2) + b * V, V, t, es.tile + idx, es.part + idx * kEsMaxWin);
 }
 
+// A few workgroups scan the tile records and take the tiles marked wide in fp64.
+__global__ __launch_bounds__(kEsThreads) void es_moments_wide_kernel(const float* __restrict__ p,
+                                                                      const float* __restrict__ q1,
+                                                                      const float* __restrict__ q2, int64_t V,
+                                                                      int64_t B, int L, EsWork es) {
+  __shared__ int s_n;
+  __shared__ int s_list[kEsThreads];
+  const int64_t N = B * es.T1 * L;
+  for (int64_t c0 = (int64_t)blockIdx.x * kEsThreads; c0 < N; c0 += (int64_t)gridDim.x * kEsThreads) {
+    if (threadIdx.x == 0) s_n = 0;
+    __syncthreads();
+    const int64_t i = c0 + threadIdx.x;
+    if (i < N && es.tile[i].wide && !es.tile[i].bad) s_list[atomicAdd(&s_n, 1)] = threadIdx.x;
+    __syncthreads();
+    const int n = s_n;
+    for (int j = 0; j < n; ++j) {
+      const int64_t idx = c0 + s_list[j];
+      const int l = (int)(idx % L);
+      const int64_t bt = idx / L, t = bt % es.T1, b = bt / es.T1;
+      es_moments_tile<double>(p + b * V, (l == 0 ? q1 : q2) + b * V, V, t, es.tile + idx,
+                              es.part + idx * kEsMaxWin);
+      __syncthreads();
+    }
+    __syncthreads();
+  }
+}
 
 // ------------------------------------------------------------------ coefficients
-// One workgroup per row: the moments of all tiles summed in tile order (fp64)
-// and the node coefficients.  K i.i.d. drafts: c_k = K h a_k S_k^(K-1) (K >= 3
-// keeps the zero-weight mass Q0 in S).  Two laws: the queries of law 1 take
-// h a_k S_k of law 2 and the queries of law 2 take h a_k S_k of law 1.
-__global__ __launch_bounds__(kEsThreads) void es_coef_kernel(int K, int L, EsWork es) {
+// One workgroup per row: the tile records merged in tile order (fp64), the
+// row's grid range, S_k from the tile windows, c_k and their prefix sums.
+// K i.i.d. drafts: c_k = K h a_k S_k^(K-1) (K >= 3 keeps the zero-weight mass
+// Q0 in S).  Two laws: the queries of law 1 take h a_k S_k of law 2 and the
+// queries of law 2 take h a_k S_k of law 1.
+__global__ __launch_bounds__(kEsThreads) void es_coef_kernel(int K, int L, EsWork es,
+                                                              int32_t* __restrict__ row_status) {
   const int64_t b = blockIdx.x;
-  const EsPlan pl = es.plan[b];
-  if (pl.flags || pl.nk == 0) return;
-  const int np = es_pad(pl.nk);
-  for (int k = threadIdx.x; k < np; k += kEsThreads) {
-    double S[2] = {0.0, 0.0};
-    if (k < pl.nk) {
-      for (int64_t t = 0; t < es.T1; ++t)
-        for (int l = 0; l < L; ++l) S[l] += es.part[((b * es.T1 + t) * L + l) * kEsMaxNodes + k];
-    }
-    const double ha = kEsStep * es.alpha[b * kEsMaxNodes + k];
-    double c[2];
-    if (L == 1) {
-      const double s = S[0] + (K >= 3 ? pl.q0[0] : 0.0);
-      double sp = 1.0;
-      for (int j = 1; j < K; ++j) sp *= s;
-      c[0] = (double)K * ha * sp;
-    } else {
-      c[0] = ha * S[1];
-      c[1] = ha * S[0];
-    }
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  __shared__ double s_d[kEsWaves][6];
+  __shared__ int s_i[kEsWaves][3];
+  __shared__ EsPlan s_plan;
+  __shared__ int s_ka[kEsThreads][2], s_nw[kEsThreads][2];
+  __shared__ double s_qp[kEsThreads][2];
+
+  double wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0, 0.0}, q0[2] = {0.0, 0.0};
+  int npos[2] = {0, 0}, bad = 0;
+  for (int64_t t = tid; t < es.T1; t += kEsThreads) {
     for (int l = 0; l < L; ++l) {
-      const double v = (k < pl.nk) ? c[l] : 0.0;
-      es.coef[(b * L + l) * kEsMaxNodes + k] = (float)v;
-      es.coef64[(b * L + l) * kEsMaxNodes + k] = v;
+      const EsTile& r = es.tile[(b * es.T1 + t) * L + l];
+      wmin[l] = fmin(wmin[l], r.wmin);
+      wmax[l] = fmax(wmax[l], r.wmax);
+      q0[l] += r.q0;
+      npos[l] += r.npos;
+      bad |= r.bad;
     }
   }
-}
-
-template <typename Real>
-__device__ __forceinline__ const_as<Real>* es_coefs(const EsWork& es, int64_t b, int l, int L);
-template <>
-__device__ __forceinline__ const_as<float>* es_coefs<float>(const EsWork& es, int64_t b, int l, int L) {
-  return (const_as<float>*)(es.coef + (b * L + l) * kEsMaxNodes);
-}
-template <>
-__device__ __forceinline__ const_as<double>* es_coefs<double>(const EsWork& es, int64_t b, int l, int L) {
-  return (const_as<double>*)(es.coef64 + (b * L + l) * kEsMaxNodes);
+  for (int l = 0; l < 2; ++l) {
+    wmin[l] = wave_min64(wmin[l]);
+    wmax[l] = wave_max64(wmax[l]);
+    q0[l] = wave_sum(q0[l]);
+    npos[l] = wave_sum_int(npos[l]);
+  }
+  bad = wave_sum_int(bad);
+  if (lane == 0) {
+    for (int l = 0; l < 2; ++l) {
+      s_d[wid][l] = wmin[l];
+      s_d[wid][2 + l] = wmax[l];
+      s_d[wid][4 + l] = q0[l];
+      s_i[wid][l] = npos[l];
+    }
+    s_i[wid][2] = bad;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int l = 0; l < 2; ++l) {
+      wmin[l] = s_d[0][l];
+      wmax[l] = s_d[0][2 + l];
+      q0[l] = s_d[0][4 + l];
+      npos[l] = s_i[0][l];
+      for (int i = 1; i < kEsWaves; ++i) {
+        wmin[l] = fmin(wmin[l], s_d[i][l]);
+        wmax[l] = fmax(wmax[l], s_d[i][2 + l]);
+        q0[l] += s_d[i][4 + l];
+        npos[l] += s_i[i][l];
+      }
+    }
+    bad = 0;
+    for (int i = 0; i < kEsWaves; ++i) bad |= s_i[i][2];
+    EsPlan pl;
+    pl.flags = bad ? kRowBadProb : 0;
+    pl.k_lo = 0;
+    pl.nk = 0;
+    pl.pad0 = 0;
+    pl.q0[0] = q0[0];
+    pl.q0[1] = q0[1];
+    for (int i = 0; i < 5; ++i) pl.pad[i] = 0.0;
+    const bool any = (L == 1) ? npos[0] > 0 : (npos[0] > 0 && npos[1] > 0);
+    if (!pl.flags && any) {
+      double dmin, dmax;
+      if (L == 1) {
+        // K = 2 takes the zero-weight tokens in closed form; K >= 3 keeps them in S (denominator w(y) alone)
+        dmin = (K == 2 || q0[0] == 0.0) ? K * wmin[0] : wmin[0];
+        dmax = K * wmax[0];
+      } else {
+        dmin = wmin[0] + wmin[1];
+        dmax = wmax[0] + wmax[1];
+      }
+      const int k_lo = (int)floor((kEsLnEps - log(dmax)) / kEsStep);
+      const int k_hi = (int)ceil((kEsLnLnInvEps - log(dmin)) / kEsStep);
+      pl.k_lo = k_lo;
+      pl.nk = k_hi - k_lo + 1;
+      if (pl.nk > kEsMaxNodes) {  // only rows with probabilities far above 1 get here
+        pl.flags = kRowRange;
+        pl.nk = 0;
+      }
+    }
+    s_plan = pl;
+    es.plan[b] = pl;
+    if (row_status && pl.flags) row_status[b] |= pl.flags;
+  }
+  __syncthreads();
+  const EsPlan pl = s_plan;
+  if (pl.nk == 0) return;
+  // S_l(k) for the two nodes of this thread, tiles taken in order
+  double S[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
+  const int kk[2] = {pl.k_lo + tid, pl.k_lo + tid + kEsThreads};
+  for (int64_t t0 = 0; t0 < es.T1; t0 += kEsThreads) {
+    __syncthreads();
+    if (t0 + tid < es.T1) {
+      for (int l = 0; l < L; ++l) {
+        const EsTile& r = es.tile[(b * es.T1 + t0 + tid) * L + l];
+        s_ka[tid][l] = r.ka;
+        s_nw[tid][l] = r.nw;
+        s_qp[tid][l] = r.qpos;
+      }
+    }
+    __syncthreads();
+    const int nt = (int)std::min<int64_t>(kEsThreads, es.T1 - t0);
+    for (int j = 0; j < nt; ++j) {
+      for (int l = 0; l < L; ++l) {
+        const int ka = s_ka[j][l], nw = s_nw[j][l];
+        if (nw == 0) continue;  // no positive weight in this tile
+        const double* pt = es.part + ((b * es.T1 + t0 + j) * L + l) * kEsMaxWin;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int k = kk[u];
+          S[u][l] += (k < ka) ? s_qp[j][l] : ((k < ka + nw) ? pt[k - ka] : 0.0);
+        }
+      }
+    }
+  }
+  for (int u = 0; u < 2; ++u) {
+    const int i = tid + u * kEsThreads;
+    if (i >= pl.nk) continue;
+    const double ha = kEsStep * exp((double)kk[u] * kEsStep);
+    if (L == 1) {
+      const double s = S[u][0] + (K >= 3 ? pl.q0[0] : 0.0);
+      double sp = 1.0;
+      for (int j = 1; j < K; ++j) sp *= s;
+      es.ctab[(b * L) * kEsMaxWin + i] = (double)K * ha * sp;
+    } else {
+      es.ctab[(b * L + 0) * kEsMaxWin + i] = ha * S[u][1];
+      es.ctab[(b * L + 1) * kEsMaxWin + i] = ha * S[u][0];
+    }
+  }
+  __syncthreads();
+  // prefix sums in node order: wave 0, eight consecutive nodes per lane
+  if (wid == 0) {
+    for (int l = 0; l < L; ++l) {
+      const double* c = es.ctab + (b * L + l) * kEsMaxWin;
+      double* pt = es.ptab + (b * L + l) * kEsMaxWin;
+      double loc = 0.0;
+      for (int j = 0; j < 8; ++j) {
+        const int i = lane * 8 + j;
+        if (i < pl.nk) loc += c[i];
+      }
+      const double incl = wave_inclusive_scan(loc, lane);
+      double run = incl - loc;
+      for (int j = 0; j < 8; ++j) {
+        const int i = lane * 8 + j;
+        if (i <= pl.nk && i < kEsMaxWin) pt[i] = run;
+        if (i < pl.nk) run += c[i];
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------------ evaluation
-// grid (T2, B): r over one tile of 2048 tokens.  The positive-weight tokens of
-// each law are compacted into LDS; a thread evaluates four of them at a time
-// over all nodes (sum_k c_k exp(-a_k w'(y)), fp32 blocks of 16 nodes folded
-// into the running sum), and r is assembled per token with the zero-weight
-// closed forms.  The fp32 instantiation also writes flagged rows (NaN) and rows
-// without a quadrature term.
+// One evaluation tile (2048 tokens) of a row: r(y) = p(y) [P + sum over the
+// window of c_k exp(-a_k w(y))] + the zero-weight closed forms, P = the sum of
+// c_k below the window.  The fp32 instantiation returns false, writing
+// nothing, for a tile it leaves to the fp64 one.
 template <typename Real, int L>
-__global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __restrict__ p,
-                                                              const float* __restrict__ q1,
-                                                              const float* __restrict__ q2, int64_t V, int K,
-                                                              float* __restrict__ r, EsWork es) {
-  const int64_t t = blockIdx.x, b = blockIdx.y;
-  const EsPlan pl = es.plan[b];
-  if (pl.wide != (sizeof(Real) == 8)) return;
-  const float* pb = p + b * V;
-  float* rb = r + b * V;
-  const int tid = threadIdx.x;
-  const int64_t base = t * kEsEvalTile;
-  if (pl.flags) {
-#pragma unroll
-    for (int i = 0; i < kEsEvalPer; ++i) {
-      const int64_t x = base + i * kEsThreads + tid;
-      if (x < V) rb[x] = NAN;
-    }
-    return;
-  }
+__device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restrict__ q1b,
+                             const float* __restrict__ q2b, int64_t V, int K, int64_t t, float* __restrict__ rb,
+                             const EsPlan& pl, const double* __restrict__ ctab, const double* __restrict__ ptab) {
+  constexpr bool f64 = sizeof(Real) == 8;
   __shared__ Real s_w[kEsEvalTile];
-  __shared__ int s_pos[kEsEvalTile];
+  __shared__ uint16_t s_pos[kEsEvalTile];
   __shared__ Real s_acc[kEsEvalTile];
-  __shared__ int s_wave[kEsThreads / 64];
+  __shared__ Real s_rate[kEsMaxWin];
+  __shared__ Real s_coef[kEsMaxWin];
+  __shared__ int s_wave[kEsWaves];
+  __shared__ double s_d[kEsWaves][2][2];
+  __shared__ int s_i[kEsWaves];
+  __shared__ int s_dec[2][2];  // per law: first row node of the window, window length
+  __shared__ int s_tau, s_go;
+  __shared__ Real s_base[2];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t base = t * kEsEvalTile;
+
   float pv[kEsEvalPer], qv[L][kEsEvalPer];
+  Real wv[L][kEsEvalPer];
+  bool pos[L][kEsEvalPer];
 #pragma unroll
   for (int i = 0; i < kEsEvalPer; ++i) {
     const int64_t x = base + i * kEsThreads + tid;
     pv[i] = (x < V) ? pb[x] : 0.0f;
-    qv[0][i] = (x < V) ? q1[b * V + x] : 0.0f;
-    if (L == 2) qv[L - 1][i] = (x < V) ? q2[b * V + x] : 0.0f;
-    s_acc[i * kEsThreads + tid] = (Real)0;
+    qv[0][i] = (x < V) ? q1b[x] : 0.0f;
+    if (L == 2) qv[L - 1][i] = (x < V) ? q2b[x] : 0.0f;
   }
   if (pl.nk > 0) {
-    const_as<Real>* rate = es_rates<Real>(es, b);
-    const int np = es_pad(pl.nk);
+    double wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0, 0.0};
+    int odd = 0;
 #pragma unroll
-    for (int l = 0; l < L; ++l) {
-      bool pos[kEsEvalPer];
-#pragma unroll
-      for (int i = 0; i < kEsEvalPer; ++i) pos[i] = pv[i] > 0.0f && qv[l][i] > 0.0f;
-      int n = 0;
-      int off = block_compact_offset<kEsEvalPer>(pos, s_wave, n);
+    for (int l = 0; l < L; ++l)
 #pragma unroll
       for (int i = 0; i < kEsEvalPer; ++i) {
-        if (pos[i]) {
-          s_w[off] = es_weight<Real>(pv[i], qv[l][i], pl);
-          s_pos[off] = i * kEsThreads + tid;
+        pos[l][i] = pv[i] > 0.0f && qv[l][i] > 0.0f;
+        const Real w = pos[l][i] ? es_ratio<Real>(pv[i], qv[l][i]) : (Real)0;
+        if (!f64 && pos[l][i]) odd |= !((float)w >= FLT_MIN && (float)w <= FLT_MAX);
+        wv[l][i] = w;
+        if (pos[l][i]) {
+          wmin[l] = fmin(wmin[l], (double)w);
+          wmax[l] = fmax(wmax[l], (double)w);
+        }
+      }
+    for (int l = 0; l < L; ++l) {
+      wmin[l] = wave_min64(wmin[l]);
+      wmax[l] = wave_max64(wmax[l]);
+    }
+    odd = wave_sum_int(odd);
+    if (lane == 0) {
+      for (int l = 0; l < L; ++l) {
+        s_d[wid][l][0] = wmin[l];
+        s_d[wid][l][1] = wmax[l];
+      }
+      s_i[wid] = odd;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int od = 0;
+      for (int i = 0; i < kEsWaves; ++i) od |= s_i[i];
+      double lo = INFINITY, hi = 0.0;
+      for (int l = 0; l < L; ++l) {
+        for (int i = 0; i < kEsWaves; ++i) {
+          wmin[l] = fmin(wmin[l], s_d[i][l][0]);
+          wmax[l] = fmax(wmax[l], s_d[i][l][1]);
+        }
+        lo = fmin(lo, wmin[l]);
+        hi = fmax(hi, wmax[l]);
+      }
+      int tau = 0, range = 0;
+      if (hi > 0.0) es_scale(lo, hi, tau, range);
+      s_go = f64 || !(od || range > kEsWideRange);
+      s_tau = f64 ? 0 : tau;
+      for (int l = 0; l < L; ++l) {
+        int i0 = pl.nk, cnt = 0;
+        if (wmax[l] > 0.0) {
+          int ka, nw;
+          es_window(wmin[l], wmax[l], ka, nw);
+          i0 = std::min(std::max(ka - pl.k_lo, 0), pl.nk);
+          const int i1 = std::min(ka + nw - 1 - pl.k_lo, pl.nk - 1);
+          cnt = std::max(0, i1 - i0 + 1);
+        }
+        s_dec[l][0] = i0;
+        s_dec[l][1] = cnt;
+      }
+    }
+    __syncthreads();
+    if (!s_go) return false;
+  }
+  const int tau = (pl.nk > 0) ? s_tau : 0;
+#pragma unroll
+  for (int i = 0; i < kEsEvalPer; ++i) s_acc[i * kEsThreads + tid] = (Real)0;
+  if (pl.nk > 0) {
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      const int i0 = s_dec[l][0], cnt = s_dec[l][1];
+      const double* c = ctab + l * kEsMaxWin;
+      for (int k = tid; k < cnt; k += kEsThreads) {
+        s_rate[k] = es_rate<Real>(pl.k_lo + i0 + k, tau);
+        s_coef[k] = (Real)ldexp(c[i0 + k], -tau);
+      }
+      if (tid == 0) s_base[l] = (Real)ldexp(ptab[l * kEsMaxWin + i0], -tau);
+      int n = 0;
+      int off = block_compact_offset<kEsEvalPer>(pos[l], s_wave, n);
+#pragma unroll
+      for (int i = 0; i < kEsEvalPer; ++i) {
+        if (pos[l][i]) {
+          s_w[off] = f64 ? wv[l][i] : (Real)ldexpf((float)wv[l][i], tau);
+          s_pos[off] = (uint16_t)(i * kEsThreads + tid);
           ++off;
         }
       }
       __syncthreads();
-      const_as<Real>* cf = es_coefs<Real>(es, b, l, L);
+      const Real pre = s_base[l];
       for (int j0 = 0; j0 < n; j0 += 4 * kEsThreads) {
         Real w[4], acc[4];
         int ps[4];
@@ -522,25 +693,36 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
           const int j = j0 + e * kEsThreads + tid;
           ok[e] = j < n;
           w[e] = ok[e] ? s_w[j] : (Real)0;
-          ps[e] = ok[e] ? s_pos[j] : 0;
+          ps[e] = ok[e] ? (int)s_pos[j] : 0;
           acc[e] = (Real)0;
         }
-        for (int nb = 0; nb < np; nb += kEsNB) {
+        int k = 0;
+        for (; k + 16 <= cnt; k += 16) {
           Real blk[4] = {(Real)0, (Real)0, (Real)0, (Real)0};
 #pragma unroll
-          for (int i = 0; i < kEsNB; ++i) {
-            const Real rt = rate[nb + i], c = cf[nb + i];
+          for (int i = 0; i < 16; ++i) {
+            const Real rt = s_rate[k + i], cf = s_coef[k + i];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) blk[e] = es_fma(c, es_decay(rt, w[e]), blk[e]);
+            for (int e = 0; e < 4; ++e) blk[e] = es_fma(cf, es_decay(rt, w[e]), blk[e]);
           }
 #pragma unroll
           for (int e = 0; e < 4; ++e) acc[e] += blk[e];
+        }
+        {
+          Real blk[4] = {(Real)0, (Real)0, (Real)0, (Real)0};
+          for (; k < cnt; ++k) {
+            const Real rt = s_rate[k], cf = s_coef[k];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) blk[e] = es_fma(cf, es_decay(rt, w[e]), blk[e]);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[e] += blk[e] + pre;
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           if (ok[e]) s_acc[ps[e]] += acc[e];  // one entry per token and law: no two threads share a slot
       }
-      __syncthreads();  // s_w / s_pos are rebuilt for the next law; s_acc is read below
+      __syncthreads();  // tables and the compacted list are rebuilt for the next law; s_acc is read below
     }
   }
   const double q0a = pl.q0[0], q0b = (L == 2) ? pl.q0[1] : 0.0;
@@ -550,54 +732,99 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
   for (int i = 0; i < kEsEvalPer; ++i) {
     const int64_t x = base + i * kEsThreads + tid;
     if (x >= V) break;
-    const double pp = (double)pv[i];
-    const double quad = ldexp((double)s_acc[i * kEsThreads + tid], pl.sigma);
-    double v = 0.0;
+    const float pp = pv[i];
+    const Real acc = s_acc[i * kEsThreads + tid];
+    const float quad = f64 ? (float)ldexp((double)pp * (double)acc, tau) : ldexpf(pp * (float)acc, tau);
+    float v = 0.0f;
     if (L == 1) {
-      const double qq = (double)qv[0][i];
-      if (qq > 0.0) v = (pp > 0.0) ? pp * quad + (K == 2 ? 2.0 * qq * q0a : 0.0) : qq * zw;
+      const float qq = qv[0][i];
+      if (qq > 0.0f) v = (pp > 0.0f) ? ((K == 2) ? fmaf(2.0f * qq, (float)q0a, quad) : quad) : (float)((double)qq * zw);
     } else {
       // two laws: a zero-weight pole of the other draft adds q_i(y) Qj_0; a zero target splits it in half
-      const double a = (double)qv[0][i], c = (double)qv[L - 1][i];
-      if (pp > 0.0) {
-        v = pp * quad + (a > 0.0 ? a * q0b : 0.0) + (c > 0.0 ? c * q0a : 0.0);
-      } else {
-        v = 0.5 * ((a > 0.0 ? a * q0b : 0.0) + (c > 0.0 ? c * q0a : 0.0));
-      }
+      const float a = qv[0][i], c = qv[L - 1][i];
+      const float za = (a > 0.0f) ? a * (float)q0b : 0.0f, zc = (c > 0.0f) ? c * (float)q0a : 0.0f;
+      v = (pp > 0.0f) ? quad + za + zc : 0.5f * (za + zc);
     }
-    rb[x] = (float)v;
+    rb[x] = v;
+  }
+  return true;
+}
+
+template <int L>
+__global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __restrict__ p,
+                                                              const float* __restrict__ q1,
+                                                              const float* __restrict__ q2, int64_t V, int K,
+                                                              float* __restrict__ r, EsWork es) {
+  const int64_t t = blockIdx.x, b = blockIdx.y;
+  const EsPlan pl = es.plan[b];
+  float* rb = r + b * V;
+  if (pl.flags) {
+    for (int i = 0; i < kEsEvalPer; ++i) {
+      const int64_t x = t * kEsEvalTile + i * kEsThreads + threadIdx.x;
+      if (x < V) rb[x] = NAN;
+    }
+    if (threadIdx.x == 0) es.wide2[b * es.T2 + t] = 0;
+    return;
+  }
+  const bool done = es_eval_tile<float, L>(p + b * V, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, rb, pl,
+                                           es.ctab + b * L * kEsMaxWin, es.ptab + b * L * kEsMaxWin);
+  if (threadIdx.x == 0) es.wide2[b * es.T2 + t] = done ? 0 : 1;
+}
+
+template <int L>
+__global__ __launch_bounds__(kEsThreads) void es_eval_wide_kernel(const float* __restrict__ p,
+                                                                   const float* __restrict__ q1,
+                                                                   const float* __restrict__ q2, int64_t V, int64_t B,
+                                                                   int K, float* __restrict__ r, EsWork es) {
+  __shared__ int s_n;
+  __shared__ int s_list[kEsThreads];
+  const int64_t N = B * es.T2;
+  for (int64_t c0 = (int64_t)blockIdx.x * kEsThreads; c0 < N; c0 += (int64_t)gridDim.x * kEsThreads) {
+    if (threadIdx.x == 0) s_n = 0;
+    __syncthreads();
+    const int64_t i = c0 + threadIdx.x;
+    if (i < N && es.wide2[i]) s_list[atomicAdd(&s_n, 1)] = threadIdx.x;
+    __syncthreads();
+    const int n = s_n;
+    for (int j = 0; j < n; ++j) {
+      const int64_t idx = c0 + s_list[j];
+      const int64_t t = idx % es.T2, b = idx / es.T2;
+      const EsPlan pl = es.plan[b];
+      es_eval_tile<double, L>(p + b * V, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, r + b * V, pl,
+                              es.ctab + b * L * kEsMaxWin, es.ptab + b * L * kEsMaxWin);
+      __syncthreads();
+    }
+    __syncthreads();
   }
 }
 
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
-  const int64_t T1 = es_tiles(V, kEsMomTile);
+  const int64_t T1 = es_tiles(V, kEsMomTile), T2 = es_tiles(V, kEsEvalTile);
   char* c = static_cast<char*>(base);
-  es->stat = reinterpret_cast<EsTileStat*>(c);
-  c += align256(sizeof(EsTileStat) * B * T1 * L);
+  es->tile = reinterpret_cast<EsTile*>(c);
+  c += align256(sizeof(EsTile) * B * T1 * L);
+  es->part = reinterpret_cast<double*>(c);
+  c += align256(sizeof(double) * B * T1 * L * kEsMaxWin);
   es->plan = reinterpret_cast<EsPlan*>(c);
   c += align256(sizeof(EsPlan) * B);
-  es->beta = reinterpret_cast<float*>(c);
-  c += align256(sizeof(float) * B * kEsMaxNodes);
-  es->alpha = reinterpret_cast<double*>(c);
-  c += align256(sizeof(double) * B * kEsMaxNodes);
-  es->part = reinterpret_cast<double*>(c);
-  c += align256(sizeof(double) * B * T1 * L * kEsMaxNodes);
-  es->coef = reinterpret_cast<float*>(c);
-  c += align256(sizeof(float) * B * L * kEsMaxNodes);
-  es->coef64 = reinterpret_cast<double*>(c);
+  es->ctab = reinterpret_cast<double*>(c);
+  c += align256(sizeof(double) * B * L * kEsMaxWin);
+  es->ptab = reinterpret_cast<double*>(c);
+  c += align256(sizeof(double) * B * L * kEsMaxWin);
+  es->wide2 = reinterpret_cast<int32_t*>(c);
   es->T1 = T1;
+  es->T2 = T2;
 }
 
 }  // namespace
 
 size_t workspace_bytes_expsum(int64_t B, int64_t V, int L) {
-  const int64_t T1 = es_tiles(V, kEsMomTile);
-  return align256(sizeof(EsTileStat) * B * T1 * L) + align256(sizeof(EsPlan) * B) +
-         align256(sizeof(float) * B * kEsMaxNodes) + align256(sizeof(double) * B * kEsMaxNodes) +
-         align256(sizeof(double) * B * T1 * L * kEsMaxNodes) + align256(sizeof(float) * B * L * kEsMaxNodes) +
-         align256(sizeof(double) * B * L * kEsMaxNodes);
+  const int64_t T1 = es_tiles(V, kEsMomTile), T2 = es_tiles(V, kEsEvalTile);
+  return align256(sizeof(EsTile) * B * T1 * L) + align256(sizeof(double) * B * T1 * L * kEsMaxWin) +
+         align256(sizeof(EsPlan) * B) + 2 * align256(sizeof(double) * B * L * kEsMaxWin) +
+         align256(sizeof(int32_t) * B * T2);
 }
 
 // q2 == nullptr: K i.i.d. drafts from q1; else two draft laws (K = 2).
@@ -606,20 +833,19 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
   const int L = (q2 != nullptr) ? 2 : 1;
   EsWork es;
   carve_es(workspace, B, V, L, &es);
-  const int64_t T2 = es_tiles(V, kEsEvalTile);
   const dim3 g1((unsigned)es.T1, (unsigned)B, (unsigned)L);
-  hipLaunchKernelGGL(es_stats_kernel, g1, dim3(kEsThreads), 0, st, p, q1, q2, V, es);
-  hipLaunchKernelGGL(es_plan_kernel, dim3((unsigned)B), dim3(64), 0, st, K, L, es, row_status);
-  hipLaunchKernelGGL(es_moments_kernel<float>, g1, dim3(kEsThreads), 0, st, p, q1, q2, V, es);
-  hipLaunchKernelGGL(es_moments_kernel<double>, g1, dim3(kEsThreads), 0, st, p, q1, q2, V, es);
-  hipLaunchKernelGGL(es_coef_kernel, dim3((unsigned)B), dim3(kEsThreads), 0, st, K, L, es);
-  const dim3 g2((unsigned)T2, (unsigned)B);
+  hipLaunchKernelGGL(es_moments_kernel, g1, dim3(kEsThreads), 0, st, p, q1, q2, V, es);
+  hipLaunchKernelGGL(es_moments_wide_kernel, dim3(kEsScanWGs), dim3(kEsThreads), 0, st, p, q1, q2, V, B, L, es);
+  hipLaunchKernelGGL(es_coef_kernel, dim3((unsigned)B), dim3(kEsThreads), 0, st, K, L, es, row_status);
+  const dim3 g2((unsigned)es.T2, (unsigned)B);
   if (L == 1) {
-    hipLaunchKernelGGL((es_eval_kernel<float, 1>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
-    hipLaunchKernelGGL((es_eval_kernel<double, 1>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
+    hipLaunchKernelGGL((es_eval_kernel<1>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
+    hipLaunchKernelGGL((es_eval_wide_kernel<1>), dim3(kEsScanWGs), dim3(kEsThreads), 0, st, p, q1, q2, V, B, K, r,
+                       es);
   } else {
-    hipLaunchKernelGGL((es_eval_kernel<float, 2>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
-    hipLaunchKernelGGL((es_eval_kernel<double, 2>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
+    hipLaunchKernelGGL((es_eval_kernel<2>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
+    hipLaunchKernelGGL((es_eval_wide_kernel<2>), dim3(kEsScanWGs), dim3(kEsThreads), 0, st, p, q1, q2, V, B, K, r,
+                       es);
   }
   return hipGetLastError();
 }
