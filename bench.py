@@ -22,6 +22,11 @@ sys.path.insert(0, ROOT)
 
 FP32_PEAK_TFLOPS = 157.3  # MI355X fp32 vector peak
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E
+# fp32 VALU issue without packed math: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3 T lane-instructions/s;
+# the exponential-sum evaluation exp(-a w) and its accumulation (mul, v_exp_f32, fma) takes 4 issue slots
+# (the transcendental two) for 4 FLOP, so its ALU ceiling is 39.3 TFLOP/s
+ES_PEAK_TFLOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+ES_FLOP_PER_EVAL = 4.0
 METRIC = "positions/sec (V=32000, K=2) + % FP32 VALU peak (r) / % HBM BW (resample)"
 
 
@@ -30,7 +35,7 @@ def kernel_source_digest() -> str:
     of api.hip are left out: they launch nothing)."""
     h = hashlib.sha256()
     for f in ("csrc/common.h", "csrc/induced.hip", "csrc/sample.hip", "csrc/tlp.hip", "csrc/rank.h",
-              "csrc/optimum.hip", "csrc/alphabet.hip", "build.py"):
+              "csrc/optimum.hip", "csrc/alphabet.hip", "csrc/expsum.hip", "build.py"):
         with open(os.path.join(ROOT, "paper_2410_18234_amd", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -83,6 +88,42 @@ def cpu_tlp_step(p, q1, q2, drafts, u, s, tail):
         betas[b, :len(res["omega1"]), :len(res["omega1"])] = res["beta"]
     _, stok, _ = tlp.select(p, q1, q2, drafts, u, om, betas, tail)
     return oracle.accept_resample(p, r, stok, u)
+
+
+def expsum_evals(p_np, q_np, K: int, q2_np=None) -> float:
+    """Nominal work of the exponential-sum r: every positive-weight token of a row
+    meets every node of the row's grid once in the moments and once in the
+    evaluation.  The grid (step 1/2 in t = ln a) spans from ln 1e-8 - ln D_max
+    to ln ln 1e8 - ln D_min, D the denominators of the row (K i.i.d. drafts:
+    K w_min (w_min alone when K >= 3 and some token has p = 0 < q) to K w_max;
+    two laws: w1_min + w2_min to w1_max + w2_max)."""
+    import math
+
+    import numpy as np
+    p64 = p_np.astype(np.float64)
+    laws = [q_np] if q2_np is None else [q_np, q2_np]
+    total = 0.0
+    for b in range(p64.shape[0]):
+        pos, wmin, wmax = [], [], []
+        for qq in laws:
+            q64 = qq[b].astype(np.float64)
+            m = (q64 > 0) & (p64[b] > 0)
+            pos.append(int(m.sum()))
+            w = p64[b][m] / q64[m]
+            wmin.append(w.min() if w.size else math.inf)
+            wmax.append(w.max() if w.size else 0.0)
+        if min(pos) == 0:
+            continue
+        if q2_np is None:
+            q0 = float(q_np[b].astype(np.float64)[(q_np[b] > 0) & (p64[b] == 0)].sum())
+            dmin = K * wmin[0] if (K == 2 or q0 == 0.0) else wmin[0]
+            dmax = K * wmax[0]
+        else:
+            dmin, dmax = wmin[0] + wmin[1], wmax[0] + wmax[1]
+        nk = math.ceil((math.log(math.log(1e8)) - math.log(dmin)) / 0.5) - \
+            math.floor((math.log(1e-8) - math.log(dmax)) / 0.5) + 1
+        total += 2.0 * sum(pos) * nk
+    return total
 
 
 def succ_flops(q_np, K: int) -> float:
@@ -156,6 +197,10 @@ def main():
     ap.add_argument("--resample-reps", type=int, default=20)
     ap.add_argument("--tlp-tail", choices=["sorted", "half"], default=None,
                     help="truncated-LP workloads: Omega_2 sorted (Algorithm 2) or halves (its sort-free variant)")
+    ap.add_argument("--method", choices=["expsum", "exact"], default="expsum",
+                    help="induced distribution: exponential-sum quadrature (O(n) per node) or the exact pairwise "
+                         "sums (O(n^2) for K=2, O(n^3) for K=3); the truncated LP, alphabet and optimum workloads "
+                         "keep their own paths")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -193,7 +238,16 @@ def main():
     s_max = cfg.s_max
     r = torch.empty_like(p)
     status = torch.zeros(B, dtype=torch.int32, device=dev)
-    if tlp_s:
+    use_es = args.method == "expsum" and not (tlp_s or cfg.alphabet or cfg.diag)
+    if use_es and (cfg.successive or cfg.pair):
+        ws_bytes = mdss.workspace_bytes_pair_expsum(B, V)
+        if cfg.successive:
+            r_stages = torch.empty((K - 1, B, V), dtype=torch.float32, device=dev)
+            r = r_stages[K - 2]
+            u_sel = torch.from_numpy(np.ascontiguousarray(w["u"][:, :1].repeat(K - 1, 1))).to(dev)
+    elif use_es:
+        ws_bytes = mdss.workspace_bytes_expsum(B, V, K)
+    elif tlp_s:
         ws_bytes = mdss.workspace_bytes_tlp(B, V, tail)
     elif cfg.successive:
         ws_bytes = mdss.workspace_bytes_successive(B, V)
@@ -207,7 +261,14 @@ def main():
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
 
     def induced():
-        if tlp_s:
+        if use_es:
+            if cfg.successive:
+                mdss.induced_dist_successive_expsum(p, q, K, r_stages=r_stages, row_status=status, workspace=ws)
+            elif cfg.pair:
+                mdss.induced_dist_pair_expsum(p, q, q2, r=r, row_status=status, workspace=ws)
+            else:
+                mdss.induced_dist_expsum(p, q, K, r=r, row_status=status, workspace=ws)
+        elif tlp_s:
             mdss.truncated_lp(p, q, q2, tlp_s, tail, r=r, omega1=omega1, w=wtab, accept=acc_prob,
                               row_status=status, workspace=ws)
         elif cfg.successive:
@@ -314,6 +375,23 @@ def main():
                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": counted_traffic(cfg.name, rank_name, digest),
                     "kernel": f"mdss_truncated_lp ({rank_name} + tlp_lp_kernel)", "avg_ms": round(r_ms, 4),
                     "bytes_per_launch": nbytes, "s": tlp_s, "tail": "sorted" if tail == 0 else "half"}
+    elif use_es:
+        stages = (K - 1) if cfg.successive else 1
+        evals = expsum_evals(w["p"], w["q"], 2 if cfg.successive else K, w.get("q2"))
+        if cfg.successive:  # later stages: two laws (the previous stage law, q); counted with q on both sides
+            evals += (K - 2) * expsum_evals(w["p"], w["q"], 2, w["q"])
+        flops = ES_FLOP_PER_EVAL * evals
+        achieved = flops / (r_ms * 1e-3) / 1e12
+        api = ("mdss_induced_dist_successive_expsum" if cfg.successive else
+               "mdss_induced_dist_pair_expsum" if cfg.pair else "mdss_induced_dist_expsum")
+        roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": round(ES_PEAK_TFLOPS, 2),
+                    "unit": "TFLOP/s", "frac": round(achieved / ES_PEAK_TFLOPS, 4),
+                    "traffic": counted_traffic(cfg.name, "es_moments_kernel", digest),
+                    "kernel": f"{api} (es_moments_kernel + es_coef_kernel + es_eval_kernel"
+                              f"{', per stage' if stages > 1 else ''})",
+                    "avg_ms": round(r_ms, 4), "flops_per_launch": flops, "evals_per_launch": evals,
+                    "peak_basis": "fp32 VALU issue without packed math (256 CU x 4 SIMD x 16 lanes x 2.4 GHz), "
+                                  "4 issue slots and 4 FLOP per node evaluation (mul, v_exp_f32 at half rate, fma)"}
     else:
         flops = succ_flops(w["q"], K) if cfg.successive else pair_flops(w["q"], K, w.get("q2"))
         achieved = flops / (r_ms * 1e-3) / 1e12
@@ -323,6 +401,36 @@ def main():
                     "traffic": counted_traffic(cfg.name, sweep_name, digest),
                     "kernel": f"{'mdss_induced_dist_successive' if cfg.successive else 'mdss_induced_dist_pair' if cfg.pair else 'mdss_induced_dist'} ({sweep_name} + "
                               "preparation)", "avg_ms": round(r_ms, 4), "flops_per_launch": flops}
+
+    exact_pairwise = None
+    if use_es:
+        # the pairwise O(n^2) (K=2) / O(n^3) (K=3) sums the quadrature replaces, measured on the same rows
+        flops_x = succ_flops(w["q"], K) if cfg.successive else pair_flops(w["q"], K, w.get("q2"))
+        if cfg.successive:
+            ws_x = torch.empty(mdss.workspace_bytes_successive(B, V), dtype=torch.uint8, device=dev)
+            run_x = lambda: mdss.induced_dist_successive(p, q, K, row_status=status, workspace=ws_x)
+        elif cfg.pair:
+            ws_x = torch.empty(mdss.workspace_bytes_pair(B, V), dtype=torch.uint8, device=dev)
+            run_x = lambda: mdss.induced_dist_pair(p, q, q2, row_status=status, workspace=ws_x)
+        else:
+            ws_x = torch.empty(mdss.workspace_bytes(B, V, K, s_max or 0), dtype=torch.uint8, device=dev)
+            run_x = lambda: mdss.induced_dist(p, q, K, s_max=s_max, row_status=status, workspace=ws_x)
+        run_x()
+        torch.cuda.synchronize()
+        xe = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(3)]
+        for a, b in xe:
+            a.record()
+            run_x()
+            b.record()
+        torch.cuda.synchronize()
+        x_ms = float(np.median([a.elapsed_time(b) for a, b in xe]))
+        del ws_x
+        exact_pairwise = {"avg_ms": round(x_ms, 4), "flops_per_launch": flops_x,
+                          "achieved": round(flops_x / (x_ms * 1e-3) / 1e12, 3), "peak": FP32_PEAK_TFLOPS,
+                          "unit": "TFLOP/s", "frac": round(flops_x / (x_ms * 1e-3) / 1e12 / FP32_PEAK_TFLOPS, 4),
+                          "speedup_of_quadrature": round(x_ms / r_ms, 2),
+                          "kernel": "mdss_induced_dist / _pair / _successive (pairwise sums; 6 FLOP per unordered "
+                                    "pair, 4 per (query, pair) for K = 3)"}
 
     # accept / resample pass over every row with the residual written (12 B per token)
     _, sel_token = select()
@@ -390,6 +498,8 @@ def main():
                    "expected_acceptance": round(expected_acc, 5)},
         "roofline": roofline,
         "roofline_resample": roofline_resample,
+        "method": "exponential-sum quadrature" if use_es else "exact pairwise sums",
+        "exact_pairwise": exact_pairwise,
         "cpu_baseline": None,
         "kernel_source_digest": digest,
     }
