@@ -35,9 +35,9 @@
 //
 // Precision: each tile scales its weights by a power of two (w' = w 2^tau, the
 // node rates by 2^-tau) and evaluates in fp32; a tile whose weight ratios leave
-// the fp32 normal range or span more than 2^160 is left to an fp64 kernel that
-// scans the tile records.  Zero-weight tokens (p = 0 < q) enter in closed
-// form; a flagged row gets NaN.
+// the fp32 normal range or span more than 2^160 is redone in fp64 by the
+// coefficient kernel, which then evaluates that row in fp64 as well.
+// Zero-weight tokens (p = 0 < q) enter in closed form; a flagged row gets NaN.
 #include "common.h"
 
 #include <float.h>
@@ -57,7 +57,6 @@ constexpr int kEsEvalPer = 8;                           // tokens per thread, ev
 constexpr int kEsEvalTile = kEsThreads * kEsEvalPer;    // 2048 tokens per evaluation tile
 constexpr int kEsMaxNodes = 480;                        // nodes of a row (weights spanning <= 2^300)
 constexpr int kEsMaxWin = 496;                          // nodes of a tile window; table stride
-constexpr int kEsScanWGs = 64;                          // workgroups of the fp64 tile kernels
 constexpr double kEsStep = 0.5;                         // h
 constexpr double kEsLnEps = -18.420680743952367;        // ln 1e-8: left-tail cut
 constexpr double kEsLnLnInvEps = 2.9134941423228814;    // ln ln 1e8: right-tail cut
@@ -76,7 +75,7 @@ struct alignas(64) EsTile {
   int32_t bad;   // a NaN, negative or infinite probability was read
   int32_t ka;    // first node of the window
   int32_t nw;    // window length (0: no positive weight)
-  int32_t wide;  // 1: the moments are taken by the fp64 kernel
+  int32_t wide;  // 1: the moments are taken in fp64 (by the coefficient kernel)
   int32_t pad[3];
 };
 
@@ -85,7 +84,7 @@ struct alignas(64) EsPlan {
   int32_t flags;  // row status bits; a flagged row gets r = NaN
   int32_t k_lo;   // first node of the row's grid
   int32_t nk;     // nodes of the row's grid (0: no quadrature term)
-  int32_t pad0;
+  int32_t fp64;   // 1: the row is evaluated in fp64 by the coefficient kernel
   double q0[2];   // per law: draft mass of zero-weight tokens
   double pad[5];
 };
@@ -96,7 +95,6 @@ struct EsWork {
   EsPlan* plan;     // [B]
   double* ctab;     // [B][L][kEsMaxWin] c_k, k = k_lo + i
   double* ptab;     // [B][L][kEsMaxWin] prefix sums: ptab[i] = c_(k_lo) + ... + c_(k_lo + i - 1)
-  int32_t* wide2;   // [B][T2] evaluation tiles left to the fp64 kernel
   int64_t T1, T2;
 };
 
@@ -209,6 +207,51 @@ __device__ __forceinline__ Real wave_reduce_scatter(Real (&v)[NB], int lane) {
   return x;
 }
 
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// fp32, 16 values: the same sum without LDS traffic.  Stages by lane bit 2 and
+// bit 3 exchange within 16-lane rows by DPP rotations (a rotation by 4 or 8
+// always flips that bit and keeps the others below bit 4, so every lane is
+// paired once), bits 4 and 5 by the row / half swaps of gfx950, and the two
+// low bits are summed across the quad.  Lane l holds the total of value
+// 8 b2 + 4 b3 + 2 b4 + b5 (b_i = bit i of l).
+__device__ __forceinline__ float wave_reduce_scatter16_f32(float (&v)[16], int lane) {
+  {
+    const bool up = (lane & 4) != 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float send = up ? v[i] : v[i + 8];
+      const float keep = up ? v[i + 8] : v[i];
+      v[i] = keep + dpp<0x124>(send);  // row_ror:4
+    }
+  }
+  {
+    const bool up = (lane & 8) != 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float send = up ? v[i] : v[i + 4];
+      const float keep = up ? v[i + 4] : v[i];
+      v[i] = keep + dpp<0x128>(send);  // row_ror:8
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]), __float_as_uint(v[i + 2]), false, false);
+    v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[0]), __float_as_uint(v[1]), false, false);
+    v[0] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  float x = v[0];
+  x += dpp<0xB1>(x);  // quad_perm [1,0,3,2]
+  x += dpp<0x4E>(x);  // quad_perm [2,3,0,1]
+  return x;
+}
+
 // ------------------------------------------------------------------ moments
 // Statistics and moments of one tile of one law.  The fp32 instantiation
 // leaves a tile with an out-of-range ratio or a weight span above 2^160 to the
@@ -230,8 +273,14 @@ __device__ __forceinline__ void es_moments_block(const Real* __restrict__ s_w, c
 #pragma unroll
     for (int i = 0; i < NB; ++i) acc[i] = es_fma(qq, es_decay(rt[i], w), acc[i]);
   }
-  const Real tot = wave_reduce_scatter<NB, Real>(acc, lane);
-  if ((lane & (64 / NB - 1)) == 0) s_red[wid][nb + lane / (64 / NB)] = tot;
+  if constexpr (NB == 16 && sizeof(Real) == 4) {
+    const Real tot = wave_reduce_scatter16_f32(acc, lane);
+    const int node = ((lane >> 2) & 1) * 8 + ((lane >> 3) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 5) & 1);
+    if ((lane & 3) == 0) s_red[wid][nb + node] = tot;
+  } else {
+    const Real tot = wave_reduce_scatter<NB, Real>(acc, lane);
+    if ((lane & (64 / NB - 1)) == 0) s_red[wid][nb + lane / (64 / NB)] = tot;
+  }
 }
 
 template <typename Real>
@@ -378,197 +427,13 @@ __global__ __launch_bounds__(kEsThreads) void es_moments_kernel(const float* __r
   es_moments_tile<float>(p + b * V, (l == 0 ? q1 : q2) + b * V, V, t, es.tile + idx, es.part + idx * kEsMaxWin);
 }
 
-// A few workgroups scan the tile records and take the tiles marked wide in fp64.
-__global__ __launch_bounds__(kEsThreads) void es_moments_wide_kernel(const float* __restrict__ p,
-                                                                      const float* __restrict__ q1,
-                                                                      const float* __restrict__ q2, int64_t V,
-                                                                      int64_t B, int L, EsWork es) {
-  __shared__ int s_n;
-  __shared__ int s_list[kEsThreads];
-  const int64_t N = B * es.T1 * L;
-  for (int64_t c0 = (int64_t)blockIdx.x * kEsThreads; c0 < N; c0 += (int64_t)gridDim.x * kEsThreads) {
-    if (threadIdx.x == 0) s_n = 0;
-    __syncthreads();
-    const int64_t i = c0 + threadIdx.x;
-    if (i < N && es.tile[i].wide && !es.tile[i].bad) s_list[atomicAdd(&s_n, 1)] = threadIdx.x;
-    __syncthreads();
-    const int n = s_n;
-    for (int j = 0; j < n; ++j) {
-      const int64_t idx = c0 + s_list[j];
-      const int l = (int)(idx % L);
-      const int64_t bt = idx / L, t = bt % es.T1, b = bt / es.T1;
-      es_moments_tile<double>(p + b * V, (l == 0 ? q1 : q2) + b * V, V, t, es.tile + idx,
-                              es.part + idx * kEsMaxWin);
-      __syncthreads();
-    }
-    __syncthreads();
-  }
-}
-
-// ------------------------------------------------------------------ coefficients
-// One workgroup per row: the tile records merged in tile order (fp64), the
-// row's grid range, S_k from the tile windows, c_k and their prefix sums.
-// K i.i.d. drafts: c_k = K h a_k S_k^(K-1) (K >= 3 keeps the zero-weight mass
-// Q0 in S).  Two laws: the queries of law 1 take h a_k S_k of law 2 and the
-// queries of law 2 take h a_k S_k of law 1.
-__global__ __launch_bounds__(kEsThreads) void es_coef_kernel(int K, int L, EsWork es,
-                                                              int32_t* __restrict__ row_status) {
-  const int64_t b = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  __shared__ double s_d[kEsWaves][6];
-  __shared__ int s_i[kEsWaves][3];
-  __shared__ EsPlan s_plan;
-  __shared__ int s_ka[kEsThreads][2], s_nw[kEsThreads][2];
-  __shared__ double s_qp[kEsThreads][2];
-
-  double wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0, 0.0}, q0[2] = {0.0, 0.0};
-  int npos[2] = {0, 0}, bad = 0;
-  for (int64_t t = tid; t < es.T1; t += kEsThreads) {
-    for (int l = 0; l < L; ++l) {
-      const EsTile& r = es.tile[(b * es.T1 + t) * L + l];
-      wmin[l] = fmin(wmin[l], r.wmin);
-      wmax[l] = fmax(wmax[l], r.wmax);
-      q0[l] += r.q0;
-      npos[l] += r.npos;
-      bad |= r.bad;
-    }
-  }
-  for (int l = 0; l < 2; ++l) {
-    wmin[l] = wave_min64(wmin[l]);
-    wmax[l] = wave_max64(wmax[l]);
-    q0[l] = wave_sum(q0[l]);
-    npos[l] = wave_sum_int(npos[l]);
-  }
-  bad = wave_sum_int(bad);
-  if (lane == 0) {
-    for (int l = 0; l < 2; ++l) {
-      s_d[wid][l] = wmin[l];
-      s_d[wid][2 + l] = wmax[l];
-      s_d[wid][4 + l] = q0[l];
-      s_i[wid][l] = npos[l];
-    }
-    s_i[wid][2] = bad;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    for (int l = 0; l < 2; ++l) {
-      wmin[l] = s_d[0][l];
-      wmax[l] = s_d[0][2 + l];
-      q0[l] = s_d[0][4 + l];
-      npos[l] = s_i[0][l];
-      for (int i = 1; i < kEsWaves; ++i) {
-        wmin[l] = fmin(wmin[l], s_d[i][l]);
-        wmax[l] = fmax(wmax[l], s_d[i][2 + l]);
-        q0[l] += s_d[i][4 + l];
-        npos[l] += s_i[i][l];
-      }
-    }
-    bad = 0;
-    for (int i = 0; i < kEsWaves; ++i) bad |= s_i[i][2];
-    EsPlan pl;
-    pl.flags = bad ? kRowBadProb : 0;
-    pl.k_lo = 0;
-    pl.nk = 0;
-    pl.pad0 = 0;
-    pl.q0[0] = q0[0];
-    pl.q0[1] = q0[1];
-    for (int i = 0; i < 5; ++i) pl.pad[i] = 0.0;
-    const bool any = (L == 1) ? npos[0] > 0 : (npos[0] > 0 && npos[1] > 0);
-    if (!pl.flags && any) {
-      double dmin, dmax;
-      if (L == 1) {
-        // K = 2 takes the zero-weight tokens in closed form; K >= 3 keeps them in S (denominator w(y) alone)
-        dmin = (K == 2 || q0[0] == 0.0) ? K * wmin[0] : wmin[0];
-        dmax = K * wmax[0];
-      } else {
-        dmin = wmin[0] + wmin[1];
-        dmax = wmax[0] + wmax[1];
-      }
-      const int k_lo = (int)floor((kEsLnEps - log(dmax)) / kEsStep);
-      const int k_hi = (int)ceil((kEsLnLnInvEps - log(dmin)) / kEsStep);
-      pl.k_lo = k_lo;
-      pl.nk = k_hi - k_lo + 1;
-      if (pl.nk > kEsMaxNodes) {  // only rows with probabilities far above 1 get here
-        pl.flags = kRowRange;
-        pl.nk = 0;
-      }
-    }
-    s_plan = pl;
-    es.plan[b] = pl;
-    if (row_status && pl.flags) row_status[b] |= pl.flags;
-  }
-  __syncthreads();
-  const EsPlan pl = s_plan;
-  if (pl.nk == 0) return;
-  // S_l(k) for the two nodes of this thread, tiles taken in order
-  double S[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
-  const int kk[2] = {pl.k_lo + tid, pl.k_lo + tid + kEsThreads};
-  for (int64_t t0 = 0; t0 < es.T1; t0 += kEsThreads) {
-    __syncthreads();
-    if (t0 + tid < es.T1) {
-      for (int l = 0; l < L; ++l) {
-        const EsTile& r = es.tile[(b * es.T1 + t0 + tid) * L + l];
-        s_ka[tid][l] = r.ka;
-        s_nw[tid][l] = r.nw;
-        s_qp[tid][l] = r.qpos;
-      }
-    }
-    __syncthreads();
-    const int nt = (int)std::min<int64_t>(kEsThreads, es.T1 - t0);
-    for (int j = 0; j < nt; ++j) {
-      for (int l = 0; l < L; ++l) {
-        const int ka = s_ka[j][l], nw = s_nw[j][l];
-        if (nw == 0) continue;  // no positive weight in this tile
-        const double* pt = es.part + ((b * es.T1 + t0 + j) * L + l) * kEsMaxWin;
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int k = kk[u];
-          S[u][l] += (k < ka) ? s_qp[j][l] : ((k < ka + nw) ? pt[k - ka] : 0.0);
-        }
-      }
-    }
-  }
-  for (int u = 0; u < 2; ++u) {
-    const int i = tid + u * kEsThreads;
-    if (i >= pl.nk) continue;
-    const double ha = kEsStep * exp((double)kk[u] * kEsStep);
-    if (L == 1) {
-      const double s = S[u][0] + (K >= 3 ? pl.q0[0] : 0.0);
-      double sp = 1.0;
-      for (int j = 1; j < K; ++j) sp *= s;
-      es.ctab[(b * L) * kEsMaxWin + i] = (double)K * ha * sp;
-    } else {
-      es.ctab[(b * L + 0) * kEsMaxWin + i] = ha * S[u][1];
-      es.ctab[(b * L + 1) * kEsMaxWin + i] = ha * S[u][0];
-    }
-  }
-  __syncthreads();
-  // prefix sums in node order: wave 0, eight consecutive nodes per lane
-  if (wid == 0) {
-    for (int l = 0; l < L; ++l) {
-      const double* c = es.ctab + (b * L + l) * kEsMaxWin;
-      double* pt = es.ptab + (b * L + l) * kEsMaxWin;
-      double loc = 0.0;
-      for (int j = 0; j < 8; ++j) {
-        const int i = lane * 8 + j;
-        if (i < pl.nk) loc += c[i];
-      }
-      const double incl = wave_inclusive_scan(loc, lane);
-      double run = incl - loc;
-      for (int j = 0; j < 8; ++j) {
-        const int i = lane * 8 + j;
-        if (i <= pl.nk && i < kEsMaxWin) pt[i] = run;
-        if (i < pl.nk) run += c[i];
-      }
-    }
-  }
-}
-
 // ------------------------------------------------------------------ evaluation
 // One evaluation tile (2048 tokens) of a row: r(y) = p(y) [P + sum over the
 // window of c_k exp(-a_k w(y))] + the zero-weight closed forms, P = the sum of
-// c_k below the window.  The fp32 instantiation returns false, writing
-// nothing, for a tile it leaves to the fp64 one.
+// c_k below the window.  The fp32 instantiation runs only on rows without an
+// fp64 tile: such a row has every ratio in the fp32 normal range and (two laws)
+// a weight span within 2^160, so every evaluation tile of it does too (an
+// evaluation tile lies inside one moments tile of each law).
 template <typename Real, int L>
 __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restrict__ q1b,
                              const float* __restrict__ q2b, int64_t V, int K, int64_t t, float* __restrict__ rb,
@@ -641,7 +506,7 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
       }
       int tau = 0, range = 0;
       if (hi > 0.0) es_scale(lo, hi, tau, range);
-      s_go = f64 || !(od || range > kEsWideRange);
+      s_go = f64 || !(od || range > kEsWideRange);  // the fp32 path never sees a wide tile (see above)
       s_tau = f64 ? 0 : tau;
       for (int l = 0; l < L; ++l) {
         int i0 = pl.nk, cnt = 0;
@@ -657,7 +522,14 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
       }
     }
     __syncthreads();
-    if (!s_go) return false;
+    if (!s_go) {
+#pragma unroll
+      for (int i = 0; i < kEsEvalPer; ++i) {
+        const int64_t x = base + i * kEsThreads + tid;
+        if (x < V) rb[x] = NAN;
+      }
+      return false;
+    }
   }
   const int tau = (pl.nk > 0) ? s_tau : 0;
 #pragma unroll
@@ -750,6 +622,202 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
   return true;
 }
 
+// ------------------------------------------------------------------ coefficients
+// One workgroup per row, after the moments.  (1) Tiles the fp32 pass left
+// aside are taken in fp64, in tile order.  (2) The tile records are merged in
+// tile order (fp64): flags, zero-weight masses, the row's grid range.  (3) S_k
+// from the tile windows, c_k and their prefix sums.  K i.i.d. drafts:
+// c_k = K h a_k S_k^(K-1) (K >= 3 keeps the zero-weight mass Q0 in S); two
+// laws: the queries of law 1 take h a_k S_k of law 2 and those of law 2 take
+// h a_k S_k of law 1.  (4) A row with an fp64 tile (or, for two laws, weights
+// spanning more than 2^160) is evaluated here in fp64.
+template <int L>
+__global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __restrict__ p,
+                                                              const float* __restrict__ q1,
+                                                              const float* __restrict__ q2, int64_t V, int K,
+                                                              float* __restrict__ r, EsWork es,
+                                                              int32_t* __restrict__ row_status) {
+  const int64_t b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t nrec = es.T1 * L;
+  EsTile* rec = es.tile + b * nrec;
+  double* part = es.part + b * nrec * kEsMaxWin;
+  const float* pb = p + b * V;
+  __shared__ double s_d[kEsWaves][6];
+  __shared__ int s_i[kEsWaves][3];
+  __shared__ EsPlan s_plan;
+  __shared__ double s_c[L][kEsMaxWin];
+  __shared__ double s_p[L][kEsMaxWin];
+
+  // (1) fp64 tiles
+  int w = 0;
+  for (int64_t i = tid; i < nrec; i += kEsThreads) w |= rec[i].wide && !rec[i].bad;
+  const int anywide = __syncthreads_or(w);
+  if (anywide) {
+    for (int64_t i = 0; i < nrec; ++i) {
+      if (!(rec[i].wide && !rec[i].bad)) continue;  // uniform: every thread reads the same record
+      const int l = (int)(i % L);
+      es_moments_tile<double>(pb, (l == 0 ? q1 : q2) + b * V, V, i / L, rec + i, part + i * kEsMaxWin);
+      __syncthreads();
+    }
+  }
+  // (2) merge
+  double wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0, 0.0}, q0[2] = {0.0, 0.0};
+  int npos[2] = {0, 0}, bad = 0;
+  for (int64_t t = tid; t < es.T1; t += kEsThreads) {
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      const EsTile& e = rec[t * L + l];
+      wmin[l] = fmin(wmin[l], e.wmin);
+      wmax[l] = fmax(wmax[l], e.wmax);
+      q0[l] += e.q0;
+      npos[l] += e.npos;
+      bad |= e.bad;
+    }
+  }
+  for (int l = 0; l < 2; ++l) {
+    wmin[l] = wave_min64(wmin[l]);
+    wmax[l] = wave_max64(wmax[l]);
+    q0[l] = wave_sum(q0[l]);
+    npos[l] = wave_sum_int(npos[l]);
+  }
+  bad = wave_sum_int(bad);
+  if (lane == 0) {
+    for (int l = 0; l < 2; ++l) {
+      s_d[wid][l] = wmin[l];
+      s_d[wid][2 + l] = wmax[l];
+      s_d[wid][4 + l] = q0[l];
+      s_i[wid][l] = npos[l];
+    }
+    s_i[wid][2] = bad;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int l = 0; l < 2; ++l) {
+      wmin[l] = s_d[0][l];
+      wmax[l] = s_d[0][2 + l];
+      q0[l] = s_d[0][4 + l];
+      npos[l] = s_i[0][l];
+      for (int i = 1; i < kEsWaves; ++i) {
+        wmin[l] = fmin(wmin[l], s_d[i][l]);
+        wmax[l] = fmax(wmax[l], s_d[i][2 + l]);
+        q0[l] += s_d[i][4 + l];
+        npos[l] += s_i[i][l];
+      }
+    }
+    bad = 0;
+    for (int i = 0; i < kEsWaves; ++i) bad |= s_i[i][2];
+    EsPlan pl;
+    pl.flags = bad ? kRowBadProb : 0;
+    pl.k_lo = 0;
+    pl.nk = 0;
+    pl.fp64 = anywide ? 1 : 0;
+    pl.q0[0] = q0[0];
+    pl.q0[1] = q0[1];
+    for (int i = 0; i < 5; ++i) pl.pad[i] = 0.0;
+    const bool any = (L == 1) ? npos[0] > 0 : (npos[0] > 0 && npos[1] > 0);
+    if (!pl.flags && any) {
+      double dmin, dmax;
+      if (L == 1) {
+        // K = 2 takes the zero-weight tokens in closed form; K >= 3 keeps them in S (denominator w(y) alone)
+        dmin = (K == 2 || q0[0] == 0.0) ? K * wmin[0] : wmin[0];
+        dmax = K * wmax[0];
+      } else {
+        dmin = wmin[0] + wmin[1];
+        dmax = wmax[0] + wmax[1];
+        int tau, range;
+        es_scale(fmin(wmin[0], wmin[1]), fmax(wmax[0], wmax[1]), tau, range);
+        if (range > kEsWideRange) pl.fp64 = 1;  // an evaluation tile mixes both laws' weights
+      }
+      const int k_lo = (int)floor((kEsLnEps - log(dmax)) / kEsStep);
+      const int k_hi = (int)ceil((kEsLnLnInvEps - log(dmin)) / kEsStep);
+      pl.k_lo = k_lo;
+      pl.nk = k_hi - k_lo + 1;
+      if (pl.nk > kEsMaxNodes) {  // only rows with probabilities far above 1 get here
+        pl.flags = kRowRange;
+        pl.nk = 0;
+      }
+    }
+    if (pl.flags) pl.fp64 = 0;
+    s_plan = pl;
+    es.plan[b] = pl;
+    if (row_status && pl.flags) row_status[b] |= pl.flags;
+  }
+  __syncthreads();
+  const EsPlan pl = s_plan;
+  if (pl.nk > 0) {
+    // (3) S_l(k), two nodes per thread, tiles in order; every load is issued
+    // (at a clamped index) and the window test selects afterwards
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int i = tid + u * kEsThreads;
+      if (i >= pl.nk) continue;
+      const int k = pl.k_lo + i;
+      double S[L];
+#pragma unroll
+      for (int l = 0; l < L; ++l) S[l] = 0.0;
+#pragma unroll 4
+      for (int64_t t = 0; t < es.T1; ++t) {
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          const EsTile& e = rec[t * L + l];
+          const int ka = e.ka, nw = e.nw;
+          const int j = min(max(k - ka, 0), kEsMaxWin - 1);
+          const double v = part[(t * L + l) * kEsMaxWin + j];
+          S[l] += (nw == 0) ? 0.0 : ((k < ka) ? e.qpos : ((k < ka + nw) ? v : 0.0));
+        }
+      }
+      const double ha = kEsStep * exp((double)k * kEsStep);
+      if (L == 1) {
+        const double sm = S[0] + (K >= 3 ? pl.q0[0] : 0.0);
+        double sp = 1.0;
+        for (int j = 1; j < K; ++j) sp *= sm;
+        s_c[0][i] = (double)K * ha * sp;
+      } else {
+        s_c[0][i] = ha * S[L - 1];
+        s_c[L - 1][i] = ha * S[0];
+      }
+    }
+    __syncthreads();
+    // prefix sums in node order: wave 0, eight consecutive nodes per lane
+    if (wid == 0) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        double loc = 0.0;
+        for (int j = 0; j < 8; ++j) {
+          const int i = lane * 8 + j;
+          if (i < pl.nk) loc += s_c[l][i];
+        }
+        const double incl = wave_inclusive_scan(loc, lane);
+        double run = incl - loc;
+        for (int j = 0; j < 8; ++j) {
+          const int i = lane * 8 + j;
+          if (i <= pl.nk && i < kEsMaxWin) s_p[l][i] = run;
+          if (i < pl.nk) run += s_c[l][i];
+        }
+      }
+    }
+    __syncthreads();
+    double* ct = es.ctab + b * L * kEsMaxWin;
+    double* pt = es.ptab + b * L * kEsMaxWin;
+    for (int i = tid; i <= pl.nk && i < kEsMaxWin; i += kEsThreads) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        if (i < pl.nk) ct[l * kEsMaxWin + i] = s_c[l][i];
+        pt[l * kEsMaxWin + i] = s_p[l][i];
+      }
+    }
+  }
+  // (4) rows in fp64, from the tables in LDS
+  if (pl.fp64) {
+    for (int64_t t = 0; t < es.T2; ++t) {
+      es_eval_tile<double, L>(pb, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, r + b * V, pl, &s_c[0][0],
+                              &s_p[0][0]);
+      __syncthreads();
+    }
+  }
+}
+
 template <int L>
 __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __restrict__ p,
                                                               const float* __restrict__ q1,
@@ -763,39 +831,11 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
       const int64_t x = t * kEsEvalTile + i * kEsThreads + threadIdx.x;
       if (x < V) rb[x] = NAN;
     }
-    if (threadIdx.x == 0) es.wide2[b * es.T2 + t] = 0;
     return;
   }
-  const bool done = es_eval_tile<float, L>(p + b * V, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, rb, pl,
-                                           es.ctab + b * L * kEsMaxWin, es.ptab + b * L * kEsMaxWin);
-  if (threadIdx.x == 0) es.wide2[b * es.T2 + t] = done ? 0 : 1;
-}
-
-template <int L>
-__global__ __launch_bounds__(kEsThreads) void es_eval_wide_kernel(const float* __restrict__ p,
-                                                                   const float* __restrict__ q1,
-                                                                   const float* __restrict__ q2, int64_t V, int64_t B,
-                                                                   int K, float* __restrict__ r, EsWork es) {
-  __shared__ int s_n;
-  __shared__ int s_list[kEsThreads];
-  const int64_t N = B * es.T2;
-  for (int64_t c0 = (int64_t)blockIdx.x * kEsThreads; c0 < N; c0 += (int64_t)gridDim.x * kEsThreads) {
-    if (threadIdx.x == 0) s_n = 0;
-    __syncthreads();
-    const int64_t i = c0 + threadIdx.x;
-    if (i < N && es.wide2[i]) s_list[atomicAdd(&s_n, 1)] = threadIdx.x;
-    __syncthreads();
-    const int n = s_n;
-    for (int j = 0; j < n; ++j) {
-      const int64_t idx = c0 + s_list[j];
-      const int64_t t = idx % es.T2, b = idx / es.T2;
-      const EsPlan pl = es.plan[b];
-      es_eval_tile<double, L>(p + b * V, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, r + b * V, pl,
-                              es.ctab + b * L * kEsMaxWin, es.ptab + b * L * kEsMaxWin);
-      __syncthreads();
-    }
-    __syncthreads();
-  }
+  if (pl.fp64) return;  // written by the coefficient kernel
+  es_eval_tile<float, L>(p + b * V, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, rb, pl,
+                         es.ctab + b * L * kEsMaxWin, es.ptab + b * L * kEsMaxWin);
 }
 
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
@@ -812,8 +852,6 @@ void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
   es->ctab = reinterpret_cast<double*>(c);
   c += align256(sizeof(double) * B * L * kEsMaxWin);
   es->ptab = reinterpret_cast<double*>(c);
-  c += align256(sizeof(double) * B * L * kEsMaxWin);
-  es->wide2 = reinterpret_cast<int32_t*>(c);
   es->T1 = T1;
   es->T2 = T2;
 }
@@ -821,10 +859,9 @@ void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
 }  // namespace
 
 size_t workspace_bytes_expsum(int64_t B, int64_t V, int L) {
-  const int64_t T1 = es_tiles(V, kEsMomTile), T2 = es_tiles(V, kEsEvalTile);
+  const int64_t T1 = es_tiles(V, kEsMomTile);
   return align256(sizeof(EsTile) * B * T1 * L) + align256(sizeof(double) * B * T1 * L * kEsMaxWin) +
-         align256(sizeof(EsPlan) * B) + 2 * align256(sizeof(double) * B * L * kEsMaxWin) +
-         align256(sizeof(int32_t) * B * T2);
+         align256(sizeof(EsPlan) * B) + 2 * align256(sizeof(double) * B * L * kEsMaxWin);
 }
 
 // q2 == nullptr: K i.i.d. drafts from q1; else two draft laws (K = 2).
@@ -834,18 +871,16 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
   EsWork es;
   carve_es(workspace, B, V, L, &es);
   const dim3 g1((unsigned)es.T1, (unsigned)B, (unsigned)L);
-  hipLaunchKernelGGL(es_moments_kernel, g1, dim3(kEsThreads), 0, st, p, q1, q2, V, es);
-  hipLaunchKernelGGL(es_moments_wide_kernel, dim3(kEsScanWGs), dim3(kEsThreads), 0, st, p, q1, q2, V, B, L, es);
-  hipLaunchKernelGGL(es_coef_kernel, dim3((unsigned)B), dim3(kEsThreads), 0, st, K, L, es, row_status);
   const dim3 g2((unsigned)es.T2, (unsigned)B);
+  hipLaunchKernelGGL(es_moments_kernel, g1, dim3(kEsThreads), 0, st, p, q1, q2, V, es);
   if (L == 1) {
+    hipLaunchKernelGGL((es_coef_kernel<1>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
+                       row_status);
     hipLaunchKernelGGL((es_eval_kernel<1>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
-    hipLaunchKernelGGL((es_eval_wide_kernel<1>), dim3(kEsScanWGs), dim3(kEsThreads), 0, st, p, q1, q2, V, B, K, r,
-                       es);
   } else {
+    hipLaunchKernelGGL((es_coef_kernel<2>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
+                       row_status);
     hipLaunchKernelGGL((es_eval_kernel<2>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
-    hipLaunchKernelGGL((es_eval_wide_kernel<2>), dim3(kEsScanWGs), dim3(kEsThreads), 0, st, p, q1, q2, V, B, K, r,
-                       es);
   }
   return hipGetLastError();
 }
