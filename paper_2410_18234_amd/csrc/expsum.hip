@@ -57,10 +57,12 @@ constexpr int kEsEvalPer = 8;                           // tokens per thread, ev
 constexpr int kEsEvalTile = kEsThreads * kEsEvalPer;    // 2048 tokens per evaluation tile
 constexpr int kEsMaxNodes = 480;                        // nodes of a row (weights spanning <= 2^300)
 constexpr int kEsMaxWin = 496;                          // nodes of a tile window; table stride
+constexpr int kEsTaylor = 8;                            // terms of the far-node expansion (j = 0..7)
+constexpr int kEsPart = kEsTaylor + kEsMaxWin;          // per tile: power sums, then the window moments
 constexpr double kEsStep = 0.5;                         // h
 constexpr double kEsLnEps = -18.420680743952367;        // ln 1e-8: left-tail cut
 constexpr double kEsLnLnInvEps = 2.9134941423228814;    // ln ln 1e8: right-tail cut
-constexpr double kEsLnOne = -17.328679513998633;        // ln 2^-25: below, exp(-z) rounds to 1
+constexpr double kEsLnFar = -1.3862943611198906;        // ln 1/4: at or below, a node is taken by the expansion
 constexpr double kEsLnZero = 4.6443908991413725;        // ln 104: above, exp(-z) < 2^-150
 constexpr double kEsLog2e = 1.4426950408889634;
 constexpr int kEsWideRange = 160;  // binary exponent range of a tile's weights kept in fp32
@@ -69,11 +71,11 @@ constexpr int kEsWideRange = 160;  // binary exponent range of a tile's weights 
 struct alignas(64) EsTile {
   double wmin;   // smallest positive weight (+inf if none)
   double wmax;   // largest weight (0 if none)
-  double qpos;   // draft mass of the positive-weight tokens
+  double pad0;
   double q0;     // draft mass of zero-weight tokens (q > 0 = p)
   int32_t npos;  // positive-weight tokens
   int32_t bad;   // a NaN, negative or infinite probability was read
-  int32_t ka;    // first node of the window
+  int32_t kt;    // last node taken by the expansion; the window is kt + 1 .. kt + nw
   int32_t nw;    // window length (0: no positive weight)
   int32_t wide;  // 1: the moments are taken in fp64 (by the coefficient kernel)
   int32_t pad[3];
@@ -91,10 +93,9 @@ struct alignas(64) EsPlan {
 
 struct EsWork {
   EsTile* tile;     // [B][T1][L]
-  double* part;     // [B][T1][L][kEsMaxWin] moments of each tile over its window
+  double* part;     // [B][T1][L][kEsPart] per tile: power sums T_j, then the moments of its window
   EsPlan* plan;     // [B]
   double* ctab;     // [B][L][kEsMaxWin] c_k, k = k_lo + i
-  double* ptab;     // [B][L][kEsMaxWin] prefix sums: ptab[i] = c_(k_lo) + ... + c_(k_lo + i - 1)
   int64_t T1, T2;
 };
 
@@ -111,13 +112,26 @@ __device__ __forceinline__ double wave_max64(double v) {
   return v;
 }
 
-// Window of a tile whose positive weights lie in [wlo, whi]: the nodes k where
-// exp(-a_k w) is neither 1 nor 0 in fp32 for some token of the tile.
-__device__ inline void es_window(double wlo, double whi, int& ka, int& nw) {
-  const int a = (int)ceil((kEsLnOne - log(whi)) / kEsStep);
+__device__ __forceinline__ float es_wave_min(float v) { return wave_min(v); }
+__device__ __forceinline__ float es_wave_max(float v) { return wave_max(v); }
+__device__ __forceinline__ double es_wave_min(double v) { return wave_min64(v); }
+__device__ __forceinline__ double es_wave_max(double v) { return wave_max64(v); }
+
+// Nodes of a tile whose positive weights lie in [wlo, whi]: up to kt, a_k whi
+// <= 1/4 and the expansion takes them; after kt + nw, a_k wlo > 104 and
+// exp(-a_k w) is 0 in fp32 for every token; the window in between is summed
+// with exponentials.
+__device__ inline void es_window(double wlo, double whi, int& kt, int& nw) {
+  kt = (int)floor((kEsLnFar - log(whi)) / kEsStep);
   const int z = (int)floor((kEsLnZero - log(wlo)) / kEsStep);
-  ka = a;
-  nw = max(0, min(z - a + 1, kEsMaxWin));
+  nw = max(0, min(z - kt, kEsMaxWin));
+}
+
+// 1 / j! for the expansion exp(-u) = sum_j (-u)^j / j!
+__device__ __forceinline__ double es_inv_fact(int j) {
+  double f = 1.0;
+  for (int i = 2; i <= j; ++i) f *= (double)i;
+  return 1.0 / f;
 }
 
 // Power-of-two scale that centres [wlo, whi] on 1 and the binary range it spans.
@@ -150,7 +164,8 @@ template <typename Real>
 __device__ __forceinline__ Real es_ratio(float p, float q);
 template <>
 __device__ __forceinline__ float es_ratio<float>(float p, float q) {
-  return p / q;  // correctly rounded: the fp64 ratio rounded once
+  // reciprocal and product: within 2 ulp of p / q, the same value in every kernel
+  return p * __builtin_amdgcn_rcpf(q);
 }
 template <>
 __device__ __forceinline__ double es_ratio<double>(float p, float q) {
@@ -291,6 +306,7 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
   __shared__ float s_q[kEsMomTile];
   __shared__ Real s_red[kEsWaves][kEsMaxWin];
   __shared__ Real s_rate[kEsMaxWin];
+  __shared__ Real s_tay[kEsWaves][kEsTaylor];
   __shared__ int s_wave[kEsWaves];
   __shared__ double s_d[kEsWaves][4];
   __shared__ int s_i[kEsWaves][3];
@@ -301,7 +317,8 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
   bool pos[kEsMomPer];
   Real wv[kEsMomPer];
   float qv[kEsMomPer];
-  double wmin = INFINITY, wmax = 0.0, q0 = 0.0, qpos = 0.0;
+  Real wlo = (Real)INFINITY, whi = (Real)0;
+  float q0f = 0.0f;
   int npos = 0, bad = 0, odd = 0;
 #pragma unroll
   for (int i = 0; i < kEsMomPer; ++i) {
@@ -314,44 +331,36 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     if (!f64 && pos[i]) odd |= !((float)w >= FLT_MIN && (float)w <= FLT_MAX);
     wv[i] = w;
     qv[i] = qq;
-    if (pos[i]) {
-      wmin = fmin(wmin, (double)w);
-      wmax = fmax(wmax, (double)w);
-      qpos += (double)qq;
-      ++npos;
-    } else if (qq > 0.0f && pp == 0.0f) {
-      q0 += (double)qq;
-    }
+    wlo = pos[i] ? fmin(wlo, w) : wlo;
+    whi = pos[i] ? fmax(whi, w) : whi;
+    npos += pos[i];
+    q0f += (qq > 0.0f && pp == 0.0f) ? qq : 0.0f;
   }
-  wmin = wave_min64(wmin);
-  wmax = wave_max64(wmax);
-  q0 = wave_sum(q0);
-  qpos = wave_sum(qpos);
+  const double wmin_w = (double)es_wave_min(wlo), wmax_w = (double)es_wave_max(whi);
+  const double q0 = wave_sum((double)q0f);
   npos = wave_sum_int(npos);
   bad = wave_sum_int(bad);
   odd = wave_sum_int(odd);
   if (lane == 0) {
-    s_d[wid][0] = wmin;
-    s_d[wid][1] = wmax;
+    s_d[wid][0] = wmin_w;
+    s_d[wid][1] = wmax_w;
     s_d[wid][2] = q0;
-    s_d[wid][3] = qpos;
+    s_d[wid][3] = 0.0;
     s_i[wid][0] = npos;
     s_i[wid][1] = bad;
     s_i[wid][2] = odd;
   }
   __syncthreads();
   if (tid == 0) {
-    wmin = s_d[0][0];
-    wmax = s_d[0][1];
+    double wmin = s_d[0][0], wmax = s_d[0][1];
     for (int i = 1; i < kEsWaves; ++i) {
       wmin = fmin(wmin, s_d[i][0]);
       wmax = fmax(wmax, s_d[i][1]);
     }
-    double a = 0.0, c = 0.0;
+    double a = 0.0;
     int n = 0, bd = 0, od = 0;
     for (int i = 0; i < kEsWaves; ++i) {
       a += s_d[i][2];
-      c += s_d[i][3];
       n += s_i[i][0];
       bd |= s_i[i][1];
       od |= s_i[i][2];
@@ -360,10 +369,10 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     o.wmin = wmin;
     o.wmax = wmax;
     o.q0 = a;
-    o.qpos = c;
+    o.pad0 = 0.0;
     o.npos = n;
     o.bad = bd != 0;
-    o.ka = 0;
+    o.kt = 0;
     o.nw = 0;
     o.wide = f64 ? 1 : 0;
     o.pad[0] = o.pad[1] = o.pad[2] = 0;
@@ -371,19 +380,21 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     if (n > 0) {
       es_scale(wmin, wmax, tau, range);
       if (!f64 && (od || range > kEsWideRange)) o.wide = 1;
-      es_window(wmin, wmax, o.ka, o.nw);
+      es_window(wmin, wmax, o.kt, o.nw);
     }
     *rec = o;
-    s_dec[0] = o.ka;
+    s_dec[0] = o.kt;
     s_dec[1] = o.nw;
     s_dec[2] = f64 ? 0 : tau;
-    s_dec[3] = (!o.bad && o.nw > 0 && (f64 || !o.wide)) ? 1 : 0;
+    s_dec[3] = (!o.bad && n > 0 && (f64 || !o.wide)) ? 1 : 0;
   }
   __syncthreads();
   if (!s_dec[3]) return;
-  const int ka = s_dec[0], nw = s_dec[1], tau = s_dec[2];
+  const int kt = s_dec[0], nw = s_dec[1], tau = s_dec[2];
   const int npad = (nw + 15) / 16 * 16;
-  for (int k = tid; k < npad; k += kEsThreads) s_rate[k] = (k < nw) ? es_rate<Real>(ka + k, tau) : (Real)1;
+  for (int k = tid; k < npad; k += kEsThreads) s_rate[k] = (k < nw) ? es_rate<Real>(kt + 1 + k, tau) : (Real)1;
+  // the expansion's variable u = a_kt w (scaled units) is at most 1/4 on this tile
+  const Real a_kt = (Real)ldexp(exp((double)kt * kEsStep), -tau);
   int n = 0;
   int off = block_compact_offset<kEsMomPer>(pos, s_wave, n);
 #pragma unroll
@@ -400,6 +411,24 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     s_q[j] = 0.0f;
   }
   __syncthreads();
+  {
+    // power sums T_j = sum q u^j of the tile (1/j! applied when they are used)
+    Real T[kEsTaylor];
+#pragma unroll
+    for (int j = 0; j < kEsTaylor; ++j) T[j] = (Real)0;
+    for (int m = 0; m < M; ++m) {
+      const int j = tid + m * kEsThreads;
+      const Real u = a_kt * s_w[j];
+      Real pw = (Real)s_q[j];
+#pragma unroll
+      for (int i = 0; i < kEsTaylor; ++i) {
+        T[i] += pw;
+        pw *= u;
+      }
+    }
+    const Real tot = wave_reduce_scatter<kEsTaylor, Real>(T, lane);
+    if ((lane & (64 / kEsTaylor - 1)) == 0) s_tay[wid][lane / (64 / kEsTaylor)] = tot;
+  }
   int nb = 0;
   for (; nb + 16 <= nw; nb += 16) es_moments_block<16, Real>(s_w, s_q, s_rate, M, nb, tid, lane, wid, s_red);
   if (nb + 8 <= nw) {
@@ -412,7 +441,13 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     Real s = s_red[0][k];
 #pragma unroll
     for (int i = 1; i < kEsWaves; ++i) s += s_red[i][k];
-    part[k] = (double)s;
+    part[kEsTaylor + k] = (double)s;
+  }
+  if (tid < kEsTaylor) {
+    Real s = s_tay[0][tid];
+#pragma unroll
+    for (int i = 1; i < kEsWaves; ++i) s += s_tay[i][tid];
+    part[tid] = (double)s;
   }
 }
 
@@ -424,7 +459,7 @@ __global__ __launch_bounds__(kEsThreads) void es_moments_kernel(const float* __r
   const int64_t t = blockIdx.x, b = blockIdx.y;
   const int l = blockIdx.z, L = gridDim.z;
   const int64_t idx = (b * es.T1 + t) * L + l;
-  es_moments_tile<float>(p + b * V, (l == 0 ? q1 : q2) + b * V, V, t, es.tile + idx, es.part + idx * kEsMaxWin);
+  es_moments_tile<float>(p + b * V, (l == 0 ? q1 : q2) + b * V, V, t, es.tile + idx, es.part + idx * kEsPart);
 }
 
 // ------------------------------------------------------------------ evaluation
@@ -437,19 +472,25 @@ __global__ __launch_bounds__(kEsThreads) void es_moments_kernel(const float* __r
 template <typename Real, int L>
 __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restrict__ q1b,
                              const float* __restrict__ q2b, int64_t V, int K, int64_t t, float* __restrict__ rb,
-                             const EsPlan& pl, const double* __restrict__ ctab, const double* __restrict__ ptab) {
+                             const EsPlan& pl, const double* __restrict__ ctab) {
   constexpr bool f64 = sizeof(Real) == 8;
   __shared__ Real s_w[kEsEvalTile];
   __shared__ uint16_t s_pos[kEsEvalTile];
   __shared__ Real s_acc[kEsEvalTile];
-  __shared__ Real s_rate[kEsMaxWin];
-  __shared__ Real s_coef[kEsMaxWin];
+  // one LDS area: first the row's fp64 coefficients up to kt (for the expansion),
+  // then the window's node rates and coefficients in the tile's precision
+  __shared__ Real s_tab[2 * kEsMaxWin];
+  static_assert(sizeof(Real) * 2 * kEsMaxWin >= sizeof(double) * kEsMaxNodes, "staging area");
+  Real* const s_rate = s_tab;
+  Real* const s_coef = s_tab + kEsMaxWin;
+  double* const s_cf = reinterpret_cast<double*>(s_tab);
   __shared__ int s_wave[kEsWaves];
   __shared__ double s_d[kEsWaves][2][2];
   __shared__ int s_i[kEsWaves];
-  __shared__ int s_dec[2][2];  // per law: first row node of the window, window length
+  __shared__ int s_dec[2][3];  // per law: first row node of the window, window length, last expansion node
+  __shared__ Real s_poly[kEsTaylor];
+  __shared__ Real s_akt;
   __shared__ int s_tau, s_go;
-  __shared__ Real s_base[2];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int64_t base = t * kEsEvalTile;
 
@@ -467,21 +508,19 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
     double wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0, 0.0};
     int odd = 0;
 #pragma unroll
-    for (int l = 0; l < L; ++l)
+    for (int l = 0; l < L; ++l) {
+      Real lo = (Real)INFINITY, hi = (Real)0;
 #pragma unroll
       for (int i = 0; i < kEsEvalPer; ++i) {
         pos[l][i] = pv[i] > 0.0f && qv[l][i] > 0.0f;
         const Real w = pos[l][i] ? es_ratio<Real>(pv[i], qv[l][i]) : (Real)0;
         if (!f64 && pos[l][i]) odd |= !((float)w >= FLT_MIN && (float)w <= FLT_MAX);
         wv[l][i] = w;
-        if (pos[l][i]) {
-          wmin[l] = fmin(wmin[l], (double)w);
-          wmax[l] = fmax(wmax[l], (double)w);
-        }
+        lo = pos[l][i] ? fmin(lo, w) : lo;
+        hi = pos[l][i] ? fmax(hi, w) : hi;
       }
-    for (int l = 0; l < L; ++l) {
-      wmin[l] = wave_min64(wmin[l]);
-      wmax[l] = wave_max64(wmax[l]);
+      wmin[l] = (double)es_wave_min(lo);
+      wmax[l] = (double)es_wave_max(hi);
     }
     odd = wave_sum_int(odd);
     if (lane == 0) {
@@ -509,16 +548,17 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
       s_go = f64 || !(od || range > kEsWideRange);  // the fp32 path never sees a wide tile (see above)
       s_tau = f64 ? 0 : tau;
       for (int l = 0; l < L; ++l) {
-        int i0 = pl.nk, cnt = 0;
+        int i0 = pl.nk, cnt = 0, kt = pl.k_lo + pl.nk;
         if (wmax[l] > 0.0) {
-          int ka, nw;
-          es_window(wmin[l], wmax[l], ka, nw);
-          i0 = std::min(std::max(ka - pl.k_lo, 0), pl.nk);
-          const int i1 = std::min(ka + nw - 1 - pl.k_lo, pl.nk - 1);
+          int nw;
+          es_window(wmin[l], wmax[l], kt, nw);
+          i0 = std::min(std::max(kt + 1 - pl.k_lo, 0), pl.nk);
+          const int i1 = std::min(kt + nw - pl.k_lo, pl.nk - 1);
           cnt = std::max(0, i1 - i0 + 1);
         }
         s_dec[l][0] = i0;
         s_dec[l][1] = cnt;
+        s_dec[l][2] = kt;
       }
     }
     __syncthreads();
@@ -537,13 +577,27 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
   if (pl.nk > 0) {
 #pragma unroll
     for (int l = 0; l < L; ++l) {
-      const int i0 = s_dec[l][0], cnt = s_dec[l][1];
+      const int i0 = s_dec[l][0], cnt = s_dec[l][1], kt = s_dec[l][2];
       const double* c = ctab + l * kEsMaxWin;
+      // expansion of the nodes up to kt: B_j = sum_(k <= kt) c_k (a_k / a_kt)^j, one thread per j,
+      // nodes in ascending order from LDS; stored as B_j / j! in the tile's scale
+      const int top = std::min(kt, pl.k_lo + pl.nk - 1);
+      for (int k = pl.k_lo + tid; k <= top; k += kEsThreads) s_cf[k - pl.k_lo] = c[k - pl.k_lo];
+      __syncthreads();
+      if (tid < kEsTaylor) {
+        const int j = tid;
+        const double dj = exp(-(double)j * kEsStep);  // (a_(k-1) / a_k)^j
+        double acc = 0.0;
+        for (int k = pl.k_lo; k <= top; ++k) acc = acc * dj + s_cf[k - pl.k_lo];
+        if (top >= pl.k_lo && kt > top) acc *= exp(-(double)j * (double)(kt - top) * kEsStep);
+        s_poly[j] = (Real)ldexp(acc * es_inv_fact(j), -tau);
+      }
+      if (tid == 0) s_akt = (Real)ldexp(exp((double)kt * kEsStep), -tau);
+      __syncthreads();  // the staging area becomes the window's tables
       for (int k = tid; k < cnt; k += kEsThreads) {
         s_rate[k] = es_rate<Real>(pl.k_lo + i0 + k, tau);
         s_coef[k] = (Real)ldexp(c[i0 + k], -tau);
       }
-      if (tid == 0) s_base[l] = (Real)ldexp(ptab[l * kEsMaxWin + i0], -tau);
       int n = 0;
       int off = block_compact_offset<kEsEvalPer>(pos[l], s_wave, n);
 #pragma unroll
@@ -555,7 +609,10 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
         }
       }
       __syncthreads();
-      const Real pre = s_base[l];
+      Real poly[kEsTaylor];
+#pragma unroll
+      for (int j = 0; j < kEsTaylor; ++j) poly[j] = s_poly[j];
+      const Real akt = s_akt;
       for (int j0 = 0; j0 < n; j0 += 4 * kEsThreads) {
         Real w[4], acc[4];
         int ps[4];
@@ -588,7 +645,14 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
             for (int e = 0; e < 4; ++e) blk[e] = es_fma(cf, es_decay(rt, w[e]), blk[e]);
           }
 #pragma unroll
-          for (int e = 0; e < 4; ++e) acc[e] += blk[e] + pre;
+          for (int e = 0; e < 4; ++e) {
+            // far nodes: sum_j (-u)^j B_j / j!, u = a_kt w <= 1/4 (Horner)
+            const Real nu = -akt * w[e];
+            Real pe = poly[kEsTaylor - 1];
+#pragma unroll
+            for (int j = kEsTaylor - 2; j >= 0; --j) pe = es_fma(pe, nu, poly[j]);
+            acc[e] += blk[e] + pe;
+          }
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -641,13 +705,13 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int64_t nrec = es.T1 * L;
   EsTile* rec = es.tile + b * nrec;
-  double* part = es.part + b * nrec * kEsMaxWin;
+  double* part = es.part + b * nrec * kEsPart;
   const float* pb = p + b * V;
   __shared__ double s_d[kEsWaves][6];
   __shared__ int s_i[kEsWaves][3];
   __shared__ EsPlan s_plan;
   __shared__ double s_c[L][kEsMaxWin];
-  __shared__ double s_p[L][kEsMaxWin];
+  __shared__ double s_rho[kEsMaxWin];  // e^(-m h): (a_k / a_kt) for k = kt - m
 
   // (1) fp64 tiles
   int w = 0;
@@ -657,7 +721,7 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
     for (int64_t i = 0; i < nrec; ++i) {
       if (!(rec[i].wide && !rec[i].bad)) continue;  // uniform: every thread reads the same record
       const int l = (int)(i % L);
-      es_moments_tile<double>(pb, (l == 0 ? q1 : q2) + b * V, V, i / L, rec + i, part + i * kEsMaxWin);
+      es_moments_tile<double>(pb, (l == 0 ? q1 : q2) + b * V, V, i / L, rec + i, part + i * kEsPart);
       __syncthreads();
     }
   }
@@ -746,8 +810,14 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
   __syncthreads();
   const EsPlan pl = s_plan;
   if (pl.nk > 0) {
-    // (3) S_l(k), two nodes per thread, tiles in order; every load is issued
-    // (at a clamped index) and the window test selects afterwards
+    // (3) S_l(k), two nodes per thread, tiles in order: nodes up to a tile's kt from
+    // its power sums, sum_j (-a_k / a_kt)^j T_j / j!; its window from the stored
+    // moments; nothing after the window
+    for (int m = tid; m < kEsMaxWin; m += kEsThreads) s_rho[m] = exp(-(double)m * kEsStep);
+    __syncthreads();
+    double inv_fact[kEsTaylor];
+#pragma unroll
+    for (int j = 0; j < kEsTaylor; ++j) inv_fact[j] = es_inv_fact(j);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int i = tid + u * kEsThreads;
@@ -756,15 +826,24 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
       double S[L];
 #pragma unroll
       for (int l = 0; l < L; ++l) S[l] = 0.0;
-#pragma unroll 4
+#pragma unroll 2
       for (int64_t t = 0; t < es.T1; ++t) {
 #pragma unroll
         for (int l = 0; l < L; ++l) {
           const EsTile& e = rec[t * L + l];
-          const int ka = e.ka, nw = e.nw;
-          const int j = min(max(k - ka, 0), kEsMaxWin - 1);
-          const double v = part[(t * L + l) * kEsMaxWin + j];
-          S[l] += (nw == 0) ? 0.0 : ((k < ka) ? e.qpos : ((k < ka + nw) ? v : 0.0));
+          if (e.npos == 0 || e.bad) continue;
+          const double* pt = part + (t * L + l) * kEsPart;
+          const int d = k - e.kt;
+          double v;
+          if (d <= 0) {
+            const double nx = -s_rho[min(-d, kEsMaxWin - 1)];
+            v = pt[kEsTaylor - 1] * inv_fact[kEsTaylor - 1];
+#pragma unroll
+            for (int j = kEsTaylor - 2; j >= 0; --j) v = fma(v, nx, pt[j] * inv_fact[j]);
+          } else {
+            v = (d <= e.nw) ? pt[kEsTaylor + d - 1] : 0.0;
+          }
+          S[l] += v;
         }
       }
       const double ha = kEsStep * exp((double)k * kEsStep);
@@ -779,40 +858,16 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
       }
     }
     __syncthreads();
-    // prefix sums in node order: wave 0, eight consecutive nodes per lane
-    if (wid == 0) {
-#pragma unroll
-      for (int l = 0; l < L; ++l) {
-        double loc = 0.0;
-        for (int j = 0; j < 8; ++j) {
-          const int i = lane * 8 + j;
-          if (i < pl.nk) loc += s_c[l][i];
-        }
-        const double incl = wave_inclusive_scan(loc, lane);
-        double run = incl - loc;
-        for (int j = 0; j < 8; ++j) {
-          const int i = lane * 8 + j;
-          if (i <= pl.nk && i < kEsMaxWin) s_p[l][i] = run;
-          if (i < pl.nk) run += s_c[l][i];
-        }
-      }
-    }
-    __syncthreads();
     double* ct = es.ctab + b * L * kEsMaxWin;
-    double* pt = es.ptab + b * L * kEsMaxWin;
-    for (int i = tid; i <= pl.nk && i < kEsMaxWin; i += kEsThreads) {
+    for (int i = tid; i < pl.nk; i += kEsThreads) {
 #pragma unroll
-      for (int l = 0; l < L; ++l) {
-        if (i < pl.nk) ct[l * kEsMaxWin + i] = s_c[l][i];
-        pt[l * kEsMaxWin + i] = s_p[l][i];
-      }
+      for (int l = 0; l < L; ++l) ct[l * kEsMaxWin + i] = s_c[l][i];
     }
   }
   // (4) rows in fp64, from the tables in LDS
   if (pl.fp64) {
     for (int64_t t = 0; t < es.T2; ++t) {
-      es_eval_tile<double, L>(pb, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, r + b * V, pl, &s_c[0][0],
-                              &s_p[0][0]);
+      es_eval_tile<double, L>(pb, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, r + b * V, pl, &s_c[0][0]);
       __syncthreads();
     }
   }
@@ -835,7 +890,7 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
   }
   if (pl.fp64) return;  // written by the coefficient kernel
   es_eval_tile<float, L>(p + b * V, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, rb, pl,
-                         es.ctab + b * L * kEsMaxWin, es.ptab + b * L * kEsMaxWin);
+                         es.ctab + b * L * kEsMaxWin);
 }
 
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
@@ -846,12 +901,10 @@ void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
   es->tile = reinterpret_cast<EsTile*>(c);
   c += align256(sizeof(EsTile) * B * T1 * L);
   es->part = reinterpret_cast<double*>(c);
-  c += align256(sizeof(double) * B * T1 * L * kEsMaxWin);
+  c += align256(sizeof(double) * B * T1 * L * kEsPart);
   es->plan = reinterpret_cast<EsPlan*>(c);
   c += align256(sizeof(EsPlan) * B);
   es->ctab = reinterpret_cast<double*>(c);
-  c += align256(sizeof(double) * B * L * kEsMaxWin);
-  es->ptab = reinterpret_cast<double*>(c);
   es->T1 = T1;
   es->T2 = T2;
 }
@@ -860,8 +913,8 @@ void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
 
 size_t workspace_bytes_expsum(int64_t B, int64_t V, int L) {
   const int64_t T1 = es_tiles(V, kEsMomTile);
-  return align256(sizeof(EsTile) * B * T1 * L) + align256(sizeof(double) * B * T1 * L * kEsMaxWin) +
-         align256(sizeof(EsPlan) * B) + 2 * align256(sizeof(double) * B * L * kEsMaxWin);
+  return align256(sizeof(EsTile) * B * T1 * L) + align256(sizeof(double) * B * T1 * L * kEsPart) +
+         align256(sizeof(EsPlan) * B) + align256(sizeof(double) * B * L * kEsMaxWin);
 }
 
 // q2 == nullptr: K i.i.d. drafts from q1; else two draft laws (K = 2).
