@@ -127,6 +127,23 @@ __device__ inline void es_window(double wlo, double whi, int& kt, int& nw) {
   nw = max(0, min(z - kt, kEsMaxWin));
 }
 
+// The same in fp32 for weights in the fp32 range (hardware log2; a boundary
+// node off by one rounding of the logarithm keeps both bounds within 1e-5 of
+// their limits, where exp(-z) is 1 or 0 to far below the rule's error).
+__device__ inline void es_window_f32(float wlo, float whi, int& kt, int& nw) {
+  constexpr float kLn2 = 0.69314718f;
+  kt = (int)floorf(((float)kEsLnFar - __builtin_amdgcn_logf(whi) * kLn2) * (float)(1.0 / kEsStep));
+  const int z = (int)floorf(((float)kEsLnZero - __builtin_amdgcn_logf(wlo) * kLn2) * (float)(1.0 / kEsStep));
+  nw = max(0, min(z - kt, kEsMaxWin));
+}
+__device__ inline void es_scale_f32(float wlo, float whi, int& tau, int& range) {
+  int e_lo, e_hi;
+  frexpf(wlo, &e_lo);
+  frexpf(whi, &e_hi);
+  tau = -((e_lo + e_hi) >> 1);
+  range = e_hi - e_lo;
+}
+
 // 1 / j! for the expansion exp(-u) = sum_j (-u)^j / j!
 __device__ __forceinline__ double es_inv_fact(int j) {
   double f = 1.0;
@@ -227,44 +244,66 @@ __device__ __forceinline__ float dpp(float x) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 
-// fp32, 16 values: the same sum without LDS traffic.  Stages by lane bit 2 and
-// bit 3 exchange within 16-lane rows by DPP rotations (a rotation by 4 or 8
-// always flips that bit and keeps the others below bit 4, so every lane is
-// paired once), bits 4 and 5 by the row / half swaps of gfx950, and the two
-// low bits are summed across the quad.  Lane l holds the total of value
-// 8 b2 + 4 b3 + 2 b4 + b5 (b_i = bit i of l).
-__device__ __forceinline__ float wave_reduce_scatter16_f32(float (&v)[16], int lane) {
-  {
-    const bool up = (lane & 4) != 0;
+// fp32: the same sums without LDS traffic.  Values are split by lane bit 2 and
+// bit 3 within 16-lane rows through DPP rotations (a rotation by 4 or 8 always
+// flips that bit and keeps the others below bit 4, so every lane is paired
+// once), by bits 4 and 5 through the row and half swaps of gfx950; the bits
+// left over are summed (swaps with the value itself, quad permutations).  For
+// NB = 16 / 8 / 4 lane l ends with the total of value 8 b2 + 4 b3 + 2 b4 + b5 /
+// 4 b2 + 2 b3 + b4 / 2 b2 + b3 (b_i = bit i of l); es_scatter_node and
+// es_scatter_writer name that value and one lane holding it.
+template <int HALF, int N, int CTRL>
+__device__ __forceinline__ void rs_dpp(float (&v)[N], bool up) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float send = up ? v[i] : v[i + 8];
-      const float keep = up ? v[i + 8] : v[i];
-      v[i] = keep + dpp<0x124>(send);  // row_ror:4
-    }
+  for (int i = 0; i < HALF; ++i) {
+    const float send = up ? v[i] : v[i + HALF];
+    const float keep = up ? v[i + HALF] : v[i];
+    v[i] = keep + dpp<CTRL>(send);
   }
-  {
-    const bool up = (lane & 8) != 0;
+}
+template <int HALF, int N, bool ROW>
+__device__ __forceinline__ void rs_swap(float (&v)[N]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float send = up ? v[i] : v[i + 4];
-      const float keep = up ? v[i + 4] : v[i];
-      v[i] = keep + dpp<0x128>(send);  // row_ror:8
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]), __float_as_uint(v[i + 2]), false, false);
+  for (int i = 0; i < HALF; ++i) {
+    const auto r = ROW ? __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]), __float_as_uint(v[i + HALF]), false, false)
+                       : __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]), __float_as_uint(v[i + HALF]), false, false);
     v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
   }
-  {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[0]), __float_as_uint(v[1]), false, false);
-    v[0] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+template <bool ROW>
+__device__ __forceinline__ float sum_swap(float x) {
+  const auto r = ROW ? __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false)
+                     : __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+template <int NB>
+__device__ __forceinline__ float wave_reduce_scatter_f32(float (&v)[NB], int lane) {
+  static_assert(NB == 4 || NB == 8 || NB == 16, "block sizes");
+  rs_dpp<NB / 2, NB, 0x124>(v, (lane & 4) != 0);  // row_ror:4
+  rs_dpp<NB / 4, NB, 0x128>(v, (lane & 8) != 0);  // row_ror:8
+  float x;
+  if constexpr (NB == 16) {
+    rs_swap<2, NB, true>(v);
+    rs_swap<1, NB, false>(v);
+    x = v[0];
+  } else if constexpr (NB == 8) {
+    rs_swap<1, NB, true>(v);
+    x = sum_swap<false>(v[0]);
+  } else {
+    x = sum_swap<false>(sum_swap<true>(v[0]));
   }
-  float x = v[0];
   x += dpp<0xB1>(x);  // quad_perm [1,0,3,2]
   x += dpp<0x4E>(x);  // quad_perm [2,3,0,1]
   return x;
+}
+template <int NB>
+__device__ __forceinline__ int es_scatter_node(int lane) {
+  const int b2 = (lane >> 2) & 1, b3 = (lane >> 3) & 1, b4 = (lane >> 4) & 1, b5 = (lane >> 5) & 1;
+  return NB == 16 ? 8 * b2 + 4 * b3 + 2 * b4 + b5 : (NB == 8 ? 4 * b2 + 2 * b3 + b4 : 2 * b2 + b3);
+}
+template <int NB>
+__device__ __forceinline__ bool es_scatter_writer(int lane) {
+  return NB == 16 ? (lane & 3) == 0 : (NB == 8 ? (lane & 0x23) == 0 : (lane & 0x33) == 0);
 }
 
 // ------------------------------------------------------------------ moments
@@ -288,10 +327,9 @@ __device__ __forceinline__ void es_moments_block(const Real* __restrict__ s_w, c
 #pragma unroll
     for (int i = 0; i < NB; ++i) acc[i] = es_fma(qq, es_decay(rt[i], w), acc[i]);
   }
-  if constexpr (NB == 16 && sizeof(Real) == 4) {
-    const Real tot = wave_reduce_scatter16_f32(acc, lane);
-    const int node = ((lane >> 2) & 1) * 8 + ((lane >> 3) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 5) & 1);
-    if ((lane & 3) == 0) s_red[wid][nb + node] = tot;
+  if constexpr (sizeof(Real) == 4) {
+    const Real tot = wave_reduce_scatter_f32<NB>(acc, lane);
+    if (es_scatter_writer<NB>(lane)) s_red[wid][nb + es_scatter_node<NB>(lane)] = tot;
   } else {
     const Real tot = wave_reduce_scatter<NB, Real>(acc, lane);
     if ((lane & (64 / NB - 1)) == 0) s_red[wid][nb + lane / (64 / NB)] = tot;
@@ -378,9 +416,15 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     o.pad[0] = o.pad[1] = o.pad[2] = 0;
     int tau = 0, range = 0;
     if (n > 0) {
-      es_scale(wmin, wmax, tau, range);
-      if (!f64 && (od || range > kEsWideRange)) o.wide = 1;
-      es_window(wmin, wmax, o.kt, o.nw);
+      if (f64 || od) {
+        es_scale(wmin, wmax, tau, range);
+        if (!f64) o.wide = 1;
+        es_window(wmin, wmax, o.kt, o.nw);
+      } else {
+        es_scale_f32((float)wmin, (float)wmax, tau, range);
+        if (range > kEsWideRange) o.wide = 1;
+        es_window_f32((float)wmin, (float)wmax, o.kt, o.nw);
+      }
     }
     *rec = o;
     s_dec[0] = o.kt;
@@ -426,8 +470,13 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
         pw *= u;
       }
     }
-    const Real tot = wave_reduce_scatter<kEsTaylor, Real>(T, lane);
-    if ((lane & (64 / kEsTaylor - 1)) == 0) s_tay[wid][lane / (64 / kEsTaylor)] = tot;
+    if constexpr (sizeof(Real) == 4) {
+      const Real tot = wave_reduce_scatter_f32<kEsTaylor>(T, lane);
+      if (es_scatter_writer<kEsTaylor>(lane)) s_tay[wid][es_scatter_node<kEsTaylor>(lane)] = tot;
+    } else {
+      const Real tot = wave_reduce_scatter<kEsTaylor, Real>(T, lane);
+      if ((lane & (64 / kEsTaylor - 1)) == 0) s_tay[wid][lane / (64 / kEsTaylor)] = tot;
+    }
   }
   int nb = 0;
   for (; nb + 16 <= nw; nb += 16) es_moments_block<16, Real>(s_w, s_q, s_rate, M, nb, tid, lane, wid, s_red);
@@ -544,14 +593,22 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
         hi = fmax(hi, wmax[l]);
       }
       int tau = 0, range = 0;
-      if (hi > 0.0) es_scale(lo, hi, tau, range);
+      if (hi > 0.0) {
+        if (f64 || od)
+          es_scale(lo, hi, tau, range);
+        else
+          es_scale_f32((float)lo, (float)hi, tau, range);
+      }
       s_go = f64 || !(od || range > kEsWideRange);  // the fp32 path never sees a wide tile (see above)
       s_tau = f64 ? 0 : tau;
       for (int l = 0; l < L; ++l) {
         int i0 = pl.nk, cnt = 0, kt = pl.k_lo + pl.nk;
         if (wmax[l] > 0.0) {
           int nw;
-          es_window(wmin[l], wmax[l], kt, nw);
+          if (f64)
+            es_window(wmin[l], wmax[l], kt, nw);
+          else
+            es_window_f32((float)wmin[l], (float)wmax[l], kt, nw);
           i0 = std::min(std::max(kt + 1 - pl.k_lo, 0), pl.nk);
           const int i1 = std::min(kt + nw - pl.k_lo, pl.nk - 1);
           cnt = std::max(0, i1 - i0 + 1);
