@@ -24,12 +24,18 @@
 // the row.  Every term is positive, so these relative bounds hold for the
 // sums and for r; fp32 evaluation adds a few 1e-8.
 //
-// Windows.  For a tile of tokens with positive weights in [wlo, whi],
-// exp(-a_k w) rounds to 1 in fp32 for every token once a_k whi < 2^-25 and to 0
-// once a_k wlo > 104.  Each tile therefore evaluates exponentials only on its
-// own window of nodes between those limits: below the window a tile adds its
-// draft mass to S_k, above it nothing, and a query tile takes the prefix sum of
-// c_k below its window.  Moments need no row-wide information, so they run
+// Windows.  Nodes where a_k w <= 1/4 for every token of a group are taken by an
+// eight-term expansion of exp(-a_k w) in powers of a_k w (truncation below
+// 4e-10 relative); nodes where a_k w > Z = 22 for a token drop that token's term.
+// The drop is a truncation of the integral: a token x with weight w_x inside a
+// denominator D >= w_x loses at most the part of its pair (or tuple) integral
+// over a > Z / w_x, which relative to 1/D is at most e^(-Z D / w_x) (1 + h Z D / w_x)
+// <= e^(-Z) (1 + h Z) = 3.3e-9 on the grid (the integrand is decreasing there),
+// once on the moment side and once on the query side.  So each group of tokens
+// needs exponentials only on the window of nodes between those limits, and a
+// group of tokens with nearby weights has a short window: the moments sort each
+// tile's tokens by binary exponent and give every run of consecutive sorted
+// tokens its own window.  Moments need no row-wide information, so they run
 // first; one workgroup per row then merges the tiles, fixes the row's grid
 // range and coefficients; evaluation follows.
 //
@@ -63,7 +69,7 @@ constexpr double kEsStep = 0.5;                         // h
 constexpr double kEsLnEps = -18.420680743952367;        // ln 1e-8: left-tail cut
 constexpr double kEsLnLnInvEps = 2.9134941423228814;    // ln ln 1e8: right-tail cut
 constexpr double kEsLnFar = -1.3862943611198906;        // ln 1/4: at or below, a node is taken by the expansion
-constexpr double kEsLnZero = 4.6443908991413725;        // ln 104: above, exp(-z) < 2^-150
+constexpr double kEsLnZero = 3.0910424533583156;        // ln 22: above, a token's term is dropped
 constexpr double kEsLog2e = 1.4426950408889634;
 constexpr int kEsWideRange = 160;  // binary exponent range of a tile's weights kept in fp32
 
@@ -117,10 +123,9 @@ __device__ __forceinline__ float es_wave_max(float v) { return wave_max(v); }
 __device__ __forceinline__ double es_wave_min(double v) { return wave_min64(v); }
 __device__ __forceinline__ double es_wave_max(double v) { return wave_max64(v); }
 
-// Nodes of a tile whose positive weights lie in [wlo, whi]: up to kt, a_k whi
-// <= 1/4 and the expansion takes them; after kt + nw, a_k wlo > 104 and
-// exp(-a_k w) is 0 in fp32 for every token; the window in between is summed
-// with exponentials.
+// Nodes of a group whose positive weights lie in [wlo, whi]: up to kt, a_k whi
+// <= 1/4 and the expansion takes them; after kt + nw, a_k wlo > 22 and every
+// token's term is dropped; the window in between is summed with exponentials.
 __device__ inline void es_window(double wlo, double whi, int& kt, int& nw) {
   kt = (int)floor((kEsLnFar - log(whi)) / kEsStep);
   const int z = (int)floor((kEsLnZero - log(wlo)) / kEsStep);
