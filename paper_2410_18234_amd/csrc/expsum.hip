@@ -505,15 +505,352 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
   }
 }
 
-// grid (T1, B, L): one tile of law l = blockIdx.z in fp32.
-__global__ __launch_bounds__(kEsThreads) void es_moments_kernel(const float* __restrict__ p,
+// ------------------------------------------------------------------ moments (fp32)
+// Persistent workgroups walk the (row, tile, law) records; while one tile is
+// summed the next one's p and q are in flight.  Per tile: statistics and the
+// record, a stable counting sort of the positive-weight tokens by binary
+// exponent into LDS, then runs of 512 consecutive sorted tokens (two per wave):
+// each run takes exponentials only on its own window [kt_r + 1, kt_r + nw_r]
+// and power sums at its own expansion node kt_r; a run's power sums are turned
+// into the tile's nodes kt + 1 .. kt_r and moved to the tile's expansion node
+// kt (u = a_kt w <= a_kt_r w <= 1/4).  The tile record is the one the fp64 tile
+// path writes: power sums at kt, moments of the nodes kt + 1 .. kt + nw.
+constexpr int kEsRun = 512;             // sorted tokens per run
+constexpr int kEsRunPer = kEsRun / 64;  // per lane
+constexpr int kEsWin32 = 240;           // window bound of an fp32 tile: a span within 2^161 needs <= 233 nodes
+
+__device__ __forceinline__ int es_expo(float w) { return (int)(__float_as_uint(w) >> 23); }  // w > 0, normal
+
+// Node rates of fp32 tiles: log2(e) a_k = log2(e) e^(k/2) as an fp32 mantissa
+// in [1, 2) and a binary exponent, for every node an fp32 tile can reach
+// (ratios in the fp32 normal range: -181 <= kt, window top <= 180, plus the
+// three filler nodes of a last block of four).  Built at compile time: e^(1/2)
+// from its series, then successive products and quotients (relative error
+// below 1e-13 over the range), rounded once to fp32.
+constexpr int kEsNodeLo = -192, kEsNodeHi = 192;
+struct EsRateTab {
+  float mant[kEsNodeHi - kEsNodeLo];
+  int expo[kEsNodeHi - kEsNodeLo];
+};
+constexpr EsRateTab es_make_rate_tab() {
+  EsRateTab t{};
+  double eh = 1.0, term = 1.0;
+  for (int i = 1; i < 24; ++i) {
+    term *= 0.5 / i;
+    eh += term;
+  }
+  for (int dir = 0; dir < 2; ++dir) {
+    double v = kEsLog2e;
+    for (int k = 0; dir == 0 ? k < kEsNodeHi : k >= kEsNodeLo; k += dir == 0 ? 1 : -1) {
+      double x = v;
+      int n = 0;
+      while (x >= 2.0) {
+        x *= 0.5;
+        ++n;
+      }
+      while (x < 1.0) {
+        x *= 2.0;
+        --n;
+      }
+      t.mant[k - kEsNodeLo] = (float)x;
+      t.expo[k - kEsNodeLo] = n;
+      v = dir == 0 ? v * eh : v / eh;
+    }
+  }
+  return t;
+}
+__constant__ EsRateTab kEsRates = es_make_rate_tab();
+
+// log2(e) a_k 2^-tau in fp32 for a uniform node k: scalar loads and an integer
+// add to the exponent field (the scaled rates of a tile's nodes are normal:
+// a_k w lies within [2^-160, 22] on the window and w 2^tau within 2^+-81).
+__device__ __forceinline__ float es_rate_f32(int k, int tau) {
+  const int i = min(max(k - kEsNodeLo, 0), kEsNodeHi - kEsNodeLo - 1);
+  return __int_as_float(__float_as_int(kEsRates.mant[i]) + ((kEsRates.expo[i] - tau) << 23));
+}
+
+
+// Batcher's odd-even merge sort of N keys held by one lane (N a power of two):
+// a fixed network of compare-exchanges on compile-time indices.
+template <int N>
+__device__ __forceinline__ void es_lane_sort(uint32_t (&k)[N]) {
+#pragma unroll
+  for (int p = 1; p < N; p <<= 1) {
+#pragma unroll
+    for (int d = p; d >= 1; d >>= 1) {
+#pragma unroll
+      for (int j = d % p; j + d < N; j += 2 * d) {
+#pragma unroll
+        for (int i = 0; i < d; ++i) {
+          const int a = i + j, b = i + j + d;
+          if (b < N && (a / (2 * p)) == (b / (2 * p))) {
+            const uint32_t x = k[a], y = k[b];
+            k[a] = min(x, y);
+            k[b] = max(x, y);
+          }
+        }
+      }
+    }
+  }
+}
+
+// NB window nodes of a run: sum over the run's tokens of q exp(-a_k w), added to
+// the wave's moments (nodes at or above lim are not written).
+template <int NB>
+__device__ __forceinline__ void es_run_block(const float (&w)[kEsRunPer], const float (&qq)[kEsRunPer], int k0,
+                                             int tau, int lane, float* __restrict__ red, int lim) {
+  float rt[NB], acc[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    rt[i] = es_rate_f32(k0 + i, tau);
+    acc[i] = 0.0f;
+  }
+#pragma unroll
+  for (int e = 0; e < kEsRunPer; ++e) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) acc[i] = fmaf(qq[e], es_decay(rt[i], w[e]), acc[i]);
+  }
+  const float tot = wave_reduce_scatter_f32<NB>(acc, lane);
+  const int node = es_scatter_node<NB>(lane);
+  if (es_scatter_writer<NB>(lane) && node < lim) red[node] += tot;
+}
+
+// One run (wave-level): LDS rows 2r and 2r + 1 of the tile (512 tokens; the
+// entries of tokens left out are zero).  red / tay: the wave's moments of the
+// tile window and power sums at the tile's expansion node.
+__device__ void es_moments_run(const float* __restrict__ s_w, const float* __restrict__ s_q, int r, int kt, int nw,
+                               int tau, int lane, float* __restrict__ red, float* __restrict__ tay) {
+  constexpr float kInvFact[kEsTaylor] = {1.0f,        1.0f,         0.5f,          1.0f / 6.0f,
+                                         1.0f / 24.0f, 1.0f / 120.0f, 1.0f / 720.0f, 1.0f / 5040.0f};
+  float w[kEsRunPer], qq[kEsRunPer];
+  float lo = INFINITY, hi = 0.0f;
+#pragma unroll
+  for (int e = 0; e < kEsRunPer; ++e) {
+    const int j = r * kEsRun + e * 64 + lane;
+    w[e] = s_w[j];
+    qq[e] = s_q[j];
+    if (qq[e] > 0.0f) {  // entries left out hold w = q = 0
+      lo = fminf(lo, w[e]);
+      hi = fmaxf(hi, w[e]);
+    }
+  }
+  lo = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(wave_min(lo))));
+  hi = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(wave_max(hi))));
+  if (!(hi > 0.0f)) return;  // uniform: an empty run
+  int ktr, nwr;
+  es_window_f32(ldexpf(lo, -tau), ldexpf(hi, -tau), ktr, nwr);
+  ktr = __builtin_amdgcn_readfirstlane(ktr);
+  nwr = __builtin_amdgcn_readfirstlane(nwr);
+  const int o = min(max(ktr - kt, 0), nw);                 // the run expands at node kt + o
+  const int cnt = max(0, min(ktr + nwr, kt + nw) - (kt + o));  // then exponentials on kt + o + 1 .. kt + o + cnt
+  // power sums at u = a'_(kt+o) w
+  const float akt = es_rate_f32(kt + o, tau) * (float)(1.0 / kEsLog2e);
+  float T[kEsTaylor];
+#pragma unroll
+  for (int j = 0; j < kEsTaylor; ++j) T[j] = 0.0f;
+#pragma unroll
+  for (int e = 0; e < kEsRunPer; ++e) {
+    const float u = akt * w[e];
+    float pw = qq[e];
+#pragma unroll
+    for (int j = 0; j < kEsTaylor; ++j) {
+      T[j] += pw;
+      pw *= u;
+    }
+  }
+  const float tt = wave_reduce_scatter_f32<kEsTaylor>(T, lane);
+  float Tj[kEsTaylor];  // uniform: read from the lane that holds each sum (node 4 b2 + 2 b3 + b4)
+#pragma unroll
+  for (int j = 0; j < kEsTaylor; ++j)
+    Tj[j] = __int_as_float(
+        __builtin_amdgcn_readlane(__float_as_int(tt), 4 * ((j >> 2) & 1) + 8 * ((j >> 1) & 1) + 16 * (j & 1)));
+  // window nodes
+  int nb = 0;
+  const int k0 = kt + o + 1;
+  for (; nb + 16 <= cnt; nb += 16) es_run_block<16>(w, qq, k0 + nb, tau, lane, red + o + nb, 16);
+  if (nb + 8 <= cnt) {
+    es_run_block<8>(w, qq, k0 + nb, tau, lane, red + o + nb, 8);
+    nb += 8;
+  }
+  for (; nb < cnt; nb += 4) es_run_block<4>(w, qq, k0 + nb, tau, lane, red + o + nb, cnt - nb);
+  // tile nodes kt + 1 .. kt + o from the run's expansion: node kt + 1 + i has a_k / a_(kt+o) = e^(-(o - 1 - i) h)
+  for (int i = lane; i < o; i += 64) {
+    const float v = __builtin_amdgcn_exp2f(-(float)(o - 1 - i) * (float)(kEsStep * kEsLog2e));
+    float s = Tj[kEsTaylor - 1] * kInvFact[kEsTaylor - 1];
+#pragma unroll
+    for (int j = kEsTaylor - 2; j >= 0; --j) s = fmaf(s, -v, Tj[j] * kInvFact[j]);
+    red[i] += s;
+  }
+  // the run's power sums at the tile's expansion node: T_j (a_kt / a_(kt+o))^j
+  if (es_scatter_writer<kEsTaylor>(lane)) {
+    const int j = es_scatter_node<kEsTaylor>(lane);
+    tay[j] += __builtin_amdgcn_exp2f(-(float)(o * j) * (float)(kEsStep * kEsLog2e)) * tt;
+  }
+}
+
+__device__ __forceinline__ void es_load_tile(const float* __restrict__ p, const float* __restrict__ q1,
+                                             const float* __restrict__ q2, int64_t V, int L, int64_t T1, int64_t g,
+                                             int tid, float (&pv)[kEsMomPer], float (&qv)[kEsMomPer]) {
+  const int l = (int)(g % L);
+  const int64_t bt = g / L, t = bt % T1, b = bt / T1;
+  const float* pb = p + b * V;
+  const float* qb = (l == 0 ? q1 : q2) + b * V;
+  const int64_t base = t * kEsMomTile + tid;
+  if (t * kEsMomTile + kEsMomTile <= V) {  // uniform: a whole tile
+#pragma unroll
+    for (int i = 0; i < kEsMomPer; ++i) {
+      pv[i] = pb[base + i * kEsThreads];
+      qv[i] = qb[base + i * kEsThreads];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kEsMomPer; ++i) {
+      const int64_t x = base + i * kEsThreads;
+      pv[i] = (x < V) ? pb[x] : 0.0f;
+      qv[i] = (x < V) ? qb[x] : 0.0f;
+    }
+  }
+}
+
+// G = B * T1 * L records, record g = (b * T1 + t) * L + l; any grid size.
+__global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* __restrict__ p,
                                                                  const float* __restrict__ q1,
-                                                                 const float* __restrict__ q2, int64_t V,
-                                                                 EsWork es) {
-  const int64_t t = blockIdx.x, b = blockIdx.y;
-  const int l = blockIdx.z, L = gridDim.z;
-  const int64_t idx = (b * es.T1 + t) * L + l;
-  es_moments_tile<float>(p + b * V, (l == 0 ? q1 : q2) + b * V, V, t, es.tile + idx, es.part + idx * kEsPart);
+                                                                 const float* __restrict__ q2, int64_t V, int L,
+                                                                 int64_t G, EsWork es) {
+  __shared__ float s_w[kEsMomTile];
+  __shared__ float s_q[kEsMomTile];
+  __shared__ float s_red[kEsWaves][kEsWin32];
+  __shared__ float s_tay[kEsWaves][kEsTaylor];
+  __shared__ float s_f[2][kEsWaves][2];  // by tile parity: the tile may be skipped without another barrier
+  __shared__ double s_q0[2][kEsWaves];
+  __shared__ int s_i[2][kEsWaves][3];
+  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  float pv[kEsMomPer], qv[kEsMomPer];
+  int64_t g = blockIdx.x;
+  if (g < G) es_load_tile(p, q1, q2, V, L, es.T1, g, tid, pv, qv);
+  for (int par = 0; g < G; g += gridDim.x, par ^= 1) {
+    const int64_t gn = g + gridDim.x;
+    // (1) ratios and statistics
+    bool pos[kEsMomPer];
+    float wv[kEsMomPer];
+    float wlo = INFINITY, whi = 0.0f, q0f = 0.0f;
+    int npos = 0, bad = 0, odd = 0;
+#pragma unroll
+    for (int i = 0; i < kEsMomPer; ++i) {
+      const float pp = pv[i], qq = qv[i];
+      bad |= (int)bad_prob(pp) | (int)bad_prob(qq);
+      pos[i] = pp > 0.0f && qq > 0.0f;
+      const float w = pos[i] ? es_ratio<float>(pp, qq) : 0.0f;
+      if (pos[i]) odd |= !(w >= FLT_MIN && w <= FLT_MAX);
+      wv[i] = w;
+      wlo = pos[i] ? fminf(wlo, w) : wlo;
+      whi = pos[i] ? fmaxf(whi, w) : whi;
+      npos += pos[i];
+      q0f += (qq > 0.0f && pp == 0.0f) ? qq : 0.0f;
+    }
+    wlo = wave_min(wlo);
+    whi = wave_max(whi);
+    const double q0w = wave_sum((double)q0f);
+    npos = wave_sum_int(npos);
+    bad = wave_sum_int(bad);
+    odd = wave_sum_int(odd);
+    if (lane == 0) {
+      s_f[par][wid][0] = wlo;
+      s_f[par][wid][1] = whi;
+      s_q0[par][wid] = q0w;
+      s_i[par][wid][0] = npos;
+      s_i[par][wid][1] = bad;
+      s_i[par][wid][2] = odd;
+    }
+    __syncthreads();
+    // every thread combines the same values in the same order
+    float wmin = s_f[par][0][0], wmax = s_f[par][0][1];
+    double q0 = s_q0[par][0];
+    int n = s_i[par][0][0], bd = s_i[par][0][1], od = s_i[par][0][2];
+#pragma unroll
+    for (int i = 1; i < kEsWaves; ++i) {
+      wmin = fminf(wmin, s_f[par][i][0]);
+      wmax = fmaxf(wmax, s_f[par][i][1]);
+      q0 += s_q0[par][i];
+      n += s_i[par][i][0];
+      bd |= s_i[par][i][1];
+      od |= s_i[par][i][2];
+    }
+    int kt = 0, nw = 0, tau = 0, wide = 0;
+    if (n > 0) {
+      if (od) {
+        wide = 1;
+      } else {
+        int range;
+        es_scale_f32(wmin, wmax, tau, range);
+        es_window_f32(wmin, wmax, kt, nw);
+        wide = (range > kEsWideRange || nw > kEsWin32) ? 1 : 0;
+      }
+    }
+    // the same in every lane: make it explicit (scalar registers, scalar table loads)
+    kt = __builtin_amdgcn_readfirstlane(kt);
+    nw = __builtin_amdgcn_readfirstlane(nw);
+    tau = __builtin_amdgcn_readfirstlane(tau);
+    n = __builtin_amdgcn_readfirstlane(n);
+    if (tid == 0) {
+      EsTile o;
+      o.wmin = n > 0 ? (double)wmin : INFINITY;
+      o.wmax = (double)wmax;
+      o.pad0 = 0.0;
+      o.q0 = q0;
+      o.npos = n;
+      o.bad = bd != 0;
+      o.kt = wide ? 0 : kt;
+      o.nw = wide ? 0 : nw;
+      o.wide = wide;
+      o.pad[0] = o.pad[1] = o.pad[2] = 0;
+      es.tile[g] = o;
+    }
+    if (bd || n == 0 || wide) {  // uniform; an fp64 tile is taken by the coefficient kernel
+      if (gn < G) es_load_tile(p, q1, q2, V, L, es.T1, gn, tid, pv, qv);
+      continue;
+    }
+    // (2) each thread sorts its tokens by weight (key: the weight's bits above the
+    // last four, then the slot; tokens left out last) and the tile is laid out
+    // rank by rank: LDS row i holds every thread's i-th smallest weight, so a run
+    // (two rows) holds weights of nearby quantiles
+    uint32_t key[kEsMomPer];
+#pragma unroll
+    for (int i = 0; i < kEsMomPer; ++i) {
+      key[i] = (pos[i] ? (__float_as_uint(wv[i]) & ~15u) : ~15u) | (uint32_t)i;
+      s_w[i * kEsThreads + tid] = pos[i] ? ldexpf(wv[i], tau) : 0.0f;  // this thread's column only
+      s_q[i * kEsThreads + tid] = pos[i] ? qv[i] : 0.0f;
+    }
+    es_lane_sort<kEsMomPer>(key);
+    {
+      float sw[kEsMomPer], sq[kEsMomPer];
+#pragma unroll
+      for (int i = 0; i < kEsMomPer; ++i) {
+        const int from = (int)(key[i] & 15u) * kEsThreads + tid;
+        sw[i] = s_w[from];
+        sq[i] = s_q[from];
+      }
+#pragma unroll
+      for (int i = 0; i < kEsMomPer; ++i) {
+        s_w[i * kEsThreads + tid] = sw[i];
+        s_q[i * kEsThreads + tid] = sq[i];
+      }
+    }
+    for (int k = lane; k < nw; k += 64) s_red[wid][k] = 0.0f;
+    if (lane < kEsTaylor) s_tay[wid][lane] = 0.0f;
+    __syncthreads();
+    if (gn < G) es_load_tile(p, q1, q2, V, L, es.T1, gn, tid, pv, qv);  // in flight during the runs
+    __asm__ volatile("" ::: "memory");  // keeps the loads here (not sunk past the runs)
+    // (3) runs: rows 2r and 2r + 1
+    for (int r = wid; r < kEsMomPer / 2; r += kEsWaves) es_moments_run(s_w, s_q, r, kt, nw, tau, lane, s_red[wid], s_tay[wid]);
+    __syncthreads();
+    // (4) the tile's moments and power sums, waves in order
+    double* part = es.part + g * kEsPart;
+    for (int k = tid; k < nw; k += kEsThreads)
+      part[kEsTaylor + k] = (double)(((s_red[0][k] + s_red[1][k]) + s_red[2][k]) + s_red[3][k]);
+    if (tid < kEsTaylor) part[tid] = (double)(((s_tay[0][tid] + s_tay[1][tid]) + s_tay[2][tid]) + s_tay[3][tid]);
+  }
 }
 
 // ------------------------------------------------------------------ evaluation
@@ -957,6 +1294,27 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
 
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
+// Workgroups of a persistent launch over `tiles` tiles: every resident slot of
+// the device once, each workgroup taking the same number of tiles (the last
+// ones one fewer).  Occupancy is measured once per device and kernel slot.
+constexpr int kEsSlotMoments = 0, kEsSlotEval1 = 1, kEsSlotEval2 = 2, kEsSlots = 3;
+template <typename Kern>
+static unsigned es_grid(Kern kernel, int64_t tiles, int slot) {
+  static int s_slots[64][kEsSlots];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  int slots = s_slots[dev][slot];
+  if (slots <= 0) {
+    int cus = 0, occ = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, kEsThreads, 0) != hipSuccess) occ = 0;
+    slots = std::max(cus, 1) * std::max(occ, 1);
+    s_slots[dev][slot] = slots;
+  }
+  const int64_t per = (tiles + slots - 1) / slots;
+  return (unsigned)std::max<int64_t>(1, (tiles + per - 1) / per);
+}
+
 void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
   const int64_t T1 = es_tiles(V, kEsMomTile), T2 = es_tiles(V, kEsEvalTile);
   char* c = static_cast<char*>(base);
@@ -985,9 +1343,10 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
   const int L = (q2 != nullptr) ? 2 : 1;
   EsWork es;
   carve_es(workspace, B, V, L, &es);
-  const dim3 g1((unsigned)es.T1, (unsigned)B, (unsigned)L);
+  const int64_t G1 = B * es.T1 * L;
   const dim3 g2((unsigned)es.T2, (unsigned)B);
-  hipLaunchKernelGGL(es_moments_kernel, g1, dim3(kEsThreads), 0, st, p, q1, q2, V, es);
+  hipLaunchKernelGGL(es_moments_kernel, dim3(es_grid(es_moments_kernel, G1, kEsSlotMoments)), dim3(kEsThreads), 0, st,
+                     p, q1, q2, V, L, G1, es);
   if (L == 1) {
     hipLaunchKernelGGL((es_coef_kernel<1>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
                        row_status);
