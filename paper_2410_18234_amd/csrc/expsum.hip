@@ -102,6 +102,7 @@ struct EsWork {
   double* part;     // [B][T1][L][kEsPart] per tile: power sums T_j, then the moments of its window
   EsPlan* plan;     // [B]
   double* ctab;     // [B][L][kEsMaxWin] c_k, k = k_lo + i
+  double* ptab;     // [B][L][kEsMaxNodes][kEsTaylor] B_j(k_lo + i) / j!: the expansion of the grid up to a node
   int64_t T1, T2;
 };
 
@@ -309,6 +310,32 @@ __device__ __forceinline__ int es_scatter_node(int lane) {
 template <int NB>
 __device__ __forceinline__ bool es_scatter_writer(int lane) {
   return NB == 16 ? (lane & 3) == 0 : (NB == 8 ? (lane & 0x23) == 0 : (lane & 0x33) == 0);
+}
+
+// Minimum / maximum of a float over the 64 lanes of a wave, in every lane
+// (quad permutations, row rotations by 4 and 8, then the gfx950 row and half
+// swaps; all lanes must be active).
+template <bool MAX>
+__device__ __forceinline__ float es_pick(float a, float b) {
+  return MAX ? fmaxf(a, b) : fminf(a, b);
+}
+template <bool MAX>
+__device__ __forceinline__ float es_wave_ext(float x) {
+  x = es_pick<MAX>(x, dpp<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = es_pick<MAX>(x, dpp<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = es_pick<MAX>(x, dpp<0x124>(x));  // row_ror:4
+  x = es_pick<MAX>(x, dpp<0x128>(x));  // row_ror:8
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = es_pick<MAX>(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return es_pick<MAX>(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+// the same, made explicit as a wave-uniform value
+__device__ __forceinline__ float es_uniform_min(float x) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(es_wave_ext<false>(x))));
+}
+__device__ __forceinline__ float es_uniform_max(float x) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(es_wave_ext<true>(x))));
 }
 
 // ------------------------------------------------------------------ moments
@@ -570,6 +597,13 @@ __device__ __forceinline__ float es_rate_f32(int k, int tau) {
 }
 
 
+// Workgroup barrier that orders LDS only: global loads issued before it stay in flight.
+__device__ __forceinline__ void es_lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Batcher's odd-even merge sort of N keys held by one lane (N a power of two):
 // a fixed network of compare-exchanges on compile-time indices.
 template <int N>
@@ -597,12 +631,13 @@ __device__ __forceinline__ void es_lane_sort(uint32_t (&k)[N]) {
 // NB window nodes of a run: sum over the run's tokens of q exp(-a_k w), added to
 // the wave's moments (nodes at or above lim are not written).
 template <int NB>
-__device__ __forceinline__ void es_run_block(const float (&w)[kEsRunPer], const float (&qq)[kEsRunPer], int k0,
-                                             int tau, int lane, float* __restrict__ red, int lim) {
+__device__ __forceinline__ void es_run_block(const float (&w)[kEsRunPer], const float (&qq)[kEsRunPer],
+                                             const float* __restrict__ rate, int lane, float* __restrict__ red,
+                                             int lim) {
   float rt[NB], acc[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
-    rt[i] = es_rate_f32(k0 + i, tau);
+    rt[i] = rate[i];
     acc[i] = 0.0f;
   }
 #pragma unroll
@@ -618,8 +653,9 @@ __device__ __forceinline__ void es_run_block(const float (&w)[kEsRunPer], const 
 // One run (wave-level): LDS rows 2r and 2r + 1 of the tile (512 tokens; the
 // entries of tokens left out are zero).  red / tay: the wave's moments of the
 // tile window and power sums at the tile's expansion node.
-__device__ void es_moments_run(const float* __restrict__ s_w, const float* __restrict__ s_q, int r, int kt, int nw,
-                               int tau, int lane, float* __restrict__ red, float* __restrict__ tay) {
+__device__ void es_moments_run(const float* __restrict__ s_w, const float* __restrict__ s_q,
+                               const float* __restrict__ s_rate, int r, int kt, int nw, int tau, int lane,
+                               float* __restrict__ red, float* __restrict__ tay) {
   constexpr float kInvFact[kEsTaylor] = {1.0f,        1.0f,         0.5f,          1.0f / 6.0f,
                                          1.0f / 24.0f, 1.0f / 120.0f, 1.0f / 720.0f, 1.0f / 5040.0f};
   float w[kEsRunPer], qq[kEsRunPer];
@@ -634,8 +670,8 @@ __device__ void es_moments_run(const float* __restrict__ s_w, const float* __res
       hi = fmaxf(hi, w[e]);
     }
   }
-  lo = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(wave_min(lo))));
-  hi = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(wave_max(hi))));
+  lo = es_uniform_min(lo);
+  hi = es_uniform_max(hi);
   if (!(hi > 0.0f)) return;  // uniform: an empty run
   int ktr, nwr;
   es_window_f32(ldexpf(lo, -tau), ldexpf(hi, -tau), ktr, nwr);
@@ -644,7 +680,7 @@ __device__ void es_moments_run(const float* __restrict__ s_w, const float* __res
   const int o = min(max(ktr - kt, 0), nw);                 // the run expands at node kt + o
   const int cnt = max(0, min(ktr + nwr, kt + nw) - (kt + o));  // then exponentials on kt + o + 1 .. kt + o + cnt
   // power sums at u = a'_(kt+o) w
-  const float akt = es_rate_f32(kt + o, tau) * (float)(1.0 / kEsLog2e);
+  const float akt = s_rate[o] * (float)(1.0 / kEsLog2e);
   float T[kEsTaylor];
 #pragma unroll
   for (int j = 0; j < kEsTaylor; ++j) T[j] = 0.0f;
@@ -666,13 +702,13 @@ __device__ void es_moments_run(const float* __restrict__ s_w, const float* __res
         __builtin_amdgcn_readlane(__float_as_int(tt), 4 * ((j >> 2) & 1) + 8 * ((j >> 1) & 1) + 16 * (j & 1)));
   // window nodes
   int nb = 0;
-  const int k0 = kt + o + 1;
-  for (; nb + 16 <= cnt; nb += 16) es_run_block<16>(w, qq, k0 + nb, tau, lane, red + o + nb, 16);
+  const float* rate = s_rate + o + 1;
+  for (; nb + 16 <= cnt; nb += 16) es_run_block<16>(w, qq, rate + nb, lane, red + o + nb, 16);
   if (nb + 8 <= cnt) {
-    es_run_block<8>(w, qq, k0 + nb, tau, lane, red + o + nb, 8);
+    es_run_block<8>(w, qq, rate + nb, lane, red + o + nb, 8);
     nb += 8;
   }
-  for (; nb < cnt; nb += 4) es_run_block<4>(w, qq, k0 + nb, tau, lane, red + o + nb, cnt - nb);
+  for (; nb < cnt; nb += 4) es_run_block<4>(w, qq, rate + nb, lane, red + o + nb, cnt - nb);
   // tile nodes kt + 1 .. kt + o from the run's expansion: node kt + 1 + i has a_k / a_(kt+o) = e^(-(o - 1 - i) h)
   for (int i = lane; i < o; i += 64) {
     const float v = __builtin_amdgcn_exp2f(-(float)(o - 1 - i) * (float)(kEsStep * kEsLog2e));
@@ -721,6 +757,7 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
   __shared__ float s_q[kEsMomTile];
   __shared__ float s_red[kEsWaves][kEsWin32];
   __shared__ float s_tay[kEsWaves][kEsTaylor];
+  __shared__ float s_rate[kEsWin32 + 5];  // log2(e) a_k 2^-tau for the nodes kt .. kt + nw + 4
   __shared__ float s_f[2][kEsWaves][2];  // by tile parity: the tile may be skipped without another barrier
   __shared__ double s_q0[2][kEsWaves];
   __shared__ int s_i[2][kEsWaves][3];
@@ -749,8 +786,8 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
       npos += pos[i];
       q0f += (qq > 0.0f && pp == 0.0f) ? qq : 0.0f;
     }
-    wlo = wave_min(wlo);
-    whi = wave_max(whi);
+    wlo = es_wave_ext<false>(wlo);
+    whi = es_wave_ext<true>(whi);
     const double q0w = wave_sum((double)q0f);
     npos = wave_sum_int(npos);
     bad = wave_sum_int(bad);
@@ -763,7 +800,7 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
       s_i[par][wid][1] = bad;
       s_i[par][wid][2] = odd;
     }
-    __syncthreads();
+    es_lds_barrier();
     // every thread combines the same values in the same order
     float wmin = s_f[par][0][0], wmax = s_f[par][0][1];
     double q0 = s_q0[par][0];
@@ -837,14 +874,15 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
         s_q[i * kEsThreads + tid] = sq[i];
       }
     }
+    for (int k = tid; k <= nw + 4; k += kEsThreads) s_rate[k] = es_rate_f32(kt + k, tau);
     for (int k = lane; k < nw; k += 64) s_red[wid][k] = 0.0f;
     if (lane < kEsTaylor) s_tay[wid][lane] = 0.0f;
-    __syncthreads();
+    es_lds_barrier();
     if (gn < G) es_load_tile(p, q1, q2, V, L, es.T1, gn, tid, pv, qv);  // in flight during the runs
     __asm__ volatile("" ::: "memory");  // keeps the loads here (not sunk past the runs)
     // (3) runs: rows 2r and 2r + 1
-    for (int r = wid; r < kEsMomPer / 2; r += kEsWaves) es_moments_run(s_w, s_q, r, kt, nw, tau, lane, s_red[wid], s_tay[wid]);
-    __syncthreads();
+    for (int r = wid; r < kEsMomPer / 2; r += kEsWaves) es_moments_run(s_w, s_q, s_rate, r, kt, nw, tau, lane, s_red[wid], s_tay[wid]);
+    es_lds_barrier();
     // (4) the tile's moments and power sums, waves in order
     double* part = es.part + g * kEsPart;
     for (int k = tid; k < nw; k += kEsThreads)
@@ -1085,6 +1123,230 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
   return true;
 }
 
+// ------------------------------------------------------------------ evaluation (fp32)
+// Persistent workgroups over the (row, tile) pairs of 2048 tokens, the next
+// tile's p and q in flight meanwhile.  Every query token takes its own nodes:
+// with k0 its first node where a_k w > 1/4, the nine nodes k0 .. k0 + 8 have
+// a_k w in (1/4, 22.5] and get exponentials, the grid nodes below k0 enter
+// through the expansion sum_j B_j(k0 - 1) (-a_(k0-1) w)^j / j!, B_j(k) =
+// sum over grid nodes k' <= k of c_k' (a_k' / a_k)^j, and the nodes above
+// k0 + 8 (a_k w > 22) are dropped.  Per tile and law three LDS tables, in the
+// tile's scale, are indexed by d = k0 - 1 - kt (kt: the tile's first such
+// node): c_k, B_j / j! and the node rates; each token reads them at its own
+// offset.
+constexpr int kEsTokNodes = 9;                  // exponentials per query token
+constexpr int kEsTabRows = kEsWin32 + 1;        // d = 0 .. 240
+constexpr int kEsPolyStride = kEsTaylor + 1;    // padded rows: neighbouring d fall in different banks
+
+template <int L>
+__device__ __forceinline__ void es_load_eval(const float* __restrict__ p, const float* __restrict__ q1,
+                                             const float* __restrict__ q2, int64_t V, int64_t T2, int64_t g,
+                                             int tid, float (&pv)[kEsEvalPer], float (&qv)[L][kEsEvalPer]) {
+  const int64_t t = g % T2, b = g / T2;
+  const int64_t base = t * kEsEvalTile + tid;
+  const float* pb = p + b * V;
+  const float* qa = q1 + b * V;
+  const float* qc = (L == 2) ? q2 + b * V : q1 + b * V;
+  if (t * kEsEvalTile + kEsEvalTile <= V) {  // uniform: a whole tile
+#pragma unroll
+    for (int i = 0; i < kEsEvalPer; ++i) {
+      pv[i] = pb[base + i * kEsThreads];
+      qv[0][i] = qa[base + i * kEsThreads];
+      if (L == 2) qv[L - 1][i] = qc[base + i * kEsThreads];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kEsEvalPer; ++i) {
+      const int64_t x = base + i * kEsThreads;
+      pv[i] = (x < V) ? pb[x] : 0.0f;
+      qv[0][i] = (x < V) ? qa[x] : 0.0f;
+      if (L == 2) qv[L - 1][i] = (x < V) ? qc[x] : 0.0f;
+    }
+  }
+}
+
+// G = B * T2 (row, tile) pairs, g = b * T2 + t; any grid size.
+template <int L>
+__global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __restrict__ p,
+                                                              const float* __restrict__ q1,
+                                                              const float* __restrict__ q2, int64_t V, int K,
+                                                              float* __restrict__ r, int64_t G, EsWork es) {
+  __shared__ float s_c[L][kEsTabRows + kEsTokNodes];          // c_(kt+1+i) 2^-tau (0 off the grid)
+  __shared__ float s_p[L][kEsTabRows * kEsPolyStride];        // B_j(kt + d) 2^-tau / j!
+  __shared__ float s_r[L][kEsTabRows];                        // log2(e) a_(kt+1+d) 2^-tau
+  __shared__ float s_f[2][kEsWaves][2][2];  // by tile parity: per wave and law, min and max weight
+  __shared__ int s_odd[2][kEsWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // e^(i h) for the nine nodes of a token, and e^(-h) / log2(e) (from log2(e) a_k0 w to a_(k0-1) w)
+  constexpr float kE[kEsTokNodes] = {1.0f,          1.6487212707f, 2.7182818285f, 4.4816890703f, 7.3890560989f,
+                                     12.182493961f, 20.085536923f, 33.115451959f, 54.598150033f};
+  constexpr float kBack = (float)(0.60653065971263342 / kEsLog2e);
+
+  float pv[kEsEvalPer], qv[L][kEsEvalPer];
+  int64_t g = blockIdx.x;
+  if (g < G) es_load_eval<L>(p, q1, q2, V, es.T2, g, tid, pv, qv);
+  for (int par = 0; g < G; g += gridDim.x, par ^= 1) {
+    const int64_t gn = g + gridDim.x;
+    const int64_t b = g / es.T2, t = g % es.T2;
+    const int64_t base = t * kEsEvalTile;
+    float* rb = r + b * V;
+    float pc[kEsEvalPer], qc[L][kEsEvalPer];
+#pragma unroll
+    for (int i = 0; i < kEsEvalPer; ++i) {
+      pc[i] = pv[i];
+#pragma unroll
+      for (int l = 0; l < L; ++l) qc[l][i] = qv[l][i];
+    }
+    if (gn < G) es_load_eval<L>(p, q1, q2, V, es.T2, gn, tid, pv, qv);
+    __asm__ volatile("" ::: "memory");  // issued here, in flight through this tile
+    const EsPlan& pl = es.plan[b];
+    const int flags = pl.flags, fp64 = pl.fp64, k_lo = pl.k_lo, nk = pl.nk;
+    if (flags) {  // uniform
+#pragma unroll
+      for (int i = 0; i < kEsEvalPer; ++i) {
+        const int64_t x = base + i * kEsThreads + tid;
+        if (x < V) rb[x] = NAN;
+      }
+      continue;
+    }
+    if (fp64) continue;  // evaluated by the coefficient kernel
+    int tau = 0;
+    float acc[kEsEvalPer];
+#pragma unroll
+    for (int i = 0; i < kEsEvalPer; ++i) acc[i] = 0.0f;
+    if (nk > 0) {
+      // (1) weights and statistics
+      float wv[L][kEsEvalPer];
+      int odd = 0;
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        float lo = INFINITY, hi = 0.0f;
+#pragma unroll
+        for (int i = 0; i < kEsEvalPer; ++i) {
+          const bool pos = pc[i] > 0.0f && qc[l][i] > 0.0f;
+          const float w = pos ? es_ratio<float>(pc[i], qc[l][i]) : 0.0f;
+          if (pos) odd |= !(w >= FLT_MIN && w <= FLT_MAX);
+          wv[l][i] = w;
+          lo = pos ? fminf(lo, w) : lo;
+          hi = pos ? fmaxf(hi, w) : hi;
+        }
+        lo = es_wave_ext<false>(lo);
+        hi = es_wave_ext<true>(hi);
+        if (lane == 0) {
+          s_f[par][wid][l][0] = lo;
+          s_f[par][wid][l][1] = hi;
+        }
+      }
+      odd = wave_sum_int(odd);
+      if (lane == 0) s_odd[par][wid] = odd;
+      es_lds_barrier();
+      float wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0f, 0.0f};
+      int od = 0;
+#pragma unroll
+      for (int i = 0; i < kEsWaves; ++i) {
+        od |= s_odd[par][i];
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          wmin[l] = fminf(wmin[l], s_f[par][i][l][0]);
+          wmax[l] = fmaxf(wmax[l], s_f[par][i][l][1]);
+        }
+      }
+      const float lo = fminf(wmin[0], wmin[L - 1]), hi = fmaxf(wmax[0], wmax[L - 1]);
+      int range = 0;
+      if (hi > 0.0f && !od) es_scale_f32(lo, hi, tau, range);
+      tau = __builtin_amdgcn_readfirstlane(tau);
+      // a row without an fp64 tile has ratios in the fp32 normal range and (two
+      // laws) a span within 2^160, and so has each of its tiles: never taken
+      if (od || range > kEsWideRange) {
+#pragma unroll
+        for (int i = 0; i < kEsEvalPer; ++i) {
+          const int64_t x = base + i * kEsThreads + tid;
+          if (x < V) rb[x] = NAN;
+        }
+        es_lds_barrier();  // every wave has read this tile's statistics
+        continue;
+      }
+      // (2) tables of the tile: kt = the last node with a_k w_max <= 1/4, rows d = 0 .. D
+      int kt[2], D[2];
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        int nw;
+        es_window_f32(fmaxf(wmin[l], FLT_MIN), fmaxf(wmax[l], FLT_MIN), kt[l], nw);
+        int ktlo, nwlo;  // the last expansion node of the smallest weight
+        es_window_f32(fmaxf(wmin[l], FLT_MIN), fmaxf(wmin[l], FLT_MIN), ktlo, nwlo);
+        kt[l] = __builtin_amdgcn_readfirstlane(kt[l]);
+        D[l] = __builtin_amdgcn_readfirstlane(min(max(ktlo - kt[l], 0), kEsTabRows - 1));
+        const double* ct = es.ctab + (b * L + l) * kEsMaxWin;
+        const double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
+        for (int i = tid; i < D[l] + 1 + kEsTokNodes; i += kEsThreads) {
+          const int idx = kt[l] + 1 + i - k_lo;
+          s_c[l][i] = (idx >= 0 && idx < nk) ? (float)ldexp(ct[idx], -tau) : 0.0f;
+        }
+        for (int e = tid; e < (D[l] + 1) * kEsTaylor; e += kEsThreads) {
+          const int d = e / kEsTaylor, j = e % kEsTaylor, idx = kt[l] + d - k_lo;
+          double v = 0.0;
+          if (idx >= 0)
+            v = (idx < nk) ? pt[idx * kEsTaylor + j]
+                           : pt[(nk - 1) * kEsTaylor + j] *
+                                 (double)__builtin_amdgcn_exp2f(-(float)(j * (idx - nk + 1)) * (float)(kEsStep * kEsLog2e));
+          s_p[l][d * kEsPolyStride + j] = (float)ldexp(v, -tau);
+        }
+        for (int d = tid; d <= D[l]; d += kEsThreads) s_r[l][d] = es_rate_f32(kt[l] + 1 + d, tau);
+      }
+      es_lds_barrier();
+      // (3) per token: nine exponentials and the expansion
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        if (!(wmax[l] > 0.0f)) continue;  // uniform: no token of this law has a positive weight
+        const float* sc = s_c[l];
+        const float* sp = s_p[l];
+        const float* sr = s_r[l];
+#pragma unroll
+        for (int i = 0; i < kEsEvalPer; ++i) {
+          const float w = wv[l][i];
+          if (!(w > 0.0f)) continue;
+          // d = kt(w) - kt, kt(w) = floor((ln 1/4 - ln w) / h)
+          const float ktw = floorf(((float)kEsLnFar - __builtin_amdgcn_logf(w) * 0.69314718f) * (float)(1.0 / kEsStep));
+          const int d = min(max((int)ktw - kt[l], 0), D[l]);
+          const float x = sr[d] * ldexpf(w, tau);  // log2(e) a_k0 w
+          float s = 0.0f;
+#pragma unroll
+          for (int m = 0; m < kEsTokNodes; ++m) s = fmaf(sc[d + m], __builtin_amdgcn_exp2f(-x * kE[m]), s);
+          const float nu = -x * kBack;  // -a_(k0-1) w
+          const float* pr = sp + d * kEsPolyStride;
+          float pe = pr[kEsTaylor - 1];
+#pragma unroll
+          for (int j = kEsTaylor - 2; j >= 0; --j) pe = fmaf(pe, nu, pr[j]);
+          acc[i] += s + pe;
+        }
+      }
+      es_lds_barrier();  // the tables are rebuilt for the next tile
+    }
+    // (4) epilogue: r(y) = p(y) 2^tau sum + the zero-weight closed forms
+    const double q0a = pl.q0[0], q0b = (L == 2) ? pl.q0[1] : 0.0;
+    double zw = q0a;  // K i.i.d. drafts: Q0^(K-1)
+    for (int j = 2; j < K; ++j) zw *= q0a;
+#pragma unroll
+    for (int i = 0; i < kEsEvalPer; ++i) {
+      const int64_t x = base + i * kEsThreads + tid;
+      if (x >= V) break;
+      const float pp = pc[i];
+      const float quad = ldexpf(pp * acc[i], tau);
+      float v = 0.0f;
+      if (L == 1) {
+        const float qq = qc[0][i];
+        if (qq > 0.0f) v = (pp > 0.0f) ? ((K == 2) ? fmaf(2.0f * qq, (float)q0a, quad) : quad) : (float)((double)qq * zw);
+      } else {
+        // two laws: a zero-weight pole of the other draft adds q_i(y) Qj_0; a zero target splits it in half
+        const float a = qc[0][i], c = qc[L - 1][i];
+        const float za = (a > 0.0f) ? a * (float)q0b : 0.0f, zc = (c > 0.0f) ? c * (float)q0a : 0.0f;
+        v = (pp > 0.0f) ? quad + za + zc : 0.5f * (za + zc);
+      }
+      rb[x] = v;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ coefficients
 // One workgroup per row, after the moments.  (1) Tiles the fp32 pass left
 // aside are taken in fp64, in tile order.  (2) The tile records are merged in
@@ -1262,6 +1524,18 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
 #pragma unroll
       for (int l = 0; l < L; ++l) ct[l * kEsMaxWin + i] = s_c[l][i];
     }
+    // the expansion of the grid up to each node: B_j(k) = sum_(k' <= k) c_k' e^(-(k - k') h j), stored / j!
+    if (!pl.fp64 && tid < L * kEsTaylor) {
+      const int l = tid / kEsTaylor, j = tid % kEsTaylor;
+      const double rho = exp(-(double)j * kEsStep), f = es_inv_fact(j);
+      double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
+      double acc = 0.0;
+#pragma unroll 8
+      for (int i = 0; i < pl.nk; ++i) {
+        acc = fma(acc, rho, s_c[l][i]);
+        pt[i * kEsTaylor + j] = acc * f;
+      }
+    }
   }
   // (4) rows in fp64, from the tables in LDS
   if (pl.fp64) {
@@ -1270,26 +1544,6 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
       __syncthreads();
     }
   }
-}
-
-template <int L>
-__global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __restrict__ p,
-                                                              const float* __restrict__ q1,
-                                                              const float* __restrict__ q2, int64_t V, int K,
-                                                              float* __restrict__ r, EsWork es) {
-  const int64_t t = blockIdx.x, b = blockIdx.y;
-  const EsPlan pl = es.plan[b];
-  float* rb = r + b * V;
-  if (pl.flags) {
-    for (int i = 0; i < kEsEvalPer; ++i) {
-      const int64_t x = t * kEsEvalTile + i * kEsThreads + threadIdx.x;
-      if (x < V) rb[x] = NAN;
-    }
-    return;
-  }
-  if (pl.fp64) return;  // written by the coefficient kernel
-  es_eval_tile<float, L>(p + b * V, q1 + b * V, (L == 2) ? q2 + b * V : nullptr, V, K, t, rb, pl,
-                         es.ctab + b * L * kEsMaxWin);
 }
 
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
@@ -1325,6 +1579,8 @@ void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
   es->plan = reinterpret_cast<EsPlan*>(c);
   c += align256(sizeof(EsPlan) * B);
   es->ctab = reinterpret_cast<double*>(c);
+  c += align256(sizeof(double) * B * L * kEsMaxWin);
+  es->ptab = reinterpret_cast<double*>(c);
   es->T1 = T1;
   es->T2 = T2;
 }
@@ -1334,7 +1590,8 @@ void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
 size_t workspace_bytes_expsum(int64_t B, int64_t V, int L) {
   const int64_t T1 = es_tiles(V, kEsMomTile);
   return align256(sizeof(EsTile) * B * T1 * L) + align256(sizeof(double) * B * T1 * L * kEsPart) +
-         align256(sizeof(EsPlan) * B) + align256(sizeof(double) * B * L * kEsMaxWin);
+         align256(sizeof(EsPlan) * B) + align256(sizeof(double) * B * L * kEsMaxWin) +
+         align256(sizeof(double) * B * L * kEsMaxNodes * kEsTaylor);
 }
 
 // q2 == nullptr: K i.i.d. drafts from q1; else two draft laws (K = 2).
@@ -1343,18 +1600,19 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
   const int L = (q2 != nullptr) ? 2 : 1;
   EsWork es;
   carve_es(workspace, B, V, L, &es);
-  const int64_t G1 = B * es.T1 * L;
-  const dim3 g2((unsigned)es.T2, (unsigned)B);
+  const int64_t G1 = B * es.T1 * L, G2 = B * es.T2;
   hipLaunchKernelGGL(es_moments_kernel, dim3(es_grid(es_moments_kernel, G1, kEsSlotMoments)), dim3(kEsThreads), 0, st,
                      p, q1, q2, V, L, G1, es);
   if (L == 1) {
     hipLaunchKernelGGL((es_coef_kernel<1>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
                        row_status);
-    hipLaunchKernelGGL((es_eval_kernel<1>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
+    hipLaunchKernelGGL((es_eval_kernel<1>), dim3(es_grid(es_eval_kernel<1>, G2, kEsSlotEval1)), dim3(kEsThreads), 0,
+                       st, p, q1, q2, V, K, r, G2, es);
   } else {
     hipLaunchKernelGGL((es_coef_kernel<2>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
                        row_status);
-    hipLaunchKernelGGL((es_eval_kernel<2>), g2, dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es);
+    hipLaunchKernelGGL((es_eval_kernel<2>), dim3(es_grid(es_eval_kernel<2>, G2, kEsSlotEval2)), dim3(kEsThreads), 0,
+                       st, p, q1, q2, V, K, r, G2, es);
   }
   return hipGetLastError();
 }
