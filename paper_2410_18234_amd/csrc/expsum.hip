@@ -119,8 +119,6 @@ __device__ __forceinline__ double wave_max64(double v) {
   return v;
 }
 
-__device__ __forceinline__ float es_wave_min(float v) { return wave_min(v); }
-__device__ __forceinline__ float es_wave_max(float v) { return wave_max(v); }
 __device__ __forceinline__ double es_wave_min(double v) { return wave_min64(v); }
 __device__ __forceinline__ double es_wave_max(double v) { return wave_max64(v); }
 
@@ -166,13 +164,9 @@ __device__ inline void es_scale(double wlo, double whi, int& tau, int& range) {
   range = e_hi - e_lo;
 }
 
-// node rate in the precision of the tile: fp32 a_k log2(e) 2^-tau (for exp2), fp64 a_k
+// node rate of an fp64 tile: a_k 2^-tau
 template <typename Real>
 __device__ __forceinline__ Real es_rate(int k, int tau);
-template <>
-__device__ __forceinline__ float es_rate<float>(int k, int tau) {
-  return (float)ldexp(exp((double)k * kEsStep) * kEsLog2e, -tau);
-}
 template <>
 __device__ __forceinline__ double es_rate<double>(int k, int tau) {
   return ldexp(exp((double)k * kEsStep), -tau);
@@ -180,7 +174,6 @@ __device__ __forceinline__ double es_rate<double>(int k, int tau) {
 
 __device__ __forceinline__ float es_decay(float beta, float w) { return __builtin_amdgcn_exp2f(-beta * w); }
 __device__ __forceinline__ double es_decay(double alpha, double w) { return exp(-alpha * w); }
-__device__ __forceinline__ float es_fma(float a, float b, float c) { return fmaf(a, b, c); }
 __device__ __forceinline__ double es_fma(double a, double b, double c) { return ::fma(a, b, c); }
 
 template <typename Real>
@@ -545,8 +538,6 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
 constexpr int kEsRun = 512;             // sorted tokens per run
 constexpr int kEsRunPer = kEsRun / 64;  // per lane
 constexpr int kEsWin32 = 240;           // window bound of an fp32 tile: a span within 2^161 needs <= 233 nodes
-
-__device__ __forceinline__ int es_expo(float w) { return (int)(__float_as_uint(w) >> 23); }  // w > 0, normal
 
 // Node rates of fp32 tiles: log2(e) a_k = log2(e) e^(k/2) as an fp32 mantissa
 // in [1, 2) and a binary exponent, for every node an fp32 tile can reach
@@ -1140,56 +1131,59 @@ constexpr int kEsPolyStride = kEsTaylor + 1;    // padded rows: neighbouring d f
 
 template <int L>
 __device__ __forceinline__ void es_load_eval(const float* __restrict__ p, const float* __restrict__ q1,
-                                             const float* __restrict__ q2, int64_t V, int64_t T2, int64_t g,
-                                             int tid, float (&pv)[kEsEvalPer], float (&qv)[L][kEsEvalPer]) {
-  const int64_t t = g % T2, b = g / T2;
-  const int64_t base = t * kEsEvalTile + tid;
-  const float* pb = p + b * V;
-  const float* qa = q1 + b * V;
-  const float* qc = (L == 2) ? q2 + b * V : q1 + b * V;
-  if (t * kEsEvalTile + kEsEvalTile <= V) {  // uniform: a whole tile
+                                             const float* __restrict__ q2, int64_t V, int64_t b, int t, int tid,
+                                             float (&pv)[kEsEvalPer], float (&qv)[L][kEsEvalPer]) {
+  const int64_t off = b * V + (int64_t)t * kEsEvalTile + tid;
+  const float* pb = p + off;
+  const float* qa = q1 + off;
+  const float* qc = ((L == 2) ? q2 : q1) + off;
+  if ((int64_t)t * kEsEvalTile + kEsEvalTile <= V) {  // uniform: a whole tile
 #pragma unroll
     for (int i = 0; i < kEsEvalPer; ++i) {
-      pv[i] = pb[base + i * kEsThreads];
-      qv[0][i] = qa[base + i * kEsThreads];
-      if (L == 2) qv[L - 1][i] = qc[base + i * kEsThreads];
+      pv[i] = pb[i * kEsThreads];
+      qv[0][i] = qa[i * kEsThreads];
+      if (L == 2) qv[L - 1][i] = qc[i * kEsThreads];
     }
   } else {
+    const int64_t rest = V - (int64_t)t * kEsEvalTile - tid;
 #pragma unroll
     for (int i = 0; i < kEsEvalPer; ++i) {
-      const int64_t x = base + i * kEsThreads;
-      pv[i] = (x < V) ? pb[x] : 0.0f;
-      qv[0][i] = (x < V) ? qa[x] : 0.0f;
-      if (L == 2) qv[L - 1][i] = (x < V) ? qc[x] : 0.0f;
+      const bool in = i * kEsThreads < rest;
+      pv[i] = in ? pb[i * kEsThreads] : 0.0f;
+      qv[0][i] = in ? qa[i * kEsThreads] : 0.0f;
+      if (L == 2) qv[L - 1][i] = in ? qc[i * kEsThreads] : 0.0f;
     }
   }
 }
 
-// G = B * T2 (row, tile) pairs, g = b * T2 + t; any grid size.
+// Workgroup w takes the tiles [w per, (w + 1) per) of the B * T2 (row, tile)
+// pairs, row-major.  A tile's weight range comes from the moments record of
+// the 4096-token tile that holds it, so evaluation needs no statistics pass.
 template <int L>
 __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __restrict__ p,
                                                               const float* __restrict__ q1,
                                                               const float* __restrict__ q2, int64_t V, int K,
-                                                              float* __restrict__ r, int64_t G, EsWork es) {
-  __shared__ float s_c[L][kEsTabRows + kEsTokNodes];          // c_(kt+1+i) 2^-tau (0 off the grid)
-  __shared__ float s_p[L][kEsTabRows * kEsPolyStride];        // B_j(kt + d) 2^-tau / j!
-  __shared__ float s_r[L][kEsTabRows];                        // log2(e) a_(kt+1+d) 2^-tau
-  __shared__ float s_f[2][kEsWaves][2][2];  // by tile parity: per wave and law, min and max weight
-  __shared__ int s_odd[2][kEsWaves];
-  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+                                                              float* __restrict__ r, int64_t G, int per, EsWork es) {
+  static_assert(kEsMomTile == 2 * kEsEvalTile, "an evaluation tile is half a moments tile");
+  __shared__ float s_c[L][kEsTabRows + kEsTokNodes];    // c_(kt+1+i) 2^-tau (0 off the grid)
+  __shared__ float s_p[L][kEsTabRows * kEsPolyStride];  // B_j(kt + d) 2^-tau / j!
+  __shared__ float s_r[L][kEsTabRows];                  // log2(e) a_(kt+1+d) 2^-tau
+  const int tid = threadIdx.x;
   // e^(i h) for the nine nodes of a token, and e^(-h) / log2(e) (from log2(e) a_k0 w to a_(k0-1) w)
   constexpr float kE[kEsTokNodes] = {1.0f,          1.6487212707f, 2.7182818285f, 4.4816890703f, 7.3890560989f,
                                      12.182493961f, 20.085536923f, 33.115451959f, 54.598150033f};
   constexpr float kBack = (float)(0.60653065971263342 / kEsLog2e);
 
+  const int64_t g0 = (int64_t)blockIdx.x * per, g1 = min(g0 + per, G);
+  if (g0 >= g1) return;
+  int64_t b = g0 / es.T2;
+  int t = (int)(g0 - b * es.T2);
   float pv[kEsEvalPer], qv[L][kEsEvalPer];
-  int64_t g = blockIdx.x;
-  if (g < G) es_load_eval<L>(p, q1, q2, V, es.T2, g, tid, pv, qv);
-  for (int par = 0; g < G; g += gridDim.x, par ^= 1) {
-    const int64_t gn = g + gridDim.x;
-    const int64_t b = g / es.T2, t = g % es.T2;
-    const int64_t base = t * kEsEvalTile;
-    float* rb = r + b * V;
+  es_load_eval<L>(p, q1, q2, V, b, t, tid, pv, qv);
+  for (int64_t g = g0; g < g1; ++g) {
+    const int64_t base = (int64_t)t * kEsEvalTile;
+    const bool whole = base + kEsEvalTile <= V;
+    float* rb = r + b * V + base + tid;  // (b, t) is this tile until advanced below
     float pc[kEsEvalPer], qc[L][kEsEvalPer];
 #pragma unroll
     for (int i = 0; i < kEsEvalPer; ++i) {
@@ -1197,16 +1191,20 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
 #pragma unroll
       for (int l = 0; l < L; ++l) qc[l][i] = qv[l][i];
     }
-    if (gn < G) es_load_eval<L>(p, q1, q2, V, es.T2, gn, tid, pv, qv);
+    const int64_t bb = b;
+    const int tt = t;
+    if (++t == es.T2) {
+      t = 0;
+      ++b;
+    }
+    if (g + 1 < g1) es_load_eval<L>(p, q1, q2, V, b, t, tid, pv, qv);
     __asm__ volatile("" ::: "memory");  // issued here, in flight through this tile
-    const EsPlan& pl = es.plan[b];
+    const EsPlan& pl = es.plan[bb];
     const int flags = pl.flags, fp64 = pl.fp64, k_lo = pl.k_lo, nk = pl.nk;
     if (flags) {  // uniform
 #pragma unroll
-      for (int i = 0; i < kEsEvalPer; ++i) {
-        const int64_t x = base + i * kEsThreads + tid;
-        if (x < V) rb[x] = NAN;
-      }
+      for (int i = 0; i < kEsEvalPer; ++i)
+        if (whole || base + i * kEsThreads + tid < V) rb[i * kEsThreads] = NAN;
       continue;
     }
     if (fp64) continue;  // evaluated by the coefficient kernel
@@ -1215,75 +1213,36 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
 #pragma unroll
     for (int i = 0; i < kEsEvalPer; ++i) acc[i] = 0.0f;
     if (nk > 0) {
-      // (1) weights and statistics
-      float wv[L][kEsEvalPer];
-      int odd = 0;
+      // (1) the tile's scale and tables from the moments records (every record of a
+      // row without an fp64 tile has its ratios in the fp32 normal range)
+      const EsTile* rec = es.tile + (bb * es.T1 + tt / 2) * L;
+      float wmin[2], wmax[2];
 #pragma unroll
       for (int l = 0; l < L; ++l) {
-        float lo = INFINITY, hi = 0.0f;
-#pragma unroll
-        for (int i = 0; i < kEsEvalPer; ++i) {
-          const bool pos = pc[i] > 0.0f && qc[l][i] > 0.0f;
-          const float w = pos ? es_ratio<float>(pc[i], qc[l][i]) : 0.0f;
-          if (pos) odd |= !(w >= FLT_MIN && w <= FLT_MAX);
-          wv[l][i] = w;
-          lo = pos ? fminf(lo, w) : lo;
-          hi = pos ? fmaxf(hi, w) : hi;
-        }
-        lo = es_wave_ext<false>(lo);
-        hi = es_wave_ext<true>(hi);
-        if (lane == 0) {
-          s_f[par][wid][l][0] = lo;
-          s_f[par][wid][l][1] = hi;
-        }
-      }
-      odd = wave_sum_int(odd);
-      if (lane == 0) s_odd[par][wid] = odd;
-      es_lds_barrier();
-      float wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0f, 0.0f};
-      int od = 0;
-#pragma unroll
-      for (int i = 0; i < kEsWaves; ++i) {
-        od |= s_odd[par][i];
-#pragma unroll
-        for (int l = 0; l < L; ++l) {
-          wmin[l] = fminf(wmin[l], s_f[par][i][l][0]);
-          wmax[l] = fmaxf(wmax[l], s_f[par][i][l][1]);
-        }
+        wmin[l] = (float)rec[l].wmin;  // +inf / 0 when the law has no positive weight here
+        wmax[l] = (float)rec[l].wmax;
       }
       const float lo = fminf(wmin[0], wmin[L - 1]), hi = fmaxf(wmax[0], wmax[L - 1]);
       int range = 0;
-      if (hi > 0.0f && !od) es_scale_f32(lo, hi, tau, range);
-      tau = __builtin_amdgcn_readfirstlane(tau);
-      // a row without an fp64 tile has ratios in the fp32 normal range and (two
-      // laws) a span within 2^160, and so has each of its tiles: never taken
-      if (od || range > kEsWideRange) {
-#pragma unroll
-        for (int i = 0; i < kEsEvalPer; ++i) {
-          const int64_t x = base + i * kEsThreads + tid;
-          if (x < V) rb[x] = NAN;
-        }
-        es_lds_barrier();  // every wave has read this tile's statistics
-        continue;
-      }
-      // (2) tables of the tile: kt = the last node with a_k w_max <= 1/4, rows d = 0 .. D
+      if (hi > 0.0f) es_scale_f32(lo, hi, tau, range);
       int kt[2], D[2];
 #pragma unroll
       for (int l = 0; l < L; ++l) {
-        int nw;
-        es_window_f32(fmaxf(wmin[l], FLT_MIN), fmaxf(wmax[l], FLT_MIN), kt[l], nw);
-        int ktlo, nwlo;  // the last expansion node of the smallest weight
-        es_window_f32(fmaxf(wmin[l], FLT_MIN), fmaxf(wmin[l], FLT_MIN), ktlo, nwlo);
-        kt[l] = __builtin_amdgcn_readfirstlane(kt[l]);
-        D[l] = __builtin_amdgcn_readfirstlane(min(max(ktlo - kt[l], 0), kEsTabRows - 1));
-        const double* ct = es.ctab + (b * L + l) * kEsMaxWin;
-        const double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
+        kt[l] = 0;
+        D[l] = -1;
+        if (!(wmax[l] > 0.0f)) continue;  // uniform
+        int nw, ktlo;
+        es_window_f32(wmin[l], wmax[l], kt[l], nw);
+        es_window_f32(wmin[l], wmin[l], ktlo, nw);  // the last expansion node of the smallest weight
+        D[l] = min(max(ktlo - kt[l], 0), kEsTabRows - 1);
+        const double* ct = es.ctab + (bb * L + l) * kEsMaxWin;
+        const double* pt = es.ptab + (bb * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
         for (int i = tid; i < D[l] + 1 + kEsTokNodes; i += kEsThreads) {
           const int idx = kt[l] + 1 + i - k_lo;
           s_c[l][i] = (idx >= 0 && idx < nk) ? (float)ldexp(ct[idx], -tau) : 0.0f;
         }
         for (int e = tid; e < (D[l] + 1) * kEsTaylor; e += kEsThreads) {
-          const int d = e / kEsTaylor, j = e % kEsTaylor, idx = kt[l] + d - k_lo;
+          const int d = e >> 3, j = e & (kEsTaylor - 1), idx = kt[l] + d - k_lo;
           double v = 0.0;
           if (idx >= 0)
             v = (idx < nk) ? pt[idx * kEsTaylor + j]
@@ -1294,26 +1253,28 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         for (int d = tid; d <= D[l]; d += kEsThreads) s_r[l][d] = es_rate_f32(kt[l] + 1 + d, tau);
       }
       es_lds_barrier();
-      // (3) per token: nine exponentials and the expansion
+      // (2) per token: nine exponentials and the expansion
 #pragma unroll
       for (int l = 0; l < L; ++l) {
-        if (!(wmax[l] > 0.0f)) continue;  // uniform: no token of this law has a positive weight
+        if (D[l] < 0) continue;  // uniform
         const float* sc = s_c[l];
         const float* sp = s_p[l];
         const float* sr = s_r[l];
 #pragma unroll
         for (int i = 0; i < kEsEvalPer; ++i) {
-          const float w = wv[l][i];
-          if (!(w > 0.0f)) continue;
+          const float pp = pc[i], qq = qc[l][i];
+          if (!(pp > 0.0f && qq > 0.0f)) continue;
+          const float w = es_ratio<float>(pp, qq);
           // d = kt(w) - kt, kt(w) = floor((ln 1/4 - ln w) / h)
-          const float ktw = floorf(((float)kEsLnFar - __builtin_amdgcn_logf(w) * 0.69314718f) * (float)(1.0 / kEsStep));
+          const float ktw =
+              floorf(((float)kEsLnFar - __builtin_amdgcn_logf(w) * 0.69314718f) * (float)(1.0 / kEsStep));
           const int d = min(max((int)ktw - kt[l], 0), D[l]);
           const float x = sr[d] * ldexpf(w, tau);  // log2(e) a_k0 w
           float s = 0.0f;
 #pragma unroll
           for (int m = 0; m < kEsTokNodes; ++m) s = fmaf(sc[d + m], __builtin_amdgcn_exp2f(-x * kE[m]), s);
           const float nu = -x * kBack;  // -a_(k0-1) w
-          const float* pr = sp + d * kEsPolyStride;
+          const float* pr = sp + (d << 3) + d;
           float pe = pr[kEsTaylor - 1];
 #pragma unroll
           for (int j = kEsTaylor - 2; j >= 0; --j) pe = fmaf(pe, nu, pr[j]);
@@ -1322,27 +1283,27 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
       }
       es_lds_barrier();  // the tables are rebuilt for the next tile
     }
-    // (4) epilogue: r(y) = p(y) 2^tau sum + the zero-weight closed forms
-    const double q0a = pl.q0[0], q0b = (L == 2) ? pl.q0[1] : 0.0;
-    double zw = q0a;  // K i.i.d. drafts: Q0^(K-1)
-    for (int j = 2; j < K; ++j) zw *= q0a;
+    // (3) epilogue: r(y) = p(y) 2^tau sum + the zero-weight closed forms
+    const float q0a = (float)pl.q0[0], q0b = (L == 2) ? (float)pl.q0[1] : 0.0f;
+    double zw = pl.q0[0];  // K i.i.d. drafts: Q0^(K-1)
+    for (int j = 2; j < K; ++j) zw *= pl.q0[0];
+    const float zwf = (float)zw;
 #pragma unroll
     for (int i = 0; i < kEsEvalPer; ++i) {
-      const int64_t x = base + i * kEsThreads + tid;
-      if (x >= V) break;
       const float pp = pc[i];
       const float quad = ldexpf(pp * acc[i], tau);
-      float v = 0.0f;
+      float v;
       if (L == 1) {
         const float qq = qc[0][i];
-        if (qq > 0.0f) v = (pp > 0.0f) ? ((K == 2) ? fmaf(2.0f * qq, (float)q0a, quad) : quad) : (float)((double)qq * zw);
+        v = (pp > 0.0f) ? ((K == 2) ? fmaf(2.0f * qq, q0a, quad) : quad) : qq * zwf;
+        v = (qq > 0.0f) ? v : 0.0f;
       } else {
         // two laws: a zero-weight pole of the other draft adds q_i(y) Qj_0; a zero target splits it in half
         const float a = qc[0][i], c = qc[L - 1][i];
-        const float za = (a > 0.0f) ? a * (float)q0b : 0.0f, zc = (c > 0.0f) ? c * (float)q0a : 0.0f;
+        const float za = (a > 0.0f) ? a * q0b : 0.0f, zc = (c > 0.0f) ? c * q0a : 0.0f;
         v = (pp > 0.0f) ? quad + za + zc : 0.5f * (za + zc);
       }
-      rb[x] = v;
+      if (whole || base + i * kEsThreads + tid < V) rb[i * kEsThreads] = v;
     }
   }
 }
@@ -1606,13 +1567,15 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
   if (L == 1) {
     hipLaunchKernelGGL((es_coef_kernel<1>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
                        row_status);
-    hipLaunchKernelGGL((es_eval_kernel<1>), dim3(es_grid(es_eval_kernel<1>, G2, kEsSlotEval1)), dim3(kEsThreads), 0,
-                       st, p, q1, q2, V, K, r, G2, es);
+    const unsigned n2 = es_grid(es_eval_kernel<1>, G2, kEsSlotEval1);
+    hipLaunchKernelGGL((es_eval_kernel<1>), dim3(n2), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, G2,
+                       (int)((G2 + n2 - 1) / n2), es);
   } else {
     hipLaunchKernelGGL((es_coef_kernel<2>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
                        row_status);
-    hipLaunchKernelGGL((es_eval_kernel<2>), dim3(es_grid(es_eval_kernel<2>, G2, kEsSlotEval2)), dim3(kEsThreads), 0,
-                       st, p, q1, q2, V, K, r, G2, es);
+    const unsigned n2 = es_grid(es_eval_kernel<2>, G2, kEsSlotEval2);
+    hipLaunchKernelGGL((es_eval_kernel<2>), dim3(n2), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, G2,
+                       (int)((G2 + n2 - 1) / n2), es);
   }
   return hipGetLastError();
 }
