@@ -248,9 +248,9 @@ __device__ __forceinline__ float dpp(float x) {
 // flips that bit and keeps the others below bit 4, so every lane is paired
 // once), by bits 4 and 5 through the row and half swaps of gfx950; the bits
 // left over are summed (swaps with the value itself, quad permutations).  For
-// NB = 16 / 8 / 4 lane l ends with the total of value 8 b2 + 4 b3 + 2 b4 + b5 /
-// 4 b2 + 2 b3 + b4 / 2 b2 + b3 (b_i = bit i of l); es_scatter_node and
-// es_scatter_writer name that value and one lane holding it.
+// NB = 16 / 8 / 4 / 2 / 1 lane l ends with the total of value 8 b2 + 4 b3 + 2 b4
+// + b5 / 4 b2 + 2 b3 + b4 / 2 b2 + b3 / b2 / 0 (b_i = bit i of l);
+// es_scatter_node and es_scatter_writer name that value and one lane holding it.
 template <int HALF, int N, int CTRL>
 __device__ __forceinline__ void rs_dpp(float (&v)[N], bool up) {
 #pragma unroll
@@ -277,10 +277,24 @@ __device__ __forceinline__ float sum_swap(float x) {
 }
 template <int NB>
 __device__ __forceinline__ float wave_reduce_scatter_f32(float (&v)[NB], int lane) {
-  static_assert(NB == 4 || NB == 8 || NB == 16, "block sizes");
+  static_assert(NB == 1 || NB == 2 || NB == 4 || NB == 8 || NB == 16, "block sizes");
+  float x;
+  if constexpr (NB <= 2) {
+    if constexpr (NB == 2) {
+      rs_dpp<1, NB, 0x124>(v, (lane & 4) != 0);  // row_ror:4
+      x = v[0];
+    } else {
+      x = v[0];
+      x += dpp<0x124>(x);
+    }
+    x += dpp<0x128>(x);  // row_ror:8
+    x = sum_swap<false>(sum_swap<true>(x));
+    x += dpp<0xB1>(x);
+    x += dpp<0x4E>(x);
+    return x;
+  }
   rs_dpp<NB / 2, NB, 0x124>(v, (lane & 4) != 0);  // row_ror:4
   rs_dpp<NB / 4, NB, 0x128>(v, (lane & 8) != 0);  // row_ror:8
-  float x;
   if constexpr (NB == 16) {
     rs_swap<2, NB, true>(v);
     rs_swap<1, NB, false>(v);
@@ -298,11 +312,14 @@ __device__ __forceinline__ float wave_reduce_scatter_f32(float (&v)[NB], int lan
 template <int NB>
 __device__ __forceinline__ int es_scatter_node(int lane) {
   const int b2 = (lane >> 2) & 1, b3 = (lane >> 3) & 1, b4 = (lane >> 4) & 1, b5 = (lane >> 5) & 1;
-  return NB == 16 ? 8 * b2 + 4 * b3 + 2 * b4 + b5 : (NB == 8 ? 4 * b2 + 2 * b3 + b4 : 2 * b2 + b3);
+  return NB == 16 ? 8 * b2 + 4 * b3 + 2 * b4 + b5
+                  : (NB == 8 ? 4 * b2 + 2 * b3 + b4 : (NB == 4 ? 2 * b2 + b3 : (NB == 2 ? b2 : 0)));
 }
 template <int NB>
 __device__ __forceinline__ bool es_scatter_writer(int lane) {
-  return NB == 16 ? (lane & 3) == 0 : (NB == 8 ? (lane & 0x23) == 0 : (lane & 0x33) == 0);
+  return NB == 16 ? (lane & 3) == 0
+                  : (NB == 8 ? (lane & 0x23) == 0
+                             : (NB == 4 ? (lane & 0x33) == 0 : (NB == 2 ? (lane & 0x3B) == 0 : lane == 0)));
 }
 
 // Minimum / maximum of a float over the 64 lanes of a wave, in every lane
@@ -645,8 +662,8 @@ __device__ __forceinline__ void es_run_block(const float (&w)[kEsRunPer], const 
 // entries of tokens left out are zero).  red / tay: the wave's moments of the
 // tile window and power sums at the tile's expansion node.
 __device__ void es_moments_run(const float* __restrict__ s_w, const float* __restrict__ s_q,
-                               const float* __restrict__ s_rate, int r, int kt, int nw, int tau, int lane,
-                               float* __restrict__ red, float* __restrict__ tay) {
+                               const float* __restrict__ s_rate, int r, int kt, int nw, int tau, bool whole,
+                               int lane, float* __restrict__ red, float* __restrict__ tay) {
   constexpr float kInvFact[kEsTaylor] = {1.0f,        1.0f,         0.5f,          1.0f / 6.0f,
                                          1.0f / 24.0f, 1.0f / 120.0f, 1.0f / 720.0f, 1.0f / 5040.0f};
   float w[kEsRunPer], qq[kEsRunPer];
@@ -656,9 +673,19 @@ __device__ void es_moments_run(const float* __restrict__ s_w, const float* __res
     const int j = r * kEsRun + e * 64 + lane;
     w[e] = s_w[j];
     qq[e] = s_q[j];
-    if (qq[e] > 0.0f) {  // entries left out hold w = q = 0
+  }
+  if (whole) {
+    // every entry is a token and each column is sorted: entry e (row 2r) <= entry e + 4 (row 2r + 1)
+#pragma unroll
+    for (int e = 0; e < kEsRunPer / 2; ++e) {
       lo = fminf(lo, w[e]);
-      hi = fmaxf(hi, w[e]);
+      hi = fmaxf(hi, w[e + kEsRunPer / 2]);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < kEsRunPer; ++e) {
+      hi = fmaxf(hi, w[e]);                     // entries left out hold w = q = 0
+      lo = (qq[e] > 0.0f) ? fminf(lo, w[e]) : lo;
     }
   }
   lo = es_uniform_min(lo);
@@ -699,7 +726,15 @@ __device__ void es_moments_run(const float* __restrict__ s_w, const float* __res
     es_run_block<8>(w, qq, rate + nb, lane, red + o + nb, 8);
     nb += 8;
   }
-  for (; nb < cnt; nb += 4) es_run_block<4>(w, qq, rate + nb, lane, red + o + nb, cnt - nb);
+  if (nb + 4 <= cnt) {
+    es_run_block<4>(w, qq, rate + nb, lane, red + o + nb, 4);
+    nb += 4;
+  }
+  if (nb + 2 <= cnt) {
+    es_run_block<2>(w, qq, rate + nb, lane, red + o + nb, 2);
+    nb += 2;
+  }
+  if (nb < cnt) es_run_block<1>(w, qq, rate + nb, lane, red + o + nb, 1);
   // tile nodes kt + 1 .. kt + o from the run's expansion: node kt + 1 + i has a_k / a_(kt+o) = e^(-(o - 1 - i) h)
   for (int i = lane; i < o; i += 64) {
     const float v = __builtin_amdgcn_exp2f(-(float)(o - 1 - i) * (float)(kEsStep * kEsLog2e));
@@ -716,34 +751,34 @@ __device__ void es_moments_run(const float* __restrict__ s_w, const float* __res
 }
 
 __device__ __forceinline__ void es_load_tile(const float* __restrict__ p, const float* __restrict__ q1,
-                                             const float* __restrict__ q2, int64_t V, int L, int64_t T1, int64_t g,
+                                             const float* __restrict__ q2, int64_t V, int64_t b, int t, int l,
                                              int tid, float (&pv)[kEsMomPer], float (&qv)[kEsMomPer]) {
-  const int l = (int)(g % L);
-  const int64_t bt = g / L, t = bt % T1, b = bt / T1;
-  const float* pb = p + b * V;
-  const float* qb = (l == 0 ? q1 : q2) + b * V;
-  const int64_t base = t * kEsMomTile + tid;
-  if (t * kEsMomTile + kEsMomTile <= V) {  // uniform: a whole tile
+  const int64_t off = b * V + (int64_t)t * kEsMomTile + tid;
+  const float* pb = p + off;
+  const float* qb = (l == 0 ? q1 : q2) + off;
+  if ((int64_t)t * kEsMomTile + kEsMomTile <= V) {  // uniform: a whole tile
 #pragma unroll
     for (int i = 0; i < kEsMomPer; ++i) {
-      pv[i] = pb[base + i * kEsThreads];
-      qv[i] = qb[base + i * kEsThreads];
+      pv[i] = pb[i * kEsThreads];
+      qv[i] = qb[i * kEsThreads];
     }
   } else {
+    const int64_t rest = V - (int64_t)t * kEsMomTile - tid;
 #pragma unroll
     for (int i = 0; i < kEsMomPer; ++i) {
-      const int64_t x = base + i * kEsThreads;
-      pv[i] = (x < V) ? pb[x] : 0.0f;
-      qv[i] = (x < V) ? qb[x] : 0.0f;
+      const bool in = i * kEsThreads < rest;
+      pv[i] = in ? pb[i * kEsThreads] : 0.0f;
+      qv[i] = in ? qb[i * kEsThreads] : 0.0f;
     }
   }
 }
 
-// G = B * T1 * L records, record g = (b * T1 + t) * L + l; any grid size.
+// G = B * T1 * L records, record g = (b * T1 + t) * L + l; workgroup w takes the
+// records [w per, (w + 1) per).
 __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* __restrict__ p,
                                                                  const float* __restrict__ q1,
                                                                  const float* __restrict__ q2, int64_t V, int L,
-                                                                 int64_t G, EsWork es) {
+                                                                 int64_t G, int per, EsWork es) {
   __shared__ float s_w[kEsMomTile];
   __shared__ float s_q[kEsMomTile];
   __shared__ float s_red[kEsWaves][kEsWin32];
@@ -755,10 +790,21 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
   const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   float pv[kEsMomPer], qv[kEsMomPer];
-  int64_t g = blockIdx.x;
-  if (g < G) es_load_tile(p, q1, q2, V, L, es.T1, g, tid, pv, qv);
-  for (int par = 0; g < G; g += gridDim.x, par ^= 1) {
-    const int64_t gn = g + gridDim.x;
+  const int64_t g0 = (int64_t)blockIdx.x * per, g1 = min(g0 + per, G);
+  if (g0 >= g1) return;
+  int64_t b = g0 / (es.T1 * L);
+  int t = (int)((g0 / L) % es.T1), l = (int)(g0 % L);
+  es_load_tile(p, q1, q2, V, b, t, l, tid, pv, qv);
+  for (int64_t g = g0, par = 0; g < g1; ++g, par ^= 1) {
+    const bool more = g + 1 < g1;
+    const bool whole = (int64_t)t * kEsMomTile + kEsMomTile <= V;
+    if (++l == L) {  // (b, t, l) of the next record
+      l = 0;
+      if (++t == es.T1) {
+        t = 0;
+        ++b;
+      }
+    }
     // (1) ratios and statistics
     bool pos[kEsMomPer];
     float wv[kEsMomPer];
@@ -767,10 +813,11 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
 #pragma unroll
     for (int i = 0; i < kEsMomPer; ++i) {
       const float pp = pv[i], qq = qv[i];
-      bad |= (int)bad_prob(pp) | (int)bad_prob(qq);
+      // NaN, -inf, negative normal or denormal, +inf (-0 is a zero probability)
+      bad |= (int)__builtin_amdgcn_class(pp, 0x21F) | (int)__builtin_amdgcn_class(qq, 0x21F);
       pos[i] = pp > 0.0f && qq > 0.0f;
       const float w = pos[i] ? es_ratio<float>(pp, qq) : 0.0f;
-      if (pos[i]) odd |= !(w >= FLT_MIN && w <= FLT_MAX);
+      if (pos[i]) odd |= !__builtin_amdgcn_class(w, 0x100);  // not a positive normal
       wv[i] = w;
       wlo = pos[i] ? fminf(wlo, w) : wlo;
       whi = pos[i] ? fmaxf(whi, w) : whi;
@@ -836,7 +883,7 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
       es.tile[g] = o;
     }
     if (bd || n == 0 || wide) {  // uniform; an fp64 tile is taken by the coefficient kernel
-      if (gn < G) es_load_tile(p, q1, q2, V, L, es.T1, gn, tid, pv, qv);
+      if (more) es_load_tile(p, q1, q2, V, b, t, l, tid, pv, qv);
       continue;
     }
     // (2) each thread sorts its tokens by weight (key: the weight's bits above the
@@ -869,10 +916,12 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
     for (int k = lane; k < nw; k += 64) s_red[wid][k] = 0.0f;
     if (lane < kEsTaylor) s_tay[wid][lane] = 0.0f;
     es_lds_barrier();
-    if (gn < G) es_load_tile(p, q1, q2, V, L, es.T1, gn, tid, pv, qv);  // in flight during the runs
+    if (more) es_load_tile(p, q1, q2, V, b, t, l, tid, pv, qv);  // in flight during the runs
     __asm__ volatile("" ::: "memory");  // keeps the loads here (not sunk past the runs)
     // (3) runs: rows 2r and 2r + 1
-    for (int r = wid; r < kEsMomPer / 2; r += kEsWaves) es_moments_run(s_w, s_q, s_rate, r, kt, nw, tau, lane, s_red[wid], s_tay[wid]);
+    const bool full = whole && n == kEsMomTile;  // every entry of the layout is a token
+    for (int r = wid; r < kEsMomPer / 2; r += kEsWaves)
+      es_moments_run(s_w, s_q, s_rate, r, kt, nw, tau, full, lane, s_red[wid], s_tay[wid]);
     es_lds_barrier();
     // (4) the tile's moments and power sums, waves in order
     double* part = es.part + g * kEsPart;
@@ -1562,8 +1611,9 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
   EsWork es;
   carve_es(workspace, B, V, L, &es);
   const int64_t G1 = B * es.T1 * L, G2 = B * es.T2;
-  hipLaunchKernelGGL(es_moments_kernel, dim3(es_grid(es_moments_kernel, G1, kEsSlotMoments)), dim3(kEsThreads), 0, st,
-                     p, q1, q2, V, L, G1, es);
+  const unsigned n1 = es_grid(es_moments_kernel, G1, kEsSlotMoments);
+  hipLaunchKernelGGL(es_moments_kernel, dim3(n1), dim3(kEsThreads), 0, st, p, q1, q2, V, L, G1,
+                     (int)((G1 + n1 - 1) / n1), es);
   if (L == 1) {
     hipLaunchKernelGGL((es_coef_kernel<1>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
                        row_status);
