@@ -1383,7 +1383,11 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
   __shared__ EsPlan s_plan;
   __shared__ double s_c[L][kEsMaxWin];
   __shared__ double s_rho[kEsMaxWin];  // e^(-m h): (a_k / a_kt) for k = kt - m
+  constexpr int kCh = 64;              // tile records staged per pass of (3)
+  __shared__ int s_rkt[kCh], s_rnw[kCh];
+  __shared__ double s_pow[kCh][kEsTaylor];
 
+  for (int m = tid; m < kEsMaxWin; m += kEsThreads) s_rho[m] = exp(-(double)m * kEsStep);
   // (1) fp64 tiles
   int w = 0;
   for (int64_t i = tid; i < nrec; i += kEsThreads) w |= rec[i].wide && !rec[i].bad;
@@ -1483,49 +1487,73 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
   if (pl.nk > 0) {
     // (3) S_l(k), two nodes per thread, tiles in order: nodes up to a tile's kt from
     // its power sums, sum_j (-a_k / a_kt)^j T_j / j!; its window from the stored
-    // moments; nothing after the window
-    for (int m = tid; m < kEsMaxWin; m += kEsThreads) s_rho[m] = exp(-(double)m * kEsStep);
-    __syncthreads();
-    double inv_fact[kEsTaylor];
+    // moments; nothing after the window.  The records and power sums are staged in
+    // LDS 64 at a time and the window moments of eight records are loaded at once.
+    double S[2][L];
 #pragma unroll
-    for (int j = 0; j < kEsTaylor; ++j) inv_fact[j] = es_inv_fact(j);
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int l = 0; l < L; ++l) S[u][l] = 0.0;
+    for (int64_t c0 = 0; c0 < nrec; c0 += kCh) {
+      const int nc = (int)min((int64_t)kCh, nrec - c0);
+      __syncthreads();  // the previous pass is consumed
+      if (tid < nc) {
+        const EsTile& e = rec[c0 + tid];
+        s_rkt[tid] = e.kt;
+        s_rnw[tid] = (e.npos > 0 && !e.bad) ? e.nw : -1;  // -1: the record adds nothing
+      }
+      for (int x = tid; x < nc * kEsTaylor; x += kEsThreads) {
+        const int i = x / kEsTaylor, j = x % kEsTaylor;
+        s_pow[i][j] = part[(c0 + i) * kEsPart + j] * es_inv_fact(j);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int i = tid + u * kEsThreads;
+        if (i >= pl.nk) continue;
+        const int k = pl.k_lo + i;
+        for (int i0 = 0; i0 < nc; i0 += 8) {
+          double win[8];
+#pragma unroll
+          for (int m = 0; m < 8; ++m) {
+            const int ri = i0 + m;
+            win[m] = 0.0;
+            if (ri < nc) {
+              const int d = k - s_rkt[ri];
+              if (d >= 1 && d <= s_rnw[ri]) win[m] = part[(c0 + ri) * kEsPart + kEsTaylor + d - 1];
+            }
+          }
+#pragma unroll
+          for (int m = 0; m < 8; ++m) {
+            const int ri = i0 + m;
+            if (ri >= nc || s_rnw[ri] < 0) continue;
+            const int d = k - s_rkt[ri];
+            double v = win[m];
+            if (d <= 0) {
+              const double nx = -s_rho[min(-d, kEsMaxWin - 1)];
+              v = s_pow[ri][kEsTaylor - 1];
+#pragma unroll
+              for (int j = kEsTaylor - 2; j >= 0; --j) v = fma(v, nx, s_pow[ri][j]);
+            }
+            S[u][ri % L] += v;  // records are (tile, law) in order; c0 is even
+          }
+        }
+      }
+    }
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int i = tid + u * kEsThreads;
       if (i >= pl.nk) continue;
       const int k = pl.k_lo + i;
-      double S[L];
-#pragma unroll
-      for (int l = 0; l < L; ++l) S[l] = 0.0;
-#pragma unroll 2
-      for (int64_t t = 0; t < es.T1; ++t) {
-#pragma unroll
-        for (int l = 0; l < L; ++l) {
-          const EsTile& e = rec[t * L + l];
-          if (e.npos == 0 || e.bad) continue;
-          const double* pt = part + (t * L + l) * kEsPart;
-          const int d = k - e.kt;
-          double v;
-          if (d <= 0) {
-            const double nx = -s_rho[min(-d, kEsMaxWin - 1)];
-            v = pt[kEsTaylor - 1] * inv_fact[kEsTaylor - 1];
-#pragma unroll
-            for (int j = kEsTaylor - 2; j >= 0; --j) v = fma(v, nx, pt[j] * inv_fact[j]);
-          } else {
-            v = (d <= e.nw) ? pt[kEsTaylor + d - 1] : 0.0;
-          }
-          S[l] += v;
-        }
-      }
       const double ha = kEsStep * exp((double)k * kEsStep);
       if (L == 1) {
-        const double sm = S[0] + (K >= 3 ? pl.q0[0] : 0.0);
+        const double sm = S[u][0] + (K >= 3 ? pl.q0[0] : 0.0);
         double sp = 1.0;
         for (int j = 1; j < K; ++j) sp *= sm;
         s_c[0][i] = (double)K * ha * sp;
       } else {
-        s_c[0][i] = ha * S[L - 1];
-        s_c[L - 1][i] = ha * S[0];
+        s_c[0][i] = ha * S[u][L - 1];
+        s_c[L - 1][i] = ha * S[u][0];
       }
     }
     __syncthreads();
