@@ -103,7 +103,7 @@ struct EsWork {
   EsPlan* plan;     // [B]
   double* ctab;     // [B][L][kEsMaxWin] c_k, k = k_lo + i
   double* ptab;     // [B][L][kEsMaxNodes][kEsTaylor] B_j(k_lo + i) / j!: the expansion of the grid up to a node
-  int64_t T1, T2;
+  int64_t T1, T2, T3;  // moments tiles, fp64 evaluation tiles, fp32 evaluation tiles (per row)
 };
 
 __host__ __device__ inline int64_t es_tiles(int64_t V, int tile) { return (V + tile - 1) / tile; }
@@ -1164,7 +1164,7 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
 }
 
 // ------------------------------------------------------------------ evaluation (fp32)
-// Persistent workgroups over the (row, tile) pairs of 2048 tokens, the next
+// Persistent workgroups over the (row, tile) pairs of 1024 tokens, the next
 // tile's p and q in flight meanwhile.  Every query token takes its own nodes:
 // with k0 its first node where a_k w > 1/4, the nine nodes k0 .. k0 + 8 have
 // a_k w in (1/4, 22.5] and get exponentials, the grid nodes below k0 enter
@@ -1175,28 +1175,30 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
 // node): c_k, B_j / j! and the node rates; each token reads them at its own
 // offset.
 constexpr int kEsTokNodes = 9;                  // exponentials per query token
+constexpr int kEsTokPer = 4;                    // tokens per thread
+constexpr int kEsTokTile = kEsThreads * kEsTokPer;  // 1024 tokens per tile
 constexpr int kEsTabRows = kEsWin32 + 1;        // d = 0 .. 240
 constexpr int kEsPolyStride = kEsTaylor + 1;    // padded rows: neighbouring d fall in different banks
 
 template <int L>
 __device__ __forceinline__ void es_load_eval(const float* __restrict__ p, const float* __restrict__ q1,
                                              const float* __restrict__ q2, int64_t V, int64_t b, int t, int tid,
-                                             float (&pv)[kEsEvalPer], float (&qv)[L][kEsEvalPer]) {
-  const int64_t off = b * V + (int64_t)t * kEsEvalTile + tid;
+                                             float (&pv)[kEsTokPer], float (&qv)[L][kEsTokPer]) {
+  const int64_t off = b * V + (int64_t)t * kEsTokTile + tid;
   const float* pb = p + off;
   const float* qa = q1 + off;
   const float* qc = ((L == 2) ? q2 : q1) + off;
-  if ((int64_t)t * kEsEvalTile + kEsEvalTile <= V) {  // uniform: a whole tile
+  if ((int64_t)t * kEsTokTile + kEsTokTile <= V) {  // uniform: a whole tile
 #pragma unroll
-    for (int i = 0; i < kEsEvalPer; ++i) {
+    for (int i = 0; i < kEsTokPer; ++i) {
       pv[i] = pb[i * kEsThreads];
       qv[0][i] = qa[i * kEsThreads];
       if (L == 2) qv[L - 1][i] = qc[i * kEsThreads];
     }
   } else {
-    const int64_t rest = V - (int64_t)t * kEsEvalTile - tid;
+    const int64_t rest = V - (int64_t)t * kEsTokTile - tid;
 #pragma unroll
-    for (int i = 0; i < kEsEvalPer; ++i) {
+    for (int i = 0; i < kEsTokPer; ++i) {
       const bool in = i * kEsThreads < rest;
       pv[i] = in ? pb[i * kEsThreads] : 0.0f;
       qv[0][i] = in ? qa[i * kEsThreads] : 0.0f;
@@ -1213,7 +1215,7 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
                                                               const float* __restrict__ q1,
                                                               const float* __restrict__ q2, int64_t V, int K,
                                                               float* __restrict__ r, int64_t G, int per, EsWork es) {
-  static_assert(kEsMomTile == 2 * kEsEvalTile, "an evaluation tile is half a moments tile");
+  static_assert(kEsMomTile % kEsTokTile == 0, "an evaluation tile lies in one moments tile");
   __shared__ float s_c[L][kEsTabRows + kEsTokNodes];    // c_(kt+1+i) 2^-tau (0 off the grid)
   __shared__ float s_p[L][kEsTabRows * kEsPolyStride];  // B_j(kt + d) 2^-tau / j!
   __shared__ float s_r[L][kEsTabRows];                  // log2(e) a_(kt+1+d) 2^-tau
@@ -1225,24 +1227,26 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
 
   const int64_t g0 = (int64_t)blockIdx.x * per, g1 = min(g0 + per, G);
   if (g0 >= g1) return;
-  int64_t b = g0 / es.T2;
-  int t = (int)(g0 - b * es.T2);
-  float pv[kEsEvalPer], qv[L][kEsEvalPer];
+  int64_t b = g0 / es.T3;
+  int t = (int)(g0 - b * es.T3);
+  int64_t built = -1;  // moments record whose tables are in LDS (both halves of it share them)
+  int tau = 0, kt[2] = {0, 0}, D[2] = {-1, -1};
+  float pv[kEsTokPer], qv[L][kEsTokPer];
   es_load_eval<L>(p, q1, q2, V, b, t, tid, pv, qv);
   for (int64_t g = g0; g < g1; ++g) {
-    const int64_t base = (int64_t)t * kEsEvalTile;
-    const bool whole = base + kEsEvalTile <= V;
+    const int64_t base = (int64_t)t * kEsTokTile;
+    const bool whole = base + kEsTokTile <= V;
     float* rb = r + b * V + base + tid;  // (b, t) is this tile until advanced below
-    float pc[kEsEvalPer], qc[L][kEsEvalPer];
+    float pc[kEsTokPer], qc[L][kEsTokPer];
 #pragma unroll
-    for (int i = 0; i < kEsEvalPer; ++i) {
+    for (int i = 0; i < kEsTokPer; ++i) {
       pc[i] = pv[i];
 #pragma unroll
       for (int l = 0; l < L; ++l) qc[l][i] = qv[l][i];
     }
     const int64_t bb = b;
     const int tt = t;
-    if (++t == es.T2) {
+    if (++t == es.T3) {
       t = 0;
       ++b;
     }
@@ -1252,19 +1256,22 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
     const int flags = pl.flags, fp64 = pl.fp64, k_lo = pl.k_lo, nk = pl.nk;
     if (flags) {  // uniform
 #pragma unroll
-      for (int i = 0; i < kEsEvalPer; ++i)
+      for (int i = 0; i < kEsTokPer; ++i)
         if (whole || base + i * kEsThreads + tid < V) rb[i * kEsThreads] = NAN;
       continue;
     }
     if (fp64) continue;  // evaluated by the coefficient kernel
-    int tau = 0;
-    float acc[kEsEvalPer];
+    float acc[kEsTokPer];
 #pragma unroll
-    for (int i = 0; i < kEsEvalPer; ++i) acc[i] = 0.0f;
-    if (nk > 0) {
+    for (int i = 0; i < kEsTokPer; ++i) acc[i] = 0.0f;
+    if (nk <= 0) tau = 0;
+    const int64_t recno = bb * es.T1 + tt / (kEsMomTile / kEsTokTile);
+    if (nk > 0 && recno != built) {  // uniform
       // (1) the tile's scale and tables from the moments records (every record of a
       // row without an fp64 tile has its ratios in the fp32 normal range)
-      const EsTile* rec = es.tile + (bb * es.T1 + tt / 2) * L;
+      if (built >= 0) es_lds_barrier();  // every wave is done with the previous tables
+      built = recno;
+      const EsTile* rec = es.tile + recno * L;
       float wmin[2], wmax[2];
 #pragma unroll
       for (int l = 0; l < L; ++l) {
@@ -1273,8 +1280,8 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
       }
       const float lo = fminf(wmin[0], wmin[L - 1]), hi = fmaxf(wmax[0], wmax[L - 1]);
       int range = 0;
+      tau = 0;
       if (hi > 0.0f) es_scale_f32(lo, hi, tau, range);
-      int kt[2], D[2];
 #pragma unroll
       for (int l = 0; l < L; ++l) {
         kt[l] = 0;
@@ -1302,6 +1309,8 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         for (int d = tid; d <= D[l]; d += kEsThreads) s_r[l][d] = es_rate_f32(kt[l] + 1 + d, tau);
       }
       es_lds_barrier();
+    }
+    if (nk > 0) {
       // (2) per token: nine exponentials and the expansion
 #pragma unroll
       for (int l = 0; l < L; ++l) {
@@ -1309,28 +1318,34 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         const float* sc = s_c[l];
         const float* sp = s_p[l];
         const float* sr = s_r[l];
+        // branch-free over the thread's tokens, so that their dependency chains interleave;
+        // a token without a positive weight is evaluated at w = 1 and its result dropped
+        bool ok[kEsTokPer];
+        int d[kEsTokPer];
+        float x[kEsTokPer];
 #pragma unroll
-        for (int i = 0; i < kEsEvalPer; ++i) {
-          const float pp = pc[i], qq = qc[l][i];
-          if (!(pp > 0.0f && qq > 0.0f)) continue;
-          const float w = es_ratio<float>(pp, qq);
+        for (int i = 0; i < kEsTokPer; ++i) {
+          ok[i] = pc[i] > 0.0f && qc[l][i] > 0.0f;
+          const float w = ok[i] ? es_ratio<float>(pc[i], qc[l][i]) : 1.0f;
           // d = kt(w) - kt, kt(w) = floor((ln 1/4 - ln w) / h)
           const float ktw =
               floorf(((float)kEsLnFar - __builtin_amdgcn_logf(w) * 0.69314718f) * (float)(1.0 / kEsStep));
-          const int d = min(max((int)ktw - kt[l], 0), D[l]);
-          const float x = sr[d] * ldexpf(w, tau);  // log2(e) a_k0 w
+          d[i] = min(max((int)ktw - kt[l], 0), D[l]);
+          x[i] = sr[d[i]] * ldexpf(w, tau);  // log2(e) a_k0 w
+        }
+#pragma unroll
+        for (int i = 0; i < kEsTokPer; ++i) {
           float s = 0.0f;
 #pragma unroll
-          for (int m = 0; m < kEsTokNodes; ++m) s = fmaf(sc[d + m], __builtin_amdgcn_exp2f(-x * kE[m]), s);
-          const float nu = -x * kBack;  // -a_(k0-1) w
-          const float* pr = sp + (d << 3) + d;
+          for (int m = 0; m < kEsTokNodes; ++m) s = fmaf(sc[d[i] + m], __builtin_amdgcn_exp2f(-x[i] * kE[m]), s);
+          const float nu = -x[i] * kBack;  // -a_(k0-1) w
+          const float* pr = sp + (d[i] << 3) + d[i];
           float pe = pr[kEsTaylor - 1];
 #pragma unroll
           for (int j = kEsTaylor - 2; j >= 0; --j) pe = fmaf(pe, nu, pr[j]);
-          acc[i] += s + pe;
+          acc[i] += ok[i] ? s + pe : 0.0f;
         }
       }
-      es_lds_barrier();  // the tables are rebuilt for the next tile
     }
     // (3) epilogue: r(y) = p(y) 2^tau sum + the zero-weight closed forms
     const float q0a = (float)pl.q0[0], q0b = (L == 2) ? (float)pl.q0[1] : 0.0f;
@@ -1338,7 +1353,7 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
     for (int j = 2; j < K; ++j) zw *= pl.q0[0];
     const float zwf = (float)zw;
 #pragma unroll
-    for (int i = 0; i < kEsEvalPer; ++i) {
+    for (int i = 0; i < kEsTokPer; ++i) {
       const float pp = pc[i];
       const float quad = ldexpf(pp * acc[i], tau);
       float v;
@@ -1621,6 +1636,7 @@ void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
   es->ptab = reinterpret_cast<double*>(c);
   es->T1 = T1;
   es->T2 = T2;
+  es->T3 = es_tiles(V, kEsTokTile);
 }
 
 }  // namespace
@@ -1638,7 +1654,7 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
   const int L = (q2 != nullptr) ? 2 : 1;
   EsWork es;
   carve_es(workspace, B, V, L, &es);
-  const int64_t G1 = B * es.T1 * L, G2 = B * es.T2;
+  const int64_t G1 = B * es.T1 * L, G2 = B * es.T3;
   const unsigned n1 = es_grid(es_moments_kernel, G1, kEsSlotMoments);
   hipLaunchKernelGGL(es_moments_kernel, dim3(n1), dim3(kEsThreads), 0, st, p, q1, q2, V, L, G1,
                      (int)((G1 + n1 - 1) / n1), es);
