@@ -604,6 +604,29 @@ __device__ __forceinline__ float es_rate_f32(int k, int tau) {
   return __int_as_float(__float_as_int(kEsRates.mant[i]) + ((kEsRates.expo[i] - tau) << 23));
 }
 
+// A load through the scalar cache (constant address space) at a wave-uniform
+// address: it waits on the scalar counter, so vector loads in flight (the next
+// tile's p and q) are not waited for.  Only for data no kernel in flight writes.
+template <typename T>
+__device__ __forceinline__ T es_sload(const T* p) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);  // the address is the same in every lane: say so
+  const uint64_t u = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
+                     (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+  return *(const __attribute__((address_space(4))) T*)(u);
+}
+// a whole record, dword by dword (merged into wide scalar loads; the scalar unit
+// has no 12-byte load, so a partial read of a record would go to the vector unit)
+template <typename T>
+__device__ __forceinline__ T es_sload_rec(const T* p) {
+  static_assert(sizeof(T) % 16 == 0, "whole 16-byte pieces");
+  uint32_t raw[sizeof(T) / 4];
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) raw[i] = es_sload(reinterpret_cast<const uint32_t*>(p) + i);
+  T out;
+  __builtin_memcpy(&out, raw, sizeof(T));
+  return out;
+}
+
 
 // Workgroup barrier that orders LDS only: global loads issued before it stay in flight.
 __device__ __forceinline__ void es_lds_barrier() {
@@ -912,7 +935,10 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
         s_q[i * kEsThreads + tid] = sq[i];
       }
     }
-    for (int k = tid; k <= nw + 4; k += kEsThreads) s_rate[k] = es_rate_f32(kt + k, tau);
+    for (int k = wid; k <= nw + 4; k += kEsWaves) {  // scalar table loads: the prefetch below is not waited for
+      const float rt = es_rate_f32(kt + k, tau);
+      if (lane == 0) s_rate[k] = rt;
+    }
     for (int k = lane; k < nw; k += 64) s_red[wid][k] = 0.0f;
     if (lane < kEsTaylor) s_tay[wid][lane] = 0.0f;
     es_lds_barrier();
@@ -1219,7 +1245,7 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
   __shared__ float s_c[L][kEsTabRows + kEsTokNodes];    // c_(kt+1+i) 2^-tau (0 off the grid)
   __shared__ float s_p[L][kEsTabRows * kEsPolyStride];  // B_j(kt + d) 2^-tau / j!
   __shared__ float s_r[L][kEsTabRows];                  // log2(e) a_(kt+1+d) 2^-tau
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   // e^(i h) for the nine nodes of a token, and e^(-h) / log2(e) (from log2(e) a_k0 w to a_(k0-1) w)
   constexpr float kE[kEsTokNodes] = {1.0f,          1.6487212707f, 2.7182818285f, 4.4816890703f, 7.3890560989f,
                                      12.182493961f, 20.085536923f, 33.115451959f, 54.598150033f};
@@ -1227,8 +1253,8 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
 
   const int64_t g0 = (int64_t)blockIdx.x * per, g1 = min(g0 + per, G);
   if (g0 >= g1) return;
-  int64_t b = g0 / es.T3;
-  int t = (int)(g0 - b * es.T3);
+  int64_t b = __builtin_amdgcn_readfirstlane((int)(g0 / es.T3));  // rows < 2^31
+  int t = __builtin_amdgcn_readfirstlane((int)(g0 - b * es.T3));
   int64_t built = -1;  // moments record whose tables are in LDS (both halves of it share them)
   int tau = 0, kt[2] = {0, 0}, D[2] = {-1, -1};
   float pv[kEsTokPer], qv[L][kEsTokPer];
@@ -1244,23 +1270,23 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
 #pragma unroll
       for (int l = 0; l < L; ++l) qc[l][i] = qv[l][i];
     }
-    const int64_t bb = b;
-    const int tt = t;
+    const int64_t bb = __builtin_amdgcn_readfirstlane((int)b);  // uniform: scalar loads below
+    const int tt = __builtin_amdgcn_readfirstlane(t);
     if (++t == es.T3) {
       t = 0;
       ++b;
     }
-    if (g + 1 < g1) es_load_eval<L>(p, q1, q2, V, b, t, tid, pv, qv);
-    __asm__ volatile("" ::: "memory");  // issued here, in flight through this tile
-    const EsPlan& pl = es.plan[bb];
+    const EsPlan pl = es_sload_rec(es.plan + bb);
     const int flags = pl.flags, fp64 = pl.fp64, k_lo = pl.k_lo, nk = pl.nk;
-    if (flags) {  // uniform
+    if (flags || fp64) {  // uniform; a row in fp64 is evaluated by the coefficient kernel
+      if (g + 1 < g1) es_load_eval<L>(p, q1, q2, V, b, t, tid, pv, qv);
+      if (flags) {
 #pragma unroll
-      for (int i = 0; i < kEsTokPer; ++i)
-        if (whole || base + i * kEsThreads + tid < V) rb[i * kEsThreads] = NAN;
+        for (int i = 0; i < kEsTokPer; ++i)
+          if (whole || base + i * kEsThreads + tid < V) rb[i * kEsThreads] = NAN;
+      }
       continue;
     }
-    if (fp64) continue;  // evaluated by the coefficient kernel
     float acc[kEsTokPer];
 #pragma unroll
     for (int i = 0; i < kEsTokPer; ++i) acc[i] = 0.0f;
@@ -1271,12 +1297,12 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
       // row without an fp64 tile has its ratios in the fp32 normal range)
       if (built >= 0) es_lds_barrier();  // every wave is done with the previous tables
       built = recno;
-      const EsTile* rec = es.tile + recno * L;
       float wmin[2], wmax[2];
 #pragma unroll
       for (int l = 0; l < L; ++l) {
-        wmin[l] = (float)rec[l].wmin;  // +inf / 0 when the law has no positive weight here
-        wmax[l] = (float)rec[l].wmax;
+        const EsTile rec = es_sload_rec(es.tile + recno * L + l);
+        wmin[l] = (float)rec.wmin;  // +inf / 0 when the law has no positive weight here
+        wmax[l] = (float)rec.wmax;
       }
       const float lo = fminf(wmin[0], wmin[L - 1]), hi = fmaxf(wmax[0], wmax[L - 1]);
       int range = 0;
@@ -1291,6 +1317,7 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         es_window_f32(wmin[l], wmax[l], kt[l], nw);
         es_window_f32(wmin[l], wmin[l], ktlo, nw);  // the last expansion node of the smallest weight
         D[l] = min(max(ktlo - kt[l], 0), kEsTabRows - 1);
+        // tables: every thread loads its entries (vector loads, all in flight at once)
         const double* ct = es.ctab + (bb * L + l) * kEsMaxWin;
         const double* pt = es.ptab + (bb * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
         for (int i = tid; i < D[l] + 1 + kEsTokNodes; i += kEsThreads) {
@@ -1310,6 +1337,10 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
       }
       es_lds_barrier();
     }
+    // the next tile's p and q: issued after the table loads, so that waiting for those
+    // never waits for these; in flight through this tile's arithmetic
+    if (g + 1 < g1) es_load_eval<L>(p, q1, q2, V, b, t, tid, pv, qv);
+    __asm__ volatile("" ::: "memory");
     if (nk > 0) {
       // (2) per token: nine exponentials and the expansion
 #pragma unroll
