@@ -251,6 +251,46 @@ def test_ragged_tiles(V):
     assert np.all(st == 0) and np.all(rel_l1(r, ro) <= TIGHT)
 
 
+def _span_rows(seed, V, spans):
+    """Rows whose positive weights span about 2^s (one row per s) with p, q and every
+    ratio fp32 normal numbers: p ~ a 2^(x/2), q ~ a 2^(-x/2), x uniform in [-s/2, s/2]."""
+    rng = np.random.default_rng(seed)
+    A = rng.dirichlet(np.full(V, 2.0), size=len(spans))
+    X = (rng.random((len(spans), V)) - 0.5) * np.asarray(spans, dtype=np.float64)[:, None]
+    P = A * np.exp2(X / 2)
+    Q = A * np.exp2(-X / 2)
+    P /= P.sum(1, keepdims=True)
+    Q /= Q.sum(1, keepdims=True)
+    return P.astype(np.float32), Q.astype(np.float32)
+
+
+def test_fp32_rows_with_wide_weight_spans():
+    # spans up to 2^150 stay in fp32 (the limit is 2^160): long moment windows, runs
+    # expanding far above their tile's expansion node, evaluation tables of up to
+    # ~200 rows, over ragged tiles (5000 = 4096 + 904; five 1024-token tiles)
+    V, spans = 5000, [40, 100, 150]
+    P, Q = _span_rows(61, V, spans)
+    w = P.astype(np.float64) / Q.astype(np.float64)
+    assert np.all(np.log2(w.max(1) / w.min(1)) > np.asarray(spans) - 2)
+    assert min(P.min(), Q.min(), w.min()) > 1.2e-38 and w.max() < 3e38
+    r, st = es_r(P, Q, 2)
+    ro, _ = oracle.induced_dist(P, Q, 2)
+    assert np.all(st == 0) and np.all(rel_l1(r, ro) <= TIGHT), rel_l1(r, ro)
+    # K = 3 on sampled entries: the largest and smallest weights of each row and random ones
+    rows = np.repeat(np.arange(len(spans)), 6)
+    ys = np.concatenate([[int(np.argmax(w[b])), int(np.argmin(w[b])), *np.random.default_rng(62 + b).integers(0, V, 4)]
+                         for b in range(len(spans))])
+    r3, st3 = es_r(P, Q, 3)
+    e3 = oracle.induced_dist_entries(P, Q, 3, rows, ys)
+    assert np.all(st3 == 0)
+    assert np.all(np.abs(r3[rows, ys] - e3) <= TIGHT * e3), np.abs(r3[rows, ys] / e3 - 1).max()
+    # two laws with different spans in one row
+    Q2 = Q[::-1].copy()
+    rp, stp = es_pair(P, Q, Q2)
+    rpo, _ = oracle.induced_dist_pair(P, Q, Q2)
+    assert np.all(stp == 0) and np.all(rel_l1(rp, rpo) <= TIGHT), rel_l1(rp, rpo)
+
+
 def test_wide_weight_range_rows_in_fp64():
     # positive weights spanning more than 2^180: the fp64 instantiation of the kernels
     rng = np.random.default_rng(44)
