@@ -385,18 +385,23 @@ __global__ __launch_bounds__(kAccThreads) void accept_kernel(
     }
     return;
   }
-  // locate the token inside super-tile st_star
+  // locate the token inside super-tile st_star (its four sub-tiles loaded at once)
   double base = prev_star;
   int32_t found = -1;
-  for (int k = 0; k < 4 && found < 0; ++k) {
+  float pvs[4][4], rvs[4][4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
     const int64_t x0 = st_star * kSuper + 256 * k + 4 * lane;
-    float pv[4], rv[4];
-    load4<kVec>(pb, x0, V, pv);
-    load4<kVec>(rb, x0, V, rv);
+    load4<kVec>(pb, x0, V, pvs[k]);
+    load4<kVec>(rb, x0, V, rvs[k]);
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (found >= 0) break;  // uniform
     double rs[4], local = 0.0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      rs[i] = residual_of(pv[i], rv[i]);
+      rs[i] = residual_of(pvs[k][i], rvs[k][i]);
       local += rs[i];
     }
     const double li = wave_inclusive_scan(local, lane);
@@ -421,14 +426,12 @@ __global__ __launch_bounds__(kAccThreads) void accept_kernel(
   if (found < 0) {
     // fallback: last token of the super-tile with positive residual
     int64_t last = -1;
+#pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int64_t x0 = st_star * kSuper + 256 * k + 4 * lane;
-      float pv[4], rv[4];
-      load4<kVec>(pb, x0, V, pv);
-      load4<kVec>(rb, x0, V, rv);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if (x0 + i < V && residual_of(pv[i], rv[i]) > 0.0) last = x0 + i;
+        if (x0 + i < V && residual_of(pvs[k][i], rvs[k][i]) > 0.0) last = x0 + i;
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
