@@ -209,6 +209,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llm32k")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline leg")
+    ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of graph replays")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample size (0: one per core, 2 rounds)")
     ap.add_argument("--resample-reps", type=int, default=20)
     ap.add_argument("--tlp-tail", choices=["sorted", "half"], default=None,
@@ -348,6 +349,7 @@ def main():
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
+    # r alone: HIP events around the induced-distribution call of eager steps
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -357,6 +359,41 @@ def main():
     wall = time.perf_counter() - t0
     r_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
     ms_per_step = wall * 1e3 / args.steps
+    timing = "eager launches, HIP events around r in every step"
+    if not args.no_graph:
+        # the whole step: one HIP graph of its kernels (status clear, r, selection,
+        # accept/resample), replayed K times; no host launch work or timing markers
+        # between the kernels.  Every replay is checked against the eager step first.
+        ref_out, ref_acc = out.clone(), acc.clone()
+        ref_r = (r_stages if cfg.successive else r).clone()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            one_step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            g_out, g_acc = one_step()
+        for rep in range(3):
+            graph.replay()
+            torch.cuda.synchronize()
+            same = (torch.equal(g_out, ref_out) and torch.equal(g_acc, ref_acc) and
+                    torch.equal(r_stages if cfg.successive else r, ref_r) and int(status.abs().sum()) == 0)
+            assert same, f"graph replay {rep} differs from the eager step"
+            one_step()  # eager work between the replays
+            torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms_per_step = wall * 1e3 / args.steps
+        out, acc = g_out, g_acc
+        timing = "one HIP graph per step (replays checked against the eager step); r by HIP events on eager steps"
     assert int(status.abs().sum()) == 0, "rows flagged during the bench"
     if cfg.diag:
         pstar_t, achieved_t = out, acc
@@ -519,6 +556,7 @@ def main():
         "roofline": roofline,
         "roofline_resample": roofline_resample,
         "method": "exponential-sum quadrature" if use_es else "exact pairwise sums",
+        "timing": timing,
         "exact_pairwise": exact_pairwise,
         "cpu_baseline": None,
         "kernel_source_digest": digest,
