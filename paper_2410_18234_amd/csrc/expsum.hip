@@ -349,9 +349,10 @@ __device__ __forceinline__ float es_uniform_max(float x) {
 }
 
 // ------------------------------------------------------------------ moments
-// Statistics and moments of one tile of one law.  The fp32 instantiation
-// leaves a tile with an out-of-range ratio or a weight span above 2^160 to the
-// fp64 one (record.wide = 1).
+// The fp64 path: statistics and moments of one tile of one law that the fp32
+// kernel left aside (a ratio outside the fp32 normal range or a weight span above
+// 2^160), taken by the coefficient kernel; the same record layout, tile windows
+// on a compacted token list (no sort).
 template <int NB, typename Real>
 __device__ __forceinline__ void es_moments_block(const Real* __restrict__ s_w, const float* __restrict__ s_q,
                                                  const Real* __restrict__ s_rate, int M, int nb, int tid, int lane,
@@ -369,19 +370,14 @@ __device__ __forceinline__ void es_moments_block(const Real* __restrict__ s_w, c
 #pragma unroll
     for (int i = 0; i < NB; ++i) acc[i] = es_fma(qq, es_decay(rt[i], w), acc[i]);
   }
-  if constexpr (sizeof(Real) == 4) {
-    const Real tot = wave_reduce_scatter_f32<NB>(acc, lane);
-    if (es_scatter_writer<NB>(lane)) s_red[wid][nb + es_scatter_node<NB>(lane)] = tot;
-  } else {
-    const Real tot = wave_reduce_scatter<NB, Real>(acc, lane);
-    if ((lane & (64 / NB - 1)) == 0) s_red[wid][nb + lane / (64 / NB)] = tot;
-  }
+  const Real tot = wave_reduce_scatter<NB, Real>(acc, lane);
+  if ((lane & (64 / NB - 1)) == 0) s_red[wid][nb + lane / (64 / NB)] = tot;
 }
 
 template <typename Real>
 __device__ void es_moments_tile(const float* __restrict__ pb, const float* __restrict__ qb, int64_t V, int64_t t,
                                 EsTile* __restrict__ rec, double* __restrict__ part) {
-  constexpr bool f64 = sizeof(Real) == 8;
+  static_assert(sizeof(Real) == 8, "the fp64 path");
   __shared__ Real s_w[kEsMomTile];
   __shared__ float s_q[kEsMomTile];
   __shared__ Real s_red[kEsWaves][kEsMaxWin];
@@ -389,7 +385,7 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
   __shared__ Real s_tay[kEsWaves][kEsTaylor];
   __shared__ int s_wave[kEsWaves];
   __shared__ double s_d[kEsWaves][4];
-  __shared__ int s_i[kEsWaves][3];
+  __shared__ int s_i[kEsWaves][2];
   __shared__ int s_dec[4];  // ka, nw, tau, proceed
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int64_t base = t * kEsMomTile;
@@ -399,7 +395,7 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
   float qv[kEsMomPer];
   Real wlo = (Real)INFINITY, whi = (Real)0;
   float q0f = 0.0f;
-  int npos = 0, bad = 0, odd = 0;
+  int npos = 0, bad = 0;
 #pragma unroll
   for (int i = 0; i < kEsMomPer; ++i) {
     const int64_t x = base + i * kEsThreads + tid;
@@ -408,7 +404,6 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     bad |= (int)bad_prob(pp) | (int)bad_prob(qq);
     pos[i] = pp > 0.0f && qq > 0.0f;
     const Real w = pos[i] ? es_ratio<Real>(pp, qq) : (Real)0;
-    if (!f64 && pos[i]) odd |= !((float)w >= FLT_MIN && (float)w <= FLT_MAX);
     wv[i] = w;
     qv[i] = qq;
     wlo = pos[i] ? fmin(wlo, w) : wlo;
@@ -420,7 +415,6 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
   const double q0 = wave_sum((double)q0f);
   npos = wave_sum_int(npos);
   bad = wave_sum_int(bad);
-  odd = wave_sum_int(odd);
   if (lane == 0) {
     s_d[wid][0] = wmin_w;
     s_d[wid][1] = wmax_w;
@@ -428,7 +422,6 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     s_d[wid][3] = 0.0;
     s_i[wid][0] = npos;
     s_i[wid][1] = bad;
-    s_i[wid][2] = odd;
   }
   __syncthreads();
   if (tid == 0) {
@@ -438,12 +431,11 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
       wmax = fmax(wmax, s_d[i][1]);
     }
     double a = 0.0;
-    int n = 0, bd = 0, od = 0;
+    int n = 0, bd = 0;
     for (int i = 0; i < kEsWaves; ++i) {
       a += s_d[i][2];
       n += s_i[i][0];
       bd |= s_i[i][1];
-      od |= s_i[i][2];
     }
     EsTile o;
     o.wmin = wmin;
@@ -454,25 +446,14 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     o.bad = bd != 0;
     o.kt = 0;
     o.nw = 0;
-    o.wide = f64 ? 1 : 0;
+    o.wide = 1;
     o.pad[0] = o.pad[1] = o.pad[2] = 0;
-    int tau = 0, range = 0;
-    if (n > 0) {
-      if (f64 || od) {
-        es_scale(wmin, wmax, tau, range);
-        if (!f64) o.wide = 1;
-        es_window(wmin, wmax, o.kt, o.nw);
-      } else {
-        es_scale_f32((float)wmin, (float)wmax, tau, range);
-        if (range > kEsWideRange) o.wide = 1;
-        es_window_f32((float)wmin, (float)wmax, o.kt, o.nw);
-      }
-    }
+    if (n > 0) es_window(wmin, wmax, o.kt, o.nw);
     *rec = o;
     s_dec[0] = o.kt;
     s_dec[1] = o.nw;
-    s_dec[2] = f64 ? 0 : tau;
-    s_dec[3] = (!o.bad && n > 0 && (f64 || !o.wide)) ? 1 : 0;
+    s_dec[2] = 0;  // no scaling in fp64
+    s_dec[3] = (!o.bad && n > 0) ? 1 : 0;
   }
   __syncthreads();
   if (!s_dec[3]) return;
@@ -486,7 +467,7 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
 #pragma unroll
   for (int i = 0; i < kEsMomPer; ++i) {
     if (pos[i]) {
-      s_w[off] = f64 ? wv[i] : (Real)ldexpf((float)wv[i], tau);
+      s_w[off] = wv[i];
       s_q[off] = qv[i];
       ++off;
     }
@@ -512,13 +493,8 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
         pw *= u;
       }
     }
-    if constexpr (sizeof(Real) == 4) {
-      const Real tot = wave_reduce_scatter_f32<kEsTaylor>(T, lane);
-      if (es_scatter_writer<kEsTaylor>(lane)) s_tay[wid][es_scatter_node<kEsTaylor>(lane)] = tot;
-    } else {
-      const Real tot = wave_reduce_scatter<kEsTaylor, Real>(T, lane);
-      if ((lane & (64 / kEsTaylor - 1)) == 0) s_tay[wid][lane / (64 / kEsTaylor)] = tot;
-    }
+    const Real tot = wave_reduce_scatter<kEsTaylor, Real>(T, lane);
+    if ((lane & (64 / kEsTaylor - 1)) == 0) s_tay[wid][lane / (64 / kEsTaylor)] = tot;
   }
   int nb = 0;
   for (; nb + 16 <= nw; nb += 16) es_moments_block<16, Real>(s_w, s_q, s_rate, M, nb, tid, lane, wid, s_red);
@@ -957,18 +933,16 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
   }
 }
 
-// ------------------------------------------------------------------ evaluation
-// One evaluation tile (2048 tokens) of a row: r(y) = p(y) [P + sum over the
-// window of c_k exp(-a_k w(y))] + the zero-weight closed forms, P = the sum of
-// c_k below the window.  The fp32 instantiation runs only on rows without an
-// fp64 tile: such a row has every ratio in the fp32 normal range and (two laws)
-// a weight span within 2^160, so every evaluation tile of it does too (an
-// evaluation tile lies inside one moments tile of each law).
+// ------------------------------------------------------------------ evaluation (fp64)
+// The fp64 path: one evaluation tile (2048 tokens) of a row with an fp64 tile,
+// run by the coefficient kernel: r(y) = p(y) [P + sum over the tile's window of
+// c_k exp(-a_k w(y))] + the zero-weight closed forms, P the expansion of the
+// grid nodes below the window.
 template <typename Real, int L>
 __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restrict__ q1b,
                              const float* __restrict__ q2b, int64_t V, int K, int64_t t, float* __restrict__ rb,
                              const EsPlan& pl, const double* __restrict__ ctab) {
-  constexpr bool f64 = sizeof(Real) == 8;
+  static_assert(sizeof(Real) == 8, "the fp64 path");
   __shared__ Real s_w[kEsEvalTile];
   __shared__ uint16_t s_pos[kEsEvalTile];
   __shared__ Real s_acc[kEsEvalTile];
@@ -981,11 +955,9 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
   double* const s_cf = reinterpret_cast<double*>(s_tab);
   __shared__ int s_wave[kEsWaves];
   __shared__ double s_d[kEsWaves][2][2];
-  __shared__ int s_i[kEsWaves];
   __shared__ int s_dec[2][3];  // per law: first row node of the window, window length, last expansion node
   __shared__ Real s_poly[kEsTaylor];
   __shared__ Real s_akt;
-  __shared__ int s_tau, s_go;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int64_t base = t * kEsEvalTile;
 
@@ -1001,7 +973,6 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
   }
   if (pl.nk > 0) {
     double wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0, 0.0};
-    int odd = 0;
 #pragma unroll
     for (int l = 0; l < L; ++l) {
       Real lo = (Real)INFINITY, hi = (Real)0;
@@ -1009,7 +980,6 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
       for (int i = 0; i < kEsEvalPer; ++i) {
         pos[l][i] = pv[i] > 0.0f && qv[l][i] > 0.0f;
         const Real w = pos[l][i] ? es_ratio<Real>(pv[i], qv[l][i]) : (Real)0;
-        if (!f64 && pos[l][i]) odd |= !((float)w >= FLT_MIN && (float)w <= FLT_MAX);
         wv[l][i] = w;
         lo = pos[l][i] ? fmin(lo, w) : lo;
         hi = pos[l][i] ? fmax(hi, w) : hi;
@@ -1017,44 +987,25 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
       wmin[l] = (double)es_wave_min(lo);
       wmax[l] = (double)es_wave_max(hi);
     }
-    odd = wave_sum_int(odd);
     if (lane == 0) {
       for (int l = 0; l < L; ++l) {
         s_d[wid][l][0] = wmin[l];
         s_d[wid][l][1] = wmax[l];
       }
-      s_i[wid] = odd;
     }
     __syncthreads();
     if (tid == 0) {
-      int od = 0;
-      for (int i = 0; i < kEsWaves; ++i) od |= s_i[i];
-      double lo = INFINITY, hi = 0.0;
       for (int l = 0; l < L; ++l) {
         for (int i = 0; i < kEsWaves; ++i) {
           wmin[l] = fmin(wmin[l], s_d[i][l][0]);
           wmax[l] = fmax(wmax[l], s_d[i][l][1]);
         }
-        lo = fmin(lo, wmin[l]);
-        hi = fmax(hi, wmax[l]);
       }
-      int tau = 0, range = 0;
-      if (hi > 0.0) {
-        if (f64 || od)
-          es_scale(lo, hi, tau, range);
-        else
-          es_scale_f32((float)lo, (float)hi, tau, range);
-      }
-      s_go = f64 || !(od || range > kEsWideRange);  // the fp32 path never sees a wide tile (see above)
-      s_tau = f64 ? 0 : tau;
       for (int l = 0; l < L; ++l) {
         int i0 = pl.nk, cnt = 0, kt = pl.k_lo + pl.nk;
         if (wmax[l] > 0.0) {
           int nw;
-          if (f64)
-            es_window(wmin[l], wmax[l], kt, nw);
-          else
-            es_window_f32((float)wmin[l], (float)wmax[l], kt, nw);
+          es_window(wmin[l], wmax[l], kt, nw);
           i0 = std::min(std::max(kt + 1 - pl.k_lo, 0), pl.nk);
           const int i1 = std::min(kt + nw - pl.k_lo, pl.nk - 1);
           cnt = std::max(0, i1 - i0 + 1);
@@ -1065,16 +1016,8 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
       }
     }
     __syncthreads();
-    if (!s_go) {
-#pragma unroll
-      for (int i = 0; i < kEsEvalPer; ++i) {
-        const int64_t x = base + i * kEsThreads + tid;
-        if (x < V) rb[x] = NAN;
-      }
-      return false;
-    }
   }
-  const int tau = (pl.nk > 0) ? s_tau : 0;
+  constexpr int tau = 0;  // no scaling in fp64
 #pragma unroll
   for (int i = 0; i < kEsEvalPer; ++i) s_acc[i * kEsThreads + tid] = (Real)0;
   if (pl.nk > 0) {
@@ -1106,7 +1049,7 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
 #pragma unroll
       for (int i = 0; i < kEsEvalPer; ++i) {
         if (pos[l][i]) {
-          s_w[off] = f64 ? wv[l][i] : (Real)ldexpf((float)wv[l][i], tau);
+          s_w[off] = wv[l][i];
           s_pos[off] = (uint16_t)(i * kEsThreads + tid);
           ++off;
         }
@@ -1173,7 +1116,7 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
     if (x >= V) break;
     const float pp = pv[i];
     const Real acc = s_acc[i * kEsThreads + tid];
-    const float quad = f64 ? (float)ldexp((double)pp * (double)acc, tau) : ldexpf(pp * (float)acc, tau);
+    const float quad = (float)((double)pp * (double)acc);
     float v = 0.0f;
     if (L == 1) {
       const float qq = qv[0][i];
@@ -1245,7 +1188,7 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
   __shared__ float s_c[L][kEsTabRows + kEsTokNodes];    // c_(kt+1+i) 2^-tau (0 off the grid)
   __shared__ float s_p[L][kEsTabRows * kEsPolyStride];  // B_j(kt + d) 2^-tau / j!
   __shared__ float s_r[L][kEsTabRows];                  // log2(e) a_(kt+1+d) 2^-tau
-  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tid = threadIdx.x;
   // e^(i h) for the nine nodes of a token, and e^(-h) / log2(e) (from log2(e) a_k0 w to a_(k0-1) w)
   constexpr float kE[kEsTokNodes] = {1.0f,          1.6487212707f, 2.7182818285f, 4.4816890703f, 7.3890560989f,
                                      12.182493961f, 20.085536923f, 33.115451959f, 54.598150033f};
