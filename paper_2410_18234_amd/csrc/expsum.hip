@@ -31,13 +31,14 @@
 // denominator D >= w_x loses at most the part of its pair (or tuple) integral
 // over a > Z / w_x, which relative to 1/D is at most e^(-Z D / w_x) (1 + h Z D / w_x)
 // <= e^(-Z) (1 + h Z) = 3.3e-9 on the grid (the integrand is decreasing there),
-// once on the moment side and once on the query side.  So each group of tokens
-// needs exponentials only on the window of nodes between those limits, and a
-// group of tokens with nearby weights has a short window: the moments sort each
-// tile's tokens by binary exponent and give every run of consecutive sorted
-// tokens its own window.  Moments need no row-wide information, so they run
-// first; one workgroup per row then merges the tiles, fixes the row's grid
-// range and coefficients; evaluation follows.
+// once on the moment side and once on the query side.  So a token needs
+// exponentials only on the nodes with a_k w in (1/4, 22]: nine of them.  The
+// evaluation gives every query token exactly those nine (its expansion of the
+// grid below comes from a prefix table); the moments, a sum over tokens per
+// node, give each run of 512 tokens of nearby weights (after a per-thread sort)
+// the union of its tokens' windows.  Moments need no row-wide information, so
+// they run first; one workgroup per row then merges the tiles, fixes the row's
+// grid range, coefficients and prefix table; evaluation follows.
 //
 // Precision: each tile scales its weights by a power of two (w' = w 2^tau, the
 // node rates by 2^-tau) and evaluates in fp32; a tile whose weight ratios leave
