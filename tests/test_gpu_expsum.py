@@ -4,7 +4,7 @@ C ABI, against the fp64 oracle's enumeration of the drafted tuples.
 
 Bars as for the pairwise path: r within 1e-5 relative L1 per row, sampled
 entries within 1e-5 relative each, selection bit-exact, Algorithm 1's
-invariants on the GPU's own r.  The quadrature's own error bound is 7e-8
+invariants on the GPU's own r.  The quadrature's own error bound is 8e-8
 relative per entry, so the bars are met with two orders of magnitude to spare;
 the tests also hold the error under 2e-6 per row to catch a node-range or
 scale mistake that would still pass 1e-5 on some rows.  Notation: p = target,
