@@ -1310,15 +1310,19 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         }
 #pragma unroll
         for (int i = 0; i < kEsTokPer; ++i) {
-          float s = 0.0f;
+          // three interleaved partial sums over the nine nodes and the expansion in
+          // Estrin's form: short dependency chains (the kernel is latency-bound)
+          float s3[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
-          for (int m = 0; m < kEsTokNodes; ++m) s = fmaf(sc[d[i] + m], __builtin_amdgcn_exp2f(-x[i] * kE[m]), s);
+          for (int m = 0; m < kEsTokNodes; ++m)
+            s3[m % 3] = fmaf(sc[d[i] + m], __builtin_amdgcn_exp2f(-x[i] * kE[m]), s3[m % 3]);
           const float nu = -x[i] * kBack;  // -a_(k0-1) w
           const float* pr = sp + (d[i] << 3) + d[i];
-          float pe = pr[kEsTaylor - 1];
-#pragma unroll
-          for (int j = kEsTaylor - 2; j >= 0; --j) pe = fmaf(pe, nu, pr[j]);
-          acc[i] += ok[i] ? s + pe : 0.0f;
+          const float nu2 = nu * nu, nu4 = nu2 * nu2;
+          const float e01 = fmaf(pr[1], nu, pr[0]), e23 = fmaf(pr[3], nu, pr[2]);
+          const float e45 = fmaf(pr[5], nu, pr[4]), e67 = fmaf(pr[7], nu, pr[6]);
+          const float pe = fmaf(fmaf(e67, nu2, e45), nu4, fmaf(e23, nu2, e01));
+          acc[i] += ok[i] ? (s3[0] + s3[1]) + (s3[2] + pe) : 0.0f;
         }
       }
     }
