@@ -786,7 +786,7 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
   __shared__ float s_rate[kEsWin32 + 5];  // log2(e) a_k 2^-tau for the nodes kt .. kt + nw + 4
   __shared__ float s_f[2][kEsWaves][2];  // by tile parity: the tile may be skipped without another barrier
   __shared__ double s_q0[2][kEsWaves];
-  __shared__ int s_i[2][kEsWaves][3];
+  __shared__ int s_i[2][kEsWaves][2];
   const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   float pv[kEsMomPer], qv[kEsMomPer];
@@ -806,43 +806,46 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
       }
     }
     // (1) ratios and statistics
-    bool pos[kEsMomPer];
-    float wv[kEsMomPer];
-    float wlo = INFINITY, whi = 0.0f, q0f = 0.0f;
-    int npos = 0, bad = 0, odd = 0;
+    float wv[kEsMomPer];  // 0 for a token left out
+    float wlo = INFINITY, whi = 0.0f;
+    bool anybad = false, anyzero = false;
+    int npos = 0;
 #pragma unroll
     for (int i = 0; i < kEsMomPer; ++i) {
       const float pp = pv[i], qq = qv[i];
       // NaN, -inf, negative normal or denormal, +inf (-0 is a zero probability)
-      bad |= (int)__builtin_amdgcn_class(pp, 0x21F) | (int)__builtin_amdgcn_class(qq, 0x21F);
-      pos[i] = pp > 0.0f && qq > 0.0f;
-      const float w = pos[i] ? es_ratio<float>(pp, qq) : 0.0f;
-      if (pos[i]) odd |= !__builtin_amdgcn_class(w, 0x100);  // not a positive normal
+      anybad |= __builtin_amdgcn_classf(pp, 0x21F) | __builtin_amdgcn_classf(qq, 0x21F);
+      const bool pos = pp > 0.0f && qq > 0.0f;
+      anyzero |= qq > 0.0f && pp == 0.0f;
+      const float w = pos ? es_ratio<float>(pp, qq) : 0.0f;
       wv[i] = w;
-      wlo = pos[i] ? fminf(wlo, w) : wlo;
-      whi = pos[i] ? fmaxf(whi, w) : whi;
-      npos += pos[i];
-      q0f += (qq > 0.0f && pp == 0.0f) ? qq : 0.0f;
+      wlo = fminf(wlo, pos ? w : INFINITY);
+      whi = fmaxf(whi, w);  // w >= 0
+      npos += pos;
     }
     wlo = es_wave_ext<false>(wlo);
     whi = es_wave_ext<true>(whi);
-    const double q0w = wave_sum((double)q0f);
     npos = wave_sum_int(npos);
-    bad = wave_sum_int(bad);
-    odd = wave_sum_int(odd);
+    const bool bad = __builtin_amdgcn_ballot_w64(anybad) != 0;
+    double q0w = 0.0;  // the draft mass on zero-weight tokens (p = 0 < q), in waves that hold one
+    if (__builtin_amdgcn_ballot_w64(anyzero) != 0) {
+      float q0f = 0.0f;
+#pragma unroll
+      for (int i = 0; i < kEsMomPer; ++i) q0f += (qv[i] > 0.0f && pv[i] == 0.0f) ? qv[i] : 0.0f;
+      q0w = wave_sum((double)q0f);
+    }
     if (lane == 0) {
       s_f[par][wid][0] = wlo;
       s_f[par][wid][1] = whi;
       s_q0[par][wid] = q0w;
       s_i[par][wid][0] = npos;
       s_i[par][wid][1] = bad;
-      s_i[par][wid][2] = odd;
     }
     es_lds_barrier();
     // every thread combines the same values in the same order
     float wmin = s_f[par][0][0], wmax = s_f[par][0][1];
     double q0 = s_q0[par][0];
-    int n = s_i[par][0][0], bd = s_i[par][0][1], od = s_i[par][0][2];
+    int n = s_i[par][0][0], bd = s_i[par][0][1];
 #pragma unroll
     for (int i = 1; i < kEsWaves; ++i) {
       wmin = fminf(wmin, s_f[par][i][0]);
@@ -850,11 +853,10 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
       q0 += s_q0[par][i];
       n += s_i[par][i][0];
       bd |= s_i[par][i][1];
-      od |= s_i[par][i][2];
     }
     int kt = 0, nw = 0, tau = 0, wide = 0;
     if (n > 0) {
-      if (od) {
+      if (!(wmin >= __FLT_MIN__) || !(wmax <= __FLT_MAX__)) {  // a weight that is not an fp32 normal
         wide = 1;
       } else {
         int range;
@@ -890,12 +892,15 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
     // last four, then the slot; tokens left out last) and the tile is laid out
     // rank by rank: LDS row i holds every thread's i-th smallest weight, so a run
     // (two rows) holds weights of nearby quantiles
+    // here a token is in the sum exactly when its weight is positive (a weight that
+    // is not an fp32 normal made the tile wide)
     uint32_t key[kEsMomPer];
 #pragma unroll
     for (int i = 0; i < kEsMomPer; ++i) {
-      key[i] = (pos[i] ? (__float_as_uint(wv[i]) & ~15u) : ~15u) | (uint32_t)i;
-      s_w[i * kEsThreads + tid] = pos[i] ? ldexpf(wv[i], tau) : 0.0f;  // this thread's column only
-      s_q[i * kEsThreads + tid] = pos[i] ? qv[i] : 0.0f;
+      const bool pos = wv[i] > 0.0f;
+      key[i] = (pos ? (__float_as_uint(wv[i]) & ~15u) : ~15u) | (uint32_t)i;
+      s_w[i * kEsThreads + tid] = ldexpf(wv[i], tau);  // this thread's column only
+      s_q[i * kEsThreads + tid] = pos ? qv[i] : 0.0f;
     }
     es_lane_sort<kEsMomPer>(key);
     {

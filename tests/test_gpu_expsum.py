@@ -313,6 +313,31 @@ def test_wide_weight_range_rows_in_fp64():
     assert np.all(st == 0) and np.all(rel_l1(r, ro) <= TIGHT)
 
 
+def test_denormal_weights_in_a_narrow_span():
+    # target entries below the fp32 normal range against a normal draft: the weights
+    # are fp32 denormals although the row spans only about 2^140, so the tile is taken
+    # in fp64 because of the denormals themselves, not because of its span
+    rng = np.random.default_rng(45)
+    V = 3000
+    P = rng.dirichlet(np.ones(V), size=3)
+    Q = rng.uniform(0.5, 1.5, size=(3, V))
+    Q /= Q.sum(1, keepdims=True)
+    P[:, :3] = 1e-42
+    P[1, 3:6] = 1e-44
+    P, Q = P.astype(np.float32), Q.astype(np.float32)
+    w32 = P / Q
+    assert np.all((w32[:, :3] > 0) & (w32[:, :3] < np.finfo(np.float32).tiny))
+    w = P.astype(np.float64) / Q
+    assert max(np.log2(wb.max() / wb[wb > 0].min()) for wb in w) < 160
+    for K in (2, 3):
+        r, st = es_r(P, Q, K)
+        ro, _ = oracle.induced_dist(P, Q, K)
+        assert np.all(st == 0)
+        assert np.all(rel_l1(r, ro) <= TIGHT), (K, rel_l1(r, ro))
+        big = ro >= 1e-30  # outputs in the fp32 normal range, per entry
+        assert np.all(np.abs(r[big] - ro[big]) <= TIGHT * ro[big]), (K, np.abs(r[big] / ro[big] - 1).max())
+
+
 def test_range_flag_and_bad_rows():
     rng = np.random.default_rng(3)
     V = 16
