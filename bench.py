@@ -336,6 +336,13 @@ def main():
         induced()
         if ev is not None:
             ev[1].record()
+        if not (tlp_s or cfg.successive):
+            # selection and Algorithm 1 in one launch
+            if cfg.pair:
+                _, _, out, acc, _, _ = mdss.select_accept_pair(p, q, q2, r, drafts, u, row_status=status)
+            else:
+                _, _, out, acc, _, _ = mdss.select_accept(p, q, r, drafts, u, row_status=status)
+            return out, acc
         _, sel_token = select()
         out, acc, _, _ = mdss.accept_or_resample(p, r, sel_token, u, row_status=status)
         return out, acc

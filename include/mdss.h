@@ -133,6 +133,21 @@ mdss_status mdss_accept_or_resample(const float* p, const float* r, const int32_
                                     uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
                                     void* stream);
 
+/* Selection and single-draft speculative sampling in one launch (Theorem 1:
+ * select the intermediate token, then run Algorithm 1 against r).  Outputs,
+ * row flags and every written value are those of mdss_select_intermediate
+ * followed by mdss_accept_or_resample with the same p, q, drafts, u, seed and
+ * offset (the selected token is passed on inside the launch); sel_index and
+ * sel_token ([B] int32) are nullable here.  r is the proposal of the selected
+ * token ([B][V] fp32, e.g. from mdss_induced_dist_expsum).  K in
+ * [2, MDSS_MAX_K].  The draft values p(x_i), q(x_i), r(x_i) are read
+ * together, so the accept test waits for one round of loads after the
+ * drafts. */
+mdss_status mdss_select_accept(const float* p, const float* q, const float* r, const int32_t* drafts,
+                               const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
+                               int32_t* sel_index, int32_t* sel_token, int32_t* out_token, uint8_t* accepted,
+                               float* residual, double* residual_mass, int32_t* row_status, void* stream);
+
 /* ---- Two drafts from different distributions (K = 2) --------------------
  * Remark 1 (and the non-identical K = 2 appendix): X1 ~ q1 and X2 ~ q2
  * independently.  The classical weight of draft i is w_i(x) = p(x)/q_i(x),
@@ -156,6 +171,14 @@ mdss_status mdss_select_intermediate_pair(const float* p, const float* q1, const
                                           const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
                                           int32_t* sel_index, int32_t* sel_token, int32_t* row_status,
                                           void* stream);
+
+/* mdss_select_intermediate_pair followed by mdss_accept_or_resample in one
+ * launch, as mdss_select_accept is for identical drafts (drafts [B][2]). */
+mdss_status mdss_select_accept_pair(const float* p, const float* q1, const float* q2, const float* r,
+                                    const int32_t* drafts, const float* u, uint64_t seed, uint64_t offset,
+                                    int64_t B, int64_t V, int32_t* sel_index, int32_t* sel_token,
+                                    int32_t* out_token, uint8_t* accepted, float* residual, double* residual_mass,
+                                    int32_t* row_status, void* stream);
 
 /* ---- Successive pairwise selection (K >= 2) -------------------------------
  * Remark 4: K drafts X1..XK i.i.d. from q are reduced two at a time.  Stage 1

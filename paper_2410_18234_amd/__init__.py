@@ -37,6 +37,8 @@ from .binding import (  # noqa: F401
     load_library,
     optimal_acceptance,
     select_intermediate,
+    select_accept,
+    select_accept_pair,
     select_intermediate_pair,
     select_successive,
     select_truncated_lp,

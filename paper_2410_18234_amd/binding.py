@@ -63,6 +63,8 @@ def load_library():
         lib.mdss_induced_dist.argtypes = [P, P, i64, i64, i32, i32, P, P, P, sz, P]
         lib.mdss_select_intermediate.argtypes = [P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P]
         lib.mdss_accept_or_resample.argtypes = [P, P, P, P, u64, u64, i64, i64, P, P, P, P, P, P]
+        lib.mdss_select_accept.argtypes = [P, P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P, P, P, P, P]
+        lib.mdss_select_accept_pair.argtypes = [P, P, P, P, P, P, u64, u64, i64, i64, P, P, P, P, P, P, P, P]
         lib.mdss_workspace_bytes_pair.argtypes = [i64, i64]
         lib.mdss_workspace_bytes_pair.restype = sz
         lib.mdss_induced_dist_pair.argtypes = [P, P, P, i64, i64, P, P, P, sz, P]
@@ -94,7 +96,8 @@ def load_library():
                   "mdss_acceptance", "mdss_induced_dist_expsum", "mdss_induced_dist_pair_expsum",
                   "mdss_induced_dist_successive_expsum"):
             getattr(lib, f).restype = ctypes.c_int
-        for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample",
+        for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample", "mdss_select_accept",
+                  "mdss_select_accept_pair",
                   "mdss_induced_dist_pair", "mdss_select_intermediate_pair", "mdss_truncated_lp",
                   "mdss_select_truncated_lp"):
             getattr(lib, f).restype = ctypes.c_int
@@ -224,6 +227,58 @@ def accept_or_resample(p: torch.Tensor, r: torch.Tensor, sel_token: torch.Tensor
     return out, acc, res, mass
 
 
+def _select_accept(fn: str, p: torch.Tensor, qs: tuple, r: torch.Tensor, drafts: torch.Tensor,
+                   u: Optional[torch.Tensor], seed: int, offset: int, want_residual: bool, want_mass: bool,
+                   row_status: Optional[torch.Tensor]):
+    lib = load_library()
+    B, V, dev = _pq(p, r)
+    for i, qi in enumerate(qs):
+        _need(qi, f"q{i + 1}" if len(qs) > 1 else "q", torch.float32, (B, V), dev)
+    if drafts.dim() != 2:
+        raise ValueError("drafts must be [B][K]")
+    K = drafts.shape[1]
+    _need(drafts, "drafts", torch.int32, (B, K), dev)
+    if len(qs) == 2 and K != 2:
+        raise ValueError("two draft distributions take drafts [B][2]")
+    if u is not None:
+        _need(u, "u", torch.float32, (B, 3), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    sel_index = torch.empty(B, dtype=torch.int32, device=dev)
+    sel_token = torch.empty(B, dtype=torch.int32, device=dev)
+    out = torch.empty(B, dtype=torch.int32, device=dev)
+    acc = torch.empty(B, dtype=torch.uint8, device=dev)
+    res = torch.empty((B, V), dtype=torch.float32, device=dev) if want_residual else None
+    mass = torch.empty(B, dtype=torch.float64, device=dev) if want_mass else None
+    tail = (_ptr(sel_index), _ptr(sel_token), _ptr(out), _ptr(acc), _ptr(res), _ptr(mass), _ptr(row_status),
+            _stream(dev))
+    if len(qs) == 1:
+        code = lib.mdss_select_accept(_ptr(p), _ptr(qs[0]), _ptr(r), _ptr(drafts), _ptr(u), ctypes.c_uint64(seed),
+                                      ctypes.c_uint64(offset), B, V, K, *tail)
+    else:
+        code = lib.mdss_select_accept_pair(_ptr(p), _ptr(qs[0]), _ptr(qs[1]), _ptr(r), _ptr(drafts), _ptr(u),
+                                           ctypes.c_uint64(seed), ctypes.c_uint64(offset), B, V, *tail)
+    _check(fn, code)
+    return sel_index, sel_token, out, acc, res, mass
+
+
+def select_accept(p: torch.Tensor, q: torch.Tensor, r: torch.Tensor, drafts: torch.Tensor,
+                  u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False,
+                  want_mass: bool = False, row_status: Optional[torch.Tensor] = None):
+    """(sel_index, sel_token, out_token, accepted, residual or None, residual_mass or None):
+    select_intermediate and accept_or_resample in one launch."""
+    return _select_accept("mdss_select_accept", p, (q,), r, drafts, u, seed, offset, want_residual, want_mass,
+                          row_status)
+
+
+def select_accept_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, r: torch.Tensor, drafts: torch.Tensor,
+                       u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False,
+                       want_mass: bool = False, row_status: Optional[torch.Tensor] = None):
+    """select_intermediate_pair and accept_or_resample in one launch (drafts [B][2])."""
+    return _select_accept("mdss_select_accept_pair", p, (q1, q2), r, drafts, u, seed, offset, want_residual,
+                          want_mass, row_status)
+
+
 def workspace_bytes_pair(B: int, V: int) -> int:
     return int(load_library().mdss_workspace_bytes_pair(B, V))
 
@@ -286,16 +341,16 @@ def step_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, drafts: torch
         r = induced_dist_pair(p, q1, q2, row_status=status)
     else:
         raise ValueError(f"method must be 'exact' or 'expsum', got {method!r}")
-    sel_index, sel_token = select_intermediate_pair(p, q1, q2, drafts, u, seed, offset, row_status=status)
-    out, acc, res, mass = accept_or_resample(p, r, sel_token, u, seed, offset, want_residual=want_residual,
-                                             want_mass=want_residual, row_status=status)
+    sel_index, sel_token, out, acc, res, mass = select_accept_pair(p, q1, q2, r, drafts, u, seed, offset,
+                                                                   want_residual=want_residual,
+                                                                   want_mass=want_residual, row_status=status)
     return {"r": r, "sel_index": sel_index, "sel_token": sel_token, "out_token": out, "accepted": acc,
             "residual": res, "mass": mass, "status": status}
 
 
 def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[torch.Tensor] = None, seed: int = 0,
          offset: int = 0, s_max: int = 0, want_residual: bool = False, method: str = "exact"):
-    """The whole path for one batch: r, selection, accept / resample (three calls on one stream).
+    """The whole path for one batch: r, then selection with accept / resample (two calls on one stream).
     method "exact": r by the pairwise sums (K in {2, 3}); "expsum": r by the exponential-sum
     quadrature (any K in [2, MDSS_MAX_K])."""
     B = p.shape[0]
@@ -307,9 +362,9 @@ def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[tor
         r = induced_dist(p, q, K, s_max=s_max, row_status=status)
     else:
         raise ValueError(f"method must be 'exact' or 'expsum', got {method!r}")
-    sel_index, sel_token = select_intermediate(p, q, drafts, u, seed, offset, row_status=status)
-    out, acc, res, mass = accept_or_resample(p, r, sel_token, u, seed, offset, want_residual=want_residual,
-                                             want_mass=want_residual, row_status=status)
+    sel_index, sel_token, out, acc, res, mass = select_accept(p, q, r, drafts, u, seed, offset,
+                                                              want_residual=want_residual, want_mass=want_residual,
+                                                              row_status=status)
     return {"r": r, "sel_index": sel_index, "sel_token": sel_token, "out_token": out, "accepted": acc,
             "residual": res, "mass": mass, "status": status}
 

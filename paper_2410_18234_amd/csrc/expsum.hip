@@ -823,10 +823,6 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
       whi = fmaxf(whi, w);  // w >= 0
       npos += pos;
     }
-    wlo = es_wave_ext<false>(wlo);
-    whi = es_wave_ext<true>(whi);
-    npos = wave_sum_int(npos);
-    const bool bad = __builtin_amdgcn_ballot_w64(anybad) != 0;
     double q0w = 0.0;  // the draft mass on zero-weight tokens (p = 0 < q), in waves that hold one
     if (__builtin_amdgcn_ballot_w64(anyzero) != 0) {
       float q0f = 0.0f;
@@ -834,6 +830,10 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
       for (int i = 0; i < kEsMomPer; ++i) q0f += (qv[i] > 0.0f && pv[i] == 0.0f) ? qv[i] : 0.0f;
       q0w = wave_sum((double)q0f);
     }
+    wlo = es_wave_ext<false>(wlo);
+    whi = es_wave_ext<true>(whi);
+    npos = wave_sum_int(npos);
+    const bool bad = __builtin_amdgcn_ballot_w64(anybad) != 0;
     if (lane == 0) {
       s_f[par][wid][0] = wlo;
       s_f[par][wid][1] = whi;

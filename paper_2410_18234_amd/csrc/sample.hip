@@ -14,49 +14,30 @@ namespace mdss {
 namespace {
 
 // ------------------------------------------------------------------ selection
-// One thread per position: w_i = p(x_i)/q(x_i) (fp64), W = sum_i w_i left to
-// right, index = smallest i with u_sel * W < w_1 + ... + w_i; floor(u_sel K)
-// when W = 0.
-__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ p, const float* __restrict__ q,
-                                                      const int32_t* __restrict__ drafts,
-                                                      const float* __restrict__ u, uint64_t seed, uint64_t offset,
-                                                      int64_t B, int64_t V, int K, int32_t* __restrict__ sel_index,
-                                                      int32_t* __restrict__ sel_token,
-                                                      int32_t* __restrict__ row_status) {
-  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
-  int st = 0;
-  double w[kMaxK];
-  int32_t x[kMaxK];
-  for (int i = 0; i < K; ++i) {
-    w[i] = 0.0;
-    x[i] = drafts[b * K + i];
-    if (x[i] < 0 || (int64_t)x[i] >= V) {
-      st |= kRowBadDraft;
-      continue;
-    }
-    const float pv = p[b * V + x[i]], qv = q[b * V + x[i]];
-    if (bad_prob(pv) || bad_prob(qv)) {
-      st |= kRowBadProb;
-      continue;
-    }
-    if (!(qv > 0.0f)) {
-      st |= kRowBadDraft;
-      continue;
-    }
-    w[i] = (double)pv / (double)qv;
+// Weight of one draft (fp64 p(x)/q(x), the classical weight of Definition 1);
+// an invalid draft (outside [0, V), q(x) = 0, or a NaN/negative/inf p or q)
+// adds its status bit and weighs 0.
+__device__ __forceinline__ double draft_weight(bool in_range, float pv, float qv, int& st) {
+  if (!in_range) {
+    st |= kRowBadDraft;
+    return 0.0;
   }
-  if (st) {
-    sel_index[b] = -1;
-    sel_token[b] = -1;
-    if (row_status) row_status[b] |= st;
-    return;
+  if (bad_prob(pv) || bad_prob(qv)) {
+    st |= kRowBadProb;
+    return 0.0;
   }
-  float uu[3];
-  position_uniforms(u, seed, offset, b, uu);
+  if (!(qv > 0.0f)) {
+    st |= kRowBadDraft;
+    return 0.0;
+  }
+  return (double)pv / (double)qv;
+}
+
+// Selected index from the weights: W = sum_i w_i left to right, the smallest i
+// with u_sel * W < w_1 + ... + w_i; floor(u_sel K) when W = 0.
+__device__ __forceinline__ int select_index(const double* w, int K, double us) {
   double W = 0.0;
   for (int i = 0; i < K; ++i) W += w[i];
-  const double us = (double)uu[0];
   int istar = K - 1;
   if (W > 0.0) {
     const double t = us * W;
@@ -71,7 +52,38 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ p
   } else {
     istar = (int)floor(us * (double)K);
   }
-  istar = istar < 0 ? 0 : (istar >= K ? K - 1 : istar);  // only a uniform outside [0, 1) can leave the range
+  return istar < 0 ? 0 : (istar >= K ? K - 1 : istar);  // only a uniform outside [0, 1) can leave the range
+}
+
+// One thread per position.  q2 == nullptr: every draft from q; else K = 2 and
+// draft i from q_{i+1} (two drafts from different distributions).
+__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ p, const float* __restrict__ q,
+                                                      const float* __restrict__ q2,
+                                                      const int32_t* __restrict__ drafts,
+                                                      const float* __restrict__ u, uint64_t seed, uint64_t offset,
+                                                      int64_t B, int64_t V, int K, int32_t* __restrict__ sel_index,
+                                                      int32_t* __restrict__ sel_token,
+                                                      int32_t* __restrict__ row_status) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int st = 0;
+  double w[kMaxK];
+  int32_t x[kMaxK];
+  for (int i = 0; i < K; ++i) {
+    x[i] = drafts[b * K + i];
+    const bool in = x[i] >= 0 && (int64_t)x[i] < V;
+    const float* qi = (q2 != nullptr && i == 1) ? q2 : q;
+    w[i] = draft_weight(in, in ? p[b * V + x[i]] : 0.0f, in ? qi[b * V + x[i]] : 0.0f, st);
+  }
+  if (st) {
+    sel_index[b] = -1;
+    sel_token[b] = -1;
+    if (row_status) row_status[b] |= st;
+    return;
+  }
+  float uu[3];
+  position_uniforms(u, seed, offset, b, uu);
+  const int istar = select_index(w, K, (double)uu[0]);
   sel_index[b] = istar;
   sel_token[b] = x[istar];
 }
@@ -143,59 +155,6 @@ __global__ __launch_bounds__(256) void select_successive_kernel(
 }
 
 
-// Two drafts proposed by different distributions: w_i = p(x_i) / q_i(x_i).
-__global__ __launch_bounds__(256) void select_pair_kernel(const float* __restrict__ p,
-                                                           const float* __restrict__ q1,
-                                                           const float* __restrict__ q2,
-                                                           const int32_t* __restrict__ drafts,
-                                                           const float* __restrict__ u, uint64_t seed,
-                                                           uint64_t offset, int64_t B, int64_t V,
-                                                           int32_t* __restrict__ sel_index,
-                                                           int32_t* __restrict__ sel_token,
-                                                           int32_t* __restrict__ row_status) {
-  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
-  int st = 0;
-  double w[2] = {0.0, 0.0};
-  int32_t x[2];
-  for (int i = 0; i < 2; ++i) {
-    x[i] = drafts[b * 2 + i];
-    if (x[i] < 0 || (int64_t)x[i] >= V) {
-      st |= kRowBadDraft;
-      continue;
-    }
-    const float pv = p[b * V + x[i]], qv = (i == 0 ? q1 : q2)[b * V + x[i]];
-    if (bad_prob(pv) || bad_prob(qv)) {
-      st |= kRowBadProb;
-      continue;
-    }
-    if (!(qv > 0.0f)) {
-      st |= kRowBadDraft;
-      continue;
-    }
-    w[i] = (double)pv / (double)qv;
-  }
-  if (st) {
-    sel_index[b] = -1;
-    sel_token[b] = -1;
-    if (row_status) row_status[b] |= st;
-    return;
-  }
-  float uu[3];
-  position_uniforms(u, seed, offset, b, uu);
-  const double W = w[0] + w[1];
-  const double us = (double)uu[0];
-  int istar;
-  if (W > 0.0) {
-    istar = (us * W < w[0]) ? 0 : 1;
-  } else {
-    istar = (int)floor(us * 2.0);
-    istar = istar < 0 ? 0 : (istar > 1 ? 1 : istar);
-  }
-  sel_index[b] = istar;
-  sel_token[b] = x[istar];
-}
-
 // ------------------------------------------------------------------ accept / resample
 // One workgroup of 16 waves per position.  Pass 1 streams the row in
 // super-tiles of 1024 tokens (wave w takes super-tiles w, w+16, ...), forms
@@ -226,24 +185,80 @@ __device__ __forceinline__ double residual_of(float pv, float rv) {
   return d > 0.0 ? d : 0.0;
 }
 
-template <bool kVec>
+// Selection arguments of the fused form (selection and Algorithm 1 in one
+// launch): drafts [B][K], q (and q2 for two drafts from different
+// distributions), and the selection outputs (each nullable).
+struct SelArgs {
+  const float* q;
+  const float* q2;
+  const int32_t* drafts;
+  int K;
+  int32_t* sel_index;
+  int32_t* sel_token;
+};
+
+template <bool kVec, bool kSel>
 __global__ __launch_bounds__(kAccThreads) void accept_kernel(
     const float* __restrict__ p, const float* __restrict__ r, const int32_t* __restrict__ sel_token,
     const float* __restrict__ u, uint64_t seed, uint64_t offset, int64_t V, int32_t* __restrict__ out_token,
     uint8_t* __restrict__ accepted, float* __restrict__ residual, double* __restrict__ residual_mass,
-    int32_t* __restrict__ row_status) {
+    int32_t* __restrict__ row_status, SelArgs sel) {
   extern __shared__ double s_tile[];  // one sum per super-tile
   __shared__ int s_bad;
   const int64_t b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const float* pb = p + b * V;
   const float* rb = r + b * V;
-  const int32_t Y = sel_token[b];
-  const bool y_ok = (Y >= 0) && ((int64_t)Y < V);
-  const float pY = y_ok ? pb[Y] : 0.0f, rY = y_ok ? rb[Y] : 0.0f;
-  const bool bad_y = !y_ok || bad_prob(pY) || bad_prob(rY);
   float uu[3];
   position_uniforms(u, seed, offset, b, uu);
+  int32_t Y;
+  float pY = 0.0f, rY = 0.0f;
+  if (kSel) {
+    // the selection of the intermediate token, with p, q and r of every draft
+    // read at once (Y is one of the drafts, so p(Y) and r(Y) come with them)
+    int32_t x[kMaxK];
+    float pv[kMaxK], qv[kMaxK], rv[kMaxK];
+    bool in[kMaxK];
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) {
+      x[i] = i < sel.K ? sel.drafts[b * sel.K + i] : -1;
+      in[i] = x[i] >= 0 && (int64_t)x[i] < V;
+    }
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) {
+      const float* qi = (sel.q2 != nullptr && i == 1) ? sel.q2 : sel.q;
+      pv[i] = in[i] ? pb[x[i]] : 0.0f;
+      qv[i] = in[i] ? qi[b * V + x[i]] : 0.0f;
+      rv[i] = in[i] ? rb[x[i]] : 0.0f;
+    }
+    int st = 0;
+    double w[kMaxK];
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) w[i] = i < sel.K ? draft_weight(in[i], pv[i], qv[i], st) : 0.0;
+    const int istar = st ? -1 : select_index(w, sel.K, (double)uu[0]);
+    Y = -1;
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) {
+      if (i == istar) {
+        Y = x[i];
+        pY = pv[i];
+        rY = rv[i];
+      }
+    }
+    if (tid == 0) {
+      if (sel.sel_index) sel.sel_index[b] = istar;
+      if (sel.sel_token) sel.sel_token[b] = Y;
+      if (st && row_status) row_status[b] |= st;
+    }
+  } else {
+    Y = sel_token[b];
+    if (Y >= 0 && (int64_t)Y < V) {
+      pY = pb[Y];
+      rY = rb[Y];
+    }
+  }
+  const bool y_ok = (Y >= 0) && ((int64_t)Y < V);
+  const bool bad_y = !y_ok || bad_prob(pY) || bad_prob(rY);
   const bool acc = !bad_y && ((double)uu[1] * (double)rY < (double)pY);
   const bool need_pass = (residual != nullptr) || (residual_mass != nullptr) || (!acc && !bad_y);
   if (!need_pass) {
@@ -451,8 +466,8 @@ __global__ __launch_bounds__(kAccThreads) void accept_kernel(
 hipError_t launch_select(const float* p, const float* q, const int32_t* drafts, const float* u, uint64_t seed,
                          uint64_t offset, int64_t B, int64_t V, int K, int32_t* sel_index, int32_t* sel_token,
                          int32_t* row_status, hipStream_t st) {
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, p, q, drafts, u, seed, offset,
-                     B, V, K, sel_index, sel_token, row_status);
+  hipLaunchKernelGGL(select_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, p, q, nullptr, drafts, u,
+                     seed, offset, B, V, K, sel_index, sel_token, row_status);
   return hipGetLastError();
 }
 
@@ -467,26 +482,50 @@ hipError_t launch_select_successive(const float* p, const float* q, const float*
 hipError_t launch_select_pair(const float* p, const float* q1, const float* q2, const int32_t* drafts,
                               const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
                               int32_t* sel_index, int32_t* sel_token, int32_t* row_status, hipStream_t st) {
-  hipLaunchKernelGGL(select_pair_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, p, q1, q2, drafts, u,
-                     seed, offset, B, V, sel_index, sel_token, row_status);
+  hipLaunchKernelGGL(select_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, p, q1, q2, drafts, u, seed,
+                     offset, B, V, 2, sel_index, sel_token, row_status);
   return hipGetLastError();
 }
 
-hipError_t launch_accept(const float* p, const float* r, const int32_t* sel_token, const float* u, uint64_t seed,
-                         uint64_t offset, int64_t B, int64_t V, int32_t* out_token, uint8_t* accepted,
-                         float* residual, double* residual_mass, int32_t* row_status, hipStream_t st) {
+namespace {
+
+template <bool kSel>
+hipError_t launch_accept_impl(const float* p, const float* r, const int32_t* sel_token, const float* u,
+                              uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t* out_token,
+                              uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
+                              const SelArgs& sel, hipStream_t st) {
   const int64_t nsuper = (V + kSuper - 1) / kSuper;
   const size_t lds = sizeof(double) * (size_t)nsuper;
   const bool vec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(r) |
                                      reinterpret_cast<uintptr_t>(residual)) % 16 == 0);
   if (vec) {
-    hipLaunchKernelGGL(accept_kernel<true>, dim3((unsigned)B), dim3(kAccThreads), lds, st, p, r, sel_token, u, seed,
-                       offset, V, out_token, accepted, residual, residual_mass, row_status);
+    hipLaunchKernelGGL((accept_kernel<true, kSel>), dim3((unsigned)B), dim3(kAccThreads), lds, st, p, r, sel_token, u,
+                       seed, offset, V, out_token, accepted, residual, residual_mass, row_status, sel);
   } else {
-    hipLaunchKernelGGL(accept_kernel<false>, dim3((unsigned)B), dim3(kAccThreads), lds, st, p, r, sel_token, u, seed,
-                       offset, V, out_token, accepted, residual, residual_mass, row_status);
+    hipLaunchKernelGGL((accept_kernel<false, kSel>), dim3((unsigned)B), dim3(kAccThreads), lds, st, p, r, sel_token,
+                       u, seed, offset, V, out_token, accepted, residual, residual_mass, row_status, sel);
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_accept(const float* p, const float* r, const int32_t* sel_token, const float* u, uint64_t seed,
+                         uint64_t offset, int64_t B, int64_t V, int32_t* out_token, uint8_t* accepted,
+                         float* residual, double* residual_mass, int32_t* row_status, hipStream_t st) {
+  const SelArgs none = {nullptr, nullptr, nullptr, 0, nullptr, nullptr};
+  return launch_accept_impl<false>(p, r, sel_token, u, seed, offset, B, V, out_token, accepted, residual,
+                                   residual_mass, row_status, none, st);
+}
+
+hipError_t launch_select_accept(const float* p, const float* q, const float* q2, const float* r,
+                                const int32_t* drafts, const float* u, uint64_t seed, uint64_t offset, int64_t B,
+                                int64_t V, int K, int32_t* sel_index, int32_t* sel_token, int32_t* out_token,
+                                uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
+                                hipStream_t st) {
+  const SelArgs sel = {q, q2, drafts, K, sel_index, sel_token};
+  return launch_accept_impl<true>(p, r, nullptr, u, seed, offset, B, V, out_token, accepted, residual,
+                                  residual_mass, row_status, sel, st);
 }
 
 }  // namespace mdss

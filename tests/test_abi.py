@@ -75,6 +75,18 @@ def test_select_and_accept_argument_errors(lib):
     a = lib.mdss_accept_or_resample
     assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, None, FAKE, None, None, None, None) == 1
     assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 1, FAKE, FAKE, None, None, None, None) == 2
+    # the fused form: sel_index, sel_token, residual, mass and row_status may be NULL
+    f = lib.mdss_select_accept
+    assert f(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 2, None, None, FAKE, FAKE, None, None, None, None) == 1
+    assert f(FAKE, FAKE, FAKE, None, None, 0, 0, 4, 16, 2, None, None, FAKE, FAKE, None, None, None, None) == 1
+    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 2, None, None, None, FAKE, None, None, None, None) == 1
+    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 9, None, None, FAKE, FAKE, None, None, None, None) == 3
+    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 1, None, None, FAKE, FAKE, None, None, None, None) == 3
+    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 1, 2, None, None, FAKE, FAKE, None, None, None, None) == 2
+    g = lib.mdss_select_accept_pair
+    assert g(FAKE, FAKE, None, FAKE, FAKE, None, 0, 0, 4, 16, None, None, FAKE, FAKE, None, None, None, None) == 1
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, None, None, FAKE, None, None, None, None, None) == 1
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 0, -1, 16, None, None, FAKE, FAKE, None, None, None, None) == 2
 
 
 def test_python_binding_refuses_cpu_tensors():
@@ -193,6 +205,9 @@ def test_empty_batch_is_a_no_op(lib):
     assert lib.mdss_select_intermediate(N, N, N, N, 0, 0, 0, 16, 2, N, N, N, N) == 0
     assert lib.mdss_select_intermediate_pair(N, N, N, N, N, 0, 0, 0, 16, N, N, N, N) == 0
     assert lib.mdss_accept_or_resample(N, N, N, N, 0, 0, 0, 16, N, N, N, N, N, N) == 0
+    assert lib.mdss_select_accept(N, N, N, N, N, 0, 0, 0, 16, 2, N, N, N, N, N, N, N, N) == 0
+    assert lib.mdss_select_accept(N, N, N, N, N, 0, 0, 0, 16, 9, N, N, N, N, N, N, N, N) == 3
+    assert lib.mdss_select_accept_pair(N, N, N, N, N, N, 0, 0, 0, 16, N, N, N, N, N, N, N, N) == 0
     assert lib.mdss_induced_dist_successive(N, N, 0, 16, 3, N, N, N, 0, N) == 0
     assert lib.mdss_induced_dist_successive(N, N, 0, 16, 9, N, N, N, 0, N) == 3
     assert lib.mdss_select_successive(N, N, N, N, N, 0, 0, 0, 16, 3, N, N, N, N) == 0
