@@ -1357,6 +1357,99 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
 }
 
 // ------------------------------------------------------------------ coefficients
+// Statistics of a row's tile records, merged in tile order.
+struct EsMerge {
+  double wmin[2], wmax[2], q0[2];  // per law
+  int npos[2], bad, wide;          // wide: a tile to be taken in fp64
+};
+
+// Every wave reads the row's records itself (the same values in every lane), so
+// that the merge and the plan need no reduction across lanes and no barrier.
+template <int L>
+__device__ EsMerge es_merge(const EsTile* __restrict__ rec, int64_t T1) {
+  EsMerge m;
+  m.wmin[0] = m.wmin[1] = INFINITY;
+  m.wmax[0] = m.wmax[1] = 0.0;
+  m.q0[0] = m.q0[1] = 0.0;
+  m.npos[0] = m.npos[1] = 0;
+  m.bad = m.wide = 0;
+  constexpr int kB = 8;  // records whose loads are issued together
+  for (int64_t t0 = 0; t0 < T1; t0 += kB) {
+    double lo[kB][L], hi[kB][L], z[kB][L];
+    int np[kB][L], bd[kB][L], wd[kB][L];
+#pragma unroll
+    for (int i = 0; i < kB; ++i)
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        const bool in = t0 + i < T1;
+        const EsTile& e = rec[(in ? t0 + i : 0) * L + l];
+        lo[i][l] = e.wmin;
+        hi[i][l] = e.wmax;
+        z[i][l] = e.q0;
+        np[i][l] = in ? e.npos : 0;
+        bd[i][l] = e.bad;
+        wd[i][l] = e.wide;
+        if (!in) {
+          lo[i][l] = INFINITY;
+          hi[i][l] = 0.0;
+          z[i][l] = 0.0;
+          bd[i][l] = wd[i][l] = 0;
+        }
+      }
+#pragma unroll
+    for (int i = 0; i < kB; ++i)
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        m.wmin[l] = fmin(m.wmin[l], lo[i][l]);
+        m.wmax[l] = fmax(m.wmax[l], hi[i][l]);
+        m.q0[l] += z[i][l];
+        m.npos[l] += np[i][l];
+        m.bad |= bd[i][l];
+        m.wide |= wd[i][l] && !bd[i][l];
+      }
+  }
+  return m;
+}
+
+// The row's plan from its merged records: flags, the grid's node range (the
+// left-tail and right-tail cuts of the quadrature), fp64 evaluation.
+template <int L>
+__device__ EsPlan es_make_plan(const EsMerge& m, int K) {
+  EsPlan pl;
+  pl.flags = m.bad ? kRowBadProb : 0;
+  pl.k_lo = 0;
+  pl.nk = 0;
+  pl.fp64 = m.wide ? 1 : 0;
+  pl.q0[0] = m.q0[0];
+  pl.q0[1] = m.q0[1];
+  for (int i = 0; i < 5; ++i) pl.pad[i] = 0.0;
+  const bool any = (L == 1) ? m.npos[0] > 0 : (m.npos[0] > 0 && m.npos[1] > 0);
+  if (!pl.flags && any) {
+    double dmin, dmax;
+    if (L == 1) {
+      // K = 2 takes the zero-weight tokens in closed form; K >= 3 keeps them in S (denominator w(y) alone)
+      dmin = (K == 2 || m.q0[0] == 0.0) ? K * m.wmin[0] : m.wmin[0];
+      dmax = K * m.wmax[0];
+    } else {
+      dmin = m.wmin[0] + m.wmin[1];
+      dmax = m.wmax[0] + m.wmax[1];
+      int tau, range;
+      es_scale(fmin(m.wmin[0], m.wmin[1]), fmax(m.wmax[0], m.wmax[1]), tau, range);
+      if (range > kEsWideRange) pl.fp64 = 1;  // an evaluation tile mixes both laws' weights
+    }
+    const int k_lo = (int)floor((kEsLnEps - log(dmax)) / kEsStep);
+    const int k_hi = (int)ceil((kEsLnLnInvEps - log(dmin)) / kEsStep);
+    pl.k_lo = k_lo;
+    pl.nk = k_hi - k_lo + 1;
+    if (pl.nk > kEsMaxNodes) {  // only rows with probabilities far above 1 get here
+      pl.flags = kRowRange;
+      pl.nk = 0;
+    }
+  }
+  if (pl.flags) pl.fp64 = 0;
+  return pl;
+}
+
 // One workgroup per row, after the moments.  (1) Tiles the fp32 pass left
 // aside are taken in fp64, in tile order.  (2) The tile records are merged in
 // tile order (fp64): flags, zero-weight masses, the row's grid range.  (3) S_k
@@ -1377,112 +1470,52 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
   EsTile* rec = es.tile + b * nrec;
   double* part = es.part + b * nrec * kEsPart;
   const float* pb = p + b * V;
-  __shared__ double s_d[kEsWaves][6];
-  __shared__ int s_i[kEsWaves][3];
-  __shared__ EsPlan s_plan;
   __shared__ double s_c[L][kEsMaxWin];
   __shared__ double s_rho[kEsMaxWin];  // e^(-m h): (a_k / a_kt) for k = kt - m
   constexpr int kCh = 64;              // tile records staged per pass of (3)
-  __shared__ int s_rkt[kCh], s_rnw[kCh];
+  __shared__ __align__(16) int s_rkt[kCh];
+  __shared__ __align__(16) int s_rnw[kCh];
   __shared__ double s_pow[kCh][kEsTaylor];
+  // a chunk of records: window starts and lengths, power sums / j!; read after a barrier
+  auto stage = [&](int64_t c0) {
+    const int nc = (int)min((int64_t)kCh, nrec - c0);
+    if (tid < nc) {
+      const EsTile& e = rec[c0 + tid];
+      s_rkt[tid] = e.kt;
+      s_rnw[tid] = (e.npos > 0 && !e.bad) ? e.nw : -1;  // -1: the record adds nothing
+    }
+    for (int x = tid; x < nc * kEsTaylor; x += kEsThreads) {
+      const int i = x / kEsTaylor, j = x % kEsTaylor;
+      s_pow[i][j] = part[(c0 + i) * kEsPart + j] * es_inv_fact(j);
+    }
+  };
 
+  // (1) the first chunk's loads go out first; the node ratios are computed meanwhile.
+  // Every wave merges the records (tile order) and takes the plan from them; fp64
+  // tiles (rare) are computed here, and the records are then read again.
+  stage(0);
   for (int m = tid; m < kEsMaxWin; m += kEsThreads) s_rho[m] = exp(-(double)m * kEsStep);
-  // (1) fp64 tiles
-  int w = 0;
-  for (int64_t i = tid; i < nrec; i += kEsThreads) w |= rec[i].wide && !rec[i].bad;
-  const int anywide = __syncthreads_or(w);
+  EsMerge mg = es_merge<L>(rec, es.T1);
+  const int anywide = mg.wide;  // the same in every wave
   if (anywide) {
+    __syncthreads();
     for (int64_t i = 0; i < nrec; ++i) {
       if (!(rec[i].wide && !rec[i].bad)) continue;  // uniform: every thread reads the same record
       const int l = (int)(i % L);
       es_moments_tile<double>(pb, (l == 0 ? q1 : q2) + b * V, V, i / L, rec + i, part + i * kEsPart);
       __syncthreads();
     }
+    stage(0);
+    mg = es_merge<L>(rec, es.T1);
+    mg.wide = 1;
   }
-  // (2) merge
-  double wmin[2] = {INFINITY, INFINITY}, wmax[2] = {0.0, 0.0}, q0[2] = {0.0, 0.0};
-  int npos[2] = {0, 0}, bad = 0;
-  for (int64_t t = tid; t < es.T1; t += kEsThreads) {
-#pragma unroll
-    for (int l = 0; l < L; ++l) {
-      const EsTile& e = rec[t * L + l];
-      wmin[l] = fmin(wmin[l], e.wmin);
-      wmax[l] = fmax(wmax[l], e.wmax);
-      q0[l] += e.q0;
-      npos[l] += e.npos;
-      bad |= e.bad;
-    }
-  }
-  for (int l = 0; l < 2; ++l) {
-    wmin[l] = wave_min64(wmin[l]);
-    wmax[l] = wave_max64(wmax[l]);
-    q0[l] = wave_sum(q0[l]);
-    npos[l] = wave_sum_int(npos[l]);
-  }
-  bad = wave_sum_int(bad);
-  if (lane == 0) {
-    for (int l = 0; l < 2; ++l) {
-      s_d[wid][l] = wmin[l];
-      s_d[wid][2 + l] = wmax[l];
-      s_d[wid][4 + l] = q0[l];
-      s_i[wid][l] = npos[l];
-    }
-    s_i[wid][2] = bad;
-  }
-  __syncthreads();
+  // (2) the plan
+  const EsPlan pl = es_make_plan<L>(mg, K);
   if (tid == 0) {
-    for (int l = 0; l < 2; ++l) {
-      wmin[l] = s_d[0][l];
-      wmax[l] = s_d[0][2 + l];
-      q0[l] = s_d[0][4 + l];
-      npos[l] = s_i[0][l];
-      for (int i = 1; i < kEsWaves; ++i) {
-        wmin[l] = fmin(wmin[l], s_d[i][l]);
-        wmax[l] = fmax(wmax[l], s_d[i][2 + l]);
-        q0[l] += s_d[i][4 + l];
-        npos[l] += s_i[i][l];
-      }
-    }
-    bad = 0;
-    for (int i = 0; i < kEsWaves; ++i) bad |= s_i[i][2];
-    EsPlan pl;
-    pl.flags = bad ? kRowBadProb : 0;
-    pl.k_lo = 0;
-    pl.nk = 0;
-    pl.fp64 = anywide ? 1 : 0;
-    pl.q0[0] = q0[0];
-    pl.q0[1] = q0[1];
-    for (int i = 0; i < 5; ++i) pl.pad[i] = 0.0;
-    const bool any = (L == 1) ? npos[0] > 0 : (npos[0] > 0 && npos[1] > 0);
-    if (!pl.flags && any) {
-      double dmin, dmax;
-      if (L == 1) {
-        // K = 2 takes the zero-weight tokens in closed form; K >= 3 keeps them in S (denominator w(y) alone)
-        dmin = (K == 2 || q0[0] == 0.0) ? K * wmin[0] : wmin[0];
-        dmax = K * wmax[0];
-      } else {
-        dmin = wmin[0] + wmin[1];
-        dmax = wmax[0] + wmax[1];
-        int tau, range;
-        es_scale(fmin(wmin[0], wmin[1]), fmax(wmax[0], wmax[1]), tau, range);
-        if (range > kEsWideRange) pl.fp64 = 1;  // an evaluation tile mixes both laws' weights
-      }
-      const int k_lo = (int)floor((kEsLnEps - log(dmax)) / kEsStep);
-      const int k_hi = (int)ceil((kEsLnLnInvEps - log(dmin)) / kEsStep);
-      pl.k_lo = k_lo;
-      pl.nk = k_hi - k_lo + 1;
-      if (pl.nk > kEsMaxNodes) {  // only rows with probabilities far above 1 get here
-        pl.flags = kRowRange;
-        pl.nk = 0;
-      }
-    }
-    if (pl.flags) pl.fp64 = 0;
-    s_plan = pl;
     es.plan[b] = pl;
     if (row_status && pl.flags) row_status[b] |= pl.flags;
   }
-  __syncthreads();
-  const EsPlan pl = s_plan;
+  __syncthreads();  // the first chunk and the node ratios are in LDS
   if (pl.nk > 0) {
     // (3) S_l(k), two nodes per thread, tiles in order: nodes up to a tile's kt from
     // its power sums, sum_j (-a_k / a_kt)^j T_j / j!; its window from the stored
@@ -1495,46 +1528,51 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
       for (int l = 0; l < L; ++l) S[u][l] = 0.0;
     for (int64_t c0 = 0; c0 < nrec; c0 += kCh) {
       const int nc = (int)min((int64_t)kCh, nrec - c0);
-      __syncthreads();  // the previous pass is consumed
-      if (tid < nc) {
-        const EsTile& e = rec[c0 + tid];
-        s_rkt[tid] = e.kt;
-        s_rnw[tid] = (e.npos > 0 && !e.bad) ? e.nw : -1;  // -1: the record adds nothing
+      if (c0 > 0) {
+        __syncthreads();  // the previous chunk is consumed
+        stage(c0);
+        __syncthreads();
       }
-      for (int x = tid; x < nc * kEsTaylor; x += kEsThreads) {
-        const int i = x / kEsTaylor, j = x % kEsTaylor;
-        s_pow[i][j] = part[(c0 + i) * kEsPart + j] * es_inv_fact(j);
-      }
-      __syncthreads();
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int i = tid + u * kEsThreads;
         if (i >= pl.nk) continue;
         const int k = pl.k_lo + i;
         for (int i0 = 0; i0 < nc; i0 += 8) {
-          double win[8];
+          // eight records at a time, branch-free, so that their LDS reads and window
+          // loads are issued together: window starts and lengths (the same in every
+          // lane), then each lane's window moment (an in-bounds dummy index when the
+          // node is outside the window), then the expansion for the nodes up to kt
+          int rkt[8], rnw[8];
+          {
+            const int4 k0 = *reinterpret_cast<const int4*>(&s_rkt[i0]), k1 = *reinterpret_cast<const int4*>(&s_rkt[i0 + 4]);
+            const int4 n0 = *reinterpret_cast<const int4*>(&s_rnw[i0]), n1 = *reinterpret_cast<const int4*>(&s_rnw[i0 + 4]);
+            const int kk[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+            const int nn[8] = {n0.x, n0.y, n0.z, n0.w, n1.x, n1.y, n1.z, n1.w};
+#pragma unroll
+            for (int m = 0; m < 8; ++m) {
+              rkt[m] = __builtin_amdgcn_readfirstlane(kk[m]);
+              rnw[m] = (i0 + m < nc) ? __builtin_amdgcn_readfirstlane(nn[m]) : -1;  // entries past nc are stale
+            }
+          }
+          double win[8], nx[8];
 #pragma unroll
           for (int m = 0; m < 8; ++m) {
-            const int ri = i0 + m;
-            win[m] = 0.0;
-            if (ri < nc) {
-              const int d = k - s_rkt[ri];
-              if (d >= 1 && d <= s_rnw[ri]) win[m] = part[(c0 + ri) * kEsPart + kEsTaylor + d - 1];
-            }
+            const int ri = min(i0 + m, nc - 1);
+            const int d = k - rkt[m];
+            const bool in = d >= 1 && d <= rnw[m];
+            const double x = part[(c0 + ri) * kEsPart + kEsTaylor + (in ? d - 1 : 0)];
+            win[m] = in ? x : 0.0;
+            nx[m] = -s_rho[max(0, min(-d, kEsMaxWin - 1))];
           }
 #pragma unroll
           for (int m = 0; m < 8; ++m) {
+            if (rnw[m] < 0) continue;  // uniform: the record adds nothing
             const int ri = i0 + m;
-            if (ri >= nc || s_rnw[ri] < 0) continue;
-            const int d = k - s_rkt[ri];
-            double v = win[m];
-            if (d <= 0) {
-              const double nx = -s_rho[min(-d, kEsMaxWin - 1)];
-              v = s_pow[ri][kEsTaylor - 1];
+            double e = s_pow[ri][kEsTaylor - 1];
 #pragma unroll
-              for (int j = kEsTaylor - 2; j >= 0; --j) v = fma(v, nx, s_pow[ri][j]);
-            }
-            S[u][ri % L] += v;  // records are (tile, law) in order; c0 is even
+            for (int j = kEsTaylor - 2; j >= 0; --j) e = fma(e, nx[m], s_pow[ri][j]);
+            S[u][ri % L] += (k - rkt[m] <= 0) ? e : win[m];  // records are (tile, law) in order; c0 is even
           }
         }
       }
@@ -1562,15 +1600,45 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
       for (int l = 0; l < L; ++l) ct[l * kEsMaxWin + i] = s_c[l][i];
     }
     // the expansion of the grid up to each node: B_j(k) = sum_(k' <= k) c_k' e^(-(k - k') h j), stored / j!
-    if (!pl.fp64 && tid < L * kEsTaylor) {
-      const int l = tid / kEsTaylor, j = tid % kEsTaylor;
-      const double rho = exp(-(double)j * kEsStep), f = es_inv_fact(j);
-      double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
-      double acc = 0.0;
-#pragma unroll 8
-      for (int i = 0; i < pl.nk; ++i) {
-        acc = fma(acc, rho, s_c[l][i]);
-        pt[i * kEsTaylor + j] = acc * f;
+    // The recurrence B_j(k) = rho_j B_j(k - 1) + c_k (rho_j = e^(-jh)) in blocks of 16 nodes: each
+    // task (law, j, block) runs it inside its block from zero, then adds the carry of the blocks
+    // before it, sum_b' last_b' rho_j^(16 (b - 1 - b')), times rho_j^(m + 1) at offset m.
+    if (!pl.fp64) {
+      constexpr int kPB = 16;
+      const int nblk = (pl.nk + kPB - 1) / kPB;  // <= 30
+      const int ntask = L * kEsTaylor * nblk;
+      __shared__ double s_last[L][kEsTaylor][(kEsMaxNodes + kPB - 1) / kPB];
+      for (int task = tid; task < ntask; task += kEsThreads) {
+        const int blk = task % nblk, j = (task / nblk) % kEsTaylor, l = task / (nblk * kEsTaylor);
+        const double rho = s_rho[j];
+        const int i0 = blk * kPB, n = min(kPB, pl.nk - i0);
+        double acc = 0.0;
+#pragma unroll
+        for (int m = 0; m < kPB; ++m) {
+          const double c = s_c[l][min(i0 + m, kEsMaxWin - 1)];
+          acc = (m < n) ? fma(acc, rho, c) : acc;
+        }
+        s_last[l][j][blk] = acc;
+      }
+      __syncthreads();
+      for (int task = tid; task < ntask; task += kEsThreads) {
+        const int blk = task % nblk, j = (task / nblk) % kEsTaylor, l = task / (nblk * kEsTaylor);
+        const double rho = s_rho[j], f = es_inv_fact(j);
+        double r16 = rho * rho;  // rho^16
+        r16 *= r16;
+        r16 *= r16;
+        r16 *= r16;
+        double carry = 0.0;
+        for (int bb = 0; bb < blk; ++bb) carry = fma(carry, r16, s_last[l][j][bb]);
+        double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
+        const int i0 = blk * kPB, n = min(kPB, pl.nk - i0);
+        double acc = 0.0, pw = rho;
+#pragma unroll
+        for (int m = 0; m < kPB; ++m) {
+          acc = fma(acc, rho, s_c[l][min(i0 + m, kEsMaxWin - 1)]);
+          if (m < n) pt[(i0 + m) * kEsTaylor + j] = fma(carry, pw, acc) * f;
+          pw *= rho;
+        }
       }
     }
   }
