@@ -46,6 +46,7 @@
 // coefficient kernel, which then evaluates that row in fp64 as well.
 // Zero-weight tokens (p = 0 < q) enter in closed form; a flagged row gets NaN.
 #include "common.h"
+#include "expsum_poly.h"
 
 #include <float.h>
 #include <math.h>
@@ -73,6 +74,8 @@ constexpr double kEsLnFar = -1.3862943611198906;        // ln 1/4: at or below, 
 constexpr double kEsLnZero = 3.0910424533583156;        // ln 22: above, a token's term is dropped
 constexpr double kEsLog2e = 1.4426950408889634;
 constexpr int kEsWideRange = 160;  // binary exponent range of a tile's weights kept in fp32
+constexpr int kEsAtabRows = kEsMaxNodes + 16;  // polynomial rows: the grid and 16 rows past its end
+constexpr int kEsTokNodesC = 9;                // node terms of a query token (a_k w in (1/4, 22.5])
 
 // Per (row, moments tile, law).
 struct alignas(64) EsTile {
@@ -102,8 +105,8 @@ struct EsWork {
   EsTile* tile;     // [B][T1][L]
   double* part;     // [B][T1][L][kEsPart] per tile: power sums T_j, then the moments of its window
   EsPlan* plan;     // [B]
-  double* ctab;     // [B][L][kEsMaxWin] c_k, k = k_lo + i
   double* ptab;     // [B][L][kEsMaxNodes][kEsTaylor] B_j(k_lo + i) / j!: the expansion of the grid up to a node
+  double* atab;     // [B][L][kEsAtabRows][kEsPolyLen] per-token polynomial of node row i (k0 = k_lo + i)
   int64_t T1, T2, T3;  // moments tiles, fp64 evaluation tiles, fp32 evaluation tiles (per row)
 };
 
@@ -1142,18 +1145,22 @@ __device__ bool es_eval_tile(const float* __restrict__ pb, const float* __restri
 // Persistent workgroups over the (row, tile) pairs of 1024 tokens, the next
 // tile's p and q in flight meanwhile.  Every query token takes its own nodes:
 // with k0 its first node where a_k w > 1/4, the nine nodes k0 .. k0 + 8 have
-// a_k w in (1/4, 22.5] and get exponentials, the grid nodes below k0 enter
-// through the expansion sum_j B_j(k0 - 1) (-a_(k0-1) w)^j / j!, B_j(k) =
-// sum over grid nodes k' <= k of c_k' (a_k' / a_k)^j, and the nodes above
-// k0 + 8 (a_k w > 22) are dropped.  Per tile and law three LDS tables, in the
-// tile's scale, are indexed by d = k0 - 1 - kt (kt: the tile's first such
-// node): c_k, B_j / j! and the node rates; each token reads them at its own
-// offset.
-constexpr int kEsTokNodes = 9;                  // exponentials per query token
+// a_k w in (1/4, 22.5], the grid nodes below k0 enter through the expansion
+// sum_j B_j(k0 - 1) (-a_(k0-1) w)^j / j!, B_j(k) = sum over grid nodes k' <= k
+// of c_k' (a_k' / a_k)^j, and the nodes above k0 + 8 (a_k w > 22) are dropped.
+// Since x = a_k0 w lies in (1/4, e^(1/2)/4], the nine node terms and the
+// expansion together are one function of x per node row, kept as a polynomial
+// of degree 10 in t = (x - x_mid) / delta (coefficients from the coefficient
+// kernel; the node terms by Chebyshev interpolation, the expansion exactly).
+// Per tile and law two LDS tables, in the tile's scale, are indexed by
+// d = k0 - 1 - kt (kt: the tile's first expansion node): the polynomial rows
+// and the node rates; each token reads them at its own offset.
+constexpr int kEsTokNodes = kEsTokNodesC;       // node terms per query token
 constexpr int kEsTokPer = 4;                    // tokens per thread
 constexpr int kEsTokTile = kEsThreads * kEsTokPer;  // 1024 tokens per tile
 constexpr int kEsTabRows = kEsWin32 + 1;        // d = 0 .. 240
-constexpr int kEsPolyStride = kEsTaylor + 1;    // padded rows: neighbouring d fall in different banks
+constexpr int kEsPolyStride = 12;               // a polynomial row padded to three 16-byte LDS reads
+static_assert(kEsPolyLen <= kEsPolyStride && kEsPolyStride % 4 == 0, "polynomial row layout");
 
 template <int L>
 __device__ __forceinline__ void es_load_eval(const float* __restrict__ p, const float* __restrict__ q1,
@@ -1191,14 +1198,11 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
                                                               const float* __restrict__ q2, int64_t V, int K,
                                                               float* __restrict__ r, int64_t G, int per, EsWork es) {
   static_assert(kEsMomTile % kEsTokTile == 0, "an evaluation tile lies in one moments tile");
-  __shared__ float s_c[L][kEsTabRows + kEsTokNodes];    // c_(kt+1+i) 2^-tau (0 off the grid)
-  __shared__ float s_p[L][kEsTabRows * kEsPolyStride];  // B_j(kt + d) 2^-tau / j!
-  __shared__ float s_r[L][kEsTabRows];                  // log2(e) a_(kt+1+d) 2^-tau
+  __shared__ __align__(16) float s_a[L][kEsTabRows * kEsPolyStride];  // A_n(k0 = kt + 1 + d) 2^-tau
+  __shared__ float s_r[L][kEsTabRows];                                // log2(e) a_(kt+1+d) 2^-tau
   const int tid = threadIdx.x;
-  // e^(i h) for the nine nodes of a token, and e^(-h) / log2(e) (from log2(e) a_k0 w to a_(k0-1) w)
-  constexpr float kE[kEsTokNodes] = {1.0f,          1.6487212707f, 2.7182818285f, 4.4816890703f, 7.3890560989f,
-                                     12.182493961f, 20.085536923f, 33.115451959f, 54.598150033f};
-  constexpr float kBack = (float)(0.60653065971263342 / kEsLog2e);
+  // t = (a_k0 w - x_mid) / delta from x = log2(e) a_k0 w
+  constexpr float kTs = (float)(1.0 / (kEsPolyDelta * kEsLog2e)), kTo = (float)(-kEsPolyXm / kEsPolyDelta);
 
   const int64_t g0 = (int64_t)blockIdx.x * per, g1 = min(g0 + per, G);
   if (g0 >= g1) return;
@@ -1266,21 +1270,14 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         es_window_f32(wmin[l], wmax[l], kt[l], nw);
         es_window_f32(wmin[l], wmin[l], ktlo, nw);  // the last expansion node of the smallest weight
         D[l] = min(max(ktlo - kt[l], 0), kEsTabRows - 1);
-        // tables: every thread loads its entries (vector loads, all in flight at once)
-        const double* ct = es.ctab + (bb * L + l) * kEsMaxWin;
-        const double* pt = es.ptab + (bb * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
-        for (int i = tid; i < D[l] + 1 + kEsTokNodes; i += kEsThreads) {
-          const int idx = kt[l] + 1 + i - k_lo;
-          s_c[l][i] = (idx >= 0 && idx < nk) ? (float)ldexp(ct[idx], -tau) : 0.0f;
-        }
-        for (int e = tid; e < (D[l] + 1) * kEsTaylor; e += kEsThreads) {
-          const int d = e >> 3, j = e & (kEsTaylor - 1), idx = kt[l] + d - k_lo;
-          double v = 0.0;
-          if (idx >= 0)
-            v = (idx < nk) ? pt[idx * kEsTaylor + j]
-                           : pt[(nk - 1) * kEsTaylor + j] *
-                                 (double)__builtin_amdgcn_exp2f(-(float)(j * (idx - nk + 1)) * (float)(kEsStep * kEsLog2e));
-          s_p[l][d * kEsPolyStride + j] = (float)ldexp(v, -tau);
+        // tables: every thread loads its entries (vector loads, all in flight at once); rows
+        // outside the coefficient kernel's rows [0, nk + 16) do not occur for tokens of
+        // the row and are zero
+        const double* at = es.atab + (bb * L + l) * (int64_t)kEsAtabRows * kEsPolyLen;
+        for (int e = tid; e < (D[l] + 1) * kEsPolyStride; e += kEsThreads) {
+          const int d = e / kEsPolyStride, n = e % kEsPolyStride, i = kt[l] + 1 + d - k_lo;
+          const double v = (n < kEsPolyLen && i >= 0 && i < nk + 16) ? at[i * kEsPolyLen + n] : 0.0;
+          s_a[l][e] = (float)ldexp(v, -tau);
         }
         for (int d = tid; d <= D[l]; d += kEsThreads) s_r[l][d] = es_rate_f32(kt[l] + 1 + d, tau);
       }
@@ -1291,12 +1288,11 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
     if (g + 1 < g1) es_load_eval<L>(p, q1, q2, V, b, t, tid, pv, qv);
     __asm__ volatile("" ::: "memory");
     if (nk > 0) {
-      // (2) per token: nine exponentials and the expansion
+      // (2) per token: the polynomial of its node row
 #pragma unroll
       for (int l = 0; l < L; ++l) {
         if (D[l] < 0) continue;  // uniform
-        const float* sc = s_c[l];
-        const float* sp = s_p[l];
+        const float* sa = s_a[l];
         const float* sr = s_r[l];
         // branch-free over the thread's tokens, so that their dependency chains interleave;
         // a token without a positive weight is evaluated at w = 1 and its result dropped
@@ -1305,8 +1301,11 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         float x[kEsTokPer];
 #pragma unroll
         for (int i = 0; i < kEsTokPer; ++i) {
-          ok[i] = pc[i] > 0.0f && qc[l][i] > 0.0f;
-          const float w = ok[i] ? es_ratio<float>(pc[i], qc[l][i]) : 1.0f;
+          // no short-circuit and the ratio for every token (its inf or NaN for q = 0 is
+          // selected away): straight-line code, no branches per token
+          ok[i] = (pc[i] > 0.0f) & (qc[l][i] > 0.0f);
+          const float ratio = es_ratio<float>(pc[i], qc[l][i]);
+          const float w = ok[i] ? ratio : 1.0f;
           // d = kt(w) - kt, kt(w) = floor((ln 1/4 - ln w) / h)
           const float ktw =
               floorf(((float)kEsLnFar - __builtin_amdgcn_logf(w) * 0.69314718f) * (float)(1.0 / kEsStep));
@@ -1315,27 +1314,33 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         }
 #pragma unroll
         for (int i = 0; i < kEsTokPer; ++i) {
-          // three interleaved partial sums over the nine nodes and the expansion in
-          // Estrin's form: short dependency chains (the kernel is latency-bound)
-          float s3[3] = {0.0f, 0.0f, 0.0f};
-#pragma unroll
-          for (int m = 0; m < kEsTokNodes; ++m)
-            s3[m % 3] = fmaf(sc[d[i] + m], __builtin_amdgcn_exp2f(-x[i] * kE[m]), s3[m % 3]);
-          const float nu = -x[i] * kBack;  // -a_(k0-1) w
-          const float* pr = sp + (d[i] << 3) + d[i];
-          const float nu2 = nu * nu, nu4 = nu2 * nu2;
-          const float e01 = fmaf(pr[1], nu, pr[0]), e23 = fmaf(pr[3], nu, pr[2]);
-          const float e45 = fmaf(pr[5], nu, pr[4]), e67 = fmaf(pr[7], nu, pr[6]);
-          const float pe = fmaf(fmaf(e67, nu2, e45), nu4, fmaf(e23, nu2, e01));
-          acc[i] += ok[i] ? (s3[0] + s3[1]) + (s3[2] + pe) : 0.0f;
+          // Horner in t; the tokens of a thread interleave their chains
+          const float tt = fmaf(x[i], kTs, kTo);
+          const float4* pa = reinterpret_cast<const float4*>(sa + __umul24((unsigned)d[i], kEsPolyStride));
+          const float4 a0 = pa[0], a1 = pa[1], a2 = pa[2];  // A_0 .. A_10 (a2.w: padding)
+          float f = a2.z;
+          f = fmaf(f, tt, a2.y);
+          f = fmaf(f, tt, a2.x);
+          f = fmaf(f, tt, a1.w);
+          f = fmaf(f, tt, a1.z);
+          f = fmaf(f, tt, a1.y);
+          f = fmaf(f, tt, a1.x);
+          f = fmaf(f, tt, a0.w);
+          f = fmaf(f, tt, a0.z);
+          f = fmaf(f, tt, a0.y);
+          f = fmaf(f, tt, a0.x);
+          acc[i] = (l == 0 ? 0.0f : acc[i]) + (ok[i] ? f : 0.0f);
         }
       }
     }
-    // (3) epilogue: r(y) = p(y) 2^tau sum + the zero-weight closed forms
+    // (3) epilogue: r(y) = p(y) 2^tau sum + the zero-weight closed forms; every form is
+    // computed and then selected (kept in registers, so that the compiler does not turn
+    // the selections into branches per token), and a whole tile stores without bounds tests
     const float q0a = (float)pl.q0[0], q0b = (L == 2) ? (float)pl.q0[1] : 0.0f;
     double zw = pl.q0[0];  // K i.i.d. drafts: Q0^(K-1)
     for (int j = 2; j < K; ++j) zw *= pl.q0[0];
     const float zwf = (float)zw;
+    float out[kEsTokPer];
 #pragma unroll
     for (int i = 0; i < kEsTokPer; ++i) {
       const float pp = pc[i];
@@ -1343,15 +1348,28 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
       float v;
       if (L == 1) {
         const float qq = qc[0][i];
-        v = (pp > 0.0f) ? ((K == 2) ? fmaf(2.0f * qq, q0a, quad) : quad) : qq * zwf;
+        float pos = (K == 2) ? fmaf(2.0f * qq, q0a, quad) : quad;
+        float zero = qq * zwf;
+        __asm__ volatile("" : "+v"(pos), "+v"(zero));
+        v = (pp > 0.0f) ? pos : zero;
         v = (qq > 0.0f) ? v : 0.0f;
       } else {
         // two laws: a zero-weight pole of the other draft adds q_i(y) Qj_0; a zero target splits it in half
         const float a = qc[0][i], c = qc[L - 1][i];
-        const float za = (a > 0.0f) ? a * q0b : 0.0f, zc = (c > 0.0f) ? c * q0a : 0.0f;
-        v = (pp > 0.0f) ? quad + za + zc : 0.5f * (za + zc);
+        float za = (a > 0.0f) ? a * q0b : 0.0f, zc = (c > 0.0f) ? c * q0a : 0.0f;
+        float pos = quad + za + zc, zero = 0.5f * (za + zc);
+        __asm__ volatile("" : "+v"(pos), "+v"(zero));
+        v = (pp > 0.0f) ? pos : zero;
       }
-      if (whole || base + i * kEsThreads + tid < V) rb[i * kEsThreads] = v;
+      out[i] = v;
+    }
+    if (whole) {
+#pragma unroll
+      for (int i = 0; i < kEsTokPer; ++i) rb[i * kEsThreads] = out[i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < kEsTokPer; ++i)
+        if (base + i * kEsThreads + tid < V) rb[i * kEsThreads] = out[i];
     }
   }
 }
@@ -1594,11 +1612,6 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
       }
     }
     __syncthreads();
-    double* ct = es.ctab + b * L * kEsMaxWin;
-    for (int i = tid; i < pl.nk; i += kEsThreads) {
-#pragma unroll
-      for (int l = 0; l < L; ++l) ct[l * kEsMaxWin + i] = s_c[l][i];
-    }
     // the expansion of the grid up to each node: B_j(k) = sum_(k' <= k) c_k' e^(-(k - k') h j), stored / j!
     // The recurrence B_j(k) = rho_j B_j(k - 1) + c_k (rho_j = e^(-jh)) in blocks of 16 nodes: each
     // task (law, j, block) runs it inside its block from zero, then adds the carry of the blocks
@@ -1639,6 +1652,40 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
           if (m < n) pt[(i0 + m) * kEsTaylor + j] = fma(carry, pw, acc) * f;
           pw *= rho;
         }
+      }
+      // the per-token polynomial of every node row i (k0 = k_lo + i): a query token with
+      // x = a_k0 w, t = (x - x_mid) / delta, takes sum_n A_n(i) t^n for its nine node terms
+      // and the expansion of the grid below k0,
+      //   A_n(i) = sum_m c_(i+m) G[m][n] + sum_j B_j(k0 - 1) / j! H[j][n]
+      // (c = 0 off the grid; past the grid's end B_j decays by e^(-jh) per node)
+      __syncthreads();  // the prefix table is written
+      const int nrow = pl.nk + 16;  // <= kEsAtabRows
+      for (int task = tid; task < L * nrow; task += kEsThreads) {
+        const int l = task / nrow, i = task % nrow;
+        const double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
+        double cm[kEsTokNodesC], pj[kEsTaylor];
+#pragma unroll
+        for (int m = 0; m < kEsTokNodesC; ++m) cm[m] = (i + m < pl.nk) ? s_c[l][i + m] : 0.0;
+        const int prow = max(0, min(i - 1, pl.nk - 1));  // B_j(k0 - 1): row i - 1, or the last row decayed
+#pragma unroll
+        for (int j = 0; j < kEsTaylor; ++j) {
+          const double v = (i >= 1) ? pt[prow * kEsTaylor + j] : 0.0;
+          pj[j] = (i - 1 > prow) ? v * exp(-(double)((i - 1 - prow) * j) * kEsStep) : v;
+        }
+        double* at = es.atab + ((b * L + l) * (int64_t)kEsAtabRows + i) * kEsPolyLen;
+        double a[kEsPolyLen];  // eleven independent sums, interleaved
+#pragma unroll
+        for (int n = 0; n < kEsPolyLen; ++n) a[n] = 0.0;
+#pragma unroll
+        for (int m = 0; m < kEsTokNodesC; ++m)
+#pragma unroll
+          for (int n = 0; n < kEsPolyLen; ++n) a[n] = fma(cm[m], kEsPolyG[m][n], a[n]);
+#pragma unroll
+        for (int j = 0; j < kEsTaylor; ++j)
+#pragma unroll
+          for (int n = 0; n < kEsPolyLen; ++n) a[n] = fma(pj[j], kEsPolyH[j][n], a[n]);
+#pragma unroll
+        for (int n = 0; n < kEsPolyLen; ++n) at[n] = a[n];
       }
     }
   }
@@ -1683,9 +1730,9 @@ void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
   c += align256(sizeof(double) * B * T1 * L * kEsPart);
   es->plan = reinterpret_cast<EsPlan*>(c);
   c += align256(sizeof(EsPlan) * B);
-  es->ctab = reinterpret_cast<double*>(c);
-  c += align256(sizeof(double) * B * L * kEsMaxWin);
   es->ptab = reinterpret_cast<double*>(c);
+  c += align256(sizeof(double) * B * L * kEsMaxNodes * kEsTaylor);
+  es->atab = reinterpret_cast<double*>(c);
   es->T1 = T1;
   es->T2 = T2;
   es->T3 = es_tiles(V, kEsTokTile);
@@ -1696,8 +1743,8 @@ void carve_es(void* base, int64_t B, int64_t V, int L, EsWork* es) {
 size_t workspace_bytes_expsum(int64_t B, int64_t V, int L) {
   const int64_t T1 = es_tiles(V, kEsMomTile);
   return align256(sizeof(EsTile) * B * T1 * L) + align256(sizeof(double) * B * T1 * L * kEsPart) +
-         align256(sizeof(EsPlan) * B) + align256(sizeof(double) * B * L * kEsMaxWin) +
-         align256(sizeof(double) * B * L * kEsMaxNodes * kEsTaylor);
+         align256(sizeof(EsPlan) * B) + align256(sizeof(double) * B * L * kEsMaxNodes * kEsTaylor) +
+         align256(sizeof(double) * B * L * kEsAtabRows * kEsPolyLen);
 }
 
 // q2 == nullptr: K i.i.d. drafts from q1; else two draft laws (K = 2).
