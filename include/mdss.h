@@ -230,10 +230,13 @@ mdss_status mdss_select_successive(const float* p, const float* q, const float* 
  * trapezoidal rule with step 1/2 on t, cut where both tails are below 1e-8
  * of every denominator of the row: about (ln(D_max/D_min) + 21.3) * 2 nodes
  * (60 on LLM-like rows).  Per token, nodes with a w <= 1/4 enter through an
- * eight-term expansion and nodes with a w > 22 are dropped.  Relative error of
- * every entry, all terms being positive: at most 2 sum_m |Gamma(1 + 4 pi i m)|
- * = 4.8e-8 for the rule, 2e-8 for the grid's tails, 7e-9 for the dropped nodes
- * and 1e-9 for the expansion, 8e-8 in all, plus fp32 rounding (a row with a
+ * eight-term expansion and nodes with a w > 22 are dropped; a token's nine node
+ * terms and its expansion are evaluated together as one degree-10 polynomial in
+ * its a_k0 w (k0 its first node with a w > 1/4, so a_k0 w lies in (1/4, e^(1/2)/4]).
+ * Relative error of every entry, all terms being positive: at most
+ * 2 sum_m |Gamma(1 + 4 pi i m)| = 4.8e-8 for the rule, 2e-8 for the grid's
+ * tails, 7e-9 for the dropped nodes, 1e-9 for the expansion and 4.7e-9 for the
+ * polynomial, 8.1e-8 in all, plus fp32 rounding (a row with a
  * ratio outside the fp32 normal range, or whose weights span more than 2^160
  * within 4096 tokens, is evaluated in fp64).  The zero-weight closed forms are
  * the ones stated above.  Any K in
