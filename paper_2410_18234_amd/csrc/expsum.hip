@@ -1667,7 +1667,7 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
         const double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
         double cm[kEsTokNodesC], pj[kEsTaylor];
 #pragma unroll
-        for (int m = 0; m < kEsTokNodesC; ++m) cm[m] = (i + m < pl.nk) ? s_c[l][i + m] : 0.0;
+        for (int m = 0; m < kEsTokNodesC; ++m) cm[m] = (i + m < pl.nk) ? s_c[l][min(i + m, kEsMaxWin - 1)] : 0.0;
         const int prow = max(0, min(i - 1, pl.nk - 1));  // B_j(k0 - 1): row i - 1, or the last row decayed
 #pragma unroll
         for (int j = 0; j < kEsTaylor; ++j) {
