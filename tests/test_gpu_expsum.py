@@ -313,6 +313,26 @@ def test_wide_weight_range_rows_in_fp64():
     assert np.all(st == 0) and np.all(rel_l1(r, ro) <= TIGHT)
 
 
+def test_weights_on_node_boundaries():
+    # every weight at a node boundary of the grid, w = e^(-k/2) / 4 (one ulp either side or exact):
+    # a token's first node k0 is then decided by the last bit of a rounded logarithm, and its
+    # a_k0 w sits at an end of the interval its polynomial covers; both neighbours are right
+    rng = np.random.default_rng(46)
+    B, V = 4, 2048
+    k = rng.integers(-20, 21, size=(B, V))
+    w = (0.25 * np.exp(-0.5 * k)).astype(np.float32)
+    w = np.where(rng.random((B, V)) < 1 / 3, np.nextafter(w, np.float32(0)), w)
+    w = np.where(rng.random((B, V)) < 1 / 3, np.nextafter(w, np.float32(np.inf)), w)
+    Q = rng.uniform(0.5, 1.5, size=(B, V))
+    Q = (Q / Q.sum(1, keepdims=True)).astype(np.float32)
+    P = (w * Q).astype(np.float32)  # unnormalised target: the weights stay where they were put (up to one rounding)
+    for K in (2, 3):
+        r, st = es_r(P, Q, K)
+        ro, _ = oracle.induced_dist(P, Q, K)
+        assert np.all(st == 0)
+        assert np.all(np.abs(r - ro) <= TIGHT * ro), (K, np.abs(r / ro - 1).max())
+
+
 def test_denormal_weights_in_a_narrow_span():
     # target entries below the fp32 normal range against a normal draft: the weights
     # are fp32 denormals although the row spans only about 2^140, so the tile is taken
