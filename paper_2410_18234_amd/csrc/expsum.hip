@@ -76,7 +76,7 @@ constexpr double kEsLnFar = -1.3862943611198906;        // ln 1/4: at or below, 
 constexpr double kEsLnZero = 3.0910424533583156;        // ln 22: above, a token's term is dropped
 constexpr double kEsLog2e = 1.4426950408889634;
 constexpr int kEsWideRange = 160;  // binary exponent range of a tile's weights kept in fp32
-constexpr int kEsAtabRows = kEsMaxNodes + 16;  // polynomial rows: the grid and 16 rows past its end
+constexpr int kEsAtabRows = kEsMaxNodes + 16;  // polynomial rows of a row and law (bound of EsPlan::nrow)
 constexpr int kEsTokNodesC = 9;                // node terms of a query token (a_k w in (1/4, 22.5])
 
 // Per (row, moments tile, law).
@@ -100,7 +100,9 @@ struct alignas(64) EsPlan {
   int32_t nk;     // nodes of the row's grid (0: no quadrature term)
   int32_t fp64;   // 1: the row is evaluated in fp64 by the coefficient kernel
   double q0[2];   // per law: draft mass of zero-weight tokens
-  double pad[5];
+  int32_t nrow;   // polynomial rows written per law: node rows 0 .. nrow - 1 (k0 = k_lo + i)
+  int32_t pad_i;
+  double pad[4];
 };
 
 struct EsWork {
@@ -1272,13 +1274,14 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         es_window_f32(wmin[l], wmax[l], kt[l], nw);
         es_window_f32(wmin[l], wmin[l], ktlo, nw);  // the last expansion node of the smallest weight
         D[l] = min(max(ktlo - kt[l], 0), kEsTabRows - 1);
-        // tables: every thread loads its entries (vector loads, all in flight at once); rows
-        // outside the coefficient kernel's rows [0, nk + 16) do not occur for tokens of
-        // the row and are zero
+        // tables: every thread loads its entries (vector loads, all in flight at once); the
+        // coefficient kernel wrote the rows [0, nrow) that the row's tokens of either law can
+        // reach (a row before the grid, i < 0, would be a node range no token takes)
         const double* at = es.atab + (bb * L + l) * (int64_t)kEsAtabRows * kEsPolyLen;
+        const int nrow = pl.nrow;
         for (int e = tid; e < (D[l] + 1) * kEsPolyStride; e += kEsThreads) {
           const int d = e / kEsPolyStride, n = e % kEsPolyStride, i = kt[l] + 1 + d - k_lo;
-          const double v = (n < kEsPolyLen && i >= 0 && i < nk + 16) ? at[i * kEsPolyLen + n] : 0.0;
+          const double v = (n < kEsPolyLen && i >= 0 && i < nrow) ? at[i * kEsPolyLen + n] : 0.0;
           s_a[l][e] = (float)ldexp(v, -tau);
         }
         for (int d = tid; d <= D[l]; d += kEsThreads) s_r[l][d] = es_rate_f32(kt[l] + 1 + d, tau);
@@ -1442,7 +1445,9 @@ __device__ EsPlan es_make_plan(const EsMerge& m, int K) {
   pl.fp64 = m.wide ? 1 : 0;
   pl.q0[0] = m.q0[0];
   pl.q0[1] = m.q0[1];
-  for (int i = 0; i < 5; ++i) pl.pad[i] = 0.0;
+  pl.nrow = 0;
+  pl.pad_i = 0;
+  for (int i = 0; i < 4; ++i) pl.pad[i] = 0.0;
   const bool any = (L == 1) ? m.npos[0] > 0 : (m.npos[0] > 0 && m.npos[1] > 0);
   if (!pl.flags && any) {
     double dmin, dmax;
@@ -1464,6 +1469,18 @@ __device__ EsPlan es_make_plan(const EsMerge& m, int K) {
     if (pl.nk > kEsMaxNodes) {  // only rows with probabilities far above 1 get here
       pl.flags = kRowRange;
       pl.nk = 0;
+    } else {
+      // polynomial rows of the evaluation: a query token with first window node k0 reads
+      // row k0 - k_lo.  One law alone: k0 of the smallest weight lies before the grid's
+      // end.  Two laws: a token of one law whose weight is far below the smallest
+      // denominator w1 + w2 has k0 past the grid (every grid node enters through its
+      // decayed expansion), so the rows run to the k0 of either law's smallest weight,
+      // two rows to spare for the evaluation's fp32 logarithm.  Rows needing more than
+      // the table holds (weights spanning far beyond the fp32 tiles' 2^160) go to fp64.
+      int nrow = pl.nk + 16;
+      for (int l = 0; l < L; ++l) nrow = max(nrow, (int)floor((kEsLnFar - log(m.wmin[l])) / kEsStep) + 3 - k_lo);
+      if (nrow > kEsAtabRows) pl.fp64 = 1;
+      pl.nrow = min(nrow, kEsAtabRows);
     }
   }
   if (pl.flags) pl.fp64 = 0;
@@ -1661,7 +1678,7 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
       //   A_n(i) = sum_m c_(i+m) G[m][n] + sum_j B_j(k0 - 1) / j! H[j][n]
       // (c = 0 off the grid; past the grid's end B_j decays by e^(-jh) per node)
       __syncthreads();  // the prefix table is written
-      const int nrow = pl.nk + 16;  // <= kEsAtabRows
+      const int nrow = pl.nrow;  // <= kEsAtabRows
       for (int task = tid; task < L * nrow; task += kEsThreads) {
         const int l = task / nrow, i = task % nrow;
         const double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
