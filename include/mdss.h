@@ -21,7 +21,8 @@
  *     are not renormalised.
  *   - All pointers are HIP device pointers unless stated otherwise.  The
  *     caller owns every buffer, including the workspace; the library never
- *     allocates, frees or keeps device memory between calls.
+ *     allocates, frees or keeps device memory between calls (the one
+ *     exception: the fixed scratch array of mdss_induced_dist_expsum_noalloc).
  *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *     Every call only enqueues work on it and returns; the caller
  *     synchronises.  Calls on one stream run in issue order.
@@ -61,7 +62,8 @@ typedef enum mdss_status {
                             the successive calls), K = 3 with s_max outside [1, MDSS_K3_MAX_SUPPORT],
                             or a truncated-LP s outside [1, MDSS_TLP_MAX_S] */
   MDSS_EDEVICE = 4,      /* a HIP call or kernel launch failed */
-  MDSS_EWORKSPACE = 5    /* workspace missing or smaller than mdss_workspace_bytes() */
+  MDSS_EWORKSPACE = 5    /* workspace missing or smaller than mdss_workspace_bytes(), or (allocation-free
+                            call) sizes beyond MDSS_NOALLOC_SCRATCH_BYTES */
 } mdss_status;
 
 /* row_status bits */
@@ -251,6 +253,30 @@ size_t mdss_workspace_bytes_expsum(int64_t B, int64_t V, int32_t K);
  * the classical weights (as mdss_induced_dist, for any K in [2, MDSS_MAX_K]). */
 mdss_status mdss_induced_dist_expsum(const float* p, const float* q, int64_t B, int64_t V, int32_t K, float* r,
                                      int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---- Allocation-free variant (for callers that cannot allocate) ----------
+ * For callers that cannot call hipMalloc or take a caller-owned workspace:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * device allocation.  The same computation as mdss_induced_dist_expsum (same
+ * kernels, bit-identical outputs and row flags), with its workspace in a fixed
+ * device array of MDSS_NOALLOC_SCRATCH_BYTES inside the library: every GPU the
+ * library runs on holds one copy of it from the first call made on that GPU
+ * until the process ends.  The call allocates and frees nothing.
+ *   - Sizes whose workspace (mdss_workspace_bytes_expsum(B, V, K)) exceeds
+ *     MDSS_NOALLOC_SCRATCH_BYTES are rejected with MDSS_EWORKSPACE before
+ *     anything is launched (256 positions of 32000 tokens need 26.2 MiB).
+ *   - Every call on one GPU uses that GPU's one array: calls that overlap on a
+ *     GPU (several streams, several host threads) race on it and must be
+ *     ordered by the caller.  The array keeps the last call's contents; no call
+ *     depends on them.
+ *   - The first call on a device looks the array's device address up
+ *     (hipGetSymbolAddress) with that device current; a failure there returns
+ *     MDSS_EDEVICE.
+ * Arguments, errors and outputs otherwise as mdss_induced_dist_expsum. */
+#define MDSS_NOALLOC_SCRATCH_BYTES (32LL << 20)
+
+mdss_status mdss_induced_dist_expsum_noalloc(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
+                                             float* r, int32_t* row_status, void* stream);
 
 /* Bytes of workspace for mdss_induced_dist_pair_expsum and
  * mdss_induced_dist_successive_expsum (0 if the shape is invalid or B = 0). */

@@ -17,6 +17,7 @@ from .binding import (  # noqa: F401
     MDSS_ROW_LP_LIMIT,
     MDSS_ROW_RANGE,
     MDSS_MAX_K,
+    MDSS_NOALLOC_SCRATCH_BYTES,
     MDSS_OPTIMUM_MAX_K,
     MDSS_ROW_SUPPORT,
     MDSS_SUCCESSIVE_MAX_K,
@@ -29,6 +30,7 @@ from .binding import (  # noqa: F401
     acceptance,
     induced_dist,
     induced_dist_expsum,
+    induced_dist_expsum_noalloc,
     induced_dist_pair,
     induced_dist_pair_expsum,
     induced_dist_successive,

@@ -92,9 +92,10 @@ def load_library():
         lib.mdss_workspace_bytes_pair_expsum.restype = sz
         lib.mdss_induced_dist_pair_expsum.argtypes = [P, P, P, i64, i64, P, P, P, sz, P]
         lib.mdss_induced_dist_successive_expsum.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P]
+        lib.mdss_induced_dist_expsum_noalloc.argtypes = [P, P, i64, i64, i32, P, P, P]
         for f in ("mdss_induced_dist_successive", "mdss_select_successive", "mdss_optimal_acceptance",
                   "mdss_acceptance", "mdss_induced_dist_expsum", "mdss_induced_dist_pair_expsum",
-                  "mdss_induced_dist_successive_expsum"):
+                  "mdss_induced_dist_successive_expsum", "mdss_induced_dist_expsum_noalloc"):
             getattr(lib, f).restype = ctypes.c_int
         for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample", "mdss_select_accept",
                   "mdss_select_accept_pair",
@@ -641,6 +642,27 @@ def induced_dist_expsum(p: torch.Tensor, q: torch.Tensor, K: int, r: Optional[to
     _check("mdss_induced_dist_expsum",
            lib.mdss_induced_dist_expsum(_ptr(p), _ptr(q), B, V, K, _ptr(r), _ptr(row_status), _ptr(workspace),
                                         workspace.numel(), _stream(dev)))
+    return r
+
+
+# the library's fixed scratch of the allocation-free call (MDSS_NOALLOC_SCRATCH_BYTES)
+MDSS_NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def induced_dist_expsum_noalloc(p: torch.Tensor, q: torch.Tensor, K: int, r: Optional[torch.Tensor] = None,
+                                row_status: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """As induced_dist_expsum, with the workspace in the library's fixed device scratch
+    array (the library allocates nothing; sizes beyond MDSS_NOALLOC_SCRATCH_BYTES are
+    rejected).  Calls that overlap on one GPU race on that array."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    _check("mdss_induced_dist_expsum_noalloc",
+           lib.mdss_induced_dist_expsum_noalloc(_ptr(p), _ptr(q), B, V, K, _ptr(r), _ptr(row_status), _stream(dev)))
     return r
 
 

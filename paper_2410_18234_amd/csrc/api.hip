@@ -41,7 +41,7 @@ const char* mdss_status_string(mdss_status s) {
     case MDSS_ESHAPE: return "invalid shape (B outside [0, MDSS_MAX_B] or V outside [2, MDSS_MAX_V])";
     case MDSS_EUNSUPPORTED: return "unsupported configuration (K out of range, K = 3 with s_max out of range, or s outside [1, MDSS_TLP_MAX_S])";
     case MDSS_EDEVICE: return "HIP error while launching";
-    case MDSS_EWORKSPACE: return "workspace missing or too small";
+    case MDSS_EWORKSPACE: return "workspace missing or too small (allocation-free call: sizes beyond MDSS_NOALLOC_SCRATCH_BYTES)";
   }
   return "unknown status";
 }
@@ -228,6 +228,17 @@ mdss_status mdss_induced_dist_expsum(const float* p, const float* q, int64_t B, 
   if (!workspace_ok(workspace, workspace_bytes, mdss::workspace_bytes_expsum(B, V, 1))) return MDSS_EWORKSPACE;
   return from_hip(mdss::launch_induced_expsum(p, q, nullptr, B, V, K, r, row_status, workspace,
                                               static_cast<hipStream_t>(stream)));
+}
+
+mdss_status mdss_induced_dist_expsum_noalloc(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
+                                             float* r, int32_t* row_status, void* stream) {
+  const mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  if (K < 2 || K > MDSS_MAX_K) return MDSS_EUNSUPPORTED;
+  if (B == 0) return MDSS_OK;
+  if (!p || !q || !r) return MDSS_EINVAL;
+  if (mdss::workspace_bytes_expsum(B, V, 1) > (size_t)MDSS_NOALLOC_SCRATCH_BYTES) return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_induced_expsum_noalloc(p, q, B, V, K, r, row_status, static_cast<hipStream_t>(stream)));
 }
 
 size_t mdss_workspace_bytes_pair_expsum(int64_t B, int64_t V) {

@@ -70,6 +70,10 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
                                  float* r, int32_t* row_status, void* workspace, hipStream_t st);
 hipError_t launch_induced_successive_expsum(const float* p, const float* q, int64_t B, int64_t V, int K,
                                             float* r_stages, int32_t* row_status, void* workspace, hipStream_t st);
+// The K-draft quadrature with its workspace in the library's fixed device scratch
+// array (no allocation); B, V must fit in MDSS_NOALLOC_SCRATCH_BYTES.
+hipError_t launch_induced_expsum_noalloc(const float* p, const float* q, int64_t B, int64_t V, int K, float* r,
+                                         int32_t* row_status, hipStream_t st);
 hipError_t launch_alphabet_truncate(const float* p, int64_t B, int64_t V, int m, float* pt, double* mass0,
                                     int32_t* row_status, hipStream_t st);
 hipError_t launch_alphabet_post(const float* p, const float* pt, const double* mass0, const int32_t* token,

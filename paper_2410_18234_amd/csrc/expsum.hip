@@ -49,11 +49,13 @@
 // Zero-weight tokens (p = 0 < q) enter in closed form; a flagged row gets NaN.
 #include "common.h"
 #include "expsum_poly.h"
+#include "mdss.h"
 
 #include <float.h>
 #include <math.h>
 
 #include <algorithm>
+#include <mutex>
 
 namespace mdss {
 
@@ -1801,6 +1803,49 @@ hipError_t launch_induced_successive_expsum(const float* p, const float* q, int6
     e = launch_induced_expsum(p, r_stages + (j - 1) * plane, q, B, V, 2, r_stages + j * plane, row_status,
                               workspace, st);
   return e;
+}
+
+// ------------------------------------------------------------------ fixed scratch
+// Workspace of the allocation-free variant of the K-draft quadrature: a fixed
+// device array, one copy on every GPU the library runs on, held until the
+// process ends.  In host code `scratch` names a host-side stand-in, never a
+// device address: host code uses only the address hipGetSymbolAddress returns
+// for the current device.  Every call on a GPU reuses that GPU's copy (calls
+// that overlap on one GPU race on it); the kernels write every scratch entry
+// they read, so nothing has to be cleared between calls.
+static __device__ __align__(256) unsigned char scratch[MDSS_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices] = {};  // per device, set on the first call made on it
+}  // namespace
+
+// Device address of the scratch array on the calling thread's current device.
+static hipError_t es_scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (ptr == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_induced_expsum_noalloc(const float* p, const float* q, int64_t B, int64_t V, int K, float* r,
+                                         int32_t* row_status, hipStream_t st) {
+  if (workspace_bytes_expsum(B, V, 1) > (size_t)MDSS_NOALLOC_SCRATCH_BYTES) return hipErrorInvalidValue;
+  void* ws = nullptr;
+  const hipError_t e = es_scratch_address(&ws);
+  if (e != hipSuccess) return e;
+  return launch_induced_expsum(p, q, nullptr, B, V, K, r, row_status, ws, st);
 }
 
 }  // namespace mdss

@@ -227,3 +227,18 @@ def test_empty_batch_is_a_no_op(lib):
     assert lib.mdss_induced_dist_successive_expsum(N, N, 0, 16, 4, N, N, N, 0, N) == 0
     assert lib.mdss_select_intermediate(N, N, N, N, 0, 0, 0, 16, 8, N, N, N, N) == 0
     assert lib.mdss_select_intermediate(N, N, N, N, 0, 0, 0, 16, 9, N, N, N, N) == 3
+
+
+def test_noalloc_argument_errors(lib):
+    f = lib.mdss_induced_dist_expsum_noalloc
+    assert f(None, FAKE, 4, 16, 2, FAKE, None, None) == 1
+    assert f(FAKE, FAKE, 4, 16, 2, None, None, None) == 1
+    assert f(FAKE, FAKE, -1, 16, 2, FAKE, None, None) == 2
+    assert f(FAKE, FAKE, 4, 1, 2, FAKE, None, None) == 2
+    assert f(FAKE, FAKE, 4, 16, 1, FAKE, None, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 9, FAKE, None, None) == 3
+    assert f(None, None, 0, 16, 2, None, None, None) == 0  # empty batch: nothing read or launched
+    # beyond the fixed scratch: rejected before the device is touched
+    assert lib.mdss_workspace_bytes_expsum(1024, 50272, 2) > 32 << 20
+    assert f(FAKE, FAKE, 1024, 50272, 2, FAKE, None, None) == 5
+    assert lib.mdss_workspace_bytes_expsum(256, 32000, 2) <= 32 << 20
