@@ -312,6 +312,8 @@ def test_wide_weight_range_rows_in_fp64():
     w = P.astype(np.float64) / np.where(Q > 0, Q, 1)
     assert np.log2(w.max(1) / w[w > 0].min()).min() > 181
     for K in (2, 3):
+        if K == 3:  # the triple enumeration costs V^3 per row: the first 600 tokens of the same rows
+            P, Q = np.ascontiguousarray(P[:, :600]), np.ascontiguousarray(Q[:, :600])
         r, st = es_r(P, Q, K)
         ro, _ = oracle.induced_dist(P, Q, K)
         assert np.all(st == 0)
@@ -335,6 +337,8 @@ def test_weights_on_node_boundaries():
     Q = (Q / Q.sum(1, keepdims=True)).astype(np.float32)
     P = (w * Q).astype(np.float32)  # unnormalised target: the weights stay where they were put (up to one rounding)
     for K in (2, 3):
+        if K == 3:  # the triple enumeration costs V^3 per row: the first 600 tokens of the same rows
+            P, Q = np.ascontiguousarray(P[:, :600]), np.ascontiguousarray(Q[:, :600])
         r, st = es_r(P, Q, K)
         ro, _ = oracle.induced_dist(P, Q, K)
         assert np.all(st == 0)
@@ -358,6 +362,8 @@ def test_denormal_weights_in_a_narrow_span():
     w = P.astype(np.float64) / Q
     assert max(np.log2(wb.max() / wb[wb > 0].min()) for wb in w) < 160
     for K in (2, 3):
+        if K == 3:  # the triple enumeration costs V^3 per row: the first 600 tokens of the same rows
+            P, Q = np.ascontiguousarray(P[:, :600]), np.ascontiguousarray(Q[:, :600])
         r, st = es_r(P, Q, K)
         ro, _ = oracle.induced_dist(P, Q, K)
         assert np.all(st == 0)
