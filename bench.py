@@ -276,6 +276,7 @@ def main():
     else:
         ws_bytes = mdss.workspace_bytes(B, V, K, s_max)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    ws_acc = torch.empty(mdss.workspace_bytes_accept(B, V), dtype=torch.uint8, device=dev)  # step 2's scratch
 
     def induced():
         if use_es:
@@ -324,7 +325,7 @@ def main():
             if ev is not None:
                 ev[1].record()
             _, sel_token = mdss.select_intermediate(ptr, q, drafts, u, row_status=status)
-            z, acc, _, _ = mdss.accept_or_resample(ptr, r, sel_token, u, row_status=status)
+            z, acc, _, _ = mdss.accept_or_resample(ptr, r, sel_token, u, row_status=status, workspace=ws_acc)
             out, _ = mdss.alphabet_post(p, ptr, m0, z, u2)
             return out, acc
         if cfg.diag:
@@ -339,12 +340,13 @@ def main():
         if not (tlp_s or cfg.successive):
             # selection and Algorithm 1 in one launch
             if cfg.pair:
-                _, _, out, acc, _, _ = mdss.select_accept_pair(p, q, q2, r, drafts, u, row_status=status)
+                _, _, out, acc, _, _ = mdss.select_accept_pair(p, q, q2, r, drafts, u, row_status=status,
+                                                                workspace=ws_acc)
             else:
-                _, _, out, acc, _, _ = mdss.select_accept(p, q, r, drafts, u, row_status=status)
+                _, _, out, acc, _, _ = mdss.select_accept(p, q, r, drafts, u, row_status=status, workspace=ws_acc)
             return out, acc
         _, sel_token = select()
-        out, acc, _, _ = mdss.accept_or_resample(p, r, sel_token, u, row_status=status)
+        out, acc, _, _ = mdss.accept_or_resample(p, r, sel_token, u, row_status=status, workspace=ws_acc)
         return out, acc
 
     if args.copy_calibration:
@@ -526,7 +528,7 @@ def main():
                                          ctypes.c_uint64(0), ctypes.c_uint64(0), B, V,
                                          ctypes.c_void_p(out_t.data_ptr()), ctypes.c_void_p(acc_t.data_ptr()),
                                          ctypes.c_void_p(res.data_ptr()), ctypes.c_void_p(mass.data_ptr()), None,
-                                         stream)
+                                         ctypes.c_void_p(ws_acc.data_ptr()), ws_acc.numel(), stream)
         assert rc == 0
 
     def time_resample(copies, reps):
@@ -550,7 +552,8 @@ def main():
     res_gbs_hot = res_bytes / (res_ms_hot * 1e-3) / 1e9
     roofline_resample = {"bound": "hbm", "achieved": round(res_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": round(res_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                         "kernel": "mdss_accept_or_resample (accept_kernel), residual and mass written for every row",
+                         "kernel": "mdss_accept_or_resample (accept_seg_kernel + accept_draw_kernel), residual and mass written for "
+                                   "every row",
                          "avg_ms": round(res_ms, 4), "bytes_per_launch": res_bytes,
                          "buffers": f"{ncopy} copies of p, r and the residual ({ncopy * res_bytes / 1e6:.0f} MB) "
                                     "taken in turn: every launch misses the 256 MB Infinity Cache",

@@ -129,13 +129,19 @@ mdss_status mdss_select_intermediate(const float* p, const float* q, const int32
  * invalid row: Y = -1, Y out of range, or NaN/negative/inf in p or r).
  * residual ([B][V] fp32, nullable) receives res for every row and
  * residual_mass ([B] fp64, nullable) receives Z; when both are NULL, rows
- * whose token is accepted do not read p or r beyond p(Y), r(Y). */
+ * whose token is accepted do not read p or r beyond p(Y), r(Y).
+ * workspace: device buffer of at least mdss_workspace_bytes_accept(B, V)
+ * bytes, 256-byte aligned (per position a record and one fp64 residual sum
+ * per 256 tokens): a row's residual is summed by one workgroup per 4096-token
+ * segment, and the draw reads the sums of its row.  Two launches. */
+size_t mdss_workspace_bytes_accept(int64_t B, int64_t V);
+
 mdss_status mdss_accept_or_resample(const float* p, const float* r, const int32_t* sel_token, const float* u,
                                     uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t* out_token,
                                     uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
-                                    void* stream);
+                                    void* workspace, size_t workspace_bytes, void* stream);
 
-/* Selection and single-draft speculative sampling in one launch (Theorem 1:
+/* Selection and single-draft speculative sampling in one call (Theorem 1:
  * select the intermediate token, then run Algorithm 1 against r).  Outputs,
  * row flags and every written value are those of mdss_select_intermediate
  * followed by mdss_accept_or_resample with the same p, q, drafts, u, seed and
@@ -144,11 +150,12 @@ mdss_status mdss_accept_or_resample(const float* p, const float* r, const int32_
  * token ([B][V] fp32, e.g. from mdss_induced_dist_expsum).  K in
  * [2, MDSS_MAX_K].  The draft values p(x_i), q(x_i), r(x_i) are read
  * together, so the accept test waits for one round of loads after the
- * drafts. */
+ * drafts.  workspace as for mdss_accept_or_resample. */
 mdss_status mdss_select_accept(const float* p, const float* q, const float* r, const int32_t* drafts,
                                const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
                                int32_t* sel_index, int32_t* sel_token, int32_t* out_token, uint8_t* accepted,
-                               float* residual, double* residual_mass, int32_t* row_status, void* stream);
+                               float* residual, double* residual_mass, int32_t* row_status, void* workspace,
+                               size_t workspace_bytes, void* stream);
 
 /* ---- Two drafts from different distributions (K = 2) --------------------
  * Remark 1 (and the non-identical K = 2 appendix): X1 ~ q1 and X2 ~ q2
@@ -175,12 +182,12 @@ mdss_status mdss_select_intermediate_pair(const float* p, const float* q1, const
                                           void* stream);
 
 /* mdss_select_intermediate_pair followed by mdss_accept_or_resample in one
- * launch, as mdss_select_accept is for identical drafts (drafts [B][2]). */
+ * call, as mdss_select_accept is for identical drafts (drafts [B][2]). */
 mdss_status mdss_select_accept_pair(const float* p, const float* q1, const float* q2, const float* r,
                                     const int32_t* drafts, const float* u, uint64_t seed, uint64_t offset,
                                     int64_t B, int64_t V, int32_t* sel_index, int32_t* sel_token,
                                     int32_t* out_token, uint8_t* accepted, float* residual, double* residual_mass,
-                                    int32_t* row_status, void* stream);
+                                    int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---- Successive pairwise selection (K >= 2) -------------------------------
  * Remark 4: K drafts X1..XK i.i.d. from q are reduced two at a time.  Stage 1

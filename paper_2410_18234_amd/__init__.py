@@ -52,6 +52,7 @@ from .binding import (  # noqa: F401
     truncate_alphabet,
     truncated_lp,
     workspace_bytes,
+    workspace_bytes_accept,
     workspace_bytes_expsum,
     workspace_bytes_pair_expsum,
     workspace_bytes_optimum,

@@ -62,9 +62,12 @@ def load_library():
         lib.mdss_workspace_bytes.restype = sz
         lib.mdss_induced_dist.argtypes = [P, P, i64, i64, i32, i32, P, P, P, sz, P]
         lib.mdss_select_intermediate.argtypes = [P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P]
-        lib.mdss_accept_or_resample.argtypes = [P, P, P, P, u64, u64, i64, i64, P, P, P, P, P, P]
-        lib.mdss_select_accept.argtypes = [P, P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P, P, P, P, P]
-        lib.mdss_select_accept_pair.argtypes = [P, P, P, P, P, P, u64, u64, i64, i64, P, P, P, P, P, P, P, P]
+        lib.mdss_workspace_bytes_accept.argtypes = [i64, i64]
+        lib.mdss_workspace_bytes_accept.restype = sz
+        lib.mdss_accept_or_resample.argtypes = [P, P, P, P, u64, u64, i64, i64, P, P, P, P, P, P, sz, P]
+        lib.mdss_select_accept.argtypes = [P, P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P, P, P, P, P, sz, P]
+        lib.mdss_select_accept_pair.argtypes = [P, P, P, P, P, P, u64, u64, i64, i64, P, P, P, P, P, P, P, P, sz,
+                                                P]
         lib.mdss_workspace_bytes_pair.argtypes = [i64, i64]
         lib.mdss_workspace_bytes_pair.restype = sz
         lib.mdss_induced_dist_pair.argtypes = [P, P, P, i64, i64, P, P, P, sz, P]
@@ -152,10 +155,16 @@ def workspace_bytes(B: int, V: int, K: int, s_max: int = 0) -> int:
 
 
 def _workspace(device: torch.device, nbytes: int) -> torch.Tensor:
-    key = (device, nbytes)
+    """Scratch for a call that was given none: one buffer per (device, stream), grown
+    when a call needs more.  A buffer is only ever replaced on its own stream, and the
+    caching allocator hands freed memory out again in that stream's order, so work in
+    flight on it is never overwritten; calls on other streams have buffers of their
+    own.  Under graph capture every call takes a fresh buffer from the capture's pool."""
+    if torch.cuda.is_current_stream_capturing():
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    key = (device, torch.cuda.current_stream(device).cuda_stream)
     ws = _ws_cache.get(key)
-    if ws is None:
-        _ws_cache.clear()
+    if ws is None or ws.numel() < nbytes:
         ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
         _ws_cache[key] = ws
     return ws
@@ -206,9 +215,13 @@ def select_intermediate(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, 
     return sel_index, sel_token
 
 
+def workspace_bytes_accept(B: int, V: int) -> int:
+    return int(load_library().mdss_workspace_bytes_accept(B, V))
+
+
 def accept_or_resample(p: torch.Tensor, r: torch.Tensor, sel_token: torch.Tensor, u: Optional[torch.Tensor] = None,
                        seed: int = 0, offset: int = 0, want_residual: bool = False, want_mass: bool = False,
-                       row_status: Optional[torch.Tensor] = None):
+                       row_status: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
     """(out_token, accepted, residual or None, residual_mass or None): Algorithm 1 with proposal r."""
     lib = load_library()
     B, V, dev = _pq(p, r)
@@ -221,16 +234,17 @@ def accept_or_resample(p: torch.Tensor, r: torch.Tensor, sel_token: torch.Tensor
     acc = torch.empty(B, dtype=torch.uint8, device=dev)
     res = torch.empty((B, V), dtype=torch.float32, device=dev) if want_residual else None
     mass = torch.empty(B, dtype=torch.float64, device=dev) if want_mass else None
+    workspace = _ws_arg(dev, int(lib.mdss_workspace_bytes_accept(B, V)), workspace)
     _check("mdss_accept_or_resample",
            lib.mdss_accept_or_resample(_ptr(p), _ptr(r), _ptr(sel_token), _ptr(u), ctypes.c_uint64(seed),
                                        ctypes.c_uint64(offset), B, V, _ptr(out), _ptr(acc), _ptr(res), _ptr(mass),
-                                       _ptr(row_status), _stream(dev)))
+                                       _ptr(row_status), _ptr(workspace), workspace.numel(), _stream(dev)))
     return out, acc, res, mass
 
 
 def _select_accept(fn: str, p: torch.Tensor, qs: tuple, r: torch.Tensor, drafts: torch.Tensor,
                    u: Optional[torch.Tensor], seed: int, offset: int, want_residual: bool, want_mass: bool,
-                   row_status: Optional[torch.Tensor]):
+                   row_status: Optional[torch.Tensor], workspace: Optional[torch.Tensor]):
     lib = load_library()
     B, V, dev = _pq(p, r)
     for i, qi in enumerate(qs):
@@ -251,8 +265,9 @@ def _select_accept(fn: str, p: torch.Tensor, qs: tuple, r: torch.Tensor, drafts:
     acc = torch.empty(B, dtype=torch.uint8, device=dev)
     res = torch.empty((B, V), dtype=torch.float32, device=dev) if want_residual else None
     mass = torch.empty(B, dtype=torch.float64, device=dev) if want_mass else None
+    workspace = _ws_arg(dev, int(lib.mdss_workspace_bytes_accept(B, V)), workspace)
     tail = (_ptr(sel_index), _ptr(sel_token), _ptr(out), _ptr(acc), _ptr(res), _ptr(mass), _ptr(row_status),
-            _stream(dev))
+            _ptr(workspace), workspace.numel(), _stream(dev))
     if len(qs) == 1:
         code = lib.mdss_select_accept(_ptr(p), _ptr(qs[0]), _ptr(r), _ptr(drafts), _ptr(u), ctypes.c_uint64(seed),
                                       ctypes.c_uint64(offset), B, V, K, *tail)
@@ -265,19 +280,21 @@ def _select_accept(fn: str, p: torch.Tensor, qs: tuple, r: torch.Tensor, drafts:
 
 def select_accept(p: torch.Tensor, q: torch.Tensor, r: torch.Tensor, drafts: torch.Tensor,
                   u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False,
-                  want_mass: bool = False, row_status: Optional[torch.Tensor] = None):
+                  want_mass: bool = False, row_status: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None):
     """(sel_index, sel_token, out_token, accepted, residual or None, residual_mass or None):
-    select_intermediate and accept_or_resample in one launch."""
+    select_intermediate and accept_or_resample in one call."""
     return _select_accept("mdss_select_accept", p, (q,), r, drafts, u, seed, offset, want_residual, want_mass,
-                          row_status)
+                          row_status, workspace)
 
 
 def select_accept_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, r: torch.Tensor, drafts: torch.Tensor,
                        u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False,
-                       want_mass: bool = False, row_status: Optional[torch.Tensor] = None):
-    """select_intermediate_pair and accept_or_resample in one launch (drafts [B][2])."""
+                       want_mass: bool = False, row_status: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None):
+    """select_intermediate_pair and accept_or_resample in one call (drafts [B][2])."""
     return _select_accept("mdss_select_accept_pair", p, (q1, q2), r, drafts, u, seed, offset, want_residual,
-                          want_mass, row_status)
+                          want_mass, row_status, workspace)
 
 
 def workspace_bytes_pair(B: int, V: int) -> int:

@@ -283,43 +283,52 @@ mdss_status mdss_select_intermediate(const float* p, const float* q, const int32
                                       static_cast<hipStream_t>(stream)));
 }
 
+size_t mdss_workspace_bytes_accept(int64_t B, int64_t V) {
+  if (check_shape(B, V) != MDSS_OK || B == 0) return 0;
+  return mdss::workspace_bytes_accept(B, V);
+}
+
 mdss_status mdss_accept_or_resample(const float* p, const float* r, const int32_t* sel_token, const float* u,
                                     uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t* out_token,
                                     uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
-                                    void* stream) {
+                                    void* workspace, size_t workspace_bytes, void* stream) {
   mdss_status s = check_shape(B, V);
   if (s != MDSS_OK) return s;
   if (B == 0) return MDSS_OK;
   if (!p || !r || !sel_token || !out_token || !accepted) return MDSS_EINVAL;
+  if (!workspace_ok(workspace, workspace_bytes, mdss::workspace_bytes_accept(B, V))) return MDSS_EWORKSPACE;
   return from_hip(mdss::launch_accept(p, r, sel_token, u, seed, offset, B, V, out_token, accepted, residual,
-                                      residual_mass, row_status, static_cast<hipStream_t>(stream)));
+                                      residual_mass, row_status, workspace, static_cast<hipStream_t>(stream)));
 }
 
 mdss_status mdss_select_accept(const float* p, const float* q, const float* r, const int32_t* drafts,
                                const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
                                int32_t* sel_index, int32_t* sel_token, int32_t* out_token, uint8_t* accepted,
-                               float* residual, double* residual_mass, int32_t* row_status, void* stream) {
+                               float* residual, double* residual_mass, int32_t* row_status, void* workspace,
+                               size_t workspace_bytes, void* stream) {
   mdss_status s = check_shape(B, V);
   if (s != MDSS_OK) return s;
   if (K < 2 || K > MDSS_MAX_K) return MDSS_EUNSUPPORTED;
   if (B == 0) return MDSS_OK;
   if (!p || !q || !r || !drafts || !out_token || !accepted) return MDSS_EINVAL;
+  if (!workspace_ok(workspace, workspace_bytes, mdss::workspace_bytes_accept(B, V))) return MDSS_EWORKSPACE;
   return from_hip(mdss::launch_select_accept(p, q, nullptr, r, drafts, u, seed, offset, B, V, K, sel_index,
                                              sel_token, out_token, accepted, residual, residual_mass, row_status,
-                                             static_cast<hipStream_t>(stream)));
+                                             workspace, static_cast<hipStream_t>(stream)));
 }
 
 mdss_status mdss_select_accept_pair(const float* p, const float* q1, const float* q2, const float* r,
                                     const int32_t* drafts, const float* u, uint64_t seed, uint64_t offset,
                                     int64_t B, int64_t V, int32_t* sel_index, int32_t* sel_token,
                                     int32_t* out_token, uint8_t* accepted, float* residual, double* residual_mass,
-                                    int32_t* row_status, void* stream) {
+                                    int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream) {
   mdss_status s = check_shape(B, V);
   if (s != MDSS_OK) return s;
   if (B == 0) return MDSS_OK;
   if (!p || !q1 || !q2 || !r || !drafts || !out_token || !accepted) return MDSS_EINVAL;
+  if (!workspace_ok(workspace, workspace_bytes, mdss::workspace_bytes_accept(B, V))) return MDSS_EWORKSPACE;
   return from_hip(mdss::launch_select_accept(p, q1, q2, r, drafts, u, seed, offset, B, V, 2, sel_index, sel_token,
-                                             out_token, accepted, residual, residual_mass, row_status,
+                                             out_token, accepted, residual, residual_mass, row_status, workspace,
                                              static_cast<hipStream_t>(stream)));
 }
 

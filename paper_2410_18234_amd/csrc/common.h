@@ -94,14 +94,16 @@ hipError_t launch_select_tlp(const float* p, const float* q1, const float* q2, c
 hipError_t launch_select(const float* p, const float* q, const int32_t* drafts, const float* u, uint64_t seed,
                          uint64_t offset, int64_t B, int64_t V, int K, int32_t* sel_index, int32_t* sel_token,
                          int32_t* row_status, hipStream_t st);
+size_t workspace_bytes_accept(int64_t B, int64_t V);
 hipError_t launch_accept(const float* p, const float* r, const int32_t* sel_token, const float* u, uint64_t seed,
                          uint64_t offset, int64_t B, int64_t V, int32_t* out_token, uint8_t* accepted,
-                         float* residual, double* residual_mass, int32_t* row_status, hipStream_t st);
+                         float* residual, double* residual_mass, int32_t* row_status, void* workspace,
+                         hipStream_t st);
 hipError_t launch_select_accept(const float* p, const float* q, const float* q2, const float* r,
                                 const int32_t* drafts, const float* u, uint64_t seed, uint64_t offset, int64_t B,
                                 int64_t V, int K, int32_t* sel_index, int32_t* sel_token, int32_t* out_token,
                                 uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
-                                hipStream_t st);
+                                void* workspace, hipStream_t st);
 
 // ---------------------------------------------------------------- device helpers
 __device__ __forceinline__ bool bad_prob(float v) { return !(v >= 0.0f) || isinf(v); }

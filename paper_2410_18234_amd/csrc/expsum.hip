@@ -193,6 +193,16 @@ __device__ __forceinline__ float es_ratio<float>(float p, float q) {
   // reciprocal and product: within 2 ulp of p / q, the same value in every kernel
   return p * __builtin_amdgcn_rcpf(q);
 }
+// The same ratio for a draft probability below the fp32 normal range, whose
+// reciprocal would overflow: q is scaled up by 2^64 first (p / q itself is
+// often far inside the range: a draft at a low temperature puts its tail there).
+// The kernels take it only in waves that hold such a q (a uniform branch).
+__device__ __forceinline__ float es_ratio_small_q(float p, float q) {
+  return (p * __builtin_amdgcn_rcpf(q * 0x1p64f)) * 0x1p64f;
+}
+// positive fp32 denormal (class bit 7; bits 0-9: signalling NaN, quiet NaN, -inf, -normal,
+// -denormal, -0, +0, +denormal, +normal, +inf)
+__device__ __forceinline__ bool es_denormal(float q) { return __builtin_amdgcn_classf(q, 0x80); }
 template <>
 __device__ __forceinline__ double es_ratio<double>(float p, float q) {
   return (double)p / (double)q;
@@ -817,19 +827,28 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
     // (1) ratios and statistics
     float wv[kEsMomPer];  // 0 for a token left out
     float wlo = INFINITY, whi = 0.0f;
-    bool anybad = false, anyzero = false;
+    bool anybad = false, anyzero = false, anysmall = false;
     int npos = 0;
 #pragma unroll
     for (int i = 0; i < kEsMomPer; ++i) {
       const float pp = pv[i], qq = qv[i];
       // NaN, -inf, negative normal or denormal, +inf (-0 is a zero probability)
       anybad |= __builtin_amdgcn_classf(pp, 0x21F) | __builtin_amdgcn_classf(qq, 0x21F);
+      anysmall |= es_denormal(qq);
       const bool pos = pp > 0.0f && qq > 0.0f;
       anyzero |= qq > 0.0f && pp == 0.0f;
-      const float w = pos ? es_ratio<float>(pp, qq) : 0.0f;
-      wv[i] = w;
-      wlo = fminf(wlo, pos ? w : INFINITY);
-      whi = fmaxf(whi, w);  // w >= 0
+      wv[i] = pos ? es_ratio<float>(pp, qq) : 0.0f;
+    }
+    if (__builtin_amdgcn_ballot_w64(anysmall) != 0) {  // uniform: a denormal draft probability in the wave
+#pragma unroll
+      for (int i = 0; i < kEsMomPer; ++i)
+        if (es_denormal(qv[i]) && pv[i] > 0.0f) wv[i] = es_ratio_small_q(pv[i], qv[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < kEsMomPer; ++i) {
+      const bool pos = pv[i] > 0.0f && qv[i] > 0.0f;
+      wlo = fminf(wlo, pos ? wv[i] : INFINITY);
+      whi = fmaxf(whi, wv[i]);  // w >= 0
       npos += pos;
     }
     double q0w = 0.0;  // the draft mass on zero-weight tokens (p = 0 < q), in waves that hold one
@@ -1306,13 +1325,24 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         bool ok[kEsTokPer];
         int d[kEsTokPer];
         float x[kEsTokPer];
+        float ratio[kEsTokPer];
+        bool small = false;
 #pragma unroll
         for (int i = 0; i < kEsTokPer; ++i) {
           // no short-circuit and the ratio for every token (its inf or NaN for q = 0 is
           // selected away): straight-line code, no branches per token
           ok[i] = (pc[i] > 0.0f) & (qc[l][i] > 0.0f);
-          const float ratio = es_ratio<float>(pc[i], qc[l][i]);
-          const float w = ok[i] ? ratio : 1.0f;
+          ratio[i] = es_ratio<float>(pc[i], qc[l][i]);
+          small |= es_denormal(qc[l][i]);
+        }
+        if (__builtin_amdgcn_ballot_w64(small) != 0) {  // uniform: a denormal draft probability in the wave
+#pragma unroll
+          for (int i = 0; i < kEsTokPer; ++i)
+            if (es_denormal(qc[l][i])) ratio[i] = es_ratio_small_q(pc[i], qc[l][i]);
+        }
+#pragma unroll
+        for (int i = 0; i < kEsTokPer; ++i) {
+          const float w = ok[i] ? ratio[i] : 1.0f;
           // d = kt(w) - kt, kt(w) = floor((ln 1/4 - ln w) / h)
           const float ktw =
               floorf(((float)kEsLnFar - __builtin_amdgcn_logf(w) * 0.69314718f) * (float)(1.0 / kEsStep));

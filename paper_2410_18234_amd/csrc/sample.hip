@@ -156,15 +156,42 @@ __global__ __launch_bounds__(256) void select_successive_kernel(
 
 
 // ------------------------------------------------------------------ accept / resample
-// One workgroup of 16 waves per position.  Pass 1 streams the row in
-// super-tiles of 1024 tokens (wave w takes super-tiles w, w+16, ...), forms
-// res = max(0, p - r) in fp64, optionally stores it, and keeps each
-// super-tile's sum in LDS.  Wave 0 then scans the super-tile sums, finds the
-// super-tile where the running sum first exceeds u_res * Z and re-reads only
-// that one (four 256-token sub-tiles, each a lane scan) to locate the token.
-constexpr int kAccThreads = 1024;
-constexpr int kAccWaves = kAccThreads / 64;
-constexpr int kSuper = 1024;
+// Two forms, the same arithmetic (Algorithm 1 with proposal r; res = max(0, p - r)
+// and its running sums in fp64).
+// Row form (neither the residual nor its mass is asked for: only rejected
+// positions read their rows): one workgroup of 8 waves per position.  The
+// selection (fused form) and the accept test come first; a rejected position
+// streams its row in 1024-token super-tiles (wave w takes super-tiles w, w + 8,
+// w + 16, w + 24 in one pass, then the next 32), keeps each super-tile's
+// residual sum in LDS and its last pass's p and r in registers; every wave then
+// scans the sums, and the wave holding the crossing super-tile finds the token
+// in it (a re-read only for rows longer than 32768 tokens whose crossing lies in
+// an earlier pass).
+// Segment form (the residual or its mass asked for: every position streams its
+// row), two launches:
+// (A) one workgroup per (position, segment of 4096 tokens): res = max(0, p - r)
+//     over the segment in fp64 (stored as fp32 if asked for) and one fp64 sum per
+//     256-token sub-tile (NaN when the sub-tile holds a bad probability);
+// (B) one wave per position: the selection (fused form) and the accept test,
+//     with the sub-tile sums read at the same time; Z from the sums in order,
+//     the first sub-tile whose running sum exceeds u_res * Z, and the token
+//     inside it from its 256 entries.
+// A position's row is so spread over all of its segments' workgroups.
+constexpr int kAccRowThreads = 512;
+constexpr int kAccRowWaves = kAccRowThreads / 64;
+constexpr int kAccRowHold = 4;                               // super-tiles per wave and pass of the row form
+constexpr int kSuper = 1024;                                 // tokens per super-tile of the row form
+constexpr int kAccSegThreads = 256;
+constexpr int kAccSub = 256;                                 // tokens per sub-tile: one float4 per lane of a wave
+constexpr int kAccSubPerWave = 4;                            // sub-tiles per wave and segment
+constexpr int kAccSeg = kAccSegThreads / 64 * kAccSubPerWave * kAccSub;  // 4096 tokens per segment
+constexpr int kAccThreads = 256;                             // (B)
+constexpr int kAccRowsPerDraw = kAccThreads / 64;            // positions per workgroup of (B)
+
+struct AccWork {
+  double* sub;   // [B][nsub] residual sums per sub-tile, written by (A), read by (B)
+  int64_t nsub;  // sub-tiles per row, ceil(V / 256)
+};
 
 template <bool kVec>
 __device__ __forceinline__ void load4(const float* __restrict__ a, int64_t x0, int64_t V, float v[4]) {
@@ -185,8 +212,59 @@ __device__ __forceinline__ double residual_of(float pv, float rv) {
   return d > 0.0 ? d : 0.0;
 }
 
+// fp64 lane moves by DPP (each 32-bit half moved the same way)
+template <int CTRL, int ROW_MASK = 0xF, bool BOUND_ZERO = false>
+__device__ __forceinline__ double dpp64(double x) {
+  const uint64_t v = __double_as_longlong(x);
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)v, CTRL, ROW_MASK, 0xF, BOUND_ZERO);
+  const uint32_t hi = __builtin_amdgcn_update_dpp(0u, (uint32_t)(v >> 32), CTRL, ROW_MASK, 0xF, BOUND_ZERO);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+// x + the value of the partner lane of a gfx950 row swap (ROW) or half swap
+template <bool ROW>
+__device__ __forceinline__ double swap_sum64(double x) {
+  const uint64_t v = __double_as_longlong(x);
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  const auto a = ROW ? __builtin_amdgcn_permlane16_swap(lo, lo, false, false)
+                     : __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+  const auto c = ROW ? __builtin_amdgcn_permlane16_swap(hi, hi, false, false)
+                     : __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+  return __longlong_as_double((long long)(((uint64_t)c[0] << 32) | a[0])) +
+         __longlong_as_double((long long)(((uint64_t)c[1] << 32) | a[1]));
+}
+// Sum over the 64 lanes of a wave, in every lane: quad permutations and row
+// rotations within each 16-lane row, then the row and half swaps (all lanes active).
+__device__ __forceinline__ double wave_sum_dpp(double x) {
+  x += dpp64<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp64<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp64<0x124>(x);  // row_ror:4
+  x += dpp64<0x128>(x);  // row_ror:8
+  x = swap_sum64<true>(x);
+  return swap_sum64<false>(x);
+}
+// Inclusive prefix sum over the 64 lanes of a wave (fixed order): Hillis-Steele
+// within each 16-lane row by DPP row shifts (lanes shifted in from outside the
+// row read 0), then each row adds the totals of the rows before it, read from
+// lanes 15, 31 and 47.
+__device__ __forceinline__ double wave_inclusive_scan_dpp(double x, int lane) {
+  x += dpp64<0x111, 0xF, true>(x);  // row_shr:1
+  x += dpp64<0x112, 0xF, true>(x);  // row_shr:2
+  x += dpp64<0x114, 0xF, true>(x);  // row_shr:4
+  x += dpp64<0x118, 0xF, true>(x);  // row_shr:8
+  const uint64_t v = __double_as_longlong(x);
+  const auto rd = [&](int l) {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, l), hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), l);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+  };
+  const double t0 = rd(15), t1 = rd(31), t2 = rd(47);
+  const int row = lane >> 4;
+  const double c01 = t0 + t1;
+  const double carry = row == 0 ? 0.0 : (row == 1 ? t0 : (row == 2 ? c01 : c01 + t2));
+  return row == 0 ? x : x + carry;
+}
+
 // Selection arguments of the fused form (selection and Algorithm 1 in one
-// launch): drafts [B][K], q (and q2 for two drafts from different
+// call): drafts [B][K], q (and q2 for two drafts from different
 // distributions), and the selection outputs (each nullable).
 struct SelArgs {
   const float* q;
@@ -197,12 +275,80 @@ struct SelArgs {
   int32_t* sel_token;
 };
 
+// The selection of the intermediate token (fused form: from the drafts, with
+// p, q and r of every draft read at once, so p(Y) and r(Y) come with them) or the
+// given selected token, and the accept test u_acc r(Y) < p(Y) in fp64.
+struct Decision {
+  int32_t Y;      // selected token (-1 if the drafts are invalid)
+  int32_t istar;  // selected index (fused form)
+  int st;         // status bits of the selection
+  bool y_ok, bad_y, acc;
+};
+
+template <bool kSel>
+__device__ __forceinline__ Decision take_decision(const float* __restrict__ pb, const float* __restrict__ rb,
+                                                  const int32_t* __restrict__ sel_token, const SelArgs& sel,
+                                                  int64_t b, int64_t V, const float (&uu)[3]) {
+  Decision d;
+  d.st = 0;
+  d.istar = -1;
+  float pY = 0.0f, rY = 0.0f;
+  if (kSel) {
+    int32_t x[kMaxK];
+    float pv[kMaxK], qv[kMaxK], rv[kMaxK];
+    bool in[kMaxK];
+    // the drafts past K are skipped by branches on K (the same in every lane)
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) {
+      x[i] = -1;
+      if (i < sel.K) x[i] = sel.drafts[b * sel.K + i];
+      in[i] = x[i] >= 0 && (int64_t)x[i] < V;
+    }
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) {
+      pv[i] = qv[i] = rv[i] = 0.0f;
+      if (i < sel.K) {
+        const float* qi = (sel.q2 != nullptr && i == 1) ? sel.q2 : sel.q;
+        pv[i] = in[i] ? pb[x[i]] : 0.0f;
+        qv[i] = in[i] ? qi[b * V + x[i]] : 0.0f;
+        rv[i] = in[i] ? rb[x[i]] : 0.0f;
+      }
+    }
+    double w[kMaxK];
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) {
+      w[i] = 0.0;
+      if (i < sel.K) w[i] = draft_weight(in[i], pv[i], qv[i], d.st);
+    }
+    d.istar = d.st ? -1 : select_index(w, sel.K, (double)uu[0]);
+    d.Y = -1;
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) {
+      if (i == d.istar) {
+        d.Y = x[i];
+        pY = pv[i];
+        rY = rv[i];
+      }
+    }
+  } else {
+    d.Y = sel_token[b];
+    if (d.Y >= 0 && (int64_t)d.Y < V) {
+      pY = pb[d.Y];
+      rY = rb[d.Y];
+    }
+  }
+  d.y_ok = (d.Y >= 0) && ((int64_t)d.Y < V);
+  d.bad_y = !d.y_ok || bad_prob(pY) || bad_prob(rY);
+  d.acc = !d.bad_y && ((double)uu[1] * (double)rY < (double)pY);
+  return d;
+}
+
+// Row form: one workgroup per position (the residual and its mass not asked for).
 template <bool kVec, bool kSel>
-__global__ __launch_bounds__(kAccThreads) void accept_kernel(
+__global__ __launch_bounds__(kAccRowThreads) void accept_row_kernel(
     const float* __restrict__ p, const float* __restrict__ r, const int32_t* __restrict__ sel_token,
     const float* __restrict__ u, uint64_t seed, uint64_t offset, int64_t V, int32_t* __restrict__ out_token,
-    uint8_t* __restrict__ accepted, float* __restrict__ residual, double* __restrict__ residual_mass,
-    int32_t* __restrict__ row_status, SelArgs sel) {
+    uint8_t* __restrict__ accepted, int32_t* __restrict__ row_status, SelArgs sel) {
   extern __shared__ double s_tile[];  // one sum per super-tile
   __shared__ int s_bad;
   const int64_t b = blockIdx.x;
@@ -211,75 +357,31 @@ __global__ __launch_bounds__(kAccThreads) void accept_kernel(
   const float* rb = r + b * V;
   float uu[3];
   position_uniforms(u, seed, offset, b, uu);
-  int32_t Y;
-  float pY = 0.0f, rY = 0.0f;
-  if (kSel) {
-    // the selection of the intermediate token, with p, q and r of every draft
-    // read at once (Y is one of the drafts, so p(Y) and r(Y) come with them)
-    int32_t x[kMaxK];
-    float pv[kMaxK], qv[kMaxK], rv[kMaxK];
-    bool in[kMaxK];
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) {
-      x[i] = i < sel.K ? sel.drafts[b * sel.K + i] : -1;
-      in[i] = x[i] >= 0 && (int64_t)x[i] < V;
-    }
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) {
-      const float* qi = (sel.q2 != nullptr && i == 1) ? sel.q2 : sel.q;
-      pv[i] = in[i] ? pb[x[i]] : 0.0f;
-      qv[i] = in[i] ? qi[b * V + x[i]] : 0.0f;
-      rv[i] = in[i] ? rb[x[i]] : 0.0f;
-    }
-    int st = 0;
-    double w[kMaxK];
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) w[i] = i < sel.K ? draft_weight(in[i], pv[i], qv[i], st) : 0.0;
-    const int istar = st ? -1 : select_index(w, sel.K, (double)uu[0]);
-    Y = -1;
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) {
-      if (i == istar) {
-        Y = x[i];
-        pY = pv[i];
-        rY = rv[i];
-      }
-    }
-    if (tid == 0) {
-      if (sel.sel_index) sel.sel_index[b] = istar;
-      if (sel.sel_token) sel.sel_token[b] = Y;
-      if (st && row_status) row_status[b] |= st;
-    }
-  } else {
-    Y = sel_token[b];
-    if (Y >= 0 && (int64_t)Y < V) {
-      pY = pb[Y];
-      rY = rb[Y];
-    }
+  const Decision d = take_decision<kSel>(pb, rb, sel_token, sel, b, V, uu);
+  if (kSel && tid == 0) {
+    if (sel.sel_index) sel.sel_index[b] = d.istar;
+    if (sel.sel_token) sel.sel_token[b] = d.Y;
+    if (d.st && row_status) row_status[b] |= d.st;
   }
-  const bool y_ok = (Y >= 0) && ((int64_t)Y < V);
-  const bool bad_y = !y_ok || bad_prob(pY) || bad_prob(rY);
-  const bool acc = !bad_y && ((double)uu[1] * (double)rY < (double)pY);
-  const bool need_pass = (residual != nullptr) || (residual_mass != nullptr) || (!acc && !bad_y);
-  if (!need_pass) {
+  if (d.acc || d.bad_y) {  // the same in every thread: the row is not read
     if (tid == 0) {
-      out_token[b] = bad_y ? -1 : Y;
-      accepted[b] = acc ? 1 : 0;
-      if (bad_y && row_status) row_status[b] |= y_ok ? kRowBadProb : kRowBadDraft;
+      out_token[b] = d.bad_y ? -1 : d.Y;
+      accepted[b] = d.acc ? 1 : 0;
+      if (d.bad_y && row_status) row_status[b] |= d.y_ok ? kRowBadProb : kRowBadDraft;
     }
     return;
   }
   if (tid == 0) s_bad = 0;
   __syncthreads();
   const int64_t nsuper = (V + kSuper - 1) / kSuper;
-  float* resb = residual ? residual + b * V : nullptr;
   int bad = 0;
-  // two super-tiles per wave and iteration: all 16 row loads are issued before any arithmetic
-  for (int64_t st0 = wid; st0 < nsuper; st0 += 2 * kAccWaves) {
-    float pv[2][4][4], rv[2][4][4];
+  // kAccRowHold super-tiles per wave and pass, all of their row loads issued before any
+  // arithmetic; the last pass's values stay in registers for the search below
+  float pv[kAccRowHold][4][4], rv[kAccRowHold][4][4];
+  for (int64_t st0 = wid; st0 < nsuper; st0 += kAccRowHold * kAccRowWaves) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int64_t st = st0 + h * kAccWaves;
+    for (int h = 0; h < kAccRowHold; ++h) {
+      const int64_t st = st0 + h * kAccRowWaves;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const int64_t x0 = st * kSuper + 256 * k + 4 * lane;
@@ -288,53 +390,252 @@ __global__ __launch_bounds__(kAccThreads) void accept_kernel(
       }
     }
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int64_t st = st0 + h * kAccWaves;
+    for (int h = 0; h < kAccRowHold; ++h) {
+      const int64_t st = st0 + h * kAccRowWaves;
       if (st >= nsuper) break;
       double local = 0.0;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int64_t x0 = st * kSuper + 256 * k + 4 * lane;
-        float rs[4];
+      for (int k = 0; k < 4; ++k)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           bad |= (int)(bad_prob(pv[h][k][i]) || bad_prob(rv[h][k][i]));
-          const double d = residual_of(pv[h][k][i], rv[h][k][i]);
-          rs[i] = (float)d;
-          local += d;
+          local += residual_of(pv[h][k][i], rv[h][k][i]);
         }
-        if (resb) {
-          if (kVec && x0 + 3 < V) {
-            typedef float f32x4v __attribute__((ext_vector_type(4)));
-            const f32x4v v = {rs[0], rs[1], rs[2], rs[3]};
-            __builtin_nontemporal_store(v, reinterpret_cast<f32x4v*>(resb + x0));
-          } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if (x0 + i < V) resb[x0 + i] = rs[i];
-          }
-        }
-      }
-      const double tot = wave_sum(local);
+      const double tot = wave_sum_dpp(local);
       if (lane == 0) s_tile[st] = tot;
     }
   }
   if (bad) atomicOr(&s_bad, 1);
   __syncthreads();
-  if (wid != 0) return;
-
-  // wave 0: totals, prefix over super-tiles, draw
+  // every wave: the totals and the prefix over the super-tiles (lane l takes a contiguous range)
   const bool row_bad = s_bad != 0;
   const int64_t per_lane = (nsuper + 63) / 64;
   const int64_t s_lo = lane * per_lane, s_hi = (s_lo + per_lane < nsuper) ? s_lo + per_lane : nsuper;
   double lane_sum = 0.0;
   for (int64_t s = s_lo; s < s_hi; ++s) lane_sum += s_tile[s];
-  const double incl = wave_inclusive_scan(lane_sum, lane);
+  const double incl = wave_inclusive_scan_dpp(lane_sum, lane);
   const double Z = __shfl(incl, 63, 64);
   double excl = __shfl_up(incl, 1, 64);
   if (lane == 0) excl = 0.0;
-  if (lane == 0 && residual_mass) residual_mass[b] = row_bad ? (double)NAN : Z;
+  if (row_bad || !(Z > 0.0)) {
+    if (wid == 0 && lane == 0) {
+      out_token[b] = row_bad ? -1 : d.Y;
+      accepted[b] = row_bad ? 0 : 1;
+      if (row_status) row_status[b] |= row_bad ? kRowBadProb : kRowForced;
+    }
+    return;
+  }
+  const double thr = (double)uu[2] * Z;
+  // first super-tile whose running sum exceeds thr
+  int64_t my_st = -1;
+  double my_prev = 0.0, run = excl;
+  for (int64_t s = s_lo; s < s_hi; ++s) {
+    const double prev = run;
+    run += s_tile[s];
+    if (run > thr) {
+      my_st = s;
+      my_prev = prev;
+      break;
+    }
+  }
+  const unsigned long long hit = __builtin_amdgcn_ballot_w64(my_st >= 0);
+  int64_t st_star;
+  double base;
+  if (hit) {
+    const int src = __ffsll((long long)hit) - 1;
+    st_star = __shfl(my_st, src, 64);
+    base = __shfl(my_prev, src, 64);
+  } else {
+    // rounding put u_res * Z at or past every running sum: the last super-tile with mass
+    int64_t last = -1;
+    for (int64_t s = s_lo; s < s_hi; ++s)
+      if (s_tile[s] > 0.0) last = s;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const int64_t o = __shfl_xor(last, off, 64);
+      last = o > last ? o : last;
+    }
+    st_star = last;
+    base = thr;  // forces the in-tile search to its own fallback
+  }
+  if (st_star < 0) {  // unreachable with Z > 0; keeps every load in bounds
+    if (wid == 0 && lane == 0) {
+      out_token[b] = d.Y;
+      accepted[b] = 1;
+      if (row_status) row_status[b] |= kRowForced;
+    }
+    return;
+  }
+  // the wave whose registers hold super-tile st_star searches it; a super-tile of an
+  // earlier pass (rows past 32768 tokens) is re-read by wave 0
+  const int owner = (int)(st_star % kAccRowWaves);
+  const int64_t own0 = owner + kAccRowHold * kAccRowWaves * ((nsuper - 1 - owner) / (kAccRowHold * kAccRowWaves));
+  const int64_t hh = (st_star - own0) / kAccRowWaves;  // which of the owner's last-pass super-tiles
+  const bool in_regs = st_star >= own0 && hh < kAccRowHold;
+  if (wid != (in_regs ? owner : 0)) return;
+  float ps[4][4], rs32[4][4];
+  if (in_regs) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float a = pv[0][k][i], c = rv[0][k][i];
+#pragma unroll
+        for (int h = 1; h < kAccRowHold; ++h) {
+          a = (hh == h) ? pv[h][k][i] : a;
+          c = (hh == h) ? rv[h][k][i] : c;
+        }
+        ps[k][i] = a;
+        rs32[k][i] = c;
+      }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t x0 = st_star * kSuper + 256 * k + 4 * lane;
+      load4<kVec>(pb, x0, V, ps[k]);
+      load4<kVec>(rb, x0, V, rs32[k]);
+    }
+  }
+  int64_t found = -1;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (found >= 0) break;  // uniform
+    double rs[4], local = 0.0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      rs[i] = residual_of(ps[k][i], rs32[k][i]);
+      local += rs[i];
+    }
+    const double li = wave_inclusive_scan_dpp(local, lane);
+    double le = __shfl_up(li, 1, 64);
+    if (lane == 0) le = 0.0;
+    double c = base + le;
+    int my = -1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      c += rs[i];
+      if (my < 0 && rs[i] > 0.0 && c > thr) my = i;
+    }
+    const unsigned long long h2 = __builtin_amdgcn_ballot_w64(my >= 0);
+    if (h2) {
+      const int src = __ffsll((long long)h2) - 1;
+      found = st_star * kSuper + 256 * k + 4 * src + __shfl(my, src, 64);
+    } else {
+      base += __shfl(li, 63, 64);
+    }
+  }
+  if (found < 0) {
+    // fallback: the last token of the super-tile with a positive residual
+    int64_t last = -1;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t x0 = st_star * kSuper + 256 * k + 4 * lane;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (x0 + i < V && residual_of(ps[k][i], rs32[k][i]) > 0.0) last = x0 + i;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const int64_t o = __shfl_xor(last, off, 64);
+      last = o > last ? o : last;
+    }
+    found = last;
+  }
+  if (lane == 0) {
+    out_token[b] = (int32_t)found;
+    accepted[b] = 0;
+  }
+}
 
+// Segment form (A).
+template <bool kVec>
+__global__ __launch_bounds__(kAccSegThreads) void accept_seg_kernel(const float* __restrict__ p,
+                                                                    const float* __restrict__ r, int64_t V,
+                                                                    float* __restrict__ residual, AccWork aw) {
+  const int64_t b = blockIdx.y;
+  const int64_t seg = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const float* pb = p + b * V;
+  const float* rb = r + b * V;
+  // the segment's sub-tiles: wave w takes kAccSubPerWave consecutive ones, all loads issued first
+  const int64_t sub0 = seg * (kAccSeg / kAccSub) + wid * kAccSubPerWave;
+  float pv[kAccSubPerWave][4], rv[kAccSubPerWave][4];
+#pragma unroll
+  for (int k = 0; k < kAccSubPerWave; ++k) {
+    const int64_t x0 = (sub0 + k) * kAccSub + 4 * lane;
+    load4<kVec>(pb, x0, V, pv[k]);  // tokens at or past V read as 0
+    load4<kVec>(rb, x0, V, rv[k]);
+  }
+  float* resb = residual ? residual + b * V : nullptr;
+  double sums[kAccSubPerWave];
+#pragma unroll
+  for (int k = 0; k < kAccSubPerWave; ++k) {
+    const int64_t x0 = (sub0 + k) * kAccSub + 4 * lane;
+    float rs[4];
+    double local = 0.0;
+    bool bad = false;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      bad |= bad_prob(pv[k][i]) || bad_prob(rv[k][i]);
+      const double dd = residual_of(pv[k][i], rv[k][i]);
+      rs[i] = (float)dd;
+      local += dd;
+    }
+    if (resb && x0 < V) {
+      if (kVec && x0 + 3 < V) {
+        typedef float f32x4v __attribute__((ext_vector_type(4)));
+        const f32x4v v = {rs[0], rs[1], rs[2], rs[3]};
+        __builtin_nontemporal_store(v, reinterpret_cast<f32x4v*>(resb + x0));
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (x0 + i < V) resb[x0 + i] = rs[i];
+      }
+    }
+    const double tot = wave_sum_dpp(local);
+    sums[k] = (__builtin_amdgcn_ballot_w64(bad) != 0) ? (double)NAN : tot;
+  }
+  double v = sums[0];
+#pragma unroll
+  for (int k = 1; k < kAccSubPerWave; ++k) v = (lane == k) ? sums[k] : v;
+  if (lane < kAccSubPerWave && sub0 + lane < aw.nsub) aw.sub[b * aw.nsub + sub0 + lane] = v;
+}
+
+// Segment form (B): one wave per position.
+template <bool kVec, bool kSel>
+__global__ __launch_bounds__(kAccThreads) void accept_draw_kernel(
+    const float* __restrict__ p, const float* __restrict__ r, const int32_t* __restrict__ sel_token,
+    const float* __restrict__ u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
+    int32_t* __restrict__ out_token, uint8_t* __restrict__ accepted, double* __restrict__ residual_mass,
+    int32_t* __restrict__ row_status, SelArgs sel, AccWork aw) {
+  const int lane = threadIdx.x & 63;
+  const int64_t b = (int64_t)blockIdx.x * kAccRowsPerDraw + (threadIdx.x >> 6);
+  if (b >= B) return;
+  const float* pb = p + b * V;
+  const float* rb = r + b * V;
+  const double* sb = aw.sub + b * aw.nsub;
+  // Z and the running sums: lane l takes the sub-tiles [l per, (l + 1) per), in order,
+  // read together with the decision's loads
+  const int64_t per = (aw.nsub + 63) / 64;
+  const int64_t s_lo = lane * per, s_hi = (s_lo + per < aw.nsub) ? s_lo + per : aw.nsub;
+  double lane_sum = 0.0;
+  for (int64_t s = s_lo; s < s_hi; ++s) lane_sum += sb[s];
+  float uu[3];
+  position_uniforms(u, seed, offset, b, uu);
+  const Decision d = take_decision<kSel>(pb, rb, sel_token, sel, b, V, uu);
+  if (kSel && lane == 0) {
+    if (sel.sel_index) sel.sel_index[b] = d.istar;
+    if (sel.sel_token) sel.sel_token[b] = d.Y;
+    if (d.st && row_status) row_status[b] |= d.st;
+  }
+  const int32_t Y = d.Y;
+  const bool acc = d.acc, bad_y = d.bad_y, y_ok = d.y_ok;
+  const bool row_bad = __builtin_amdgcn_ballot_w64(lane_sum != lane_sum) != 0;  // a NaN sub-tile sum
+  const double incl = wave_inclusive_scan_dpp(lane_sum, lane);
+  const double Z = __shfl(incl, 63, 64);
+  double excl = __shfl_up(incl, 1, 64);  // the running sum before this lane's sub-tiles
+  if (lane == 0) excl = 0.0;
+  if (lane == 0 && residual_mass) residual_mass[b] = row_bad ? (double)NAN : Z;
   if (row_bad || bad_y) {
     if (lane == 0) {
       out_token[b] = -1;
@@ -359,40 +660,39 @@ __global__ __launch_bounds__(kAccThreads) void accept_kernel(
     return;
   }
   const double thr = (double)uu[2] * Z;
-  // first super-tile whose running sum exceeds thr
-  int64_t my_st = -1;
+  // first sub-tile whose running sum exceeds thr
+  int64_t my_s = -1;
   double my_prev = 0.0, run = excl;
   for (int64_t s = s_lo; s < s_hi; ++s) {
     const double prev = run;
-    run += s_tile[s];
+    run += sb[s];
     if (run > thr) {
-      my_st = s;
+      my_s = s;
       my_prev = prev;
       break;
     }
   }
-  const unsigned long long hit = __ballot(my_st >= 0);
-  int64_t st_star;
-  double prev_star;
+  const unsigned long long hit = __builtin_amdgcn_ballot_w64(my_s >= 0);
+  int64_t s_star;
+  double base;
   if (hit) {
     const int src = __ffsll((long long)hit) - 1;
-    st_star = __shfl(my_st, src, 64);
-    prev_star = __shfl(my_prev, src, 64);
+    s_star = __shfl(my_s, src, 64);
+    base = __shfl(my_prev, src, 64);
   } else {
-    // rounding put u_res * Z at or past every running sum: last super-tile with mass
+    // rounding put u_res * Z at or past every running sum: the last sub-tile with mass
     int64_t last = -1;
     for (int64_t s = s_lo; s < s_hi; ++s)
-      if (s_tile[s] > 0.0) last = s;
-    int64_t m = last;
+      if (sb[s] > 0.0) last = s;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
-      const int64_t o = __shfl_xor(m, off, 64);
-      m = o > m ? o : m;
+      const int64_t o = __shfl_xor(last, off, 64);
+      last = o > last ? o : last;
     }
-    st_star = m;
-    prev_star = thr;  // forces the in-tile search to its own fallback
+    s_star = last;
+    base = thr;  // forces the in-tile search to its own fallback
   }
-  if (st_star < 0) {  // unreachable with Z > 0; keeps every load in bounds
+  if (s_star < 0) {  // unreachable with Z > 0; keeps every load in bounds
     if (lane == 0) {
       out_token[b] = Y;
       accepted[b] = 1;
@@ -400,63 +700,47 @@ __global__ __launch_bounds__(kAccThreads) void accept_kernel(
     }
     return;
   }
-  // locate the token inside super-tile st_star (its four sub-tiles loaded at once)
-  double base = prev_star;
-  int32_t found = -1;
-  float pvs[4][4], rvs[4][4];
+  // the token inside sub-tile s_star: 4 entries per lane, lane prefix, then the lane's own entries
+  const int64_t x0 = s_star * kAccSub + 4 * lane;
+  float pv[4], rv[4];
+  load4<kVec>(pb, x0, V, pv);
+  load4<kVec>(rb, x0, V, rv);
+  double rs[4], local = 0.0;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int64_t x0 = st_star * kSuper + 256 * k + 4 * lane;
-    load4<kVec>(pb, x0, V, pvs[k]);
-    load4<kVec>(rb, x0, V, rvs[k]);
+  for (int i = 0; i < 4; ++i) {
+    rs[i] = residual_of(pv[i], rv[i]);
+    local += rs[i];
   }
+  const double li = wave_inclusive_scan_dpp(local, lane);
+  double le = __shfl_up(li, 1, 64);
+  if (lane == 0) le = 0.0;
+  double c = base + le;
+  int my = -1;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if (found >= 0) break;  // uniform
-    double rs[4], local = 0.0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      rs[i] = residual_of(pvs[k][i], rvs[k][i]);
-      local += rs[i];
-    }
-    const double li = wave_inclusive_scan(local, lane);
-    double le = __shfl_up(li, 1, 64);
-    if (lane == 0) le = 0.0;
-    double c = base + le;
-    int my = -1;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      c += rs[i];
-      if (my < 0 && rs[i] > 0.0 && c > thr) my = i;
-    }
-    const unsigned long long h2 = __ballot(my >= 0);
-    if (h2) {
-      const int src = __ffsll((long long)h2) - 1;
-      const int mi = __shfl(my, src, 64);
-      found = (int32_t)(st_star * kSuper + 256 * k + 4 * src + mi);
-    } else {
-      base += __shfl(li, 63, 64);
-    }
+  for (int i = 0; i < 4; ++i) {
+    c += rs[i];
+    if (my < 0 && rs[i] > 0.0 && c > thr) my = i;
   }
-  if (found < 0) {
-    // fallback: last token of the super-tile with positive residual
+  const unsigned long long h2 = __builtin_amdgcn_ballot_w64(my >= 0);
+  int64_t found;
+  if (h2) {
+    const int src = __ffsll((long long)h2) - 1;
+    found = s_star * kAccSub + 4 * src + __shfl(my, src, 64);
+  } else {
+    // fallback: the last token of the sub-tile with a positive residual
     int64_t last = -1;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int64_t x0 = st_star * kSuper + 256 * k + 4 * lane;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (x0 + i < V && residual_of(pvs[k][i], rvs[k][i]) > 0.0) last = x0 + i;
-    }
+    for (int i = 0; i < 4; ++i)
+      if (x0 + i < V && rs[i] > 0.0) last = x0 + i;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
       const int64_t o = __shfl_xor(last, off, 64);
       last = o > last ? o : last;
     }
-    found = (int32_t)last;
+    found = last;
   }
   if (lane == 0) {
-    out_token[b] = found;
+    out_token[b] = (int32_t)found;
     accepted[b] = 0;
   }
 }
@@ -489,43 +773,68 @@ hipError_t launch_select_pair(const float* p, const float* q1, const float* q2, 
 
 namespace {
 
+size_t align256_acc(size_t x) { return (x + 255) / 256 * 256; }
+
 template <bool kSel>
 hipError_t launch_accept_impl(const float* p, const float* r, const int32_t* sel_token, const float* u,
                               uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t* out_token,
                               uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
-                              const SelArgs& sel, hipStream_t st) {
-  const int64_t nsuper = (V + kSuper - 1) / kSuper;
-  const size_t lds = sizeof(double) * (size_t)nsuper;
+                              const SelArgs& sel, void* workspace, hipStream_t st) {
   const bool vec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(r) |
                                      reinterpret_cast<uintptr_t>(residual)) % 16 == 0);
+  if (residual == nullptr && residual_mass == nullptr) {  // row form: only rejected positions read their rows
+    const size_t lds = sizeof(double) * (size_t)((V + kSuper - 1) / kSuper);
+    if (vec) {
+      hipLaunchKernelGGL((accept_row_kernel<true, kSel>), dim3((unsigned)B), dim3(kAccRowThreads), lds, st, p, r,
+                         sel_token, u, seed, offset, V, out_token, accepted, row_status, sel);
+    } else {
+      hipLaunchKernelGGL((accept_row_kernel<false, kSel>), dim3((unsigned)B), dim3(kAccRowThreads), lds, st, p, r,
+                         sel_token, u, seed, offset, V, out_token, accepted, row_status, sel);
+    }
+    return hipGetLastError();
+  }
+  AccWork aw;
+  aw.sub = static_cast<double*>(workspace);
+  aw.nsub = (V + kAccSub - 1) / kAccSub;
+  const int64_t nseg = (V + kAccSeg - 1) / kAccSeg;
+  const dim3 ga((unsigned)nseg, (unsigned)B);
+  const dim3 gb((unsigned)((B + kAccRowsPerDraw - 1) / kAccRowsPerDraw));
   if (vec) {
-    hipLaunchKernelGGL((accept_kernel<true, kSel>), dim3((unsigned)B), dim3(kAccThreads), lds, st, p, r, sel_token, u,
-                       seed, offset, V, out_token, accepted, residual, residual_mass, row_status, sel);
+    hipLaunchKernelGGL((accept_seg_kernel<true>), ga, dim3(kAccSegThreads), 0, st, p, r, V, residual, aw);
+    hipLaunchKernelGGL((accept_draw_kernel<true, kSel>), gb, dim3(kAccThreads), 0, st, p, r, sel_token, u, seed,
+                       offset, B, V, out_token, accepted, residual_mass, row_status, sel, aw);
   } else {
-    hipLaunchKernelGGL((accept_kernel<false, kSel>), dim3((unsigned)B), dim3(kAccThreads), lds, st, p, r, sel_token,
-                       u, seed, offset, V, out_token, accepted, residual, residual_mass, row_status, sel);
+    hipLaunchKernelGGL((accept_seg_kernel<false>), ga, dim3(kAccSegThreads), 0, st, p, r, V, residual, aw);
+    hipLaunchKernelGGL((accept_draw_kernel<false, kSel>), gb, dim3(kAccThreads), 0, st, p, r, sel_token, u, seed,
+                       offset, B, V, out_token, accepted, residual_mass, row_status, sel, aw);
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
+size_t workspace_bytes_accept(int64_t B, int64_t V) {
+  const int64_t nsub = (V + kAccSub - 1) / kAccSub;
+  return align256_acc(sizeof(double) * (size_t)(B * nsub));
+}
+
 hipError_t launch_accept(const float* p, const float* r, const int32_t* sel_token, const float* u, uint64_t seed,
                          uint64_t offset, int64_t B, int64_t V, int32_t* out_token, uint8_t* accepted,
-                         float* residual, double* residual_mass, int32_t* row_status, hipStream_t st) {
+                         float* residual, double* residual_mass, int32_t* row_status, void* workspace,
+                         hipStream_t st) {
   const SelArgs none = {nullptr, nullptr, nullptr, 0, nullptr, nullptr};
   return launch_accept_impl<false>(p, r, sel_token, u, seed, offset, B, V, out_token, accepted, residual,
-                                   residual_mass, row_status, none, st);
+                                   residual_mass, row_status, none, workspace, st);
 }
 
 hipError_t launch_select_accept(const float* p, const float* q, const float* q2, const float* r,
                                 const int32_t* drafts, const float* u, uint64_t seed, uint64_t offset, int64_t B,
                                 int64_t V, int K, int32_t* sel_index, int32_t* sel_token, int32_t* out_token,
                                 uint8_t* accepted, float* residual, double* residual_mass, int32_t* row_status,
-                                hipStream_t st) {
+                                void* workspace, hipStream_t st) {
   const SelArgs sel = {q, q2, drafts, K, sel_index, sel_token};
   return launch_accept_impl<true>(p, r, nullptr, u, seed, offset, B, V, out_token, accepted, residual,
-                                  residual_mass, row_status, sel, st);
+                                  residual_mass, row_status, sel, workspace, st);
 }
 
 }  // namespace mdss

@@ -73,21 +73,31 @@ def test_select_and_accept_argument_errors(lib):
     assert s(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 1, FAKE, FAKE, None, None) == 3
     assert s(FAKE, FAKE, FAKE, None, 0, 0, -1, 16, 2, FAKE, FAKE, None, None) == 2
     a = lib.mdss_accept_or_resample
-    assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, None, FAKE, None, None, None, None) == 1
-    assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 1, FAKE, FAKE, None, None, None, None) == 2
+    wsb = lib.mdss_workspace_bytes_accept(4, 16)
+    assert wsb > 0 and lib.mdss_workspace_bytes_accept(0, 16) == 0 and lib.mdss_workspace_bytes_accept(4, 1) == 0
+    assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, None, FAKE, None, None, None, FAKE, wsb, None) == 1
+    assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 1, FAKE, FAKE, None, None, None, FAKE, wsb, None) == 2
+    assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, FAKE, FAKE, None, None, None, None, wsb, None) == 5
+    assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, FAKE, FAKE, None, None, None, FAKE, wsb - 1, None) == 5
+    assert a(FAKE, FAKE, FAKE, None, 0, 0, 4, 16, FAKE, FAKE, None, None, None, ctypes.c_void_p(0x1010), wsb,
+             None) == 5  # misaligned
     # the fused form: sel_index, sel_token, residual, mass and row_status may be NULL
     f = lib.mdss_select_accept
-    assert f(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 2, None, None, FAKE, FAKE, None, None, None, None) == 1
-    assert f(FAKE, FAKE, FAKE, None, None, 0, 0, 4, 16, 2, None, None, FAKE, FAKE, None, None, None, None) == 1
-    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 2, None, None, None, FAKE, None, None, None, None) == 1
-    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 9, None, None, FAKE, FAKE, None, None, None, None) == 3
-    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 1, None, None, FAKE, FAKE, None, None, None, None) == 3
-    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 1, 2, None, None, FAKE, FAKE, None, None, None, None) == 2
+    W = (FAKE, wsb, None)
+    assert f(FAKE, FAKE, None, FAKE, None, 0, 0, 4, 16, 2, None, None, FAKE, FAKE, None, None, None, *W) == 1
+    assert f(FAKE, FAKE, FAKE, None, None, 0, 0, 4, 16, 2, None, None, FAKE, FAKE, None, None, None, *W) == 1
+    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 2, None, None, None, FAKE, None, None, None, *W) == 1
+    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 9, None, None, FAKE, FAKE, None, None, None, *W) == 3
+    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 1, None, None, FAKE, FAKE, None, None, None, *W) == 3
+    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 1, 2, None, None, FAKE, FAKE, None, None, None, *W) == 2
+    assert f(FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, 2, None, None, FAKE, FAKE, None, None, None, None, wsb,
+             None) == 5
     g = lib.mdss_select_accept_pair
-    assert g(FAKE, FAKE, None, FAKE, FAKE, None, 0, 0, 4, 16, None, None, FAKE, FAKE, None, None, None, None) == 1
-    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, None, None, FAKE, None, None, None, None, None) == 1
-    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 0, -1, 16, None, None, FAKE, FAKE, None, None, None, None) == 2
-
+    assert g(FAKE, FAKE, None, FAKE, FAKE, None, 0, 0, 4, 16, None, None, FAKE, FAKE, None, None, None, *W) == 1
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, None, None, FAKE, None, None, None, None, *W) == 1
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 0, -1, 16, None, None, FAKE, FAKE, None, None, None, *W) == 2
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 0, 4, 16, None, None, FAKE, FAKE, None, None, None, FAKE, 8,
+             None) == 5
 
 def test_python_binding_refuses_cpu_tensors():
     import torch
@@ -204,10 +214,10 @@ def test_empty_batch_is_a_no_op(lib):
     assert lib.mdss_induced_dist_pair(N, N, N, 0, 16, N, N, N, 0, N) == 0
     assert lib.mdss_select_intermediate(N, N, N, N, 0, 0, 0, 16, 2, N, N, N, N) == 0
     assert lib.mdss_select_intermediate_pair(N, N, N, N, N, 0, 0, 0, 16, N, N, N, N) == 0
-    assert lib.mdss_accept_or_resample(N, N, N, N, 0, 0, 0, 16, N, N, N, N, N, N) == 0
-    assert lib.mdss_select_accept(N, N, N, N, N, 0, 0, 0, 16, 2, N, N, N, N, N, N, N, N) == 0
-    assert lib.mdss_select_accept(N, N, N, N, N, 0, 0, 0, 16, 9, N, N, N, N, N, N, N, N) == 3
-    assert lib.mdss_select_accept_pair(N, N, N, N, N, N, 0, 0, 0, 16, N, N, N, N, N, N, N, N) == 0
+    assert lib.mdss_accept_or_resample(N, N, N, N, 0, 0, 0, 16, N, N, N, N, N, N, 0, N) == 0
+    assert lib.mdss_select_accept(N, N, N, N, N, 0, 0, 0, 16, 2, N, N, N, N, N, N, N, N, 0, N) == 0
+    assert lib.mdss_select_accept(N, N, N, N, N, 0, 0, 0, 16, 9, N, N, N, N, N, N, N, N, 0, N) == 3
+    assert lib.mdss_select_accept_pair(N, N, N, N, N, N, 0, 0, 0, 16, N, N, N, N, N, N, N, N, 0, N) == 0
     assert lib.mdss_induced_dist_successive(N, N, 0, 16, 3, N, N, N, 0, N) == 0
     assert lib.mdss_induced_dist_successive(N, N, 0, 16, 9, N, N, N, 0, N) == 3
     assert lib.mdss_select_successive(N, N, N, N, N, 0, 0, 0, 16, 3, N, N, N, N) == 0

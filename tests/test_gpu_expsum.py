@@ -90,7 +90,7 @@ def test_lp_instances_small_vocab():
 
 
 # ------------------------------------------------------------------ full sizes
-@pytest.mark.parametrize("name", ["llm32k", "batch50k", "zipf128k", "k3top1024"])
+@pytest.mark.parametrize("name", ["llm32k", "batch50k", "zipf128k", "k3top1024", "cold32k"])
 def test_full_size(name):
     cfg = CONFIGS[name]
     w = generate(name)
@@ -166,6 +166,38 @@ def test_pair_small_rows():
     rk, _ = es_r(p, q1, 2)
     ro2, _ = oracle.induced_dist(p, q1, 2)
     assert np.all(rel_l1(ri, ro2) <= TIGHT) and np.all(rel_l1(rk, ro2) <= TIGHT)
+
+
+def test_denormal_drafts_stay_in_fp32():
+    # a draft at temperature 0.3 (cold32k): 114 of the 256 rows hold draft probabilities
+    # below the fp32 normal range, with weights p / q up to 3e31 (inside the fp32 range).
+    # Their reciprocals would overflow, so their ratios are taken with q scaled up, which
+    # keeps these tiles on the fp32 path; every row meets the bar against the oracle on
+    # sampled entries (largest-r tokens, the denormal-q tokens themselves, random support
+    # tokens).
+    w = generate("cold32k")
+    p, q = w["p"], w["q"]
+    tiny = np.finfo(np.float32).tiny
+    den = (q > 0) & (q < tiny)
+    assert den.any(1).sum() >= 100
+    r, st = es_r(p, q, 2)
+    assert np.all(st == 0)
+    mass_q = q.astype(np.float64).sum(1) ** 2
+    assert np.all(np.abs(r.astype(np.float64).sum(1) - mass_q) / mass_q <= TIGHT)
+    rng = np.random.default_rng(303)
+    rows, ys = [], []
+    for b in np.flatnonzero(den.any(1))[:40]:
+        for y in np.flatnonzero(den[b])[:3]:
+            rows.append(b)
+            ys.append(y)
+        rows.append(b)
+        ys.append(int(np.argmax(r[b])))
+        rows.append(b)
+        ys.append(int(rng.choice(np.flatnonzero(q[b] > 0))))
+    rows, ys = np.array(rows), np.array(ys)
+    e = oracle.induced_dist_entries(p, q, 2, rows, ys)
+    got = r[rows, ys].astype(np.float64)
+    assert np.all(np.abs(got - e) <= RTOL_ROW * e), np.max(np.abs(got - e) / e)
 
 
 def test_pair32k_full_size():

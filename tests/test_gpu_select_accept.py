@@ -154,8 +154,9 @@ def test_fused_nullable_selection_outputs():
     acc = torch.empty(B, dtype=torch.uint8, device=DEV)
     st = torch.zeros(B, dtype=torch.int32, device=DEV)
     P_ = lambda t: ctypes.c_void_p(t.data_ptr())
+    ws = torch.empty(mdss.workspace_bytes_accept(B, V), dtype=torch.uint8, device=DEV)
     code = lib.mdss_select_accept(P_(p), P_(q), P_(r), P_(d), P_(uu), ctypes.c_uint64(0), ctypes.c_uint64(0), B, V,
-                                  K, None, None, P_(out), P_(acc), None, None, P_(st),
+                                  K, None, None, P_(out), P_(acc), None, None, P_(st), P_(ws), ws.numel(),
                                   ctypes.c_void_p(torch.cuda.current_stream(DEV).cuda_stream))
     assert code == 0
     torch.cuda.synchronize()

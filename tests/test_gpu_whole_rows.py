@@ -30,7 +30,9 @@ from workloads import CONFIGS, generate
 pytestmark = pytest.mark.gpu
 
 # rows taken whole by the oracle, spread over the batch (first and last included)
-ROWS = {"llm32k": [0, 31, 77, 128, 170, 200, 231, 255], "batch50k": [0, 1023], "zipf128k": [511], "k3top1024": [0, 1]}
+ROWS = {"llm32k": [0, 31, 77, 128, 170, 200, 231, 255], "batch50k": [0, 1023], "zipf128k": [511], "k3top1024": [0, 1],
+        # draft at temperature 0.3: rows 0 and 4 hold 0 and 6 draft probabilities below the fp32 normal range
+        "cold32k": [0, 4, 255]}
 BAR = {"exact": 1e-5, "expsum": 2e-6}
 
 

@@ -76,6 +76,15 @@ def _row_gauss(sigma: float, noise: float, temp: float):
     return f
 
 
+def _row_gauss_temps(sigma: float, noise: float, t_target: float, t_draft: float):
+    """Target softmax(l / t_target), draft softmax((l + e) / t_draft), l ~ N(0, sigma^2), e ~ N(0, noise^2)."""
+    def f(cfg: Config, b: int):
+        ell = _rng(cfg.seed, _S_LOGIT, b).normal(0.0, sigma, cfg.V)
+        eps = _rng(cfg.seed, _S_NOISE, b).normal(0.0, noise, cfg.V)
+        return _softmax64(ell / t_target), _softmax64((ell + eps) / t_draft)
+    return f
+
+
 def _row_zipf(cfg: Config, b: int):
     k = np.arange(1, cfg.V + 1, dtype=np.float64)
     mass = k ** -1.1
@@ -151,6 +160,10 @@ CONFIGS: Dict[str, Config] = {
         Config("maxbatch", 1008, 65535, 16, 2,
                "the largest accepted batch: 65535 positions, V=16, K=2, p and q independent Dirichlet(0.5)",
                _row_dirichlet),
+        Config("cold32k", 1009, 256, 32000, 2,
+               "V=32000, K=2, 256 positions, logits N(0,3^2), target T=1, draft softmax((logits + N(0,1)) / 0.3): "
+               "a draft at temperature 0.3 puts the far tail of q below the fp32 normal range",
+               _row_gauss_temps(3.0, 1.0, 1.0, 0.3)),
         Config("tlp_llm32k", 1002, 256, 32000, 2,
                "truncated LP (Algorithm 2), s = 5, sorted Omega_2, identical drafts, on the llm32k rows",
                _row_gauss(3.0, 1.0, 1.0), tlp_s=5),
