@@ -47,19 +47,23 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def counted_traffic(workload: str, kernel: str, digest: str):
-    """HBM bytes per launch from the committed PMC summary of this workload, only if
-    it was taken on the current kernel sources (else None)."""
+def counted_traffic(workload: str, kernels, digest: str):
+    """HBM bytes per launch of a call (the sum over its kernels) from the committed PMC
+    summary of this workload, only if every figure was taken on the current kernel
+    sources (else None)."""
     path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
     try:
         with open(path) as fh:
             d = json.load(fh)
     except (OSError, ValueError):
         return None
-    e = d.get(workload, {}).get(kernel)
-    if not e or e.get("source_digest") != digest:
-        return None
-    return e.get("bytes_per_launch")
+    total = 0
+    for kernel in ([kernels] if isinstance(kernels, str) else kernels):
+        e = d.get(workload, {}).get(kernel)
+        if not e or e.get("source_digest") != digest:
+            return None
+        total += e.get("bytes_per_launch")
+    return total
 
 
 def pair_flops(q_np, K: int, q2_np=None) -> float:
@@ -450,7 +454,8 @@ def main():
                "mdss_induced_dist_pair_expsum" if cfg.pair else "mdss_induced_dist_expsum")
         roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS,
                     "unit": "TFLOP/s", "frac": round(achieved / FP32_PEAK_TFLOPS, 4),
-                    "traffic": counted_traffic(cfg.name, "es_moments_kernel", digest),
+                    "traffic": counted_traffic(cfg.name, ["es_moments_kernel", f"es_coef_kernel<{2 if cfg.pair else 1}>",
+                                                          f"es_eval_kernel<{2 if cfg.pair else 1}>"], digest),
                     "kernel": f"{api} (es_moments_kernel + es_coef_kernel + es_eval_kernel"
                               f"{', per stage' if stages > 1 else ''})",
                     "avg_ms": round(r_ms, 4), "flops_per_launch": flops,
@@ -550,8 +555,11 @@ def main():
     del bufs
     res_gbs = res_bytes / (res_ms * 1e-3) / 1e9
     res_gbs_hot = res_bytes / (res_ms_hot * 1e-3) / 1e9
+    # L2 fetch and write bytes do not depend on where the line comes from (Infinity Cache or HBM):
+    # the counted figure of the same kernels serves both placements
+    res_traffic = counted_traffic(cfg.name, ["accept_seg_kernel<true>", "accept_draw_kernel<true, false>"], digest)
     roofline_resample = {"bound": "hbm", "achieved": round(res_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": round(res_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                         "frac": round(res_gbs / HBM_PEAK_GBS, 4), "traffic": res_traffic,
                          "kernel": "mdss_accept_or_resample (accept_seg_kernel + accept_draw_kernel), residual and mass written for "
                                    "every row",
                          "avg_ms": round(res_ms, 4), "bytes_per_launch": res_bytes,
@@ -559,7 +567,7 @@ def main():
                                     "taken in turn: every launch misses the 256 MB Infinity Cache",
                          "cache_resident": {"avg_ms": round(res_ms_hot, 4), "achieved": round(res_gbs_hot, 1),
                                             "frac": round(res_gbs_hot / HBM_PEAK_GBS, 4),
-                                            "traffic": counted_traffic(cfg.name, "accept_kernel", digest),
+                                            "traffic": res_traffic,
                                             "note": "the step's own buffers, %.1f MB per launch: %s the 256 MB "
                                                     "Infinity Cache" % (res_bytes / 1e6, "fit in" if res_bytes < 256e6
                                                                         else "exceed")}}

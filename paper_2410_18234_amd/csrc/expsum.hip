@@ -92,7 +92,8 @@ struct alignas(64) EsTile {
   int32_t kt;    // last node taken by the expansion; the window is kt + 1 .. kt + nw
   int32_t nw;    // window length (0: no positive weight)
   int32_t wide;  // 1: the moments are taken in fp64 (by the coefficient kernel)
-  int32_t pad[3];
+  int32_t small; // 1: a positive-weight token has a draft probability below the fp32 normal range
+  int32_t pad[2];
 };
 
 // Per row.
@@ -467,7 +468,8 @@ __device__ void es_moments_tile(const float* __restrict__ pb, const float* __res
     o.kt = 0;
     o.nw = 0;
     o.wide = 1;
-    o.pad[0] = o.pad[1] = o.pad[2] = 0;
+    o.small = 0;
+    o.pad[0] = o.pad[1] = 0;
     if (n > 0) es_window(wmin, wmax, o.kt, o.nw);
     *rec = o;
     s_dec[0] = o.kt;
@@ -827,29 +829,38 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
     // (1) ratios and statistics
     float wv[kEsMomPer];  // 0 for a token left out
     float wlo = INFINITY, whi = 0.0f;
-    bool anybad = false, anyzero = false, anysmall = false;
+    bool anyspec = false, anyzero = false;
     int npos = 0;
 #pragma unroll
     for (int i = 0; i < kEsMomPer; ++i) {
       const float pp = pv[i], qq = qv[i];
-      // NaN, -inf, negative normal or denormal, +inf (-0 is a zero probability)
-      anybad |= __builtin_amdgcn_classf(pp, 0x21F) | __builtin_amdgcn_classf(qq, 0x21F);
-      anysmall |= es_denormal(qq);
+      // NaN, -inf, negative normal or denormal, +inf (-0 is a zero probability); for q
+      // also a positive denormal (its ratio is taken below)
+      anyspec |= __builtin_amdgcn_classf(pp, 0x21F) | __builtin_amdgcn_classf(qq, 0x29F);
       const bool pos = pp > 0.0f && qq > 0.0f;
       anyzero |= qq > 0.0f && pp == 0.0f;
-      wv[i] = pos ? es_ratio<float>(pp, qq) : 0.0f;
-    }
-    if (__builtin_amdgcn_ballot_w64(anysmall) != 0) {  // uniform: a denormal draft probability in the wave
-#pragma unroll
-      for (int i = 0; i < kEsMomPer; ++i)
-        if (es_denormal(qv[i]) && pv[i] > 0.0f) wv[i] = es_ratio_small_q(pv[i], qv[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < kEsMomPer; ++i) {
-      const bool pos = pv[i] > 0.0f && qv[i] > 0.0f;
-      wlo = fminf(wlo, pos ? wv[i] : INFINITY);
-      whi = fmaxf(whi, wv[i]);  // w >= 0
+      const float w = pos ? es_ratio<float>(pp, qq) : 0.0f;
+      wv[i] = w;
+      wlo = fminf(wlo, pos ? w : INFINITY);
+      whi = fmaxf(whi, w);  // w >= 0
       npos += pos;
+    }
+    bool anybad = false, anysmall = false;
+    if (__builtin_amdgcn_ballot_w64(anyspec) != 0) {  // uniform and rare: a bad or a denormal probability
+      __asm__ volatile("");  // keeps this path a branch (not computed for every token and selected)
+      wlo = INFINITY;
+      whi = 0.0f;
+#pragma unroll
+      for (int i = 0; i < kEsMomPer; ++i) {
+        const float pp = pv[i], qq = qv[i];
+        anybad |= __builtin_amdgcn_classf(pp, 0x21F) | __builtin_amdgcn_classf(qq, 0x21F);
+        const bool small = es_denormal(qq) && pp > 0.0f;
+        anysmall |= small;
+        if (small) wv[i] = es_ratio_small_q(pp, qq);
+        const bool pos = pp > 0.0f && qq > 0.0f;
+        wlo = fminf(wlo, pos ? wv[i] : INFINITY);
+        whi = fmaxf(whi, wv[i]);
+      }
     }
     double q0w = 0.0;  // the draft mass on zero-weight tokens (p = 0 < q), in waves that hold one
     if (__builtin_amdgcn_ballot_w64(anyzero) != 0) {
@@ -861,7 +872,8 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
     wlo = es_wave_ext<false>(wlo);
     whi = es_wave_ext<true>(whi);
     npos = wave_sum_int(npos);
-    const bool bad = __builtin_amdgcn_ballot_w64(anybad) != 0;
+    const int bad = (__builtin_amdgcn_ballot_w64(anybad) != 0 ? 1 : 0) |
+                    (__builtin_amdgcn_ballot_w64(anysmall) != 0 ? 2 : 0);  // bit 1: a denormal draft probability
     if (lane == 0) {
       s_f[par][wid][0] = wlo;
       s_f[par][wid][1] = whi;
@@ -873,7 +885,7 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
     // every thread combines the same values in the same order
     float wmin = s_f[par][0][0], wmax = s_f[par][0][1];
     double q0 = s_q0[par][0];
-    int n = s_i[par][0][0], bd = s_i[par][0][1];
+    int n = s_i[par][0][0], bd = s_i[par][0][1], smallq;
 #pragma unroll
     for (int i = 1; i < kEsWaves; ++i) {
       wmin = fminf(wmin, s_f[par][i][0]);
@@ -882,6 +894,8 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
       n += s_i[par][i][0];
       bd |= s_i[par][i][1];
     }
+    smallq = (bd >> 1) & 1;
+    bd &= 1;
     int kt = 0, nw = 0, tau = 0, wide = 0;
     if (n > 0) {
       if (!(wmin >= __FLT_MIN__) || !(wmax <= __FLT_MAX__)) {  // a weight that is not an fp32 normal
@@ -909,7 +923,8 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
       o.kt = wide ? 0 : kt;
       o.nw = wide ? 0 : nw;
       o.wide = wide;
-      o.pad[0] = o.pad[1] = o.pad[2] = 0;
+      o.small = smallq;
+      o.pad[0] = o.pad[1] = 0;
       es.tile[g] = o;
     }
     if (bd || n == 0 || wide) {  // uniform; an fp64 tile is taken by the coefficient kernel
@@ -1234,7 +1249,7 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
   int64_t b = __builtin_amdgcn_readfirstlane((int)(g0 / es.T3));  // rows < 2^31
   int t = __builtin_amdgcn_readfirstlane((int)(g0 - b * es.T3));
   int64_t built = -1;  // moments record whose tables are in LDS (both halves of it share them)
-  int tau = 0, kt[2] = {0, 0}, D[2] = {-1, -1};
+  int tau = 0, kt[2] = {0, 0}, D[2] = {-1, -1}, smallq[2] = {0, 0};
   float pv[kEsTokPer], qv[L][kEsTokPer];
   es_load_eval<L>(p, q1, q2, V, b, t, tid, pv, qv);
   for (int64_t g = g0; g < g1; ++g) {
@@ -1281,6 +1296,7 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         const EsTile rec = es_sload_rec(es.tile + recno * L + l);
         wmin[l] = (float)rec.wmin;  // +inf / 0 when the law has no positive weight here
         wmax[l] = (float)rec.wmax;
+        smallq[l] = rec.small;
       }
       const float lo = fminf(wmin[0], wmin[L - 1]), hi = fmaxf(wmax[0], wmax[L - 1]);
       int range = 0;
@@ -1326,16 +1342,15 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
         int d[kEsTokPer];
         float x[kEsTokPer];
         float ratio[kEsTokPer];
-        bool small = false;
 #pragma unroll
         for (int i = 0; i < kEsTokPer; ++i) {
           // no short-circuit and the ratio for every token (its inf or NaN for q = 0 is
           // selected away): straight-line code, no branches per token
           ok[i] = (pc[i] > 0.0f) & (qc[l][i] > 0.0f);
           ratio[i] = es_ratio<float>(pc[i], qc[l][i]);
-          small |= es_denormal(qc[l][i]);
         }
-        if (__builtin_amdgcn_ballot_w64(small) != 0) {  // uniform: a denormal draft probability in the wave
+        if (smallq[l]) {  // uniform and rare: the moments record saw a denormal draft probability
+          __asm__ volatile("");  // keeps this path a branch
 #pragma unroll
           for (int i = 0; i < kEsTokPer; ++i)
             if (es_denormal(qc[l][i])) ratio[i] = es_ratio_small_q(pc[i], qc[l][i]);
