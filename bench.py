@@ -23,6 +23,7 @@ sys.path.insert(0, ROOT)
 FP32_PEAK_TFLOPS = 157.3  # MI355X fp32 vector peak (packed FMA: 4 FLOP per lane and cycle)
 FP32_NONPACKED_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12  # 78.6: one FMA per lane and cycle (packed fp32 is not built)
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E
+R_REPS = 10               # r calls per graph in the r timing
 # fp32 VALU issue without packed math: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3 T lane-instructions/s
 ES_PEAK_SLOTS = 256 * 4 * 16 * 2.4e9
 # Least work of the truncated quadrature per positive-weight token and law: the moments
@@ -260,12 +261,16 @@ def main():
     r = torch.empty_like(p)
     status = torch.zeros(B, dtype=torch.int32, device=dev)
     use_es = args.method == "expsum" and not (tlp_s or cfg.alphabet or cfg.diag)
+    # K >= 3 i.i.d. drafts from a top-s draft: the quadrature over each row's support
+    use_topk = use_es and K >= 3 and bool(s_max) and not (cfg.successive or cfg.pair)
     if use_es and (cfg.successive or cfg.pair):
         ws_bytes = mdss.workspace_bytes_pair_expsum(B, V)
         if cfg.successive:
             r_stages = torch.empty((K - 1, B, V), dtype=torch.float32, device=dev)
             r = r_stages[K - 2]
             u_sel = torch.from_numpy(np.ascontiguousarray(w["u"][:, :1].repeat(K - 1, 1))).to(dev)
+    elif use_topk:
+        ws_bytes = 0  # the top-s call takes no workspace
     elif use_es:
         ws_bytes = mdss.workspace_bytes_expsum(B, V, K)
     elif tlp_s:
@@ -288,6 +293,8 @@ def main():
                 mdss.induced_dist_successive_expsum(p, q, K, r_stages=r_stages, row_status=status, workspace=ws)
             elif cfg.pair:
                 mdss.induced_dist_pair_expsum(p, q, q2, r=r, row_status=status, workspace=ws)
+            elif use_topk:
+                mdss.induced_dist_topk_expsum(p, q, K, s_max, r=r, row_status=status)
             else:
                 mdss.induced_dist_expsum(p, q, K, r=r, row_status=status, workspace=ws)
         elif tlp_s:
@@ -371,6 +378,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     r_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    r_eager_ms = None
     ms_per_step = wall * 1e3 / args.steps
     timing = "eager launches, HIP events around r in every step"
     if not args.no_graph:
@@ -406,7 +414,23 @@ def main():
         wall = time.perf_counter() - t0
         ms_per_step = wall * 1e3 / args.steps
         out, acc = g_out, g_acc
-        timing = "one HIP graph per step (replays checked against the eager step); r by HIP events on eager steps"
+        # r alone without host launch gaps: a graph of R_REPS back-to-back r calls, HIP events around replays
+        r_graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(r_graph):
+            for _ in range(R_REPS):
+                induced()
+        r_graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            r_graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        r_eager_ms = r_ms
+        r_ms = e0.elapsed_time(e1) / (args.steps * R_REPS)
+        timing = ("one HIP graph per step (replays checked against the eager step); r by HIP events around "
+                  f"replays of a graph of {R_REPS} back-to-back r calls")
     assert int(status.abs().sum()) == 0, "rows flagged during the bench"
     if cfg.diag:
         pstar_t, achieved_t = out, acc
@@ -441,6 +465,18 @@ def main():
                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": counted_traffic(cfg.name, rank_name, digest),
                     "kernel": f"mdss_truncated_lp ({rank_name} + tlp_lp_kernel)", "avg_ms": round(r_ms, 4),
                     "bytes_per_launch": nbytes, "s": tlp_s, "tail": "sorted" if tail == 0 else "half"}
+    elif use_topk:
+        # HBM-bound by design: one pass reads p and q (8 B/token) and writes r (4 B/token)
+        nbytes = float(B) * V * 12
+        gbs = nbytes / (r_ms * 1e-3) / 1e9
+        ntok = expsum_positive_tokens(w["p"], w["q"])
+        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(gbs / HBM_PEAK_GBS, 4),
+                    "traffic": counted_traffic(cfg.name, ["es_topk_kernel"], digest),
+                    "kernel": "mdss_induced_dist_topk_expsum (es_topk_kernel)", "avg_ms": round(r_ms, 4),
+                    "bytes_per_launch": nbytes, "byte_basis": "p and q read once (8 B/token), r written once "
+                                                             "(4 B/token), every token of the row",
+                    "support_tokens_with_weight": ntok}
     elif use_es:
         stages = (K - 1) if cfg.successive else 1
         evals = expsum_evals(w["p"], w["q"], 2 if cfg.successive else K, w.get("q2"))
@@ -600,6 +636,7 @@ def main():
         "roofline_resample": roofline_resample,
         "method": "exponential-sum quadrature" if use_es else "exact pairwise sums",
         "timing": timing,
+        "r_eager_ms": None if r_eager_ms is None else round(r_eager_ms, 4),
         "exact_pairwise": exact_pairwise,
         "cpu_baseline": None,
         "kernel_source_digest": digest,

@@ -285,6 +285,23 @@ mdss_status mdss_induced_dist_expsum(const float* p, const float* q, int64_t B, 
 mdss_status mdss_induced_dist_expsum_noalloc(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
                                              float* r, int32_t* row_status, void* stream);
 
+/* r: [B][V] fp32 out, the induced distribution of K i.i.d. drafts from a draft
+ * truncated to at most s_max tokens (the top-s setting of mdss_induced_dist for
+ * K = 3): the r of mdss_induced_dist_expsum, by the same trapezoidal rule on
+ * the same node grid, with every (node, token) term of S(a_k) and of each
+ * token's sum taken directly over the support (no windows, expansions or
+ * polynomial tables), so its error is the rule's 4.8e-8 and the grid's 2e-8
+ * plus rounding.  One workgroup per row streams p and q once and holds the
+ * row's support on chip.
+ *   - A row with more than s_max tokens of q > 0 is flagged MDSS_ROW_SUPPORT
+ *     and gets r = NaN, as mdss_induced_dist does for K = 3; other flags
+ *     (MDSS_ROW_BAD_PROB, MDSS_ROW_RANGE) and outputs as
+ *     mdss_induced_dist_expsum.
+ *   - K in [2, MDSS_MAX_K], s_max in [1, MDSS_K3_MAX_SUPPORT] (else
+ *     MDSS_EUNSUPPORTED).  No workspace: the call allocates nothing. */
+mdss_status mdss_induced_dist_topk_expsum(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
+                                          int32_t s_max, float* r, int32_t* row_status, void* stream);
+
 /* Bytes of workspace for mdss_induced_dist_pair_expsum and
  * mdss_induced_dist_successive_expsum (0 if the shape is invalid or B = 0). */
 size_t mdss_workspace_bytes_pair_expsum(int64_t B, int64_t V);

@@ -31,6 +31,7 @@ from .binding import (  # noqa: F401
     induced_dist,
     induced_dist_expsum,
     induced_dist_expsum_noalloc,
+    induced_dist_topk_expsum,
     induced_dist_pair,
     induced_dist_pair_expsum,
     induced_dist_successive,

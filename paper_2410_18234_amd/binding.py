@@ -96,9 +96,11 @@ def load_library():
         lib.mdss_induced_dist_pair_expsum.argtypes = [P, P, P, i64, i64, P, P, P, sz, P]
         lib.mdss_induced_dist_successive_expsum.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P]
         lib.mdss_induced_dist_expsum_noalloc.argtypes = [P, P, i64, i64, i32, P, P, P]
+        lib.mdss_induced_dist_topk_expsum.argtypes = [P, P, i64, i64, i32, i32, P, P, P]
         for f in ("mdss_induced_dist_successive", "mdss_select_successive", "mdss_optimal_acceptance",
                   "mdss_acceptance", "mdss_induced_dist_expsum", "mdss_induced_dist_pair_expsum",
-                  "mdss_induced_dist_successive_expsum", "mdss_induced_dist_expsum_noalloc"):
+                  "mdss_induced_dist_successive_expsum", "mdss_induced_dist_expsum_noalloc",
+                  "mdss_induced_dist_topk_expsum"):
             getattr(lib, f).restype = ctypes.c_int
         for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample", "mdss_select_accept",
                   "mdss_select_accept_pair",
@@ -370,11 +372,14 @@ def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[tor
          offset: int = 0, s_max: int = 0, want_residual: bool = False, method: str = "exact"):
     """The whole path for one batch: r, then selection with accept / resample (two calls on one stream).
     method "exact": r by the pairwise sums (K in {2, 3}); "expsum": r by the exponential-sum
-    quadrature (any K in [2, MDSS_MAX_K])."""
+    quadrature (any K in [2, MDSS_MAX_K]; for K >= 3 with s_max > 0, the top-s form taken over
+    each row's support, rows with more than s_max tokens of q > 0 flagged as in "exact")."""
     B = p.shape[0]
     K = drafts.shape[1]
     status = torch.zeros(B, dtype=torch.int32, device=p.device)
-    if method == "expsum":
+    if method == "expsum" and K >= 3 and s_max > 0:
+        r = induced_dist_topk_expsum(p, q, K, s_max, row_status=status)
+    elif method == "expsum":
         r = induced_dist_expsum(p, q, K, row_status=status)
     elif method == "exact":
         r = induced_dist(p, q, K, s_max=s_max, row_status=status)
@@ -659,6 +664,24 @@ def induced_dist_expsum(p: torch.Tensor, q: torch.Tensor, K: int, r: Optional[to
     _check("mdss_induced_dist_expsum",
            lib.mdss_induced_dist_expsum(_ptr(p), _ptr(q), B, V, K, _ptr(r), _ptr(row_status), _ptr(workspace),
                                         workspace.numel(), _stream(dev)))
+    return r
+
+
+def induced_dist_topk_expsum(p: torch.Tensor, q: torch.Tensor, K: int, s_max: int, r: Optional[torch.Tensor] = None,
+                             row_status: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """r [B][V] fp32 of K i.i.d. drafts from a top-s draft (at most s_max tokens of q > 0 per
+    row, else the row is flagged and r = NaN there), by the quadrature taken directly over
+    each row's support (K in [2, MDSS_MAX_K], s_max in [1, MDSS_K3_MAX_SUPPORT]); no workspace."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    _check("mdss_induced_dist_topk_expsum",
+           lib.mdss_induced_dist_topk_expsum(_ptr(p), _ptr(q), B, V, K, s_max, _ptr(r), _ptr(row_status),
+                                             _stream(dev)))
     return r
 
 

@@ -74,6 +74,8 @@ hipError_t launch_induced_successive_expsum(const float* p, const float* q, int6
 // array (no allocation); B, V must fit in MDSS_NOALLOC_SCRATCH_BYTES.
 hipError_t launch_induced_expsum_noalloc(const float* p, const float* q, int64_t B, int64_t V, int K, float* r,
                                          int32_t* row_status, hipStream_t st);
+hipError_t launch_induced_topk_expsum(const float* p, const float* q, int64_t B, int64_t V, int K, int s_max,
+                                      float* r, int32_t* row_status, hipStream_t st);
 hipError_t launch_alphabet_truncate(const float* p, int64_t B, int64_t V, int m, float* pt, double* mass0,
                                     int32_t* row_status, hipStream_t st);
 hipError_t launch_alphabet_post(const float* p, const float* pt, const double* mass0, const int32_t* token,

@@ -659,10 +659,9 @@ __device__ __forceinline__ void es_lane_sort(uint32_t (&k)[N]) {
 
 // NB window nodes of a run: sum over the run's tokens of q exp(-a_k w), added to
 // the wave's moments (nodes at or above lim are not written).
-template <int NB>
-__device__ __forceinline__ void es_run_block(const float (&w)[kEsRunPer], const float (&qq)[kEsRunPer],
-                                             const float* __restrict__ rate, int lane, float* __restrict__ red,
-                                             int lim) {
+template <int NB, int E>
+__device__ __forceinline__ void es_run_block(const float (&w)[E], const float (&qq)[E], const float* __restrict__ rate,
+                                             int lane, float* __restrict__ red, int lim) {
   float rt[NB], acc[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
@@ -670,7 +669,7 @@ __device__ __forceinline__ void es_run_block(const float (&w)[kEsRunPer], const 
     acc[i] = 0.0f;
   }
 #pragma unroll
-  for (int e = 0; e < kEsRunPer; ++e) {
+  for (int e = 0; e < E; ++e) {
 #pragma unroll
     for (int i = 0; i < NB; ++i) acc[i] = fmaf(qq[e], es_decay(rt[i], w[e]), acc[i]);
   }
@@ -1848,6 +1847,330 @@ hipError_t launch_induced_successive_expsum(const float* p, const float* q, int6
     e = launch_induced_expsum(p, r_stages + (j - 1) * plane, q, B, V, 2, r_stages + j * plane, row_status,
                               workspace, st);
   return e;
+}
+
+// ------------------------------------------------------------------ top-s rows
+// K i.i.d. drafts from a draft truncated to at most s_max tokens (a top-s draft):
+// one workgroup of 1024 threads per row streams p and q once, writes r = 0 at
+// q = 0, keeps the support (index, p, q, w) in LDS and takes the trapezoidal rule
+// of the tiled path, on the same grid, directly over it:
+//   S_k = sum over the support of q(x) exp(-a_k w(x))      (p(x) > 0),
+//   r(y) = p(y) sum_k c_k exp(-a_k w(y)),  c_k = K h a_k (S_k [+ Q0 for K >= 3])^(K-1),
+// every (node, token) term exactly (no windows, expansions or polynomial tables),
+// plus the zero-weight closed forms.  fp32 terms with the tile path's power-of-two
+// scale (w' = w 2^tau, rates a_k 2^-tau), fp64 sums of the per-lane partials; a
+// row whose weights leave the fp32 normal range, span more than 2^kTkMaxRange or
+// need nodes outside the rate table is taken in fp64.
+namespace {
+
+constexpr int kTkThreads = 1024;
+constexpr int kTkWaves = kTkThreads / 64;
+constexpr int kTkCap = MDSS_K3_MAX_SUPPORT;   // support entries held in LDS
+constexpr int kTkPer = 4;                     // tokens per thread per streaming step
+constexpr int kTkStep = kTkThreads * kTkPer;  // 4096 tokens per step
+constexpr int kTkE = 4;                       // support entries per lane in the node sums
+constexpr int kTkGroup = 64 * kTkE;           // entries of one wave group
+constexpr int kTkMaxRange = 100;              // binary exponent span of the weights kept in fp32
+static_assert(kTkCap % kTkGroup == 0 && kTkCap / kTkGroup <= kTkWaves, "groups of 256 entries, one a wave at most");
+static_assert(kTkPer * kTkWaves == 64, "one (slot, wave) count per lane");
+
+// Inclusive scan of an int over the wave: row_shr steps inside each 16-lane row (DPP,
+// lanes before a row's start read 0), then the row totals carried by readlane.
+__device__ __forceinline__ int tk_scan_int(int v, int lane) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true);  // row_shr:8
+  const int t0 = __builtin_amdgcn_readlane(v, 15), t1 = __builtin_amdgcn_readlane(v, 31),
+            t2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = lane >> 4;
+  return v + (row == 0 ? 0 : (row == 1 ? t0 : (row == 2 ? t0 + t1 : t0 + t1 + t2)));
+}
+
+__device__ __forceinline__ void tk_load(const float* __restrict__ pb, const float* __restrict__ qb, int64_t V,
+                                        int64_t x0, int tid, float (&pv)[kTkPer], float (&qv)[kTkPer]) {
+#pragma unroll
+  for (int i = 0; i < kTkPer; ++i) {
+    const int64_t x = x0 + i * kTkThreads + tid;
+    pv[i] = (x < V) ? pb[x] : 0.0f;
+    qv[i] = (x < V) ? qb[x] : 0.0f;
+  }
+}
+
+__global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __restrict__ p, const float* __restrict__ q,
+                                                             int64_t V, int K, int s_max, float* __restrict__ r,
+                                                             int32_t* __restrict__ row_status) {
+  __shared__ int s_idx[kTkCap];
+  __shared__ float s_p[kTkCap];
+  __shared__ float s_q[kTkCap];
+  __shared__ float s_w[kTkCap];                    // the weight (unscaled, then w 2^tau in fp32)
+  __shared__ float s_part[kTkWaves][kEsMaxNodes];  // per wave: its entries' share of S_k at its nodes
+  __shared__ float s_rate[kEsMaxNodes + 16];       // fp32: log2(e) a_k 2^-tau (16 spare entries: 0)
+  __shared__ float s_cf[kEsMaxNodes + 16];         // fp32: c_k 2^-tau (0 on the spare entries)
+  __shared__ double s_c64[kEsMaxNodes];            // fp64: c_k
+  __shared__ int s_cnt[2][64];
+  __shared__ int s_flag[kTkWaves];
+  __shared__ float s_f[kTkWaves][2];
+  __shared__ double s_d[kTkWaves];
+  __shared__ double s_e[kTkWaves][2];
+  __shared__ int s_n[kTkWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t b = blockIdx.x;
+  const float* pb = p + b * V;
+  const float* qb = q + b * V;
+  float* rb = r + b * V;
+
+  // (1) stream the row, two steps in flight: r = 0 at q = 0 and the support compacted in
+  //     token order (token x0 + 1024 i + thread; counts per (slot i, wave), one scan a step)
+  float pa[kTkPer], qa[kTkPer], pn[kTkPer], qn[kTkPer];
+  tk_load(pb, qb, V, 0, tid, pa, qa);
+  tk_load(pb, qb, V, kTkStep, tid, pn, qn);
+  int bad = 0, running = 0;
+  const int64_t nstep = (V + kTkStep - 1) / kTkStep;
+  for (int64_t st = 0; st < nstep; ++st) {
+    const int par = (int)(st & 1);
+    const int64_t x0 = st * kTkStep;
+    float pc[kTkPer], qc[kTkPer];
+#pragma unroll
+    for (int i = 0; i < kTkPer; ++i) {
+      pc[i] = pa[i];
+      qc[i] = qa[i];
+      pa[i] = pn[i];
+      qa[i] = qn[i];
+    }
+    if (st + 2 < nstep) tk_load(pb, qb, V, x0 + 2 * kTkStep, tid, pn, qn);
+#pragma unroll
+    for (int i = 0; i < kTkPer; ++i) {
+      const int64_t x = x0 + i * kTkThreads + tid;
+      // NaN, -inf, a negative normal or denormal, +inf (-0 is a zero probability)
+      bad |= __builtin_amdgcn_classf(pc[i], 0x21F) | __builtin_amdgcn_classf(qc[i], 0x21F);
+      const bool sup = qc[i] > 0.0f;
+      if (!sup && x < V) rb[x] = 0.0f;
+      const int cnt = __builtin_popcountll(__builtin_amdgcn_ballot_w64(sup));
+      if (lane == 0) s_cnt[par][i * kTkWaves + wid] = cnt;
+    }
+    es_lds_barrier();  // (s_cnt by step parity: a step's counts are read before the next barrier)
+    const int c = s_cnt[par][lane];
+    const int incl = tk_scan_int(c, lane);
+    const int ex = incl - c;
+#pragma unroll
+    for (int i = 0; i < kTkPer; ++i) {
+      const bool sup = qc[i] > 0.0f;
+      const uint64_t mask = __builtin_amdgcn_ballot_w64(sup);
+      const int pos = running + __builtin_amdgcn_readlane(ex, i * kTkWaves + wid) +
+                      (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+      if (sup && pos < kTkCap) {
+        s_idx[pos] = (int)(x0 + i * kTkThreads + tid);
+        s_p[pos] = pc[i];
+        s_q[pos] = qc[i];
+      }
+    }
+    running += __builtin_amdgcn_readlane(incl, 63);  // the same in every wave
+  }
+  const int n = running;
+  const bool wave_bad = __builtin_amdgcn_ballot_w64(bad != 0) != 0;  // every lane votes
+  if (lane == 0) s_flag[wid] = wave_bad ? 1 : 0;
+  __syncthreads();  // the list is complete (and a flagged row's NaN below follows its zeros)
+  int flags = 0;
+#pragma unroll
+  for (int i = 0; i < kTkWaves; ++i) flags |= s_flag[i];
+  flags = flags ? kRowBadProb : (n > s_max ? kRowSupport : 0);
+  const int nl = min(n, kTkCap);  // entries in LDS (n itself when the row is not flagged)
+
+  // (2) weights and the row's statistics (entry e = thread + 1024 j)
+  float wlo = INFINITY, whi = 0.0f;
+  double q0 = 0.0;
+  int npos = 0;
+  for (int e = tid; e < nl; e += kTkThreads) {
+    const float pp = s_p[e], qq = s_q[e];
+    float w = 0.0f;
+    if (pp > 0.0f) {
+      w = es_denormal(qq) ? es_ratio_small_q(pp, qq) : es_ratio<float>(pp, qq);
+      wlo = fminf(wlo, w);
+      whi = fmaxf(whi, w);
+      ++npos;
+    } else {
+      q0 += (double)qq;
+    }
+    s_w[e] = w;
+  }
+  wlo = es_wave_ext<false>(wlo);
+  whi = es_wave_ext<true>(whi);
+  q0 = wave_sum(q0);
+  npos = wave_sum_int(npos);
+  if (lane == 0) {
+    s_f[wid][0] = wlo;
+    s_f[wid][1] = whi;
+    s_d[wid] = q0;
+    s_n[wid] = npos;
+  }
+  __syncthreads();
+  float wmin = s_f[0][0], wmax = s_f[0][1];
+  q0 = s_d[0];
+  npos = s_n[0];
+#pragma unroll
+  for (int i = 1; i < kTkWaves; ++i) {
+    wmin = fminf(wmin, s_f[i][0]);
+    wmax = fmaxf(wmax, s_f[i][1]);
+    q0 += s_d[i];
+    npos += s_n[i];
+  }
+  // weights outside the fp32 normal range (a ratio that overflowed or a denormal one):
+  // the row's range again in fp64, and the fp64 form below
+  const bool wide = !flags && npos > 0 && (!(wmin >= __FLT_MIN__) || !(wmax <= __FLT_MAX__));
+  double wmin64 = (double)wmin, wmax64 = (double)wmax;
+  if (wide) {  // uniform
+    double lo = INFINITY, hi = 0.0;
+    for (int e = tid; e < nl; e += kTkThreads) {
+      const float pp = s_p[e], qq = s_q[e];
+      if (pp > 0.0f) {
+        const double w = es_ratio<double>(pp, qq);
+        lo = fmin(lo, w);
+        hi = fmax(hi, w);
+      }
+    }
+    lo = wave_min64(lo);
+    hi = wave_max64(hi);
+    if (lane == 0) {
+      s_e[wid][0] = lo;
+      s_e[wid][1] = hi;
+    }
+    __syncthreads();
+    wmin64 = s_e[0][0];
+    wmax64 = s_e[0][1];
+#pragma unroll
+    for (int i = 1; i < kTkWaves; ++i) {
+      wmin64 = fmin(wmin64, s_e[i][0]);
+      wmax64 = fmax(wmax64, s_e[i][1]);
+    }
+  }
+  // the grid of the tiled path (same merge statistics, same plan)
+  EsMerge m;
+  m.wmin[0] = m.wmin[1] = npos > 0 ? wmin64 : INFINITY;
+  m.wmax[0] = m.wmax[1] = wmax64;
+  m.q0[0] = q0;
+  m.q0[1] = 0.0;
+  m.npos[0] = npos;
+  m.npos[1] = 0;
+  m.bad = 0;
+  m.wide = 0;
+  const EsPlan pl = es_make_plan<1>(m, K);
+  if (!flags) flags = pl.flags;
+  if (flags) {  // NaN over the whole row
+    if (tid == 0 && row_status) row_status[b] |= flags;
+    for (int64_t x = tid; x < V; x += kTkThreads) rb[x] = NAN;
+    return;
+  }
+  const int k_lo = pl.k_lo, nk = pl.nk;
+  // fp32 unless a weight is not an fp32 normal (an overflowed or denormal ratio), the
+  // weights span more than 2^kTkMaxRange, or a node lies outside the rate table
+  bool fp64 = wide;
+  int tau = 0, range = 0;
+  if (nk > 0 && !fp64) {
+    es_scale_f32(wmin, wmax, tau, range);
+    fp64 = range > kTkMaxRange || k_lo < kEsNodeLo || k_lo + nk > kEsNodeHi;
+  }
+  double zw = q0;  // K i.i.d. drafts: Q0^(K-1)
+  for (int j = 2; j < K; ++j) zw *= q0;
+  if (nk > 0 && !fp64) {
+    // (3) fp32: S_k.  Entries in groups of 256 (four a lane); with G groups (a power of
+    //     two), wave w takes group w % G and the node blocks of 16 congruent to w / G
+    //     modulo 16 / G; each block summed across the wave (reduce-scatter)
+    for (int e = tid; e < nl; e += kTkThreads) s_w[e] = ldexpf(s_w[e], tau);
+    for (int k = tid; k < nk + 16; k += kTkThreads)  // past the grid: rate 0 (a term of 1, times c = 0)
+      s_rate[k] = k < nk ? es_rate_f32(k_lo + k, tau) : 0.0f;
+    for (int k = lane; k < nk; k += 64) s_part[wid][k] = 0.0f;
+    __syncthreads();
+    int G = 1;
+    while (G * kTkGroup < nl) G *= 2;  // <= kTkWaves
+    const int gi = wid % G, bs = kTkWaves / G;
+    float w[kTkE], qq[kTkE];
+#pragma unroll
+    for (int e = 0; e < kTkE; ++e) {
+      const int x = gi * kTkGroup + e * 64 + lane;  // < kTkCap
+      const bool in = x < nl && s_p[x] > 0.0f;
+      w[e] = in ? s_w[x] : 0.0f;
+      qq[e] = in ? s_q[x] : 0.0f;
+    }
+    for (int blk = wid / G; blk * 16 < nk; blk += bs)
+      es_run_block<16>(w, qq, s_rate + blk * 16, lane, s_part[wid] + blk * 16, min(16, nk - blk * 16));
+    __syncthreads();
+    // (4) c_k 2^-tau from the fp64 sum of the waves' shares (a wave adds 0 at nodes it does not take)
+    for (int k = tid; k < nk; k += kTkThreads) {
+      double S = 0.0;
+#pragma unroll
+      for (int i = 0; i < kTkWaves; ++i) S += (double)s_part[i][k];  // 0 from the waves that did not take node k
+      const double sm = S + (K >= 3 ? q0 : 0.0);
+      double sp = 1.0;
+      for (int j = 1; j < K; ++j) sp *= sm;
+      s_cf[k] = (float)ldexp((double)K * kEsStep * exp((double)(k_lo + k) * kEsStep) * sp, -tau);
+    }
+    for (int k = nk + tid; k < nk + 16; k += kTkThreads) s_cf[k] = 0.0f;
+    __syncthreads();
+    // (5) r at the support: every node, blocks of 16 in fp32, the blocks summed in fp64
+    for (int e = tid; e < nl; e += kTkThreads) {
+      const float pp = s_p[e], qq1 = s_q[e];
+      double v;
+      if (pp > 0.0f) {
+        const float we = s_w[e];
+        double acc = 0.0;
+        for (int k0 = 0; k0 < nk; k0 += 16) {
+          float a = 0.0f;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) a = fmaf(s_cf[k0 + i], es_decay(s_rate[k0 + i], we), a);
+          acc += (double)a;
+        }
+        const double quad = ldexp((double)pp * acc, tau);
+        v = (K == 2) ? fma(2.0 * (double)qq1, q0, quad) : quad;
+      } else {
+        v = (double)qq1 * zw;
+      }
+      rb[s_idx[e]] = (float)v;
+    }
+  } else if (nk > 0) {
+    // (3') fp64: S_k per node (wave w takes the nodes congruent to w), lanes over the entries
+    for (int kk = wid; kk < nk; kk += kTkWaves) {
+      const double a = exp((double)(k_lo + kk) * kEsStep);
+      double acc = 0.0;
+      for (int e = lane; e < nl; e += 64) {
+        const float pp = s_p[e], qq1 = s_q[e];
+        if (pp > 0.0f) acc += (double)qq1 * exp(-a * es_ratio<double>(pp, qq1));
+      }
+      acc = wave_sum(acc);
+      if (lane == 0) {
+        const double sm = acc + (K >= 3 ? q0 : 0.0);
+        double sp = 1.0;
+        for (int j = 1; j < K; ++j) sp *= sm;
+        s_c64[kk] = (double)K * kEsStep * a * sp;
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < nl; e += kTkThreads) {
+      const float pp = s_p[e], qq1 = s_q[e];
+      double v;
+      if (pp > 0.0f) {
+        const double w = es_ratio<double>(pp, qq1);
+        double acc = 0.0;
+        for (int kk = 0; kk < nk; ++kk) acc += s_c64[kk] * exp(-exp((double)(k_lo + kk) * kEsStep) * w);
+        const double quad = (double)pp * acc;
+        v = (K == 2) ? fma(2.0 * (double)qq1, q0, quad) : quad;
+      } else {
+        v = (double)qq1 * zw;
+      }
+      rb[s_idx[e]] = (float)v;
+    }
+  } else {
+    // no positive weight: zero-weight tokens only
+    for (int e = tid; e < nl; e += kTkThreads) rb[s_idx[e]] = (float)((double)s_q[e] * zw);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_induced_topk_expsum(const float* p, const float* q, int64_t B, int64_t V, int K, int s_max,
+                                      float* r, int32_t* row_status, hipStream_t st) {
+  hipLaunchKernelGGL(es_topk_kernel, dim3((unsigned)B), dim3(kTkThreads), 0, st, p, q, V, K, s_max, r, row_status);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ fixed scratch

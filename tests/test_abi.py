@@ -252,3 +252,18 @@ def test_noalloc_argument_errors(lib):
     assert lib.mdss_workspace_bytes_expsum(1024, 50272, 2) > 32 << 20
     assert f(FAKE, FAKE, 1024, 50272, 2, FAKE, None, None) == 5
     assert lib.mdss_workspace_bytes_expsum(256, 32000, 2) <= 32 << 20
+
+
+def test_topk_expsum_argument_errors(lib):
+    f = lib.mdss_induced_dist_topk_expsum
+    f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    assert f(None, FAKE, 4, 16, 3, 8, FAKE, None, None) == 1
+    assert f(FAKE, FAKE, 4, 16, 3, 8, None, None, None) == 1
+    assert f(FAKE, FAKE, -1, 16, 3, 8, FAKE, None, None) == 2
+    assert f(FAKE, FAKE, 4, 1, 3, 8, FAKE, None, None) == 2
+    assert f(FAKE, FAKE, 4, 16, 1, 8, FAKE, None, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 9, 8, FAKE, None, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 3, 0, FAKE, None, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 3, 4097, FAKE, None, None) == 3
+    assert f(None, None, 0, 16, 3, 8, None, None, None) == 0  # empty batch: nothing read or launched

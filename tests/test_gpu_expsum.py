@@ -291,6 +291,93 @@ def test_ragged_tiles(V):
     assert np.all(st == 0) and np.all(rel_l1(r, ro) <= TIGHT)
 
 
+# ------------------------------------------------------------------ sparse draft supports
+# Rows whose draft puts mass on a few tokens per 4096-token moments tile (a top-k
+# or top-p draft), one batch holding: tiles of 192 and 193 supported tokens, empty
+# tiles, supports of zero-weight tokens only (p = 0 < q), a lone token, supports on
+# moments and evaluation tile edges, a ragged last tile, draft probabilities below
+# the fp32 normal range, and rows that mix sparse and fuller tiles.  The same rows
+# serve the top-s form.
+SPARSE_V = 3 * 4096 + 700  # three whole moments tiles and a ragged one
+
+
+def _sparse_rows(seed):
+    rng = np.random.default_rng(seed)
+    V, T = SPARSE_V, 4096
+    tiles = [(t * T, min(V, (t + 1) * T)) for t in range(4)]
+    # per row: support size of each moments tile (above 192: the sorted path), p = 0 share;
+    # supports of a few hundred tokens keep the oracle's K = 3 enumeration within seconds
+    plan = [
+        ([192, 193, 0, 50], 0.0),
+        ([20, 100, 1, 250], 0.3),
+        ([150, 150, 150, 150], 0.1),
+        ([60, 0, 0, 0], 0.0),
+        ([300, 193, 5, 5], 0.05),
+        ([1, 0, 0, 0], 0.0),
+        ([0, 0, 0, 0], 0.0),  # filled below: tokens on tile edges
+        ([0, 0, 0, 400], 0.5),
+    ]
+    B = len(plan)
+    P = np.zeros((B, V), np.float64)
+    Q = np.zeros((B, V), np.float64)
+    for b, (sizes, pzero) in enumerate(plan):
+        for (lo, hi), n in zip(tiles, sizes):
+            idx = rng.choice(np.arange(lo, hi), size=n, replace=False)
+            Q[b, idx] = rng.gamma(0.5, size=idx.size) + 1e-3
+        # the target: most of its mass on the support, the rest anywhere (r ignores it)
+        sup = np.flatnonzero(Q[b] > 0)
+        if sup.size == 0:
+            sup = np.array([4095, 4096, 1023, 1024, 8191, 8192, 12287, 12288, SPARSE_V - 1])
+            Q[b, sup] = rng.gamma(2.0, size=sup.size)
+        P[b, sup] = rng.gamma(0.7, size=sup.size)
+        P[b, rng.integers(0, V, 300)] += rng.gamma(0.7, size=300) * 0.01
+        P[b, sup[rng.random(sup.size) < pzero]] = 0.0
+        if b == 1:
+            P[b, np.flatnonzero(Q[b, :4096] > 0)] = 0.0  # tile 0: zero weights only
+    P /= P.sum(1, keepdims=True)
+    Q /= Q.sum(1, keepdims=True)
+    P, Q = P.astype(np.float32), Q.astype(np.float32)
+    # row 3: ten draft probabilities below the fp32 normal range, their weights in range
+    den = np.flatnonzero(Q[3] > 0)[:10]
+    Q[3, den] = np.float32(2e-39)
+    P[3, den] = np.float32(3e-38)
+    for A in (P, Q):  # the rest of the row rescaled to total 1
+        rest = np.ones(SPARSE_V, bool)
+        rest[den] = False
+        A[3, rest] *= np.float32((1.0 - A[3, den].astype(np.float64).sum()) / A[3, rest].astype(np.float64).sum())
+    return P, Q
+
+
+@pytest.mark.parametrize("K", [2, 3])
+def test_sparse_support_tiles(K):
+    P, Q = _sparse_rows(900 + K)
+    r, st = es_r(P, Q, K)
+    assert np.all(st == 0), st
+    rows, ys = np.nonzero(Q > 0)
+    ro = np.zeros(P.shape, np.float64)
+    ro[rows, ys] = oracle.induced_dist_entries(P, Q, K, rows, ys)
+    assert np.all(r[Q == 0] == 0.0)  # no tuple holds a token of q = 0
+    err = rel_l1(r, ro)
+    print(f"\nK={K}: relative L1 per row {[f'{e:.1e}' for e in err]}")
+    assert np.all(err <= TIGHT), err
+    # every entry, including the smallest and the denormal-q ones
+    big = ro > 0
+    assert np.all(np.abs(r[big] - ro[big]) <= RTOL_ROW * ro[big])
+
+
+def test_sparse_tiles_in_a_full_batch():
+    # the sparse rows repeated over a batch that spreads them across the persistent
+    # kernels' workgroups (a workgroup takes consecutive tiles of different kinds)
+    P, Q = _sparse_rows(77)
+    reps = 37
+    Pb, Qb = np.tile(P, (reps, 1)), np.tile(Q, (reps, 1))
+    r, st = es_r(Pb, Qb, 3)
+    assert np.all(st == 0)
+    r1, _ = es_r(P, Q, 3)
+    # rows are computed independently: each copy equals the single-batch result
+    np.testing.assert_array_equal(r, np.tile(r1, (reps, 1)))
+
+
 def _span_rows(seed, V, spans):
     """Rows whose positive weights span about 2^s (one row per s) with p, q and every
     ratio fp32 normal numbers: p ~ a 2^(x/2), q ~ a 2^(-x/2), x uniform in [-s/2, s/2]."""
