@@ -263,6 +263,9 @@ def main():
     use_es = args.method == "expsum" and not (tlp_s or cfg.alphabet or cfg.diag)
     # K >= 3 i.i.d. drafts from a top-s draft: the quadrature over each row's support
     use_topk = use_es and K >= 3 and bool(s_max) and not (cfg.successive or cfg.pair)
+    # K i.i.d. drafts by the tiled quadrature: r and Algorithm 1's residual sums in one pass, then the
+    # selection and Algorithm 1 from those sums
+    use_sums = use_es and not (use_topk or cfg.successive or cfg.pair)
     if use_es and (cfg.successive or cfg.pair):
         ws_bytes = mdss.workspace_bytes_pair_expsum(B, V)
         if cfg.successive:
@@ -295,6 +298,8 @@ def main():
                 mdss.induced_dist_pair_expsum(p, q, q2, r=r, row_status=status, workspace=ws)
             elif use_topk:
                 mdss.induced_dist_topk_expsum(p, q, K, s_max, r=r, row_status=status)
+            elif use_sums:
+                mdss.induced_dist_expsum_sums(p, q, K, ws_acc, r=r, row_status=status, workspace=ws)
             else:
                 mdss.induced_dist_expsum(p, q, K, r=r, row_status=status, workspace=ws)
         elif tlp_s:
@@ -353,6 +358,8 @@ def main():
             if cfg.pair:
                 _, _, out, acc, _, _ = mdss.select_accept_pair(p, q, q2, r, drafts, u, row_status=status,
                                                                 workspace=ws_acc)
+            elif use_sums:
+                _, _, out, acc, _ = mdss.select_accept_sums(p, q, r, drafts, ws_acc, u, row_status=status)
             else:
                 _, _, out, acc, _, _ = mdss.select_accept(p, q, r, drafts, u, row_status=status, workspace=ws_acc)
             return out, acc
@@ -491,12 +498,15 @@ def main():
         slots = ES_SLOTS_PER_TOKEN * ntok
         achieved = flops / (r_ms * 1e-3) / 1e12
         api = ("mdss_induced_dist_successive_expsum" if cfg.successive else
-               "mdss_induced_dist_pair_expsum" if cfg.pair else "mdss_induced_dist_expsum")
+               "mdss_induced_dist_pair_expsum" if cfg.pair else
+               "mdss_induced_dist_expsum_sums" if use_sums else "mdss_induced_dist_expsum")
+        eval_name = f"es_eval_kernel<{2 if cfg.pair else 1}, {'true' if use_sums else 'false'}>"
         roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_PEAK_TFLOPS,
                     "unit": "TFLOP/s", "frac": round(achieved / FP32_PEAK_TFLOPS, 4),
                     "traffic": counted_traffic(cfg.name, ["es_moments_kernel", f"es_coef_kernel<{2 if cfg.pair else 1}>",
-                                                          f"es_eval_kernel<{2 if cfg.pair else 1}>"], digest),
+                                                          eval_name], digest),
                     "kernel": f"{api} (es_moments_kernel + es_coef_kernel + es_eval_kernel"
+                              f"{' with the residual sums of Algorithm 1' if use_sums else ''}"
                               f"{', per stage' if stages > 1 else ''})",
                     "avg_ms": round(r_ms, 4), "flops_per_launch": flops,
                     "flop_basis": f"{ES_FLOPS_PER_TOKEN} FLOP per positive-weight token and law, the least work of "

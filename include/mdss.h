@@ -131,9 +131,11 @@ mdss_status mdss_select_intermediate(const float* p, const float* q, const int32
  * residual_mass ([B] fp64, nullable) receives Z; when both are NULL, rows
  * whose token is accepted do not read p or r beyond p(Y), r(Y).
  * workspace: device buffer of at least mdss_workspace_bytes_accept(B, V)
- * bytes, 256-byte aligned (per position a record and one fp64 residual sum
- * per 256 tokens): a row's residual is summed by one workgroup per 4096-token
- * segment, and the draw reads the sums of its row.  Two launches. */
+ * bytes, 256-byte aligned (room for one fp64 residual sum per 256 tokens, or
+ * four per 1024 tokens, of every position): when a residual output is asked for, a row's residual is
+ * summed by one workgroup per 4096-token segment and the draw reads the sums
+ * of its row (two launches); otherwise one workgroup per position reads its
+ * drafts' entries and, if it rejects, its own row (one launch). */
 size_t mdss_workspace_bytes_accept(int64_t B, int64_t V);
 
 mdss_status mdss_accept_or_resample(const float* p, const float* r, const int32_t* sel_token, const float* u,
@@ -156,6 +158,32 @@ mdss_status mdss_select_accept(const float* p, const float* q, const float* r, c
                                int32_t* sel_index, int32_t* sel_token, int32_t* out_token, uint8_t* accepted,
                                float* residual, double* residual_mass, int32_t* row_status, void* workspace,
                                size_t workspace_bytes, void* stream);
+
+/* Theorem 1's two steps sharing one pass over the rows.
+ * mdss_induced_dist_expsum_sums: r as mdss_induced_dist_expsum (the same
+ * kernels, bit-identical r and row flags), and, from the same pass, the sums
+ * Algorithm 1 with proposal r needs: for every position and 1024-token
+ * sub-tile, four fp64 partial sums of res(x) = max(0, p(x) - r(x)) (NaN where
+ * a p or r is not a probability), written into accept_workspace (at least
+ * mdss_workspace_bytes_accept(B, V) bytes).
+ * mdss_select_accept_sums: selection and Algorithm 1 as mdss_select_accept,
+ * with Z and the running sums taken from those partial sums instead of a pass
+ * over the rows (the crossing sub-tile's 1024 entries are read again to find
+ * the token); residual_mass (nullable) receives Z; there is no residual
+ * output.  accept_workspace must hold the sums of the last
+ * mdss_induced_dist_expsum_sums call, with p and r unchanged since.  The
+ * selection, the accept decision, the flags and Z agree with
+ * mdss_select_accept; Z and the running sums are the same fp64 sums taken in
+ * another order, so a resampled token can differ only where u_res Z lies
+ * within the rounding of an fp64 sum of a CDF edge. */
+mdss_status mdss_induced_dist_expsum_sums(const float* p, const float* q, int64_t B, int64_t V, int32_t K, float* r,
+                                          int32_t* row_status, void* workspace, size_t workspace_bytes,
+                                          void* accept_workspace, size_t accept_workspace_bytes, void* stream);
+mdss_status mdss_select_accept_sums(const float* p, const float* q, const float* r, const int32_t* drafts,
+                                    const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
+                                    int32_t* sel_index, int32_t* sel_token, int32_t* out_token, uint8_t* accepted,
+                                    double* residual_mass, int32_t* row_status, void* accept_workspace,
+                                    size_t accept_workspace_bytes, void* stream);
 
 /* ---- Two drafts from different distributions (K = 2) --------------------
  * Remark 1 (and the non-identical K = 2 appendix): X1 ~ q1 and X2 ~ q2

@@ -91,6 +91,8 @@ def load_library():
         lib.mdss_workspace_bytes_expsum.argtypes = [i64, i64, i32]
         lib.mdss_workspace_bytes_expsum.restype = sz
         lib.mdss_induced_dist_expsum.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P]
+        lib.mdss_induced_dist_expsum_sums.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P, sz, P]
+        lib.mdss_select_accept_sums.argtypes = [P, P, P, P, P, u64, u64, i64, i64, i32, P, P, P, P, P, P, P, sz, P]
         lib.mdss_workspace_bytes_pair_expsum.argtypes = [i64, i64]
         lib.mdss_workspace_bytes_pair_expsum.restype = sz
         lib.mdss_induced_dist_pair_expsum.argtypes = [P, P, P, i64, i64, P, P, P, sz, P]
@@ -100,7 +102,7 @@ def load_library():
         for f in ("mdss_induced_dist_successive", "mdss_select_successive", "mdss_optimal_acceptance",
                   "mdss_acceptance", "mdss_induced_dist_expsum", "mdss_induced_dist_pair_expsum",
                   "mdss_induced_dist_successive_expsum", "mdss_induced_dist_expsum_noalloc",
-                  "mdss_induced_dist_topk_expsum"):
+                  "mdss_induced_dist_topk_expsum", "mdss_induced_dist_expsum_sums", "mdss_select_accept_sums"):
             getattr(lib, f).restype = ctypes.c_int
         for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample", "mdss_select_accept",
                   "mdss_select_accept_pair",
@@ -290,6 +292,36 @@ def select_accept(p: torch.Tensor, q: torch.Tensor, r: torch.Tensor, drafts: tor
                           row_status, workspace)
 
 
+def select_accept_sums(p: torch.Tensor, q: torch.Tensor, r: torch.Tensor, drafts: torch.Tensor,
+                       accept_workspace: torch.Tensor, u: Optional[torch.Tensor] = None, seed: int = 0,
+                       offset: int = 0, want_mass: bool = False, row_status: Optional[torch.Tensor] = None):
+    """(sel_index, sel_token, out_token, accepted, residual_mass or None): select_accept with the
+    residual sums that induced_dist_expsum_sums wrote into accept_workspace (same p and r)."""
+    lib = load_library()
+    B, V, dev = _pq(p, r)
+    _need(q, "q", torch.float32, (B, V), dev)
+    if drafts.dim() != 2:
+        raise ValueError("drafts must be [B][K]")
+    K = drafts.shape[1]
+    _need(drafts, "drafts", torch.int32, (B, K), dev)
+    if u is not None:
+        _need(u, "u", torch.float32, (B, 3), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    accept_workspace = _ws_arg(dev, int(lib.mdss_workspace_bytes_accept(B, V)), accept_workspace)
+    sel_index = torch.empty(B, dtype=torch.int32, device=dev)
+    sel_token = torch.empty(B, dtype=torch.int32, device=dev)
+    out = torch.empty(B, dtype=torch.int32, device=dev)
+    acc = torch.empty(B, dtype=torch.uint8, device=dev)
+    mass = torch.empty(B, dtype=torch.float64, device=dev) if want_mass else None
+    _check("mdss_select_accept_sums",
+           lib.mdss_select_accept_sums(_ptr(p), _ptr(q), _ptr(r), _ptr(drafts), _ptr(u), ctypes.c_uint64(seed),
+                                       ctypes.c_uint64(offset), B, V, K, _ptr(sel_index), _ptr(sel_token), _ptr(out),
+                                       _ptr(acc), _ptr(mass), _ptr(row_status), _ptr(accept_workspace),
+                                       accept_workspace.numel(), _stream(dev)))
+    return sel_index, sel_token, out, acc, mass
+
+
 def select_accept_pair(p: torch.Tensor, q1: torch.Tensor, q2: torch.Tensor, r: torch.Tensor, drafts: torch.Tensor,
                        u: Optional[torch.Tensor] = None, seed: int = 0, offset: int = 0, want_residual: bool = False,
                        want_mass: bool = False, row_status: Optional[torch.Tensor] = None,
@@ -379,6 +411,14 @@ def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[tor
     status = torch.zeros(B, dtype=torch.int32, device=p.device)
     if method == "expsum" and K >= 3 and s_max > 0:
         r = induced_dist_topk_expsum(p, q, K, s_max, row_status=status)
+    elif method == "expsum" and not want_residual:
+        # Theorem 1's two steps sharing one pass over the rows: r and Algorithm 1's residual sums together
+        acc_ws = torch.empty(workspace_bytes_accept(B, p.shape[1]), dtype=torch.uint8, device=p.device)
+        r = induced_dist_expsum_sums(p, q, K, acc_ws, row_status=status)
+        sel_index, sel_token, out, acc, _ = select_accept_sums(p, q, r, drafts, acc_ws, u, seed, offset,
+                                                               row_status=status)
+        return {"r": r, "sel_index": sel_index, "sel_token": sel_token, "out_token": out, "accepted": acc,
+                "residual": None, "mass": None, "status": status}
     elif method == "expsum":
         r = induced_dist_expsum(p, q, K, row_status=status)
     elif method == "exact":
@@ -681,6 +721,33 @@ def induced_dist_topk_expsum(p: torch.Tensor, q: torch.Tensor, K: int, s_max: in
         _need(row_status, "row_status", torch.int32, (B,), dev)
     _check("mdss_induced_dist_topk_expsum",
            lib.mdss_induced_dist_topk_expsum(_ptr(p), _ptr(q), B, V, K, s_max, _ptr(r), _ptr(row_status),
+                                             _stream(dev)))
+    return r
+
+
+def induced_dist_expsum_sums(p: torch.Tensor, q: torch.Tensor, K: int, accept_workspace: torch.Tensor,
+                             r: Optional[torch.Tensor] = None, row_status: Optional[torch.Tensor] = None,
+                             workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """induced_dist_expsum, writing also the residual sums of Algorithm 1 into accept_workspace
+    (a uint8 tensor of at least workspace_bytes_accept(B, V) bytes, kept for select_accept_sums;
+    it must not be the r call's own workspace)."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    need = int(lib.mdss_workspace_bytes_expsum(B, V, K))
+    if need == 0 and B > 0:
+        _check("mdss_workspace_bytes_expsum", 3 if not 2 <= K <= MDSS_MAX_K else 2)
+    workspace = _ws_arg(dev, need, workspace)
+    accept_workspace = _ws_arg(dev, int(lib.mdss_workspace_bytes_accept(B, V)), accept_workspace)
+    if accept_workspace.data_ptr() == workspace.data_ptr():
+        raise ValueError("accept_workspace must be a buffer of its own")
+    _check("mdss_induced_dist_expsum_sums",
+           lib.mdss_induced_dist_expsum_sums(_ptr(p), _ptr(q), B, V, K, _ptr(r), _ptr(row_status), _ptr(workspace),
+                                             workspace.numel(), _ptr(accept_workspace), accept_workspace.numel(),
                                              _stream(dev)))
     return r
 

@@ -328,6 +328,39 @@ mdss_status mdss_select_accept(const float* p, const float* q, const float* r, c
                                              workspace, static_cast<hipStream_t>(stream)));
 }
 
+mdss_status mdss_induced_dist_expsum_sums(const float* p, const float* q, int64_t B, int64_t V, int32_t K, float* r,
+                                          int32_t* row_status, void* workspace, size_t workspace_bytes,
+                                          void* accept_workspace, size_t accept_workspace_bytes, void* stream) {
+  const mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  if (K < 2 || K > MDSS_MAX_K) return MDSS_EUNSUPPORTED;
+  if (B == 0) return MDSS_OK;
+  if (!p || !q || !r) return MDSS_EINVAL;
+  if (!workspace_ok(workspace, workspace_bytes, mdss::workspace_bytes_expsum(B, V, 1))) return MDSS_EWORKSPACE;
+  if (!workspace_ok(accept_workspace, accept_workspace_bytes, mdss::workspace_bytes_accept(B, V)))
+    return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_induced_expsum(p, q, nullptr, B, V, K, r, row_status, workspace,
+                                              static_cast<hipStream_t>(stream),
+                                              static_cast<double*>(accept_workspace)));
+}
+
+mdss_status mdss_select_accept_sums(const float* p, const float* q, const float* r, const int32_t* drafts,
+                                    const float* u, uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K,
+                                    int32_t* sel_index, int32_t* sel_token, int32_t* out_token, uint8_t* accepted,
+                                    double* residual_mass, int32_t* row_status, void* accept_workspace,
+                                    size_t accept_workspace_bytes, void* stream) {
+  mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  if (K < 2 || K > MDSS_MAX_K) return MDSS_EUNSUPPORTED;
+  if (B == 0) return MDSS_OK;
+  if (!p || !q || !r || !drafts || !out_token || !accepted) return MDSS_EINVAL;
+  if (!workspace_ok(accept_workspace, accept_workspace_bytes, mdss::workspace_bytes_accept(B, V)))
+    return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_select_accept_sums(p, q, nullptr, r, drafts, u, seed, offset, B, V, K, sel_index,
+                                                  sel_token, out_token, accepted, residual_mass, row_status,
+                                                  accept_workspace, static_cast<hipStream_t>(stream)));
+}
+
 mdss_status mdss_select_accept_pair(const float* p, const float* q1, const float* q2, const float* r,
                                     const int32_t* drafts, const float* u, uint64_t seed, uint64_t offset,
                                     int64_t B, int64_t V, int32_t* sel_index, int32_t* sel_token,

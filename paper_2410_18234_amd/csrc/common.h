@@ -66,14 +66,25 @@ hipError_t launch_select_successive(const float* p, const float* q, const float*
 constexpr int kSuccessiveMaxK = 8;
 size_t workspace_bytes_optimum(int64_t B, int64_t V);
 size_t workspace_bytes_expsum(int64_t B, int64_t V, int L);
+// rsum (nullable): also the residual sums of Algorithm 1 with proposal r, kResParts fp64
+// partial sums of max(0, p - r) per kResSub-token sub-tile, [B][ceil(V / kResSub)][kResParts]
+// (the layout launch_select_accept_sums reads).
+constexpr int kResSub = 1024;
+constexpr int kResParts = 4;
 hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, int K,
-                                 float* r, int32_t* row_status, void* workspace, hipStream_t st);
+                                 float* r, int32_t* row_status, void* workspace, hipStream_t st,
+                                 double* rsum = nullptr);
 hipError_t launch_induced_successive_expsum(const float* p, const float* q, int64_t B, int64_t V, int K,
                                             float* r_stages, int32_t* row_status, void* workspace, hipStream_t st);
 // The K-draft quadrature with its workspace in the library's fixed device scratch
 // array (no allocation); B, V must fit in MDSS_NOALLOC_SCRATCH_BYTES.
 hipError_t launch_induced_expsum_noalloc(const float* p, const float* q, int64_t B, int64_t V, int K, float* r,
                                          int32_t* row_status, hipStream_t st);
+hipError_t launch_select_accept_sums(const float* p, const float* q, const float* q2, const float* r,
+                                     const int32_t* drafts, const float* u, uint64_t seed, uint64_t offset,
+                                     int64_t B, int64_t V, int K, int32_t* sel_index, int32_t* sel_token,
+                                     int32_t* out_token, uint8_t* accepted, double* residual_mass,
+                                     int32_t* row_status, void* workspace, hipStream_t st);
 hipError_t launch_induced_topk_expsum(const float* p, const float* q, int64_t B, int64_t V, int K, int s_max,
                                       float* r, int32_t* row_status, hipStream_t st);
 hipError_t launch_alphabet_truncate(const float* p, int64_t B, int64_t V, int m, float* pt, double* mass0,
@@ -109,6 +120,64 @@ hipError_t launch_select_accept(const float* p, const float* q, const float* q2,
 
 // ---------------------------------------------------------------- device helpers
 __device__ __forceinline__ bool bad_prob(float v) { return !(v >= 0.0f) || isinf(v); }
+
+// The residual of Algorithm 1 at one token, max(0, p - r), in fp64 (exact for fp32 p and r).
+__device__ __forceinline__ double residual_of(float pv, float rv) {
+  const double d = (double)pv - (double)rv;
+  return d > 0.0 ? d : 0.0;
+}
+
+// fp64 lane moves by DPP (each 32-bit half moved the same way)
+template <int CTRL, int ROW_MASK = 0xF, bool BOUND_ZERO = false>
+__device__ __forceinline__ double dpp64(double x) {
+  const uint64_t v = __double_as_longlong(x);
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)v, CTRL, ROW_MASK, 0xF, BOUND_ZERO);
+  const uint32_t hi = __builtin_amdgcn_update_dpp(0u, (uint32_t)(v >> 32), CTRL, ROW_MASK, 0xF, BOUND_ZERO);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+// x + the value of the partner lane of a gfx950 row swap (ROW) or half swap
+template <bool ROW>
+__device__ __forceinline__ double swap_sum64(double x) {
+  const uint64_t v = __double_as_longlong(x);
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  const auto a = ROW ? __builtin_amdgcn_permlane16_swap(lo, lo, false, false)
+                     : __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+  const auto c = ROW ? __builtin_amdgcn_permlane16_swap(hi, hi, false, false)
+                     : __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+  return __longlong_as_double((long long)(((uint64_t)c[0] << 32) | a[0])) +
+         __longlong_as_double((long long)(((uint64_t)c[1] << 32) | a[1]));
+}
+// Sum over the 64 lanes of a wave, in every lane: quad permutations and row
+// rotations within each 16-lane row, then the row and half swaps (all lanes active).
+__device__ __forceinline__ double wave_sum_dpp(double x) {
+  x += dpp64<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp64<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp64<0x124>(x);  // row_ror:4
+  x += dpp64<0x128>(x);  // row_ror:8
+  x = swap_sum64<true>(x);
+  return swap_sum64<false>(x);
+}
+// Inclusive prefix sum over the 64 lanes of a wave (fixed order): Hillis-Steele
+// within each 16-lane row by DPP row shifts (lanes shifted in from outside the
+// row read 0), then each row adds the totals of the rows before it, read from
+// lanes 15, 31 and 47.
+__device__ __forceinline__ double wave_inclusive_scan_dpp(double x, int lane) {
+  x += dpp64<0x111, 0xF, true>(x);  // row_shr:1
+  x += dpp64<0x112, 0xF, true>(x);  // row_shr:2
+  x += dpp64<0x114, 0xF, true>(x);  // row_shr:4
+  x += dpp64<0x118, 0xF, true>(x);  // row_shr:8
+  const uint64_t v = __double_as_longlong(x);
+  const auto rd = [&](int l) {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, l), hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), l);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+  };
+  const double t0 = rd(15), t1 = rd(31), t2 = rd(47);
+  const int row = lane >> 4;
+  const double c01 = t0 + t1;
+  const double carry = row == 0 ? 0.0 : (row == 1 ? t0 : (row == 2 ? c01 : c01 + t2));
+  return row == 0 ? x : x + carry;
+}
+
 
 // Philox4x32-10 (Salmon et al., SC'11): ten rounds of the 4x32 S-box with the
 // published multipliers and Weyl key increments.

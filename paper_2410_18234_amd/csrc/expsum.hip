@@ -1228,14 +1228,34 @@ __device__ __forceinline__ void es_load_eval(const float* __restrict__ p, const 
   }
 }
 
+// Residual sums of Algorithm 1 (kRes): per 1024-token tile, each wave's fp64 sum of
+// max(0, p - r) over its 256 tokens (r as stored), at rsum[(b nsub + tile) 4 + wave]
+// (NaN where a p or r is not a probability).
+__device__ __forceinline__ void es_residual_sums(const float (&pc)[kEsTokPer], const float (&rc)[kEsTokPer],
+                                                 double* __restrict__ rsum, int64_t b, int64_t tile, int64_t nsub,
+                                                 int lane, int wid) {
+  double local = 0.0;
+  bool bad = false;
+#pragma unroll
+  for (int i = 0; i < kEsTokPer; ++i) {
+    bad |= bad_prob(pc[i]) || bad_prob(rc[i]);
+    local += residual_of(pc[i], rc[i]);
+  }
+  const double tot = wave_sum_dpp(local);
+  const bool any_bad = __builtin_amdgcn_ballot_w64(bad) != 0;
+  if (lane == 0) rsum[(b * nsub + tile) * kEsWaves + wid] = any_bad ? (double)NAN : tot;
+}
+
 // Workgroup w takes the tiles [w per, (w + 1) per) of the B * T2 (row, tile)
 // pairs, row-major.  A tile's weight range comes from the moments record of
 // the 4096-token tile that holds it, so evaluation needs no statistics pass.
-template <int L>
+// kRes: the residual sums of Algorithm 1 are written too (rsum).
+template <int L, bool kRes>
 __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __restrict__ p,
                                                               const float* __restrict__ q1,
                                                               const float* __restrict__ q2, int64_t V, int K,
-                                                              float* __restrict__ r, int64_t G, int per, EsWork es) {
+                                                              float* __restrict__ r, int64_t G, int per, EsWork es,
+                                                              double* __restrict__ rsum, int64_t nsub) {
   static_assert(kEsMomTile % kEsTokTile == 0, "an evaluation tile lies in one moments tile");
   __shared__ __align__(16) float s_a[L][kEsTabRows * kEsPolyStride];  // A_n(k0 = kt + 1 + d) 2^-tau
   __shared__ float s_r[L][kEsTabRows];                                // log2(e) a_(kt+1+d) 2^-tau
@@ -1276,6 +1296,13 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
 #pragma unroll
         for (int i = 0; i < kEsTokPer; ++i)
           if (whole || base + i * kEsThreads + tid < V) rb[i * kEsThreads] = NAN;
+      }
+      if (kRes) {  // the residual sums from the r written (a flagged row: NaN)
+        float rc[kEsTokPer];
+#pragma unroll
+        for (int i = 0; i < kEsTokPer; ++i)
+          rc[i] = flags ? NAN : ((whole || base + i * kEsThreads + tid < V) ? rb[i * kEsThreads] : 0.0f);
+        es_residual_sums(pc, rc, rsum, bb, tt, nsub, tid & 63, tid >> 6);
       }
       continue;
     }
@@ -1422,6 +1449,7 @@ __global__ __launch_bounds__(kEsThreads) void es_eval_kernel(const float* __rest
       for (int i = 0; i < kEsTokPer; ++i)
         if (base + i * kEsThreads + tid < V) rb[i * kEsThreads] = out[i];
     }
+    if (kRes) es_residual_sums(pc, out, rsum, bb, tt, nsub, tid & 63, tid >> 6);  // tokens past V: p = r = 0
   }
 }
 
@@ -1814,7 +1842,9 @@ size_t workspace_bytes_expsum(int64_t B, int64_t V, int L) {
 
 // q2 == nullptr: K i.i.d. drafts from q1; else two draft laws (K = 2).
 hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, int K,
-                                 float* r, int32_t* row_status, void* workspace, hipStream_t st) {
+                                 float* r, int32_t* row_status, void* workspace, hipStream_t st, double* rsum) {
+  static_assert(kEsTokTile == kResSub && kEsWaves == kResParts, "one residual sum per wave and evaluation tile");
+  const int64_t nsub = (V + kResSub - 1) / kResSub;
   const int L = (q2 != nullptr) ? 2 : 1;
   EsWork es;
   carve_es(workspace, B, V, L, &es);
@@ -1825,15 +1855,27 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
   if (L == 1) {
     hipLaunchKernelGGL((es_coef_kernel<1>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
                        row_status);
-    const unsigned n2 = es_grid(es_eval_kernel<1>, G2, kEsSlotEval1);
-    hipLaunchKernelGGL((es_eval_kernel<1>), dim3(n2), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, G2,
-                       (int)((G2 + n2 - 1) / n2), es);
+    if (rsum) {  // on the plain variant's grid (its lower occupancy: 1 us faster on 256 x 32000 than its own)
+      const unsigned n2 = es_grid(es_eval_kernel<1, false>, G2, kEsSlotEval1);
+      hipLaunchKernelGGL((es_eval_kernel<1, true>), dim3(n2), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, G2,
+                         (int)((G2 + n2 - 1) / n2), es, rsum, nsub);
+    } else {
+      const unsigned n2 = es_grid(es_eval_kernel<1, false>, G2, kEsSlotEval1);
+      hipLaunchKernelGGL((es_eval_kernel<1, false>), dim3(n2), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, G2,
+                         (int)((G2 + n2 - 1) / n2), es, rsum, nsub);
+    }
   } else {
     hipLaunchKernelGGL((es_coef_kernel<2>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
                        row_status);
-    const unsigned n2 = es_grid(es_eval_kernel<2>, G2, kEsSlotEval2);
-    hipLaunchKernelGGL((es_eval_kernel<2>), dim3(n2), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, G2,
-                       (int)((G2 + n2 - 1) / n2), es);
+    if (rsum) {
+      const unsigned n2 = es_grid(es_eval_kernel<2, false>, G2, kEsSlotEval2);
+      hipLaunchKernelGGL((es_eval_kernel<2, true>), dim3(n2), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, G2,
+                         (int)((G2 + n2 - 1) / n2), es, rsum, nsub);
+    } else {
+      const unsigned n2 = es_grid(es_eval_kernel<2, false>, G2, kEsSlotEval2);
+      hipLaunchKernelGGL((es_eval_kernel<2, false>), dim3(n2), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, G2,
+                         (int)((G2 + n2 - 1) / n2), es, rsum, nsub);
+    }
   }
   return hipGetLastError();
 }

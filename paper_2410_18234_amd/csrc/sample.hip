@@ -7,6 +7,8 @@
 // uniforms as 24-bit dyadics, so the accept test u * r(Y) < p(Y) is exact.
 #include "common.h"
 
+#include <algorithm>
+
 #include <math.h>
 
 namespace mdss {
@@ -189,9 +191,11 @@ constexpr int kAccThreads = 256;                             // (B)
 constexpr int kAccRowsPerDraw = kAccThreads / 64;            // positions per workgroup of (B)
 
 struct AccWork {
-  double* sub;   // [B][nsub] residual sums per sub-tile, written by (A), read by (B)
-  int64_t nsub;  // sub-tiles per row, ceil(V / 256)
+  double* sub;   // [B][nsub][parts] residual sums per sub-tile: one per 256 tokens (written by (A)) or four
+                 // partial sums per 1024 tokens (written with r by the quadrature's evaluation), read by (B)
+  int64_t nsub;  // sub-tiles per row
 };
+static_assert(kAccSub % 256 == 0 && kResSub % 256 == 0, "whole float4 per lane in a sub-tile's search");
 
 template <bool kVec>
 __device__ __forceinline__ void load4(const float* __restrict__ a, int64_t x0, int64_t V, float v[4]) {
@@ -205,62 +209,6 @@ __device__ __forceinline__ void load4(const float* __restrict__ a, int64_t x0, i
 #pragma unroll
     for (int i = 0; i < 4; ++i) v[i] = (x0 + i < V) ? a[x0 + i] : 0.0f;
   }
-}
-
-__device__ __forceinline__ double residual_of(float pv, float rv) {
-  const double d = (double)pv - (double)rv;
-  return d > 0.0 ? d : 0.0;
-}
-
-// fp64 lane moves by DPP (each 32-bit half moved the same way)
-template <int CTRL, int ROW_MASK = 0xF, bool BOUND_ZERO = false>
-__device__ __forceinline__ double dpp64(double x) {
-  const uint64_t v = __double_as_longlong(x);
-  const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)v, CTRL, ROW_MASK, 0xF, BOUND_ZERO);
-  const uint32_t hi = __builtin_amdgcn_update_dpp(0u, (uint32_t)(v >> 32), CTRL, ROW_MASK, 0xF, BOUND_ZERO);
-  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
-// x + the value of the partner lane of a gfx950 row swap (ROW) or half swap
-template <bool ROW>
-__device__ __forceinline__ double swap_sum64(double x) {
-  const uint64_t v = __double_as_longlong(x);
-  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-  const auto a = ROW ? __builtin_amdgcn_permlane16_swap(lo, lo, false, false)
-                     : __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
-  const auto c = ROW ? __builtin_amdgcn_permlane16_swap(hi, hi, false, false)
-                     : __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
-  return __longlong_as_double((long long)(((uint64_t)c[0] << 32) | a[0])) +
-         __longlong_as_double((long long)(((uint64_t)c[1] << 32) | a[1]));
-}
-// Sum over the 64 lanes of a wave, in every lane: quad permutations and row
-// rotations within each 16-lane row, then the row and half swaps (all lanes active).
-__device__ __forceinline__ double wave_sum_dpp(double x) {
-  x += dpp64<0xB1>(x);   // quad_perm [1,0,3,2]
-  x += dpp64<0x4E>(x);   // quad_perm [2,3,0,1]
-  x += dpp64<0x124>(x);  // row_ror:4
-  x += dpp64<0x128>(x);  // row_ror:8
-  x = swap_sum64<true>(x);
-  return swap_sum64<false>(x);
-}
-// Inclusive prefix sum over the 64 lanes of a wave (fixed order): Hillis-Steele
-// within each 16-lane row by DPP row shifts (lanes shifted in from outside the
-// row read 0), then each row adds the totals of the rows before it, read from
-// lanes 15, 31 and 47.
-__device__ __forceinline__ double wave_inclusive_scan_dpp(double x, int lane) {
-  x += dpp64<0x111, 0xF, true>(x);  // row_shr:1
-  x += dpp64<0x112, 0xF, true>(x);  // row_shr:2
-  x += dpp64<0x114, 0xF, true>(x);  // row_shr:4
-  x += dpp64<0x118, 0xF, true>(x);  // row_shr:8
-  const uint64_t v = __double_as_longlong(x);
-  const auto rd = [&](int l) {
-    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, l), hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), l);
-    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-  };
-  const double t0 = rd(15), t1 = rd(31), t2 = rd(47);
-  const int row = lane >> 4;
-  const double c01 = t0 + t1;
-  const double carry = row == 0 ? 0.0 : (row == 1 ? t0 : (row == 2 ? c01 : c01 + t2));
-  return row == 0 ? x : x + carry;
 }
 
 // Selection arguments of the fused form (selection and Algorithm 1 in one
@@ -601,8 +549,10 @@ __global__ __launch_bounds__(kAccSegThreads) void accept_seg_kernel(const float*
   if (lane < kAccSubPerWave && sub0 + lane < aw.nsub) aw.sub[b * aw.nsub + sub0 + lane] = v;
 }
 
-// Segment form (B): one wave per position.
-template <bool kVec, bool kSel>
+// Segment form (B): one wave per position.  kParts partial sums per kSub-token sub-tile
+// in the workspace (one per 256 tokens from (A); four per 1024 tokens from the
+// quadrature's evaluation), added in order.
+template <bool kVec, bool kSel, int kParts, int kSub>
 __global__ __launch_bounds__(kAccThreads) void accept_draw_kernel(
     const float* __restrict__ p, const float* __restrict__ r, const int32_t* __restrict__ sel_token,
     const float* __restrict__ u, uint64_t seed, uint64_t offset, int64_t B, int64_t V,
@@ -613,13 +563,19 @@ __global__ __launch_bounds__(kAccThreads) void accept_draw_kernel(
   if (b >= B) return;
   const float* pb = p + b * V;
   const float* rb = r + b * V;
-  const double* sb = aw.sub + b * aw.nsub;
+  const double* sb = aw.sub + b * aw.nsub * kParts;
+  const auto sub_at = [&](int64_t s) -> double {  // the residual sum of sub-tile s
+    double v = sb[s * kParts];
+#pragma unroll
+    for (int k = 1; k < kParts; ++k) v += sb[s * kParts + k];
+    return v;
+  };
   // Z and the running sums: lane l takes the sub-tiles [l per, (l + 1) per), in order,
   // read together with the decision's loads
   const int64_t per = (aw.nsub + 63) / 64;
   const int64_t s_lo = lane * per, s_hi = (s_lo + per < aw.nsub) ? s_lo + per : aw.nsub;
   double lane_sum = 0.0;
-  for (int64_t s = s_lo; s < s_hi; ++s) lane_sum += sb[s];
+  for (int64_t s = s_lo; s < s_hi; ++s) lane_sum += sub_at(s);
   float uu[3];
   position_uniforms(u, seed, offset, b, uu);
   const Decision d = take_decision<kSel>(pb, rb, sel_token, sel, b, V, uu);
@@ -665,7 +621,7 @@ __global__ __launch_bounds__(kAccThreads) void accept_draw_kernel(
   double my_prev = 0.0, run = excl;
   for (int64_t s = s_lo; s < s_hi; ++s) {
     const double prev = run;
-    run += sb[s];
+    run += sub_at(s);
     if (run > thr) {
       my_s = s;
       my_prev = prev;
@@ -683,7 +639,7 @@ __global__ __launch_bounds__(kAccThreads) void accept_draw_kernel(
     // rounding put u_res * Z at or past every running sum: the last sub-tile with mass
     int64_t last = -1;
     for (int64_t s = s_lo; s < s_hi; ++s)
-      if (sb[s] > 0.0) last = s;
+      if (sub_at(s) > 0.0) last = s;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
       const int64_t o = __shfl_xor(last, off, 64);
@@ -700,14 +656,18 @@ __global__ __launch_bounds__(kAccThreads) void accept_draw_kernel(
     }
     return;
   }
-  // the token inside sub-tile s_star: 4 entries per lane, lane prefix, then the lane's own entries
-  const int64_t x0 = s_star * kAccSub + 4 * lane;
-  float pv[4], rv[4];
-  load4<kVec>(pb, x0, V, pv);
-  load4<kVec>(rb, x0, V, rv);
-  double rs[4], local = 0.0;
+  // the token inside sub-tile s_star: kPer consecutive entries per lane, lane prefix, then the lane's own entries
+  constexpr int kPer = kSub / 64;
+  const int64_t x0 = s_star * kSub + kPer * lane;
+  float pv[kPer], rv[kPer];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int j = 0; j < kPer; j += 4) {
+    load4<kVec>(pb, x0 + j, V, pv + j);
+    load4<kVec>(rb, x0 + j, V, rv + j);
+  }
+  double rs[kPer], local = 0.0;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
     rs[i] = residual_of(pv[i], rv[i]);
     local += rs[i];
   }
@@ -717,7 +677,7 @@ __global__ __launch_bounds__(kAccThreads) void accept_draw_kernel(
   double c = base + le;
   int my = -1;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < kPer; ++i) {
     c += rs[i];
     if (my < 0 && rs[i] > 0.0 && c > thr) my = i;
   }
@@ -725,12 +685,12 @@ __global__ __launch_bounds__(kAccThreads) void accept_draw_kernel(
   int64_t found;
   if (h2) {
     const int src = __ffsll((long long)h2) - 1;
-    found = s_star * kAccSub + 4 * src + __shfl(my, src, 64);
+    found = s_star * kSub + kPer * src + __shfl(my, src, 64);
   } else {
     // fallback: the last token of the sub-tile with a positive residual
     int64_t last = -1;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < kPer; ++i)
       if (x0 + i < V && rs[i] > 0.0) last = x0 + i;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -801,11 +761,11 @@ hipError_t launch_accept_impl(const float* p, const float* r, const int32_t* sel
   const dim3 gb((unsigned)((B + kAccRowsPerDraw - 1) / kAccRowsPerDraw));
   if (vec) {
     hipLaunchKernelGGL((accept_seg_kernel<true>), ga, dim3(kAccSegThreads), 0, st, p, r, V, residual, aw);
-    hipLaunchKernelGGL((accept_draw_kernel<true, kSel>), gb, dim3(kAccThreads), 0, st, p, r, sel_token, u, seed,
+    hipLaunchKernelGGL((accept_draw_kernel<true, kSel, 1, kAccSub>), gb, dim3(kAccThreads), 0, st, p, r, sel_token, u, seed,
                        offset, B, V, out_token, accepted, residual_mass, row_status, sel, aw);
   } else {
     hipLaunchKernelGGL((accept_seg_kernel<false>), ga, dim3(kAccSegThreads), 0, st, p, r, V, residual, aw);
-    hipLaunchKernelGGL((accept_draw_kernel<false, kSel>), gb, dim3(kAccThreads), 0, st, p, r, sel_token, u, seed,
+    hipLaunchKernelGGL((accept_draw_kernel<false, kSel, 1, kAccSub>), gb, dim3(kAccThreads), 0, st, p, r, sel_token, u, seed,
                        offset, B, V, out_token, accepted, residual_mass, row_status, sel, aw);
   }
   return hipGetLastError();
@@ -814,8 +774,30 @@ hipError_t launch_accept_impl(const float* p, const float* r, const int32_t* sel
 }  // namespace
 
 size_t workspace_bytes_accept(int64_t B, int64_t V) {
-  const int64_t nsub = (V + kAccSub - 1) / kAccSub;
-  return align256_acc(sizeof(double) * (size_t)(B * nsub));
+  const int64_t n1 = (V + kAccSub - 1) / kAccSub, n4 = (V + kResSub - 1) / kResSub;  // the two layouts
+  return align256_acc(sizeof(double) * (size_t)(B * std::max(n1, n4 * kResParts)));
+}
+
+// Selection and Algorithm 1 from the residual sums the quadrature's evaluation wrote
+// with r (four partial sums per 1024-token sub-tile): the segment form's (B) alone.
+hipError_t launch_select_accept_sums(const float* p, const float* q, const float* q2, const float* r,
+                                     const int32_t* drafts, const float* u, uint64_t seed, uint64_t offset,
+                                     int64_t B, int64_t V, int K, int32_t* sel_index, int32_t* sel_token,
+                                     int32_t* out_token, uint8_t* accepted, double* residual_mass,
+                                     int32_t* row_status, void* workspace, hipStream_t st) {
+  const SelArgs sel = {q, q2, drafts, K, sel_index, sel_token};
+  const bool vec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(r)) % 16 == 0);
+  AccWork aw;
+  aw.sub = static_cast<double*>(workspace);
+  aw.nsub = (V + kResSub - 1) / kResSub;
+  const dim3 gb((unsigned)((B + kAccRowsPerDraw - 1) / kAccRowsPerDraw));
+  if (vec)
+    hipLaunchKernelGGL((accept_draw_kernel<true, true, kResParts, kResSub>), gb, dim3(kAccThreads), 0, st, p, r, nullptr, u,
+                       seed, offset, B, V, out_token, accepted, residual_mass, row_status, sel, aw);
+  else
+    hipLaunchKernelGGL((accept_draw_kernel<false, true, kResParts, kResSub>), gb, dim3(kAccThreads), 0, st, p, r, nullptr, u,
+                       seed, offset, B, V, out_token, accepted, residual_mass, row_status, sel, aw);
+  return hipGetLastError();
 }
 
 hipError_t launch_accept(const float* p, const float* r, const int32_t* sel_token, const float* u, uint64_t seed,

@@ -267,3 +267,30 @@ def test_topk_expsum_argument_errors(lib):
     assert f(FAKE, FAKE, 4, 16, 3, 0, FAKE, None, None) == 3
     assert f(FAKE, FAKE, 4, 16, 3, 4097, FAKE, None, None) == 3
     assert f(None, None, 0, 16, 3, 8, None, None, None) == 0  # empty batch: nothing read or launched
+
+
+def test_summed_form_argument_errors(lib):
+    f = lib.mdss_induced_dist_expsum_sums
+    f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    ws = lib.mdss_workspace_bytes_expsum(4, 16, 2)
+    acc = lib.mdss_workspace_bytes_accept(4, 16)
+    assert f(None, FAKE, 4, 16, 2, FAKE, None, FAKE, ws, FAKE, acc, None) == 1
+    assert f(FAKE, FAKE, 4, 1, 2, FAKE, None, FAKE, ws, FAKE, acc, None) == 2
+    assert f(FAKE, FAKE, 4, 16, 9, FAKE, None, FAKE, ws, FAKE, acc, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 2, FAKE, None, FAKE, ws - 1, FAKE, acc, None) == 5
+    assert f(FAKE, FAKE, 4, 16, 2, FAKE, None, FAKE, ws, None, acc, None) == 5
+    assert f(FAKE, FAKE, 4, 16, 2, FAKE, None, FAKE, ws, FAKE, acc - 1, None) == 5
+    assert f(None, None, 0, 16, 2, None, None, None, 0, None, 0, None) == 0
+    g = lib.mdss_select_accept_sums
+    g.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64,
+                                          ctypes.c_int32] + [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p]
+    args = lambda **kw: [kw.get("p", FAKE), FAKE, FAKE, FAKE, None, 0, 0, kw.get("B", 4), 16, kw.get("K", 2),
+                         None, None, kw.get("out", FAKE), FAKE, None, None, kw.get("ws", FAKE),
+                         kw.get("wsb", acc), None]
+    assert g(*args(p=None)) == 1
+    assert g(*args(out=None)) == 1
+    assert g(*args(K=9)) == 3
+    assert g(*args(ws=None)) == 5
+    assert g(*args(wsb=acc - 1)) == 5
+    assert g(*args(B=0, p=None)) == 0
