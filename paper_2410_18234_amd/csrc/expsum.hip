@@ -1893,9 +1893,10 @@ hipError_t launch_induced_successive_expsum(const float* p, const float* q, int6
 
 // ------------------------------------------------------------------ top-s rows
 // K i.i.d. drafts from a draft truncated to at most s_max tokens (a top-s draft):
-// one workgroup of 1024 threads per row streams p and q once, writes r = 0 at
-// q = 0, keeps the support (index, p, q, w) in LDS and takes the trapezoidal rule
-// of the tiled path, on the same grid, directly over it:
+// one workgroup of 1024 threads per row streams p and q once (twice when one wave
+// meets more than kTkSeg support tokens), writes r = 0 (the support's entries are
+// written again at the end), keeps the support (index, p, q, w) in LDS and takes the
+// trapezoidal rule of the tiled path, on the same grid, directly over it:
 //   S_k = sum over the support of q(x) exp(-a_k w(x))      (p(x) > 0),
 //   r(y) = p(y) sum_k c_k exp(-a_k w(y)),  c_k = K h a_k (S_k [+ Q0 for K >= 3])^(K-1),
 // every (node, token) term exactly (no windows, expansions or polynomial tables),
@@ -1910,6 +1911,8 @@ constexpr int kTkWaves = kTkThreads / 64;
 constexpr int kTkCap = MDSS_K3_MAX_SUPPORT;   // support entries held in LDS
 constexpr int kTkPer = 4;                     // tokens per thread per streaming step
 constexpr int kTkStep = kTkThreads * kTkPer;  // 4096 tokens per step
+constexpr int kTkSeg = kTkCap / kTkWaves;     // support tokens of one wave's stream segment
+constexpr int kTkAhead = 2;                   // streaming steps in flight (64 KB of p and q per workgroup)
 constexpr int kTkE = 4;                       // support entries per lane in the node sums
 constexpr int kTkGroup = 64 * kTkE;           // entries of one wave group
 constexpr int kTkMaxRange = 100;              // binary exponent span of the weights kept in fp32
@@ -1929,13 +1932,24 @@ __device__ __forceinline__ int tk_scan_int(int v, int lane) {
   return v + (row == 0 ? 0 : (row == 1 ? t0 : (row == 2 ? t0 + t1 : t0 + t1 + t2)));
 }
 
+// A streaming step's p and q (0 past the row's end); a whole step without bounds checks.
 __device__ __forceinline__ void tk_load(const float* __restrict__ pb, const float* __restrict__ qb, int64_t V,
                                         int64_t x0, int tid, float (&pv)[kTkPer], float (&qv)[kTkPer]) {
+  const float* ps = pb + x0 + tid;
+  const float* qs = qb + x0 + tid;
+  if (x0 + kTkStep <= V) {  // uniform
 #pragma unroll
-  for (int i = 0; i < kTkPer; ++i) {
-    const int64_t x = x0 + i * kTkThreads + tid;
-    pv[i] = (x < V) ? pb[x] : 0.0f;
-    qv[i] = (x < V) ? qb[x] : 0.0f;
+    for (int i = 0; i < kTkPer; ++i) {
+      pv[i] = ps[i * kTkThreads];
+      qv[i] = qs[i * kTkThreads];
+    }
+  } else {
+    const int rest = (int)(V - x0) - tid;
+#pragma unroll
+    for (int i = 0; i < kTkPer; ++i) {
+      pv[i] = (i * kTkThreads < rest) ? ps[i * kTkThreads] : 0.0f;
+      qv[i] = (i * kTkThreads < rest) ? qs[i * kTkThreads] : 0.0f;
+    }
   }
 }
 
@@ -1956,67 +1970,141 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
   __shared__ double s_d[kTkWaves];
   __shared__ double s_e[kTkWaves][2];
   __shared__ int s_n[kTkWaves];
+  __shared__ EsPlan s_plan;
+  __shared__ int s_sidx[kTkCap];  // while streaming: wave w's support tokens at [w kTkSeg, (w + 1) kTkSeg)
+  __shared__ float s_sp[kTkCap];
+  __shared__ float s_sq[kTkCap];
+  __shared__ int s_wn[kTkWaves];
   const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t b = blockIdx.x;
   const float* pb = p + b * V;
   const float* qb = q + b * V;
   float* rb = r + b * V;
 
-  // (1) stream the row, two steps in flight: r = 0 at q = 0 and the support compacted in
-  //     token order (token x0 + 1024 i + thread; counts per (slot i, wave), one scan a step)
-  float pa[kTkPer], qa[kTkPer], pn[kTkPer], qn[kTkPer];
-  tk_load(pb, qb, V, 0, tid, pa, qa);
-  tk_load(pb, qb, V, kTkStep, tid, pn, qn);
-  int bad = 0, running = 0;
+  // (1) stream the row, kTkAhead steps in flight: r = 0, the probability checks, and each
+  //     wave's support tokens appended to its own LDS segment (no barrier a step)
+  float pf[kTkAhead][kTkPer], qf[kTkAhead][kTkPer];  // the next kTkAhead steps, in flight
+#pragma unroll
+  for (int j = 0; j < kTkAhead; ++j) tk_load(pb, qb, V, (int64_t)j * kTkStep, tid, pf[j], qf[j]);
+  int bad = 0, wn = 0;  // wn: this wave's support tokens so far (uniform)
   const int64_t nstep = (V + kTkStep - 1) / kTkStep;
   for (int64_t st = 0; st < nstep; ++st) {
-    const int par = (int)(st & 1);
     const int64_t x0 = st * kTkStep;
     float pc[kTkPer], qc[kTkPer];
 #pragma unroll
     for (int i = 0; i < kTkPer; ++i) {
-      pc[i] = pa[i];
-      qc[i] = qa[i];
-      pa[i] = pn[i];
-      qa[i] = qn[i];
-    }
-    if (st + 2 < nstep) tk_load(pb, qb, V, x0 + 2 * kTkStep, tid, pn, qn);
+      pc[i] = pf[0][i];
+      qc[i] = qf[0][i];
 #pragma unroll
-    for (int i = 0; i < kTkPer; ++i) {
-      const int64_t x = x0 + i * kTkThreads + tid;
-      // NaN, -inf, a negative normal or denormal, +inf (-0 is a zero probability)
-      bad |= __builtin_amdgcn_classf(pc[i], 0x21F) | __builtin_amdgcn_classf(qc[i], 0x21F);
-      const bool sup = qc[i] > 0.0f;
-      if (!sup && x < V) rb[x] = 0.0f;
-      const int cnt = __builtin_popcountll(__builtin_amdgcn_ballot_w64(sup));
-      if (lane == 0) s_cnt[par][i * kTkWaves + wid] = cnt;
-    }
-    es_lds_barrier();  // (s_cnt by step parity: a step's counts are read before the next barrier)
-    const int c = s_cnt[par][lane];
-    const int incl = tk_scan_int(c, lane);
-    const int ex = incl - c;
-#pragma unroll
-    for (int i = 0; i < kTkPer; ++i) {
-      const bool sup = qc[i] > 0.0f;
-      const uint64_t mask = __builtin_amdgcn_ballot_w64(sup);
-      const int pos = running + __builtin_amdgcn_readlane(ex, i * kTkWaves + wid) +
-                      (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-      if (sup && pos < kTkCap) {
-        s_idx[pos] = (int)(x0 + i * kTkThreads + tid);
-        s_p[pos] = pc[i];
-        s_q[pos] = qc[i];
+      for (int j = 0; j + 1 < kTkAhead; ++j) {
+        pf[j][i] = pf[j + 1][i];
+        qf[j][i] = qf[j + 1][i];
       }
     }
-    running += __builtin_amdgcn_readlane(incl, 63);  // the same in every wave
-  }
-  const int n = running;
-  const bool wave_bad = __builtin_amdgcn_ballot_w64(bad != 0) != 0;  // every lane votes
-  if (lane == 0) s_flag[wid] = wave_bad ? 1 : 0;
-  __syncthreads();  // the list is complete (and a flagged row's NaN below follows its zeros)
-  int flags = 0;
+    if (st + kTkAhead < nstep) tk_load(pb, qb, V, x0 + kTkAhead * kTkStep, tid, pf[kTkAhead - 1], qf[kTkAhead - 1]);
+    float* rs = rb + x0 + tid;
+    const int rest = (x0 + kTkStep <= V) ? kTkStep : (int)(V - x0) - tid;  // a whole step: every token
+    // r = 0 over the whole step in full lines (a masked store would leave partial lines);
+    // the support's values overwrite these after the sums, past workgroup barriers
+    if (rest >= kTkStep) {  // uniform
 #pragma unroll
-  for (int i = 0; i < kTkWaves; ++i) flags |= s_flag[i];
+      for (int i = 0; i < kTkPer; ++i) rs[i * kTkThreads] = 0.0f;
+    } else {
+#pragma unroll
+      for (int i = 0; i < kTkPer; ++i)
+        if (i * kTkThreads < rest) rs[i * kTkThreads] = 0.0f;
+    }
+    const int xs = (int)x0 + tid;  // rows < 2^31 tokens
+#pragma unroll
+    for (int i = 0; i < kTkPer; ++i) {
+      // NaN, -inf, a negative normal or denormal, +inf (-0 is a zero probability)
+      bad |= __builtin_amdgcn_classf(pc[i], 0x21F) | __builtin_amdgcn_classf(qc[i], 0x21F);
+      const bool sup = qc[i] > 0.0f;  // 0 past the row's end
+      const uint64_t mask = __builtin_amdgcn_ballot_w64(sup);
+      const int pos = wn + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+      if (sup && pos < kTkSeg) {
+        const int at = wid * kTkSeg + pos;
+        s_sidx[at] = xs + i * kTkThreads;
+        s_sp[at] = pc[i];
+        s_sq[at] = qc[i];
+      }
+      wn += (int)__builtin_popcountll(mask);
+    }
+  }
+  const bool wave_bad = __builtin_amdgcn_ballot_w64(bad != 0) != 0;  // every lane votes
+  if (lane == 0) {
+    s_flag[wid] = wave_bad ? 1 : 0;
+    s_wn[wid] = wn;
+  }
+  __syncthreads();  // the segments are complete (and a flagged row's NaN below follows its zeros)
+  int flags = 0, n = 0, wmax_n = 0, base = 0;
+#pragma unroll
+  for (int i = 0; i < kTkWaves; ++i) {
+    flags |= s_flag[i];
+    base += (i < wid) ? s_wn[i] : 0;
+    n += s_wn[i];
+    wmax_n = max(wmax_n, s_wn[i]);
+  }
   flags = flags ? kRowBadProb : (n > s_max ? kRowSupport : 0);
+  if (!flags) {  // uniform; here n <= s_max <= kTkCap
+    if (wmax_n <= kTkSeg) {
+      // (1b) the list: the segments in wave order (each in its tokens' stream order)
+      for (int j = lane; j < wn; j += 64) {
+        s_idx[base + j] = s_sidx[wid * kTkSeg + j];
+        s_p[base + j] = s_sp[wid * kTkSeg + j];
+        s_q[base + j] = s_sq[wid * kTkSeg + j];
+      }
+    } else {
+      // (1c) a wave met more than kTkSeg support tokens: the row once more, its support
+      //      compacted in token order (token x0 + 1024 i + thread; counts per (slot i,
+      //      wave), one scan a step)
+#pragma unroll
+      for (int j = 0; j < kTkAhead; ++j) tk_load(pb, qb, V, (int64_t)j * kTkStep, tid, pf[j], qf[j]);
+      int running = 0;
+      for (int64_t st = 0; st < nstep; ++st) {
+        const int par = (int)(st & 1);
+        const int64_t x0 = st * kTkStep;
+        float pc[kTkPer], qc[kTkPer];
+#pragma unroll
+        for (int i = 0; i < kTkPer; ++i) {
+          pc[i] = pf[0][i];
+          qc[i] = qf[0][i];
+#pragma unroll
+          for (int j = 0; j + 1 < kTkAhead; ++j) {
+            pf[j][i] = pf[j + 1][i];
+            qf[j][i] = qf[j + 1][i];
+          }
+        }
+        if (st + kTkAhead < nstep)
+          tk_load(pb, qb, V, x0 + kTkAhead * kTkStep, tid, pf[kTkAhead - 1], qf[kTkAhead - 1]);
+        uint64_t mask[kTkPer];
+#pragma unroll
+        for (int i = 0; i < kTkPer; ++i) {
+          mask[i] = __builtin_amdgcn_ballot_w64(qc[i] > 0.0f);
+          if (lane == 0) s_cnt[par][i * kTkWaves + wid] = (int)__builtin_popcountll(mask[i]);
+        }
+        es_lds_barrier();  // (s_cnt by step parity: a step's counts are read before the next barrier)
+        const int c = s_cnt[par][lane];
+        const int incl = tk_scan_int(c, lane);
+        const int ex = incl - c;
+        const int xs = (int)x0 + tid;
+#pragma unroll
+        for (int i = 0; i < kTkPer; ++i) {
+          const int pos = running + __builtin_amdgcn_readlane(ex, i * kTkWaves + wid) +
+                          (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask[i] >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)mask[i], 0u));
+          if (qc[i] > 0.0f && pos < kTkCap) {
+            s_idx[pos] = xs + i * kTkThreads;
+            s_p[pos] = pc[i];
+            s_q[pos] = qc[i];
+          }
+        }
+        running += __builtin_amdgcn_readlane(incl, 63);  // the same in every wave
+      }
+    }
+  }
+  __syncthreads();  // the list is complete
   const int nl = min(n, kTkCap);  // entries in LDS (n itself when the row is not flagged)
 
   // (2) weights and the row's statistics (entry e = thread + 1024 j)
@@ -2086,17 +2174,23 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
       wmax64 = fmax(wmax64, s_e[i][1]);
     }
   }
-  // the grid of the tiled path (same merge statistics, same plan)
-  EsMerge m;
-  m.wmin[0] = m.wmin[1] = npos > 0 ? wmin64 : INFINITY;
-  m.wmax[0] = m.wmax[1] = wmax64;
-  m.q0[0] = q0;
-  m.q0[1] = 0.0;
-  m.npos[0] = npos;
-  m.npos[1] = 0;
-  m.bad = 0;
-  m.wide = 0;
-  const EsPlan pl = es_make_plan<1>(m, K);
+  // the grid of the tiled path (same merge statistics, same plan), by wave 0 alone: its
+  // fp64 logarithms in every one of the sixteen waves would cost each SIMD four times over
+  if (wid == 0) {
+    EsMerge m;
+    m.wmin[0] = m.wmin[1] = npos > 0 ? wmin64 : INFINITY;
+    m.wmax[0] = m.wmax[1] = wmax64;
+    m.q0[0] = q0;
+    m.q0[1] = 0.0;
+    m.npos[0] = npos;
+    m.npos[1] = 0;
+    m.bad = 0;
+    m.wide = 0;
+    const EsPlan pw = es_make_plan<1>(m, K);
+    if (lane == 0) s_plan = pw;
+  }
+  __syncthreads();
+  const EsPlan pl = s_plan;
   if (!flags) flags = pl.flags;
   if (flags) {  // NaN over the whole row
     if (tid == 0 && row_status) row_status[b] |= flags;

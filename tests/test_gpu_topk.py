@@ -135,6 +135,38 @@ def test_support_of_the_whole_cap():
     assert np.all(np.abs(r3[rows, ys] - e3) <= RTOL_ROW * e3)
 
 
+def test_wave_segments_and_the_token_order_pass():
+    # while a row streams, each of the 16 waves keeps up to 256 support tokens of its own
+    # (wave w reads tokens 4096 s + 1024 i + 64 w + lane); a row in which one wave meets
+    # more is streamed again and compacted in token order.  Rows: wave 0 at exactly 256
+    # support tokens, wave 0 at 257, 1024 tokens spread over every wave
+    rng = np.random.default_rng(47)
+    V, B = 8192, 3
+    lanes = np.arange(64)
+    wave0 = lambda s: np.concatenate([s * 4096 + i * 1024 + lanes for i in range(4)])
+    P = rng.dirichlet(np.full(V, 0.4), size=B)
+    Q = np.zeros((B, V))
+    sup = [wave0(0), np.concatenate([wave0(0), wave0(1)[:1]]), rng.choice(V, 1024, replace=False)]
+    for b in range(B):
+        Q[b, sup[b]] = rng.gamma(0.5, size=len(sup[b])) + 1e-6
+    Q /= Q.sum(1, keepdims=True)
+    P, Q = P.astype(np.float32), Q.astype(np.float32)
+    assert [len(x) for x in sup] == [256, 257, 1024]
+    r2, st2 = tk_r(P, Q, 2, 1024)
+    assert np.all(st2 == 0)
+    assert np.all(r2[Q == 0] == 0.0)
+    ro2 = support_oracle(P, Q, 2)
+    assert np.all(rel_l1(r2, ro2) <= TIGHT), rel_l1(r2, ro2)
+    r3, st3 = tk_r(P, Q, 3, 1024)
+    rt3, _ = es_r(P, Q, 3)
+    assert np.all(st3 == 0)
+    assert np.all(r3[Q == 0] == 0.0)
+    assert np.all(rel_l1(r3, rt3) <= TIGHT), rel_l1(r3, rt3)
+    # the same rows again: bit-identical
+    r3b, _ = tk_r(P, Q, 3, 1024)
+    assert np.array_equal(r3, r3b)
+
+
 def test_k3top1024_full_size():
     # the 256 top-1024 rows of 32000 tokens: against the tiled quadrature (every row) and
     # the oracle (sampled entries: the largest r, the smallest weight, random support tokens)
