@@ -331,7 +331,8 @@ def main():
         ws_opt = torch.empty(mdss.workspace_bytes_optimum(B, V), dtype=torch.uint8, device=dev)
 
     def one_step(ev=None):
-        status.zero_()
+        if not use_sums:  # the summed form's r call sets the status words itself
+            status.zero_()
         if ev is not None:
             ev[0].record()
         if cfg.alphabet:

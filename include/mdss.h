@@ -165,7 +165,9 @@ mdss_status mdss_select_accept(const float* p, const float* q, const float* r, c
  * Algorithm 1 with proposal r needs: for every position and 1024-token
  * sub-tile, four fp64 partial sums of res(x) = max(0, p(x) - r(x)) (NaN where
  * a p or r is not a probability), written into accept_workspace (at least
- * mdss_workspace_bytes_accept(B, V) bytes).
+ * mdss_workspace_bytes_accept(B, V) bytes).  Unlike every other call, it SETS
+ * row_status[b] (nullable) to its own flags instead of OR-ing them in, so the
+ * status words need no clearing before it (it is the first call of a step).
  * mdss_select_accept_sums: selection and Algorithm 1 as mdss_select_accept,
  * with Z and the running sums taken from those partial sums instead of a pass
  * over the rows (the crossing sub-tile's 1024 entries are read again to find

@@ -408,10 +408,12 @@ def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[tor
     each row's support, rows with more than s_max tokens of q > 0 flagged as in "exact")."""
     B = p.shape[0]
     K = drafts.shape[1]
-    status = torch.zeros(B, dtype=torch.int32, device=p.device)
+    summed = method == "expsum" and not (K >= 3 and s_max > 0) and not want_residual
+    # the summed form's r call sets the status words itself; every other call ORs into them
+    status = (torch.empty if summed else torch.zeros)(B, dtype=torch.int32, device=p.device)
     if method == "expsum" and K >= 3 and s_max > 0:
         r = induced_dist_topk_expsum(p, q, K, s_max, row_status=status)
-    elif method == "expsum" and not want_residual:
+    elif summed:
         # Theorem 1's two steps sharing one pass over the rows: r and Algorithm 1's residual sums together
         acc_ws = torch.empty(workspace_bytes_accept(B, p.shape[1]), dtype=torch.uint8, device=p.device)
         r = induced_dist_expsum_sums(p, q, K, acc_ws, row_status=status)
@@ -730,7 +732,8 @@ def induced_dist_expsum_sums(p: torch.Tensor, q: torch.Tensor, K: int, accept_wo
                              workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """induced_dist_expsum, writing also the residual sums of Algorithm 1 into accept_workspace
     (a uint8 tensor of at least workspace_bytes_accept(B, V) bytes, kept for select_accept_sums;
-    it must not be the r call's own workspace)."""
+    it must not be the r call's own workspace).  row_status is set to this call's flags (not
+    OR-ed into): it needs no clearing before."""
     lib = load_library()
     B, V, dev = _pq(p, q)
     if r is None:

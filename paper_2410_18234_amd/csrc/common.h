@@ -68,7 +68,8 @@ size_t workspace_bytes_optimum(int64_t B, int64_t V);
 size_t workspace_bytes_expsum(int64_t B, int64_t V, int L);
 // rsum (nullable): also the residual sums of Algorithm 1 with proposal r, kResParts fp64
 // partial sums of max(0, p - r) per kResSub-token sub-tile, [B][ceil(V / kResSub)][kResParts]
-// (the layout launch_select_accept_sums reads).
+// (the layout launch_select_accept_sums reads).  With rsum, row_status (nullable) is set
+// to the call's flags rather than OR-ed into.
 constexpr int kResSub = 1024;
 constexpr int kResParts = 4;
 hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q2, int64_t B, int64_t V, int K,

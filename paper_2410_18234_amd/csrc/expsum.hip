@@ -794,11 +794,13 @@ __device__ __forceinline__ void es_load_tile(const float* __restrict__ p, const 
 }
 
 // G = B * T1 * L records, record g = (b * T1 + t) * L + l; workgroup w takes the
-// records [w per, (w + 1) per).
+// records [w per, (w + 1) per).  status_set (nullable): row b's status word is set
+// to 0 with its first record (the kernels after this one OR the row's flags into it).
 __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* __restrict__ p,
                                                                  const float* __restrict__ q1,
                                                                  const float* __restrict__ q2, int64_t V, int L,
-                                                                 int64_t G, int per, EsWork es) {
+                                                                 int64_t G, int per, EsWork es,
+                                                                 int32_t* __restrict__ status_set) {
   __shared__ float s_w[kEsMomTile];
   __shared__ float s_q[kEsMomTile];
   __shared__ float s_red[kEsWaves][kEsWin32];
@@ -818,6 +820,7 @@ __global__ __launch_bounds__(kEsThreads, 4) void es_moments_kernel(const float* 
   for (int64_t g = g0, par = 0; g < g1; ++g, par ^= 1) {
     const bool more = g + 1 < g1;
     const bool whole = (int64_t)t * kEsMomTile + kEsMomTile <= V;
+    if (status_set && t == 0 && l == 0 && tid == 0) status_set[b] = 0;
     if (++l == L) {  // (b, t, l) of the next record
       l = 0;
       if (++t == es.T1) {
@@ -1850,8 +1853,10 @@ hipError_t launch_induced_expsum(const float* p, const float* q1, const float* q
   carve_es(workspace, B, V, L, &es);
   const int64_t G1 = B * es.T1 * L, G2 = B * es.T3;
   const unsigned n1 = es_grid(es_moments_kernel, G1, kEsSlotMoments);
+  // the summed form (rsum) sets row_status instead of adding to it: cleared here, ahead of the
+  // coefficient kernel's flags
   hipLaunchKernelGGL(es_moments_kernel, dim3(n1), dim3(kEsThreads), 0, st, p, q1, q2, V, L, G1,
-                     (int)((G1 + n1 - 1) / n1), es);
+                     (int)((G1 + n1 - 1) / n1), es, rsum ? row_status : nullptr);
   if (L == 1) {
     hipLaunchKernelGGL((es_coef_kernel<1>), dim3((unsigned)B), dim3(kEsThreads), 0, st, p, q1, q2, V, K, r, es,
                        row_status);

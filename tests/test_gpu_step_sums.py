@@ -30,7 +30,9 @@ def both_forms(p, q, drafts, u):
     K = drafts.shape[1]
     out = {}
     for form in ("sums", "calls"):
-        st = torch.zeros(B, dtype=torch.int32, device=DEV)
+        # the summed r call sets the status words (any prior content is overwritten); the
+        # two-call form ORs into cleared ones
+        st = torch.full((B,), -1 if form == "sums" else 0, dtype=torch.int32, device=DEV)
         if form == "sums":
             acc_ws = torch.empty(mdss.workspace_bytes_accept(B, V), dtype=torch.uint8, device=DEV)
             r = mdss.induced_dist_expsum_sums(p, q, K, acc_ws, row_status=st)
