@@ -1763,10 +1763,14 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
 #pragma unroll
         for (int m = 0; m < kEsTokNodesC; ++m) cm[m] = (i + m < pl.nk) ? s_c[l][min(i + m, kEsMaxWin - 1)] : 0.0;
         const int prow = max(0, min(i - 1, pl.nk - 1));  // B_j(k0 - 1): row i - 1, or the last row decayed
+        const int past = max(0, i - 1 - prow);              // rows past the grid's end: e^(-jh) a node
 #pragma unroll
         for (int j = 0; j < kEsTaylor; ++j) {
           const double v = (i >= 1) ? pt[prow * kEsTaylor + j] : 0.0;
-          pj[j] = (i - 1 > prow) ? v * exp(-(double)((i - 1 - prow) * j) * kEsStep) : v;
+          // e^(-past j h) from the table of e^(-mh) (the same expression as its entries);
+          // past j beyond the table (weights spanning far beyond the grid) takes exp
+          const int m = past * j;
+          pj[j] = (m == 0) ? v : v * ((m < kEsMaxWin) ? s_rho[m] : exp(-(double)m * kEsStep));
         }
         double* at = es.atab + ((b * L + l) * (int64_t)kEsAtabRows + i) * kEsPolyLen;
         double a[kEsPolyLen];  // eleven independent sums, interleaved
