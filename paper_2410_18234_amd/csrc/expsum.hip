@@ -361,6 +361,23 @@ __device__ __forceinline__ float es_wave_ext(float x) {
   r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return es_pick<MAX>(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
+// The same for the bit patterns of non-negative floats (+0 .. +inf order as unsigned
+// integers): no NaN handling around each step, and each step one DPP-fused min / max.
+template <bool MAX>
+__device__ __forceinline__ uint32_t es_pick_u(uint32_t a, uint32_t b) {
+  return MAX ? (a > b ? a : b) : (a < b ? a : b);
+}
+template <bool MAX>
+__device__ __forceinline__ uint32_t es_wave_ext_u(uint32_t x) {
+  x = es_pick_u<MAX>(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
+  x = es_pick_u<MAX>(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
+  x = es_pick_u<MAX>(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x124, 0xF, 0xF, false));  // row_ror:4
+  x = es_pick_u<MAX>(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x128, 0xF, 0xF, false));  // row_ror:8
+  auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = es_pick_u<MAX>(r[0], r[1]);
+  r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return es_pick_u<MAX>(r[0], r[1]);
+}
 // the same, made explicit as a wave-uniform value
 __device__ __forceinline__ float es_uniform_min(float x) {
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(es_wave_ext<false>(x))));
@@ -687,7 +704,9 @@ __device__ void es_moments_run(const float* __restrict__ s_w, const float* __res
   constexpr float kInvFact[kEsTaylor] = {1.0f,        1.0f,         0.5f,          1.0f / 6.0f,
                                          1.0f / 24.0f, 1.0f / 120.0f, 1.0f / 720.0f, 1.0f / 5040.0f};
   float w[kEsRunPer], qq[kEsRunPer];
-  float lo = INFINITY, hi = 0.0f;
+  // the run's weight range on the weights' bit patterns (every w here is +0 or a positive
+  // normal, so unsigned order is float order)
+  uint32_t lo_u = 0x7F800000u, hi_u = 0u;  // +inf, +0
 #pragma unroll
   for (int e = 0; e < kEsRunPer; ++e) {
     const int j = r * kEsRun + e * 64 + lane;
@@ -698,18 +717,18 @@ __device__ void es_moments_run(const float* __restrict__ s_w, const float* __res
     // every entry is a token and each column is sorted: entry e (row 2r) <= entry e + 4 (row 2r + 1)
 #pragma unroll
     for (int e = 0; e < kEsRunPer / 2; ++e) {
-      lo = fminf(lo, w[e]);
-      hi = fmaxf(hi, w[e + kEsRunPer / 2]);
+      lo_u = min(lo_u, __float_as_uint(w[e]));
+      hi_u = max(hi_u, __float_as_uint(w[e + kEsRunPer / 2]));
     }
   } else {
 #pragma unroll
     for (int e = 0; e < kEsRunPer; ++e) {
-      hi = fmaxf(hi, w[e]);                     // entries left out hold w = q = 0
-      lo = (qq[e] > 0.0f) ? fminf(lo, w[e]) : lo;
+      hi_u = max(hi_u, __float_as_uint(w[e]));  // entries left out hold w = q = 0
+      lo_u = (qq[e] > 0.0f) ? min(lo_u, __float_as_uint(w[e])) : lo_u;
     }
   }
-  lo = es_uniform_min(lo);
-  hi = es_uniform_max(hi);
+  const float lo = __uint_as_float(__builtin_amdgcn_readfirstlane(es_wave_ext_u<false>(lo_u)));
+  const float hi = __uint_as_float(__builtin_amdgcn_readfirstlane(es_wave_ext_u<true>(hi_u)));
   if (!(hi > 0.0f)) return;  // uniform: an empty run
   int ktr, nwr;
   es_window_f32(ldexpf(lo, -tau), ldexpf(hi, -tau), ktr, nwr);
