@@ -263,9 +263,9 @@ def main():
     use_es = args.method == "expsum" and not (tlp_s or cfg.alphabet or cfg.diag)
     # K >= 3 i.i.d. drafts from a top-s draft: the quadrature over each row's support
     use_topk = use_es and K >= 3 and bool(s_max) and not (cfg.successive or cfg.pair)
-    # K i.i.d. drafts by the tiled quadrature: r and Algorithm 1's residual sums in one pass, then the
-    # selection and Algorithm 1 from those sums
-    use_sums = use_es and not (use_topk or cfg.successive or cfg.pair)
+    # K i.i.d. drafts by the quadrature (tiled or top-s): r and Algorithm 1's residual sums in one pass,
+    # then the selection and Algorithm 1 from those sums
+    use_sums = use_es and not (cfg.successive or cfg.pair)
     if use_es and (cfg.successive or cfg.pair):
         ws_bytes = mdss.workspace_bytes_pair_expsum(B, V)
         if cfg.successive:
@@ -297,7 +297,7 @@ def main():
             elif cfg.pair:
                 mdss.induced_dist_pair_expsum(p, q, q2, r=r, row_status=status, workspace=ws)
             elif use_topk:
-                mdss.induced_dist_topk_expsum(p, q, K, s_max, r=r, row_status=status)
+                mdss.induced_dist_topk_expsum_sums(p, q, K, s_max, ws_acc, r=r, row_status=status)
             elif use_sums:
                 mdss.induced_dist_expsum_sums(p, q, K, ws_acc, r=r, row_status=status, workspace=ws)
             else:
@@ -484,8 +484,9 @@ def main():
         ntok = expsum_positive_tokens(w["p"], w["q"])
         roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(gbs / HBM_PEAK_GBS, 4),
-                    "traffic": counted_traffic(cfg.name, ["es_topk_kernel"], digest),
-                    "kernel": "mdss_induced_dist_topk_expsum (es_topk_kernel)", "avg_ms": round(r_ms, 4),
+                    "traffic": counted_traffic(cfg.name, ["es_topk_kernel<true>"], digest),
+                    "kernel": "mdss_induced_dist_topk_expsum_sums (es_topk_kernel<true>, with the residual sums "
+                              "of Algorithm 1)", "avg_ms": round(r_ms, 4),
                     "bytes_per_launch": nbytes, "byte_basis": "p and q read once (8 B/token), r written once "
                                                              "(4 B/token), every token of the row",
                     "support_tokens_with_weight": ntok}

@@ -173,7 +173,8 @@ mdss_status mdss_select_accept(const float* p, const float* q, const float* r, c
  * over the rows (the crossing sub-tile's 1024 entries are read again to find
  * the token); residual_mass (nullable) receives Z; there is no residual
  * output.  accept_workspace must hold the sums of the last
- * mdss_induced_dist_expsum_sums call, with p and r unchanged since.  The
+ * mdss_induced_dist_expsum_sums (or mdss_induced_dist_topk_expsum_sums) call,
+ * with p and r unchanged since.  The
  * selection, the accept decision, the flags and Z agree with
  * mdss_select_accept; Z and the running sums are the same fp64 sums taken in
  * another order, so a resampled token can differ only where u_res Z lies
@@ -331,6 +332,19 @@ mdss_status mdss_induced_dist_expsum_noalloc(const float* p, const float* q, int
  *     MDSS_EUNSUPPORTED).  No workspace: the call allocates nothing. */
 mdss_status mdss_induced_dist_topk_expsum(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
                                           int32_t s_max, float* r, int32_t* row_status, void* stream);
+
+/* The summed form of the top-s call (Theorem 1's two steps sharing one pass,
+ * as mdss_induced_dist_expsum_sums): r bit-identical to
+ * mdss_induced_dist_topk_expsum, and, from the same pass over the row, the
+ * residual sums Algorithm 1 with proposal r needs, in the layout
+ * mdss_select_accept_sums reads (four fp64 partial sums of max(0, p - r) per
+ * 1024-token sub-tile, NaN for a flagged row), written into accept_workspace
+ * (at least mdss_workspace_bytes_accept(B, V) bytes).  It SETS row_status[b]
+ * (nullable) to its own flags.
+ * Then call mdss_select_accept_sums with the same p, q, r and workspace. */
+mdss_status mdss_induced_dist_topk_expsum_sums(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
+                                               int32_t s_max, float* r, int32_t* row_status, void* accept_workspace,
+                                               size_t accept_workspace_bytes, void* stream);
 
 /* Bytes of workspace for mdss_induced_dist_pair_expsum and
  * mdss_induced_dist_successive_expsum (0 if the shape is invalid or B = 0). */

@@ -99,10 +99,12 @@ def load_library():
         lib.mdss_induced_dist_successive_expsum.argtypes = [P, P, i64, i64, i32, P, P, P, sz, P]
         lib.mdss_induced_dist_expsum_noalloc.argtypes = [P, P, i64, i64, i32, P, P, P]
         lib.mdss_induced_dist_topk_expsum.argtypes = [P, P, i64, i64, i32, i32, P, P, P]
+        lib.mdss_induced_dist_topk_expsum_sums.argtypes = [P, P, i64, i64, i32, i32, P, P, P, sz, P]
         for f in ("mdss_induced_dist_successive", "mdss_select_successive", "mdss_optimal_acceptance",
                   "mdss_acceptance", "mdss_induced_dist_expsum", "mdss_induced_dist_pair_expsum",
                   "mdss_induced_dist_successive_expsum", "mdss_induced_dist_expsum_noalloc",
-                  "mdss_induced_dist_topk_expsum", "mdss_induced_dist_expsum_sums", "mdss_select_accept_sums"):
+                  "mdss_induced_dist_topk_expsum", "mdss_induced_dist_expsum_sums", "mdss_select_accept_sums",
+                  "mdss_induced_dist_topk_expsum_sums"):
             getattr(lib, f).restype = ctypes.c_int
         for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample", "mdss_select_accept",
                   "mdss_select_accept_pair",
@@ -408,10 +410,19 @@ def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[tor
     each row's support, rows with more than s_max tokens of q > 0 flagged as in "exact")."""
     B = p.shape[0]
     K = drafts.shape[1]
-    summed = method == "expsum" and not (K >= 3 and s_max > 0) and not want_residual
-    # the summed form's r call sets the status words itself; every other call ORs into them
+    topk = method == "expsum" and K >= 3 and s_max > 0
+    summed = method == "expsum" and not want_residual
+    # the summed forms' r calls set the status words themselves; every other call ORs into them
     status = (torch.empty if summed else torch.zeros)(B, dtype=torch.int32, device=p.device)
-    if method == "expsum" and K >= 3 and s_max > 0:
+    if topk and summed:
+        # Theorem 1's two steps sharing one pass over the rows, on the top-s form
+        acc_ws = torch.empty(workspace_bytes_accept(B, p.shape[1]), dtype=torch.uint8, device=p.device)
+        r = induced_dist_topk_expsum_sums(p, q, K, s_max, acc_ws, row_status=status)
+        sel_index, sel_token, out, acc, _ = select_accept_sums(p, q, r, drafts, acc_ws, u, seed, offset,
+                                                               row_status=status)
+        return {"r": r, "sel_index": sel_index, "sel_token": sel_token, "out_token": out, "accepted": acc,
+                "residual": None, "mass": None, "status": status}
+    if topk:
         r = induced_dist_topk_expsum(p, q, K, s_max, row_status=status)
     elif summed:
         # Theorem 1's two steps sharing one pass over the rows: r and Algorithm 1's residual sums together
@@ -724,6 +735,26 @@ def induced_dist_topk_expsum(p: torch.Tensor, q: torch.Tensor, K: int, s_max: in
     _check("mdss_induced_dist_topk_expsum",
            lib.mdss_induced_dist_topk_expsum(_ptr(p), _ptr(q), B, V, K, s_max, _ptr(r), _ptr(row_status),
                                              _stream(dev)))
+    return r
+
+
+def induced_dist_topk_expsum_sums(p: torch.Tensor, q: torch.Tensor, K: int, s_max: int, accept_workspace: torch.Tensor,
+                                  r: Optional[torch.Tensor] = None,
+                                  row_status: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """induced_dist_topk_expsum, writing also the residual sums of Algorithm 1 into
+    accept_workspace (a uint8 tensor of at least workspace_bytes_accept(B, V) bytes, kept for
+    select_accept_sums).  row_status is set to this call's flags (not OR-ed into)."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    accept_workspace = _ws_arg(dev, int(lib.mdss_workspace_bytes_accept(B, V)), accept_workspace)
+    _check("mdss_induced_dist_topk_expsum_sums",
+           lib.mdss_induced_dist_topk_expsum_sums(_ptr(p), _ptr(q), B, V, K, s_max, _ptr(r), _ptr(row_status),
+                                                  _ptr(accept_workspace), accept_workspace.numel(), _stream(dev)))
     return r
 
 

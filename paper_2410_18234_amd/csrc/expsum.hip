@@ -1940,6 +1940,7 @@ constexpr int kTkCap = MDSS_K3_MAX_SUPPORT;   // support entries held in LDS
 constexpr int kTkPer = 4;                     // tokens per thread per streaming step
 constexpr int kTkStep = kTkThreads * kTkPer;  // 4096 tokens per step
 constexpr int kTkSeg = kTkCap / kTkWaves;     // support tokens of one wave's stream segment
+constexpr int kTkLdsParts = 1024;             // residual parts kept in LDS: rows of up to 262144 tokens
 constexpr int kTkAhead = 2;                   // streaming steps in flight (64 KB of p and q per workgroup)
 constexpr int kTkE = 4;                       // support entries per lane in the node sums
 constexpr int kTkGroup = 64 * kTkE;           // entries of one wave group
@@ -1960,7 +1961,27 @@ __device__ __forceinline__ int tk_scan_int(int v, int lane) {
   return v + (row == 0 ? 0 : (row == 1 ? t0 : (row == 2 ? t0 + t1 : t0 + t1 + t2)));
 }
 
-// A streaming step's p and q (0 past the row's end); a whole step without bounds checks.
+// A streaming step's p and q, thread t holding the four consecutive tokens x0 + 4t ..
+// x0 + 4t + 3 (one 16-byte load each when the rows are 16-byte aligned); 0 past the row.
+__device__ __forceinline__ void tk_load4(const float* __restrict__ pb, const float* __restrict__ qb, int64_t V,
+                                         int64_t x0, int tid, bool vec, float (&pv)[kTkPer], float (&qv)[kTkPer]) {
+  static_assert(kTkPer == 4, "one float4 a thread and step");
+  const int64_t x = x0 + 4 * tid;
+  if (vec && x + 3 < V) {
+    const float4 a = *reinterpret_cast<const float4*>(pb + x), c = *reinterpret_cast<const float4*>(qb + x);
+    pv[0] = a.x; pv[1] = a.y; pv[2] = a.z; pv[3] = a.w;
+    qv[0] = c.x; qv[1] = c.y; qv[2] = c.z; qv[3] = c.w;
+  } else {
+#pragma unroll
+    for (int i = 0; i < kTkPer; ++i) {
+      pv[i] = (x + i < V) ? pb[x + i] : 0.0f;
+      qv[i] = (x + i < V) ? qb[x + i] : 0.0f;
+    }
+  }
+}
+
+// The token-order pass's step: thread t holding tokens x0 + 1024 i + t (0 past the row's
+// end); a whole step without bounds checks.
 __device__ __forceinline__ void tk_load(const float* __restrict__ pb, const float* __restrict__ qb, int64_t V,
                                         int64_t x0, int tid, float (&pv)[kTkPer], float (&qv)[kTkPer]) {
   const float* ps = pb + x0 + tid;
@@ -1981,9 +2002,18 @@ __device__ __forceinline__ void tk_load(const float* __restrict__ pb, const floa
   }
 }
 
+// kRes: also the residual sums of Algorithm 1 with proposal r (the summed form), one fp64
+// sum per 256-token part (rsum[b][part], four parts per 1024-token sub-tile): while the
+// row streams, each wave writes the sum of p over its part; once r is written, each
+// support token's correction max(0, p - r) - p is added to its part's sum.  row_status is
+// set, not OR-ed into.
+template <bool kRes>
 __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __restrict__ p, const float* __restrict__ q,
                                                              int64_t V, int K, int s_max, float* __restrict__ r,
-                                                             int32_t* __restrict__ row_status) {
+                                                             int32_t* __restrict__ row_status,
+                                                             double* __restrict__ rsum, int64_t nsub) {
+  static_assert(kTkStep == 4 * kResSub && kResSub / kResParts == 256 && kTkThreads / 4 == 256,
+                "a wave's 256 tokens of a step are one part of the residual sums");
   __shared__ int s_idx[kTkCap];
   __shared__ float s_p[kTkCap];
   __shared__ float s_q[kTkCap];
@@ -1999,21 +2029,37 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
   __shared__ double s_e[kTkWaves][2];
   __shared__ int s_n[kTkWaves];
   __shared__ EsPlan s_plan;
-  __shared__ int s_sidx[kTkCap];  // while streaming: wave w's support tokens at [w kTkSeg, (w + 1) kTkSeg)
-  __shared__ float s_sp[kTkCap];
-  __shared__ float s_sq[kTkCap];
+  // while streaming: wave w's support tokens (index, p, q) at [w kTkSeg, (w + 1) kTkSeg);
+  // once the list is joined, kRes keeps each entry's residual correction here (fp64)
+  __shared__ __align__(16) uint32_t s_seg[3 * kTkCap];
+  int* const s_sidx = reinterpret_cast<int*>(s_seg);
+  float* const s_sp = reinterpret_cast<float*>(s_seg + kTkCap);
+  float* const s_sq = reinterpret_cast<float*>(s_seg + 2 * kTkCap);
+  double* const s_dres = reinterpret_cast<double*>(s_seg);
   __shared__ int s_wn[kTkWaves];
+  // kRes: the parts' sums of a row of up to kTkLdsParts parts are kept here and written
+  // out once at the end; longer rows keep them in rsum itself
+  __shared__ double s_parts[kRes ? kTkLdsParts : 1];
   const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t b = blockIdx.x;
   const float* pb = p + b * V;
   const float* qb = q + b * V;
   float* rb = r + b * V;
+  if (kRes && tid == 0 && row_status) row_status[b] = 0;  // thread 0 adds the flags below
+  const int64_t nparts = nsub * kResParts;
+  const bool lds_parts = kRes && nparts <= kTkLdsParts;  // uniform
+  double* const parts = lds_parts ? s_parts : rsum + b * nparts;
 
-  // (1) stream the row, kTkAhead steps in flight: r = 0, the probability checks, and each
-  //     wave's support tokens appended to its own LDS segment (no barrier a step)
+  // (1) stream the row, kTkAhead steps in flight, thread t on the four consecutive tokens
+  //     x0 + 4t .. x0 + 4t + 3 of each step (wave w on the 256 tokens x0 + 256w ..): r = 0,
+  //     the probability checks, each wave's support tokens appended to its own LDS segment
+  //     (no barrier a step), and for kRes each wave's fp64 sum of p over its 256 tokens:
+  //     part (x0 >> 8) + w of the residual sums' layout
+  const bool vec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(q) |
+                                     reinterpret_cast<uintptr_t>(r)) % 16 == 0);
   float pf[kTkAhead][kTkPer], qf[kTkAhead][kTkPer];  // the next kTkAhead steps, in flight
 #pragma unroll
-  for (int j = 0; j < kTkAhead; ++j) tk_load(pb, qb, V, (int64_t)j * kTkStep, tid, pf[j], qf[j]);
+  for (int j = 0; j < kTkAhead; ++j) tk_load4(pb, qb, V, (int64_t)j * kTkStep, tid, vec, pf[j], qf[j]);
   int bad = 0, wn = 0;  // wn: this wave's support tokens so far (uniform)
   const int64_t nstep = (V + kTkStep - 1) / kTkStep;
   for (int64_t st = 0; st < nstep; ++st) {
@@ -2029,20 +2075,26 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
         qf[j][i] = qf[j + 1][i];
       }
     }
-    if (st + kTkAhead < nstep) tk_load(pb, qb, V, x0 + kTkAhead * kTkStep, tid, pf[kTkAhead - 1], qf[kTkAhead - 1]);
-    float* rs = rb + x0 + tid;
-    const int rest = (x0 + kTkStep <= V) ? kTkStep : (int)(V - x0) - tid;  // a whole step: every token
+    if (st + kTkAhead < nstep)
+      tk_load4(pb, qb, V, x0 + kTkAhead * kTkStep, tid, vec, pf[kTkAhead - 1], qf[kTkAhead - 1]);
+    const int64_t x = x0 + 4 * tid;
     // r = 0 over the whole step in full lines (a masked store would leave partial lines);
     // the support's values overwrite these after the sums, past workgroup barriers
-    if (rest >= kTkStep) {  // uniform
-#pragma unroll
-      for (int i = 0; i < kTkPer; ++i) rs[i * kTkThreads] = 0.0f;
+    if (vec && x + 3 < V) {
+      *reinterpret_cast<float4*>(rb + x) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     } else {
 #pragma unroll
       for (int i = 0; i < kTkPer; ++i)
-        if (i * kTkThreads < rest) rs[i * kTkThreads] = 0.0f;
+        if (x + i < V) rb[x + i] = 0.0f;
     }
-    const int xs = (int)x0 + tid;  // rows < 2^31 tokens
+    if (kRes) {
+      double loc = 0.0;
+#pragma unroll
+      for (int i = 0; i < kTkPer; ++i) loc += (double)pc[i];  // p = 0 past the row's end
+      const double tot = wave_sum_dpp(loc);
+      const int64_t part = (x0 >> 8) + wid;
+      if (lane == 0 && part < nparts) parts[part] = tot;
+    }
 #pragma unroll
     for (int i = 0; i < kTkPer; ++i) {
       // NaN, -inf, a negative normal or denormal, +inf (-0 is a zero probability)
@@ -2053,7 +2105,7 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
                                                           __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
       if (sup && pos < kTkSeg) {
         const int at = wid * kTkSeg + pos;
-        s_sidx[at] = xs + i * kTkThreads;
+        s_sidx[at] = (int)x + i;  // rows < 2^31 tokens
         s_sp[at] = pc[i];
         s_sq[at] = qc[i];
       }
@@ -2223,6 +2275,8 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
   if (flags) {  // NaN over the whole row
     if (tid == 0 && row_status) row_status[b] |= flags;
     for (int64_t x = tid; x < V; x += kTkThreads) rb[x] = NAN;
+    if (kRes)
+      for (int64_t t = tid; t < nparts; t += kTkThreads) rsum[b * nparts + t] = NAN;
     return;
   }
   const int k_lo = pl.k_lo, nk = pl.nk;
@@ -2290,6 +2344,7 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
         v = (double)qq1 * zw;
       }
       rb[s_idx[e]] = (float)v;
+      if (kRes) s_dres[e] = residual_of(pp, (float)v) - (double)pp;
     }
   } else if (nk > 0) {
     // (3') fp64: S_k per node (wave w takes the nodes congruent to w), lanes over the entries
@@ -2322,18 +2377,47 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
         v = (double)qq1 * zw;
       }
       rb[s_idx[e]] = (float)v;
+      if (kRes) s_dres[e] = residual_of(pp, (float)v) - (double)pp;
     }
   } else {
     // no positive weight: zero-weight tokens only
-    for (int e = tid; e < nl; e += kTkThreads) rb[s_idx[e]] = (float)((double)s_q[e] * zw);
+    for (int e = tid; e < nl; e += kTkThreads) {
+      const float v = (float)((double)s_q[e] * zw);
+      rb[s_idx[e]] = v;
+      if (kRes) s_dres[e] = residual_of(s_p[e], v) - (double)s_p[e];
+    }
+  }
+  if (kRes) {
+    // (6) the residual sums: the support entries of one 256-token part are consecutive in
+    //     the list (a wave's segment holds its parts in stream order; the token-order list
+    //     is sorted); the first entry of each run adds the run's corrections, in list order,
+    //     to its part's sum of p
+    __syncthreads();  // every correction is in LDS, every part's sum of p written
+    for (int e = tid; e < nl; e += kTkThreads) {
+      const int key = s_idx[e] >> 8;
+      if (e > 0 && (s_idx[e - 1] >> 8) == key) continue;  // not the first entry of its run
+      double corr = 0.0;
+      for (int f = e; f < nl && (s_idx[f] >> 8) == key; ++f) corr += s_dres[f];
+      parts[key] += corr;
+    }
+    if (lds_parts) {
+      __syncthreads();
+      for (int64_t t = tid; t < nparts; t += kTkThreads) rsum[b * nparts + t] = s_parts[t];
+    }
   }
 }
 
 }  // namespace
 
 hipError_t launch_induced_topk_expsum(const float* p, const float* q, int64_t B, int64_t V, int K, int s_max,
-                                      float* r, int32_t* row_status, hipStream_t st) {
-  hipLaunchKernelGGL(es_topk_kernel, dim3((unsigned)B), dim3(kTkThreads), 0, st, p, q, V, K, s_max, r, row_status);
+                                      float* r, int32_t* row_status, hipStream_t st, double* rsum) {
+  const int64_t nsub = (V + kResSub - 1) / kResSub;
+  if (rsum)
+    hipLaunchKernelGGL(es_topk_kernel<true>, dim3((unsigned)B), dim3(kTkThreads), 0, st, p, q, V, K, s_max, r,
+                       row_status, rsum, nsub);
+  else
+    hipLaunchKernelGGL(es_topk_kernel<false>, dim3((unsigned)B), dim3(kTkThreads), 0, st, p, q, V, K, s_max, r,
+                       row_status, nullptr, nsub);
   return hipGetLastError();
 }
 

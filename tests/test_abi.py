@@ -294,3 +294,21 @@ def test_summed_form_argument_errors(lib):
     assert g(*args(ws=None)) == 5
     assert g(*args(wsb=acc - 1)) == 5
     assert g(*args(B=0, p=None)) == 0
+
+
+def test_topk_summed_form_argument_errors(lib):
+    f = lib.mdss_induced_dist_topk_expsum_sums
+    f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    acc = lib.mdss_workspace_bytes_accept(4, 16)
+    assert f(None, FAKE, 4, 16, 3, 8, FAKE, None, FAKE, acc, None) == 1
+    assert f(FAKE, FAKE, 4, 16, 3, 8, None, None, FAKE, acc, None) == 1
+    assert f(FAKE, FAKE, 4, 1, 3, 8, FAKE, None, FAKE, acc, None) == 2
+    assert f(FAKE, FAKE, 4, 16, 9, 8, FAKE, None, FAKE, acc, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 3, 0, FAKE, None, FAKE, acc, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 3, 4097, FAKE, None, FAKE, acc, None) == 3
+    assert f(FAKE, FAKE, 4, 16, 3, 8, FAKE, None, None, acc, None) == 5
+    assert f(FAKE, FAKE, 4, 16, 3, 8, FAKE, None, FAKE, acc - 1, None) == 5
+    assert f(None, None, 0, 16, 3, 8, None, None, None, 0, None) == 0
+    # the accept workspace holds the summed forms' four sums per 1024 tokens
+    assert acc >= 8 * 4 * 4

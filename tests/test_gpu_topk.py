@@ -137,13 +137,12 @@ def test_support_of_the_whole_cap():
 
 def test_wave_segments_and_the_token_order_pass():
     # while a row streams, each of the 16 waves keeps up to 256 support tokens of its own
-    # (wave w reads tokens 4096 s + 1024 i + 64 w + lane); a row in which one wave meets
-    # more is streamed again and compacted in token order.  Rows: wave 0 at exactly 256
-    # support tokens, wave 0 at 257, 1024 tokens spread over every wave
+    # (wave w reads the tokens 4096 s + 256 w .. 4096 s + 256 w + 255 of step s); a row in
+    # which one wave meets more is streamed again and compacted in token order.  Rows:
+    # wave 0 at exactly 256 support tokens, wave 0 at 257, 1024 tokens spread over every wave
     rng = np.random.default_rng(47)
     V, B = 8192, 3
-    lanes = np.arange(64)
-    wave0 = lambda s: np.concatenate([s * 4096 + i * 1024 + lanes for i in range(4)])
+    wave0 = lambda s: s * 4096 + np.arange(256)
     P = rng.dirichlet(np.full(V, 0.4), size=B)
     Q = np.zeros((B, V))
     sup = [wave0(0), np.concatenate([wave0(0), wave0(1)[:1]]), rng.choice(V, 1024, replace=False)]
@@ -298,3 +297,111 @@ def test_step_uses_the_top_s_form():
     assert np.all(out["status"].cpu().numpy() == 0)
     si, stok, st = oracle.select(P, Q, drafts3, w["u"])
     assert np.array_equal(out["sel_index"].cpu().numpy(), si)
+
+
+# ---- the summed form (mdss_induced_dist_topk_expsum_sums + mdss_select_accept_sums) ----
+
+def both_forms_tk(P, Q, drafts, u, K, s_max):
+    """(summed form, two-call form) outputs as numpy arrays; the summed form's status words
+    start as all ones (the r call sets them), the two-call form's cleared."""
+    p, q, d = dev(P), dev(Q), dev(drafts)
+    uu = dev(u) if u is not None else None
+    B, V = P.shape
+    out = {}
+    for form in ("sums", "calls"):
+        st = torch.full((B,), -1 if form == "sums" else 0, dtype=torch.int32, device=DEV)
+        if form == "sums":
+            acc_ws = torch.empty(mdss.workspace_bytes_accept(B, V), dtype=torch.uint8, device=DEV)
+            r = mdss.induced_dist_topk_expsum_sums(p, q, K, s_max, acc_ws, row_status=st)
+            si, stok, tok, acc, mass = mdss.select_accept_sums(p, q, r, d, acc_ws, uu, seed=13, offset=2,
+                                                                want_mass=True, row_status=st)
+        else:
+            r = mdss.induced_dist_topk_expsum(p, q, K, s_max, row_status=st)
+            si, stok, tok, acc, _, mass = mdss.select_accept(p, q, r, d, uu, seed=13, offset=2, want_mass=True,
+                                                             row_status=st)
+        torch.cuda.synchronize()
+        out[form] = {k: v.cpu().numpy() for k, v in dict(r=r, sel_index=si, sel_token=stok, out=tok, acc=acc,
+                                                        mass=mass, status=st).items()}
+    return out["sums"], out["calls"]
+
+
+def _drafts_from(Q, K, seed):
+    rng = np.random.default_rng(seed)
+    d = np.zeros((Q.shape[0], K), np.int32)
+    for b in range(Q.shape[0]):
+        sup = np.flatnonzero(Q[b] > 0)
+        if len(sup):
+            d[b] = rng.choice(sup, K)
+    return d
+
+
+def test_summed_form_k3top1024():
+    from test_gpu_step_sums import check_forms
+    w = generate("k3top1024")
+    a, b = both_forms_tk(w["p"], w["q"], w["drafts"], w["u"], 3, 1024)
+    assert np.all(a["status"] == 0)
+    n = check_forms(w["p"], a, b, w["u"][:, 2])
+    rej = int((a["acc"] == 0).sum())
+    print(f"\nk3top1024: {rej} rejected rows, {n} draws differing at an edge")
+    assert rej > 0
+
+
+@pytest.mark.parametrize("K", [2, 3, 5])
+def test_summed_form_edge_rows(K):
+    # empty support, zero weights only, one token of support, a two-token vocabulary,
+    # ragged steps, a row above s_max (flagged), a NaN probability (flagged), weights in
+    # the fp64 form, and rows whose support overflows a wave's stream segment (the row
+    # streamed again in token order)
+    from test_gpu_step_sums import check_forms
+    rng = np.random.default_rng(60 + K)
+    rows = []
+    for V in (2, 7, 4097, 5000):
+        P = rng.dirichlet(np.ones(V), size=4)
+        Q = rng.dirichlet(np.ones(V), size=4)
+        Q[0] = 0.0
+        P[1] = 0.0
+        P[1, 0] = 1.0
+        Q[1, 0] = 0.0
+        Q[1] = top_s(Q[1:2], min(V, 1000))[0]
+        Q[2] = 0.0
+        Q[2, V - 1] = 1.0
+        Q[3] = top_s(Q[3:4], min(V, 1000))[0]
+        rows.append((P.astype(np.float32), Q.astype(np.float32), min(V, 1000)))
+    V = 8192
+    wave0 = lambda s: s * 4096 + np.arange(256)  # wave 0's tokens of step s
+    P = rng.dirichlet(np.full(V, 0.4), size=5)
+    Q = np.zeros((5, V))
+    sup = [wave0(0), np.concatenate([wave0(0), wave0(1)[:1]]), rng.choice(V, 1024, replace=False),
+           rng.choice(V, 1025, replace=False), rng.choice(V, 700, replace=False)]
+    for b in range(5):
+        Q[b, sup[b]] = rng.gamma(0.5, size=len(sup[b])) + 1e-6
+    Q /= Q.sum(1, keepdims=True)
+    P[4, sup[4][3]] = np.nan  # a bad probability: the row is flagged
+    rows.append((P.astype(np.float32), Q.astype(np.float32), 1024))
+    Ps, Qs = _span_rows(67 + K, 3000, [110, 150])  # the fp64 form
+    rows.append((Ps, Qs, 3000))
+    flagged = 0
+    for P, Q, s_max in rows:
+        drafts = _drafts_from(Q, K, P.shape[1] + K)
+        u = rng.integers(0, 1 << 24, size=(P.shape[0], 3)).astype(np.float32) / np.float32(1 << 24)
+        u[:, 1] = 0.999  # mostly rejections: the draw from the sums is exercised
+        a, b = both_forms_tk(P, Q, drafts, u, K, s_max)
+        check_forms(np.nan_to_num(P), a, b, u[:, 2])
+        flagged += int(np.count_nonzero(a["status"] & 1)) + int(np.count_nonzero(a["status"] & 4))
+        bad = (a["status"] & 1) != 0
+        assert np.all(a["out"][bad] == -1) and np.all(np.isnan(a["mass"][bad]))
+    assert flagged >= 2  # the row above s_max and the NaN row
+
+
+def test_step_uses_the_top_s_summed_form():
+    # the whole path with method "expsum", K = 3 and s_max (no residual asked for) runs the
+    # summed top-s form; asked for the residual it runs the two calls: the same tokens
+    w = generate("k3top1024", rows=list(range(64)))
+    args = (dev(w["p"]), dev(w["q"]), dev(w["drafts"]), dev(w["u"]))
+    s1 = mdss.step(*args, method="expsum", s_max=1024)
+    s2 = mdss.step(*args, method="expsum", s_max=1024, want_residual=True)
+    torch.cuda.synchronize()
+    assert s1["residual"] is None and s2["residual"] is not None
+    for k in ("r", "sel_index", "sel_token", "accepted", "status"):
+        assert torch.equal(s1[k], s2[k]), k
+    assert torch.equal(s1["out_token"], s2["out_token"])
