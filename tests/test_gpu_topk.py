@@ -405,3 +405,22 @@ def test_step_uses_the_top_s_summed_form():
     for k in ("r", "sel_index", "sel_token", "accepted", "status"):
         assert torch.equal(s1[k], s2[k]), k
     assert torch.equal(s1["out_token"], s2["out_token"])
+
+
+def test_summed_form_long_rows():
+    # rows of 128256 tokens (parts' sums in LDS) and of 300000 tokens (past 262144 tokens:
+    # the parts' sums kept in the workspace itself), top 1024, K = 3
+    from test_gpu_step_sums import check_forms
+    w = generate("zipf128k", rows=[0, 1, 2, 3])
+    rng = np.random.default_rng(71)
+    V2 = 300000
+    P2 = rng.dirichlet(np.full(V2, 0.2), size=3).astype(np.float32)
+    Q2 = top_s(rng.dirichlet(np.full(V2, 0.2), size=3), 1024)
+    for P, Q in ((w["p"], top_s(w["q"], 1024)), (P2, Q2)):
+        drafts = _drafts_from(Q, 3, P.shape[1])
+        u = rng.integers(0, 1 << 24, size=(P.shape[0], 3)).astype(np.float32) / np.float32(1 << 24)
+        u[:, 1] = 0.999
+        a, b = both_forms_tk(P, Q, drafts, u, 3, 1024)
+        assert np.all(a["status"] == 0)
+        check_forms(P, a, b, u[:, 2])
+        assert np.any(a["acc"] == 0)  # draws from the sums (a row with p(Y) >= r(Y) accepts at any u)
