@@ -215,6 +215,9 @@ def main():
     ap.add_argument("--config", default="llm32k")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline leg")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of graph replays")
+    ap.add_argument("--graph-steps", type=int, default=10,
+                    help="steps captured back to back in each HIP graph (each graph launch leaves the GPU idle "
+                         "for ~8 us; a serving loop captures the sampler inside its decode graph)")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample size (0: one per core, 2 rounds)")
     ap.add_argument("--resample-reps", type=int, default=20)
     ap.add_argument("--tlp-tail", choices=["sorted", "half"], default=None,
@@ -388,11 +391,12 @@ def main():
     r_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
     r_eager_ms = None
     ms_per_step = wall * 1e3 / args.steps
+    ms_one_per_graph = None
     timing = "eager launches, HIP events around r in every step"
     if not args.no_graph:
-        # the whole step: one HIP graph of its kernels (status clear, r, selection,
-        # accept/resample), replayed K times; no host launch work or timing markers
-        # between the kernels.  Every replay is checked against the eager step first.
+        # the whole step (status clear, r, selection, accept/resample) in HIP graphs: no host
+        # launch work or timing markers between the kernels.  Every graph is checked against
+        # the eager step first.
         ref_out, ref_acc = out.clone(), acc.clone()
         ref_r = (r_stages if cfg.successive else r).clone()
         side = torch.cuda.Stream()
@@ -401,27 +405,53 @@ def main():
             one_step()
         torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            g_out, g_acc = one_step()
-        for rep in range(3):
-            graph.replay()
+        # graphs of n whole steps each, back to back on the same inputs (every step recomputes r, the
+        # selection and Algorithm 1 from p, q, the drafts and u; the last step's outputs are kept)
+        def capture(n):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for _ in range(n):
+                    o = one_step()
+            return g, o
+
+        def check(g, o, what):
+            for rep in range(3):
+                g.replay()
+                torch.cuda.synchronize()
+                same = (torch.equal(o[0], ref_out) and torch.equal(o[1], ref_acc) and
+                        torch.equal(r_stages if cfg.successive else r, ref_r) and int(status.abs().sum()) == 0)
+                assert same, f"{what}: replay {rep} differs from the eager step"
+                one_step()  # eager work between the replays
+                torch.cuda.synchronize()
+
+        def timed(graphs):
             torch.cuda.synchronize()
-            same = (torch.equal(g_out, ref_out) and torch.equal(g_acc, ref_acc) and
-                    torch.equal(r_stages if cfg.successive else r, ref_r) and int(status.abs().sum()) == 0)
-            assert same, f"graph replay {rep} differs from the eager step"
-            one_step()  # eager work between the replays
+            t0 = time.perf_counter()
+            for g in graphs:
+                g.replay()
             torch.cuda.synchronize()
+            return (time.perf_counter() - t0) * 1e3 / args.steps
+
+        # one step per graph: each replay pays the graph launch
+        graph1, o1 = capture(1)
+        check(graph1, o1, "one-step graph")
         for _ in range(args.warmup):
+            graph1.replay()
+        ms_one_per_graph = timed([graph1] * args.steps)
+        # the timed form: K steps as replays of graphs of --graph-steps steps (a shorter graph for the rest)
+        gs = max(1, min(args.graph_steps, args.steps))
+        graph, g_o = capture(gs)
+        check(graph, g_o, f"{gs}-step graph")
+        plan = [graph] * (args.steps // gs)
+        if args.steps % gs:
+            tail, t_o = capture(args.steps % gs)
+            check(tail, t_o, f"{args.steps % gs}-step graph")
+            plan.append(tail)
+        for _ in range(max(1, args.warmup // gs)):
             graph.replay()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            graph.replay()
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        ms_per_step = wall * 1e3 / args.steps
-        out, acc = g_out, g_acc
+        ms_per_step = timed(plan)
+        out, acc = g_o
+        del graph1
     if not args.no_graph and not (cfg.alphabet or cfg.diag):
         # r alone without host launch gaps: a graph of R_REPS back-to-back r calls, HIP events around replays
         # (the alphabet and optimum workloads time their own segments of the eager step instead)
@@ -439,10 +469,12 @@ def main():
         torch.cuda.synchronize()
         r_eager_ms = r_ms
         r_ms = e0.elapsed_time(e1) / (args.steps * R_REPS)
-        timing = ("one HIP graph per step (replays checked against the eager step); r by HIP events around "
-                  f"replays of a graph of {R_REPS} back-to-back r calls")
+        timing = (f"K steps as replays of HIP graphs of {min(args.graph_steps, args.steps)} whole steps each "
+                  "(replays checked against the eager step); r by HIP events around replays of a graph of "
+                  f"{R_REPS} back-to-back r calls")
     elif not args.no_graph:
-        timing = "one HIP graph per step (replays checked against the eager step); r by HIP events on eager steps"
+        timing = (f"K steps as replays of HIP graphs of {min(args.graph_steps, args.steps)} whole steps each "
+                  "(replays checked against the eager step); r by HIP events on eager steps")
     assert int(status.abs().sum()) == 0, "rows flagged during the bench"
     if cfg.diag:
         pstar_t, achieved_t = out, acc
@@ -652,6 +684,7 @@ def main():
         "roofline_resample": roofline_resample,
         "method": "exponential-sum quadrature" if use_es else "exact pairwise sums",
         "timing": timing,
+        "ms_per_step_one_graph_each": None if ms_one_per_graph is None else round(ms_one_per_graph, 4),
         "r_eager_ms": None if r_eager_ms is None else round(r_eager_ms, 4),
         "exact_pairwise": exact_pairwise,
         "cpu_baseline": None,
