@@ -346,6 +346,22 @@ mdss_status mdss_induced_dist_topk_expsum_sums(const float* p, const float* q, i
                                                int32_t s_max, float* r, int32_t* row_status, void* accept_workspace,
                                                size_t accept_workspace_bytes, void* stream);
 
+/* The whole step of the top-s call in one launch (Theorem 1's selection, then
+ * Algorithm 1 with proposal r): mdss_induced_dist_topk_expsum_sums followed by
+ * mdss_select_accept_sums with the same arguments, with the same outputs value
+ * for value (the draw is the same code, run by the row's workgroup once r and the
+ * sums are written).  r, the residual sums in accept_workspace, sel_index and
+ * sel_token (nullable), out_token, accepted, residual_mass (nullable) and
+ * row_status (nullable; SET to the row's flags) as those two calls; u: [B][3] or
+ * NULL for Philox(seed, offset + b).  Errors: as the two calls (EUNSUPPORTED for K
+ * or s_max out of range, EINVAL for a NULL p, q, r, drafts, out_token or accepted,
+ * EWORKSPACE for a workspace under mdss_workspace_bytes_accept(B, V)). */
+mdss_status mdss_step_topk_expsum(const float* p, const float* q, const int32_t* drafts, const float* u,
+                                  uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K, int32_t s_max,
+                                  float* r, int32_t* sel_index, int32_t* sel_token, int32_t* out_token,
+                                  uint8_t* accepted, double* residual_mass, int32_t* row_status,
+                                  void* accept_workspace, size_t accept_workspace_bytes, void* stream);
+
 /* Bytes of workspace for mdss_induced_dist_pair_expsum and
  * mdss_induced_dist_successive_expsum (0 if the shape is invalid or B = 0). */
 size_t mdss_workspace_bytes_pair_expsum(int64_t B, int64_t V);

@@ -33,6 +33,7 @@ from .binding import (  # noqa: F401
     induced_dist_expsum_noalloc,
     induced_dist_topk_expsum,
     induced_dist_topk_expsum_sums,
+    step_topk_expsum,
     induced_dist_expsum_sums,
     select_accept_sums,
     induced_dist_pair,

@@ -100,11 +100,13 @@ def load_library():
         lib.mdss_induced_dist_expsum_noalloc.argtypes = [P, P, i64, i64, i32, P, P, P]
         lib.mdss_induced_dist_topk_expsum.argtypes = [P, P, i64, i64, i32, i32, P, P, P]
         lib.mdss_induced_dist_topk_expsum_sums.argtypes = [P, P, i64, i64, i32, i32, P, P, P, sz, P]
+        lib.mdss_step_topk_expsum.argtypes = [P, P, P, P, u64, u64, i64, i64, i32, i32, P, P, P, P, P, P, P, P, sz,
+                                              P]
         for f in ("mdss_induced_dist_successive", "mdss_select_successive", "mdss_optimal_acceptance",
                   "mdss_acceptance", "mdss_induced_dist_expsum", "mdss_induced_dist_pair_expsum",
                   "mdss_induced_dist_successive_expsum", "mdss_induced_dist_expsum_noalloc",
                   "mdss_induced_dist_topk_expsum", "mdss_induced_dist_expsum_sums", "mdss_select_accept_sums",
-                  "mdss_induced_dist_topk_expsum_sums"):
+                  "mdss_induced_dist_topk_expsum_sums", "mdss_step_topk_expsum"):
             getattr(lib, f).restype = ctypes.c_int
         for f in ("mdss_induced_dist", "mdss_select_intermediate", "mdss_accept_or_resample", "mdss_select_accept",
                   "mdss_select_accept_pair",
@@ -415,11 +417,10 @@ def step(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, u: Optional[tor
     # the summed forms' r calls set the status words themselves; every other call ORs into them
     status = (torch.empty if summed else torch.zeros)(B, dtype=torch.int32, device=p.device)
     if topk and summed:
-        # Theorem 1's two steps sharing one pass over the rows, on the top-s form
+        # Theorem 1's two steps in one launch on the top-s form: r, the residual sums, then the draw
         acc_ws = torch.empty(workspace_bytes_accept(B, p.shape[1]), dtype=torch.uint8, device=p.device)
-        r = induced_dist_topk_expsum_sums(p, q, K, s_max, acc_ws, row_status=status)
-        sel_index, sel_token, out, acc, _ = select_accept_sums(p, q, r, drafts, acc_ws, u, seed, offset,
-                                                               row_status=status)
+        r, sel_index, sel_token, out, acc, _ = step_topk_expsum(p, q, drafts, K, s_max, acc_ws, u, seed, offset,
+                                                                row_status=status)
         return {"r": r, "sel_index": sel_index, "sel_token": sel_token, "out_token": out, "accepted": acc,
                 "residual": None, "mass": None, "status": status}
     if topk:
@@ -756,6 +757,39 @@ def induced_dist_topk_expsum_sums(p: torch.Tensor, q: torch.Tensor, K: int, s_ma
            lib.mdss_induced_dist_topk_expsum_sums(_ptr(p), _ptr(q), B, V, K, s_max, _ptr(r), _ptr(row_status),
                                                   _ptr(accept_workspace), accept_workspace.numel(), _stream(dev)))
     return r
+
+
+def step_topk_expsum(p: torch.Tensor, q: torch.Tensor, drafts: torch.Tensor, K: int, s_max: int,
+                     accept_workspace: torch.Tensor, u: Optional[torch.Tensor] = None, seed: int = 0,
+                     offset: int = 0, want_mass: bool = False, r: Optional[torch.Tensor] = None,
+                     row_status: Optional[torch.Tensor] = None):
+    """(r, sel_index, sel_token, out_token, accepted, residual_mass or None): the top-s summed
+    form and select_accept_sums in one launch (the same outputs as those two calls); K is the
+    law's draft count (drafts has K columns).  row_status is set to the row's flags."""
+    lib = load_library()
+    B, V, dev = _pq(p, q)
+    if drafts.dim() != 2 or drafts.shape[1] != K:
+        raise ValueError("drafts must be [B][K]")
+    _need(drafts, "drafts", torch.int32, (B, K), dev)
+    if r is None:
+        r = torch.empty((B, V), dtype=torch.float32, device=dev)
+    _need(r, "r", torch.float32, (B, V), dev)
+    if u is not None:
+        _need(u, "u", torch.float32, (B, 3), dev)
+    if row_status is not None:
+        _need(row_status, "row_status", torch.int32, (B,), dev)
+    accept_workspace = _ws_arg(dev, int(lib.mdss_workspace_bytes_accept(B, V)), accept_workspace)
+    sel_index = torch.empty(B, dtype=torch.int32, device=dev)
+    sel_token = torch.empty(B, dtype=torch.int32, device=dev)
+    out = torch.empty(B, dtype=torch.int32, device=dev)
+    acc = torch.empty(B, dtype=torch.uint8, device=dev)
+    mass = torch.empty(B, dtype=torch.float64, device=dev) if want_mass else None
+    _check("mdss_step_topk_expsum",
+           lib.mdss_step_topk_expsum(_ptr(p), _ptr(q), _ptr(drafts), _ptr(u), ctypes.c_uint64(seed),
+                                     ctypes.c_uint64(offset), B, V, K, s_max, _ptr(r), _ptr(sel_index),
+                                     _ptr(sel_token), _ptr(out), _ptr(acc), _ptr(mass), _ptr(row_status),
+                                     _ptr(accept_workspace), accept_workspace.numel(), _stream(dev)))
+    return r, sel_index, sel_token, out, acc, mass
 
 
 def induced_dist_expsum_sums(p: torch.Tensor, q: torch.Tensor, K: int, accept_workspace: torch.Tensor,

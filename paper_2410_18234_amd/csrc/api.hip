@@ -256,6 +256,24 @@ mdss_status mdss_induced_dist_topk_expsum_sums(const float* p, const float* q, i
                                                    static_cast<double*>(accept_workspace)));
 }
 
+mdss_status mdss_step_topk_expsum(const float* p, const float* q, const int32_t* drafts, const float* u,
+                                  uint64_t seed, uint64_t offset, int64_t B, int64_t V, int32_t K, int32_t s_max,
+                                  float* r, int32_t* sel_index, int32_t* sel_token, int32_t* out_token,
+                                  uint8_t* accepted, double* residual_mass, int32_t* row_status,
+                                  void* accept_workspace, size_t accept_workspace_bytes, void* stream) {
+  const mdss_status s = check_shape(B, V);
+  if (s != MDSS_OK) return s;
+  if (K < 2 || K > MDSS_MAX_K || s_max < 1 || s_max > MDSS_K3_MAX_SUPPORT) return MDSS_EUNSUPPORTED;
+  if (B == 0) return MDSS_OK;
+  if (!p || !q || !r || !drafts || !out_token || !accepted) return MDSS_EINVAL;
+  if (!workspace_ok(accept_workspace, accept_workspace_bytes, mdss::workspace_bytes_accept(B, V)))
+    return MDSS_EWORKSPACE;
+  return from_hip(mdss::launch_step_topk_expsum(p, q, drafts, u, seed, offset, B, V, K, s_max, r, sel_index,
+                                                sel_token, out_token, accepted, residual_mass, row_status,
+                                                static_cast<double*>(accept_workspace),
+                                                static_cast<hipStream_t>(stream)));
+}
+
 mdss_status mdss_induced_dist_expsum_noalloc(const float* p, const float* q, int64_t B, int64_t V, int32_t K,
                                              float* r, int32_t* row_status, void* stream) {
   const mdss_status s = check_shape(B, V);

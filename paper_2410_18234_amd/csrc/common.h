@@ -89,6 +89,12 @@ hipError_t launch_select_accept_sums(const float* p, const float* q, const float
 // rsum (nullable): the summed form, the residual sums in the layout above; row_status set.
 hipError_t launch_induced_topk_expsum(const float* p, const float* q, int64_t B, int64_t V, int K, int s_max,
                                       float* r, int32_t* row_status, hipStream_t st, double* rsum = nullptr);
+// The top-s summed form and the draw from its sums (selection and Algorithm 1 as
+// launch_select_accept_sums) in one launch.
+hipError_t launch_step_topk_expsum(const float* p, const float* q, const int32_t* drafts, const float* u, uint64_t seed,
+                                   uint64_t offset, int64_t B, int64_t V, int K, int s_max, float* r,
+                                   int32_t* sel_index, int32_t* sel_token, int32_t* out_token, uint8_t* accepted,
+                                   double* residual_mass, int32_t* row_status, double* rsum, hipStream_t st);
 hipError_t launch_alphabet_truncate(const float* p, int64_t B, int64_t V, int m, float* pt, double* mass0,
                                     int32_t* row_status, hipStream_t st);
 hipError_t launch_alphabet_post(const float* p, const float* pt, const double* mass0, const int32_t* token,

@@ -48,6 +48,7 @@
 // coefficient kernel, which then evaluates that row in fp64 as well.
 // Zero-weight tokens (p = 0 < q) enter in closed form; a flagged row gets NaN.
 #include "common.h"
+#include "draw.h"
 #include "expsum_poly.h"
 #include "mdss.h"
 
@@ -2007,13 +2008,25 @@ __device__ __forceinline__ void tk_load(const float* __restrict__ pb, const floa
 // row streams, each wave writes the sum of p over its part; once r is written, each
 // support token's correction max(0, p - r) - p is added to its part's sum.  row_status is
 // set, not OR-ed into.
-template <bool kRes>
+// kDraw (with kRes): the step in one launch; once r and the sums are complete, wave 0
+// takes the row's selection and Algorithm 1 from them (draw_from_sums, the code of
+// the summed form's draw), with the drafts, uniforms and outputs of dr.
+struct TkDraw {
+  const float* u;
+  uint64_t seed, offset;
+  SelArgs sel;
+  int32_t* out_token;
+  uint8_t* accepted;
+  double* residual_mass;
+};
+template <bool kRes, bool kDraw>
 __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __restrict__ p, const float* __restrict__ q,
                                                              int64_t V, int K, int s_max, float* __restrict__ r,
                                                              int32_t* __restrict__ row_status,
-                                                             double* __restrict__ rsum, int64_t nsub) {
+                                                             double* __restrict__ rsum, int64_t nsub, TkDraw dr) {
   static_assert(kTkStep == 4 * kResSub && kResSub / kResParts == 256 && kTkThreads / 4 == 256,
                 "a wave's 256 tokens of a step are one part of the residual sums");
+  static_assert(kRes || !kDraw, "the fused draw takes the residual sums");
   __shared__ int s_idx[kTkCap];
   __shared__ float s_p[kTkCap];
   __shared__ float s_q[kTkCap];
@@ -2049,6 +2062,18 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
   const int64_t nparts = nsub * kResParts;
   const bool lds_parts = kRes && nparts <= kTkLdsParts;  // uniform
   double* const parts = lds_parts ? s_parts : rsum + b * nparts;
+  // the fused draw, by wave 0 once every thread's r and sums are written (after a barrier);
+  // the same 16-byte-load condition as the summed form's draw launch
+  const auto draw = [&](const double* sb) {
+    if (wid != 0) return;
+    const bool dvec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(r)) % 16 == 0);
+    if (dvec)
+      draw_from_sums<true, true, kResParts, kResSub>(pb, rb, sb, nsub, nullptr, dr.u, dr.seed, dr.offset, b, V, lane,
+                                                     dr.out_token, dr.accepted, dr.residual_mass, row_status, dr.sel);
+    else
+      draw_from_sums<false, true, kResParts, kResSub>(pb, rb, sb, nsub, nullptr, dr.u, dr.seed, dr.offset, b, V, lane,
+                                                      dr.out_token, dr.accepted, dr.residual_mass, row_status, dr.sel);
+  };
 
   // (1) stream the row, kTkAhead steps in flight, thread t on the four consecutive tokens
   //     x0 + 4t .. x0 + 4t + 3 of each step (wave w on the 256 tokens x0 + 256w ..): r = 0,
@@ -2277,133 +2302,137 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
     for (int64_t x = tid; x < V; x += kTkThreads) rb[x] = NAN;
     if (kRes)
       for (int64_t t = tid; t < nparts; t += kTkThreads) rsum[b * nparts + t] = NAN;
-    return;
-  }
-  const int k_lo = pl.k_lo, nk = pl.nk;
-  // fp32 unless a weight is not an fp32 normal (an overflowed or denormal ratio), the
-  // weights span more than 2^kTkMaxRange, or a node lies outside the rate table
-  bool fp64 = wide;
-  int tau = 0, range = 0;
-  if (nk > 0 && !fp64) {
-    es_scale_f32(wmin, wmax, tau, range);
-    fp64 = range > kTkMaxRange || k_lo < kEsNodeLo || k_lo + nk > kEsNodeHi;
-  }
-  double zw = q0;  // K i.i.d. drafts: Q0^(K-1)
-  for (int j = 2; j < K; ++j) zw *= q0;
-  if (nk > 0 && !fp64) {
-    // (3) fp32: S_k.  Entries in groups of 256 (four a lane); with G groups (a power of
-    //     two), wave w takes group w % G and the node blocks of 16 congruent to w / G
-    //     modulo 16 / G; each block summed across the wave (reduce-scatter)
-    for (int e = tid; e < nl; e += kTkThreads) s_w[e] = ldexpf(s_w[e], tau);
-    for (int k = tid; k < nk + 16; k += kTkThreads)  // past the grid: rate 0 (a term of 1, times c = 0)
-      s_rate[k] = k < nk ? es_rate_f32(k_lo + k, tau) : 0.0f;
-    for (int k = lane; k < nk; k += 64) s_part[wid][k] = 0.0f;
-    __syncthreads();
-    int G = 1;
-    while (G * kTkGroup < nl) G *= 2;  // <= kTkWaves
-    const int gi = wid % G, bs = kTkWaves / G;
-    float w[kTkE], qq[kTkE];
-#pragma unroll
-    for (int e = 0; e < kTkE; ++e) {
-      const int x = gi * kTkGroup + e * 64 + lane;  // < kTkCap
-      const bool in = x < nl && s_p[x] > 0.0f;
-      w[e] = in ? s_w[x] : 0.0f;
-      qq[e] = in ? s_q[x] : 0.0f;
+  } else {
+    const int k_lo = pl.k_lo, nk = pl.nk;
+    // fp32 unless a weight is not an fp32 normal (an overflowed or denormal ratio), the
+    // weights span more than 2^kTkMaxRange, or a node lies outside the rate table
+    bool fp64 = wide;
+    int tau = 0, range = 0;
+    if (nk > 0 && !fp64) {
+      es_scale_f32(wmin, wmax, tau, range);
+      fp64 = range > kTkMaxRange || k_lo < kEsNodeLo || k_lo + nk > kEsNodeHi;
     }
-    for (int blk = wid / G; blk * 16 < nk; blk += bs)
-      es_run_block<16>(w, qq, s_rate + blk * 16, lane, s_part[wid] + blk * 16, min(16, nk - blk * 16));
-    __syncthreads();
-    // (4) c_k 2^-tau from the fp64 sum of the waves' shares (a wave adds 0 at nodes it does not take)
-    for (int k = tid; k < nk; k += kTkThreads) {
-      double S = 0.0;
-#pragma unroll
-      for (int i = 0; i < kTkWaves; ++i) S += (double)s_part[i][k];  // 0 from the waves that did not take node k
-      const double sm = S + (K >= 3 ? q0 : 0.0);
-      double sp = 1.0;
-      for (int j = 1; j < K; ++j) sp *= sm;
-      s_cf[k] = (float)ldexp((double)K * kEsStep * exp((double)(k_lo + k) * kEsStep) * sp, -tau);
-    }
-    for (int k = nk + tid; k < nk + 16; k += kTkThreads) s_cf[k] = 0.0f;
-    __syncthreads();
-    // (5) r at the support: every node, blocks of 16 in fp32, the blocks summed in fp64
-    for (int e = tid; e < nl; e += kTkThreads) {
-      const float pp = s_p[e], qq1 = s_q[e];
-      double v;
-      if (pp > 0.0f) {
-        const float we = s_w[e];
-        double acc = 0.0;
-        for (int k0 = 0; k0 < nk; k0 += 16) {
-          float a = 0.0f;
-#pragma unroll
-          for (int i = 0; i < 16; ++i) a = fmaf(s_cf[k0 + i], es_decay(s_rate[k0 + i], we), a);
-          acc += (double)a;
-        }
-        const double quad = ldexp((double)pp * acc, tau);
-        v = (K == 2) ? fma(2.0 * (double)qq1, q0, quad) : quad;
-      } else {
-        v = (double)qq1 * zw;
+    double zw = q0;  // K i.i.d. drafts: Q0^(K-1)
+    for (int j = 2; j < K; ++j) zw *= q0;
+    if (nk > 0 && !fp64) {
+      // (3) fp32: S_k.  Entries in groups of 256 (four a lane); with G groups (a power of
+      //     two), wave w takes group w % G and the node blocks of 16 congruent to w / G
+      //     modulo 16 / G; each block summed across the wave (reduce-scatter)
+      for (int e = tid; e < nl; e += kTkThreads) s_w[e] = ldexpf(s_w[e], tau);
+      for (int k = tid; k < nk + 16; k += kTkThreads)  // past the grid: rate 0 (a term of 1, times c = 0)
+        s_rate[k] = k < nk ? es_rate_f32(k_lo + k, tau) : 0.0f;
+      for (int k = lane; k < nk; k += 64) s_part[wid][k] = 0.0f;
+      __syncthreads();
+      int G = 1;
+      while (G * kTkGroup < nl) G *= 2;  // <= kTkWaves
+      const int gi = wid % G, bs = kTkWaves / G;
+      float w[kTkE], qq[kTkE];
+  #pragma unroll
+      for (int e = 0; e < kTkE; ++e) {
+        const int x = gi * kTkGroup + e * 64 + lane;  // < kTkCap
+        const bool in = x < nl && s_p[x] > 0.0f;
+        w[e] = in ? s_w[x] : 0.0f;
+        qq[e] = in ? s_q[x] : 0.0f;
       }
-      rb[s_idx[e]] = (float)v;
-      if (kRes) s_dres[e] = residual_of(pp, (float)v) - (double)pp;
-    }
-  } else if (nk > 0) {
-    // (3') fp64: S_k per node (wave w takes the nodes congruent to w), lanes over the entries
-    for (int kk = wid; kk < nk; kk += kTkWaves) {
-      const double a = exp((double)(k_lo + kk) * kEsStep);
-      double acc = 0.0;
-      for (int e = lane; e < nl; e += 64) {
-        const float pp = s_p[e], qq1 = s_q[e];
-        if (pp > 0.0f) acc += (double)qq1 * exp(-a * es_ratio<double>(pp, qq1));
-      }
-      acc = wave_sum(acc);
-      if (lane == 0) {
-        const double sm = acc + (K >= 3 ? q0 : 0.0);
+      for (int blk = wid / G; blk * 16 < nk; blk += bs)
+        es_run_block<16>(w, qq, s_rate + blk * 16, lane, s_part[wid] + blk * 16, min(16, nk - blk * 16));
+      __syncthreads();
+      // (4) c_k 2^-tau from the fp64 sum of the waves' shares (a wave adds 0 at nodes it does not take)
+      for (int k = tid; k < nk; k += kTkThreads) {
+        double S = 0.0;
+  #pragma unroll
+        for (int i = 0; i < kTkWaves; ++i) S += (double)s_part[i][k];  // 0 from the waves that did not take node k
+        const double sm = S + (K >= 3 ? q0 : 0.0);
         double sp = 1.0;
         for (int j = 1; j < K; ++j) sp *= sm;
-        s_c64[kk] = (double)K * kEsStep * a * sp;
+        s_cf[k] = (float)ldexp((double)K * kEsStep * exp((double)(k_lo + k) * kEsStep) * sp, -tau);
       }
-    }
-    __syncthreads();
-    for (int e = tid; e < nl; e += kTkThreads) {
-      const float pp = s_p[e], qq1 = s_q[e];
-      double v;
-      if (pp > 0.0f) {
-        const double w = es_ratio<double>(pp, qq1);
+      for (int k = nk + tid; k < nk + 16; k += kTkThreads) s_cf[k] = 0.0f;
+      __syncthreads();
+      // (5) r at the support: every node, blocks of 16 in fp32, the blocks summed in fp64
+      for (int e = tid; e < nl; e += kTkThreads) {
+        const float pp = s_p[e], qq1 = s_q[e];
+        double v;
+        if (pp > 0.0f) {
+          const float we = s_w[e];
+          double acc = 0.0;
+          for (int k0 = 0; k0 < nk; k0 += 16) {
+            float a = 0.0f;
+  #pragma unroll
+            for (int i = 0; i < 16; ++i) a = fmaf(s_cf[k0 + i], es_decay(s_rate[k0 + i], we), a);
+            acc += (double)a;
+          }
+          const double quad = ldexp((double)pp * acc, tau);
+          v = (K == 2) ? fma(2.0 * (double)qq1, q0, quad) : quad;
+        } else {
+          v = (double)qq1 * zw;
+        }
+        rb[s_idx[e]] = (float)v;
+        if (kRes) s_dres[e] = residual_of(pp, (float)v) - (double)pp;
+      }
+    } else if (nk > 0) {
+      // (3') fp64: S_k per node (wave w takes the nodes congruent to w), lanes over the entries
+      for (int kk = wid; kk < nk; kk += kTkWaves) {
+        const double a = exp((double)(k_lo + kk) * kEsStep);
         double acc = 0.0;
-        for (int kk = 0; kk < nk; ++kk) acc += s_c64[kk] * exp(-exp((double)(k_lo + kk) * kEsStep) * w);
-        const double quad = (double)pp * acc;
-        v = (K == 2) ? fma(2.0 * (double)qq1, q0, quad) : quad;
-      } else {
-        v = (double)qq1 * zw;
+        for (int e = lane; e < nl; e += 64) {
+          const float pp = s_p[e], qq1 = s_q[e];
+          if (pp > 0.0f) acc += (double)qq1 * exp(-a * es_ratio<double>(pp, qq1));
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) {
+          const double sm = acc + (K >= 3 ? q0 : 0.0);
+          double sp = 1.0;
+          for (int j = 1; j < K; ++j) sp *= sm;
+          s_c64[kk] = (double)K * kEsStep * a * sp;
+        }
       }
-      rb[s_idx[e]] = (float)v;
-      if (kRes) s_dres[e] = residual_of(pp, (float)v) - (double)pp;
+      __syncthreads();
+      for (int e = tid; e < nl; e += kTkThreads) {
+        const float pp = s_p[e], qq1 = s_q[e];
+        double v;
+        if (pp > 0.0f) {
+          const double w = es_ratio<double>(pp, qq1);
+          double acc = 0.0;
+          for (int kk = 0; kk < nk; ++kk) acc += s_c64[kk] * exp(-exp((double)(k_lo + kk) * kEsStep) * w);
+          const double quad = (double)pp * acc;
+          v = (K == 2) ? fma(2.0 * (double)qq1, q0, quad) : quad;
+        } else {
+          v = (double)qq1 * zw;
+        }
+        rb[s_idx[e]] = (float)v;
+        if (kRes) s_dres[e] = residual_of(pp, (float)v) - (double)pp;
+      }
+    } else {
+      // no positive weight: zero-weight tokens only
+      for (int e = tid; e < nl; e += kTkThreads) {
+        const float v = (float)((double)s_q[e] * zw);
+        rb[s_idx[e]] = v;
+        if (kRes) s_dres[e] = residual_of(s_p[e], v) - (double)s_p[e];
+      }
     }
-  } else {
-    // no positive weight: zero-weight tokens only
-    for (int e = tid; e < nl; e += kTkThreads) {
-      const float v = (float)((double)s_q[e] * zw);
-      rb[s_idx[e]] = v;
-      if (kRes) s_dres[e] = residual_of(s_p[e], v) - (double)s_p[e];
+    if (kRes) {
+      // (6) the residual sums: the support entries of one 256-token part are consecutive in
+      //     the list (a wave's segment holds its parts in stream order; the token-order list
+      //     is sorted); the first entry of each run adds the run's corrections, in list order,
+      //     to its part's sum of p
+      __syncthreads();  // every correction is in LDS, every part's sum of p written
+      for (int e = tid; e < nl; e += kTkThreads) {
+        const int key = s_idx[e] >> 8;
+        if (e > 0 && (s_idx[e - 1] >> 8) == key) continue;  // not the first entry of its run
+        double corr = 0.0;
+        for (int f = e; f < nl && (s_idx[f] >> 8) == key; ++f) corr += s_dres[f];
+        parts[key] += corr;
+      }
+      if (lds_parts) {
+        __syncthreads();
+        for (int64_t t = tid; t < nparts; t += kTkThreads) rsum[b * nparts + t] = s_parts[t];
+      }
     }
   }
-  if (kRes) {
-    // (6) the residual sums: the support entries of one 256-token part are consecutive in
-    //     the list (a wave's segment holds its parts in stream order; the token-order list
-    //     is sorted); the first entry of each run adds the run's corrections, in list order,
-    //     to its part's sum of p
-    __syncthreads();  // every correction is in LDS, every part's sum of p written
-    for (int e = tid; e < nl; e += kTkThreads) {
-      const int key = s_idx[e] >> 8;
-      if (e > 0 && (s_idx[e - 1] >> 8) == key) continue;  // not the first entry of its run
-      double corr = 0.0;
-      for (int f = e; f < nl && (s_idx[f] >> 8) == key; ++f) corr += s_dres[f];
-      parts[key] += corr;
-    }
-    if (lds_parts) {
-      __syncthreads();
-      for (int64_t t = tid; t < nparts; t += kTkThreads) rsum[b * nparts + t] = s_parts[t];
-    }
+  if (kDraw) {
+    __syncthreads();  // r and the residual sums are complete (a flagged row: NaN sums in rsum)
+    draw(flags ? rsum + b * nparts : parts);
   }
 }
 
@@ -2412,12 +2441,25 @@ __global__ __launch_bounds__(kTkThreads) void es_topk_kernel(const float* __rest
 hipError_t launch_induced_topk_expsum(const float* p, const float* q, int64_t B, int64_t V, int K, int s_max,
                                       float* r, int32_t* row_status, hipStream_t st, double* rsum) {
   const int64_t nsub = (V + kResSub - 1) / kResSub;
+  const TkDraw none = {nullptr, 0, 0, {nullptr, nullptr, nullptr, 0, nullptr, nullptr}, nullptr, nullptr, nullptr};
   if (rsum)
-    hipLaunchKernelGGL(es_topk_kernel<true>, dim3((unsigned)B), dim3(kTkThreads), 0, st, p, q, V, K, s_max, r,
-                       row_status, rsum, nsub);
+    hipLaunchKernelGGL((es_topk_kernel<true, false>), dim3((unsigned)B), dim3(kTkThreads), 0, st, p, q, V, K, s_max, r,
+                       row_status, rsum, nsub, none);
   else
-    hipLaunchKernelGGL(es_topk_kernel<false>, dim3((unsigned)B), dim3(kTkThreads), 0, st, p, q, V, K, s_max, r,
-                       row_status, nullptr, nsub);
+    hipLaunchKernelGGL((es_topk_kernel<false, false>), dim3((unsigned)B), dim3(kTkThreads), 0, st, p, q, V, K, s_max,
+                       r, row_status, nullptr, nsub, none);
+  return hipGetLastError();
+}
+
+hipError_t launch_step_topk_expsum(const float* p, const float* q, const int32_t* drafts, const float* u, uint64_t seed,
+                                   uint64_t offset, int64_t B, int64_t V, int K, int s_max, float* r,
+                                   int32_t* sel_index, int32_t* sel_token, int32_t* out_token, uint8_t* accepted,
+                                   double* residual_mass, int32_t* row_status, double* rsum, hipStream_t st) {
+  const int64_t nsub = (V + kResSub - 1) / kResSub;
+  const TkDraw dr = {u, seed, offset, {q, nullptr, drafts, K, sel_index, sel_token}, out_token, accepted,
+                     residual_mass};
+  hipLaunchKernelGGL((es_topk_kernel<true, true>), dim3((unsigned)B), dim3(kTkThreads), 0, st, p, q, V, K, s_max, r,
+                     row_status, rsum, nsub, dr);
   return hipGetLastError();
 }
 

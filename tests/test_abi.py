@@ -312,3 +312,20 @@ def test_topk_summed_form_argument_errors(lib):
     assert f(None, None, 0, 16, 3, 8, None, None, None, 0, None) == 0
     # the accept workspace holds the summed forms' four sums per 1024 tokens
     assert acc >= 8 * 4 * 4
+
+
+def test_topk_step_argument_errors(lib):
+    f = lib.mdss_step_topk_expsum
+    P, i64, i32, u64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
+    f.argtypes = [P, P, P, P, u64, u64, i64, i64, i32, i32, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    acc = lib.mdss_workspace_bytes_accept(4, 16)
+
+    def call(p=FAKE, q=FAKE, d=FAKE, B=4, V=16, K=3, s=8, r=FAKE, out=FAKE, ok=FAKE, ws=FAKE, n=acc):
+        return f(p, q, d, None, 0, 0, B, V, K, s, r, None, None, out, ok, None, None, ws, n, None)
+
+    assert call(p=None) == 1 and call(q=None) == 1 and call(d=None) == 1 and call(r=None) == 1
+    assert call(out=None) == 1 and call(ok=None) == 1
+    assert call(V=1) == 2
+    assert call(K=1) == 3 and call(K=9) == 3 and call(s=0) == 3 and call(s=4097) == 3
+    assert call(ws=None) == 5 and call(n=acc - 1) == 5
+    assert call(p=None, q=None, d=None, B=0, r=None, out=None, ok=None, ws=None, n=0) == 0

@@ -299,7 +299,8 @@ def test_step_uses_the_top_s_form():
     assert np.array_equal(out["sel_index"].cpu().numpy(), si)
 
 
-# ---- the summed form (mdss_induced_dist_topk_expsum_sums + mdss_select_accept_sums) ----
+# ---- the summed form (mdss_induced_dist_topk_expsum_sums + mdss_select_accept_sums, and the two
+# in one launch: mdss_step_topk_expsum) ----
 
 def both_forms_tk(P, Q, drafts, u, K, s_max):
     """(summed form, two-call form) outputs as numpy arrays; the summed form's status words
@@ -322,6 +323,17 @@ def both_forms_tk(P, Q, drafts, u, K, s_max):
         torch.cuda.synchronize()
         out[form] = {k: v.cpu().numpy() for k, v in dict(r=r, sel_index=si, sel_token=stok, out=tok, acc=acc,
                                                         mass=mass, status=st).items()}
+    # the fused step (one launch): the summed form's outputs bit for bit, status words set
+    st = torch.full((B,), -1, dtype=torch.int32, device=DEV)
+    acc_ws = torch.empty(mdss.workspace_bytes_accept(B, V), dtype=torch.uint8, device=DEV)
+    r, si, stok, tok, acc, mass = mdss.step_topk_expsum(p, q, d, K, s_max, acc_ws, uu, seed=13, offset=2,
+                                                        want_mass=True, row_status=st)
+    torch.cuda.synchronize()
+    fused = {k: v.cpu().numpy() for k, v in dict(r=r, sel_index=si, sel_token=stok, out=tok, acc=acc, mass=mass,
+                                                 status=st).items()}
+    for k, v in fused.items():
+        x = out["sums"][k]
+        assert x.dtype == v.dtype and np.array_equal(x.view(np.uint8), v.view(np.uint8)), f"fused step: {k}"
     return out["sums"], out["calls"]
 
 
