@@ -41,8 +41,9 @@ def kernel_source_digest() -> str:
     """Digest of the device code and its build flags (the host-side argument checks
     of api.hip are left out: they launch nothing)."""
     h = hashlib.sha256()
-    for f in ("csrc/common.h", "csrc/induced.hip", "csrc/sample.hip", "csrc/tlp.hip", "csrc/rank.h",
-              "csrc/optimum.hip", "csrc/alphabet.hip", "csrc/expsum.hip", "csrc/expsum_poly.h", "build.py"):
+    csrc = os.path.join(ROOT, "paper_2410_18234_amd", "csrc")
+    files = sorted(f for f in os.listdir(csrc) if f.endswith((".h", ".hip")) and f != "api.hip")
+    for f in [os.path.join("csrc", f) for f in files] + ["build.py"]:
         with open(os.path.join(ROOT, "paper_2410_18234_amd", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

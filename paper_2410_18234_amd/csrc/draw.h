@@ -162,7 +162,6 @@ __device__ __forceinline__ void draw_from_sums(const float* __restrict__ pb, con
   const int64_t per = (nsub + 63) / 64;
   const int64_t s_lo = lane * per, s_hi = (s_lo + per < nsub) ? s_lo + per : nsub;
   double lane_sum = 0.0;
-  #pragma unroll 1
   for (int64_t s = s_lo; s < s_hi; ++s) lane_sum += sub_at(s);
   float uu[3];
   position_uniforms(u, seed, offset, b, uu);
@@ -207,7 +206,6 @@ __device__ __forceinline__ void draw_from_sums(const float* __restrict__ pb, con
   // first sub-tile whose running sum exceeds thr
   int64_t my_s = -1;
   double my_prev = 0.0, run = excl;
-  #pragma unroll 1
   for (int64_t s = s_lo; s < s_hi; ++s) {
     const double prev = run;
     run += sub_at(s);
@@ -227,7 +225,6 @@ __device__ __forceinline__ void draw_from_sums(const float* __restrict__ pb, con
   } else {
     // rounding put u_res * Z at or past every running sum: the last sub-tile with mass
     int64_t last = -1;
-    #pragma unroll 1
     for (int64_t s = s_lo; s < s_hi; ++s)
       if (sub_at(s) > 0.0) last = s;
 #pragma unroll
