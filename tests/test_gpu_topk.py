@@ -436,3 +436,33 @@ def test_summed_form_long_rows():
         assert np.all(a["status"] == 0)
         check_forms(P, a, b, u[:, 2])
         assert np.any(a["acc"] == 0)  # draws from the sums (a row with p(Y) >= r(Y) accepts at any u)
+
+
+def test_fused_step_philox_and_null_outputs():
+    # mdss_step_topk_expsum with the uniforms from Philox (u = NULL), K = 8, and every
+    # nullable output left out (sel_index, sel_token, residual_mass, row_status): the same
+    # tokens and decisions as the two summed-form calls with the same seed and offset
+    import ctypes
+    rng = np.random.default_rng(91)
+    B, V, K = 40, 3000, 8
+    P = rng.dirichlet(np.full(V, 0.5), size=B).astype(np.float32)
+    Q = top_s(rng.dirichlet(np.full(V, 0.5), size=B), 700)
+    drafts = _drafts_from(Q, K, 92)
+    p, q, d = dev(P), dev(Q), dev(drafts)
+    acc_ws = torch.empty(mdss.workspace_bytes_accept(B, V), dtype=torch.uint8, device=DEV)
+    r1 = mdss.induced_dist_topk_expsum_sums(p, q, K, 1024, acc_ws)
+    _, _, tok1, acc1, _ = mdss.select_accept_sums(p, q, r1, d, acc_ws, None, seed=77, offset=5)
+    lib = mdss.load_library()
+    r2 = torch.empty_like(p)
+    tok2 = torch.empty(B, dtype=torch.int32, device=DEV)
+    acc2 = torch.empty(B, dtype=torch.uint8, device=DEV)
+    ws2 = torch.empty_like(acc_ws)
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr())
+    code = lib.mdss_step_topk_expsum(ptr(p), ptr(q), ptr(d), None, ctypes.c_uint64(77), ctypes.c_uint64(5), B, V, K,
+                                     1024, ptr(r2), None, None, ptr(tok2), ptr(acc2), None, None, ptr(ws2),
+                                     ws2.numel(), ctypes.c_void_p(torch.cuda.current_stream(DEV).cuda_stream))
+    torch.cuda.synchronize()
+    assert code == 0
+    assert torch.equal(r1, r2)
+    assert torch.equal(tok1, tok2) and torch.equal(acc1, acc2)
+    assert 0 < int(acc2.sum()) < B  # both branches of Algorithm 1
