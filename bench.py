@@ -650,7 +650,7 @@ def main():
     res_gbs_hot = res_bytes / (res_ms_hot * 1e-3) / 1e9
     # L2 fetch and write bytes do not depend on where the line comes from (Infinity Cache or HBM):
     # the counted figure of the same kernels serves both placements
-    res_traffic = counted_traffic(cfg.name, ["accept_seg_kernel<true>", "accept_draw_kernel<true, false>"], digest)
+    res_traffic = counted_traffic(cfg.name, ["accept_seg_kernel<true>", "accept_draw_kernel<true, false, 1, 256>"], digest)
     roofline_resample = {"bound": "hbm", "achieved": round(res_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": round(res_gbs / HBM_PEAK_GBS, 4), "traffic": res_traffic,
                          "kernel": "mdss_accept_or_resample (accept_seg_kernel + accept_draw_kernel), residual and mass written for "
