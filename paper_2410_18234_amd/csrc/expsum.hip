@@ -1741,11 +1741,16 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
         const int blk = task % nblk, j = (task / nblk) % kEsTaylor, l = task / (nblk * kEsTaylor);
         const double rho = s_rho[j];
         const int i0 = blk * kPB, n = min(kPB, pl.nk - i0);
+        // the block's c loaded first and the recurrence selected, not branched on, per node
+        double cv[kPB];
+#pragma unroll
+        for (int m = 0; m < kPB; ++m) cv[m] = s_c[l][min(i0 + m, kEsMaxWin - 1)];
         double acc = 0.0;
 #pragma unroll
         for (int m = 0; m < kPB; ++m) {
-          const double c = s_c[l][min(i0 + m, kEsMaxWin - 1)];
-          acc = (m < n) ? fma(acc, rho, c) : acc;
+          double t = fma(acc, rho, cv[m]);
+          __asm__ volatile("" : "+v"(t));
+          acc = (m < n) ? t : acc;
         }
         s_last[l][j][blk] = acc;
       }
@@ -1761,13 +1766,19 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
         for (int bb = 0; bb < blk; ++bb) carry = fma(carry, r16, s_last[l][j][bb]);
         double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
         const int i0 = blk * kPB, n = min(kPB, pl.nk - i0);
-        double acc = 0.0, pw = rho;
+        double cv[kPB];
+#pragma unroll
+        for (int m = 0; m < kPB; ++m) cv[m] = s_c[l][min(i0 + m, kEsMaxWin - 1)];
+        double acc = 0.0, pw = rho, out[kPB];
 #pragma unroll
         for (int m = 0; m < kPB; ++m) {
-          acc = fma(acc, rho, s_c[l][min(i0 + m, kEsMaxWin - 1)]);
-          if (m < n) pt[(i0 + m) * kEsTaylor + j] = fma(carry, pw, acc) * f;
+          acc = fma(acc, rho, cv[m]);
+          out[m] = fma(carry, pw, acc) * f;
           pw *= rho;
         }
+#pragma unroll
+        for (int m = 0; m < kPB; ++m)
+          if (m < n) pt[(i0 + m) * kEsTaylor + j] = out[m];
       }
       // the per-token polynomial of every node row i (k0 = k_lo + i): a query token with
       // x = a_k0 w, t = (x - x_mid) / delta, takes sum_n A_n(i) t^n for its nine node terms
@@ -1779,14 +1790,19 @@ __global__ __launch_bounds__(kEsThreads) void es_coef_kernel(const float* __rest
       for (int task = tid; task < L * nrow; task += kEsThreads) {
         const int l = task / nrow, i = task % nrow;
         const double* pt = es.ptab + (b * L + l) * (int64_t)kEsMaxNodes * kEsTaylor;
-        double cm[kEsTokNodesC], pj[kEsTaylor];
-#pragma unroll
-        for (int m = 0; m < kEsTokNodesC; ++m) cm[m] = (i + m < pl.nk) ? s_c[l][min(i + m, kEsMaxWin - 1)] : 0.0;
+        double cm[kEsTokNodesC], pj[kEsTaylor], pv[kEsTaylor];
         const int prow = max(0, min(i - 1, pl.nk - 1));  // B_j(k0 - 1): row i - 1, or the last row decayed
         const int past = max(0, i - 1 - prow);              // rows past the grid's end: e^(-jh) a node
+        // every load issued unconditionally (clamped indices), then selected
+#pragma unroll
+        for (int j = 0; j < kEsTaylor; ++j) pv[j] = pt[prow * kEsTaylor + j];
+#pragma unroll
+        for (int m = 0; m < kEsTokNodesC; ++m) cm[m] = s_c[l][min(i + m, kEsMaxWin - 1)];
+#pragma unroll
+        for (int m = 0; m < kEsTokNodesC; ++m) cm[m] = (i + m < pl.nk) ? cm[m] : 0.0;
 #pragma unroll
         for (int j = 0; j < kEsTaylor; ++j) {
-          const double v = (i >= 1) ? pt[prow * kEsTaylor + j] : 0.0;
+          const double v = (i >= 1) ? pv[j] : 0.0;
           // e^(-past j h) from the table of e^(-mh) (the same expression as its entries);
           // past j beyond the table (weights spanning far beyond the grid) takes exp
           const int m = past * j;
